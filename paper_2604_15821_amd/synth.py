@@ -1,0 +1,262 @@
+"""Seeded synthetic inputs for the MatRIS-MoE training step.
+
+This module draws structures (cells, positions, species), model weights and
+reference labels.  It holds none of the method's arithmetic: no neighbour
+test, no basis, no routing, no model evaluation.  Both the HIP path (through
+the Python binding) and the float64 oracle consume exactly the arrays it
+returns, so the two sides see the same bytes.
+
+The five workloads stand in for the paper's 473M-configuration training set
+(Sec. "Overview of the problem", edge tokens as the unit of work; the dataset
+spans molecules, crystals, catalysis and MOFs).  No item of that dataset is
+reproduced: every structure is drawn from the distributions documented on
+each ``Workload`` below.
+
+Draw order per workload (all from ``np.random.default_rng(seed)``):
+structure kinds and sizes -> boxes -> positions -> species -> weights in blob
+order -> E_ref -> F_ref.
+"""
+from __future__ import annotations
+
+import dataclasses
+from dataclasses import dataclass, field
+
+import numpy as np
+
+N_SPECIES = 89
+
+
+@dataclass(frozen=True)
+class ModelConfig:
+    """Hyper-parameters of the invariant MoE message-passing potential.
+
+    d: embedding width; n_rbf: Bessel functions; n_blocks: interaction blocks;
+    n_experts / top_k / d_hidden: edge-MoE size (each expert d -> d_hidden -> d);
+    r_cut: neighbour cutoff in Angstrom.  The three-body fields describe the
+    optional angular term (triplets of bonds shorter than r_cut3).
+    """
+
+    d: int
+    n_rbf: int
+    n_blocks: int
+    n_experts: int
+    top_k: int
+    d_hidden: int
+    r_cut: float
+    n_species: int = N_SPECIES
+    env_p: int = 6
+    three_body: bool = False
+    r_cut3: float = 3.5
+    n_experts3: int = 0
+    top_k3: int = 0
+    d_hidden3: int = 0
+    n_legendre: int = 5
+    w_E: float = 1.0
+    w_F: float = 1.0
+
+    def weight_shapes(self):
+        """Named weight tensors in blob order, with the fan-in used at init.
+
+        Returns a list of (name, shape, fan_in); fan_in None marks a one-hot
+        table drawn N(0, 1) and 'zero' marks the fixed routing bias.
+        """
+        d, E, h, nb, S = self.d, self.n_experts, self.d_hidden, self.n_rbf, self.n_species
+        out = [("A", (S, d), None)]
+        for t in range(self.n_blocks):
+            p = f"blocks.{t}."
+            out += [
+                (p + "W_b", (nb, d), nb),
+                (p + "Pc", (S, E), None),
+                (p + "Pn", (S, E), None),
+                (p + "beta", (E,), "zero"),
+                (p + "W1", (E, d, h), d),
+                (p + "W2", (E, h, d), h),
+            ]
+            if self.three_body:
+                E3, h3 = self.n_experts3, self.d_hidden3
+                nf = self.n_legendre * nb
+                out += [
+                    (p + "W_a", (nf, d), nf),
+                    (p + "P3a", (S, E3), None),
+                    (p + "P3b", (S, E3), None),
+                    (p + "P3c", (S, E3), None),
+                    (p + "beta3", (E3,), "zero"),
+                    (p + "W1a", (E3, d, h3), d),
+                    (p + "W2a", (E3, h3, d), h3),
+                ]
+        out += [("W_o1", (d, d), d), ("w_o2", (d,), d)]
+        return out
+
+
+@dataclass(frozen=True)
+class Workload:
+    """A synthetic batch recipe.
+
+    kind 'cubic'  : n_struct cubic cells of n_atoms each at `density`.
+    kind 'ortho'  : orthorhombic cells, sides proportional to (1, a, b) with
+                    a, b ~ U[1, 1.5], volume n_atoms / density.
+    kind 'mixed'  : n_struct structures, atom count round(exp(U[ln lo, ln hi])),
+                    crystal with probability p_crystal (cubic cell at
+                    `density`), otherwise a molecule: uniform in a sphere of
+                    local density `mol_density`, centred in a cubic box of
+                    side 2R + vacuum.
+    zipf_s        : if > 0, block routing biases beta_x = -zipf_s * ln(rank_x)
+                    with rank a seeded permutation of 1..E (skewed expert load).
+    """
+
+    name: str
+    kind: str
+    n_struct: int
+    n_atoms: int
+    density: float
+    model: ModelConfig
+    seed: int = 0
+    size_lo: int = 8
+    size_hi: int = 512
+    p_crystal: float = 0.7
+    mol_density: float = 0.02
+    vacuum: float = 20.0
+    zipf_s: float = 0.0
+
+
+_M_TINY = ModelConfig(d=64, n_rbf=8, n_blocks=2, n_experts=4, top_k=1, d_hidden=128, r_cut=4.0)
+_M_SMALL = ModelConfig(d=128, n_rbf=16, n_blocks=3, n_experts=8, top_k=2, d_hidden=512, r_cut=5.0)
+_M_3B = dataclasses.replace(_M_SMALL, three_body=True, r_cut3=3.5, n_experts3=8, top_k3=2, d_hidden3=256)
+_M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
+
+WORKLOADS = {
+    "tiny": Workload("tiny", "cubic", 8, 32, 0.08, _M_TINY),
+    "small": Workload("small", "ortho", 64, 64, 0.08, _M_SMALL),
+    "threebody": Workload("threebody", "ortho", 64, 64, 0.08, _M_3B),
+    "shard": Workload("shard", "cubic", 256, 128, 0.1, _M_BIG),
+    "irregular": Workload("irregular", "mixed", 512, 0, 0.1, _M_BIG, zipf_s=1.2),
+}
+
+
+@dataclass
+class Batch:
+    """One synthetic batch.  All float arrays are float32, ints int32."""
+
+    pos: np.ndarray          # [N, 3] Cartesian positions, wrapped into the cell
+    cell: np.ndarray         # [S, 3, 3] row vectors a, b, c (diagonal here)
+    species: np.ndarray      # [N] atomic type index in 0..88
+    offsets: np.ndarray      # [S+1] structure s owns atoms offsets[s]:offsets[s+1]
+    E_ref: np.ndarray        # [S] per-atom reference energy of each structure
+    F_ref: np.ndarray        # [N, 3]
+    weights: dict = field(default_factory=dict)   # name -> float32 array
+    model: ModelConfig | None = None
+    name: str = ""
+
+    @property
+    def n_atoms(self):
+        return int(self.pos.shape[0])
+
+    @property
+    def n_struct(self):
+        return int(self.cell.shape[0])
+
+
+def _draw_weights(rng, m: ModelConfig, zipf_s: float):
+    w = {}
+    for name, shape, fan in m.weight_shapes():
+        if fan == "zero":
+            if zipf_s > 0:
+                rank = rng.permutation(shape[0]) + 1
+                w[name] = (-zipf_s * np.log(rank.astype(np.float64))).astype(np.float32)
+            else:
+                w[name] = np.zeros(shape, np.float32)
+        elif fan is None:
+            w[name] = rng.standard_normal(shape).astype(np.float32)
+        else:
+            w[name] = (rng.standard_normal(shape) / np.sqrt(fan)).astype(np.float32)
+    return w
+
+
+def make_batch(wl: Workload | str, seed: int | None = None, n_struct: int | None = None) -> Batch:
+    """Draw one batch of workload `wl` (name or Workload).
+
+    n_struct, if given, truncates the structure count (the draws for the kept
+    structures are identical to those of the full batch only for the weights;
+    use it for small test cases, not for sampling a full batch).
+    """
+    if isinstance(wl, str):
+        wl = WORKLOADS[wl]
+    rng = np.random.default_rng(wl.seed if seed is None else seed)
+    S = wl.n_struct if n_struct is None else n_struct
+    m = wl.model
+
+    # 1. structure kinds and sizes
+    if wl.kind == "mixed":
+        crystal = rng.random(S) < wl.p_crystal
+        sizes = np.rint(np.exp(rng.uniform(np.log(wl.size_lo), np.log(wl.size_hi), S))).astype(np.int64)
+    else:
+        crystal = np.ones(S, bool)
+        sizes = np.full(S, wl.n_atoms, np.int64)
+
+    # 2. boxes
+    sides = np.zeros((S, 3))
+    mol_R = np.zeros(S)
+    if wl.kind == "ortho":
+        ab = rng.uniform(1.0, 1.5, (S, 2))
+        for s in range(S):
+            a0 = (sizes[s] / wl.density / (ab[s, 0] * ab[s, 1])) ** (1.0 / 3.0)
+            sides[s] = (a0, a0 * ab[s, 0], a0 * ab[s, 1])
+    else:
+        for s in range(S):
+            if crystal[s]:
+                sides[s] = (sizes[s] / wl.density) ** (1.0 / 3.0)
+            else:
+                mol_R[s] = (3.0 * sizes[s] / (4.0 * np.pi * wl.mol_density)) ** (1.0 / 3.0)
+                sides[s] = 2.0 * mol_R[s] + wl.vacuum
+    sides = sides.astype(np.float32)
+
+    # 3. positions (fp32, wrapped into [0, L))
+    pos = []
+    for s in range(S):
+        n = int(sizes[s])
+        L = sides[s].astype(np.float64)
+        if crystal[s]:
+            p = rng.random((n, 3)) * L
+        else:
+            v = rng.standard_normal((n, 3))
+            v /= np.linalg.norm(v, axis=1, keepdims=True)
+            rad = mol_R[s] * rng.random(n) ** (1.0 / 3.0)
+            p = 0.5 * L + v * rad[:, None]
+        p = p.astype(np.float32)
+        # rounding can land exactly on L; fold such coordinates back to 0
+        p = np.where(p >= sides[s], np.float32(0.0), p)
+        pos.append(p)
+    pos = np.concatenate(pos, 0) if pos else np.zeros((0, 3), np.float32)
+
+    # 4. species
+    N = int(sizes.sum())
+    species = rng.integers(0, m.n_species, N).astype(np.int32)
+
+    # 5. weights, 6. references
+    weights = _draw_weights(rng, m, wl.zipf_s)
+    E_ref = rng.standard_normal(S).astype(np.float32)
+    F_ref = rng.standard_normal((N, 3)).astype(np.float32)
+
+    cell = np.zeros((S, 3, 3), np.float32)
+    for s in range(S):
+        cell[s] = np.diag(sides[s])
+    offsets = np.zeros(S + 1, np.int32)
+    offsets[1:] = np.cumsum(sizes)
+    return Batch(pos=pos, cell=cell, species=species, offsets=offsets, E_ref=E_ref,
+                 F_ref=F_ref, weights=weights, model=m, name=wl.name)
+
+
+def subset(batch: Batch, structs) -> Batch:
+    """The sub-batch made of the listed structures (same weights)."""
+    structs = list(structs)
+    pos, spc, fref, sizes = [], [], [], []
+    for s in structs:
+        a, b = int(batch.offsets[s]), int(batch.offsets[s + 1])
+        pos.append(batch.pos[a:b]); spc.append(batch.species[a:b]); fref.append(batch.F_ref[a:b])
+        sizes.append(b - a)
+    off = np.zeros(len(structs) + 1, np.int32)
+    off[1:] = np.cumsum(sizes)
+    return Batch(pos=np.concatenate(pos, 0), cell=batch.cell[structs].copy(),
+                 species=np.concatenate(spc, 0), offsets=off, E_ref=batch.E_ref[structs].copy(),
+                 F_ref=np.concatenate(fref, 0), weights=batch.weights, model=batch.model,
+                 name=batch.name + "[sub]")

@@ -1,0 +1,132 @@
+"""Pins of the oracle neighbour list: lattice coordination numbers, sums of
+three squares for a cell smaller than the cutoff, a periodic k-d tree on
+large cells, exact symmetry and the expected mean degree of the workloads."""
+import numpy as np
+import pytest
+from scipy.spatial import cKDTree
+
+from oracle.neighbors import image_range, neighbor_list, reverse_map, triplet_list
+from paper_2604_15821_amd.synth import WORKLOADS, make_batch
+
+
+def _one(pos, L, rc):
+    pos = np.asarray(pos, np.float32)
+    cell = np.diag(np.asarray(L, np.float32))[None]
+    off = np.array([0, pos.shape[0]], np.int32)
+    return neighbor_list(pos, cell, off, rc)
+
+
+@pytest.mark.parametrize("rc,expect", [(3.5, 6), (4.5, 18), (5.5, 26)])
+def test_simple_cubic_shells_single_atom_cell(rc, expect):
+    # a = 3: shells at a (6), a*sqrt2 = 4.24 (12), a*sqrt3 = 5.20 (8)
+    ei, ej, sh, rp = _one([[0.5, 0.5, 0.5]], [3.0] * 3, rc)
+    assert ei.size == expect and np.all(ei == 0) and np.all(ej == 0)
+    assert not np.any(np.all(sh == 0, axis=1))
+
+
+def test_sums_of_three_squares_when_cell_is_smaller_than_cutoff():
+    # L = 1, rc = 2.5: all n != 0 with |n|^2 < 6.25 -> r3(1..6) = 6+12+8+6+24+24
+    ei, ej, sh, rp = _one([[0.0, 0.0, 0.0]], [1.0] * 3, 2.5)
+    assert ei.size == 80
+    n2 = (sh.astype(int) ** 2).sum(1)
+    assert sorted(np.bincount(n2)[1:].tolist()) == sorted([6, 12, 8, 6, 24, 24])
+
+
+def test_fcc_and_bcc_coordination():
+    a = 4.0
+    fcc = np.array([[0, 0, 0], [0, .5, .5], [.5, 0, .5], [.5, .5, 0]]) * a + 0.1
+    ei, ej, sh, rp = _one(fcc, [a] * 3, 3.0)          # nn = a/sqrt2 = 2.83
+    assert np.all(np.diff(rp) == 12)
+    ei, ej, sh, rp = _one(fcc, [a] * 3, 4.2)          # + 6 at a
+    assert np.all(np.diff(rp) == 18)
+    a = 3.0
+    bcc = np.array([[0, 0, 0], [.5, .5, .5]]) * a + 0.2
+    ei, ej, sh, rp = _one(bcc, [a] * 3, 2.8)          # nn = a*sqrt3/2 = 2.60
+    assert np.all(np.diff(rp) == 8)
+    ei, ej, sh, rp = _one(bcc, [a] * 3, 3.5)          # + 6 at a
+    assert np.all(np.diff(rp) == 14)
+
+
+def test_against_periodic_kdtree_on_large_cells():
+    rng = np.random.default_rng(3)
+    L = np.array([14.0, 15.5, 17.0], np.float32)
+    pos = (rng.random((300, 3)) * L).astype(np.float32)
+    rc = 4.0                                          # < L/2: at most one image per pair
+    ei, ej, sh, rp = _one(pos, L, rc)
+    tree = cKDTree(pos.astype(np.float64), boxsize=L.astype(np.float64))
+    pairs = tree.query_pairs(rc - 1e-4, output_type="ndarray")
+    pairs_outer = tree.query_pairs(rc + 1e-4, output_type="ndarray")
+    got = set(zip(ei.tolist(), ej.tolist()))
+    inner = {(int(i), int(j)) for i, j in pairs} | {(int(j), int(i)) for i, j in pairs}
+    outer = {(int(i), int(j)) for i, j in pairs_outer} | {(int(j), int(i)) for i, j in pairs_outer}
+    assert inner <= got <= outer
+    assert len(got) == ei.size                        # one image per pair
+
+
+def test_canonical_order_symmetry_and_cutoff():
+    b = make_batch("tiny")
+    ei, ej, sh, rp = neighbor_list(b.pos, b.cell, b.offsets, b.model.r_cut)
+    N = b.pos.shape[0]
+    rev = reverse_map(ei, ej, sh, N)                  # raises unless symmetric and sorted
+    assert np.array_equal(rev[rev], np.arange(ei.size))
+    assert np.array_equal(ei[rev], ej) and np.array_equal(sh[rev], -sh)
+    # all within the structure, no self edge at n = 0
+    sid = np.searchsorted(b.offsets, np.arange(N), side="right") - 1
+    assert np.array_equal(sid[ei], sid[ej])
+    assert not np.any((ei == ej) & np.all(sh == 0, axis=1))
+    d = b.pos[ej].astype(np.float64) - b.pos[ei] + sh * np.diagonal(b.cell[sid[ei]], axis1=1, axis2=2)
+    assert np.sqrt((d * d).sum(1)).max() < b.model.r_cut + 1e-5
+
+
+def test_small_cell_has_self_images_and_multi_images():
+    # L = 4.3 < rc = 6: an atom sees its own images and several images of each neighbour
+    rng = np.random.default_rng(5)
+    pos = (rng.random((8, 3)) * 4.3).astype(np.float32)
+    ei, ej, sh, rp = _one(pos, [4.3] * 3, 6.0)
+    assert image_range(np.diag([4.3] * 3), 6.0) == (2, 2, 2)
+    assert np.any(ei == ej)
+    pairs, counts = np.unique(ei.astype(np.int64) * 8 + ej, return_counts=True)
+    assert counts.max() > 1
+    reverse_map(ei, ej, sh, 8)
+    # brute force on the tiny input: loop over every (i, j, n) candidate
+    rc2 = np.float32(6.0) * np.float32(6.0)
+    L = np.float32(4.3)
+    want = []
+    for i in range(8):
+        for j in range(8):
+            for nx in range(-2, 3):
+                for ny in range(-2, 3):
+                    for nz in range(-2, 3):
+                        if i == j and nx == ny == nz == 0:
+                            continue
+                        dx = (pos[j, 0] - pos[i, 0]) + np.float32(nx) * L
+                        dy = (pos[j, 1] - pos[i, 1]) + np.float32(ny) * L
+                        dz = (pos[j, 2] - pos[i, 2]) + np.float32(nz) * L
+                        if (dx * dx + dy * dy) + dz * dz < rc2:
+                            want.append((i, j, nx, ny, nz))
+    got = [(int(a), int(b_), *map(int, s)) for a, b_, s in zip(ei, ej, sh)]
+    assert got == want
+
+
+@pytest.mark.parametrize("name", ["tiny", "small"])
+def test_mean_degree_matches_density(name):
+    b = make_batch(name)
+    wl = WORKLOADS[name]
+    ei, ej, sh, rp = neighbor_list(b.pos, b.cell, b.offsets, b.model.r_cut)
+    expect = 4.0 / 3.0 * np.pi * b.model.r_cut ** 3 * wl.density
+    got = ei.size / b.pos.shape[0]
+    assert abs(got / expect - 1.0) < 0.05
+
+
+def test_triplets_are_ordered_pairs_of_short_bonds():
+    b = make_batch("tiny", n_struct=2)
+    ei, ej, sh, rp = neighbor_list(b.pos, b.cell, b.offsets, 4.0)
+    te, te2, trp = triplet_list(ei, ej, sh, b.pos, b.cell, b.offsets, rp, 3.0)
+    assert np.all(te != te2) and np.array_equal(ei[te], ei[te2])
+    # per centre: n_short * (n_short - 1) ordered pairs
+    d = b.pos[ej].astype(np.float64) - b.pos[ei] + sh * np.diagonal(b.cell[0])
+    short = np.sqrt((d * d).sum(1)) < 3.0
+    ns = np.bincount(ei[short], minlength=b.pos.shape[0])
+    assert te.size == int((ns * (ns - 1)).sum())
+    key = te.astype(np.int64) * ei.size + te2
+    assert np.all(np.diff(key) > 0)

@@ -1,0 +1,69 @@
+"""Third implementation on the tiny workload: the model's forward written with
+torch float64 CPU ops, forces from torch.autograd (create_graph=True) and the
+weight gradients from a second autograd pass.  Its derivatives are derived by
+the library, not by hand, so it pins the oracle's hand-derived force and
+second-order sweeps."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle.model import training_step
+from paper_2604_15821_amd.synth import make_batch
+
+
+def _torch_step(b, aux):
+    g, rts = aux["graph"], aux["routing"]
+    m = b.model
+    dt = torch.float64
+    pos = torch.tensor(b.pos, dtype=dt, requires_grad=True)
+    cell = torch.tensor(b.cell, dtype=dt)
+    W = {k: torch.tensor(v, dtype=dt, requires_grad=not k.endswith("beta")) for k, v in b.weights.items()}
+    Z = torch.tensor(b.species, dtype=torch.long)
+    ei = torch.tensor(g.ei, dtype=torch.long)
+    ej = torch.tensor(g.ej, dtype=torch.long)
+    sid = torch.tensor(g.struct_of_atom, dtype=torch.long)
+    shift = torch.tensor(g.shift, dtype=dt)
+    d = pos[ej] - pos[ei] + torch.einsum("ek,ekc->ec", shift, cell[sid[ei]])
+    r = torch.sqrt((d * d).sum(1))
+    n = torch.arange(1, m.n_rbf + 1, dtype=dt)
+    x = r / m.r_cut
+    u = 1 - 28 * x ** 6 + 48 * x ** 7 - 21 * x ** 8
+    B = (2.0 / m.r_cut) ** 0.5 * torch.sin(n[None] * np.pi * r[:, None] / m.r_cut) / r[:, None] * u[:, None]
+    h = W["A"][Z]
+    N = pos.shape[0]
+    for t in range(m.n_blocks):
+        p = f"blocks.{t}."
+        X = (B @ W[p + "W_b"]) * h[ej]
+        prob = torch.softmax(W[p + "Pc"][Z[ei]] + W[p + "Pn"][Z[ej]] + W[p + "beta"], dim=1)
+        eid = torch.tensor(rts[t].eid, dtype=torch.long)
+        msg = torch.zeros_like(X)
+        for c in range(m.top_k):
+            for xx in range(m.n_experts):
+                rows = torch.nonzero(eid[:, c] == xx).flatten()
+                if rows.numel() == 0:
+                    continue
+                y = torch.nn.functional.silu(X[rows] @ W[p + "W1"][xx]) @ W[p + "W2"][xx]
+                msg = msg.index_add(0, rows, prob[rows, xx][:, None] * y)
+        h = h.index_add(0, ei, msg)
+    eps = torch.nn.functional.silu(h @ W["W_o1"]) @ W["w_o2"]
+    E = torch.zeros(b.n_struct, dtype=dt).index_add(0, sid, eps)
+    F = -torch.autograd.grad(E.sum(), pos, create_graph=True)[0]
+    nat = torch.tensor(np.diff(b.offsets), dtype=dt)
+    loss = ((E / nat - torch.tensor(b.E_ref, dtype=dt)) ** 2).mean() \
+        + ((F - torch.tensor(b.F_ref, dtype=dt)) ** 2).sum() / (3 * N)
+    names = [k for k in W if not k.endswith("beta")]
+    grads = torch.autograd.grad(loss, [W[k] for k in names])
+    return loss.item(), E.detach().numpy(), F.detach().numpy(), dict(zip(names, [x.numpy() for x in grads]))
+
+
+def test_oracle_matches_torch_double_backward_on_tiny():
+    b = make_batch("tiny")
+    loss, E, F, grad, aux = training_step(b, return_aux=True)
+    tl, tE, tF, tg = _torch_step(b, aux)
+    assert loss == pytest.approx(tl, rel=1e-12)
+    np.testing.assert_allclose(E, tE, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(F, tF, rtol=1e-9, atol=1e-12)
+    for k, v in tg.items():
+        scale = np.abs(v).max()
+        np.testing.assert_allclose(grad[k], v, rtol=0, atol=1e-9 * scale + 1e-15, err_msg=k)
