@@ -1,0 +1,240 @@
+/*
+ * janus.h -- C ABI of the MI355X training-step library for the MoE
+ * interatomic potential (MatRIS-MoE, arXiv 2604.15821).
+ *
+ * The library computes one full training step of an invariant
+ * message-passing potential whose per-block edge MLP is a top-k
+ * Mixture-of-Experts layer: the forward pass to per-structure energies,
+ * the first backward pass to forces F = -dE/dR, and the second-order
+ * backward pass of an energy-plus-force loss to every weight gradient
+ * (paper Sec. "Overview of the problem": the force loss needs second
+ * derivatives and makes training roughly twice as expensive; Sec.
+ * "Runtime for multi-phase double-backward execution": forward, first
+ * backward for the forces, double backward for the force loss, final
+ * backward for the energy loss).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every array argument is a DEVICE pointer owned by the caller, unless
+ *    the comment says "host".  The library keeps no caller pointer after
+ *    a call returns.
+ *  - Floating-point arrays are IEEE fp32, integer arrays int32, unless
+ *    noted.  Matrices are row-major.
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL is the default stream).  Outputs are valid once the stream has
+ *    been synchronised.  janus_build_edges and janus_step each perform one
+ *    small synchronous device-to-host read (edge count, input validation
+ *    flag) on that stream before they launch the rest of their work.
+ *  - Return value: JANUS_OK (0) or a negative JANUS_E* code; a message for
+ *    it comes from janus_strerror().  On error no output has been written,
+ *    except *n_edges for JANUS_ECAPACITY.
+ *  - Results are deterministic run to run: no kernel uses floating-point
+ *    atomics; every reduction has a fixed order.
+ *  - A context is bound to the device that was current when it was created
+ *    and must be used from one host thread at a time.
+ */
+#ifndef JANUS_H
+#define JANUS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  JANUS_OK = 0,
+  JANUS_EINVAL = -1,       /* bad argument: sizes, offsets, species or edge indices */
+  JANUS_ECAPACITY = -2,    /* edge buffers too small; *n_edges holds the count needed */
+  JANUS_ENOMEM = -3,       /* device allocation of the context workspace failed */
+  JANUS_EHIP = -4,         /* a HIP runtime call failed */
+  JANUS_EUNSUPPORTED = -5  /* valid input that this build does not handle (non-diagonal cell,
+                              widths that are not multiples of 64, ...) */
+};
+
+/*
+ * Model hyper-parameters (paper Sec. "Model scaling", Table 2, for the
+ * meaning of width / experts / top-k; the radial basis, envelope and loss
+ * weights are the readings stated in the oracle and the design notes).
+ *   n_species  size of the element vocabulary (89)
+ *   d          atom / edge feature width; multiple of 64
+ *   n_rbf      number of Bessel radial functions (1..32)
+ *   n_blocks   number of interaction blocks T (>= 0)
+ *   n_experts  experts per edge-MoE layer (1..64)
+ *   top_k      experts per edge token (1..n_experts, at most 4)
+ *   d_hidden   expert hidden width; multiple of 64
+ *   env_p      envelope exponent; only 6 is implemented
+ *   r_cut      neighbour cutoff in Angstrom
+ *   three_body non-zero enables the angular triplet term (not in this build:
+ *              JANUS_EUNSUPPORTED)
+ *   w_E, w_F   loss weights of the energy and force terms
+ */
+typedef struct janus_config {
+  int32_t n_species;
+  int32_t d;
+  int32_t n_rbf;
+  int32_t n_blocks;
+  int32_t n_experts;
+  int32_t top_k;
+  int32_t d_hidden;
+  int32_t env_p;
+  float r_cut;
+  int32_t three_body;
+  float r_cut3;
+  int32_t n_experts3;
+  int32_t top_k3;
+  int32_t d_hidden3;
+  int32_t n_legendre;
+  float w_E;
+  float w_F;
+} janus_config;
+
+typedef struct janus_ctx janus_ctx;
+
+/* One entry of the flat weight blob (host struct, filled by janus_weight_layout). */
+typedef struct janus_tensor_desc {
+  char name[48];      /* e.g. "A", "blocks.0.W1", "W_o1" */
+  int64_t offset;     /* in floats from the start of the blob */
+  int32_t ndim;
+  int64_t shape[3];
+} janus_tensor_desc;
+
+/*
+ * Neighbour list in canonical order (paper Sec. "MatRIS": the graph
+ * generation module turns a periodically repeated structure into an atom
+ * graph).  Edge e = (i, j, n) joins atom i to the image of atom j shifted by
+ * the integer lattice vector n; edges are sorted by (i, j, n_a, n_b, n_c).
+ *   n_edges  number of directed edges Ne (host value)
+ *   ei, ej   [Ne] centre and neighbour atom
+ *   shift    [Ne*3] int8 lattice shift n
+ *   rowptr   [N+1] CSR offsets of the edges of each centre atom
+ *   rev      [Ne] index of the reverse edge (j, i, -n)
+ */
+typedef struct janus_edges {
+  int64_t n_edges;
+  const int32_t* ei;
+  const int32_t* ej;
+  const int8_t* shift;
+  const int32_t* rowptr;
+  const int32_t* rev;
+} janus_edges;
+
+/*
+ * Optional debug outputs of janus_step (any pointer may be NULL).
+ *   eid     [T*Ne*top_k] int32  chosen experts, descending logit, lower index on ties
+ *   gate    [T*Ne*top_k] fp32   softmax probability of each chosen expert
+ *   counts  [T*n_experts] int32 tokens routed to each expert
+ *   pos     [T*Ne*top_k] int32  slot of (edge, choice) in the expert-grouped order
+ *   basis   [Ne*n_rbf]   fp32   Bessel basis with envelope at each edge length
+ */
+typedef struct janus_debug {
+  int32_t* eid;
+  float* gate;
+  int32_t* counts;
+  int32_t* pos;
+  float* basis;
+} janus_debug;
+
+/* Create a context for `cfg` on the current device.  The context owns its
+ * workspace, which grows on demand inside janus_step and is freed by
+ * janus_destroy.  Errors: JANUS_EINVAL (cfg out of range),
+ * JANUS_EUNSUPPORTED, JANUS_EHIP. */
+int janus_create(const janus_config* cfg /* host */, janus_ctx** out /* host */);
+
+/* Free the context and its workspace (NULL is ignored).  The caller must
+ * have synchronised every stream the context was used on. */
+void janus_destroy(janus_ctx* ctx);
+
+/* Layout of the flat weight blob for `cfg`.  Order: A [n_species, d]; for
+ * each block t: W_b [n_rbf, d], Pc [n_species, E], Pn [n_species, E],
+ * beta [E], W1 [E, d, d_hidden], W2 [E, d_hidden, d]; then W_o1 [d, d],
+ * w_o2 [d].  If `out` is NULL only the counts are written.  *n_tensors (in:
+ * capacity of out, out: number of tensors) and *n_floats (total blob size)
+ * are host pointers.  Errors: JANUS_EINVAL (capacity too small). */
+int janus_weight_layout(const janus_config* cfg, janus_tensor_desc* out, int32_t* n_tensors,
+                        int64_t* n_floats);
+
+/*
+ * Build the neighbour list of a batch (paper Sec. "MatRIS", graph
+ * generation).  An edge is kept iff, in fp32 with each operation rounded
+ * separately (no fused multiply-add),
+ *     s_k  = (n_a * a_k + n_b * b_k) + n_c * c_k
+ *     d_k  = (X_j,k - X_i,k) + s_k
+ *     r2   = (d_x * d_x + d_y * d_y) + d_z * d_z  <  r_cut * r_cut
+ * with i, j in the same structure and (i, n) != (j, 0); n_k ranges over
+ * [-m_k, m_k], m_k = floor(r_cut / L_k) + 1.
+ *   pos     [N*3] Cartesian positions; the image range above covers every
+ *           neighbour when they are wrapped into the cell
+ *   cell    [S*9] lattice rows a, b, c of each structure; must be diagonal
+ *           with positive entries (JANUS_EUNSUPPORTED otherwise)
+ *   offsets [S+1] structure s owns atoms offsets[s] .. offsets[s+1]-1;
+ *           offsets[0] = 0, non-decreasing, offsets[S] = N
+ *   capacity  size of the edge buffers in edges
+ *   ei, ej, rev [capacity], shift [capacity*3] int8, rowptr [N+1]: outputs
+ *   n_edges (host) receives Ne
+ * Two-call pattern: if Ne > capacity, returns JANUS_ECAPACITY with *n_edges
+ * set and nothing else written.  Errors: JANUS_EINVAL (bad offsets or
+ * sizes), JANUS_EUNSUPPORTED (cell), JANUS_EHIP.
+ */
+int janus_build_edges(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* offsets,
+                      int32_t n_atoms, int32_t n_struct, int64_t capacity, int32_t* ei, int32_t* ej,
+                      int8_t* shift, int32_t* rowptr, int32_t* rev, int64_t* n_edges, void* stream);
+
+/*
+ * One training step (paper Sec. "Runtime for multi-phase double-backward
+ * execution": forward, force backward, double backward of the force loss,
+ * final backward of the energy loss).
+ *   pos [N*3], cell [S*9], species [N] in 0..n_species-1, offsets [S+1]
+ *   nl        neighbour list from janus_build_edges for the same positions
+ *   W         flat weight blob (janus_weight_layout)
+ *   E_ref [S] reference energy per atom of each structure; F_ref [N*3]
+ * Outputs:
+ *   loss [1]   w_E/S * sum_s (E_s/n_s - E_ref_s)^2 + w_F/(3N) * sum |F - F_ref|^2
+ *   E [S]      per-structure energies
+ *   F [N*3]    forces -dE/dR
+ *   dLdW       gradient of loss with respect to W, same layout as W; the
+ *              routing biases beta receive exactly zero
+ *   dbg        optional debug outputs (may be NULL)
+ * Inputs are validated on the device first (species range, offsets, edge
+ * indices, CSR and reverse map); a failure returns JANUS_EINVAL and writes
+ * nothing.  Errors: JANUS_EINVAL, JANUS_ENOMEM (workspace), JANUS_EHIP.
+ */
+int janus_step(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
+               const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
+               const float* W, const float* E_ref, const float* F_ref, float* loss, float* E,
+               float* F, float* dLdW, const janus_debug* dbg, void* stream);
+
+/*
+ * Grouped fp32 GEMM on the matrix cores, the building block of the expert
+ * layers (paper Sec. "Platform-specific optimizations": MoE dispatch and
+ * combine with batched GEMM invocation).  Rows of A and C are grouped:
+ * group g owns rows row_off[g] .. row_off[g+1]-1 (row_off on the device,
+ * non-decreasing, row_off[0] = 0, row_off[n_groups] = M).
+ *   trans_b = 0:  C[r, :] = A[r, :] (K) x B_g,   B_g = B + g*K*N stored [K, N]
+ *   trans_b = 1:  C[r, :] = A[r, :] (K) x B_g^T, B_g = B + g*N*K stored [N, K]
+ * A [M*K], C [M*N]; K and N multiples of 16 and 64 respectively.
+ * Errors: JANUS_EINVAL, JANUS_EHIP.
+ */
+int janus_grouped_gemm(janus_ctx* ctx, const float* A, const float* B, float* C,
+                       const int32_t* row_off, int32_t n_groups, int64_t M, int32_t K, int32_t N,
+                       int32_t trans_b, void* stream);
+
+/*
+ * Grouped weight-gradient GEMM: for each group g,
+ *   G_g[p, q] = sum over rows r of group g of  A[r, p] * B[r, q]
+ * with A [M*P], B [M*Q], G [n_groups*P*Q]; P, Q multiples of 4.  Groups
+ * with no rows produce exact zeros.  The sum is split over row chunks and
+ * reduced in a fixed order.  Errors: JANUS_EINVAL, JANUS_EHIP.
+ */
+int janus_grouped_wgrad(janus_ctx* ctx, const float* A, const float* B, float* G,
+                        const int32_t* row_off, int32_t n_groups, int64_t M, int32_t P, int32_t Q,
+                        void* stream);
+
+/* Static message for a return code. */
+const char* janus_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JANUS_H */

@@ -1,0 +1,173 @@
+// Tables, chunk reduction and the standalone grouped-GEMM entry points.
+#include <cstring>
+
+#include "internal.h"
+
+namespace janus {
+
+__global__ void build_rows_tiles_kernel(const int* __restrict__ row_off, int n_groups, RowsTile* tiles,
+                                        int* n_tiles) {
+  __shared__ int pre[1025];
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int g = 0; g < n_groups; ++g) {
+      pre[g] = acc;
+      int m = row_off[g + 1] - row_off[g];
+      acc += (m + GBM - 1) / GBM;
+    }
+    pre[n_groups] = acc;
+    *n_tiles = acc;
+  }
+  __syncthreads();
+  const int total = pre[n_groups];
+  for (int t = threadIdx.x; t < total; t += blockDim.x) {
+    int lo = 0, hi = n_groups;   // pre[lo] <= t < pre[hi]
+    while (hi - lo > 1) {
+      int mid = (lo + hi) >> 1;
+      if (pre[mid] <= t) lo = mid; else hi = mid;
+    }
+    RowsTile e;
+    e.group = lo;
+    e.r0 = row_off[lo] + (t - pre[lo]) * GBM;
+    e.r1 = row_off[lo + 1];
+    e.pad = 0;
+    tiles[t] = e;
+  }
+}
+
+__global__ void build_wchunks_kernel(const int* __restrict__ row_off, int n_groups, int kc, WChunk* chunks,
+                                     int* n_chunks, int* chunk_first) {
+  __shared__ int pre[1025];
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int g = 0; g < n_groups; ++g) {
+      pre[g] = acc;
+      chunk_first[g] = acc;
+      int m = row_off[g + 1] - row_off[g];
+      acc += (m + kc - 1) / kc;
+    }
+    pre[n_groups] = acc;
+    chunk_first[n_groups] = acc;
+    *n_chunks = acc;
+  }
+  __syncthreads();
+  const int total = pre[n_groups];
+  for (int t = threadIdx.x; t < total; t += blockDim.x) {
+    int lo = 0, hi = n_groups;
+    while (hi - lo > 1) {
+      int mid = (lo + hi) >> 1;
+      if (pre[mid] <= t) lo = mid; else hi = mid;
+    }
+    WChunk e;
+    e.group = lo;
+    e.r0 = row_off[lo] + (t - pre[lo]) * kc;
+    e.r1 = min(e.r0 + kc, row_off[lo + 1]);
+    e.pad = 0;
+    chunks[t] = e;
+  }
+}
+
+__global__ void wgrad_reduce_kernel(const float* __restrict__ partial, const int* __restrict__ chunk_first,
+                                    int n_groups, long long PQ, float* __restrict__ G, int accumulate) {
+  const int g = blockIdx.y;
+  const long long i4 = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (4 * i4 >= PQ) return;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4* out = reinterpret_cast<float4*>(G + (long long)g * PQ) + i4;
+  if (accumulate) s = *out;
+  const int c0 = chunk_first[g], c1 = chunk_first[g + 1];
+  for (int c = c0; c < c1; ++c) {
+    float4 v = reinterpret_cast<const float4*>(partial + (long long)c * PQ)[i4];
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  *out = s;
+}
+
+void launch_wgrad_reduce(hipStream_t st, const float* partial, const int* chunk_first, int groups,
+                         long long PQ, float* G, int accumulate) {
+  dim3 rg(cdiv(PQ / 4, 256), groups);
+  hipLaunchKernelGGL(wgrad_reduce_kernel, rg, dim3(256), 0, st, partial, chunk_first, groups, PQ, G, accumulate);
+}
+
+// Tile and chunk tables from group row offsets (one workgroup).
+void build_tables(hipStream_t st, const int* row_off, int groups, int kc, RowsTile* tiles, int* n_tiles,
+                  WChunk* chunks, int* n_chunks, int* chunk_first) {
+  if (tiles) hipLaunchKernelGGL(build_rows_tiles_kernel, dim3(1), dim3(256), 0, st, row_off, groups, tiles, n_tiles);
+  if (chunks)
+    hipLaunchKernelGGL(build_wchunks_kernel, dim3(1), dim3(256), 0, st, row_off, groups, kc, chunks, n_chunks,
+                       chunk_first);
+}
+
+int ensure(janus_buffer& b, size_t bytes) {
+  if (bytes <= b.bytes && b.ptr) return JANUS_OK;
+  if (b.ptr) {
+    hipError_t e = hipFree(b.ptr);
+    b.ptr = nullptr;
+    b.bytes = 0;
+    if (e != hipSuccess) return janus_set_hip_error(e);
+  }
+  size_t want = bytes < 256 ? 256 : bytes;
+  if (hipMalloc(&b.ptr, want) != hipSuccess) {
+    (void)hipGetLastError();
+    b.ptr = nullptr;
+    return JANUS_ENOMEM;
+  }
+  b.bytes = want;
+  return JANUS_OK;
+}
+
+}  // namespace janus
+
+using namespace janus;
+
+extern "C" int janus_grouped_gemm(janus_ctx* ctx, const float* A, const float* B, float* C,
+                                  const int32_t* row_off, int32_t n_groups, int64_t M, int32_t K, int32_t N,
+                                  int32_t trans_b, void* stream) {
+  if (!ctx || (M > 0 && (!A || !C)) || !B || !row_off || n_groups < 1 || n_groups > 1024 || M < 0 || M > INT32_MAX ||
+      K <= 0 || K % GBK || N <= 0 || N % 64)
+    return JANUS_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int mt = max_rows_tiles(M, n_groups);
+  Carver cv(nullptr);
+  cv.take<RowsTile>(mt);
+  cv.take<int>(1);
+  int rc = ensure(ctx->aux, cv.size());
+  if (rc) return rc;
+  Carver c2(ctx->aux.ptr);
+  RowsTile* tiles = c2.take<RowsTile>(mt);
+  int* nt = c2.take<int>(1);
+  build_tables(st, row_off, n_groups, 0, tiles, nt, nullptr, nullptr, nullptr);
+  if (trans_b)
+    launch_rows<true>(st, LoadPlain{A, K}, B, K, N, tiles, nt, mt, EpiStore{C, N});
+  else
+    launch_rows<false>(st, LoadPlain{A, K}, B, K, N, tiles, nt, mt, EpiStore{C, N});
+  JANUS_HIP_TRY(hipGetLastError());
+  return JANUS_OK;
+}
+
+extern "C" int janus_grouped_wgrad(janus_ctx* ctx, const float* A, const float* B, float* G,
+                                   const int32_t* row_off, int32_t n_groups, int64_t M, int32_t P, int32_t Q,
+                                   void* stream) {
+  if (!ctx || (M > 0 && (!A || !B)) || !G || !row_off || n_groups < 1 || n_groups > 1024 || M < 0 || M > INT32_MAX ||
+      P <= 0 || P % 4 || Q <= 0 || Q % 4)
+    return JANUS_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int kc = wgrad_chunk_rows(M, P, Q);
+  const int mc = max_wchunks(M, n_groups, kc);
+  Carver cv(nullptr);
+  cv.take<WChunk>(mc);
+  cv.take<int>(1);
+  cv.take<int>(n_groups + 1);
+  cv.take<float>((size_t)mc * P * Q);
+  int rc = ensure(ctx->aux, cv.size());
+  if (rc) return rc;
+  Carver c2(ctx->aux.ptr);
+  WChunk* chunks = c2.take<WChunk>(mc);
+  int* nc = c2.take<int>(1);
+  int* first = c2.take<int>(n_groups + 1);
+  float* partial = c2.take<float>((size_t)mc * P * Q);
+  build_tables(st, row_off, n_groups, kc, nullptr, nullptr, chunks, nc, first);
+  launch_wgrad(st, LoadPlain{A, P}, LoadPlain{B, Q}, P, Q, chunks, nc, first, mc, n_groups, partial, G, 0);
+  JANUS_HIP_TRY(hipGetLastError());
+  return JANUS_OK;
+}

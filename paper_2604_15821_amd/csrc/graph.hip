@@ -1,0 +1,285 @@
+// Neighbour list, reverse-edge map, edge geometry and the radial basis.
+//
+// Paper Sec. "MatRIS": the graph generation module repeats a structure
+// periodically and connects atoms closer than the cutoff; the embedding
+// module turns distances into edge features.  The inclusion rule (an fp32
+// expression with a fixed operation order and no fused multiply-add), the
+// canonical (i, j, n) order and the basis are the readings documented with
+// janus_build_edges and in the design notes.
+#include <cmath>
+
+#include "internal.h"
+#include "kernels.h"
+
+namespace janus {
+
+// Image half-widths m_k = floor(r_cut / L_k) + 1 of a diagonal cell.
+__device__ __forceinline__ void image_range(const float* L, float rc, int& mx, int& my, int& mz) {
+  mx = (int)floor((double)rc / (double)L[0]) + 1;
+  my = (int)floor((double)rc / (double)L[4]) + 1;
+  mz = (int)floor((double)rc / (double)L[8]) + 1;
+}
+
+__global__ void validate_struct_kernel(const int* __restrict__ offsets, int S, int N, const float* __restrict__ cell,
+                                       float rc, int* __restrict__ flag) {
+  int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s > S) return;
+  int bad = 0;
+  if (s == 0 && offsets[0] != 0) bad |= 1;
+  if (s == S && offsets[S] != N) bad |= 1;
+  if (s < S) {
+    if (offsets[s] > offsets[s + 1]) bad |= 1;
+    if (rc > 0.f) {
+      const float* L = cell + 9 * s;
+      if (L[1] != 0.f || L[2] != 0.f || L[3] != 0.f || L[5] != 0.f || L[6] != 0.f || L[7] != 0.f) bad |= 2;
+      if (!(L[0] > 0.f) || !(L[4] > 0.f) || !(L[8] > 0.f)) bad |= 2;
+      // image shifts are stored as int8 and the candidate count must stay small
+      else if ((double)rc / L[0] > 60.0 || (double)rc / L[4] > 60.0 || (double)rc / L[8] > 60.0) bad |= 2;
+    }
+  }
+  if (bad) atomicOr(flag, bad);
+}
+
+// sid[a] = structure of atom a (clamped so that bad offsets cannot write out of range).
+__global__ void atom_struct_kernel(const int* __restrict__ offsets, int S, int N, int* __restrict__ sid) {
+  int s = blockIdx.x;
+  if (s >= S) return;
+  int a0 = max(0, min(N, offsets[s])), a1 = max(0, min(N, offsets[s + 1]));
+  for (int a = a0 + threadIdx.x; a < a1; a += blockDim.x) sid[a] = s;
+}
+
+// One wave per centre atom; candidates (j, image) are tested 64 at a time in
+// canonical order and compacted with a ballot, so the output order is exact.
+template <bool WRITE>
+__global__ void nl_kernel(const float* __restrict__ pos, const float* __restrict__ cell,
+                          const int* __restrict__ offsets, const int* __restrict__ sid, float rc, int N,
+                          int* __restrict__ count, const int* __restrict__ rowptr, int* __restrict__ ei,
+                          int* __restrict__ ej, int8_t* __restrict__ shift) {
+  const int i = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  if (i >= N) return;
+  const int s = sid[i];
+  const int a = offsets[s], n = offsets[s + 1] - a;
+  const float* L = cell + 9 * s;
+  int mx, my, mz;
+  image_range(L, rc, mx, my, mz);
+  const int ny = 2 * my + 1, nz = 2 * mz + 1;
+  const int nimg = (2 * mx + 1) * ny * nz;
+  const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
+  const float rc2 = __fmul_rn(rc, rc);
+  const long long ncand = (long long)n * nimg;
+  const int base = WRITE ? rowptr[i] : 0;
+  int cnt = 0;
+  for (long long c0 = 0; c0 < ncand; c0 += 64) {
+    const long long c = c0 + lane;
+    bool keep = false;
+    int j = 0, ix = 0, iy = 0, iz = 0;
+    if (c < ncand) {
+      j = a + (int)(c / nimg);
+      const int im = (int)(c % nimg);
+      ix = im / (ny * nz) - mx;
+      iy = (im / nz) % ny - my;
+      iz = im % nz - mz;
+      const float fx = (float)ix, fy = (float)iy, fz = (float)iz;
+      const float sx = __fadd_rn(__fadd_rn(__fmul_rn(fx, L[0]), __fmul_rn(fy, L[3])), __fmul_rn(fz, L[6]));
+      const float sy = __fadd_rn(__fadd_rn(__fmul_rn(fx, L[1]), __fmul_rn(fy, L[4])), __fmul_rn(fz, L[7]));
+      const float sz = __fadd_rn(__fadd_rn(__fmul_rn(fx, L[2]), __fmul_rn(fy, L[5])), __fmul_rn(fz, L[8]));
+      const float dx = __fadd_rn(__fsub_rn(pos[3 * j], xi), sx);
+      const float dy = __fadd_rn(__fsub_rn(pos[3 * j + 1], yi), sy);
+      const float dz = __fadd_rn(__fsub_rn(pos[3 * j + 2], zi), sz);
+      const float r2 = __fadd_rn(__fadd_rn(__fmul_rn(dx, dx), __fmul_rn(dy, dy)), __fmul_rn(dz, dz));
+      keep = (r2 < rc2) && !(j == i && ix == 0 && iy == 0 && iz == 0);
+    }
+    const unsigned long long m = __ballot(keep);
+    if (WRITE && keep) {
+      const int p = base + cnt + __popcll(m & ((1ull << lane) - 1ull));
+      ei[p] = i;
+      ej[p] = j;
+      shift[3 * p] = (int8_t)ix;
+      shift[3 * p + 1] = (int8_t)iy;
+      shift[3 * p + 2] = (int8_t)iz;
+    }
+    cnt += __popcll(m);
+  }
+  if (!WRITE && lane == 0) count[i] = cnt;
+}
+
+// Exclusive scan of n int32 values into out[0..n] (one workgroup of 1024).
+// out[n] is the total; totals that do not fit int32 raise flag bit 4.
+__global__ void exclusive_scan_kernel(const int* __restrict__ in, int n, int* __restrict__ out,
+                                      int* __restrict__ flag) {
+  __shared__ long long part[1024];
+  const int t = threadIdx.x;
+  const int per = (n + 1023) / 1024;
+  const int lo = min(n, t * per), hi = min(n, lo + per);
+  long long s = 0;
+  for (int k = lo; k < hi; ++k) s += in[k];
+  part[t] = s;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    long long v = t >= o ? part[t - o] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  long long run = part[t] - s;
+  for (int k = lo; k < hi; ++k) {
+    out[k] = (int)run;
+    run += in[k];
+  }
+  if (t == 1023) {
+    out[n] = (int)part[1023];
+    if (part[1023] > 0x7fffffffLL && flag) atomicOr(flag, 16);
+  }
+}
+
+// rev[e] = the edge (j, i, -n), found by binary search in the sorted segment of j.
+__global__ void reverse_kernel(const int* __restrict__ ei, const int* __restrict__ ej,
+                               const int8_t* __restrict__ shift, const int* __restrict__ rowptr, int Ne,
+                               int* __restrict__ rev, int* __restrict__ flag) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  const int i = ei[e], j = ej[e];
+  const int kx = -shift[3 * e], ky = -shift[3 * e + 1], kz = -shift[3 * e + 2];
+  // key of an edge within the segment of j: (ej, sx, sy, sz) lexicographic
+  auto less = [&](int f) {
+    int fj = ej[f];
+    if (fj != i) return fj < i;
+    int fx = shift[3 * f], fy = shift[3 * f + 1], fz = shift[3 * f + 2];
+    if (fx != kx) return fx < kx;
+    if (fy != ky) return fy < ky;
+    return fz < kz;
+  };
+  int lo = rowptr[j], hi = rowptr[j + 1];
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if (less(mid)) lo = mid + 1; else hi = mid;
+  }
+  bool ok = lo < rowptr[j + 1] && ej[lo] == i && shift[3 * lo] == kx && shift[3 * lo + 1] == ky &&
+            shift[3 * lo + 2] == kz;
+  rev[e] = ok ? lo : e;
+  if (!ok) atomicOr(flag, 8);
+}
+
+// Edge geometry in float64 from the fp32 inputs, then stored as fp32:
+// d = X_j + n.L - X_i, r = |d|, u = d / r, and the Bessel basis with the p = 6
+// polynomial envelope and its radial derivative,
+//   B_n(r)  = sqrt(2/rc) sin(n pi r / rc) / r * u(r / rc),
+//   u(x)    = 1 - 28 x^6 + 48 x^7 - 21 x^8   (x < 1).
+__global__ void geometry_kernel(const float* __restrict__ pos, const float* __restrict__ cell,
+                                const int* __restrict__ sid, const int* __restrict__ ei,
+                                const int* __restrict__ ej, const int8_t* __restrict__ shift, int Ne,
+                                float rc, int nb, float4* __restrict__ geo, float* __restrict__ B,
+                                float* __restrict__ dB) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  const int i = ei[e], j = ej[e];
+  const float* L = cell + 9 * sid[i];
+  const double nx = shift[3 * e], ny = shift[3 * e + 1], nz = shift[3 * e + 2];
+  double d[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k)
+    d[k] = ((double)pos[3 * j + k] - (double)pos[3 * i + k]) +
+           (nx * (double)L[k] + ny * (double)L[3 + k] + nz * (double)L[6 + k]);
+  const double r = sqrt(d[0] * d[0] + d[1] * d[1] + d[2] * d[2]);
+  geo[e] = make_float4((float)(d[0] / r), (float)(d[1] / r), (float)(d[2] / r), (float)r);
+  const double rcd = (double)rc;
+  const double x = r / rcd;
+  double u = 0.0, du = 0.0;
+  if (x < 1.0) {
+    const double x2 = x * x, x5 = x2 * x2 * x, x6 = x5 * x;
+    u = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
+    du = (-168.0 * x5 + 336.0 * x6 - 168.0 * x6 * x) / rcd;
+  }
+  const double c = sqrt(2.0 / rcd);
+  const double th = M_PI / rcd;
+  for (int n = 1; n <= nb; ++n) {
+    const double k = n * th;
+    double sn, cs;
+    sincos(k * r, &sn, &cs);
+    const double s = sn / r;
+    const double ds = (k * r * cs - sn) / (r * r);
+    B[(long long)e * nb + n - 1] = (float)(c * s * u);
+    dB[(long long)e * nb + n - 1] = (float)(c * (ds * u + s * du));
+  }
+}
+
+void launch_validate_struct(hipStream_t st, const int* offsets, int S, int N, const float* cell, float rc,
+                            int* flag) {
+  hipLaunchKernelGGL(validate_struct_kernel, dim3(cdiv(S + 1, 256)), dim3(256), 0, st, offsets, S, N, cell,
+                     rc, flag);
+}
+
+void launch_atom_struct(hipStream_t st, const int* offsets, int S, int N, int* sid) {
+  hipLaunchKernelGGL(atom_struct_kernel, dim3(S), dim3(256), 0, st, offsets, S, N, sid);
+}
+
+void launch_exclusive_scan(hipStream_t st, const int* in, int n, int* out, int* flag) {
+  hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, st, in, n, out, flag);
+}
+
+void launch_geometry(hipStream_t st, const float* pos, const float* cell, const int* sid, const int* ei,
+                     const int* ej, const int8_t* shift, int Ne, float rc, int nb, float4* geo, float* B,
+                     float* dB) {
+  if (Ne <= 0) return;
+  hipLaunchKernelGGL(geometry_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, pos, cell, sid, ei, ej, shift, Ne,
+                     rc, nb, geo, B, dB);
+}
+
+}  // namespace janus
+
+using namespace janus;
+
+extern "C" int janus_build_edges(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* offsets,
+                                 int32_t n_atoms, int32_t n_struct, int64_t capacity, int32_t* ei, int32_t* ej,
+                                 int8_t* shift, int32_t* rowptr, int32_t* rev, int64_t* n_edges, void* stream) {
+  if (!ctx || !pos || !cell || !offsets || !rowptr || !n_edges || n_atoms < 1 || n_struct < 1 || capacity < 0)
+    return JANUS_EINVAL;
+  if (capacity > 0 && (!ei || !ej || !shift || !rev)) return JANUS_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int N = n_atoms, S = n_struct;
+  Carver cv(nullptr);
+  cv.take<int>(1);
+  cv.take<int>(N);
+  cv.take<int>(N);
+  cv.take<int>(N + 1);
+  int rc = ensure(ctx->nl, cv.size());
+  if (rc) return rc;
+  Carver c2(ctx->nl.ptr);
+  int* flag = c2.take<int>(1);
+  int* sid = c2.take<int>(N);
+  int* count = c2.take<int>(N);
+  int* rp = c2.take<int>(N + 1);
+  int* hw = ctx->host_word;
+
+  JANUS_HIP_TRY(hipMemsetAsync(flag, 0, sizeof(int), st));
+  launch_validate_struct(st, offsets, S, N, cell, ctx->cfg.r_cut, flag);
+  launch_atom_struct(st, offsets, S, N, sid);
+  JANUS_HIP_TRY(hipGetLastError());
+  JANUS_HIP_TRY(hipMemcpyAsync(hw, flag, sizeof(int), hipMemcpyDeviceToHost, st));
+  JANUS_HIP_TRY(hipStreamSynchronize(st));
+  if (hw[0] & 1) return JANUS_EINVAL;
+  if (hw[0] & 2) return JANUS_EUNSUPPORTED;
+
+  const float r_cut = ctx->cfg.r_cut;
+  hipLaunchKernelGGL((nl_kernel<false>), dim3(cdiv((long long)N * 64, 256)), dim3(256), 0, st, pos, cell, offsets,
+                     sid, r_cut, N, count, nullptr, nullptr, nullptr, nullptr);
+  launch_exclusive_scan(st, count, N, rp, flag);
+  JANUS_HIP_TRY(hipGetLastError());
+  JANUS_HIP_TRY(hipMemcpyAsync(hw, rp + N, sizeof(int), hipMemcpyDeviceToHost, st));
+  JANUS_HIP_TRY(hipMemcpyAsync(hw + 1, flag, sizeof(int), hipMemcpyDeviceToHost, st));
+  JANUS_HIP_TRY(hipStreamSynchronize(st));
+  if (hw[1] & 16) return JANUS_EUNSUPPORTED;   // more than 2^31 - 1 edges
+  const long long ne = hw[0];
+  *n_edges = ne;
+  if (ne > capacity) return JANUS_ECAPACITY;
+  JANUS_HIP_TRY(hipMemcpyAsync(rowptr, rp, sizeof(int) * (N + 1), hipMemcpyDeviceToDevice, st));
+  if (ne > 0) {
+    hipLaunchKernelGGL((nl_kernel<true>), dim3(cdiv((long long)N * 64, 256)), dim3(256), 0, st, pos, cell, offsets,
+                       sid, r_cut, N, nullptr, rp, ei, ej, shift);
+    hipLaunchKernelGGL(reverse_kernel, dim3(cdiv(ne, 256)), dim3(256), 0, st, ei, ej, shift, rp, (int)ne, rev,
+                       flag);
+  }
+  JANUS_HIP_TRY(hipGetLastError());
+  return JANUS_OK;
+}

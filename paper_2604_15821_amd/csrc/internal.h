@@ -1,0 +1,85 @@
+// Host-side internals shared by the translation units of libjanus.
+#pragma once
+
+#include <vector>
+
+#include "common.h"
+#include "gemm.h"
+
+// Device memory owned by a context, grown on demand and never shrunk.
+struct janus_buffer {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
+struct janus_ctx {
+  janus_config cfg;
+  int device = 0;
+  janus_buffer ws;        // per-step workspace of janus_step
+  janus_buffer aux;       // tables and partials of the standalone GEMM entry points
+  janus_buffer nl;        // per-atom counts and flags of janus_build_edges
+  int* host_word = nullptr;   // 4 pinned host ints for the flag / count reads
+};
+
+namespace janus {
+
+// Grow `b` to at least `bytes` (contents are not preserved).
+int ensure(janus_buffer& b, size_t bytes);
+
+// Bump allocator over one device buffer; every region is 256-byte aligned.
+struct Carver {
+  uintptr_t base;
+  size_t off = 0;
+  explicit Carver(void* p) : base(reinterpret_cast<uintptr_t>(p)) {}
+  template <class T>
+  T* take(size_t n) {
+    off = (off + 255) & ~size_t(255);
+    T* p = reinterpret_cast<T*>(base + off);
+    off += n * sizeof(T);
+    return p;
+  }
+  size_t size() const { return (off + 255) & ~size_t(255); }
+};
+
+// Upper bounds on the tile / chunk tables of a grouped GEMM over M rows.
+inline int max_rows_tiles(long long M, int groups) { return (int)((M + GBM - 1) / GBM) + groups; }
+inline int max_wchunks(long long M, int groups, int kc) { return (int)((M + kc - 1) / kc) + groups; }
+
+// Chunk length of the weight-gradient contraction: long enough to keep the
+// partials small, short enough to give the GPU a few thousand workgroups.
+inline int wgrad_chunk_rows(long long M, int P, int Q) {
+  long long tiles = (long long)((P + GBM - 1) / GBM) * ((Q + GBN - 1) / GBN);
+  long long kc = 1024;
+  while (kc < 16384 && ((M + kc - 1) / kc) * tiles > 4096) kc *= 2;
+  return (int)kc;
+}
+
+void launch_wgrad_reduce(hipStream_t st, const float* partial, const int* chunk_first, int groups,
+                         long long PQ, float* G, int accumulate);
+
+// Launch helpers (the tables must have been built on `st` beforehand).
+template <bool NT, class ALoad, class Epi>
+void launch_rows(hipStream_t st, const ALoad& al, const float* B, int K, int N, const RowsTile* tiles,
+                 const int* n_tiles, int max_tiles, const Epi& epi, float* rowsum = nullptr) {
+  if (max_tiles <= 0) return;
+  dim3 grid(max_tiles, (N + GBN - 1) / GBN);
+  hipLaunchKernelGGL((gemm_rows_kernel<NT, ALoad, Epi>), grid, dim3(256), 0, st, al, B, K, N, tiles,
+                     n_tiles, epi, rowsum);
+}
+
+template <class ALoad, class BLoad>
+void launch_wgrad(hipStream_t st, const ALoad& al, const BLoad& bl, int P, int Q, const WChunk* chunks,
+                  const int* n_chunks, const int* chunk_first, int max_chunks, int groups,
+                  float* partial, float* G, int accumulate) {
+  if (max_chunks > 0) {
+    dim3 grid(max_chunks, ((P + GBM - 1) / GBM) * ((Q + GBN - 1) / GBN));
+    hipLaunchKernelGGL((gemm_wgrad_kernel<ALoad, BLoad>), grid, dim3(256), 0, st, al, bl, P, Q, chunks,
+                       n_chunks, partial);
+  }
+  launch_wgrad_reduce(st, partial, chunk_first, groups, (long long)P * Q, G, accumulate);
+}
+
+void build_tables(hipStream_t st, const int* row_off, int groups, int kc, RowsTile* tiles, int* n_tiles,
+                  WChunk* chunks, int* n_chunks, int* chunk_first);
+
+}  // namespace janus

@@ -1,0 +1,19 @@
+// Launchers of kernels defined in graph.hip and used by the step driver.
+#pragma once
+
+#include "common.h"
+
+namespace janus {
+
+// Bit 1: bad offsets; bit 2 (only when rc > 0): cell not diagonal-positive or far smaller than rc.
+void launch_validate_struct(hipStream_t st, const int* offsets, int S, int N, const float* cell, float rc,
+                            int* flag);
+void launch_atom_struct(hipStream_t st, const int* offsets, int S, int N, int* sid);
+// out[0..n] = exclusive prefix sums of in[0..n-1]; bit 16 of flag if the total overflows int32.
+void launch_exclusive_scan(hipStream_t st, const int* in, int n, int* out, int* flag);
+// geo[e] = (u_x, u_y, u_z, r); B, dB [Ne, nb].
+void launch_geometry(hipStream_t st, const float* pos, const float* cell, const int* sid, const int* ei,
+                     const int* ej, const int8_t* shift, int Ne, float rc, int nb, float4* geo, float* B,
+                     float* dB);
+
+}  // namespace janus

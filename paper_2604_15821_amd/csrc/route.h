@@ -1,0 +1,34 @@
+// Routing launchers (route.hip).
+#pragma once
+
+#include "common.h"
+
+namespace janus {
+
+struct RouteArgs {
+  const float* Pc;        // [nsp, E]
+  const float* Pn;        // [nsp, E]
+  const float* beta;      // [E]
+  const int* species;     // [N]
+  const int* ei;
+  const int* ej;
+  int Ne, nsp, E, k;
+  int* peid;              // [nsp*nsp, k]  chosen experts per species pair
+  float* pgate;           // [nsp*nsp, k]  their gates
+  float* pprob;           // [nsp*nsp, E]  full softmax per pair
+  int* pair;              // [Ne]          species pair of each edge
+  int* eid;               // [Ne, k]
+  float* gate;            // [Ne, k]
+  int* cnt;               // [sort_chunks(Ne*k), E] scratch
+  int* colpre;            // [sort_chunks(Ne*k), E] scratch
+  int* total;             // [E]           tokens per expert
+  int* off;               // [E+1]         first slot of each expert
+  int* pos;               // [Ne, k]       slot of (edge, choice)
+  float* slot_gate;       // [Ne*k]        gate of the token in each slot
+};
+
+__global__ void zero_ints_kernel(int* p, int n);
+void route_block(hipStream_t st, const RouteArgs& a);
+int sort_chunks(long long M);
+
+}  // namespace janus

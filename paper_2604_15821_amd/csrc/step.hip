@@ -1,0 +1,891 @@
+// The training step: validation, workspace plan and the four phases of the
+// double-backward schedule (paper Sec. "Runtime for multi-phase
+// double-backward execution"): forward to the energy, first backward to the
+// forces, double backward of the force loss, final backward of the energy
+// loss.  Gradient contributions of the double and final backward passes to
+// the same weight are accumulated in a fixed order.
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "edge.h"
+#include "internal.h"
+#include "kernels.h"
+#include "route.h"
+
+namespace janus {
+
+// ------------------------------------------------------------ small kernels
+
+// Bit 1: bad species / offsets; bit 2: bad CSR; bit 4: bad edge indices or reverse map.
+__global__ void validate_atoms_kernel(const int* __restrict__ species, int N, int nsp, const int* __restrict__ rowptr,
+                                      const int* __restrict__ ei, long long Ne, const int* __restrict__ offsets, int S,
+                                      int* __restrict__ flag) {
+  const int a = blockIdx.x * blockDim.x + threadIdx.x;
+  if (a < S && offsets[a] >= offsets[a + 1]) atomicOr(flag, 1);   // every structure holds an atom
+  if (a > N) return;
+  int bad = 0;
+  if (a == 0 && rowptr[0] != 0) bad |= 2;
+  if (a == N) {
+    if (rowptr[N] != Ne) bad |= 2;
+  } else {
+    if (species[a] < 0 || species[a] >= nsp) bad |= 1;
+    const int e0 = rowptr[a], e1 = rowptr[a + 1];
+    if (e0 < 0 || e1 < e0 || e1 > Ne) {
+      bad |= 2;
+    } else {
+      for (int e = e0; e < e1; ++e)
+        if (ei[e] != a) { bad |= 2; break; }
+    }
+  }
+  if (bad) atomicOr(flag, bad);
+}
+
+__global__ void validate_edges_kernel(const int* __restrict__ ei, const int* __restrict__ ej,
+                                      const int8_t* __restrict__ shift, const int* __restrict__ rev,
+                                      const int* __restrict__ sid, int N, long long Ne, int* __restrict__ flag) {
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  const int i = ei[e], j = ej[e], r = rev[e];
+  bool ok = i >= 0 && i < N && j >= 0 && j < N && r >= 0 && r < Ne;
+  if (ok) {
+    ok = rev[r] == e && ei[r] == j && ej[r] == i && sid[i] == sid[j] && shift[3 * r] == -shift[3 * e] &&
+         shift[3 * r + 1] == -shift[3 * e + 1] && shift[3 * r + 2] == -shift[3 * e + 2] &&
+         !(i == j && shift[3 * e] == 0 && shift[3 * e + 1] == 0 && shift[3 * e + 2] == 0);
+  }
+  if (!ok) atomicOr(flag, 4);
+}
+
+// Per-atom readout energy eps_i = w_o2 . SiLU(z_i)  (z = h^T W_o1).
+template <int VPL>
+__global__ void readout_kernel(const float* __restrict__ z, const float* __restrict__ wo2, int N, int d,
+                               float* __restrict__ eps) {
+  JANUS_WAVE_LOOP(i, N) {
+    float s = 0.f;
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) s += silu(z[i * d + v * 64 + l]) * wo2[v * 64 + l];
+    s = wave_sum(s);
+    if (l == 0) eps[i] = s;
+  }
+}
+
+// E_s = sum of eps over the atoms of s, accumulated in float64.
+__global__ void energy_kernel(const float* __restrict__ eps, const int* __restrict__ offsets, int S,
+                              double* __restrict__ Ed, float* __restrict__ E) {
+  JANUS_WAVE_LOOP(s, S) {
+    double acc = 0.0;
+    for (int a = offsets[s] + l; a < offsets[s + 1]; a += 64) acc += (double)eps[a];
+    acc = wave_sum_d(acc);
+    if (l == 0) {
+      Ed[s] = acc;
+      E[s] = (float)acc;
+    }
+  }
+}
+
+// F_a = sum_{e in seg(a)} (G_e - G_rev(e)),  G_e = rbar_e u_e = dE/dd_e.
+__global__ void force_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev,
+                             const float* __restrict__ rbar, const float4* __restrict__ geo, int N,
+                             float* __restrict__ F) {
+  const int a = blockIdx.x * blockDim.x + threadIdx.x;
+  if (a >= N) return;
+  double fx = 0, fy = 0, fz = 0;
+  for (int e = rowptr[a]; e < rowptr[a + 1]; ++e) {
+    const float4 u = geo[e], ur = geo[rev[e]];
+    const double g = rbar[e], gr = rbar[rev[e]];
+    fx += g * u.x - gr * ur.x;
+    fy += g * u.y - gr * ur.y;
+    fz += g * u.z - gr * ur.z;
+  }
+  F[3 * a] = (float)fx;
+  F[3 * a + 1] = (float)fy;
+  F[3 * a + 2] = (float)fz;
+}
+
+// Loss and adjoint seeds (one workgroup of 1024, fixed reduction order):
+//   loss = w_E/S sum_s (E_s/n_s - Eref_s)^2 + w_F/(3N) sum_a |F_a - Fref_a|^2
+//   lam_s = dloss/dE_s,  phi_a = dloss/dF_a.
+__global__ void loss_kernel(const double* __restrict__ Ed, const float* __restrict__ Eref,
+                            const int* __restrict__ offsets, int S, const float* __restrict__ F,
+                            const float* __restrict__ Fref, int N, float wE, float wF, float* __restrict__ loss,
+                            float* __restrict__ lam, float* __restrict__ phi) {
+  __shared__ double red[1024];
+  const int t = threadIdx.x;
+  double se = 0.0, sf = 0.0;
+  for (int s = t; s < S; s += 1024) {
+    const double n = (double)(offsets[s + 1] - offsets[s]);
+    const double de = Ed[s] / n - (double)Eref[s];
+    se += de * de;
+    lam[s] = (float)(2.0 * wE * de / ((double)S * n));
+  }
+  for (int q = t; q < 3 * N; q += 1024) {
+    const double df = (double)F[q] - (double)Fref[q];
+    sf += df * df;
+    phi[q] = (float)(2.0 * wF * df / (3.0 * N));
+  }
+  red[t] = wE * se / S + wF * sf / (3.0 * N);
+  __syncthreads();
+  for (int o = 512; o > 0; o >>= 1) {
+    if (t < o) red[t] += red[t + o];
+    __syncthreads();
+  }
+  if (t == 0) *loss = (float)red[0];
+}
+
+// rt_e = (phi_i - phi_j) . u_e: the loss adjoint of rbar_e.
+__global__ void rtilde_kernel(const int* __restrict__ ei, const int* __restrict__ ej, const float4* __restrict__ geo,
+                              const float* __restrict__ phi, long long Ne, float* __restrict__ rt) {
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  const int i = ei[e], j = ej[e];
+  const float4 u = geo[e];
+  rt[e] = (phi[3 * i] - phi[3 * j]) * u.x + (phi[3 * i + 1] - phi[3 * j + 1]) * u.y +
+          (phi[3 * i + 2] - phi[3 * j + 2]) * u.z;
+}
+
+// Readout of the double + final backward, per atom and column:
+//   Z   = lam_s SiLU'(z) w_o2 + SiLU''(z) w_o2 vt   (loss adjoint of z)
+//   T   = lam_s SiLU(z) + SiLU'(z) vt                (summed over atoms -> dw_o2)
+template <int VPL>
+__global__ void readout_bwd_kernel(const float* __restrict__ z, const float* __restrict__ vt,
+                                   const float* __restrict__ wo2, const float* __restrict__ lam,
+                                   const int* __restrict__ sid, int N, int d, float* __restrict__ Z,
+                                   float* __restrict__ T) {
+  JANUS_WAVE_LOOP(i, N) {
+    const float la = lam[sid[i]];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      const long long o = i * d + v * 64 + l;
+      const float a = z[o], w = wo2[v * 64 + l], q = vt[o];
+      const float s = sig(a);
+      const float d1 = s + a * s * (1.f - s);
+      const float d2 = s * (1.f - s) * (2.f + a * (1.f - 2.f * s));
+      Z[o] = la * d1 * w + d2 * w * q;
+      T[o] = la * a * s + d1 * q;
+    }
+  }
+}
+
+// Column sums in two fixed-order stages.
+constexpr int kColChunk = 256;
+__global__ void colsum_partial_kernel(const float* __restrict__ M, long long rows, int cols,
+                                      float* __restrict__ part) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cols) return;
+  const long long r0 = (long long)blockIdx.y * kColChunk, r1 = min(rows, r0 + kColChunk);
+  float s = 0.f;
+  for (long long r = r0; r < r1; ++r) s += M[r * cols + c];
+  part[(long long)blockIdx.y * cols + c] = s;
+}
+__global__ void colsum_final_kernel(const float* __restrict__ part, int nch, int cols, float* __restrict__ out) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cols) return;
+  float s = 0.f;
+  for (int q = 0; q < nch; ++q) s += part[(long long)q * cols + c];
+  out[c] = s;
+}
+
+// Total gate adjoint of (e, c): double-backward part plus the final-backward
+// row sums of S~ . SiLU(A) over the column tiles of the slot.
+__global__ void gate_total_kernel(const float* __restrict__ g3, const float* __restrict__ gpart,
+                                  const int* __restrict__ pos, long long Mk, int ntile, float* __restrict__ gt) {
+  const long long f = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (f >= Mk) return;
+  float s = g3[f];
+  const float* p = gpart + (long long)pos[f] * ntile;
+  for (int q = 0; q < ntile; ++q) s += p[q];
+  gt[f] = s;
+}
+
+// Router logit adjoints summed per atom (lane x = expert x):
+//   lt_e[x] = p_e[x] (pt_e[x] - sum_y p_e[y] pt_e[y]),  pt_e[x] = sum_c [eid_ec = x] gt_ec
+// partC[i] = sum over edges out of i, partN[i] = sum over edges into i.
+__device__ __forceinline__ float logit_adjoint(long long e, int k, int lane, int E, const int* __restrict__ pair,
+                                               const float* __restrict__ pprob, const int* __restrict__ eid,
+                                               const float* __restrict__ gt) {
+  const float px = lane < E ? pprob[(long long)pair[e] * E + lane] : 0.f;
+  float pt = 0.f;
+  for (int c = 0; c < k; ++c)
+    if (eid[e * k + c] == lane) pt += gt[e * k + c];
+  const float s = wave_sum(px * pt);
+  return px * (pt - s);
+}
+
+__global__ void router_atom_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev, int k, int E,
+                                   const int* __restrict__ pair, const float* __restrict__ pprob,
+                                   const int* __restrict__ eid, const float* __restrict__ gt, int N,
+                                   float* __restrict__ partC, float* __restrict__ partN) {
+  JANUS_WAVE_LOOP(i, N) {
+    float ac = 0.f, an = 0.f;
+    for (int e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+      ac += logit_adjoint(e, k, l, E, pair, pprob, eid, gt);
+      an += logit_adjoint(rev[e], k, l, E, pair, pprob, eid, gt);
+    }
+    if (l < E) {
+      partC[i * E + l] = ac;
+      partN[i * E + l] = an;
+    }
+  }
+}
+
+// out[s] = sum over the atoms of species s (in atom order) of rows of M [N, w]; w <= 64 * VPLW.
+__global__ void species_rows_kernel(const int* __restrict__ sp_off, const int* __restrict__ sp_atoms,
+                                    const float* __restrict__ M, int w, int nsp, float* __restrict__ out) {
+  const int s = blockIdx.x;
+  if (s >= nsp) return;
+  for (int c = threadIdx.x; c < w; c += blockDim.x) {
+    float acc = 0.f;
+    for (int q = sp_off[s]; q < sp_off[s + 1]; ++q) acc += M[(long long)sp_atoms[q] * w + c];
+    out[(long long)s * w + c] = acc;
+  }
+}
+
+// Atoms grouped by species in ascending atom order (one wave per species).
+__global__ void species_count_kernel(const int* __restrict__ species, int N, int nsp, int* __restrict__ cnt) {
+  const int s = blockIdx.x;
+  const int l = threadIdx.x;
+  int c = 0;
+  for (int a0 = 0; a0 < N; a0 += 64) {
+    const int a = a0 + l;
+    c += __popcll(__ballot(a < N && species[a] == s));
+  }
+  if (l == 0) cnt[s] = c;
+}
+__global__ void species_write_kernel(const int* __restrict__ species, int N, const int* __restrict__ sp_off,
+                                     int* __restrict__ sp_atoms) {
+  const int s = blockIdx.x;
+  const int l = threadIdx.x;
+  int c = sp_off[s];
+  for (int a0 = 0; a0 < N; a0 += 64) {
+    const int a = a0 + l;
+    const bool m = a < N && species[a] == s;
+    const unsigned long long b = __ballot(m);
+    if (m) sp_atoms[c + __popcll(b & ((1ull << l) - 1ull))] = a;
+    c += __popcll(b);
+  }
+}
+
+// ------------------------------------------------------------ epilogues of the expert GEMMs
+
+// Force backward, after Sbar = Ybar W2^T: keep Sbar and Abar = SiLU'(A) Sbar.
+struct EpiP2 {
+  const float* A;
+  float* Sb;
+  float* Ab;
+  long long ld;
+  static constexpr bool kRowSum = false;
+  __device__ __forceinline__ float operator()(long long r, int c, float v) const {
+    const long long i = r * ld + c;
+    Sb[i] = v;
+    Ab[i] = silu_d1(A[i]) * v;
+    return 0.f;
+  }
+};
+
+// Double backward, after Abt = Xbt W1:
+//   Sbt = SiLU'(A) Abt  (overwrites Abar, which the weight gradient has consumed)
+//   C   = SiLU''(A) Sbar Abt  (overwrites Sbar; consumed by the final backward)
+struct EpiP3 {
+  const float* A;
+  float* Sb;
+  float* Ab;
+  long long ld;
+  static constexpr bool kRowSum = false;
+  __device__ __forceinline__ float operator()(long long r, int c, float v) const {
+    const long long i = r * ld + c;
+    const float a = A[i], s = sig(a);
+    const float d1 = s + a * s * (1.f - s);
+    const float d2 = s * (1.f - s) * (2.f + a * (1.f - 2.f * s));
+    Ab[i] = d1 * v;
+    Sb[i] = d2 * Sb[i] * v;
+    return 0.f;
+  }
+};
+
+// Final backward, after St = mt W2^T (ungated adjoint of the message):
+//   At = g SiLU'(A) St + C  (overwrites C); returns St . SiLU(A) for the gate adjoint.
+struct EpiP4 {
+  const float* A;
+  float* Sb;
+  const float* gate;
+  long long ld;
+  static constexpr bool kRowSum = true;
+  __device__ __forceinline__ float operator()(long long r, int c, float v) const {
+    const long long i = r * ld + c;
+    const float a = A[i], s = sig(a);
+    const float d1 = s + a * s * (1.f - s);
+    Sb[i] = gate[r] * d1 * v + Sb[i];
+    return v * a * s;
+  }
+};
+
+// ------------------------------------------------------------ launch helpers
+
+#define LAUNCH_VPL(kern, d, grid, block, lds, st, ...)                          \
+  do {                                                                          \
+    switch ((d) / 64) {                                                         \
+      case 1: hipLaunchKernelGGL(kern<1>, grid, block, lds, st, __VA_ARGS__); break; \
+      case 2: hipLaunchKernelGGL(kern<2>, grid, block, lds, st, __VA_ARGS__); break; \
+      case 4: hipLaunchKernelGGL(kern<4>, grid, block, lds, st, __VA_ARGS__); break; \
+      case 8: hipLaunchKernelGGL(kern<8>, grid, block, lds, st, __VA_ARGS__); break; \
+      default: break;                                                           \
+    }                                                                           \
+  } while (0)
+
+// h0_i = A[Z_i]
+__global__ void species_rows_gather_kernel(const float* __restrict__ A, const int* __restrict__ species, int N, int d,
+                                           float* __restrict__ h) {
+  const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= (long long)N * d) return;
+  const long long i = q / d;
+  h[q] = A[(long long)species[i] * d + (q - i * d)];
+}
+
+inline dim3 wave_grid(long long items) {
+  long long blocks = (items + 3) / 4;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  return dim3((unsigned)blocks);
+}
+
+// ------------------------------------------------------------ weight layout
+
+struct Layout {
+  struct Ent {
+    std::string name;
+    long long off;
+    int ndim;
+    long long shape[3];
+  };
+  std::vector<Ent> ents;
+  long long total = 0;
+  void add(const std::string& n, std::initializer_list<long long> sh) {
+    Ent e;
+    e.name = n;
+    e.off = total;
+    e.ndim = (int)sh.size();
+    long long sz = 1;
+    int q = 0;
+    for (long long s : sh) {
+      e.shape[q++] = s;
+      sz *= s;
+    }
+    for (; q < 3; ++q) e.shape[q] = 0;
+    ents.push_back(e);
+    total += sz;
+  }
+  long long at(const std::string& n) const {
+    for (const auto& e : ents)
+      if (e.name == n) return e.off;
+    return -1;
+  }
+};
+
+Layout make_layout(const janus_config& c) {
+  Layout L;
+  const long long S = c.n_species, d = c.d, E = c.n_experts, h = c.d_hidden, nb = c.n_rbf;
+  L.add("A", {S, d});
+  for (int t = 0; t < c.n_blocks; ++t) {
+    const std::string p = "blocks." + std::to_string(t) + ".";
+    L.add(p + "W_b", {nb, d});
+    L.add(p + "Pc", {S, E});
+    L.add(p + "Pn", {S, E});
+    L.add(p + "beta", {E});
+    L.add(p + "W1", {E, d, h});
+    L.add(p + "W2", {E, h, d});
+  }
+  L.add("W_o1", {d, d});
+  L.add("w_o2", {d});
+  return L;
+}
+
+int check_config(const janus_config* c) {
+  if (!c) return JANUS_EINVAL;
+  if (c->n_species < 1 || c->n_species > 128 || c->d < 64 || c->n_rbf < 1 || c->n_rbf > 32 || c->n_blocks < 0 ||
+      c->n_blocks > 16 || c->n_experts < 1 || c->n_experts > 64 || c->top_k < 1 || c->top_k > 4 ||
+      c->top_k > c->n_experts || c->d_hidden < 64 || !(c->r_cut > 0.f))
+    return JANUS_EINVAL;
+  if (c->d % 64 || (c->d / 64 != 1 && c->d / 64 != 2 && c->d / 64 != 4 && c->d / 64 != 8) || c->d_hidden % 64 ||
+      c->n_rbf % 4 || c->env_p != 6 || c->three_body)
+    return JANUS_EUNSUPPORTED;
+  return JANUS_OK;
+}
+
+// ------------------------------------------------------------ workspace plan
+
+struct Plan {
+  // shared
+  int* flag;
+  int* sid;
+  float4* geo;
+  float *B, *dB, *rt, *rbar;
+  int *sp_cnt, *sp_off, *sp_atoms;
+  float *z, *eps, *lam, *phi, *vt, *Zr, *Tr, *colpart;
+  double* Ed;
+  float *h, *hh, *hht, *h3;   // [(T+1) or T][N, d]; the final-backward adjoint reuses hh
+  // routing, per block
+  int *peid, *pair, *eid, *pos, *total, *off, *cnt, *colpre;
+  float *pgate, *pprob, *gate, *slot_gate;
+  RowsTile* tiles;
+  int* ntiles;
+  WChunk* chunks;
+  int *nchunks, *cfirst;
+  // dense tables: atoms (group of N rows) and edges (group of Ne rows)
+  int *rowN, *rowE;
+  RowsTile* tilesN;
+  int* ntN;
+  WChunk *chunksN, *chunksE;
+  int *ncN, *cfN, *ncE, *cfE;
+  // per block activations
+  float *Xs, *A, *Sb, *Ab, *Ybs, *Xbar, *Fbar, *g3;
+  // temporaries
+  float *T1, *T2, *Pe, *Ft, *gpart, *gt, *partC, *partN, *partial;
+  // sizes
+  int T, E, k, d, hdim, nb, nsp, N, S;
+  long long Ne, M;
+  int mt, mc, kc, mtN, kcN, mcN, kcE, mcE, nch, ntile;
+};
+
+size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, long long Ne) {
+  Carver cv(base);
+  p.T = c.n_blocks;
+  p.E = c.n_experts;
+  p.k = c.top_k;
+  p.d = c.d;
+  p.hdim = c.d_hidden;
+  p.nb = c.n_rbf;
+  p.nsp = c.n_species;
+  p.N = N;
+  p.S = S;
+  p.Ne = Ne;
+  p.M = Ne * c.top_k;
+  const int T = p.T, E = p.E, d = p.d, h = p.hdim;
+  const long long M = p.M, Nd = (long long)N * d;
+  const long long np = (long long)p.nsp * p.nsp;
+  p.mt = max_rows_tiles(M, E);
+  p.kc = wgrad_chunk_rows(M, d, h);
+  p.mc = max_wchunks(M, E, p.kc);
+  p.mtN = max_rows_tiles(N, 1);
+  p.kcN = wgrad_chunk_rows(N, d, d);
+  p.mcN = max_wchunks(N, 1, p.kcN);
+  p.kcE = wgrad_chunk_rows(Ne, p.nb, d);
+  p.mcE = max_wchunks(Ne, 1, p.kcE);
+  p.nch = sort_chunks(M);
+  p.ntile = (h + GBN - 1) / GBN;
+
+  p.flag = cv.take<int>(4);
+  p.sid = cv.take<int>(N);
+  p.geo = cv.take<float4>(Ne);
+  p.B = cv.take<float>(Ne * p.nb);
+  p.dB = cv.take<float>(Ne * p.nb);
+  p.rt = cv.take<float>(Ne);
+  p.rbar = cv.take<float>(Ne);
+  p.sp_cnt = cv.take<int>(p.nsp);
+  p.sp_off = cv.take<int>(p.nsp + 1);
+  p.sp_atoms = cv.take<int>(N);
+  p.z = cv.take<float>(Nd);
+  p.eps = cv.take<float>(N);
+  p.lam = cv.take<float>(S);
+  p.phi = cv.take<float>(3LL * N);
+  p.vt = cv.take<float>(Nd);
+  p.Zr = cv.take<float>(Nd);
+  p.Tr = cv.take<float>(Nd);
+  p.colpart = cv.take<float>(((N + kColChunk - 1) / kColChunk) * (long long)d);
+  p.Ed = cv.take<double>(S);
+  p.h = cv.take<float>((T + 1) * Nd);
+  p.hh = cv.take<float>((T + 1) * Nd);
+  p.hht = cv.take<float>((T + 1) * Nd);
+  p.h3 = cv.take<float>(T * Nd + 1);
+
+  p.peid = cv.take<int>(T * np * p.k);
+  p.pgate = cv.take<float>(T * np * p.k);
+  p.pprob = cv.take<float>(T * np * E);
+  p.pair = cv.take<int>(T * Ne);
+  p.eid = cv.take<int>(T * M);
+  p.gate = cv.take<float>(T * M);
+  p.pos = cv.take<int>(T * M);
+  p.slot_gate = cv.take<float>(T * M);
+  p.total = cv.take<int>(T * E);
+  p.off = cv.take<int>(T * (E + 1));
+  p.cnt = cv.take<int>((long long)p.nch * E + 1);
+  p.colpre = cv.take<int>((long long)p.nch * E + 1);
+  p.tiles = cv.take<RowsTile>((long long)T * p.mt);
+  p.ntiles = cv.take<int>(T + 1);
+  p.chunks = cv.take<WChunk>((long long)T * p.mc);
+  p.nchunks = cv.take<int>(T + 1);
+  p.cfirst = cv.take<int>(T * (E + 1) + 1);
+
+  p.rowN = cv.take<int>(2);
+  p.rowE = cv.take<int>(2);
+  p.tilesN = cv.take<RowsTile>(p.mtN);
+  p.ntN = cv.take<int>(1);
+  p.chunksN = cv.take<WChunk>(p.mcN);
+  p.ncN = cv.take<int>(1);
+  p.cfN = cv.take<int>(2);
+  p.chunksE = cv.take<WChunk>(p.mcE);
+  p.ncE = cv.take<int>(1);
+  p.cfE = cv.take<int>(2);
+
+  p.Xs = cv.take<float>(T * M * d);
+  p.A = cv.take<float>(T * M * h);
+  p.Sb = cv.take<float>(T * M * h);
+  p.Ab = cv.take<float>(T * M * h);
+  p.Ybs = cv.take<float>(T * M * d);
+  p.Xbar = cv.take<float>(T * Ne * d);
+  p.Fbar = cv.take<float>(T * Ne * d);
+  p.g3 = cv.take<float>(T * M);
+
+  p.T1 = cv.take<float>(M * d);
+  p.T2 = cv.take<float>(M * d);
+  p.Pe = cv.take<float>(Ne * d);
+  p.Ft = cv.take<float>(Ne * d);
+  p.gpart = cv.take<float>(M * p.ntile);
+  p.gt = cv.take<float>(M);
+  p.partC = cv.take<float>((long long)N * E);
+  p.partN = cv.take<float>((long long)N * E);
+  long long part = (long long)p.mc * d * h;
+  part = std::max(part, (long long)p.mcN * d * d);
+  part = std::max(part, (long long)p.mcE * p.nb * d);
+  p.partial = cv.take<float>(part);
+  return cv.size();
+}
+
+__global__ void set_rows_kernel(int* rowN, int N, int* rowE, long long Ne) {
+  if (threadIdx.x == 0) {
+    rowN[0] = 0;
+    rowN[1] = N;
+    rowE[0] = 0;
+    rowE[1] = (int)Ne;
+  }
+}
+
+}  // namespace janus
+
+using namespace janus;
+
+// ------------------------------------------------------------------ API
+
+static thread_local int g_last_hip = 0;
+
+int janus_set_hip_error(hipError_t e) {
+  g_last_hip = (int)e;
+  return JANUS_EHIP;
+}
+
+extern "C" const char* janus_strerror(int code) {
+  switch (code) {
+    case JANUS_OK: return "ok";
+    case JANUS_EINVAL: return "invalid argument (sizes, offsets, species or edge indices)";
+    case JANUS_ECAPACITY: return "edge buffers too small";
+    case JANUS_ENOMEM: return "device allocation failed";
+    case JANUS_EHIP: return "HIP runtime error";
+    case JANUS_EUNSUPPORTED: return "configuration or input not supported by this build";
+    default: return "unknown error";
+  }
+}
+
+extern "C" int janus_create(const janus_config* cfg, janus_ctx** out) {
+  if (!out) return JANUS_EINVAL;
+  *out = nullptr;
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  janus_ctx* c = new janus_ctx();
+  c->cfg = *cfg;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return JANUS_EHIP;
+  }
+  if (hipHostMalloc((void**)&c->host_word, 4 * sizeof(int), hipHostMallocDefault) != hipSuccess) {
+    delete c;
+    return JANUS_EHIP;
+  }
+  *out = c;
+  return JANUS_OK;
+}
+
+extern "C" void janus_destroy(janus_ctx* c) {
+  if (!c) return;
+  if (c->ws.ptr) (void)hipFree(c->ws.ptr);
+  if (c->aux.ptr) (void)hipFree(c->aux.ptr);
+  if (c->nl.ptr) (void)hipFree(c->nl.ptr);
+  if (c->host_word) (void)hipHostFree(c->host_word);
+  delete c;
+}
+
+extern "C" int janus_weight_layout(const janus_config* cfg, janus_tensor_desc* out, int32_t* n_tensors,
+                                   int64_t* n_floats) {
+  if (!cfg || !n_tensors || !n_floats) return JANUS_EINVAL;
+  int rc = check_config(cfg);
+  if (rc == JANUS_EINVAL) return rc;
+  Layout L = make_layout(*cfg);
+  const int cap = *n_tensors;
+  *n_tensors = (int)L.ents.size();
+  *n_floats = L.total;
+  if (!out) return JANUS_OK;
+  if (cap < (int)L.ents.size()) return JANUS_EINVAL;
+  for (size_t q = 0; q < L.ents.size(); ++q) {
+    std::memset(&out[q], 0, sizeof(janus_tensor_desc));
+    std::strncpy(out[q].name, L.ents[q].name.c_str(), sizeof(out[q].name) - 1);
+    out[q].offset = L.ents[q].off;
+    out[q].ndim = L.ents[q].ndim;
+    for (int k = 0; k < 3; ++k) out[q].shape[k] = L.ents[q].shape[k];
+  }
+  return JANUS_OK;
+}
+
+extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
+                          const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
+                          const float* W, const float* E_ref, const float* F_ref, float* loss, float* E, float* F,
+                          float* dLdW, const janus_debug* dbg, void* stream) {
+  if (!ctx || !pos || !cell || !species || !offsets || !nl || !W || !E_ref || !F_ref || !loss || !E || !F ||
+      !dLdW || n_atoms < 1 || n_struct < 1 || n_struct > n_atoms)
+    return JANUS_EINVAL;
+  if (nl->n_edges < 0 || nl->n_edges > INT32_MAX / 4 || !nl->rowptr) return JANUS_EINVAL;
+  if (nl->n_edges > 0 && (!nl->ei || !nl->ej || !nl->shift || !nl->rev)) return JANUS_EINVAL;
+  const janus_config& cfg = ctx->cfg;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int N = n_atoms, S = n_struct;
+  const long long Ne = nl->n_edges;
+
+  Plan p;
+  size_t bytes = plan_layout(p, nullptr, cfg, N, S, Ne);
+  int rc = ensure(ctx->ws, bytes);
+  if (rc) return rc;
+  plan_layout(p, ctx->ws.ptr, cfg, N, S, Ne);
+  const int T = p.T, Ee = p.E, k = p.k, d = p.d, h = p.hdim, nb = p.nb, nsp = p.nsp;
+  const long long M = p.M, Nd = (long long)N * d;
+  const Layout L = make_layout(cfg);
+
+  // ---- validation (one synchronous flag read)
+  JANUS_HIP_TRY(hipMemsetAsync(p.flag, 0, 4 * sizeof(int), st));
+  launch_validate_struct(st, offsets, S, N, cell, 0.f, p.flag);
+  launch_atom_struct(st, offsets, S, N, p.sid);
+  hipLaunchKernelGGL(validate_atoms_kernel, dim3(cdiv(std::max(N, S) + 1, 256)), dim3(256), 0, st, species, N, nsp,
+                     nl->rowptr, nl->ei, Ne, offsets, S, p.flag);
+  if (Ne > 0)
+    hipLaunchKernelGGL(validate_edges_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, nl->ei, nl->ej, nl->shift,
+                       nl->rev, p.sid, N, Ne, p.flag);
+  JANUS_HIP_TRY(hipGetLastError());
+  JANUS_HIP_TRY(hipMemcpyAsync(ctx->host_word, p.flag, sizeof(int), hipMemcpyDeviceToHost, st));
+  JANUS_HIP_TRY(hipStreamSynchronize(st));
+  if (ctx->host_word[0]) return JANUS_EINVAL;
+
+  const int* ei = nl->ei;
+  const int* ej = nl->ej;
+  const int* rowptr = nl->rowptr;
+  const int* rev = nl->rev;
+  auto Wp = [&](const std::string& n) { return W + L.at(n); };
+  auto Gp = [&](const std::string& n) { return dLdW + L.at(n); };
+  auto blk = [](int t, const char* n) { return "blocks." + std::to_string(t) + "." + n; };
+  const size_t ldsW = (size_t)nb * d * sizeof(float);
+  const dim3 gE = wave_grid(Ne), gN = wave_grid(N), b256(256);
+
+  JANUS_HIP_TRY(hipMemsetAsync(dLdW, 0, sizeof(float) * L.total, st));
+
+  // ---- setup: geometry, species groups, routing of every block, GEMM tables
+  launch_geometry(st, pos, cell, p.sid, ei, ej, nl->shift, (int)Ne, cfg.r_cut, nb, p.geo, p.B, p.dB);
+  hipLaunchKernelGGL(species_count_kernel, dim3(nsp), dim3(64), 0, st, species, N, nsp, p.sp_cnt);
+  launch_exclusive_scan(st, p.sp_cnt, nsp, p.sp_off, nullptr);
+  hipLaunchKernelGGL(species_write_kernel, dim3(nsp), dim3(64), 0, st, species, N, p.sp_off, p.sp_atoms);
+  hipLaunchKernelGGL(set_rows_kernel, dim3(1), dim3(64), 0, st, p.rowN, N, p.rowE, Ne);
+  build_tables(st, p.rowN, 1, p.kcN, p.tilesN, p.ntN, p.chunksN, p.ncN, p.cfN);
+  build_tables(st, p.rowE, 1, p.kcE, nullptr, nullptr, p.chunksE, p.ncE, p.cfE);
+  const long long np = (long long)nsp * nsp;
+  for (int t = 0; t < T; ++t) {
+    RouteArgs ra;
+    ra.Pc = Wp(blk(t, "Pc"));
+    ra.Pn = Wp(blk(t, "Pn"));
+    ra.beta = Wp(blk(t, "beta"));
+    ra.species = species;
+    ra.ei = ei;
+    ra.ej = ej;
+    ra.Ne = (int)Ne;
+    ra.nsp = nsp;
+    ra.E = Ee;
+    ra.k = k;
+    ra.peid = p.peid + t * np * k;
+    ra.pgate = p.pgate + t * np * k;
+    ra.pprob = p.pprob + t * np * Ee;
+    ra.pair = p.pair + t * Ne;
+    ra.eid = p.eid + t * M;
+    ra.gate = p.gate + t * M;
+    ra.cnt = p.cnt;
+    ra.colpre = p.colpre;
+    ra.total = p.total + t * Ee;
+    ra.off = p.off + t * (Ee + 1);
+    ra.pos = p.pos + t * M;
+    ra.slot_gate = p.slot_gate + t * M;
+    route_block(st, ra);
+    build_tables(st, ra.off, Ee, p.kc, p.tiles + (long long)t * p.mt, p.ntiles + t, p.chunks + (long long)t * p.mc,
+                 p.nchunks + t, p.cfirst + t * (Ee + 1));
+  }
+  JANUS_HIP_TRY(hipGetLastError());
+
+  // per-block views
+  auto Xs = [&](int t) { return p.Xs + t * M * d; };
+  auto Ab = [&](int t) { return p.Ab + t * M * h; };
+  auto Aa = [&](int t) { return p.A + t * M * h; };
+  auto Sb = [&](int t) { return p.Sb + t * M * h; };
+  auto Ybs = [&](int t) { return p.Ybs + t * M * d; };
+  auto Xbar = [&](int t) { return p.Xbar + t * Ne * d; };
+  auto Fbar = [&](int t) { return p.Fbar + t * Ne * d; };
+  auto POS = [&](int t) { return p.pos + t * M; };
+  auto GATE = [&](int t) { return p.gate + t * M; };
+  auto SG = [&](int t) { return p.slot_gate + t * M; };
+  auto TL = [&](int t) { return p.tiles + (long long)t * p.mt; };
+  auto CH = [&](int t) { return p.chunks + (long long)t * p.mc; };
+  auto CF = [&](int t) { return p.cfirst + t * (Ee + 1); };
+  auto HV = [&](float* base, int t) { return base + t * Nd; };
+
+  // ---- phase 1: forward
+  hipLaunchKernelGGL(species_rows_gather_kernel, dim3(cdiv(Nd, 256)), b256, 0, st, Wp("A"), species, N, d, p.h);
+  for (int t = 0; t < T; ++t) {
+    const float* Wb = Wp(blk(t, "W_b"));
+    const float* W1 = Wp(blk(t, "W1"));
+    const float* W2 = Wp(blk(t, "W2"));
+    if (Ne > 0)
+      LAUNCH_VPL(dispatch_x_kernel, d, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
+                                    (const int*)POS(t), k, Ne, d, Xs(t));
+    launch_rows<false>(st, LoadPlain{Xs(t), d}, W1, d, h, TL(t), p.ntiles + t, p.mt, EpiStore{Aa(t), h});
+    launch_rows<false>(st, LoadSilu{Aa(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiRowScale{p.T1, SG(t), d});
+    LAUNCH_VPL(combine_fwd_kernel, d, gN, b256, 0, st, rowptr, (const int*)POS(t), k, (const float*)p.T1,
+                                   (const float*)HV(p.h, t), N, d, HV(p.h, t + 1));
+  }
+  const float* Wo1 = Wp("W_o1");
+  const float* wo2 = Wp("w_o2");
+  const float* hT = HV(p.h, T);
+  launch_rows<false>(st, LoadPlain{hT, d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiStore{p.z, d});
+  LAUNCH_VPL(readout_kernel, d, gN, b256, 0, st, (const float*)p.z, wo2, N, d, p.eps);
+  hipLaunchKernelGGL(energy_kernel, wave_grid(S), b256, 0, st, (const float*)p.eps, offsets, S, p.Ed, E);
+
+  // ---- phase 2: force backward (hh[t] = dE/dh^t)
+  launch_rows<true>(st, LoadSiluD1Scaled{p.z, wo2, d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiStore{HV(p.hh, T), d});
+  JANUS_HIP_TRY(hipMemsetAsync(p.rbar, 0, sizeof(float) * std::max<long long>(Ne, 1), st));
+  for (int t = T - 1; t >= 0; --t) {
+    const float* Wb = Wp(blk(t, "W_b"));
+    const float* W1 = Wp(blk(t, "W1"));
+    const float* W2 = Wp(blk(t, "W2"));
+    LAUNCH_VPL(gather_atom_kernel, d, gN, b256, 0, st, rowptr, (const int*)POS(t), k, (const float*)GATE(t),
+                                   (const float*)HV(p.hh, t + 1), N, d, Ybs(t));
+    launch_rows<true>(st, LoadPlain{Ybs(t), d}, W2, d, h, TL(t), p.ntiles + t, p.mt, EpiP2{Aa(t), Sb(t), Ab(t), h});
+    launch_rows<true>(st, LoadPlain{Ab(t), h}, W1, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T1, d});
+    if (Ne > 0)
+      LAUNCH_VPL(edge_p2_kernel, d, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
+                                 (const float*)HV(p.h, t), ej, (const int*)POS(t), k, Ne, d, (const float*)p.T1,
+                                 Xbar(t), Fbar(t), p.rbar, p.Pe);
+    LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe,
+                                   (const float*)HV(p.hh, t + 1), (const float*)nullptr, N, d, HV(p.hh, t));
+  }
+  hipLaunchKernelGGL(force_kernel, dim3(cdiv(N, 256)), b256, 0, st, rowptr, rev, (const float*)p.rbar,
+                     (const float4*)p.geo, N, F);
+  hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
+                     (const float*)F, F_ref, N, cfg.w_E, cfg.w_F, loss, p.lam, p.phi);
+  if (Ne > 0)
+    hipLaunchKernelGGL(rtilde_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, ei, ej, (const float4*)p.geo,
+                       (const float*)p.phi, Ne, p.rt);
+  JANUS_HIP_TRY(hipGetLastError());
+
+  // ---- phase 3: double backward of the force loss (hht[t] = loss adjoint of hh[t])
+  for (int t = 0; t < T; ++t) {
+    const float* Wb = Wp(blk(t, "W_b"));
+    const float* W1 = Wp(blk(t, "W1"));
+    const float* W2 = Wp(blk(t, "W2"));
+    const float* hht_t = t == 0 ? nullptr : HV(p.hht, t);
+    if (Ne > 0)
+      LAUNCH_VPL(edge_p3_kernel, d, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
+                                 (const float*)HV(p.h, t), ej, (const int*)POS(t), k, Ne, d,
+                                 (const float*)Xbar(t), hht_t, (const float*)p.rt, p.T1, p.Pe);
+    // dW_b (part 1): (rt B')^T Fbar
+    launch_wgrad(st, LoadRowScale{p.dB, p.rt, nb}, LoadPlain{Fbar(t), d}, nb, d, p.chunksE, p.ncE, p.cfE, p.mcE, 1,
+                 p.partial, Gp(blk(t, "W_b")), 0);
+    LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe, (const float*)nullptr,
+                                   (const float*)nullptr, N, d, HV(p.h3, t));
+    // G7: dW1 = Xbt^T Abar
+    launch_wgrad(st, LoadPlain{p.T1, d}, LoadPlain{Ab(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee, p.partial,
+                 Gp(blk(t, "W1")), 0);
+    // G5: Abt = Xbt W1 -> Sbt (into Ab), C (into Sb)
+    launch_rows<false>(st, LoadPlain{p.T1, d}, W1, d, h, TL(t), p.ntiles + t, p.mt, EpiP3{Aa(t), Sb(t), Ab(t), h});
+    // G6: Ybt = Sbt W2
+    launch_rows<false>(st, LoadPlain{Ab(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
+    // G8: dW2 = Sbt^T Ybar
+    launch_wgrad(st, LoadPlain{Ab(t), h}, LoadPlain{Ybs(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
+                 p.partial, Gp(blk(t, "W2")), 0);
+    LAUNCH_VPL(combine_p3_kernel, d, gN, b256, 0, st, rowptr, (const int*)POS(t), k, (const float*)GATE(t),
+                                  (const float*)p.T2, (const float*)HV(p.hh, t + 1), hht_t, N, d, p.g3 + t * M,
+                                  HV(p.hht, t + 1));
+  }
+  // readout part: vt = hht^T W_o1
+  launch_rows<false>(st, LoadPlain{HV(p.hht, T), d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiStore{p.vt, d});
+  JANUS_HIP_TRY(hipGetLastError());
+
+  // ---- phase 4: final backward (adjoint of h^t reuses hh)
+  LAUNCH_VPL(readout_bwd_kernel, d, gN, b256, 0, st, (const float*)p.z, (const float*)p.vt, wo2,
+                                 (const float*)p.lam, (const int*)p.sid, N, d, p.Zr, p.Tr);
+  launch_wgrad(st, LoadPlain{hT, d}, LoadPlain{p.Zr, d}, d, d, p.chunksN, p.ncN, p.cfN, p.mcN, 1, p.partial,
+               Gp("W_o1"), 0);
+  launch_wgrad(st, LoadPlain{HV(p.hht, T), d}, LoadSiluD1Scaled{p.z, wo2, d}, d, d, p.chunksN, p.ncN, p.cfN, p.mcN,
+               1, p.partial, Gp("W_o1"), 1);
+  {
+    const int nch = (N + kColChunk - 1) / kColChunk;
+    hipLaunchKernelGGL(colsum_partial_kernel, dim3(cdiv(d, 256), nch), b256, 0, st, (const float*)p.Tr,
+                       (long long)N, d, p.colpart);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3(cdiv(d, 256)), b256, 0, st, (const float*)p.colpart, nch, d,
+                       Gp("w_o2"));
+  }
+  launch_rows<true>(st, LoadPlain{p.Zr, d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiStore{HV(p.hh, T), d});
+  for (int t = T - 1; t >= 0; --t) {
+    const float* Wb = Wp(blk(t, "W_b"));
+    const float* W1 = Wp(blk(t, "W1"));
+    const float* W2 = Wp(blk(t, "W2"));
+    const float* hht_t = t == 0 ? nullptr : HV(p.hht, t);
+    // message adjoint, ungated, into the slots
+    LAUNCH_VPL(gather_atom_kernel, d, gN, b256, 0, st, rowptr, (const int*)POS(t), k, (const float*)nullptr,
+                                   (const float*)HV(p.hh, t + 1), N, d, p.T1);
+    // G9: St = mt W2^T -> At = g SiLU'(A) St + C (into Sb); row sums for the gate adjoint
+    launch_rows<true>(st, LoadPlain{p.T1, d}, W2, d, h, TL(t), p.ntiles + t, p.mt,
+                      EpiP4{Aa(t), Sb(t), SG(t), h}, p.gpart);
+    // G10: Xt = At W1^T
+    launch_rows<true>(st, LoadPlain{Sb(t), h}, W1, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
+    // G11: dW1 += X^T At ;  G12: dW2 += SiLU(A)^T (g mt)
+    launch_wgrad(st, LoadPlain{Xs(t), d}, LoadPlain{Sb(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
+                 p.partial, Gp(blk(t, "W1")), 1);
+    launch_wgrad(st, LoadSilu{Aa(t), h}, LoadRowScale{p.T1, SG(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
+                 p.partial, Gp(blk(t, "W2")), 1);
+    if (Ne > 0) {
+      LAUNCH_VPL(edge_p4_kernel, d, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
+                                 (const int*)POS(t), k, Ne, d, (const float*)p.T2, (const float*)Xbar(t), hht_t, p.Ft,
+                                 p.Pe);
+      // dW_b (part 2): B^T Ft
+      launch_wgrad(st, LoadPlain{p.B, nb}, LoadPlain{p.Ft, d}, nb, d, p.chunksE, p.ncE, p.cfE, p.mcE, 1, p.partial,
+                   Gp(blk(t, "W_b")), 1);
+      hipLaunchKernelGGL(gate_total_kernel, dim3(cdiv(M, 256)), b256, 0, st, (const float*)(p.g3 + t * M),
+                         (const float*)p.gpart, (const int*)POS(t), M, p.ntile, p.gt);
+      hipLaunchKernelGGL(router_atom_kernel, gN, b256, 0, st, rowptr, rev, k, Ee, (const int*)(p.pair + t * Ne),
+                         (const float*)(p.pprob + t * np * Ee), (const int*)(p.eid + t * M), (const float*)p.gt, N,
+                         p.partC, p.partN);
+      hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+                         (const int*)p.sp_atoms, (const float*)p.partC, Ee, nsp, Gp(blk(t, "Pc")));
+      hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+                         (const int*)p.sp_atoms, (const float*)p.partN, Ee, nsp, Gp(blk(t, "Pn")));
+    }
+    LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe, (const float*)HV(p.hh, t + 1),
+                                   (const float*)HV(p.h3, t), N, d, HV(p.hh, t));
+  }
+  hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(256), 0, st, (const int*)p.sp_off, (const int*)p.sp_atoms,
+                     (const float*)HV(p.hh, 0), d, nsp, Gp("A"));
+  JANUS_HIP_TRY(hipGetLastError());
+
+  // ---- debug copies
+  if (dbg) {
+    for (int t = 0; t < T; ++t) {
+      if (dbg->eid) JANUS_HIP_TRY(hipMemcpyAsync(dbg->eid + t * M, p.eid + t * M, sizeof(int) * M, hipMemcpyDeviceToDevice, st));
+      if (dbg->gate) JANUS_HIP_TRY(hipMemcpyAsync(dbg->gate + t * M, p.gate + t * M, sizeof(float) * M, hipMemcpyDeviceToDevice, st));
+      if (dbg->pos) JANUS_HIP_TRY(hipMemcpyAsync(dbg->pos + t * M, p.pos + t * M, sizeof(int) * M, hipMemcpyDeviceToDevice, st));
+      if (dbg->counts) JANUS_HIP_TRY(hipMemcpyAsync(dbg->counts + t * Ee, p.total + t * Ee, sizeof(int) * Ee, hipMemcpyDeviceToDevice, st));
+    }
+    if (dbg->basis && Ne > 0)
+      JANUS_HIP_TRY(hipMemcpyAsync(dbg->basis, p.B, sizeof(float) * Ne * nb, hipMemcpyDeviceToDevice, st));
+  }
+  return JANUS_OK;
+}

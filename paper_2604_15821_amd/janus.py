@@ -1,0 +1,275 @@
+"""Thin ctypes binding of libjanus (argument marshalling only).
+
+Every computation runs in the HIP library; PyTorch is used here only to
+allocate device memory and to pick the stream.  Importing this module loads
+the in-tree ``_lib/libjanus.so`` and raises if it has not been built: there
+is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libjanus.so")
+
+JANUS_OK, JANUS_EINVAL, JANUS_ECAPACITY, JANUS_ENOMEM, JANUS_EHIP, JANUS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+
+
+class JanusError(RuntimeError):
+    def __init__(self, code, where):
+        self.code = code
+        super().__init__(f"{where}: {_lib().janus_strerror(code).decode()} (code {code})")
+
+
+class Config(C.Structure):
+    _fields_ = [
+        ("n_species", C.c_int32), ("d", C.c_int32), ("n_rbf", C.c_int32), ("n_blocks", C.c_int32),
+        ("n_experts", C.c_int32), ("top_k", C.c_int32), ("d_hidden", C.c_int32), ("env_p", C.c_int32),
+        ("r_cut", C.c_float), ("three_body", C.c_int32), ("r_cut3", C.c_float), ("n_experts3", C.c_int32),
+        ("top_k3", C.c_int32), ("d_hidden3", C.c_int32), ("n_legendre", C.c_int32), ("w_E", C.c_float),
+        ("w_F", C.c_float),
+    ]
+
+
+class TensorDesc(C.Structure):
+    _fields_ = [("name", C.c_char * 48), ("offset", C.c_int64), ("ndim", C.c_int32), ("shape", C.c_int64 * 3)]
+
+
+class Edges(C.Structure):
+    _fields_ = [("n_edges", C.c_int64), ("ei", C.c_void_p), ("ej", C.c_void_p), ("shift", C.c_void_p),
+                ("rowptr", C.c_void_p), ("rev", C.c_void_p)]
+
+
+class Debug(C.Structure):
+    _fields_ = [("eid", C.c_void_p), ("gate", C.c_void_p), ("counts", C.c_void_p), ("pos", C.c_void_p),
+                ("basis", C.c_void_p)]
+
+
+_LIB = None
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"libjanus is not built ({LIB_PATH}); run paper_2604_15821_amd.build")
+        lib = C.CDLL(LIB_PATH)
+        vp, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
+        lib.janus_strerror.restype = C.c_char_p
+        lib.janus_strerror.argtypes = [C.c_int]
+        lib.janus_create.argtypes = [C.POINTER(Config), C.POINTER(vp)]
+        lib.janus_destroy.argtypes = [vp]
+        lib.janus_destroy.restype = None
+        lib.janus_weight_layout.argtypes = [C.POINTER(Config), C.POINTER(TensorDesc), C.POINTER(i32), C.POINTER(i64)]
+        lib.janus_build_edges.argtypes = [vp, vp, vp, vp, i32, i32, i64, vp, vp, vp, vp, vp, C.POINTER(i64), vp]
+        lib.janus_step.argtypes = [vp, vp, vp, vp, vp, i32, i32, C.POINTER(Edges), vp, vp, vp, vp, vp, vp, vp,
+                                   C.POINTER(Debug), vp]
+        lib.janus_grouped_gemm.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
+        lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
+        _LIB = lib
+    return _LIB
+
+
+def exported_symbols():
+    """Names the library exports (checked against include/janus.h by the CPU tests)."""
+    lib = _lib()
+    names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
+             "janus_grouped_gemm", "janus_grouped_wgrad", "janus_strerror"]
+    return [n for n in names if hasattr(lib, n)]
+
+
+def make_config(model) -> Config:
+    """Config from a ModelConfig-like object (attribute names as in the C struct)."""
+    c = Config()
+    for name, _ in Config._fields_:
+        v = getattr(model, name)
+        setattr(c, name, int(v) if not isinstance(v, float) else v)
+    return c
+
+
+def weight_layout(model):
+    """[(name, offset, shape)] and the blob size, from the library."""
+    lib = _lib()
+    cfg = make_config(model)
+    n = C.c_int32(0)
+    tot = C.c_int64(0)
+    rc = lib.janus_weight_layout(C.byref(cfg), None, C.byref(n), C.byref(tot))
+    if rc:
+        raise JanusError(rc, "janus_weight_layout")
+    descs = (TensorDesc * n.value)()
+    rc = lib.janus_weight_layout(C.byref(cfg), descs, C.byref(n), C.byref(tot))
+    if rc:
+        raise JanusError(rc, "janus_weight_layout")
+    out = [(d.name.decode(), int(d.offset), tuple(int(d.shape[k]) for k in range(d.ndim))) for d in descs]
+    return out, int(tot.value)
+
+
+def pack_weights(weights: dict, model) -> np.ndarray:
+    layout, total = weight_layout(model)
+    blob = np.zeros(total, np.float32)
+    for name, off, shape in layout:
+        w = np.asarray(weights[name], np.float32)
+        if w.shape != shape:
+            raise ValueError(f"{name}: shape {w.shape} != {shape}")
+        blob[off:off + w.size] = w.reshape(-1)
+    return blob
+
+
+def unpack(blob: np.ndarray, model) -> dict:
+    layout, _ = weight_layout(model)
+    return {name: blob[off:off + int(np.prod(shape))].reshape(shape) for name, off, shape in layout}
+
+
+def _ptr(t):
+    return C.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _stream():
+    import torch
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+@dataclass
+class NeighborList:
+    n_edges: int
+    ei: object
+    ej: object
+    shift: object
+    rowptr: object
+    rev: object
+
+    def as_struct(self) -> Edges:
+        return Edges(self.n_edges, _ptr(self.ei).value, _ptr(self.ej).value, _ptr(self.shift).value,
+                     _ptr(self.rowptr).value, _ptr(self.rev).value)
+
+
+class Context:
+    """A libjanus context on the current device."""
+
+    def __init__(self, model):
+        self.model = model
+        self.cfg = make_config(model)
+        h = C.c_void_p()
+        rc = _lib().janus_create(C.byref(self.cfg), C.byref(h))
+        if rc:
+            raise JanusError(rc, "janus_create")
+        self.h = h
+        self.capacity = 0
+        self._nl_bufs = None
+
+    def close(self):
+        if self.h:
+            import torch
+            torch.cuda.synchronize()
+            _lib().janus_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---------------------------------------------------------------- edges
+    def build_edges(self, pos, cell, offsets, capacity=None) -> NeighborList:
+        """Neighbour list of device tensors pos [N,3] f32, cell [S,3,3] f32, offsets [S+1] i32."""
+        import torch
+        dev = pos.device
+        N = pos.shape[0]
+        S = cell.shape[0]
+        rowptr = torch.empty(N + 1, dtype=torch.int32, device=dev)
+        ne = C.c_int64(0)
+        cap = int(capacity if capacity is not None else max(self.capacity, 1))
+        for _ in range(2):
+            ei = torch.empty(cap, dtype=torch.int32, device=dev)
+            ej = torch.empty(cap, dtype=torch.int32, device=dev)
+            rev = torch.empty(cap, dtype=torch.int32, device=dev)
+            sh = torch.empty(cap * 3, dtype=torch.int8, device=dev)
+            rc = _lib().janus_build_edges(self.h, _ptr(pos), _ptr(cell), _ptr(offsets), N, S, cap, _ptr(ei), _ptr(ej),
+                                          _ptr(sh), _ptr(rowptr), _ptr(rev), C.byref(ne), _stream())
+            if rc == JANUS_ECAPACITY and capacity is None:
+                cap = int(ne.value)
+                self.capacity = cap
+                continue
+            if rc:
+                raise JanusError(rc, "janus_build_edges")
+            n = int(ne.value)
+            return NeighborList(n, ei[:n], ej[:n], sh[:3 * n].view(n, 3) if n else sh[:0].view(0, 3), rowptr,
+                                rev[:n])
+        raise RuntimeError("edge capacity did not converge")
+
+    def build_edges_into(self, pos, cell, offsets, nl: NeighborList):
+        """Rebuild into existing buffers (capacity = their size); returns the edge count."""
+        ne = C.c_int64(0)
+        cap = int(nl.ei.shape[0])
+        rc = _lib().janus_build_edges(self.h, _ptr(pos), _ptr(cell), _ptr(offsets), pos.shape[0], cell.shape[0],
+                                      cap, _ptr(nl.ei), _ptr(nl.ej), _ptr(nl.shift), _ptr(nl.rowptr), _ptr(nl.rev),
+                                      C.byref(ne), _stream())
+        if rc:
+            raise JanusError(rc, "janus_build_edges")
+        return int(ne.value)
+
+    # ----------------------------------------------------------------- step
+    def step(self, pos, cell, species, offsets, nl: NeighborList, W, E_ref, F_ref, out=None, debug=None):
+        """One training step; returns (loss [1], E [S], F [N,3], dLdW [like W]) device tensors."""
+        import torch
+        dev = pos.device
+        N = pos.shape[0]
+        S = cell.shape[0]
+        if out is None:
+            out = (torch.empty(1, dtype=torch.float32, device=dev), torch.empty(S, dtype=torch.float32, device=dev),
+                   torch.empty(N, 3, dtype=torch.float32, device=dev), torch.empty_like(W))
+        loss, E, F, dW = out
+        edges = nl.as_struct()
+        dbg = None
+        if debug is not None:
+            dbg = Debug(*[_ptr(debug.get(k)).value for k in ("eid", "gate", "counts", "pos", "basis")])
+        rc = _lib().janus_step(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S, C.byref(edges),
+                               _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(loss), _ptr(E), _ptr(F), _ptr(dW),
+                               C.byref(dbg) if dbg is not None else None, _stream())
+        if rc:
+            raise JanusError(rc, "janus_step")
+        return loss, E, F, dW
+
+    # ---------------------------------------------------------------- GEMMs
+    def grouped_gemm(self, A, B, row_off, K, N, trans_b, out=None):
+        import torch
+        M = A.shape[0]
+        if out is None:
+            out = torch.empty(M, N, dtype=torch.float32, device=A.device)
+        rc = _lib().janus_grouped_gemm(self.h, _ptr(A), _ptr(B), _ptr(out), _ptr(row_off), row_off.shape[0] - 1, M,
+                                       K, N, int(trans_b), _stream())
+        if rc:
+            raise JanusError(rc, "janus_grouped_gemm")
+        return out
+
+    def grouped_wgrad(self, A, B, row_off, out=None):
+        import torch
+        M, P = A.shape
+        Q = B.shape[1]
+        G = row_off.shape[0] - 1
+        if out is None:
+            out = torch.empty(G, P, Q, dtype=torch.float32, device=A.device)
+        rc = _lib().janus_grouped_wgrad(self.h, _ptr(A), _ptr(B), _ptr(out), _ptr(row_off), G, M, P, Q, _stream())
+        if rc:
+            raise JanusError(rc, "janus_grouped_wgrad")
+        return out
+
+
+def upload(batch, device="cuda:0"):
+    """Device copies of a synthetic batch: dict with pos, cell, species, offsets, E_ref, F_ref, W."""
+    import torch
+    t = lambda a, dt: torch.as_tensor(np.ascontiguousarray(a)).to(device=device, dtype=dt)
+    return {
+        "pos": t(batch.pos, torch.float32),
+        "cell": t(batch.cell, torch.float32),
+        "species": t(batch.species, torch.int32),
+        "offsets": t(batch.offsets, torch.int32),
+        "E_ref": t(batch.E_ref, torch.float32),
+        "F_ref": t(batch.F_ref, torch.float32),
+        "W": t(pack_weights(batch.weights, batch.model), torch.float32),
+    }

@@ -1,0 +1,75 @@
+"""Host-side checks of the C ABI: the library loads, exports every entry point
+declared in include/janus.h, reports the weight layout the synthetic
+generator uses, and rejects bad configurations before touching a GPU."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2604_15821_amd import janus
+from paper_2604_15821_amd.synth import WORKLOADS, ModelConfig
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "janus.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(janus_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_entry_point():
+    lib = C.CDLL(janus.LIB_PATH)
+    names = _declared()
+    assert len(names) >= 8
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+@pytest.mark.parametrize("name", [n for n, w in WORKLOADS.items() if not w.model.three_body])
+def test_weight_layout_matches_generator(name):
+    m = WORKLOADS[name].model
+    layout, total = janus.weight_layout(m)
+    assert [(n, s) for n, _, s in layout] == [(n, s) for n, s, _ in m.weight_shapes()]
+    off = 0
+    for _, o, s in layout:
+        assert o == off
+        n = 1
+        for x in s:
+            n *= x
+        off += n
+    assert off == total
+
+
+def test_pack_unpack_roundtrip():
+    from paper_2604_15821_amd.synth import make_batch
+    b = make_batch("tiny")
+    blob = janus.pack_weights(b.weights, b.model)
+    back = janus.unpack(blob, b.model)
+    for k, v in b.weights.items():
+        assert (back[k] == v).all()
+
+
+@pytest.mark.parametrize("change,code", [
+    (dict(d=96), janus.JANUS_EUNSUPPORTED),
+    (dict(top_k=5), janus.JANUS_EINVAL),
+    (dict(n_experts=65), janus.JANUS_EINVAL),
+    (dict(env_p=5), janus.JANUS_EUNSUPPORTED),
+    (dict(d_hidden=32), janus.JANUS_EINVAL),
+    (dict(r_cut=0.0), janus.JANUS_EINVAL),
+])
+def test_bad_configs_are_rejected_on_the_host(change, code):
+    import dataclasses
+    m = dataclasses.replace(WORKLOADS["tiny"].model, **change)
+    cfg = janus.make_config(m)
+    h = C.c_void_p()
+    assert janus._lib().janus_create(C.byref(cfg), C.byref(h)) == code
+    assert not h.value
+
+
+def test_strerror_messages():
+    lib = janus._lib()
+    for code in (0, -1, -2, -3, -4, -5):
+        assert lib.janus_strerror(code)
+    assert b"unknown" in lib.janus_strerror(17)

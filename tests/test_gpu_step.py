@@ -1,0 +1,104 @@
+"""End-to-end parity of the training step (janus_step) with the float64
+oracle on the same seeded inputs: routing bit-exact, energy 1e-5 relative,
+loss 1e-5 relative, forces and every weight gradient 1e-3 relative L2."""
+import numpy as np
+import pytest
+
+from helpers import TOL_E, TOL_F, TOL_LOSS, TOL_W, banner, energy_error, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+STEP_CASES = [("tiny", None), ("small", 4)]
+
+
+def _batch(name, n):
+    from paper_2604_15821_amd.synth import make_batch, subset
+    b = make_batch(name)
+    return b if n is None else subset(b, range(n))
+
+
+def _run(b, debug=True, reps=1):
+    import torch
+    from paper_2604_15821_amd import janus
+    d = janus.upload(b)
+    ctx = janus.Context(b.model)
+    nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+    m = b.model
+    T, k, Ne = m.n_blocks, m.top_k, nl.n_edges
+    dbg = None
+    if debug:
+        dbg = {"eid": torch.empty(T * Ne * k, dtype=torch.int32, device="cuda:0"),
+               "gate": torch.empty(T * Ne * k, device="cuda:0"),
+               "counts": torch.empty(T * m.n_experts, dtype=torch.int32, device="cuda:0"),
+               "pos": torch.empty(T * Ne * k, dtype=torch.int32, device="cuda:0")}
+    outs = []
+    for _ in range(reps):
+        loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"],
+                                  d["F_ref"], debug=dbg)
+        torch.cuda.synchronize()
+        outs.append((float(loss.cpu()[0]), E.cpu().numpy(), F.cpu().numpy(), dW.cpu().numpy()))
+    dbgh = {kk: v.cpu().numpy() for kk, v in dbg.items()} if dbg else None
+    ctx.close()
+    return outs, dbgh, Ne
+
+
+@pytest.fixture(scope="module", params=STEP_CASES, ids=lambda c: f"{c[0]}-{c[1]}")
+def case(request):
+    from oracle.model import training_step
+    name, n = request.param
+    b = _batch(name, n)
+    banner("step", name, n, b.n_atoms)
+    outs, dbg, Ne = _run(b, reps=2)
+    loss, E, F, grad, aux = training_step(b, return_aux=True)
+    return b, outs, dbg, Ne, (loss, E, F, grad, aux)
+
+
+def test_routing_is_bit_exact(case):
+    b, outs, dbg, Ne, (loss, E, F, grad, aux) = case
+    m = b.model
+    T, k = m.n_blocks, m.top_k
+    for t, rt in enumerate(aux["routing"]):
+        assert (dbg["eid"][t * Ne * k:(t + 1) * Ne * k].reshape(Ne, k) == rt.eid).all()
+        assert (dbg["counts"][t * m.n_experts:(t + 1) * m.n_experts] == rt.counts).all()
+        assert (dbg["pos"][t * Ne * k:(t + 1) * Ne * k].reshape(Ne, k) == rt.pos).all()
+        g = dbg["gate"][t * Ne * k:(t + 1) * Ne * k].reshape(Ne, k)
+        assert np.abs(g - rt.gate).max() <= 1e-6
+
+
+def test_energy_and_loss(case):
+    b, outs, dbg, Ne, (loss, E, F, grad, aux) = case
+    g_loss, g_E, g_F, g_W = outs[0]
+    from oracle.model import Params, forward_energy
+    _, cache = forward_energy(b.species, aux["graph"], Params.from_weights(b.weights, b.model), aux["routing"])
+    err = energy_error(g_E, E, cache["eps"], b.offsets)
+    print("energy error", err)
+    assert err <= TOL_E
+    assert abs(g_loss - loss) <= TOL_LOSS * abs(loss)
+
+
+def test_forces(case):
+    b, outs, dbg, Ne, (loss, E, F, grad, aux) = case
+    err = rel_l2(outs[0][2], F)
+    print("force rel L2", err)
+    assert err <= TOL_F
+
+
+def test_weight_gradients(case):
+    from paper_2604_15821_amd import janus
+    b, outs, dbg, Ne, (loss, E, F, grad, aux) = case
+    got = janus.unpack(outs[0][3], b.model)
+    worst = {}
+    for name, ref in grad.items():
+        if name.endswith("beta"):
+            assert (got[name] == 0).all()
+            continue
+        worst[name] = rel_l2(got[name], ref)
+    print("dW rel L2", {k: f"{v:.2e}" for k, v in worst.items()})
+    assert max(worst.values()) <= TOL_W, worst
+
+
+def test_step_is_deterministic(case):
+    b, outs, dbg, Ne, _ = case
+    (l1, E1, F1, W1), (l2, E2, F2, W2) = outs
+    assert l1 == l2
+    assert (E1 == E2).all() and (F1 == F2).all() and (W1 == W2).all()
