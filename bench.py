@@ -1,0 +1,166 @@
+"""Throughput of the MoE-potential training step on one MI355X.
+
+One step = the whole hot path on one batch: neighbour list, geometry and
+basis, routing, forward to the energy, force backward, double backward of
+the force loss and final backward to every weight gradient.  Inputs are
+seeded synthetic batches resident in HBM before the timed region.
+
+Prints ONE JSON line on stdout (details on stderr).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload small]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA = 157.3e12      # dense fp32 matrix peak of MI355X, FLOP/s
+PEAK_HBM = 8.0e12              # HBM3E bandwidth, B/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(workload: str, n_struct: int):
+    """The float64 oracle, untuned, on the first n_struct structures of the batch."""
+    from oracle.model import training_step
+    from paper_2604_15821_amd.synth import make_batch, subset
+    b = subset(make_batch(workload), range(n_struct))
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas = None
+    try:
+        aff = len(os.sched_getaffinity(0))
+    except AttributeError:
+        aff = os.cpu_count()
+    t0 = time.perf_counter()
+    training_step(b)
+    dt = time.perf_counter() - t0
+    cores = min(aff, blas) if blas else aff
+    return {"value": b.n_atoms / dt, "unit": "atoms/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n_struct} of the batch's structures ({b.n_atoms} atoms), one full training step, "
+                      f"{dt:.1f} s; float64 NumPy, BLAS threads {blas}, affinity {aff}"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="small")
+    ap.add_argument("--cpu-structs", type=int, default=12)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2604_15821_amd import janus
+    from paper_2604_15821_amd.synth import WORKLOADS, make_batch
+
+    wl = WORKLOADS[args.workload]
+    m = wl.model
+    b = make_batch(args.workload)
+    d = janus.upload(b, "cuda:0")
+    ctx = janus.Context(m)
+    nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+    Ne = nl.n_edges
+    N, S = b.n_atoms, b.n_struct
+    out = (torch.empty(1, device="cuda:0"), torch.empty(S, device="cuda:0"), torch.empty(N, 3, device="cuda:0"),
+           torch.empty_like(d["W"]))
+
+    def step():
+        ne = ctx.build_edges_into(d["pos"], d["cell"], d["offsets"], nl)
+        assert ne == Ne
+        ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"], out=out)
+
+    log(f"workload {args.workload}: {S} structures, {N} atoms, {Ne} edges, d={m.d} h={m.d_hidden} "
+        f"E={m.n_experts} k={m.top_k} T={m.n_blocks}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ctx.profile(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = ctx.profile_read()
+    ctx.profile(False)
+    ms = (t1 - t0) * 1e3 / args.steps
+    log(f"{ms:.3f} ms/step, loss {float(out[0].cpu()[0]):.6g}")
+
+    kernels = {}
+    for name, r in prof.items():
+        per = r["ms"] / max(r["launches"], 1)
+        e = {"launches_per_step": r["launches"] / args.steps, "ms_per_step": r["ms"] / args.steps,
+             "avg_launch_ms": per}
+        if r["flops"] > 0:
+            e["tflops"] = r["flops"] / (r["ms"] * 1e-3) / 1e12
+            e["mfma_frac"] = e["tflops"] * 1e12 / PEAK_FP32_MFMA
+        if r["bytes"] > 0:
+            e["gbs"] = r["bytes"] / (r["ms"] * 1e-3) / 1e9
+            e["hbm_frac"] = e["gbs"] * 1e9 / PEAK_HBM
+        kernels[name] = e
+        log(f"  {name:13s} {r['ms'] / args.steps:8.3f} ms/step  {r['launches'] / args.steps:6.1f} launches  "
+            + (f"{e.get('tflops', 0):7.2f} TFLOP/s " if 'tflops' in e else "")
+            + (f"{e.get('gbs', 0):8.1f} GB/s" if 'gbs' in e else ""))
+
+    # dominant kernel: the family with the most time
+    dom = max(prof, key=lambda n: prof[n]["ms"])
+    r = prof[dom]
+    if r["flops"] > 0:
+        ach = r["flops"] / r["launches"] / (r["ms"] / r["launches"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": ach, "peak": PEAK_FP32_MFMA / 1e12, "unit": "TFLOP/s",
+                "frac": ach * 1e12 / PEAK_FP32_MFMA, "traffic": None,
+                "flops_per_launch": r["flops"] / r["launches"], "avg_launch_ms": r["ms"] / r["launches"]}
+    else:
+        ach = r["bytes"] / r["launches"] / (r["ms"] / r["launches"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                "frac": ach * 1e9 / PEAK_HBM, "traffic": None,
+                "bytes_per_launch": r["bytes"] / r["launches"], "avg_launch_ms": r["ms"] / r["launches"]}
+
+    res = {
+        "metric": "atoms/s per training step (E+F+2nd-order dL/dW) on 1 MI355X",
+        "value": N / (ms * 1e-3),
+        "unit": "atoms/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "structures": S, "atoms": N, "edges": Ne, "d": m.d,
+                   "d_hidden": m.d_hidden, "experts": m.n_experts, "top_k": m.top_k, "blocks": m.n_blocks,
+                   "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none"},
+        "edges_per_s": Ne / (ms * 1e-3),
+        "expert_gemm_flops_per_step": 24.0 * m.top_k * m.d * m.d_hidden * Ne * m.n_blocks,
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    ctx.close()
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(args.workload, min(args.cpu_structs, S))
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -230,6 +230,29 @@ int janus_grouped_wgrad(janus_ctx* ctx, const float* A, const float* B, float* G
                         const int32_t* row_off, int32_t n_groups, int64_t M, int32_t P, int32_t Q,
                         void* stream);
 
+/*
+ * Optional profiler of the kernel families of janus_build_edges and
+ * janus_step (host-side bookkeeping; HIP events recorded on the caller's
+ * stream around each family of launches).
+ * janus_profile_enable(ctx, 1) starts recording (and clears earlier
+ * records); 0 stops it.  janus_profile_read synchronises the recorded
+ * events, fills up to `cap` entries of `out` (host array) with one line per
+ * family that ran, returns the number of entries (or a negative code), and
+ * clears the records.  `flops` and `bytes` are the algorithmic work of the
+ * timed launches (matrix products: 2*M*N*K; memory-bound kernels: bytes
+ * that must cross HBM at least once).
+ */
+typedef struct janus_profile_entry {
+  char name[32];
+  int64_t launches;
+  double ms;
+  double flops;
+  double bytes;
+} janus_profile_entry;
+
+int janus_profile_enable(janus_ctx* ctx, int on);
+int janus_profile_read(janus_ctx* ctx, janus_profile_entry* out /* host */, int32_t cap);
+
 /* Static message for a return code. */
 const char* janus_strerror(int code);
 

@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(OUT_DIR, "libjanus.so")
-SOURCES = ["gemm.hip", "graph.hip", "route.hip", "step.hip"]
+SOURCES = ["gemm.hip", "graph.hip", "route.hip", "prof.hip", "driver.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -5,10 +5,10 @@
 //  * gemm_rows: C[r, :] = op(A)[r, :] x B_g for the rows r of group g.
 //    A is a slot buffer [M, K] (row r = one routed edge token, grouped by
 //    expert), B_g the expert weight, stored [K, N] ("NN") or [N, K] ("NT").
-//    The A loader may transform elements on the way in (SiLU of stored
-//    pre-activations, ...) and the epilogue functor decides what is written
-//    (plain store, gate scaling, SiLU'/SiLU'' products of the double
-//    backward, per-row partial sums).
+//    The A loader may transform elements on their way into LDS (SiLU of
+//    stored pre-activations, ...) and the epilogue functor decides what is
+//    written (plain store, gate scaling, the SiLU'/SiLU'' products of the
+//    double backward, per-row partial sums).
 //
 //  * gemm_wgrad: G_g[p, q] = sum_{r in group g} A[r, p] B[r, q], the weight
 //    gradients, whose contraction runs over the tokens of an expert.  The
@@ -19,11 +19,17 @@
 // Work decomposition: a workgroup of 256 threads (4 waves as 2 x 2) owns a
 // 128 x 128 output tile; each wave owns 64 x 64 = 2 x 2 MFMA blocks of
 // 32 x 32, i.e. 64 accumulator floats per lane.  K advances in stages of 16
-// through double-buffered LDS.  Inside a stage the k index of MFMA step s
-// for lane half hf is 8g + 4hf + s (g = 0, 1), so an operand stored
+// through double-buffered LDS; the global loads of stage s+1 are in flight
+// while stage s is multiplied, and operand transforms run only when the
+// loaded values are written to LDS.  Inside a stage the k index of MFMA step
+// j for lane half hf is 8g + 4hf + j (g = 0, 1), so an operand stored
 // k-contiguous is read from LDS with one 16-byte load per lane per 8 k, and
 // an operand stored m-contiguous with 4-byte loads whose 32-lane halves read
 // consecutive words.
+//
+// Epilogue: the accumulators are staged through LDS, 64 rows at a time, and
+// then visited row-major as float4, so every epilogue read and write of
+// global memory is a coalesced 512-byte row segment.
 #pragma once
 
 #include "common.h"
@@ -37,6 +43,10 @@ constexpr int GBN = 128;            // tile cols
 constexpr int GBK = 16;             // k per LDS stage
 constexpr int LD_MK = GBK + 4;      // row stride of an [m][k] LDS tile (floats)
 constexpr int LD_KM = GBM + 8;      // row stride of a [k][m] LDS tile (floats)
+constexpr int LD_C = GBN + 8;       // row stride of the staged output (floats)
+constexpr int SMEM_MAIN = 2 * GBM * LD_MK + 2 * GBN * LD_MK;   // floats, >= the NN and wgrad layouts
+constexpr int SMEM_EPI = 64 * LD_C;
+constexpr int SMEM_FLOATS = SMEM_MAIN > SMEM_EPI ? SMEM_MAIN : SMEM_EPI;
 
 struct RowsTile {   // one 128-row tile of a group
   int group;
@@ -45,22 +55,28 @@ struct RowsTile {   // one 128-row tile of a group
   int pad;
 };
 
-// ---------------------------------------------------------------- A loaders
-// A loader returns 4 consecutive k-elements of row r starting at column k.
+__device__ __forceinline__ float4 f4zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+
+// ---------------------------------------------------------------- loaders
+// load(r, k) fetches what element (r, k..k+3) needs from global memory;
+// apply(raw, k) turns it into the 4 operand values (only for valid rows).
 
 struct LoadPlain {
   const float* p;
   long long ld;
-  __device__ __forceinline__ float4 operator()(long long r, int k) const {
-    return *reinterpret_cast<const float4*>(p + r * ld + k);
-  }
+  using Raw = float4;
+  __device__ __forceinline__ Raw load(long long r, int k) const { return ld4(p + r * ld + k); }
+  __device__ __forceinline__ float4 apply(const Raw& v, int) const { return v; }
 };
 
 struct LoadSilu {   // SiLU of stored pre-activations
   const float* p;
   long long ld;
-  __device__ __forceinline__ float4 operator()(long long r, int k) const {
-    float4 v = *reinterpret_cast<const float4*>(p + r * ld + k);
+  using Raw = float4;
+  __device__ __forceinline__ Raw load(long long r, int k) const { return ld4(p + r * ld + k); }
+  __device__ __forceinline__ float4 apply(const Raw& v, int) const {
     return make_float4(silu(v.x), silu(v.y), silu(v.z), silu(v.w));
   }
 };
@@ -69,10 +85,13 @@ struct LoadRowScale {   // s[r] * p[r, k]
   const float* p;
   const float* s;
   long long ld;
-  __device__ __forceinline__ float4 operator()(long long r, int k) const {
-    float4 v = *reinterpret_cast<const float4*>(p + r * ld + k);
-    float a = s[r];
-    return make_float4(a * v.x, a * v.y, a * v.z, a * v.w);
+  struct Raw {
+    float4 v;
+    float s;
+  };
+  __device__ __forceinline__ Raw load(long long r, int k) const { return Raw{ld4(p + r * ld + k), s[r]}; }
+  __device__ __forceinline__ float4 apply(const Raw& x, int) const {
+    return make_float4(x.s * x.v.x, x.s * x.v.y, x.s * x.v.z, x.s * x.v.w);
   }
 };
 
@@ -80,101 +99,221 @@ struct LoadSiluD1Scaled {   // SiLU'(z[r, k]) * w[k]
   const float* z;
   const float* w;
   long long ld;
-  __device__ __forceinline__ float4 operator()(long long r, int k) const {
-    float4 v = *reinterpret_cast<const float4*>(z + r * ld + k);
-    return make_float4(silu_d1(v.x) * w[k], silu_d1(v.y) * w[k + 1], silu_d1(v.z) * w[k + 2],
-                       silu_d1(v.w) * w[k + 3]);
+  using Raw = float4;
+  __device__ __forceinline__ Raw load(long long r, int k) const { return ld4(z + r * ld + k); }
+  __device__ __forceinline__ float4 apply(const Raw& v, int k) const {
+    const float4 ww = ld4(w + k);
+    return make_float4(silu_d1(v.x) * ww.x, silu_d1(v.y) * ww.y, silu_d1(v.z) * ww.z, silu_d1(v.w) * ww.w);
   }
 };
 
 // ---------------------------------------------------------------- epilogues
-// An epilogue sees (row, col, value) for every valid output element.
+// operator()(r, c, v) receives output row r, columns c..c+3 (c % 4 == 0) and
+// returns this piece's contribution to the row sum (used when kRowSum).
 
 struct EpiStore {
   float* c;
   long long ld;
   static constexpr bool kRowSum = false;
-  __device__ __forceinline__ float operator()(long long r, int col, float v) const {
-    c[r * ld + col] = v;
+  __device__ __forceinline__ float operator()(long long r, int col, float4 v) const {
+    st4(c + r * ld + col, v);
     return 0.f;
   }
-  __device__ __forceinline__ void rowsum(long long, int, float) const {}
 };
+
+// Same store for the dense readout products (a distinct type keeps their
+// kernels apart from the expert ones in profiles).
+struct EpiDense : EpiStore {};
 
 struct EpiRowScale {   // c = s[r] * v
   float* c;
   const float* s;
   long long ld;
   static constexpr bool kRowSum = false;
-  __device__ __forceinline__ float operator()(long long r, int col, float v) const {
-    c[r * ld + col] = s[r] * v;
+  __device__ __forceinline__ float operator()(long long r, int col, float4 v) const {
+    const float a = s[r];
+    st4(c + r * ld + col, make_float4(a * v.x, a * v.y, a * v.z, a * v.w));
     return 0.f;
   }
-  __device__ __forceinline__ void rowsum(long long, int, float) const {}
+};
+
+// Force backward, after Sbar = Ybar W2^T: keep Sbar and Abar = SiLU'(A) Sbar.
+struct EpiP2 {
+  const float* A;
+  float* Sb;
+  float* Ab;
+  long long ld;
+  static constexpr bool kRowSum = false;
+  __device__ __forceinline__ float operator()(long long r, int c, float4 v) const {
+    const long long i = r * ld + c;
+    const float4 a = ld4(A + i);
+    st4(Sb + i, v);
+    st4(Ab + i, make_float4(silu_d1(a.x) * v.x, silu_d1(a.y) * v.y, silu_d1(a.z) * v.z, silu_d1(a.w) * v.w));
+    return 0.f;
+  }
+};
+
+// Double backward, after Abt = Xbt W1:
+//   Sbt = SiLU'(A) Abt        (overwrites Abar, which the weight gradient has consumed)
+//   C   = SiLU''(A) Sbar Abt  (overwrites Sbar; consumed by the final backward)
+struct EpiP3 {
+  const float* A;
+  float* Sb;
+  float* Ab;
+  long long ld;
+  static constexpr bool kRowSum = false;
+  __device__ __forceinline__ static void d12(float a, float& d1, float& d2) {
+    const float s = sig(a);
+    d1 = s + a * s * (1.f - s);
+    d2 = s * (1.f - s) * (2.f + a * (1.f - 2.f * s));
+  }
+  __device__ __forceinline__ float operator()(long long r, int c, float4 v) const {
+    const long long i = r * ld + c;
+    const float4 a = ld4(A + i), sb = ld4(Sb + i);
+    float4 o1, o2;
+    float d1, d2;
+    d12(a.x, d1, d2); o1.x = d1 * v.x; o2.x = d2 * sb.x * v.x;
+    d12(a.y, d1, d2); o1.y = d1 * v.y; o2.y = d2 * sb.y * v.y;
+    d12(a.z, d1, d2); o1.z = d1 * v.z; o2.z = d2 * sb.z * v.z;
+    d12(a.w, d1, d2); o1.w = d1 * v.w; o2.w = d2 * sb.w * v.w;
+    st4(Ab + i, o1);
+    st4(Sb + i, o2);
+    return 0.f;
+  }
+};
+
+// Final backward, after St = mt W2^T (ungated adjoint of the message):
+//   At = g SiLU'(A) St + C  (overwrites C); returns St . SiLU(A) for the gate adjoint.
+struct EpiP4 {
+  const float* A;
+  float* Sb;
+  const float* gate;
+  long long ld;
+  static constexpr bool kRowSum = true;
+  __device__ __forceinline__ static float one(float a, float v, float c, float g, float& sum) {
+    const float s = sig(a);
+    sum += v * a * s;
+    return g * (s + a * s * (1.f - s)) * v + c;
+  }
+  __device__ __forceinline__ float operator()(long long r, int c, float4 v) const {
+    const long long i = r * ld + c;
+    const float4 a = ld4(A + i), cc = ld4(Sb + i);
+    const float g = gate[r];
+    float sum = 0.f;
+    float4 o;
+    o.x = one(a.x, v.x, cc.x, g, sum);
+    o.y = one(a.y, v.y, cc.y, g, sum);
+    o.z = one(a.z, v.z, cc.z, g, sum);
+    o.w = one(a.w, v.w, cc.w, g, sum);
+    st4(Sb + i, o);
+    return sum;
+  }
 };
 
 // ------------------------------------------------------------ LDS staging
 
-template <class ALoad>
-__device__ __forceinline__ void load_a_stage(const ALoad& al, int r0, int r1, int k0, int tid,
-                                             float4 (&ra)[2]) {
+// [m][k] tile from a k-contiguous operand: thread q loads row q/4, k-quad q%4.
+template <class L>
+struct StageMK {
+  typename L::Raw raw[2];
+  bool ok[2];
+  __device__ __forceinline__ void load(const L& ld, int r0, int r1, int k0, int tid) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    int q = tid + 256 * i;
-    int m = q >> 2, kq = q & 3;
-    long long r = (long long)r0 + m;
-    ra[i] = (r < r1) ? al(r, k0 + 4 * kq) : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-}
-
-__device__ __forceinline__ void store_mk(float* s, int tid, const float4 (&ra)[2]) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    int q = tid + 256 * i;
-    int m = q >> 2, kq = q & 3;
-    *reinterpret_cast<float4*>(s + m * LD_MK + 4 * kq) = ra[i];
-  }
-}
-
-__device__ __forceinline__ void store_km(float* s, int tid, const float4 (&rb)[2]) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    int q = tid + 256 * i;
-    int k = q >> 5, mq = q & 31;
-    *reinterpret_cast<float4*>(s + k * LD_KM + 4 * mq) = rb[i];
-  }
-}
-
-// B operand of gemm_rows.  NT: B_g stored [N, K] (k-contiguous) -> [n][k] LDS.
-// NN: B_g stored [K, N] (n-contiguous) -> [k][n] LDS.
-template <bool NT>
-__device__ __forceinline__ void load_b_stage(const float* __restrict__ Bg, int K, int N, int n0,
-                                             int k0, int tid, float4 (&rb)[2]) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    int q = tid + 256 * i;
-    if (NT) {
-      int n = q >> 2, kq = q & 3;
-      int col = n0 + n;
-      rb[i] = (col < N) ? *reinterpret_cast<const float4*>(Bg + (long long)col * K + k0 + 4 * kq)
-                        : make_float4(0.f, 0.f, 0.f, 0.f);
-    } else {
-      int k = q >> 5, nq = q & 31;
-      int col = n0 + 4 * nq;
-      rb[i] = (col < N) ? *reinterpret_cast<const float4*>(Bg + (long long)(k0 + k) * N + col)
-                        : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i;
+      const long long r = (long long)r0 + (q >> 2);
+      ok[i] = r < r1;
+      if (ok[i]) raw[i] = ld.load(r, k0 + 4 * (q & 3));
     }
+  }
+  __device__ __forceinline__ void store(const L& ld, float* s, int k0, int tid) const {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i;
+      st4(s + (q >> 2) * LD_MK + 4 * (q & 3), ok[i] ? ld.apply(raw[i], k0 + 4 * (q & 3)) : f4zero());
+    }
+  }
+};
+
+// [k][m] tile from an m-contiguous operand: thread q loads k-row q/32, m-quad q%32.
+template <class L>
+struct StageKM {
+  typename L::Raw raw[2];
+  bool ok[2];
+  __device__ __forceinline__ void load(const L& ld, long long rk, long long rk_end, int m0, int m_end, int tid) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i;
+      const long long r = rk + (q >> 5);
+      const int m = m0 + 4 * (q & 31);
+      ok[i] = r < rk_end && m < m_end;
+      if (ok[i]) raw[i] = ld.load(r, m);
+    }
+  }
+  __device__ __forceinline__ void store(const L& ld, float* s, int m0, int tid) const {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i;
+      st4(s + (q >> 5) * LD_KM + 4 * (q & 31), ok[i] ? ld.apply(raw[i], m0 + 4 * (q & 31)) : f4zero());
+    }
+  }
+};
+
+__device__ __forceinline__ void zero_acc(f32x16 (&acc)[2][2]) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+}
+
+// One LDS stage of MFMAs.  AMK / BMK: operand tile stored [m][k] (else [k][m]).
+template <bool AMK, bool BMK>
+__device__ __forceinline__ void mfma_stage(const float* a_s, const float* b_s, int wm, int wn, int lr, int hf,
+                                           f32x16 (&acc)[2][2]) {
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    float af[2][4], bf[2][4];
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+      const int m = wm * 64 + bi * 32 + lr;
+      if (AMK) {
+        const float4 v = ld4(a_s + m * LD_MK + 8 * g + 4 * hf);
+        af[bi][0] = v.x; af[bi][1] = v.y; af[bi][2] = v.z; af[bi][3] = v.w;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) af[bi][j] = a_s[(8 * g + 4 * hf + j) * LD_KM + m];
+      }
+    }
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) {
+      const int n = wn * 64 + bj * 32 + lr;
+      if (BMK) {
+        const float4 v = ld4(b_s + n * LD_MK + 8 * g + 4 * hf);
+        bf[bj][0] = v.x; bf[bj][1] = v.y; bf[bj][2] = v.z; bf[bj][3] = v.w;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bf[bj][j] = b_s[(8 * g + 4 * hf + j) * LD_KM + n];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[bi][j], bf[bj][j], acc[bi][bj], 0, 0, 0);
   }
 }
 
 // ---------------------------------------------------------------- gemm_rows
 
 template <bool NT, class ALoad, class Epi>
-__global__ __launch_bounds__(256) void gemm_rows_kernel(ALoad al, const float* __restrict__ B,
-                                                        int K, int N,
-                                                        const RowsTile* __restrict__ tiles,
-                                                        const int* __restrict__ n_tiles, Epi epi,
-                                                        float* __restrict__ rowsum_out) {
+__global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float* __restrict__ B, int K, int N,
+                                                           const RowsTile* __restrict__ tiles,
+                                                           const int* __restrict__ n_tiles, Epi epi,
+                                                           float* __restrict__ rowsum_out) {
   const int t = blockIdx.x;
   if (t >= *n_tiles) return;
   const RowsTile tile = tiles[t];
@@ -182,8 +321,10 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(ALoad al, const float* _
   const int r0 = tile.r0, r1 = tile.r1;
   const float* Bg = B + (long long)tile.group * K * N;
 
-  __shared__ __attribute__((aligned(16))) float sA[2][GBM * LD_MK];
-  __shared__ __attribute__((aligned(16))) float sB[2][NT ? GBN * LD_MK : GBK * LD_KM];
+  __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
+  // double buffers: A at smem + b * GBM * LD_MK, B after both A buffers
+  auto sA = [&](int b) { return smem + b * (GBM * LD_MK); };
+  auto sB = [&](int b) { return smem + 2 * GBM * LD_MK + b * (GBN * LD_MK); };
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, l = tid & 63;
@@ -191,109 +332,68 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(ALoad al, const float* _
   const int lr = l & 31, hf = l >> 5;
 
   f32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  zero_acc(acc);
 
-  float4 ra[2], rb[2];
-  load_a_stage(al, r0, r1, 0, tid, ra);
-  load_b_stage<NT>(Bg, K, N, n0, 0, tid, rb);
-  store_mk(sA[0], tid, ra);
-  if (NT) store_mk(sB[0], tid, rb); else store_km(sB[0], tid, rb);
+  StageMK<ALoad> sa;
+  LoadPlain lb{Bg, NT ? (long long)K : (long long)N};
+  StageMK<LoadPlain> sbt;   // NT: B stored [N, K]
+  StageKM<LoadPlain> sbn;   // NN: B stored [K, N]
+
+  sa.load(al, r0, r1, 0, tid);
+  if (NT) sbt.load(lb, n0, N, 0, tid); else sbn.load(lb, 0, K, n0, N, tid);
+  sa.store(al, sA(0), 0, tid);
+  if (NT) sbt.store(lb, sB(0), 0, tid); else sbn.store(lb, sB(0), n0, tid);
   __syncthreads();
 
   const int nk = K / GBK;
   int cur = 0;
   for (int kt = 0; kt < nk; ++kt) {
     const bool more = kt + 1 < nk;
+    const int k1 = (kt + 1) * GBK;
     if (more) {
-      load_a_stage(al, r0, r1, (kt + 1) * GBK, tid, ra);
-      load_b_stage<NT>(Bg, K, N, n0, (kt + 1) * GBK, tid, rb);
+      sa.load(al, r0, r1, k1, tid);
+      if (NT) sbt.load(lb, n0, N, k1, tid); else sbn.load(lb, k1, K, n0, N, tid);
     }
-    const float* a_s = sA[cur];
-    const float* b_s = sB[cur];
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      float4 af[2];
-      float bf[2][4];
-#pragma unroll
-      for (int bi = 0; bi < 2; ++bi)
-        af[bi] = *reinterpret_cast<const float4*>(a_s + (wm * 64 + bi * 32 + lr) * LD_MK + 8 * g + 4 * hf);
-#pragma unroll
-      for (int bj = 0; bj < 2; ++bj) {
-        if (NT) {
-          float4 v = *reinterpret_cast<const float4*>(b_s + (wn * 64 + bj * 32 + lr) * LD_MK + 8 * g + 4 * hf);
-          bf[bj][0] = v.x; bf[bj][1] = v.y; bf[bj][2] = v.z; bf[bj][3] = v.w;
-        } else {
-#pragma unroll
-          for (int s = 0; s < 4; ++s) bf[bj][s] = b_s[(8 * g + 4 * hf + s) * LD_KM + wn * 64 + bj * 32 + lr];
-        }
-      }
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi) {
-          float a = s == 0 ? af[bi].x : s == 1 ? af[bi].y : s == 2 ? af[bi].z : af[bi].w;
-#pragma unroll
-          for (int bj = 0; bj < 2; ++bj)
-            acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bf[bj][s], acc[bi][bj], 0, 0, 0);
-        }
-      }
-    }
+    mfma_stage<true, NT>(sA(cur), sB(cur), wm, wn, lr, hf, acc);
     if (more) {
-      store_mk(sA[cur ^ 1], tid, ra);
-      if (NT) store_mk(sB[cur ^ 1], tid, rb); else store_km(sB[cur ^ 1], tid, rb);
+      sa.store(al, sA(cur ^ 1), k1, tid);
+      if (NT) sbt.store(lb, sB(cur ^ 1), 0, tid); else sbn.store(lb, sB(cur ^ 1), n0, tid);
     }
     __syncthreads();
     cur ^= 1;
   }
 
-  // Epilogue.  Lane l of block (bi, bj) holds column lr and rows
-  // 8 (v / 4) + 4 hf + (v % 4), v = 0..15.
-  float part[2][16];
+  // Epilogue in two halves of 64 rows: the waves of row half `half` stage
+  // their accumulators (lane l of block (bi, bj) holds column lr and rows
+  // 8 (v / 4) + 4 hf + v % 4), then every thread visits float4 pieces.
+  float* sC = smem;
 #pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) part[bi][v] = 0.f;
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi) {
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj) {
-      const int col = n0 + wn * 64 + bj * 32 + lr;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const long long row = (long long)r0 + wm * 64 + bi * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-        if (row < r1 && col < N) part[bi][v] += epi(row, col, acc[bi][bj][v]);
-      }
-    }
-  }
-  if (Epi::kRowSum) {
-    // Sum over the 128 columns of the tile: 32 lanes of a half, then the two
-    // column waves through LDS.  Written to rowsum_out[row * gridDim.y + blockIdx.y].
-    __shared__ float red[2][GBM];
-#pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float x = part[bi][v];
-#pragma unroll
-        for (int o = 16; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
-        part[bi][v] = x;
-      }
-    if (lr == 0) {
+  for (int half = 0; half < 2; ++half) {
+    if (wm == half) {
 #pragma unroll
       for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) red[wn][wm * 64 + bi * 32 + 8 * (v >> 2) + 4 * hf + (v & 3)] = part[bi][v];
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            sC[(bi * 32 + 8 * (v >> 2) + 4 * hf + (v & 3)) * LD_C + wn * 64 + bj * 32 + lr] = acc[bi][bj][v];
     }
     __syncthreads();
-    if (tid < GBM) {
-      const long long row = (long long)r0 + tid;
-      if (row < r1) rowsum_out[row * gridDim.y + blockIdx.y] = red[0][tid] + red[1][tid];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int idx = tid + 256 * i;
+      const int rl = idx >> 5, c4 = idx & 31;
+      const long long row = (long long)r0 + half * 64 + rl;
+      const int col = n0 + 4 * c4;
+      float part = 0.f;
+      if (row < r1 && col < N) part = epi(row, col, ld4(sC + rl * LD_C + 4 * c4));
+      if (Epi::kRowSum) {
+#pragma unroll
+        for (int o = 16; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+        if (c4 == 0 && row < r1) rowsum_out[row * gridDim.y + blockIdx.y] = part;
+      }
     }
+    __syncthreads();
   }
 }
 
@@ -308,10 +408,10 @@ struct WChunk {
 };
 
 template <class ALoad, class BLoad>
-__global__ __launch_bounds__(256) void gemm_wgrad_kernel(ALoad al, BLoad bl, int P, int Q,
-                                                         const WChunk* __restrict__ chunks,
-                                                         const int* __restrict__ n_chunks,
-                                                         float* __restrict__ partial) {
+__global__ __launch_bounds__(256, 2) void gemm_wgrad_kernel(ALoad al, BLoad bl, int P, int Q,
+                                                            const WChunk* __restrict__ chunks,
+                                                            const int* __restrict__ n_chunks,
+                                                            float* __restrict__ partial) {
   const int c = blockIdx.x;
   if (c >= *n_chunks) return;
   const WChunk ch = chunks[c];
@@ -319,8 +419,9 @@ __global__ __launch_bounds__(256) void gemm_wgrad_kernel(ALoad al, BLoad bl, int
   const int p0 = (blockIdx.y / ntq) * GBM;
   const int q0 = (blockIdx.y % ntq) * GBN;
 
-  __shared__ __attribute__((aligned(16))) float sA[2][GBK * LD_KM];
-  __shared__ __attribute__((aligned(16))) float sB[2][GBK * LD_KM];
+  __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
+  auto sA = [&](int b) { return smem + b * (GBK * LD_KM); };
+  auto sB = [&](int b) { return smem + (2 + b) * (GBK * LD_KM); };
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, l = tid & 63;
@@ -328,60 +429,29 @@ __global__ __launch_bounds__(256) void gemm_wgrad_kernel(ALoad al, BLoad bl, int
   const int lr = l & 31, hf = l >> 5;
 
   f32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  zero_acc(acc);
 
-  auto load = [&](int rk, float4 (&ra)[2], float4 (&rb)[2]) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      int q = tid + 256 * i;
-      int k = q >> 5, mq = q & 31;
-      long long r = (long long)rk + k;
-      bool rv = r < ch.r1;
-      int pc = p0 + 4 * mq, qc = q0 + 4 * mq;
-      ra[i] = (rv && pc < P) ? al(r, pc) : make_float4(0.f, 0.f, 0.f, 0.f);
-      rb[i] = (rv && qc < Q) ? bl(r, qc) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-  };
-
-  float4 ra[2], rb[2];
-  load(ch.r0, ra, rb);
-  store_km(sA[0], tid, ra);
-  store_km(sB[0], tid, rb);
+  StageKM<ALoad> sa;
+  StageKM<BLoad> sb;
+  sa.load(al, ch.r0, ch.r1, p0, P, tid);
+  sb.load(bl, ch.r0, ch.r1, q0, Q, tid);
+  sa.store(al, sA(0), p0, tid);
+  sb.store(bl, sB(0), q0, tid);
   __syncthreads();
 
   const int nk = (ch.r1 - ch.r0 + GBK - 1) / GBK;
   int cur = 0;
   for (int kt = 0; kt < nk; ++kt) {
     const bool more = kt + 1 < nk;
-    if (more) load(ch.r0 + (kt + 1) * GBK, ra, rb);
-    const float* a_s = sA[cur];
-    const float* b_s = sB[cur];
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      float af[2][4], bf[2][4];
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi) af[bi][s] = a_s[(8 * g + 4 * hf + s) * LD_KM + wm * 64 + bi * 32 + lr];
-#pragma unroll
-        for (int bj = 0; bj < 2; ++bj) bf[bj][s] = b_s[(8 * g + 4 * hf + s) * LD_KM + wn * 64 + bj * 32 + lr];
-      }
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-          for (int bj = 0; bj < 2; ++bj)
-            acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[bi][s], bf[bj][s], acc[bi][bj], 0, 0, 0);
-    }
+    const long long rk = (long long)ch.r0 + (kt + 1) * GBK;
     if (more) {
-      store_km(sA[cur ^ 1], tid, ra);
-      store_km(sB[cur ^ 1], tid, rb);
+      sa.load(al, rk, ch.r1, p0, P, tid);
+      sb.load(bl, rk, ch.r1, q0, Q, tid);
+    }
+    mfma_stage<false, false>(sA(cur), sB(cur), wm, wn, lr, hf, acc);
+    if (more) {
+      sa.store(al, sA(cur ^ 1), p0, tid);
+      sb.store(bl, sB(cur ^ 1), q0, tid);
     }
     __syncthreads();
     cur ^= 1;

@@ -262,9 +262,12 @@ extern "C" int janus_build_edges(janus_ctx* ctx, const float* pos, const float* 
   if (hw[0] & 2) return JANUS_EUNSUPPORTED;
 
   const float r_cut = ctx->cfg.r_cut;
-  hipLaunchKernelGGL((nl_kernel<false>), dim3(cdiv((long long)N * 64, 256)), dim3(256), 0, st, pos, cell, offsets,
-                     sid, r_cut, N, count, nullptr, nullptr, nullptr, nullptr);
-  launch_exclusive_scan(st, count, N, rp, flag);
+  {
+    ProfScope ps(ctx, st, PROF_GRAPH, 0.0, 16.0 * N);
+    hipLaunchKernelGGL((nl_kernel<false>), dim3(cdiv((long long)N * 64, 256)), dim3(256), 0, st, pos, cell,
+                       offsets, sid, r_cut, N, count, nullptr, nullptr, nullptr, nullptr);
+    launch_exclusive_scan(st, count, N, rp, flag);
+  }
   JANUS_HIP_TRY(hipGetLastError());
   JANUS_HIP_TRY(hipMemcpyAsync(hw, rp + N, sizeof(int), hipMemcpyDeviceToHost, st));
   JANUS_HIP_TRY(hipMemcpyAsync(hw + 1, flag, sizeof(int), hipMemcpyDeviceToHost, st));
@@ -275,6 +278,7 @@ extern "C" int janus_build_edges(janus_ctx* ctx, const float* pos, const float* 
   if (ne > capacity) return JANUS_ECAPACITY;
   JANUS_HIP_TRY(hipMemcpyAsync(rowptr, rp, sizeof(int) * (N + 1), hipMemcpyDeviceToDevice, st));
   if (ne > 0) {
+    ProfScope ps(ctx, st, PROF_GRAPH, 0.0, 16.0 * N + 23.0 * ne);
     hipLaunchKernelGGL((nl_kernel<true>), dim3(cdiv((long long)N * 64, 256)), dim3(256), 0, st, pos, cell, offsets,
                        sid, r_cut, N, nullptr, rp, ei, ej, shift);
     hipLaunchKernelGGL(reverse_kernel, dim3(cdiv(ne, 256)), dim3(256), 0, st, ei, ej, shift, rp, (int)ne, rev,

@@ -12,6 +12,25 @@ struct janus_buffer {
   size_t bytes = 0;
 };
 
+// Kernel families timed by the optional profiler (janus_profile_*).
+enum JanusProfClass {
+  PROF_EXPERT_GEMM = 0,   // expert token x weight products (forward and the three backward passes)
+  PROF_EXPERT_WGRAD,      // expert weight gradients (chunked products and their fixed-order reduction)
+  PROF_DENSE_GEMM,        // readout and radial-filter products and their gradients
+  PROF_EDGE,              // per-edge gather / dispatch / adjoint kernels
+  PROF_ATOM,              // per-atom combine / scatter kernels
+  PROF_ROUTE,             // routing and the expert permutation
+  PROF_GRAPH,             // neighbour list, reverse map, geometry and basis
+  PROF_OTHER,             // validation, readout, loss, forces, router and embedding gradients
+  PROF_NCLASS
+};
+
+struct janus_prof_rec {
+  int cls;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+
 struct janus_ctx {
   janus_config cfg;
   int device = 0;
@@ -19,9 +38,24 @@ struct janus_ctx {
   janus_buffer aux;       // tables and partials of the standalone GEMM entry points
   janus_buffer nl;        // per-atom counts and flags of janus_build_edges
   int* host_word = nullptr;   // 4 pinned host ints for the flag / count reads
+  // profiler: event pairs recorded around kernel families while enabled
+  bool prof_on = false;
+  std::vector<janus_prof_rec> prof_recs;
+  std::vector<hipEvent_t> prof_pool;
+  size_t prof_used = 0;
 };
 
 namespace janus {
+
+// Records an event pair around the launches issued during its lifetime.
+struct ProfScope {
+  janus_ctx* c;
+  hipStream_t st;
+  janus_prof_rec rec;
+  bool on;
+  ProfScope(janus_ctx* ctx, hipStream_t s, int cls, double flops, double bytes);
+  ~ProfScope();
+};
 
 // Grow `b` to at least `bytes` (contents are not preserved).
 int ensure(janus_buffer& b, size_t bytes);

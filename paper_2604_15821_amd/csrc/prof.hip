@@ -1,0 +1,80 @@
+// Event-pair profiler of the kernel families (janus_profile_enable / _read).
+#include <cstring>
+
+#include "internal.h"
+
+namespace janus {
+
+static const char* kProfNames[PROF_NCLASS] = {"expert_gemm", "expert_wgrad", "dense_gemm", "edge",
+                                              "atom",        "route",        "graph",      "other"};
+
+static hipEvent_t take_event(janus_ctx* c) {
+  if (c->prof_used == c->prof_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->prof_pool.push_back(e);
+  }
+  return c->prof_pool[c->prof_used++];
+}
+
+ProfScope::ProfScope(janus_ctx* ctx, hipStream_t s, int cls, double flops, double bytes)
+    : c(ctx), st(s), on(ctx && ctx->prof_on) {
+  if (!on) return;
+  rec.cls = cls;
+  rec.flops = flops;
+  rec.bytes = bytes;
+  rec.a = take_event(c);
+  rec.b = take_event(c);
+  if (!rec.a || !rec.b) {
+    on = false;
+    return;
+  }
+  (void)hipEventRecord(rec.a, st);
+}
+
+ProfScope::~ProfScope() {
+  if (!on) return;
+  (void)hipEventRecord(rec.b, st);
+  c->prof_recs.push_back(rec);
+}
+
+}  // namespace janus
+
+using namespace janus;
+
+extern "C" int janus_profile_enable(janus_ctx* ctx, int on) {
+  if (!ctx) return JANUS_EINVAL;
+  ctx->prof_on = on != 0;
+  if (on) {
+    ctx->prof_recs.clear();
+    ctx->prof_used = 0;
+  }
+  return JANUS_OK;
+}
+
+extern "C" int janus_profile_read(janus_ctx* ctx, janus_profile_entry* out, int32_t cap) {
+  if (!ctx || (cap > 0 && !out) || cap < 0) return JANUS_EINVAL;
+  janus_profile_entry acc[PROF_NCLASS];
+  std::memset(acc, 0, sizeof(acc));
+  for (const auto& r : ctx->prof_recs) {
+    JANUS_HIP_TRY(hipEventSynchronize(r.b));
+    float ms = 0.f;
+    JANUS_HIP_TRY(hipEventElapsedTime(&ms, r.a, r.b));
+    acc[r.cls].launches += 1;
+    acc[r.cls].ms += ms;
+    acc[r.cls].flops += r.flops;
+    acc[r.cls].bytes += r.bytes;
+  }
+  ctx->prof_recs.clear();
+  ctx->prof_used = 0;
+  int n = 0;
+  for (int q = 0; q < PROF_NCLASS; ++q) {
+    if (!acc[q].launches) continue;
+    if (n < cap) {
+      out[n] = acc[q];
+      std::strncpy(out[n].name, kProfNames[q], sizeof(out[n].name) - 1);
+    }
+    ++n;
+  }
+  return n < cap ? n : cap;
+}

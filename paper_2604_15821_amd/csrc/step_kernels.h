@@ -1,4 +1,6 @@
-// The training step: validation, workspace plan and the four phases of the
+#pragma once
+// Kernels, epilogues, weight layout and workspace plan of the training step
+// (included once, by driver.hip).  The step runs the four phases of the
 // double-backward schedule (paper Sec. "Runtime for multi-phase
 // double-backward execution"): forward to the energy, first backward to the
 // forces, double backward of the force loss, final backward of the energy
@@ -266,60 +268,6 @@ __global__ void species_write_kernel(const int* __restrict__ species, int N, con
   }
 }
 
-// ------------------------------------------------------------ epilogues of the expert GEMMs
-
-// Force backward, after Sbar = Ybar W2^T: keep Sbar and Abar = SiLU'(A) Sbar.
-struct EpiP2 {
-  const float* A;
-  float* Sb;
-  float* Ab;
-  long long ld;
-  static constexpr bool kRowSum = false;
-  __device__ __forceinline__ float operator()(long long r, int c, float v) const {
-    const long long i = r * ld + c;
-    Sb[i] = v;
-    Ab[i] = silu_d1(A[i]) * v;
-    return 0.f;
-  }
-};
-
-// Double backward, after Abt = Xbt W1:
-//   Sbt = SiLU'(A) Abt  (overwrites Abar, which the weight gradient has consumed)
-//   C   = SiLU''(A) Sbar Abt  (overwrites Sbar; consumed by the final backward)
-struct EpiP3 {
-  const float* A;
-  float* Sb;
-  float* Ab;
-  long long ld;
-  static constexpr bool kRowSum = false;
-  __device__ __forceinline__ float operator()(long long r, int c, float v) const {
-    const long long i = r * ld + c;
-    const float a = A[i], s = sig(a);
-    const float d1 = s + a * s * (1.f - s);
-    const float d2 = s * (1.f - s) * (2.f + a * (1.f - 2.f * s));
-    Ab[i] = d1 * v;
-    Sb[i] = d2 * Sb[i] * v;
-    return 0.f;
-  }
-};
-
-// Final backward, after St = mt W2^T (ungated adjoint of the message):
-//   At = g SiLU'(A) St + C  (overwrites C); returns St . SiLU(A) for the gate adjoint.
-struct EpiP4 {
-  const float* A;
-  float* Sb;
-  const float* gate;
-  long long ld;
-  static constexpr bool kRowSum = true;
-  __device__ __forceinline__ float operator()(long long r, int c, float v) const {
-    const long long i = r * ld + c;
-    const float a = A[i], s = sig(a);
-    const float d1 = s + a * s * (1.f - s);
-    Sb[i] = gate[r] * d1 * v + Sb[i];
-    return v * a * s;
-  }
-};
-
 // ------------------------------------------------------------ launch helpers
 
 #define LAUNCH_VPL(kern, d, grid, block, lds, st, ...)                          \
@@ -562,330 +510,3 @@ __global__ void set_rows_kernel(int* rowN, int N, int* rowE, long long Ne) {
 
 }  // namespace janus
 
-using namespace janus;
-
-// ------------------------------------------------------------------ API
-
-static thread_local int g_last_hip = 0;
-
-int janus_set_hip_error(hipError_t e) {
-  g_last_hip = (int)e;
-  return JANUS_EHIP;
-}
-
-extern "C" const char* janus_strerror(int code) {
-  switch (code) {
-    case JANUS_OK: return "ok";
-    case JANUS_EINVAL: return "invalid argument (sizes, offsets, species or edge indices)";
-    case JANUS_ECAPACITY: return "edge buffers too small";
-    case JANUS_ENOMEM: return "device allocation failed";
-    case JANUS_EHIP: return "HIP runtime error";
-    case JANUS_EUNSUPPORTED: return "configuration or input not supported by this build";
-    default: return "unknown error";
-  }
-}
-
-extern "C" int janus_create(const janus_config* cfg, janus_ctx** out) {
-  if (!out) return JANUS_EINVAL;
-  *out = nullptr;
-  int rc = check_config(cfg);
-  if (rc) return rc;
-  janus_ctx* c = new janus_ctx();
-  c->cfg = *cfg;
-  if (hipGetDevice(&c->device) != hipSuccess) {
-    delete c;
-    return JANUS_EHIP;
-  }
-  if (hipHostMalloc((void**)&c->host_word, 4 * sizeof(int), hipHostMallocDefault) != hipSuccess) {
-    delete c;
-    return JANUS_EHIP;
-  }
-  *out = c;
-  return JANUS_OK;
-}
-
-extern "C" void janus_destroy(janus_ctx* c) {
-  if (!c) return;
-  if (c->ws.ptr) (void)hipFree(c->ws.ptr);
-  if (c->aux.ptr) (void)hipFree(c->aux.ptr);
-  if (c->nl.ptr) (void)hipFree(c->nl.ptr);
-  if (c->host_word) (void)hipHostFree(c->host_word);
-  delete c;
-}
-
-extern "C" int janus_weight_layout(const janus_config* cfg, janus_tensor_desc* out, int32_t* n_tensors,
-                                   int64_t* n_floats) {
-  if (!cfg || !n_tensors || !n_floats) return JANUS_EINVAL;
-  int rc = check_config(cfg);
-  if (rc == JANUS_EINVAL) return rc;
-  Layout L = make_layout(*cfg);
-  const int cap = *n_tensors;
-  *n_tensors = (int)L.ents.size();
-  *n_floats = L.total;
-  if (!out) return JANUS_OK;
-  if (cap < (int)L.ents.size()) return JANUS_EINVAL;
-  for (size_t q = 0; q < L.ents.size(); ++q) {
-    std::memset(&out[q], 0, sizeof(janus_tensor_desc));
-    std::strncpy(out[q].name, L.ents[q].name.c_str(), sizeof(out[q].name) - 1);
-    out[q].offset = L.ents[q].off;
-    out[q].ndim = L.ents[q].ndim;
-    for (int k = 0; k < 3; ++k) out[q].shape[k] = L.ents[q].shape[k];
-  }
-  return JANUS_OK;
-}
-
-extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
-                          const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
-                          const float* W, const float* E_ref, const float* F_ref, float* loss, float* E, float* F,
-                          float* dLdW, const janus_debug* dbg, void* stream) {
-  if (!ctx || !pos || !cell || !species || !offsets || !nl || !W || !E_ref || !F_ref || !loss || !E || !F ||
-      !dLdW || n_atoms < 1 || n_struct < 1 || n_struct > n_atoms)
-    return JANUS_EINVAL;
-  if (nl->n_edges < 0 || nl->n_edges > INT32_MAX / 4 || !nl->rowptr) return JANUS_EINVAL;
-  if (nl->n_edges > 0 && (!nl->ei || !nl->ej || !nl->shift || !nl->rev)) return JANUS_EINVAL;
-  const janus_config& cfg = ctx->cfg;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  const int N = n_atoms, S = n_struct;
-  const long long Ne = nl->n_edges;
-
-  Plan p;
-  size_t bytes = plan_layout(p, nullptr, cfg, N, S, Ne);
-  int rc = ensure(ctx->ws, bytes);
-  if (rc) return rc;
-  plan_layout(p, ctx->ws.ptr, cfg, N, S, Ne);
-  const int T = p.T, Ee = p.E, k = p.k, d = p.d, h = p.hdim, nb = p.nb, nsp = p.nsp;
-  const long long M = p.M, Nd = (long long)N * d;
-  const Layout L = make_layout(cfg);
-
-  // ---- validation (one synchronous flag read)
-  JANUS_HIP_TRY(hipMemsetAsync(p.flag, 0, 4 * sizeof(int), st));
-  launch_validate_struct(st, offsets, S, N, cell, 0.f, p.flag);
-  launch_atom_struct(st, offsets, S, N, p.sid);
-  hipLaunchKernelGGL(validate_atoms_kernel, dim3(cdiv(std::max(N, S) + 1, 256)), dim3(256), 0, st, species, N, nsp,
-                     nl->rowptr, nl->ei, Ne, offsets, S, p.flag);
-  if (Ne > 0)
-    hipLaunchKernelGGL(validate_edges_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, nl->ei, nl->ej, nl->shift,
-                       nl->rev, p.sid, N, Ne, p.flag);
-  JANUS_HIP_TRY(hipGetLastError());
-  JANUS_HIP_TRY(hipMemcpyAsync(ctx->host_word, p.flag, sizeof(int), hipMemcpyDeviceToHost, st));
-  JANUS_HIP_TRY(hipStreamSynchronize(st));
-  if (ctx->host_word[0]) return JANUS_EINVAL;
-
-  const int* ei = nl->ei;
-  const int* ej = nl->ej;
-  const int* rowptr = nl->rowptr;
-  const int* rev = nl->rev;
-  auto Wp = [&](const std::string& n) { return W + L.at(n); };
-  auto Gp = [&](const std::string& n) { return dLdW + L.at(n); };
-  auto blk = [](int t, const char* n) { return "blocks." + std::to_string(t) + "." + n; };
-  const size_t ldsW = (size_t)nb * d * sizeof(float);
-  const dim3 gE = wave_grid(Ne), gN = wave_grid(N), b256(256);
-
-  JANUS_HIP_TRY(hipMemsetAsync(dLdW, 0, sizeof(float) * L.total, st));
-
-  // ---- setup: geometry, species groups, routing of every block, GEMM tables
-  launch_geometry(st, pos, cell, p.sid, ei, ej, nl->shift, (int)Ne, cfg.r_cut, nb, p.geo, p.B, p.dB);
-  hipLaunchKernelGGL(species_count_kernel, dim3(nsp), dim3(64), 0, st, species, N, nsp, p.sp_cnt);
-  launch_exclusive_scan(st, p.sp_cnt, nsp, p.sp_off, nullptr);
-  hipLaunchKernelGGL(species_write_kernel, dim3(nsp), dim3(64), 0, st, species, N, p.sp_off, p.sp_atoms);
-  hipLaunchKernelGGL(set_rows_kernel, dim3(1), dim3(64), 0, st, p.rowN, N, p.rowE, Ne);
-  build_tables(st, p.rowN, 1, p.kcN, p.tilesN, p.ntN, p.chunksN, p.ncN, p.cfN);
-  build_tables(st, p.rowE, 1, p.kcE, nullptr, nullptr, p.chunksE, p.ncE, p.cfE);
-  const long long np = (long long)nsp * nsp;
-  for (int t = 0; t < T; ++t) {
-    RouteArgs ra;
-    ra.Pc = Wp(blk(t, "Pc"));
-    ra.Pn = Wp(blk(t, "Pn"));
-    ra.beta = Wp(blk(t, "beta"));
-    ra.species = species;
-    ra.ei = ei;
-    ra.ej = ej;
-    ra.Ne = (int)Ne;
-    ra.nsp = nsp;
-    ra.E = Ee;
-    ra.k = k;
-    ra.peid = p.peid + t * np * k;
-    ra.pgate = p.pgate + t * np * k;
-    ra.pprob = p.pprob + t * np * Ee;
-    ra.pair = p.pair + t * Ne;
-    ra.eid = p.eid + t * M;
-    ra.gate = p.gate + t * M;
-    ra.cnt = p.cnt;
-    ra.colpre = p.colpre;
-    ra.total = p.total + t * Ee;
-    ra.off = p.off + t * (Ee + 1);
-    ra.pos = p.pos + t * M;
-    ra.slot_gate = p.slot_gate + t * M;
-    route_block(st, ra);
-    build_tables(st, ra.off, Ee, p.kc, p.tiles + (long long)t * p.mt, p.ntiles + t, p.chunks + (long long)t * p.mc,
-                 p.nchunks + t, p.cfirst + t * (Ee + 1));
-  }
-  JANUS_HIP_TRY(hipGetLastError());
-
-  // per-block views
-  auto Xs = [&](int t) { return p.Xs + t * M * d; };
-  auto Ab = [&](int t) { return p.Ab + t * M * h; };
-  auto Aa = [&](int t) { return p.A + t * M * h; };
-  auto Sb = [&](int t) { return p.Sb + t * M * h; };
-  auto Ybs = [&](int t) { return p.Ybs + t * M * d; };
-  auto Xbar = [&](int t) { return p.Xbar + t * Ne * d; };
-  auto Fbar = [&](int t) { return p.Fbar + t * Ne * d; };
-  auto POS = [&](int t) { return p.pos + t * M; };
-  auto GATE = [&](int t) { return p.gate + t * M; };
-  auto SG = [&](int t) { return p.slot_gate + t * M; };
-  auto TL = [&](int t) { return p.tiles + (long long)t * p.mt; };
-  auto CH = [&](int t) { return p.chunks + (long long)t * p.mc; };
-  auto CF = [&](int t) { return p.cfirst + t * (Ee + 1); };
-  auto HV = [&](float* base, int t) { return base + t * Nd; };
-
-  // ---- phase 1: forward
-  hipLaunchKernelGGL(species_rows_gather_kernel, dim3(cdiv(Nd, 256)), b256, 0, st, Wp("A"), species, N, d, p.h);
-  for (int t = 0; t < T; ++t) {
-    const float* Wb = Wp(blk(t, "W_b"));
-    const float* W1 = Wp(blk(t, "W1"));
-    const float* W2 = Wp(blk(t, "W2"));
-    if (Ne > 0)
-      LAUNCH_VPL(dispatch_x_kernel, d, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
-                                    (const int*)POS(t), k, Ne, d, Xs(t));
-    launch_rows<false>(st, LoadPlain{Xs(t), d}, W1, d, h, TL(t), p.ntiles + t, p.mt, EpiStore{Aa(t), h});
-    launch_rows<false>(st, LoadSilu{Aa(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiRowScale{p.T1, SG(t), d});
-    LAUNCH_VPL(combine_fwd_kernel, d, gN, b256, 0, st, rowptr, (const int*)POS(t), k, (const float*)p.T1,
-                                   (const float*)HV(p.h, t), N, d, HV(p.h, t + 1));
-  }
-  const float* Wo1 = Wp("W_o1");
-  const float* wo2 = Wp("w_o2");
-  const float* hT = HV(p.h, T);
-  launch_rows<false>(st, LoadPlain{hT, d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiStore{p.z, d});
-  LAUNCH_VPL(readout_kernel, d, gN, b256, 0, st, (const float*)p.z, wo2, N, d, p.eps);
-  hipLaunchKernelGGL(energy_kernel, wave_grid(S), b256, 0, st, (const float*)p.eps, offsets, S, p.Ed, E);
-
-  // ---- phase 2: force backward (hh[t] = dE/dh^t)
-  launch_rows<true>(st, LoadSiluD1Scaled{p.z, wo2, d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiStore{HV(p.hh, T), d});
-  JANUS_HIP_TRY(hipMemsetAsync(p.rbar, 0, sizeof(float) * std::max<long long>(Ne, 1), st));
-  for (int t = T - 1; t >= 0; --t) {
-    const float* Wb = Wp(blk(t, "W_b"));
-    const float* W1 = Wp(blk(t, "W1"));
-    const float* W2 = Wp(blk(t, "W2"));
-    LAUNCH_VPL(gather_atom_kernel, d, gN, b256, 0, st, rowptr, (const int*)POS(t), k, (const float*)GATE(t),
-                                   (const float*)HV(p.hh, t + 1), N, d, Ybs(t));
-    launch_rows<true>(st, LoadPlain{Ybs(t), d}, W2, d, h, TL(t), p.ntiles + t, p.mt, EpiP2{Aa(t), Sb(t), Ab(t), h});
-    launch_rows<true>(st, LoadPlain{Ab(t), h}, W1, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T1, d});
-    if (Ne > 0)
-      LAUNCH_VPL(edge_p2_kernel, d, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
-                                 (const float*)HV(p.h, t), ej, (const int*)POS(t), k, Ne, d, (const float*)p.T1,
-                                 Xbar(t), Fbar(t), p.rbar, p.Pe);
-    LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe,
-                                   (const float*)HV(p.hh, t + 1), (const float*)nullptr, N, d, HV(p.hh, t));
-  }
-  hipLaunchKernelGGL(force_kernel, dim3(cdiv(N, 256)), b256, 0, st, rowptr, rev, (const float*)p.rbar,
-                     (const float4*)p.geo, N, F);
-  hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
-                     (const float*)F, F_ref, N, cfg.w_E, cfg.w_F, loss, p.lam, p.phi);
-  if (Ne > 0)
-    hipLaunchKernelGGL(rtilde_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, ei, ej, (const float4*)p.geo,
-                       (const float*)p.phi, Ne, p.rt);
-  JANUS_HIP_TRY(hipGetLastError());
-
-  // ---- phase 3: double backward of the force loss (hht[t] = loss adjoint of hh[t])
-  for (int t = 0; t < T; ++t) {
-    const float* Wb = Wp(blk(t, "W_b"));
-    const float* W1 = Wp(blk(t, "W1"));
-    const float* W2 = Wp(blk(t, "W2"));
-    const float* hht_t = t == 0 ? nullptr : HV(p.hht, t);
-    if (Ne > 0)
-      LAUNCH_VPL(edge_p3_kernel, d, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
-                                 (const float*)HV(p.h, t), ej, (const int*)POS(t), k, Ne, d,
-                                 (const float*)Xbar(t), hht_t, (const float*)p.rt, p.T1, p.Pe);
-    // dW_b (part 1): (rt B')^T Fbar
-    launch_wgrad(st, LoadRowScale{p.dB, p.rt, nb}, LoadPlain{Fbar(t), d}, nb, d, p.chunksE, p.ncE, p.cfE, p.mcE, 1,
-                 p.partial, Gp(blk(t, "W_b")), 0);
-    LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe, (const float*)nullptr,
-                                   (const float*)nullptr, N, d, HV(p.h3, t));
-    // G7: dW1 = Xbt^T Abar
-    launch_wgrad(st, LoadPlain{p.T1, d}, LoadPlain{Ab(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee, p.partial,
-                 Gp(blk(t, "W1")), 0);
-    // G5: Abt = Xbt W1 -> Sbt (into Ab), C (into Sb)
-    launch_rows<false>(st, LoadPlain{p.T1, d}, W1, d, h, TL(t), p.ntiles + t, p.mt, EpiP3{Aa(t), Sb(t), Ab(t), h});
-    // G6: Ybt = Sbt W2
-    launch_rows<false>(st, LoadPlain{Ab(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
-    // G8: dW2 = Sbt^T Ybar
-    launch_wgrad(st, LoadPlain{Ab(t), h}, LoadPlain{Ybs(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
-                 p.partial, Gp(blk(t, "W2")), 0);
-    LAUNCH_VPL(combine_p3_kernel, d, gN, b256, 0, st, rowptr, (const int*)POS(t), k, (const float*)GATE(t),
-                                  (const float*)p.T2, (const float*)HV(p.hh, t + 1), hht_t, N, d, p.g3 + t * M,
-                                  HV(p.hht, t + 1));
-  }
-  // readout part: vt = hht^T W_o1
-  launch_rows<false>(st, LoadPlain{HV(p.hht, T), d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiStore{p.vt, d});
-  JANUS_HIP_TRY(hipGetLastError());
-
-  // ---- phase 4: final backward (adjoint of h^t reuses hh)
-  LAUNCH_VPL(readout_bwd_kernel, d, gN, b256, 0, st, (const float*)p.z, (const float*)p.vt, wo2,
-                                 (const float*)p.lam, (const int*)p.sid, N, d, p.Zr, p.Tr);
-  launch_wgrad(st, LoadPlain{hT, d}, LoadPlain{p.Zr, d}, d, d, p.chunksN, p.ncN, p.cfN, p.mcN, 1, p.partial,
-               Gp("W_o1"), 0);
-  launch_wgrad(st, LoadPlain{HV(p.hht, T), d}, LoadSiluD1Scaled{p.z, wo2, d}, d, d, p.chunksN, p.ncN, p.cfN, p.mcN,
-               1, p.partial, Gp("W_o1"), 1);
-  {
-    const int nch = (N + kColChunk - 1) / kColChunk;
-    hipLaunchKernelGGL(colsum_partial_kernel, dim3(cdiv(d, 256), nch), b256, 0, st, (const float*)p.Tr,
-                       (long long)N, d, p.colpart);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3(cdiv(d, 256)), b256, 0, st, (const float*)p.colpart, nch, d,
-                       Gp("w_o2"));
-  }
-  launch_rows<true>(st, LoadPlain{p.Zr, d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiStore{HV(p.hh, T), d});
-  for (int t = T - 1; t >= 0; --t) {
-    const float* Wb = Wp(blk(t, "W_b"));
-    const float* W1 = Wp(blk(t, "W1"));
-    const float* W2 = Wp(blk(t, "W2"));
-    const float* hht_t = t == 0 ? nullptr : HV(p.hht, t);
-    // message adjoint, ungated, into the slots
-    LAUNCH_VPL(gather_atom_kernel, d, gN, b256, 0, st, rowptr, (const int*)POS(t), k, (const float*)nullptr,
-                                   (const float*)HV(p.hh, t + 1), N, d, p.T1);
-    // G9: St = mt W2^T -> At = g SiLU'(A) St + C (into Sb); row sums for the gate adjoint
-    launch_rows<true>(st, LoadPlain{p.T1, d}, W2, d, h, TL(t), p.ntiles + t, p.mt,
-                      EpiP4{Aa(t), Sb(t), SG(t), h}, p.gpart);
-    // G10: Xt = At W1^T
-    launch_rows<true>(st, LoadPlain{Sb(t), h}, W1, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
-    // G11: dW1 += X^T At ;  G12: dW2 += SiLU(A)^T (g mt)
-    launch_wgrad(st, LoadPlain{Xs(t), d}, LoadPlain{Sb(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
-                 p.partial, Gp(blk(t, "W1")), 1);
-    launch_wgrad(st, LoadSilu{Aa(t), h}, LoadRowScale{p.T1, SG(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
-                 p.partial, Gp(blk(t, "W2")), 1);
-    if (Ne > 0) {
-      LAUNCH_VPL(edge_p4_kernel, d, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
-                                 (const int*)POS(t), k, Ne, d, (const float*)p.T2, (const float*)Xbar(t), hht_t, p.Ft,
-                                 p.Pe);
-      // dW_b (part 2): B^T Ft
-      launch_wgrad(st, LoadPlain{p.B, nb}, LoadPlain{p.Ft, d}, nb, d, p.chunksE, p.ncE, p.cfE, p.mcE, 1, p.partial,
-                   Gp(blk(t, "W_b")), 1);
-      hipLaunchKernelGGL(gate_total_kernel, dim3(cdiv(M, 256)), b256, 0, st, (const float*)(p.g3 + t * M),
-                         (const float*)p.gpart, (const int*)POS(t), M, p.ntile, p.gt);
-      hipLaunchKernelGGL(router_atom_kernel, gN, b256, 0, st, rowptr, rev, k, Ee, (const int*)(p.pair + t * Ne),
-                         (const float*)(p.pprob + t * np * Ee), (const int*)(p.eid + t * M), (const float*)p.gt, N,
-                         p.partC, p.partN);
-      hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
-                         (const int*)p.sp_atoms, (const float*)p.partC, Ee, nsp, Gp(blk(t, "Pc")));
-      hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
-                         (const int*)p.sp_atoms, (const float*)p.partN, Ee, nsp, Gp(blk(t, "Pn")));
-    }
-    LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe, (const float*)HV(p.hh, t + 1),
-                                   (const float*)HV(p.h3, t), N, d, HV(p.hh, t));
-  }
-  hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(256), 0, st, (const int*)p.sp_off, (const int*)p.sp_atoms,
-                     (const float*)HV(p.hh, 0), d, nsp, Gp("A"));
-  JANUS_HIP_TRY(hipGetLastError());
-
-  // ---- debug copies
-  if (dbg) {
-    for (int t = 0; t < T; ++t) {
-      if (dbg->eid) JANUS_HIP_TRY(hipMemcpyAsync(dbg->eid + t * M, p.eid + t * M, sizeof(int) * M, hipMemcpyDeviceToDevice, st));
-      if (dbg->gate) JANUS_HIP_TRY(hipMemcpyAsync(dbg->gate + t * M, p.gate + t * M, sizeof(float) * M, hipMemcpyDeviceToDevice, st));
-      if (dbg->pos) JANUS_HIP_TRY(hipMemcpyAsync(dbg->pos + t * M, p.pos + t * M, sizeof(int) * M, hipMemcpyDeviceToDevice, st));
-      if (dbg->counts) JANUS_HIP_TRY(hipMemcpyAsync(dbg->counts + t * Ee, p.total + t * Ee, sizeof(int) * Ee, hipMemcpyDeviceToDevice, st));
-    }
-    if (dbg->basis && Ne > 0)
-      JANUS_HIP_TRY(hipMemcpyAsync(dbg->basis, p.B, sizeof(float) * Ne * nb, hipMemcpyDeviceToDevice, st));
-  }
-  return JANUS_OK;
-}

@@ -44,6 +44,11 @@ class Edges(C.Structure):
                 ("rowptr", C.c_void_p), ("rev", C.c_void_p)]
 
 
+class ProfileEntry(C.Structure):
+    _fields_ = [("name", C.c_char * 32), ("launches", C.c_int64), ("ms", C.c_double), ("flops", C.c_double),
+                ("bytes", C.c_double)]
+
+
 class Debug(C.Structure):
     _fields_ = [("eid", C.c_void_p), ("gate", C.c_void_p), ("counts", C.c_void_p), ("pos", C.c_void_p),
                 ("basis", C.c_void_p)]
@@ -70,6 +75,8 @@ def _lib():
                                    C.POINTER(Debug), vp]
         lib.janus_grouped_gemm.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
         lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
+        lib.janus_profile_enable.argtypes = [vp, C.c_int]
+        lib.janus_profile_read.argtypes = [vp, C.POINTER(ProfileEntry), i32]
         _LIB = lib
     return _LIB
 
@@ -78,7 +85,8 @@ def exported_symbols():
     """Names the library exports (checked against include/janus.h by the CPU tests)."""
     lib = _lib()
     names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
-             "janus_grouped_gemm", "janus_grouped_wgrad", "janus_strerror"]
+             "janus_grouped_gemm", "janus_grouped_wgrad", "janus_profile_enable", "janus_profile_read",
+             "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
 
@@ -234,6 +242,22 @@ class Context:
         if rc:
             raise JanusError(rc, "janus_step")
         return loss, E, F, dW
+
+    # ------------------------------------------------------------- profiler
+    def profile(self, on: bool):
+        rc = _lib().janus_profile_enable(self.h, int(on))
+        if rc:
+            raise JanusError(rc, "janus_profile_enable")
+
+    def profile_read(self) -> dict:
+        """{family: {launches, ms, flops, bytes}} since profile(True) or the last read."""
+        buf = (ProfileEntry * 16)()
+        n = _lib().janus_profile_read(self.h, buf, 16)
+        if n < 0:
+            raise JanusError(n, "janus_profile_read")
+        return {buf[q].name.decode(): {"launches": int(buf[q].launches), "ms": float(buf[q].ms),
+                                        "flops": float(buf[q].flops), "bytes": float(buf[q].bytes)}
+                for q in range(n)}
 
     # ---------------------------------------------------------------- GEMMs
     def grouped_gemm(self, A, B, row_off, K, N, trans_b, out=None):
