@@ -123,8 +123,10 @@ typedef struct janus_edges {
  * Optional debug outputs of janus_step (any pointer may be NULL).
  *   eid     [T*Ne*top_k] int32  chosen experts, descending logit, lower index on ties
  *   gate    [T*Ne*top_k] fp32   softmax probability of each chosen expert
- *   counts  [T*n_experts] int32 tokens routed to each expert
- *   pos     [T*Ne*top_k] int32  slot of (edge, choice) in the expert-grouped order
+ *   counts  [T*n_experts] int32 tokens routed to each expert (whole batch)
+ *   pos     [T*Ne*top_k] int32  slot of (edge, choice) in the expert-grouped order;
+ *                               when the step ran in several chunks (janus_last_chunks
+ *                               > 1) slots are numbered within each chunk
  *   basis   [Ne*n_rbf]   fp32   Bessel basis with envelope at each edge length
  */
 typedef struct janus_debug {
@@ -203,6 +205,20 @@ int janus_step(janus_ctx* ctx, const float* pos, const float* cell, const int32_
                const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
                const float* W, const float* E_ref, const float* F_ref, float* loss, float* E,
                float* F, float* dLdW, const janus_debug* dbg, void* stream);
+
+/*
+ * Workspace of janus_step.  Structures are independent apart from the loss
+ * normalisation, so janus_step processes the batch in chunks of whole
+ * structures, in order, each sized so that its workspace fits `bytes`
+ * (0, the default: 90% of the device memory free at the time of the call
+ * plus what the context already holds).  Results do not depend on the
+ * chunking except through floating-point summation order of the weight
+ * gradients and loss, which is fixed for a given chunking.  A structure too
+ * large for the cap makes janus_step return JANUS_ENOMEM.
+ * janus_last_chunks returns how many chunks the last janus_step used.
+ */
+int janus_set_workspace_limit(janus_ctx* ctx, int64_t bytes);
+int janus_last_chunks(const janus_ctx* ctx);
 
 /*
  * Grouped fp32 GEMM on the matrix cores, the building block of the expert

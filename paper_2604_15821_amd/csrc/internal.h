@@ -37,7 +37,12 @@ struct janus_ctx {
   janus_buffer ws;        // per-step workspace of janus_step
   janus_buffer aux;       // tables and partials of the standalone GEMM entry points
   janus_buffer nl;        // per-atom counts and flags of janus_build_edges
+  janus_buffer gbuf;      // whole-batch arrays of janus_step (flags, structure ids, loss shares)
   int* host_word = nullptr;   // 4 pinned host ints for the flag / count reads
+  int* host_plan = nullptr;   // pinned host ints for the chunk plan
+  size_t host_plan_n = 0;
+  long long ws_limit = 0;     // workspace cap in bytes (0: from free device memory)
+  int last_chunks = 0;        // chunks used by the last janus_step
   // profiler: event pairs recorded around kernel families while enabled
   bool prof_on = false;
   std::vector<janus_prof_rec> prof_recs;

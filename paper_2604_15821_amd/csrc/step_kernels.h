@@ -108,10 +108,12 @@ __global__ void force_kernel(const int* __restrict__ rowptr, const int* __restri
 // Loss and adjoint seeds (one workgroup of 1024, fixed reduction order):
 //   loss = w_E/S sum_s (E_s/n_s - Eref_s)^2 + w_F/(3N) sum_a |F_a - Fref_a|^2
 //   lam_s = dloss/dE_s,  phi_a = dloss/dF_a.
+// S, N: structures and atoms of this chunk; S_tot, N_tot: of the whole batch
+// (the normalisation).  Writes this chunk's share of the loss to *loss_part.
 __global__ void loss_kernel(const double* __restrict__ Ed, const float* __restrict__ Eref,
                             const int* __restrict__ offsets, int S, const float* __restrict__ F,
-                            const float* __restrict__ Fref, int N, float wE, float wF, float* __restrict__ loss,
-                            float* __restrict__ lam, float* __restrict__ phi) {
+                            const float* __restrict__ Fref, int N, int S_tot, int N_tot, float wE, float wF,
+                            double* __restrict__ loss_part, float* __restrict__ lam, float* __restrict__ phi) {
   __shared__ double red[1024];
   const int t = threadIdx.x;
   double se = 0.0, sf = 0.0;
@@ -119,20 +121,56 @@ __global__ void loss_kernel(const double* __restrict__ Ed, const float* __restri
     const double n = (double)(offsets[s + 1] - offsets[s]);
     const double de = Ed[s] / n - (double)Eref[s];
     se += de * de;
-    lam[s] = (float)(2.0 * wE * de / ((double)S * n));
+    lam[s] = (float)(2.0 * wE * de / ((double)S_tot * n));
   }
   for (int q = t; q < 3 * N; q += 1024) {
     const double df = (double)F[q] - (double)Fref[q];
     sf += df * df;
-    phi[q] = (float)(2.0 * wF * df / (3.0 * N));
+    phi[q] = (float)(2.0 * wF * df / (3.0 * N_tot));
   }
-  red[t] = wE * se / S + wF * sf / (3.0 * N);
+  red[t] = wE * se / S_tot + wF * sf / (3.0 * N_tot);
   __syncthreads();
   for (int o = 512; o > 0; o >>= 1) {
     if (t < o) red[t] += red[t + o];
     __syncthreads();
   }
-  if (t == 0) *loss = (float)red[0];
+  if (t == 0) *loss_part = red[0];
+}
+
+// loss = sum of the chunk shares in chunk order.
+__global__ void loss_total_kernel(const double* __restrict__ part, int n, float* __restrict__ loss) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  double s = 0.0;
+  for (int q = 0; q < n; ++q) s += part[q];
+  *loss = (float)s;
+}
+
+// Chunk-local copies of the neighbour list: atom indices minus a0, edge
+// indices minus e0; rowptr of the chunk's atoms and offsets of its structures.
+__global__ void rebase_kernel(const int* __restrict__ ei, const int* __restrict__ ej, const int* __restrict__ rev,
+                              const int* __restrict__ rowptr, const int* __restrict__ offsets, int a0, int e0, int s0,
+                              int n_atoms, long long n_edges, int n_struct, int* __restrict__ cei,
+                              int* __restrict__ cej, int* __restrict__ crev, int* __restrict__ crow,
+                              int* __restrict__ coff) {
+  const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < n_edges) {
+    cei[q] = ei[e0 + q] - a0;
+    cej[q] = ej[e0 + q] - a0;
+    crev[q] = rev[e0 + q] - e0;
+  }
+  if (q <= n_atoms) crow[q] = rowptr[a0 + q] - e0;
+  if (q <= n_struct) coff[q] = offsets[s0 + q] - a0;
+}
+
+// First edge of each structure (for the host's chunk plan); indices clamped
+// so that offsets that fail validation cannot read out of range.
+__global__ void struct_edges_kernel(const int* __restrict__ offsets, const int* __restrict__ rowptr, int S, int N,
+                                    int* __restrict__ out) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s > S) return;
+  const int a = min(max(offsets[s], 0), N);
+  out[s] = rowptr[a];
+  out[S + 1 + s] = offsets[s];
 }
 
 // rt_e = (phi_i - phi_j) . u_e: the loss adjoint of rbar_e.
@@ -185,7 +223,7 @@ __global__ void colsum_final_kernel(const float* __restrict__ part, int nch, int
   if (c >= cols) return;
   float s = 0.f;
   for (int q = 0; q < nch; ++q) s += part[(long long)q * cols + c];
-  out[c] = s;
+  out[c] += s;
 }
 
 // Total gate adjoint of (e, c): double-backward part plus the final-backward
@@ -239,7 +277,7 @@ __global__ void species_rows_kernel(const int* __restrict__ sp_off, const int* _
   for (int c = threadIdx.x; c < w; c += blockDim.x) {
     float acc = 0.f;
     for (int q = sp_off[s]; q < sp_off[s + 1]; ++q) acc += M[(long long)sp_atoms[q] * w + c];
-    out[(long long)s * w + c] = acc;
+    out[(long long)s * w + c] += acc;
   }
 }
 
@@ -389,6 +427,8 @@ struct Plan {
   float *Xs, *A, *Sb, *Ab, *Ybs, *Xbar, *Fbar, *g3;
   // temporaries
   float *T1, *T2, *Pe, *Ft, *gpart, *gt, *partC, *partN, *partial;
+  // chunk-local neighbour list (indices relative to the chunk)
+  int *cei, *cej, *crev, *crow, *coff;
   // sizes
   int T, E, k, d, hdim, nb, nsp, N, S;
   long long Ne, M;
@@ -496,6 +536,11 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   part = std::max(part, (long long)p.mcN * d * d);
   part = std::max(part, (long long)p.mcE * p.nb * d);
   p.partial = cv.take<float>(part);
+  p.cei = cv.take<int>(Ne + 1);
+  p.cej = cv.take<int>(Ne + 1);
+  p.crev = cv.take<int>(Ne + 1);
+  p.crow = cv.take<int>(N + 1);
+  p.coff = cv.take<int>(S + 1);
   return cv.size();
 }
 

@@ -1,0 +1,61 @@
+"""The chunked step (batch split into runs of whole structures to fit the
+workspace) against the single-pass step and the oracle."""
+import numpy as np
+import pytest
+
+from helpers import TOL_E, TOL_F, TOL_LOSS, TOL_W, banner, energy_error, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+
+def _step(b, limit=None):
+    import torch
+    from paper_2604_15821_amd import janus
+    d = janus.upload(b)
+    ctx = janus.Context(b.model)
+    if limit is not None:
+        ctx.set_workspace_limit(limit)
+    nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+    loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"])
+    torch.cuda.synchronize()
+    out = (float(loss.cpu()[0]), E.cpu().numpy(), F.cpu().numpy(), dW.cpu().numpy(), ctx.last_chunks())
+    ctx.close()
+    return out
+
+
+def test_chunked_step_matches_single_pass_and_oracle():
+    from oracle.model import Params, forward_energy, training_step
+    from paper_2604_15821_amd import janus
+    from paper_2604_15821_amd.synth import make_batch, subset
+    b = subset(make_batch("small"), range(6))
+    banner("chunks small-6")
+    l1, E1, F1, W1, c1 = _step(b)
+    assert c1 == 1
+    # a cap of ~2.5 structures' workspace forces three or more chunks
+    l2, E2, F2, W2, c2 = _step(b, limit=int(2.5 * 1.1e8))
+    print("chunks", c2)
+    assert c2 >= 3
+    # energies and forces are per structure: identical bit for bit
+    assert (E1 == E2).all() and (F1 == F2).all()
+    # gradients and loss only change summation order
+    assert abs(l1 - l2) <= 1e-6 * abs(l1)
+    assert rel_l2(W2, W1) <= 1e-6
+    loss, E, F, grad, aux = training_step(b, return_aux=True)
+    _, cache = forward_energy(b.species, aux["graph"], Params.from_weights(b.weights, b.model), aux["routing"])
+    assert energy_error(E2, E, cache["eps"], b.offsets) <= TOL_E
+    assert abs(l2 - loss) <= TOL_LOSS * abs(loss)
+    assert rel_l2(F2, F) <= TOL_F
+    got = janus.unpack(W2, b.model)
+    for name, ref in grad.items():
+        if not name.endswith("beta"):
+            assert rel_l2(got[name], ref) <= TOL_W, name
+
+
+def test_structure_larger_than_workspace_is_rejected():
+    from paper_2604_15821_amd import janus
+    from paper_2604_15821_amd.synth import make_batch, subset
+    b = subset(make_batch("small"), range(2))
+    banner("chunks too small")
+    with pytest.raises(janus.JanusError) as ex:
+        _step(b, limit=1 << 20)
+    assert ex.value.code == janus.JANUS_ENOMEM
