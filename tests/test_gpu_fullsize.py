@@ -1,0 +1,148 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py
+uses (whole batch, default workspace), on outputs the oracle can compute
+structure by structure, plus properties that hold at any size:
+
+* energies and forces of sampled structures against the oracle (structures
+  are independent, so a one-structure oracle run gives them exactly);
+* net force of every structure is zero; outputs are finite; the loss equals
+  the loss recomputed from the returned energies and forces;
+* the weight gradient of the batch equals the sum of the gradients of a
+  partition of its structures, each computed with the batch normalisation
+  (w_E * S_part / S and w_F * N_part / N), and one part is checked against
+  the oracle's weight gradient.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from helpers import TOL_E, TOL_F, TOL_W, banner, energy_error, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+FULL = ["small", "shard", "irregular"]
+
+
+def _gpu_step(b, model=None):
+    import torch
+    from paper_2604_15821_amd import janus
+    m = model or b.model
+    d = janus.upload(b)
+    ctx = janus.Context(m)
+    nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+    loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"])
+    torch.cuda.synchronize()
+    out = {"loss": float(loss.cpu()[0]), "E": E.cpu().numpy(), "F": F.cpu().numpy(), "dW": dW.cpu().numpy(),
+           "chunks": ctx.last_chunks(), "edges": nl.n_edges}
+    ctx.close()
+    del d, nl, loss, E, F, dW
+    torch.cuda.empty_cache()
+    return out
+
+
+def _scaled_part(b, structs):
+    """Sub-batch of `structs` with loss weights that reproduce its share of the batch gradient."""
+    from paper_2604_15821_amd.synth import subset
+    sb = subset(b, structs)
+    m = dataclasses.replace(b.model, w_E=b.model.w_E * sb.n_struct / b.n_struct,
+                            w_F=b.model.w_F * sb.n_atoms / b.n_atoms)
+    return dataclasses.replace(sb, model=m)
+
+
+@pytest.fixture(scope="module", params=FULL)
+def full(request):
+    from paper_2604_15821_amd.synth import make_batch
+    name = request.param
+    b = make_batch(name)
+    banner("full-size", name, b.n_struct, "structures", b.n_atoms, "atoms")
+    out = _gpu_step(b)
+    print(f"  {out['edges']} edges, {out['chunks']} chunk(s)", flush=True)
+    return name, b, out
+
+
+def test_outputs_finite_and_net_force_zero(full):
+    name, b, out = full
+    assert np.isfinite(out["E"]).all() and np.isfinite(out["F"]).all() and np.isfinite(out["dW"]).all()
+    F = out["F"].astype(np.float64)
+    for s in range(b.n_struct):
+        a0, a1 = b.offsets[s], b.offsets[s + 1]
+        net = np.abs(F[a0:a1].sum(0)).max()
+        assert net <= 1e-5 * np.abs(F[a0:a1]).sum() + 1e-12, (s, net)
+
+
+def test_loss_matches_returned_energies_and_forces(full):
+    name, b, out = full
+    m = b.model
+    n = np.diff(b.offsets).astype(np.float64)
+    de = out["E"].astype(np.float64) / n - b.E_ref.astype(np.float64)
+    dF = out["F"].astype(np.float64) - b.F_ref.astype(np.float64)
+    loss = m.w_E * (de * de).sum() / b.n_struct + m.w_F * (dF * dF).sum() / (3.0 * b.n_atoms)
+    assert abs(out["loss"] - loss) <= 1e-5 * abs(loss)
+
+
+def test_sampled_structures_energy_and_forces(full):
+    from oracle.model import Params, build_graph, forces, forward_energy, route_all
+    from paper_2604_15821_amd.synth import subset
+    name, b, out = full
+    sizes = np.diff(b.offsets)
+    rng = np.random.default_rng(0)
+    # the smallest structure and one random one
+    picks = sorted({int(np.argmin(sizes)), int(rng.integers(0, b.n_struct))})
+    for s in picks:
+        banner("oracle E/F", name, "structure", s, int(sizes[s]), "atoms")
+        sb = subset(b, [s])
+        m = sb.model
+        P = Params.from_weights(sb.weights, m)
+        g = build_graph(sb.pos, sb.cell, sb.offsets, m.r_cut, m.n_rbf)
+        rt = route_all(sb.species, g, P)
+        E, cache = forward_energy(sb.species, g, P, rt)
+        F = forces(sb.species, g, P, rt, cache)
+        a0, a1 = b.offsets[s], b.offsets[s + 1]
+        err = energy_error(out["E"][s:s + 1], E, cache["eps"], np.array([0, a1 - a0]))
+        ferr = rel_l2(out["F"][a0:a1], F)
+        print(f"  structure {s}: energy error {err:.2e}, force rel L2 {ferr:.2e}", flush=True)
+        assert err <= TOL_E
+        assert ferr <= TOL_F
+
+
+def test_weight_gradient_is_sum_over_structure_groups(full):
+    name, b, out = full
+    bounds = np.linspace(0, b.n_struct, 4).astype(int)
+    total = np.zeros_like(out["dW"], dtype=np.float64)
+    for q in range(3):
+        banner("partition", name, bounds[q], bounds[q + 1])
+        part = _gpu_step(_scaled_part(b, range(bounds[q], bounds[q + 1])))
+        total += part["dW"]
+    from paper_2604_15821_amd import janus
+    got = janus.unpack(out["dW"], b.model)
+    ref = janus.unpack(total, b.model)
+    for k in got:
+        if not k.endswith("beta"):
+            assert rel_l2(got[k], ref[k]) <= 1e-5, (k, rel_l2(got[k], ref[k]))
+
+
+def test_sampled_weight_gradient_against_oracle(full):
+    from oracle.model import training_step
+    from paper_2604_15821_amd import janus
+    name, b, out = full
+    s = int(np.argmin(np.diff(b.offsets)))
+    banner("oracle dW", name, "structure", s)
+    part = _scaled_part(b, [s])
+    g = _gpu_step(part)
+    loss, E, F, grad = training_step(part)
+    got = janus.unpack(g["dW"], part.model)
+    worst = 0.0
+    for k, ref in grad.items():
+        if k.endswith("beta"):
+            continue
+        if np.linalg.norm(ref) == 0.0:
+            assert (got[k] == 0).all(), k
+            continue
+        e = rel_l2(got[k], ref)
+        worst = max(worst, e)
+        assert e <= TOL_W, (k, e)
+        if k.endswith("W1") or k.endswith("W2"):
+            for x in range(ref.shape[0]):          # experts without tokens: exact zeros
+                if not ref[x].any():
+                    assert not got[k][x].any(), (k, x)
+    print(f"  worst per-tensor rel L2 {worst:.2e}", flush=True)
