@@ -59,6 +59,8 @@ def main():
     ap.add_argument("--workload", default="small")
     ap.add_argument("--cpu-structs", type=int, default=12)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="one device-to-device copy of this many MiB before the run (calibrates HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path",
@@ -70,6 +72,14 @@ def main():
 
     from paper_2604_15821_amd import janus
     from paper_2604_15821_amd.synth import WORKLOADS, make_batch
+
+    if args.copy_mib > 0:
+        src = torch.ones(args.copy_mib << 18, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {args.copy_mib} MiB read + {args.copy_mib} MiB written")
+        del src, dst
 
     wl = WORKLOADS[args.workload]
     m = wl.model
