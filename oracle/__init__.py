@@ -17,6 +17,8 @@ together with the model reading written out in the module docstrings):
 * ``model``      -- energy, conservative forces F = -dE/dR, the
                     energy+force loss, and every weight gradient of the
                     loss (second order), hand-derived.
+* ``threebody``  -- bond-triplet features (Legendre of the bond angle times a
+                    radial basis), their tangents and displacement adjoints.
 
 Every function cites the passage of the paper it follows.  Where the paper
 is silent the reading used is stated in the docstring.

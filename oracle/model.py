@@ -24,6 +24,11 @@ taken in float32 so that both sides take them identically.
 
 beta is a fixed routing bias (it receives no gradient).
 
+With the angular three-body term (``threebody.py``) the edge token gains
+the messages of the bond triplets whose first bond is e:
+    X_e   = F_e * h_{j(e)} + q_e,   q_e = sum_{tau = (e, .)} MoE3(Z_tau)
+and the forces and second-order sweeps carry the angle derivatives.
+
 Second order (paper Sec. "Runtime for multi-phase double-backward
 execution": the force loss needs derivatives of F with respect to the
 weights).  With lam_s = dL/dE_s and phi_a = dL/dF_a held fixed,
@@ -44,8 +49,9 @@ from dataclasses import dataclass
 import numpy as np
 import scipy.sparse as sp
 
+from . import threebody as tb
 from .basis import bessel_basis, silu, silu_d1, silu_d2, silu_family
-from .neighbors import neighbor_list, reverse_map
+from .neighbors import neighbor_list, reverse_map, triplet_list
 
 
 # --------------------------------------------------------------------------- helpers
@@ -65,11 +71,15 @@ class Params:
     T: int
     k: int
     E: int
+    three: bool = False
+    k3: int = 0
+    E3: int = 0
 
     @classmethod
     def from_weights(cls, weights, model):
         w = {n: np.asarray(v, np.float64) for n, v in weights.items()}
-        return cls(w=w, T=model.n_blocks, k=model.top_k, E=model.n_experts)
+        return cls(w=w, T=model.n_blocks, k=model.top_k, E=model.n_experts, three=bool(model.three_body),
+                   k3=model.top_k3, E3=model.n_experts3)
 
     def blk(self, t, name):
         return self.w[f"blocks.{t}.{name}"]
@@ -90,6 +100,7 @@ class Graph:
     dB: np.ndarray      # [Ne, Nb]
     struct_of_atom: np.ndarray
     n_atoms_struct: np.ndarray
+    tri: object = None  # threebody.Triplets when the model has the angular term
 
 
 def edge_geometry(pos, cell, offsets, ei, ej, shift):
@@ -107,16 +118,30 @@ def edge_geometry(pos, cell, offsets, ei, ej, shift):
     return d, r, d / r[:, None], sid
 
 
-def build_graph(batch_pos, cell, offsets, r_cut, n_rbf, edges=None):
-    """Neighbour list (unless given as (ei, ej, shift, rowptr)) plus geometry and basis."""
+def build_graph(batch_pos, cell, offsets, r_cut, n_rbf, edges=None, three=None):
+    """Neighbour list (unless given as (ei, ej, shift, rowptr)) plus geometry and basis.
+
+    three = (r_cut3, n_legendre) adds the bond triplets and their features.
+    """
     if edges is None:
         edges = neighbor_list(batch_pos, cell, offsets, r_cut)
     ei, ej, shift, rowptr = edges
     d, r, u, sid = edge_geometry(batch_pos, cell, offsets, ei, ej, shift)
     B, dB, _ = bessel_basis(r, r_cut, n_rbf)
     nst = np.diff(np.asarray(offsets, np.int64))
+    tri = None
+    if three is not None:
+        r3, n_l = three
+        te, te2, trp = triplet_list(ei, ej, shift, batch_pos, cell, offsets, rowptr, r3)
+        tri = tb.triplet_features(te, te2, trp, r, u, r3, n_rbf, n_l)
     return Graph(ei=ei, ej=ej, shift=shift, rowptr=rowptr, d=d, r=r, u=u, B=B, dB=dB,
-                 struct_of_atom=sid, n_atoms_struct=nst)
+                 struct_of_atom=sid, n_atoms_struct=nst, tri=tri)
+
+
+def build_graph_for(batch, edges=None):
+    m = batch.model
+    three = (m.r_cut3, m.n_legendre) if m.three_body else None
+    return build_graph(batch.pos, batch.cell, batch.offsets, m.r_cut, m.n_rbf, edges, three)
 
 
 # --------------------------------------------------------------------------- routing
@@ -129,6 +154,7 @@ class Routing:
     counts: np.ndarray   # [E] int32 tokens per expert
     pos: np.ndarray      # [Ne, k] int32 slot of (e, c) in the expert-grouped order
     inv: np.ndarray      # [Ne*k] int32 flattened (e*k + c) held by each slot
+    tri: object = None   # routing of the triplet tokens of the same block (three-body term)
 
 
 def route(species, ei, ej, Pc, Pn, beta, k):
@@ -140,8 +166,25 @@ def route(species, ei, ej, Pc, Pn, beta, k):
     """
     Zi = species[ei]; Zj = species[ej]
     l32 = (np.asarray(Pc, np.float32)[Zi] + np.asarray(Pn, np.float32)[Zj]) + np.asarray(beta, np.float32)[None, :]
-    eid = np.argsort(-l32, axis=1, kind="stable")[:, :k].astype(np.int32)
     l64 = (np.asarray(Pc, np.float64)[Zi] + np.asarray(Pn, np.float64)[Zj]) + np.asarray(beta, np.float64)[None, :]
+    return _route_logits(l32, l64, k)
+
+
+def route_triplets(species, g, P3a, P3b, P3c, beta3, k3):
+    """Routing of triplet tokens by the species of the vertex and of both neighbours:
+    logits ((P3a[Z_i] + P3b[Z_j(e)]) + P3c[Z_j(e2)]) + beta3, decided in float32."""
+    tri = g.tri
+    Zi, Z1, Z2 = species[g.ei[tri.te]], species[g.ej[tri.te]], species[g.ej[tri.te2]]
+    f32 = lambda a: np.asarray(a, np.float32)
+    f64 = lambda a: np.asarray(a, np.float64)
+    l32 = ((f32(P3a)[Zi] + f32(P3b)[Z1]) + f32(P3c)[Z2]) + f32(beta3)[None, :]
+    l64 = ((f64(P3a)[Zi] + f64(P3b)[Z1]) + f64(P3c)[Z2]) + f64(beta3)[None, :]
+    return _route_logits(l32, l64, k3)
+
+
+def _route_logits(l32, l64, k):
+    """Top-k on float32 logits (lower index first on ties), gates from the float64 softmax."""
+    eid = np.argsort(-l32, axis=1, kind="stable")[:, :k].astype(np.int32)
     l64 = l64 - l64.max(1, keepdims=True)
     ex = np.exp(l64)
     prob = ex / ex.sum(1, keepdims=True)
@@ -156,14 +199,21 @@ def route(species, ei, ej, Pc, Pn, beta, k):
 
 
 def route_all(species, g: Graph, P: Params):
-    return [route(species, g.ei, g.ej, P.blk(t, "Pc"), P.blk(t, "Pn"), P.blk(t, "beta"), P.k)
-            for t in range(P.T)]
+    """Routing of every block (edges, and triplets when the model has the angular term)."""
+    out = []
+    for t in range(P.T):
+        rt = route(species, g.ei, g.ej, P.blk(t, "Pc"), P.blk(t, "Pn"), P.blk(t, "beta"), P.k)
+        if g.tri is not None:
+            rt.tri = route_triplets(species, g, P.blk(t, "P3a"), P.blk(t, "P3b"), P.blk(t, "P3c"),
+                                    P.blk(t, "beta3"), P.k3)
+        out.append(rt)
+    return out
 
 
 # --------------------------------------------------------------------------- forward
 
 def _expert_groups(rt: Routing, E):
-    """For each (choice c, expert x): the edge rows that send slot c to x."""
+    """For each (choice c, expert x): the token rows that send slot c to x."""
     out = []
     for c in range(rt.eid.shape[1]):
         for x in range(E):
@@ -173,19 +223,45 @@ def _expert_groups(rt: Routing, E):
     return out
 
 
+def _moe(rt, E, W1, W2, X):
+    """sum_c g_c W2_x^T SiLU(W1_x^T X) for every token row of X."""
+    m = np.zeros((X.shape[0], W2.shape[2]))
+    for c, x, rows in _expert_groups(rt, E):
+        m[rows] += rt.gate[rows, c][:, None] * (silu(X[rows] @ W1[x]) @ W2[x])
+    return m
+
+
+def _moe_backward(rt, E, W1, W2, X, mbar):
+    """Adjoint of the MoE input X given the adjoint mbar of its output."""
+    Xbar = np.zeros_like(X)
+    for c, x, rows in _expert_groups(rt, E):
+        A = X[rows] @ W1[x]
+        Sbar = (rt.gate[rows, c][:, None] * mbar[rows]) @ W2[x].T
+        Xbar[rows] += (silu_d1(A) * Sbar) @ W1[x].T
+    return Xbar
+
+
+def _tri_tokens(g, P, t, h):
+    """Z_tau = (G_tau W_a) * h_{j(e2)}; returns (G W_a, h_{j(e2)}, Z)."""
+    Zpre = g.tri.G @ P.blk(t, "W_a")
+    hj2 = h[g.ej[g.tri.te2]]
+    return Zpre, hj2, Zpre * hj2
+
+
 def forward_energy(species, g: Graph, P: Params, routing):
     """Forward pass: per-structure energies and the stored atom features h^t."""
     N = species.shape[0]
+    Ne = g.ei.shape[0]
     h = P.w["A"][species]
     hs = [h]
     for t in range(P.T):
         F = g.B @ P.blk(t, "W_b")
         X = F * h[g.ej]
-        m = np.zeros_like(X)
-        W1, W2 = P.blk(t, "W1"), P.blk(t, "W2")
-        for c, x, rows in _expert_groups(routing[t], P.E):
-            Y = silu(X[rows] @ W1[x]) @ W2[x]
-            m[rows] += routing[t].gate[rows, c][:, None] * Y
+        if g.tri is not None:
+            _, _, Z = _tri_tokens(g, P, t, h)
+            y = _moe(routing[t].tri, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z)
+            X = X + _seg(g.tri.te, Ne, y)
+        m = _moe(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X)
         h = h + _seg(g.ei, N, m)
         hs.append(h)
     z = h @ P.w["W_o1"]
@@ -194,28 +270,40 @@ def forward_energy(species, g: Graph, P: Params, routing):
     return E, {"h": hs, "z": z, "eps": eps}
 
 
+def _block_tokens(g, P, t, h, routing):
+    """X_e of block t (edge part plus the triplet messages)."""
+    F = g.B @ P.blk(t, "W_b")
+    X = F * h[g.ej]
+    if g.tri is not None:
+        _, _, Z = _tri_tokens(g, P, t, h)
+        y = _moe(routing[t].tri, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z)
+        X = X + _seg(g.tri.te, g.ei.shape[0], y)
+    return F, X
+
+
 def forces(species, g: Graph, P: Params, routing, cache):
     """Conservative forces F = -dE/dR by one hand-derived reverse sweep."""
     N = species.shape[0]
+    Ne = g.ei.shape[0]
     hs, z = cache["h"], cache["z"]
     hbar = (silu_d1(z) * P.w["w_o2"][None, :]) @ P.w["W_o1"].T      # dE/dh^T
-    rbar = np.zeros(g.r.shape[0])                                     # dE/dr_e
+    rbar = np.zeros(Ne)                                               # dE/dr_e (radial filter)
+    Gvec = np.zeros((Ne, 3))                                          # dE/dd_e (triplet features)
     for t in reversed(range(P.T)):
         h = hs[t]
-        F = g.B @ P.blk(t, "W_b")
-        X = F * h[g.ej]
-        mbar = hbar[g.ei]
-        Xbar = np.zeros_like(X)
-        W1, W2 = P.blk(t, "W1"), P.blk(t, "W2")
-        rt = routing[t]
-        for c, x, rows in _expert_groups(rt, P.E):
-            A = X[rows] @ W1[x]
-            Sbar = (rt.gate[rows, c][:, None] * mbar[rows]) @ W2[x].T
-            Xbar[rows] += (silu_d1(A) * Sbar) @ W1[x].T
+        F, X = _block_tokens(g, P, t, h, routing)
+        Xbar = _moe_backward(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, hbar[g.ei])
+        hbar_next = hbar + _seg(g.ej, N, Xbar * F)
+        if g.tri is not None:
+            Zpre, hj2, Z = _tri_tokens(g, P, t, h)
+            Zbar = _moe_backward(routing[t].tri, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z, Xbar[g.tri.te])
+            hbar_next = hbar_next + _seg(g.ej[g.tri.te2], N, Zbar * Zpre)
+            Gbar = (Zbar * hj2) @ P.blk(t, "W_a").T
+            Gvec += tb.displacement_adjoint(g.tri, g.r, g.u, Gbar, Ne)
         Fbar = Xbar * h[g.ej]
         rbar += ((Fbar @ P.blk(t, "W_b").T) * g.dB).sum(1)
-        hbar = hbar + _seg(g.ej, N, Xbar * F)
-    G = rbar[:, None] * g.u                                           # dE/dd_e
+        hbar = hbar_next
+    G = rbar[:, None] * g.u + Gvec                                    # dE/dd_e
     dEdR = _seg(g.ej, N, G) - _seg(g.ei, N, G)
     return -dEdR
 
@@ -239,6 +327,43 @@ def loss_and_seeds(E, F, E_ref, F_ref, n_atoms_struct, w_E=1.0, w_F=1.0):
 
 # --------------------------------------------------------------------------- second order
 
+def _moe_tangent(rt, E, W1, W2, X, Xd):
+    """MoE output and its tangent for input X and input tangent Xd."""
+    m = np.zeros((X.shape[0], W2.shape[2]))
+    md = np.zeros_like(m)
+    for c, x, rows in _expert_groups(rt, E):
+        A, Ad = X[rows] @ W1[x], Xd[rows] @ W1[x]
+        gt = rt.gate[rows, c][:, None]
+        s0, s1, _ = silu_family(A)
+        m[rows] += gt * (s0 @ W2[x])
+        md[rows] += gt * ((s1 * Ad) @ W2[x])
+    return m, md
+
+
+def _tri_tangent_tokens(g, P, t, h, hd, Gd):
+    """Triplet tokens and their tangents: Z = (G W_a) h_j2, Zd = (Gd W_a) h_j2 + (G W_a) hd_j2."""
+    Wa = P.blk(t, "W_a")
+    Zpre, Zpred = g.tri.G @ Wa, Gd @ Wa
+    j2 = g.ej[g.tri.te2]
+    hj2, hdj2 = h[j2], hd[j2]
+    return Zpre, Zpred, hj2, hdj2, Zpre * hj2, Zpred * hj2 + Zpre * hdj2
+
+
+def _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing):
+    """X_e, its tangent, and the radial filter with its tangent for block t."""
+    Wb = P.blk(t, "W_b")
+    F, Fd = g.B @ Wb, Bdot @ Wb
+    X = F * h[g.ej]
+    Xd = Fd * h[g.ej] + F * hd[g.ej]
+    if g.tri is not None:
+        Ne = g.ei.shape[0]
+        _, _, _, _, Z, Zd = _tri_tangent_tokens(g, P, t, h, hd, Gd)
+        y, yd = _moe_tangent(routing[t].tri, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z, Zd)
+        X = X + _seg(g.tri.te, Ne, y)
+        Xd = Xd + _seg(g.tri.te, Ne, yd)
+    return F, Fd, X, Xd
+
+
 def energy_tangent(species, g: Graph, P: Params, routing, phi):
     """Tangent forward sweep along positions R + e*phi.
 
@@ -246,30 +371,59 @@ def energy_tangent(species, g: Graph, P: Params, routing, phi):
     tangent atom features for the reverse sweep.
     """
     N = species.shape[0]
-    rdot = ((phi[g.ej] - phi[g.ei]) * g.u).sum(1)                      # dr_e/de
+    ddot = phi[g.ej] - phi[g.ei]                                       # d(d_e)/de
+    rdot = (ddot * g.u).sum(1)                                         # dr_e/de
     Bdot = g.dB * rdot[:, None]
+    Gd = tb.feature_tangent(g.tri, g.r, g.u, ddot) if g.tri is not None else None
     h = P.w["A"][species]
     hd = np.zeros_like(h)
     hs, hds = [h], [hd]
     for t in range(P.T):
-        Wb = P.blk(t, "W_b")
-        F, Fd = g.B @ Wb, Bdot @ Wb
-        X = F * h[g.ej]
-        Xd = Fd * h[g.ej] + F * hd[g.ej]
-        m = np.zeros_like(X); md = np.zeros_like(X)
-        W1, W2 = P.blk(t, "W1"), P.blk(t, "W2")
-        for c, x, rows in _expert_groups(routing[t], P.E):
-            A, Ad = X[rows] @ W1[x], Xd[rows] @ W1[x]
-            gt = routing[t].gate[rows, c][:, None]
-            s0, s1, _ = silu_family(A)
-            m[rows] += gt * (s0 @ W2[x])
-            md[rows] += gt * ((s1 * Ad) @ W2[x])
+        F, Fd, X, Xd = _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing)
+        m, md = _moe_tangent(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd)
         h = h + _seg(g.ei, N, m)
         hd = hd + _seg(g.ei, N, md)
         hs.append(h); hds.append(hd)
     z, zd = h @ P.w["W_o1"], hd @ P.w["W_o1"]
     epsd = (silu_d1(z) * zd) @ P.w["w_o2"]
-    return epsd.sum(), {"h": hs, "hd": hds, "z": z, "zd": zd, "rdot": rdot, "Bdot": Bdot}
+    return epsd.sum(), {"h": hs, "hd": hds, "z": z, "zd": zd, "rdot": rdot, "Bdot": Bdot, "Gd": Gd}
+
+
+def _moe_reverse(rt, E, W1, W2, X, Xd, Pm, Tm):
+    """Reverse sweep of a MoE layer through its primal and tangent outputs.
+
+    Pm, Tm: adjoints of the output and of its tangent.  Returns the adjoints
+    of the input and its tangent, the expert weight gradients and the
+    adjoint of every gate.
+    """
+    PX = np.zeros_like(X)
+    TX = np.zeros_like(X)
+    Pg = np.zeros(rt.gate.shape)
+    dW1, dW2 = np.zeros_like(W1), np.zeros_like(W2)
+    for c, x, rows in _expert_groups(rt, E):
+        gt = rt.gate[rows, c][:, None]
+        A, Ad = X[rows] @ W1[x], Xd[rows] @ W1[x]
+        s0, s1, s2 = silu_family(A)
+        S, Sd = s0, s1 * Ad
+        Y, Yd = S @ W2[x], Sd @ W2[x]
+        Pg[rows, c] = (Y * Pm[rows]).sum(1) + (Yd * Tm[rows]).sum(1)
+        PY, TY = gt * Pm[rows], gt * Tm[rows]
+        dW2[x] += S.T @ PY + Sd.T @ TY
+        PS, TS = PY @ W2[x].T, TY @ W2[x].T
+        TAd = s1 * TS
+        PA = s1 * PS + s2 * Ad * TS
+        dW1[x] += X[rows].T @ PA + Xd[rows].T @ TAd
+        PX[rows] += PA @ W1[x].T
+        TX[rows] += TAd @ W1[x].T
+    return PX, TX, dW1, dW2, Pg
+
+
+def _logit_adjoint(rt, Pg):
+    """Adjoint of the router logits from the adjoints of the chosen gates
+    (gates are softmax probabilities: dp_x/dl_y = p_x (delta_xy - p_y))."""
+    Pp = np.zeros(rt.prob.shape)
+    np.put_along_axis(Pp, rt.eid.astype(np.int64), Pg, 1)
+    return rt.prob * (Pp - (rt.prob * Pp).sum(1, keepdims=True))
 
 
 def weight_gradient(species, g: Graph, P: Params, routing, lam, phi):
@@ -278,10 +432,12 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi):
     Adjoint names: Pq is the adjoint of primal q, Tq the adjoint of tangent q.
     """
     N = species.shape[0]
+    Ne = g.ei.shape[0]
     _, tc = energy_tangent(species, g, P, routing, phi)
-    hs, hds, z, zd, Bdot = tc["h"], tc["hd"], tc["z"], tc["zd"], tc["Bdot"]
+    hs, hds, z, zd, Bdot, Gd = tc["h"], tc["hd"], tc["z"], tc["zd"], tc["Bdot"], tc["Gd"]
     wo1, wo2 = P.w["W_o1"], P.w["w_o2"]
     grad = {n: np.zeros_like(v) for n, v in P.w.items()}
+    S_ = P.w["A"].shape[0]
 
     lam_atom = lam[g.struct_of_atom][:, None]
     # Psi = sum_i lam_s(i) w_o2.SiLU(z_i) - sum_i w_o2.(SiLU'(z_i) zd_i)
@@ -293,46 +449,41 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi):
 
     for t in reversed(range(P.T)):
         h, hd = hs[t], hds[t]
-        Wb = P.blk(t, "W_b")
-        F, Fd = g.B @ Wb, Bdot @ Wb
-        X = F * h[g.ej]
-        Xd = Fd * h[g.ej] + F * hd[g.ej]
-        Pm, Tm = Ph[g.ei], Th[g.ei]
-        PX = np.zeros_like(X); TX = np.zeros_like(X)
+        F, Fd, X, Xd = _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing)
         rt = routing[t]
-        Pg = np.zeros(rt.gate.shape)
-        W1, W2 = P.blk(t, "W1"), P.blk(t, "W2")
-        dW1, dW2 = np.zeros_like(W1), np.zeros_like(W2)
-        for c, x, rows in _expert_groups(rt, P.E):
-            gt = rt.gate[rows, c][:, None]
-            A, Ad = X[rows] @ W1[x], Xd[rows] @ W1[x]
-            s0, s1, s2 = silu_family(A)
-            S, Sd = s0, s1 * Ad
-            Y, Yd = S @ W2[x], Sd @ W2[x]
-            Pg[rows, c] = (Y * Pm[rows]).sum(1) + (Yd * Tm[rows]).sum(1)
-            PY, TY = gt * Pm[rows], gt * Tm[rows]
-            dW2[x] += S.T @ PY + Sd.T @ TY
-            PS, TS = PY @ W2[x].T, TY @ W2[x].T
-            TAd = s1 * TS
-            PA = s1 * PS + s2 * Ad * TS
-            dW1[x] += X[rows].T @ PA + Xd[rows].T @ TAd
-            PX[rows] += PA @ W1[x].T
-            TX[rows] += TAd @ W1[x].T
+        PX, TX, dW1, dW2, Pg = _moe_reverse(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd, Ph[g.ei], Th[g.ei])
         grad[f"blocks.{t}.W1"] = dW1
         grad[f"blocks.{t}.W2"] = dW2
-        # X = F * h_j ;  Xd = Fd * h_j + F * hd_j
+        # X = F * h_j (+ q) ;  Xd = Fd * h_j + F * hd_j (+ qd)
         PF = PX * h[g.ej] + TX * hd[g.ej]
         TFd = TX * h[g.ej]
         grad[f"blocks.{t}.W_b"] = g.B.T @ PF + Bdot.T @ TFd
-        Ph = Ph + _seg(g.ej, N, PX * F + TX * Fd)
-        Th = Th + _seg(g.ej, N, TX * F)
+        Ph_new = Ph + _seg(g.ej, N, PX * F + TX * Fd)
+        Th_new = Th + _seg(g.ej, N, TX * F)
         # gates: g_ec = softmax(l_e)[eid_ec];  l_e = Pc[Z_i] + Pn[Z_j] + beta
-        Pp = np.zeros(rt.prob.shape)
-        np.put_along_axis(Pp, rt.eid.astype(np.int64), Pg, 1)
-        Pl = rt.prob * (Pp - (rt.prob * Pp).sum(1, keepdims=True))
-        S_ = P.w["A"].shape[0]
+        Pl = _logit_adjoint(rt, Pg)
         grad[f"blocks.{t}.Pc"] = _seg(species[g.ei], S_, Pl)
         grad[f"blocks.{t}.Pn"] = _seg(species[g.ej], S_, Pl)
+        if g.tri is not None:
+            tri, rt3 = g.tri, rt.tri
+            Zpre, Zpred, hj2, hdj2, Z, Zd = _tri_tangent_tokens(g, P, t, h, hd, Gd)
+            # q_e = sum over the triplets of e, so the token adjoints are those of X_e
+            PZ, TZ, dW1a, dW2a, Pg3 = _moe_reverse(rt3, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z, Zd,
+                                                  PX[tri.te], TX[tri.te])
+            grad[f"blocks.{t}.W1a"] = dW1a
+            grad[f"blocks.{t}.W2a"] = dW2a
+            # Z = Zpre * h_j2 ;  Zd = Zpred * h_j2 + Zpre * hd_j2 ;  Zpre = G W_a, Zpred = Gd W_a
+            PZpre = PZ * hj2 + TZ * hdj2
+            TZpred = TZ * hj2
+            grad[f"blocks.{t}.W_a"] = tri.G.T @ PZpre + Gd.T @ TZpred
+            j2 = g.ej[tri.te2]
+            Ph_new = Ph_new + _seg(j2, N, PZ * Zpre + TZ * Zpred)
+            Th_new = Th_new + _seg(j2, N, TZ * Zpre)
+            Pl3 = _logit_adjoint(rt3, Pg3)
+            grad[f"blocks.{t}.P3a"] = _seg(species[g.ei[tri.te]], S_, Pl3)
+            grad[f"blocks.{t}.P3b"] = _seg(species[g.ej[tri.te]], S_, Pl3)
+            grad[f"blocks.{t}.P3c"] = _seg(species[j2], S_, Pl3)
+        Ph, Th = Ph_new, Th_new
     grad["A"] = _seg(species, P.w["A"].shape[0], Ph)
     return grad
 
@@ -346,10 +497,8 @@ def training_step(batch, edges=None, return_aux=False):
     weight's shape).  With return_aux, also the graph and routing.
     """
     m = batch.model
-    if m.three_body:
-        raise NotImplementedError("three-body term: see oracle.threebody")
     P = Params.from_weights(batch.weights, m)
-    g = build_graph(batch.pos, batch.cell, batch.offsets, m.r_cut, m.n_rbf, edges)
+    g = build_graph_for(batch, edges)
     routing = route_all(batch.species, g, P)
     E, cache = forward_energy(batch.species, g, P, routing)
     F = forces(batch.species, g, P, routing, cache)
