@@ -65,8 +65,12 @@ enum {
  *   d_hidden   expert hidden width; multiple of 64
  *   env_p      envelope exponent; only 6 is implemented
  *   r_cut      neighbour cutoff in Angstrom
- *   three_body non-zero enables the angular triplet term (not in this build:
- *              JANUS_EUNSUPPORTED)
+ *   three_body non-zero enables the angular triplet term: triplets of bonds
+ *              shorter than r_cut3 sharing an atom, features Legendre P_l(cos
+ *              theta), l < n_legendre (at most 8), times the Bessel basis at
+ *              r_cut3, routed over n_experts3 experts (top_k3) of width
+ *              d_hidden3 (multiple of 64); n_legendre * n_rbf * d * 4 bytes
+ *              must fit 64 KB
  *   w_E, w_F   loss weights of the energy and force terms
  */
 typedef struct janus_config {
@@ -128,6 +132,12 @@ typedef struct janus_edges {
  *                               when the step ran in several chunks (janus_last_chunks
  *                               > 1) slots are numbered within each chunk
  *   basis   [Ne*n_rbf]   fp32   Bessel basis with envelope at each edge length
+ * With the three-body term (Nt = number of bond triplets; the caller sizes
+ * these from its own count):
+ *   tri_e, tri_e2 [Nt] int32   first and second edge of every triplet, in
+ *                               (e, e2) order
+ *   eid3   [T*Nt*top_k3] int32 chosen triplet experts
+ *   gate3  [T*Nt*top_k3] fp32  their gates
  */
 typedef struct janus_debug {
   int32_t* eid;
@@ -135,6 +145,10 @@ typedef struct janus_debug {
   int32_t* counts;
   int32_t* pos;
   float* basis;
+  int32_t* tri_e;
+  int32_t* tri_e2;
+  int32_t* eid3;
+  float* gate3;
 } janus_debug;
 
 /* Create a context for `cfg` on the current device.  The context owns its
@@ -149,8 +163,10 @@ void janus_destroy(janus_ctx* ctx);
 
 /* Layout of the flat weight blob for `cfg`.  Order: A [n_species, d]; for
  * each block t: W_b [n_rbf, d], Pc [n_species, E], Pn [n_species, E],
- * beta [E], W1 [E, d, d_hidden], W2 [E, d_hidden, d]; then W_o1 [d, d],
- * w_o2 [d].  If `out` is NULL only the counts are written.  *n_tensors (in:
+ * beta [E], W1 [E, d, d_hidden], W2 [E, d_hidden, d], and with the
+ * three-body term W_a [n_legendre*n_rbf, d], P3a, P3b, P3c [n_species, E3],
+ * beta3 [E3], W1a [E3, d, d_hidden3], W2a [E3, d_hidden3, d]; then
+ * W_o1 [d, d], w_o2 [d].  If `out` is NULL only the counts are written.  *n_tensors (in:
  * capacity of out, out: number of tensors) and *n_floats (total blob size)
  * are host pointers.  Errors: JANUS_EINVAL (capacity too small). */
 int janus_weight_layout(const janus_config* cfg, janus_tensor_desc* out, int32_t* n_tensors,

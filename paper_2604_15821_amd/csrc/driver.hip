@@ -108,7 +108,15 @@ struct ChunkArgs {
   int S_tot, N_tot;
   long long Ne_tot;
   int index;
+  long long Nt;                  // triplets of the chunk (three-body term)
+  long long t0, Nt_tot;          // first triplet of the chunk, triplets of the batch
+  const unsigned char* tshort;   // whole-batch short-bond flags
 };
+
+__global__ void copy_add_kernel(int* __restrict__ dst, const int* __restrict__ src, long long n, int add) {
+  const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < n) dst[q] = src[q] + add;
+}
 
 int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const ChunkArgs& ca, const float* pos_g,
               const float* cell_g, const int32_t* species_g, const int32_t* offsets_g, const janus_edges* nl,
@@ -162,9 +170,28 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   const double by_p4 = Ne * (4.0 * k * d + 4.0 * k + 4.0 * nb + 20.0 * d);
 
   // ---- setup: geometry, species groups, routing of every block, GEMM tables
+  const bool three = p.three != 0;
+  const long long Nt = p.Nt, M3 = p.M3;
+  const int E3 = p.E3, k3 = p.k3, h3 = p.hd3, L3 = p.L3, nf = p.nf;
   {
     PROF(PROF_GRAPH, 0, Ne * (12.0 + 3.0 + 16.0 + 8.0 * nb));
-    launch_geometry(st, pos, cell, p.sid, ei, ej, shift, (int)Ne, cfg.r_cut, nb, p.geo, p.B, p.dB);
+    launch_geometry(st, pos, cell, p.sid, ei, ej, shift, (int)Ne, cfg.r_cut, nb, p.geo, p.B, p.dB,
+                    three ? cfg.r_cut3 : 0.f, p.B3, p.dB3, p.u3, p.du3);
+  }
+  if (three) {
+    // triplets of the chunk: CSR by first edge, reverse map, cosines
+    PROF(PROF_GRAPH, 0, Ne * 8.0 + Nt * 16.0);
+    const unsigned char* tsh = ca.tshort + ca.e0;
+    hipLaunchKernelGGL(tri_count_kernel, dim3(cdiv(N, 256)), dim3(256), 0, st, rowptr, tsh, N, p.tcount);
+    launch_exclusive_scan(st, p.tcount, (int)Ne, p.trow, nullptr);
+    if (Nt > 0) {
+      hipLaunchKernelGGL(tri_write_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, ei, rowptr, tsh,
+                         (const int*)p.trow, Ne, p.te, p.te2);
+      hipLaunchKernelGGL(tri_rev_kernel, dim3(cdiv(Nt, 256)), dim3(256), 0, st, (const int*)p.te,
+                         (const int*)p.te2, (const int*)p.trow, (const float4*)p.geo, Nt, p.trev, p.tc);
+    }
+    hipLaunchKernelGGL(set_rows_kernel, dim3(1), dim3(64), 0, st, p.rowT, (int)Nt, p.rowT, Nt);
+    build_tables(st, p.rowT, 1, p.kcT, nullptr, nullptr, p.chunksT, p.ncT, p.cfT);
   }
   const long long np = (long long)nsp * nsp;
   {
@@ -202,9 +229,38 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       route_block(st, ra);
       build_tables(st, ra.off, Ee, p.kc, p.tiles + (long long)t * p.mt, p.ntiles + t,
                    p.chunks + (long long)t * p.mc, p.nchunks + t, p.cfirst + t * (Ee + 1));
+      if (three) {
+        if (Nt > 0)
+          hipLaunchKernelGGL(tri_route_kernel, dim3(cdiv(Nt, 128)), dim3(128), 0, st, species, ei, ej,
+                             (const int*)p.te, (const int*)p.te2, Nt, Wp(blk(t, "P3a")), Wp(blk(t, "P3b")),
+                             Wp(blk(t, "P3c")), Wp(blk(t, "beta3")), E3, k3, p.eid3 + t * M3, p.gate3 + t * M3);
+        sort_tokens(st, p.eid3 + t * M3, p.gate3 + t * M3, M3, E3, p.cnt3, p.colpre3, p.total3 + t * E3,
+                    p.off3 + t * (E3 + 1), p.pos3 + t * M3, p.slot_gate3 + t * M3);
+        build_tables(st, p.off3 + t * (E3 + 1), E3, p.kc3, p.tiles3 + (long long)t * p.mt3, p.ntiles3 + t,
+                     p.chunks3 + (long long)t * p.mc3, p.nchunks3 + t, p.cfirst3 + t * (E3 + 1));
+      }
     }
   }
   JANUS_HIP_TRY(hipGetLastError());
+
+  // triplet views of block t
+  auto POS3 = [&](int t) { return (const int*)(p.pos3 + t * M3); };
+  auto GATE3 = [&](int t) { return (const float*)(p.gate3 + t * M3); };
+  auto SG3 = [&](int t) { return (const float*)(p.slot_gate3 + t * M3); };
+  auto TL3 = [&](int t) { return (const RowsTile*)(p.tiles3 + (long long)t * p.mt3); };
+  auto CH3 = [&](int t) { return (const WChunk*)(p.chunks3 + (long long)t * p.mc3); };
+  auto CF3 = [&](int t) { return (const int*)(p.cfirst3 + t * (E3 + 1)); };
+  auto Z3s = [&](int t) { return p.Z3s + t * M3 * d; };
+  auto A3 = [&](int t) { return p.A3 + t * M3 * h3; };
+  auto S3b = [&](int t) { return p.S3b + t * M3 * h3; };
+  auto A3b = [&](int t) { return p.A3b + t * M3 * h3; };
+  auto Y3bs = [&](int t) { return p.Y3bs + t * M3 * d; };
+  auto Zbar3 = [&](int t) { return p.Zbar3 + t * Nt * d; };
+  const size_t ldsWa = (size_t)nf * d * sizeof(float);
+  const dim3 gT = wave_grid(Nt);
+  const double f_tri = 2.0 * M3 * d * h3;
+  const double f_wa = 2.0 * Nt * nf * d;
+  const double by_tri = Nt * (8.0 * d + 4.0 * k3 * d + 24.0);
 
   // per-block views
   auto Xs = [&](int t) { return p.Xs + t * M * d; };
@@ -231,10 +287,35 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     const float* Wb = Wp(blk(t, "W_b"));
     const float* W1 = Wp(blk(t, "W1"));
     const float* W2 = Wp(blk(t, "W2"));
+    if (three && Nt > 0) {
+      // triplet tokens -> triplet experts -> messages Q_e of each edge's triplets
+      {
+        PROF(PROF_EDGE, 0, by_tri);
+        LAUNCH_VPL(tri_dispatch_kernel, d, gT, b256, ldsWa, st, (const int*)p.te, (const int*)p.te2,
+                   (const float*)p.tc, (const float*)p.B3, (const float*)p.dB3, (const float*)p.u3,
+                   (const float*)p.du3, Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), POS3(t), k3, Nt, d,
+                   Z3s(t));
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_tri, 0);
+        launch_rows<false>(st, LoadPlain{Z3s(t), d}, Wp(blk(t, "W1a")), d, h3, TL3(t), p.ntiles3 + t, p.mt3,
+                           EpiStore{A3(t), h3});
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_tri, 0);
+        launch_rows<false>(st, LoadSilu{A3(t), h3}, Wp(blk(t, "W2a")), h3, d, TL3(t), p.ntiles3 + t, p.mt3,
+                           EpiRowScale{p.T3a, SG3(t), d});
+      }
+      {
+        PROF(PROF_EDGE, 0, Ne * 8.0 * d + M3 * 4.0 * d);
+        LAUNCH_VPL(tri_combine_kernel, d, gE, b256, 0, st, (const int*)p.trow, POS3(t), k3, (const float*)p.T3a, Ne,
+                   d, p.Q);
+      }
+    }
     if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_dispatch);
       LAUNCH_VPL(dispatch_x_kernel, d, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
-                 POS(t), k, Ne, d, Xs(t));
+                 POS(t), k, Ne, d, Xs(t), (const float*)(three && Nt > 0 ? p.Q : nullptr));
     }
     {
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
@@ -270,6 +351,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                       EpiDense{HV(p.hh, T), d});
   }
   JANUS_HIP_TRY(hipMemsetAsync(p.rbar, 0, sizeof(float) * std::max<long long>(Ne, 1), st));
+  if (three) JANUS_HIP_TRY(hipMemsetAsync(p.tacc, 0, sizeof(float4) * (Nt + 1), st));
   for (int t = T - 1; t >= 0; --t) {
     const float* Wb = Wp(blk(t, "W_b"));
     const float* W1 = Wp(blk(t, "W1"));
@@ -293,6 +375,33 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       LAUNCH_VPL(edge_p2_kernel, d, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
                  (const float*)HV(p.h, t), ej, POS(t), k, Ne, d, (const float*)p.T1, Xbar(t), Fbar(t), p.rbar, p.Pe);
     }
+    if (three && Nt > 0) {
+      // triplet messages' backward: Ybar3 = g3 Xbar_e -> experts -> Zbar; feature-geometry adjoints
+      {
+        PROF(PROF_EDGE, 0, Ne * 4.0 * d + M3 * 4.0 * d);
+        LAUNCH_VPL(tri_gather_kernel, d, gE, b256, 0, st, (const int*)p.trow, POS3(t), k3, GATE3(t),
+                   (const float*)Xbar(t), Ne, d, Y3bs(t));
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_tri, 0);
+        launch_rows<true>(st, LoadPlain{Y3bs(t), d}, Wp(blk(t, "W2a")), d, h3, TL3(t), p.ntiles3 + t, p.mt3,
+                          EpiP2{A3(t), S3b(t), A3b(t), h3});
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_tri, 0);
+        launch_rows<true>(st, LoadPlain{A3b(t), h3}, Wp(blk(t, "W1a")), h3, d, TL3(t), p.ntiles3 + t, p.mt3,
+                          EpiStore{p.T3a, d});
+      }
+      {
+        PROF(PROF_EDGE, 0, by_tri + Nt * 8.0 * d);
+        LAUNCH_VPL(tri_p2_kernel, d, gT, b256, ldsWa, st, (const int*)p.te, (const int*)p.te2, (const float*)p.tc,
+                   (const float*)p.B3, (const float*)p.dB3, (const float*)p.u3, (const float*)p.du3,
+                   Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), POS3(t), k3, Nt, d,
+                   (const float*)p.T3a, Zbar3(t), p.PT, p.tacc);
+        LAUNCH_VPL(tri_second_sum_kernel, d, gE, b256, 0, st, (const int*)p.trow, (const int*)p.trev,
+                   (const float*)p.PT, Ne, d, p.Pe);
+      }
+    }
     {
       PROF(PROF_ATOM, 0, by_scatter);
       LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe,
@@ -301,13 +410,21 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   }
   {
     PROF(PROF_OTHER, 0, Ne * 40.0 + N * 24.0);
+    if (three && Ne > 0)
+      hipLaunchKernelGGL(tri_edge_vec_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, (const int*)p.trow,
+                         (const int*)p.trev, (const int*)p.te2, (const float*)p.tc, (const float4*)p.geo,
+                         (const float4*)p.tacc, Ne, p.gvec);
     hipLaunchKernelGGL(force_kernel, dim3(cdiv(N, 256)), b256, 0, st, rowptr, rev, (const float*)p.rbar,
-                       (const float4*)p.geo, N, F);
+                       (const float4*)p.geo, (const float4*)(three ? p.gvec : nullptr), N, F);
     hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
                        (const float*)F, F_ref, N, ca.S_tot, ca.N_tot, cfg.w_E, cfg.w_F, loss_part, p.lam, p.phi);
     if (Ne > 0)
       hipLaunchKernelGGL(rtilde_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, ei, ej, (const float4*)p.geo,
                          (const float*)p.phi, Ne, p.rt);
+    if (three && Nt > 0)
+      hipLaunchKernelGGL(tri_ctilde_kernel, dim3(cdiv(Nt, 256)), b256, 0, st, (const int*)p.te, (const int*)p.te2,
+                         (const float*)p.tc, (const float4*)p.geo, ei, ej, (const float*)p.phi, (const float*)p.rt,
+                         Nt, p.tct);
   }
   JANUS_HIP_TRY(hipGetLastError());
 
@@ -317,11 +434,59 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     const float* W1 = Wp(blk(t, "W1"));
     const float* W2 = Wp(blk(t, "W2"));
     const float* hht_t = t == 0 ? nullptr : HV(p.hht, t);
+    const bool tri_t = three && Nt > 0;
+    if (tri_t) {
+      // double backward of the triplet messages: Zbar~ -> triplet experts -> Ybar3~ -> QX_e
+      const float* W1a = Wp(blk(t, "W1a"));
+      const float* W2a = Wp(blk(t, "W2a"));
+      {
+        PROF(PROF_EDGE, 0, by_tri + Nt * 12.0 * d);
+        LAUNCH_VPL(tri_p3_kernel, d, gT, b256, ldsWa, st, (const int*)p.te, (const int*)p.te2, (const float*)p.tc,
+                   (const float*)p.B3, (const float*)p.dB3, (const float*)p.u3, (const float*)p.du3,
+                   Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), hht_t, (const float4*)p.tct,
+                   (const float*)Zbar3(t), POS3(t), k3, Nt, d, p.T3a, p.VT, p.PT);
+      }
+      {
+        // dW_a (part 1): Gt^T (Zbar * h_j2)
+        PROF(PROF_DENSE_GEMM, f_wa, 0);
+        launch_wgrad(st, LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, p.tct, nb}, LoadPlain{p.VT, d}, nf,
+                     d, p.chunksT, p.ncT, p.cfT, p.mcT, 1, p.partial, Gp(blk(t, "W_a")), 1);
+      }
+      {
+        PROF(PROF_EXPERT_WGRAD, f_tri, 0);
+        launch_wgrad(st, LoadPlain{p.T3a, d}, LoadPlain{A3b(t), h3}, d, h3, CH3(t), p.nchunks3 + t, CF3(t), p.mc3,
+                     E3, p.partial, Gp(blk(t, "W1a")), 1);
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_tri, 0);
+        launch_rows<false>(st, LoadPlain{p.T3a, d}, W1a, d, h3, TL3(t), p.ntiles3 + t, p.mt3,
+                           EpiP3{A3(t), S3b(t), A3b(t), h3});
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_tri, 0);
+        launch_rows<false>(st, LoadPlain{A3b(t), h3}, W2a, h3, d, TL3(t), p.ntiles3 + t, p.mt3, EpiStore{p.T3b, d});
+      }
+      {
+        PROF(PROF_EXPERT_WGRAD, f_tri, 0);
+        launch_wgrad(st, LoadPlain{A3b(t), h3}, LoadPlain{Y3bs(t), d}, h3, d, CH3(t), p.nchunks3 + t, CF3(t), p.mc3,
+                     E3, p.partial, Gp(blk(t, "W2a")), 1);
+      }
+      {
+        PROF(PROF_EDGE, 0, Ne * 8.0 * d + M3 * (8.0 + 4.0 * d));
+        LAUNCH_VPL(tri_combine_p3_kernel, d, gE, b256, 0, st, (const int*)p.trow, POS3(t), k3, GATE3(t),
+                   (const float*)p.T3b, (const float*)Xbar(t), Ne, d, p.g3t + t * M3, p.Q);
+      }
+    }
     if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_p3);
       LAUNCH_VPL(edge_p3_kernel, d, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
                  (const float*)HV(p.h, t), ej, POS(t), k, Ne, d, (const float*)Xbar(t), hht_t, (const float*)p.rt,
-                 p.T1, p.Pe);
+                 p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr));
+    }
+    if (tri_t) {
+      PROF(PROF_EDGE, 0, Ne * 8.0 * d + Nt * 4.0 * d);
+      LAUNCH_VPL(tri_second_sum_kernel, d, gE, b256, 0, st, (const int*)p.trow, (const int*)p.trev,
+                 (const float*)p.PT, Ne, d, p.Pe);
     }
     {
       // dW_b (part 1): (rt B')^T Fbar
@@ -427,7 +592,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       {
         PROF(PROF_EDGE, 0, by_p4);
         LAUNCH_VPL(edge_p4_kernel, d, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
-                   POS(t), k, Ne, d, (const float*)p.T2, (const float*)Xbar(t), hht_t, p.Ft, p.Pe);
+                   POS(t), k, Ne, d, (const float*)p.T2, (const float*)Xbar(t), hht_t, p.Ft, p.Pe,
+                   three ? p.Q : (float*)nullptr);
       }
       {
         // dW_b (part 2): B^T Ft
@@ -446,6 +612,68 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                            (const int*)p.sp_atoms, (const float*)p.partC, Ee, nsp, Gp(blk(t, "Pc")));
         hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
                            (const int*)p.sp_atoms, (const float*)p.partN, Ee, nsp, Gp(blk(t, "Pn")));
+      }
+    }
+    if (three && Nt > 0) {
+      // final backward of the triplet messages: mt = Xt_e (adjoint of X_e) -> experts -> Zt
+      const float* W1a = Wp(blk(t, "W1a"));
+      const float* W2a = Wp(blk(t, "W2a"));
+      {
+        PROF(PROF_EDGE, 0, Ne * 4.0 * d + M3 * 4.0 * d);
+        LAUNCH_VPL(tri_gather_kernel, d, gE, b256, 0, st, (const int*)p.trow, POS3(t), k3, (const float*)nullptr,
+                   (const float*)p.Q, Ne, d, p.T3a);
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_tri, 0);
+        launch_rows<true>(st, LoadPlain{p.T3a, d}, W2a, d, h3, TL3(t), p.ntiles3 + t, p.mt3,
+                          EpiP4{A3(t), S3b(t), SG3(t), h3}, p.gpart3);
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_tri, 0);
+        launch_rows<true>(st, LoadPlain{S3b(t), h3}, W1a, h3, d, TL3(t), p.ntiles3 + t, p.mt3, EpiStore{p.T3b, d});
+      }
+      {
+        PROF(PROF_EXPERT_WGRAD, f_tri, 0);
+        launch_wgrad(st, LoadPlain{Z3s(t), d}, LoadPlain{S3b(t), h3}, d, h3, CH3(t), p.nchunks3 + t, CF3(t), p.mc3,
+                     E3, p.partial, Gp(blk(t, "W1a")), 1);
+      }
+      {
+        PROF(PROF_EXPERT_WGRAD, f_tri, 0);
+        launch_wgrad(st, LoadSilu{A3(t), h3}, LoadRowScale{p.T3a, SG3(t), d}, h3, d, CH3(t), p.nchunks3 + t, CF3(t),
+                     p.mc3, E3, p.partial, Gp(blk(t, "W2a")), 1);
+      }
+      {
+        PROF(PROF_EDGE, 0, by_tri + Nt * 8.0 * d);
+        LAUNCH_VPL(tri_p4_kernel, d, gT, b256, ldsWa, st, (const int*)p.te, (const int*)p.te2, (const float*)p.tc,
+                   (const float*)p.B3, (const float*)p.dB3, (const float*)p.u3, (const float*)p.du3,
+                   Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), hht_t, (const float*)Zbar3(t), POS3(t),
+                   k3, Nt, d, (const float*)p.T3b, p.VT, p.PT);
+        LAUNCH_VPL(tri_second_sum_kernel, d, gE, b256, 0, st, (const int*)p.trow, (const int*)p.trev,
+                   (const float*)p.PT, Ne, d, p.Pe);
+      }
+      {
+        // dW_a (part 2): G^T (Zt * h_j2 + Q * Zbar)
+        PROF(PROF_DENSE_GEMM, f_wa, 0);
+        launch_wgrad(st, LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, nullptr, nb}, LoadPlain{p.VT, d},
+                     nf, d, p.chunksT, p.ncT, p.cfT, p.mcT, 1, p.partial, Gp(blk(t, "W_a")), 1);
+      }
+      {
+        // triplet router tables: logit adjoints summed per vertex / neighbour species
+        PROF(PROF_OTHER, 0, 0);
+        hipLaunchKernelGGL(gate_total_kernel, dim3(cdiv(M3, 256)), b256, 0, st, (const float*)(p.g3t + t * M3),
+                           (const float*)p.gpart3, POS3(t), M3, p.ntile3, p.gt3);
+        hipLaunchKernelGGL(tri_router_edge_kernel, gE, b256, 0, st, (const int*)p.trow, (const int*)p.trev, E3, k3,
+                           species, ei, ej, (const int*)p.te, (const int*)p.te2, Wp(blk(t, "P3a")),
+                           Wp(blk(t, "P3b")), Wp(blk(t, "P3c")), Wp(blk(t, "beta3")),
+                           (const int*)(p.eid3 + t * M3), (const float*)p.gt3, Ne, p.LB, p.LC);
+        hipLaunchKernelGGL(tri_router_atom_kernel, gN, b256, 0, st, rowptr, rev, E3, (const float*)p.LB,
+                           (const float*)p.LC, N, p.pa, p.pb, p.pc);
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+                           (const int*)p.sp_atoms, (const float*)p.pa, E3, nsp, Gp(blk(t, "P3a")));
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+                           (const int*)p.sp_atoms, (const float*)p.pb, E3, nsp, Gp(blk(t, "P3b")));
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+                           (const int*)p.sp_atoms, (const float*)p.pc, E3, nsp, Gp(blk(t, "P3c")));
       }
     }
     {
@@ -481,6 +709,23 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     if (dbg->basis && Ne > 0)
       JANUS_HIP_TRY(hipMemcpyAsync(dbg->basis + ca.e0 * nb, p.B, sizeof(float) * Ne * nb, hipMemcpyDeviceToDevice,
                                    st));
+    if (three && Nt > 0) {
+      if (dbg->tri_e)
+        hipLaunchKernelGGL(copy_add_kernel, dim3(cdiv(Nt, 256)), dim3(256), 0, st, dbg->tri_e + ca.t0,
+                           (const int*)p.te, Nt, (int)ca.e0);
+      if (dbg->tri_e2)
+        hipLaunchKernelGGL(copy_add_kernel, dim3(cdiv(Nt, 256)), dim3(256), 0, st, dbg->tri_e2 + ca.t0,
+                           (const int*)p.te2, Nt, (int)ca.e0);
+      const long long Mt3 = ca.Nt_tot * k3, f3 = ca.t0 * k3;
+      for (int t = 0; t < T; ++t) {
+        if (dbg->eid3)
+          JANUS_HIP_TRY(hipMemcpyAsync(dbg->eid3 + t * Mt3 + f3, p.eid3 + t * M3, sizeof(int) * M3,
+                                       hipMemcpyDeviceToDevice, st));
+        if (dbg->gate3)
+          JANUS_HIP_TRY(hipMemcpyAsync(dbg->gate3 + t * Mt3 + f3, p.gate3 + t * M3, sizeof(float) * M3,
+                                       hipMemcpyDeviceToDevice, st));
+      }
+    }
   }
   return JANUS_OK;
 }
@@ -503,11 +748,14 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
   const Layout L = make_layout(cfg);
 
   // ---- whole-batch buffers and host plan buffer
+  const bool three = cfg.three_body != 0;
   Carver gv(nullptr);
   gv.take<int>(4);
   gv.take<int>(N);
   gv.take<int>(2 * (S + 1));
   gv.take<double>(S + 1);
+  gv.take<unsigned char>(three ? Ne + 1 : 1);
+  gv.take<long long>(S + 1);
   int rc = ensure(ctx->gbuf, gv.size());
   if (rc) return rc;
   Carver g2(ctx->gbuf.ptr);
@@ -515,7 +763,9 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
   int* sid = g2.take<int>(N);
   int* sedge = g2.take<int>(2 * (S + 1));
   double* loss_part = g2.take<double>(S + 1);
-  const size_t need_host = 4 + 2 * (size_t)(S + 1);
+  unsigned char* tshort = g2.take<unsigned char>(three ? Ne + 1 : 1);
+  long long* scount = g2.take<long long>(S + 1);
+  const size_t need_host = 4 + 2 * (size_t)(S + 1) + 2 * (size_t)(S + 2);
   if (ctx->host_plan_n < need_host) {
     if (ctx->host_plan) (void)hipHostFree(ctx->host_plan);
     ctx->host_plan = nullptr;
@@ -546,6 +796,24 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
   if (hp[0]) return JANUS_EINVAL;
   const int* h_erow = hp + 4;            // first edge of structure s
   const int* h_off = hp + 4 + (S + 1);   // first atom of structure s
+  // triplets per structure (second read, once the indices are known to be valid)
+  long long* h_tri = reinterpret_cast<long long*>(hp + 4 + 2 * (S + 1) + ((4 + 2 * (S + 1)) & 1));
+  if (three) {
+    {
+      PROF(PROF_GRAPH, 0, Ne * 32.0);
+      if (Ne > 0)
+        hipLaunchKernelGGL(tri_short_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, pos, cell, (const int*)sid,
+                           nl->ei, nl->ej, nl->shift, Ne, cfg.r_cut3, tshort);
+      hipLaunchKernelGGL(tri_struct_count_kernel, wave_grid(S), dim3(256), 0, st, offsets, nl->rowptr,
+                         (const unsigned char*)tshort, S, scount);
+    }
+    JANUS_HIP_TRY(hipGetLastError());
+    JANUS_HIP_TRY(hipMemcpyAsync(h_tri, scount, sizeof(long long) * S, hipMemcpyDeviceToHost, st));
+    JANUS_HIP_TRY(hipStreamSynchronize(st));
+  }
+  std::vector<long long> tpre(S + 1, 0);
+  for (int s = 0; s < S && three; ++s) tpre[s + 1] = tpre[s] + h_tri[s];
+  auto tri_between = [&](int s0, int s1) { return tpre[s1] - tpre[s0]; };
 
   // ---- chunk plan: greedy runs of whole structures whose workspace fits the budget
   size_t budget = (size_t)ctx->ws_limit;
@@ -561,14 +829,15 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
     int s0 = 0;
     while (s0 < S) {
       int s1 = s0 + 1;
-      size_t b1 = plan_layout(tmp, nullptr, cfg, h_off[s1] - h_off[s0], 1, (long long)h_erow[s1] - h_erow[s0]);
+      size_t b1 = plan_layout(tmp, nullptr, cfg, h_off[s1] - h_off[s0], 1, (long long)h_erow[s1] - h_erow[s0],
+                              tri_between(s0, s1));
       if (b1 > budget) return JANUS_ENOMEM;
       // grow by doubling, then bisect, to keep the plan O(S log S)
       int step = 1;
       while (s1 < S) {
         const int s2 = std::min(S, s1 + step);
         const size_t b = plan_layout(tmp, nullptr, cfg, h_off[s2] - h_off[s0], s2 - s0,
-                                     (long long)h_erow[s2] - h_erow[s0]);
+                                     (long long)h_erow[s2] - h_erow[s0], tri_between(s0, s2));
         if (b > budget) {
           if (step == 1) break;
           step = 1;
@@ -589,6 +858,10 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
       ca.N_tot = N;
       ca.Ne_tot = Ne;
       ca.index = (int)chunks.size();
+      ca.Nt = tri_between(s0, s1);
+      ca.t0 = tpre[s0];
+      ca.Nt_tot = tpre[S];
+      ca.tshort = tshort;
       chunks.push_back(ca);
       need = std::max(need, b1);
       s0 = s1;
@@ -602,7 +875,7 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
   if (dbg && dbg->counts) JANUS_HIP_TRY(hipMemsetAsync(dbg->counts, 0, sizeof(int) * cfg.n_blocks * cfg.n_experts, st));
   for (const ChunkArgs& ca : chunks) {
     Plan p;
-    plan_layout(p, ctx->ws.ptr, cfg, ca.N, ca.S, ca.Ne);
+    plan_layout(p, ctx->ws.ptr, cfg, ca.N, ca.S, ca.Ne, ca.Nt);
     rc = run_chunk(ctx, st, p, L, ca, pos, cell, species, offsets, nl, W, E_ref, F_ref, loss_part + ca.index, E, F,
                    dLdW, dbg);
     if (rc) return rc;

@@ -40,11 +40,13 @@ __device__ __forceinline__ void load_lds(float* s, const float* g, int n) {
   for (long long var = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); \
        var < (count); var += nw_)
 
-// Phase 1: X_e = F_e * h_j, written to the slots of its k experts.
+// Phase 1: X_e = F_e * h_j (+ Q_e, the triplet messages of e when present),
+// written to the slots of its k experts.
 template <int VPL>
 __global__ void dispatch_x_kernel(const float* __restrict__ B, int nb, const float* __restrict__ Wb,
                                   const float* __restrict__ h, const int* __restrict__ ej,
-                                  const int* __restrict__ pos, int k, long long Ne, int d, float* __restrict__ Xs) {
+                                  const int* __restrict__ pos, int k, long long Ne, int d, float* __restrict__ Xs,
+                                  const float* __restrict__ Q) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
@@ -53,7 +55,7 @@ __global__ void dispatch_x_kernel(const float* __restrict__ B, int nb, const flo
     const float* hj = h + (long long)ej[e] * d;
     float X[VPL];
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) X[v] = F[v] * hj[v * 64 + l];
+    for (int v = 0; v < VPL; ++v) X[v] = F[v] * hj[v * 64 + l] + (Q ? Q[e * d + v * 64 + l] : 0.f);
     for (int c = 0; c < k; ++c) {
       float* o = Xs + (long long)pos[e * k + c] * d;
 #pragma unroll
@@ -173,7 +175,7 @@ __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restr
                                const float* __restrict__ Wb, const float* __restrict__ h, const int* __restrict__ ej,
                                const int* __restrict__ pos, int k, long long Ne, int d, const float* __restrict__ Xbar,
                                const float* __restrict__ hht, const float* __restrict__ rt, float* __restrict__ Xbts,
-                               float* __restrict__ P) {
+                               float* __restrict__ P, const float* __restrict__ QX) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
@@ -188,7 +190,7 @@ __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restr
       const int col = v * 64 + l;
       const float fbt = r * Fp[v];
       const float q = hht ? hht[j * d + col] : 0.f;
-      X[v] = q * F[v] + fbt * h[j * d + col];
+      X[v] = q * F[v] + fbt * h[j * d + col] + (QX ? QX[e * d + col] : 0.f);
       P[e * d + col] = fbt * Xbar[e * d + col];
     }
     for (int c = 0; c < k; ++c) {
@@ -241,7 +243,7 @@ __global__ void edge_p4_kernel(const float* __restrict__ B, int nb, const float*
                                const float* __restrict__ h, const int* __restrict__ ej, const int* __restrict__ pos,
                                int k, long long Ne, int d, const float* __restrict__ Xts,
                                const float* __restrict__ Xbar, const float* __restrict__ hht,
-                               float* __restrict__ Ft, float* __restrict__ P) {
+                               float* __restrict__ Ft, float* __restrict__ P, float* __restrict__ XT) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
@@ -262,6 +264,7 @@ __global__ void edge_p4_kernel(const float* __restrict__ B, int nb, const float*
       const float q = hht ? hht[j * d + col] : 0.f;
       Ft[e * d + col] = xt[v] * h[j * d + col] + q * Xbar[e * d + col];
       P[e * d + col] = xt[v] * F[v];
+      if (XT) XT[e * d + col] = xt[v];
     }
   }
 }

@@ -166,11 +166,44 @@ __global__ void reverse_kernel(const int* __restrict__ ei, const int* __restrict
 // polynomial envelope and its radial derivative,
 //   B_n(r)  = sqrt(2/rc) sin(n pi r / rc) / r * u(r / rc),
 //   u(x)    = 1 - 28 x^6 + 48 x^7 - 21 x^8   (x < 1).
+// Envelope u(r / rc) and its radial derivative (zero beyond the cutoff).
+__device__ __forceinline__ void envelope_at(double r, double rcd, double& u, double& du) {
+  const double x = r / rcd;
+  u = 0.0;
+  du = 0.0;
+  if (x < 1.0) {
+    const double x2 = x * x, x5 = x2 * x2 * x, x6 = x5 * x;
+    u = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
+    du = (-168.0 * x5 + 336.0 * x6 - 168.0 * x6 * x) / rcd;
+  }
+}
+
+// B_n(r) and dB_n/dr, n = 1..nb, for cutoff rc, into B[0..nb), dB[0..nb).
+__device__ __forceinline__ void bessel_at(double r, double rcd, int nb, float* __restrict__ B,
+                                          float* __restrict__ dB) {
+  double u, du;
+  envelope_at(r, rcd, u, du);
+  const double c = sqrt(2.0 / rcd);
+  const double th = M_PI / rcd;
+  for (int n = 1; n <= nb; ++n) {
+    const double k = n * th;
+    double sn, cs;
+    sincos(k * r, &sn, &cs);
+    const double s = sn / r;
+    const double ds = (k * r * cs - sn) / (r * r);
+    B[n - 1] = (float)(c * s * u);
+    dB[n - 1] = (float)(c * (ds * u + s * du));
+  }
+}
+
+// With rc3 > 0 also the three-body basis B3, dB3 (cutoff rc3) and the
+// envelope u(r / rc3) with its derivative, per edge.
 __global__ void geometry_kernel(const float* __restrict__ pos, const float* __restrict__ cell,
                                 const int* __restrict__ sid, const int* __restrict__ ei,
                                 const int* __restrict__ ej, const int8_t* __restrict__ shift, int Ne,
                                 float rc, int nb, float4* __restrict__ geo, float* __restrict__ B,
-                                float* __restrict__ dB) {
+                                float* __restrict__ dB, float rc3, float* __restrict__ B3, float* __restrict__ dB3,
+                                float* __restrict__ u3, float* __restrict__ du3) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= Ne) return;
   const int i = ei[e], j = ej[e];
@@ -183,24 +216,13 @@ __global__ void geometry_kernel(const float* __restrict__ pos, const float* __re
            (nx * (double)L[k] + ny * (double)L[3 + k] + nz * (double)L[6 + k]);
   const double r = sqrt(d[0] * d[0] + d[1] * d[1] + d[2] * d[2]);
   geo[e] = make_float4((float)(d[0] / r), (float)(d[1] / r), (float)(d[2] / r), (float)r);
-  const double rcd = (double)rc;
-  const double x = r / rcd;
-  double u = 0.0, du = 0.0;
-  if (x < 1.0) {
-    const double x2 = x * x, x5 = x2 * x2 * x, x6 = x5 * x;
-    u = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
-    du = (-168.0 * x5 + 336.0 * x6 - 168.0 * x6 * x) / rcd;
-  }
-  const double c = sqrt(2.0 / rcd);
-  const double th = M_PI / rcd;
-  for (int n = 1; n <= nb; ++n) {
-    const double k = n * th;
-    double sn, cs;
-    sincos(k * r, &sn, &cs);
-    const double s = sn / r;
-    const double ds = (k * r * cs - sn) / (r * r);
-    B[(long long)e * nb + n - 1] = (float)(c * s * u);
-    dB[(long long)e * nb + n - 1] = (float)(c * (ds * u + s * du));
+  bessel_at(r, (double)rc, nb, B + (long long)e * nb, dB + (long long)e * nb);
+  if (rc3 > 0.f) {
+    bessel_at(r, (double)rc3, nb, B3 + (long long)e * nb, dB3 + (long long)e * nb);
+    double u, du;
+    envelope_at(r, (double)rc3, u, du);
+    u3[e] = (float)u;
+    du3[e] = (float)du;
   }
 }
 
@@ -220,10 +242,10 @@ void launch_exclusive_scan(hipStream_t st, const int* in, int n, int* out, int* 
 
 void launch_geometry(hipStream_t st, const float* pos, const float* cell, const int* sid, const int* ei,
                      const int* ej, const int8_t* shift, int Ne, float rc, int nb, float4* geo, float* B,
-                     float* dB) {
+                     float* dB, float rc3, float* B3, float* dB3, float* u3, float* du3) {
   if (Ne <= 0) return;
   hipLaunchKernelGGL(geometry_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, pos, cell, sid, ei, ej, shift, Ne,
-                     rc, nb, geo, B, dB);
+                     rc, nb, geo, B, dB, rc3, B3, dB3, u3, du3);
 }
 
 }  // namespace janus

@@ -11,9 +11,11 @@ void launch_validate_struct(hipStream_t st, const int* offsets, int S, int N, co
 void launch_atom_struct(hipStream_t st, const int* offsets, int S, int N, int* sid);
 // out[0..n] = exclusive prefix sums of in[0..n-1]; bit 16 of flag if the total overflows int32.
 void launch_exclusive_scan(hipStream_t st, const int* in, int n, int* out, int* flag);
-// geo[e] = (u_x, u_y, u_z, r); B, dB [Ne, nb].
+// geo[e] = (u_x, u_y, u_z, r); B, dB [Ne, nb].  With rc3 > 0 also the
+// three-body basis B3, dB3 [Ne, nb] and envelope u3, du3 [Ne] at cutoff rc3.
 void launch_geometry(hipStream_t st, const float* pos, const float* cell, const int* sid, const int* ei,
                      const int* ej, const int8_t* shift, int Ne, float rc, int nb, float4* geo, float* B,
-                     float* dB);
+                     float* dB, float rc3 = 0.f, float* B3 = nullptr, float* dB3 = nullptr, float* u3 = nullptr,
+                     float* du3 = nullptr);
 
 }  // namespace janus

@@ -29,6 +29,11 @@ struct RouteArgs {
 
 __global__ void zero_ints_kernel(int* p, int n);
 void route_block(hipStream_t st, const RouteArgs& a);
+// Stable counting sort of M tokens (flattened (token, choice) entries with
+// expert ids eid) into expert-grouped slots: total[E], off[E+1], pos[M],
+// slot_gate[M]; cnt and colpre are scratch of sort_chunks(M) * E ints.
+void sort_tokens(hipStream_t st, const int* eid, const float* gate, long long M, int E, int* cnt, int* colpre,
+                 int* total, int* off, int* pos, float* slot_gate);
 int sort_chunks(long long M);
 
 }  // namespace janus

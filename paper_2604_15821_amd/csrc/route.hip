@@ -158,18 +158,22 @@ void route_block(hipStream_t st, const RouteArgs& a) {
   if (a.Ne > 0)
     hipLaunchKernelGGL(route_edges_kernel, dim3(cdiv(a.Ne, 256)), dim3(256), 0, st, a.species, a.ei, a.ej, a.Ne,
                        a.nsp, a.k, a.peid, a.pgate, a.pair, a.eid, a.gate);
-  const long long M = (long long)a.Ne * a.k;
+  sort_tokens(st, a.eid, a.gate, (long long)a.Ne * a.k, a.E, a.cnt, a.colpre, a.total, a.off, a.pos, a.slot_gate);
+}
+
+void sort_tokens(hipStream_t st, const int* eid, const float* gate, long long M, int E, int* cnt, int* colpre,
+                 int* total, int* off, int* pos, float* slot_gate) {
   const int nch = (int)((M + kSortChunk - 1) / kSortChunk);
   if (nch > 0) {
-    hipLaunchKernelGGL(sort_count_kernel, dim3(nch), dim3(256), 0, st, a.eid, M, a.E, a.cnt);
-    hipLaunchKernelGGL(sort_colscan_kernel, dim3(a.E), dim3(256), 0, st, a.cnt, nch, a.E, a.colpre, a.total);
+    hipLaunchKernelGGL(sort_count_kernel, dim3(nch), dim3(256), 0, st, eid, M, E, cnt);
+    hipLaunchKernelGGL(sort_colscan_kernel, dim3(E), dim3(256), 0, st, cnt, nch, E, colpre, total);
   } else {
-    hipLaunchKernelGGL(zero_ints_kernel, dim3(1), dim3(64), 0, st, a.total, a.E);
+    hipLaunchKernelGGL(zero_ints_kernel, dim3(1), dim3(64), 0, st, total, E);
   }
-  hipLaunchKernelGGL(sort_offsets_kernel, dim3(1), dim3(1), 0, st, a.total, a.E, a.off);
+  hipLaunchKernelGGL(sort_offsets_kernel, dim3(1), dim3(1), 0, st, total, E, off);
   if (nch > 0)
-    hipLaunchKernelGGL(sort_scatter_kernel, dim3(nch), dim3(64), 0, st, a.eid, a.gate, M, a.E, a.off, a.colpre,
-                       a.pos, a.slot_gate);
+    hipLaunchKernelGGL(sort_scatter_kernel, dim3(nch), dim3(64), 0, st, eid, gate, M, E, off, colpre, pos,
+                       slot_gate);
 }
 
 int sort_chunks(long long M) { return (int)((M + kSortChunk - 1) / kSortChunk); }

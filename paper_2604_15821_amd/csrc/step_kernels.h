@@ -15,6 +15,7 @@
 #include "internal.h"
 #include "kernels.h"
 #include "route.h"
+#include "tri.h"
 
 namespace janus {
 
@@ -87,18 +88,26 @@ __global__ void energy_kernel(const float* __restrict__ eps, const int* __restri
 }
 
 // F_a = sum_{e in seg(a)} (G_e - G_rev(e)),  G_e = rbar_e u_e = dE/dd_e.
+// With the three-body term, G_e gains the triplet displacement adjoint gvec[e].
 __global__ void force_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev,
-                             const float* __restrict__ rbar, const float4* __restrict__ geo, int N,
-                             float* __restrict__ F) {
+                             const float* __restrict__ rbar, const float4* __restrict__ geo,
+                             const float4* __restrict__ gvec, int N, float* __restrict__ F) {
   const int a = blockIdx.x * blockDim.x + threadIdx.x;
   if (a >= N) return;
   double fx = 0, fy = 0, fz = 0;
   for (int e = rowptr[a]; e < rowptr[a + 1]; ++e) {
-    const float4 u = geo[e], ur = geo[rev[e]];
-    const double g = rbar[e], gr = rbar[rev[e]];
+    const int er = rev[e];
+    const float4 u = geo[e], ur = geo[er];
+    const double g = rbar[e], gr = rbar[er];
     fx += g * u.x - gr * ur.x;
     fy += g * u.y - gr * ur.y;
     fz += g * u.z - gr * ur.z;
+    if (gvec) {
+      const float4 v = gvec[e], vr = gvec[er];
+      fx += (double)v.x - vr.x;
+      fy += (double)v.y - vr.y;
+      fz += (double)v.z - vr.z;
+    }
   }
   F[3 * a] = (float)fx;
   F[3 * a + 1] = (float)fy;
@@ -380,6 +389,16 @@ Layout make_layout(const janus_config& c) {
     L.add(p + "beta", {E});
     L.add(p + "W1", {E, d, h});
     L.add(p + "W2", {E, h, d});
+    if (c.three_body) {
+      const long long E3 = c.n_experts3, h3 = c.d_hidden3, nf = (long long)c.n_legendre * nb;
+      L.add(p + "W_a", {nf, d});
+      L.add(p + "P3a", {S, E3});
+      L.add(p + "P3b", {S, E3});
+      L.add(p + "P3c", {S, E3});
+      L.add(p + "beta3", {E3});
+      L.add(p + "W1a", {E3, d, h3});
+      L.add(p + "W2a", {E3, h3, d});
+    }
   }
   L.add("W_o1", {d, d});
   L.add("w_o2", {d});
@@ -393,8 +412,16 @@ int check_config(const janus_config* c) {
       c->top_k > c->n_experts || c->d_hidden < 64 || !(c->r_cut > 0.f))
     return JANUS_EINVAL;
   if (c->d % 64 || (c->d / 64 != 1 && c->d / 64 != 2 && c->d / 64 != 4 && c->d / 64 != 8) || c->d_hidden % 64 ||
-      c->n_rbf % 4 || c->env_p != 6 || c->three_body)
+      c->n_rbf % 4 || c->env_p != 6)
     return JANUS_EUNSUPPORTED;
+  if (c->three_body) {
+    if (c->n_experts3 < 1 || c->n_experts3 > 64 || c->top_k3 < 1 || c->top_k3 > 4 || c->top_k3 > c->n_experts3 ||
+        c->d_hidden3 < 64 || c->n_legendre < 1 || !(c->r_cut3 > 0.f) || c->r_cut3 > c->r_cut)
+      return JANUS_EINVAL;
+    // the feature-to-width matrix W_a is staged in LDS (at most 64 KB)
+    if (c->d_hidden3 % 64 || c->n_legendre > 8 || (size_t)c->n_legendre * c->n_rbf * c->d * 4 > 65536)
+      return JANUS_EUNSUPPORTED;
+  }
   return JANUS_OK;
 }
 
@@ -429,13 +456,32 @@ struct Plan {
   float *T1, *T2, *Pe, *Ft, *gpart, *gt, *partC, *partN, *partial;
   // chunk-local neighbour list (indices relative to the chunk)
   int *cei, *cej, *crev, *crow, *coff;
+  // three-body term: triplets (CSR by first edge), per-edge basis at r3,
+  // per-block triplet routing, activations and adjoints
+  int *tcount, *trow, *te, *te2, *trev;
+  float *tc, *B3, *dB3, *u3, *du3;
+  float4 *tacc, *tct, *gvec;
+  int *eid3, *pos3, *total3, *off3, *cnt3, *colpre3;
+  float *gate3, *slot_gate3, *g3t;
+  RowsTile* tiles3;
+  int* ntiles3;
+  WChunk* chunks3;
+  int *nchunks3, *cfirst3;
+  int *rowT;
+  WChunk* chunksT;
+  int *ncT, *cfT;
+  float *Z3s, *A3, *S3b, *A3b, *Y3bs, *Zbar3;
+  float *Q, *PT, *VT, *T3a, *T3b, *gpart3, *gt3, *LB, *LC, *pa, *pb, *pc;
   // sizes
   int T, E, k, d, hdim, nb, nsp, N, S;
   long long Ne, M;
   int mt, mc, kc, mtN, kcN, mcN, kcE, mcE, nch, ntile;
+  int three, E3, k3, hd3, L3, nf;
+  long long Nt, M3;
+  int mt3, mc3, kc3, kcT, mcT, nch3, ntile3;
 };
 
-size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, long long Ne) {
+size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, long long Ne, long long Nt = 0) {
   Carver cv(base);
   p.T = c.n_blocks;
   p.E = c.n_experts;
@@ -535,12 +581,87 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   long long part = (long long)p.mc * d * h;
   part = std::max(part, (long long)p.mcN * d * d);
   part = std::max(part, (long long)p.mcE * p.nb * d);
+  if (c.three_body) {   // triplet expert and W_a gradients (same chunking as below)
+    const long long M3 = Nt * c.top_k3;
+    const int nf = c.n_legendre * c.n_rbf;
+    part = std::max(part, (long long)max_wchunks(M3, c.n_experts3, wgrad_chunk_rows(M3, d, c.d_hidden3)) * d *
+                              c.d_hidden3);
+    part = std::max(part, (long long)max_wchunks(Nt, 1, wgrad_chunk_rows(Nt, nf, d)) * nf * d);
+  }
   p.partial = cv.take<float>(part);
   p.cei = cv.take<int>(Ne + 1);
   p.cej = cv.take<int>(Ne + 1);
   p.crev = cv.take<int>(Ne + 1);
   p.crow = cv.take<int>(N + 1);
   p.coff = cv.take<int>(S + 1);
+
+  p.three = c.three_body ? 1 : 0;
+  p.Nt = p.three ? Nt : 0;
+  p.E3 = c.n_experts3;
+  p.k3 = c.top_k3;
+  p.hd3 = c.d_hidden3;
+  p.L3 = c.n_legendre;
+  p.nf = c.n_legendre * c.n_rbf;
+  p.M3 = p.Nt * c.top_k3;
+  if (p.three) {
+    const long long M3 = p.M3, Ntt = p.Nt, h3 = p.hd3, E3 = p.E3;
+    p.mt3 = max_rows_tiles(M3, p.E3);
+    p.kc3 = wgrad_chunk_rows(M3, d, p.hd3);
+    p.mc3 = max_wchunks(M3, p.E3, p.kc3);
+    p.kcT = wgrad_chunk_rows(Ntt, p.nf, d);
+    p.mcT = max_wchunks(Ntt, 1, p.kcT);
+    p.nch3 = sort_chunks(M3);
+    p.ntile3 = (p.hd3 + GBN - 1) / GBN;
+    p.tcount = cv.take<int>(Ne + 1);
+    p.trow = cv.take<int>(Ne + 1);
+    p.te = cv.take<int>(Ntt + 1);
+    p.te2 = cv.take<int>(Ntt + 1);
+    p.trev = cv.take<int>(Ntt + 1);
+    p.tc = cv.take<float>(Ntt + 1);
+    p.B3 = cv.take<float>(Ne * p.nb + 4);
+    p.dB3 = cv.take<float>(Ne * p.nb + 4);
+    p.u3 = cv.take<float>(Ne + 1);
+    p.du3 = cv.take<float>(Ne + 1);
+    p.tacc = cv.take<float4>(Ntt + 1);
+    p.tct = cv.take<float4>(Ntt + 1);
+    p.gvec = cv.take<float4>(Ne + 1);
+    p.eid3 = cv.take<int>(T * M3 + 1);
+    p.gate3 = cv.take<float>(T * M3 + 1);
+    p.pos3 = cv.take<int>(T * M3 + 1);
+    p.slot_gate3 = cv.take<float>(T * M3 + 1);
+    p.g3t = cv.take<float>(T * M3 + 1);
+    p.total3 = cv.take<int>(T * E3);
+    p.off3 = cv.take<int>(T * (E3 + 1));
+    p.cnt3 = cv.take<int>((long long)p.nch3 * E3 + 1);
+    p.colpre3 = cv.take<int>((long long)p.nch3 * E3 + 1);
+    p.tiles3 = cv.take<RowsTile>((long long)T * p.mt3);
+    p.ntiles3 = cv.take<int>(T + 1);
+    p.chunks3 = cv.take<WChunk>((long long)T * p.mc3);
+    p.nchunks3 = cv.take<int>(T + 1);
+    p.cfirst3 = cv.take<int>(T * (E3 + 1) + 1);
+    p.rowT = cv.take<int>(2);
+    p.chunksT = cv.take<WChunk>(p.mcT);
+    p.ncT = cv.take<int>(1);
+    p.cfT = cv.take<int>(2);
+    p.Z3s = cv.take<float>(T * M3 * d + 4);
+    p.A3 = cv.take<float>(T * M3 * h3 + 4);
+    p.S3b = cv.take<float>(T * M3 * h3 + 4);
+    p.A3b = cv.take<float>(T * M3 * h3 + 4);
+    p.Y3bs = cv.take<float>(T * M3 * d + 4);
+    p.Zbar3 = cv.take<float>(T * Ntt * d + 4);
+    p.Q = cv.take<float>(Ne * d + 4);
+    p.PT = cv.take<float>(Ntt * d + 4);
+    p.VT = cv.take<float>(Ntt * d + 4);
+    p.T3a = cv.take<float>(M3 * d + 4);
+    p.T3b = cv.take<float>(M3 * d + 4);
+    p.gpart3 = cv.take<float>(M3 * p.ntile3 + 4);
+    p.gt3 = cv.take<float>(M3 + 1);
+    p.LB = cv.take<float>(Ne * E3 + 1);
+    p.LC = cv.take<float>(Ne * E3 + 1);
+    p.pa = cv.take<float>((long long)N * E3 + 1);
+    p.pb = cv.take<float>((long long)N * E3 + 1);
+    p.pc = cv.take<float>((long long)N * E3 + 1);
+  }
   return cv.size();
 }
 

@@ -1,0 +1,640 @@
+// Bond-triplet (three-body) kernels of the training step.
+//
+// Paper Sec. "MatRIS": pairs of bonds sharing an atom define bond angles that
+// become angle features; each interaction block has a three-body operation.
+// Reading (the one the whole build follows): a triplet tau = (e, e2) is an
+// ordered pair of distinct edges out of one centre, both shorter than r3
+// under the pinned fp32 test; its features are
+//   G[l, n] = P_l(c) B3_n(r_e2) u3(r_e),   c = u_e . u_e2,
+// its token Z = (G W_a) * h_{j(e2)} goes through a routed expert MLP, and the
+// messages of the triplets of e are added to the edge token X_e.
+//
+// Triplets are stored in CSR order by their first edge e (tseg(e)); trev[tau]
+// is the triplet (e2, e).  Sums over "triplets whose second edge is e2" walk
+// tseg(e2) through trev, and sums over "triplets whose second edge points to
+// atom a" then walk seg(a) through the edge reverse map, so no kernel needs
+// atomics.
+//
+// Inside the kernels the product of the features with W_a never materialises
+// G: with s_l[col] = sum_n B3_n W_a[l Nb + n, col] (and s'_l with B3'),
+//   (G W_a)       = u3 sum_l P_l  s_l
+//   (dG/dc W_a)   = u3 sum_l P'_l s_l
+//   (dG/dr2 W_a)  = u3 sum_l P_l  s'_l
+//   (dG/dr1 W_a)  = u3' sum_l P_l s_l .
+#pragma once
+
+#include "edge.h"
+#include "gemm.h"
+
+namespace janus {
+
+constexpr int kMaxL = 8;
+
+__device__ __forceinline__ void legendre_d(float c, int L, float* P, float* dP) {
+  P[0] = 1.f;
+  dP[0] = 0.f;
+  if (L > 1) {
+    P[1] = c;
+    dP[1] = 1.f;
+  }
+  for (int l = 1; l + 1 < L; ++l) {
+    P[l + 1] = ((2 * l + 1) * c * P[l] - l * P[l - 1]) / (l + 1);
+    dP[l + 1] = (l + 1) * P[l] + c * dP[l];
+  }
+}
+
+// ---------------------------------------------------------------- builder
+
+// short[e] = 1 iff the pinned fp32 test holds with r3 (same expression as the
+// neighbour list).
+__global__ void tri_short_kernel(const float* __restrict__ pos, const float* __restrict__ cell,
+                                 const int* __restrict__ sid, const int* __restrict__ ei, const int* __restrict__ ej,
+                                 const int8_t* __restrict__ shift, long long Ne, float rc3,
+                                 unsigned char* __restrict__ sh) {
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  const int i = ei[e], j = ej[e];
+  const float* L = cell + 9 * sid[i];
+  const float fx = shift[3 * e], fy = shift[3 * e + 1], fz = shift[3 * e + 2];
+  const float sx = __fadd_rn(__fadd_rn(__fmul_rn(fx, L[0]), __fmul_rn(fy, L[3])), __fmul_rn(fz, L[6]));
+  const float sy = __fadd_rn(__fadd_rn(__fmul_rn(fx, L[1]), __fmul_rn(fy, L[4])), __fmul_rn(fz, L[7]));
+  const float sz = __fadd_rn(__fadd_rn(__fmul_rn(fx, L[2]), __fmul_rn(fy, L[5])), __fmul_rn(fz, L[8]));
+  const float dx = __fadd_rn(__fsub_rn(pos[3 * j], pos[3 * i]), sx);
+  const float dy = __fadd_rn(__fsub_rn(pos[3 * j + 1], pos[3 * i + 1]), sy);
+  const float dz = __fadd_rn(__fsub_rn(pos[3 * j + 2], pos[3 * i + 2]), sz);
+  const float r2 = __fadd_rn(__fadd_rn(__fmul_rn(dx, dx), __fmul_rn(dy, dy)), __fmul_rn(dz, dz));
+  sh[e] = r2 < __fmul_rn(rc3, rc3) ? 1 : 0;
+}
+
+// Triplets of each edge: n_short(i) - 1 when e is short, else 0.
+__global__ void tri_count_kernel(const int* __restrict__ rowptr, const unsigned char* __restrict__ sh, int N,
+                                 int* __restrict__ tcount) {
+  const int a = blockIdx.x * blockDim.x + threadIdx.x;
+  if (a >= N) return;
+  int ns = 0;
+  for (int e = rowptr[a]; e < rowptr[a + 1]; ++e) ns += sh[e];
+  for (int e = rowptr[a]; e < rowptr[a + 1]; ++e) tcount[e] = sh[e] ? ns - 1 : 0;
+}
+
+// Triplets per structure: sum over its atoms of ns (ns - 1).
+__global__ void tri_struct_count_kernel(const int* __restrict__ offsets, const int* __restrict__ rowptr,
+                                        const unsigned char* __restrict__ sh, int S, long long* __restrict__ out) {
+  JANUS_WAVE_LOOP(s, S) {
+    long long acc = 0;
+    for (int a = offsets[s] + l; a < offsets[s + 1]; a += 64) {
+      int ns = 0;
+      for (int e = rowptr[a]; e < rowptr[a + 1]; ++e) ns += sh[e];
+      acc += (long long)ns * (ns - 1);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+    if (l == 0) out[s] = acc;
+  }
+}
+
+__global__ void tri_write_kernel(const int* __restrict__ ei, const int* __restrict__ rowptr,
+                                 const unsigned char* __restrict__ sh, const int* __restrict__ trowptr, long long Ne,
+                                 int* __restrict__ te, int* __restrict__ te2) {
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne || !sh[e]) return;
+  const int i = ei[e];
+  int p = trowptr[e];
+  for (int f = rowptr[i]; f < rowptr[i + 1]; ++f)
+    if (sh[f] && f != e) {
+      te[p] = (int)e;
+      te2[p] = f;
+      ++p;
+    }
+}
+
+// trev[tau] = index of (e2, e) in tseg(e2) (binary search on te2, which is
+// increasing inside a segment); c[tau] = u_e . u_e2.
+__global__ void tri_rev_kernel(const int* __restrict__ te, const int* __restrict__ te2,
+                               const int* __restrict__ trowptr, const float4* __restrict__ geo, long long Nt,
+                               int* __restrict__ trev, float* __restrict__ tc) {
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Nt) return;
+  const int e = te[t], e2 = te2[t];
+  int lo = trowptr[e2], hi = trowptr[e2 + 1];
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (te2[mid] < e) lo = mid + 1; else hi = mid;
+  }
+  trev[t] = (lo < trowptr[e2 + 1] && te2[lo] == e) ? lo : (int)t;
+  const float4 a = geo[e], b = geo[e2];
+  tc[t] = a.x * b.x + a.y * b.y + a.z * b.z;
+}
+
+// ---------------------------------------------------------------- routing
+
+// Per triplet: logits ((P3a[Z_i] + P3b[Z_j(e)]) + P3c[Z_j(e2)]) + beta3 in
+// fp32 for the top-k decision (lower index first on ties), gates from the
+// float64 softmax.
+__global__ void tri_route_kernel(const int* __restrict__ species, const int* __restrict__ ei,
+                                 const int* __restrict__ ej, const int* __restrict__ te, const int* __restrict__ te2,
+                                 long long Nt, const float* __restrict__ Pa, const float* __restrict__ Pb,
+                                 const float* __restrict__ Pc, const float* __restrict__ beta, int E, int k,
+                                 int* __restrict__ eid, float* __restrict__ gate) {
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Nt) return;
+  const int za = species[ei[te[t]]], zb = species[ej[te[t]]], zc = species[ej[te2[t]]];
+  float l[64];
+  double mx = -1e300;
+  for (int x = 0; x < E; ++x) {
+    const float a = Pa[za * E + x], b = Pb[zb * E + x], c = Pc[zc * E + x], bt = beta[x];
+    l[x] = __fadd_rn(__fadd_rn(__fadd_rn(a, b), c), bt);
+    const double ld = (((double)a + (double)b) + (double)c) + (double)bt;
+    mx = ld > mx ? ld : mx;
+  }
+  double den = 0.0;
+  for (int x = 0; x < E; ++x)
+    den += exp(((((double)Pa[za * E + x] + (double)Pb[zb * E + x]) + (double)Pc[zc * E + x]) + (double)beta[x]) - mx);
+  unsigned long long taken = 0;
+  for (int c = 0; c < k; ++c) {
+    int best = -1;
+    for (int x = 0; x < E; ++x) {
+      if (taken >> x & 1ull) continue;
+      if (best < 0 || l[x] > l[best]) best = x;
+    }
+    taken |= 1ull << best;
+    eid[t * k + c] = best;
+    gate[t * k + c] = (float)(exp(((((double)Pa[za * E + best] + (double)Pb[zb * E + best]) +
+                                    (double)Pc[zc * E + best]) + (double)beta[best]) - mx) / den);
+  }
+}
+
+// ---------------------------------------------------------------- feature rows
+
+// Per lane (columns v*64 + l): the four products of the features with W_a
+// (shared memory sWa [L*Nb, d]) for one triplet.
+template <int VPL>
+struct TriRows {
+  float z[VPL];    // G W_a
+  float wc[VPL];   // dG/dc W_a
+  float w1[VPL];   // dG/dr1 W_a
+  float w2[VPL];   // dG/dr2 W_a
+};
+
+template <int VPL, bool DERIV>
+__device__ __forceinline__ void tri_rows(long long t, const int* __restrict__ te, const int* __restrict__ te2,
+                                         const float* __restrict__ tc, const float* __restrict__ B3,
+                                         const float* __restrict__ dB3, const float* __restrict__ u3,
+                                         const float* __restrict__ du3, const float* sWa, int nb, int L, int d, int l,
+                                         TriRows<VPL>& o) {
+  const int e1 = te[t], e2 = te2[t];
+  float P[kMaxL], dP[kMaxL];
+  legendre_d(tc[t], L, P, dP);
+  const float* b3 = B3 + (long long)e2 * nb;
+  const float* db3 = dB3 + (long long)e2 * nb;
+  float s[VPL], sp[VPL];
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) o.z[v] = o.wc[v] = o.w1[v] = o.w2[v] = 0.f;
+  for (int q = 0; q < L; ++q) {
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) s[v] = sp[v] = 0.f;
+    for (int n = 0; n < nb; ++n) {
+      const float bn = b3[n], dbn = DERIV ? db3[n] : 0.f;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) {
+        const float w = sWa[(q * nb + n) * d + v * 64 + l];
+        s[v] += bn * w;
+        if (DERIV) sp[v] += dbn * w;
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      o.z[v] += P[q] * s[v];
+      if (DERIV) {
+        o.wc[v] += dP[q] * s[v];
+        o.w2[v] += P[q] * sp[v];
+      }
+    }
+  }
+  const float u = u3[e1], du = du3[e1];
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) {
+    if (DERIV) {
+      o.w1[v] = du * o.z[v];
+      o.wc[v] *= u;
+      o.w2[v] *= u;
+    }
+    o.z[v] *= u;
+  }
+}
+
+// ---------------------------------------------------------------- phase 1
+
+// Z = (G W_a) * h_{j(e2)} into the triplet expert slots.
+template <int VPL>
+__global__ void tri_dispatch_kernel(const int* __restrict__ te, const int* __restrict__ te2,
+                                    const float* __restrict__ tc, const float* __restrict__ B3,
+                                    const float* __restrict__ dB3, const float* __restrict__ u3,
+                                    const float* __restrict__ du3, const float* __restrict__ Wa, int nb, int L,
+                                    const int* __restrict__ ej, const float* __restrict__ h,
+                                    const int* __restrict__ pos3, int k3, long long Nt, int d,
+                                    float* __restrict__ Zs) {
+  extern __shared__ float sWa[];
+  load_lds(sWa, Wa, L * nb * d);
+  JANUS_WAVE_LOOP(t, Nt) {
+    TriRows<VPL> o;
+    tri_rows<VPL, false>(t, te, te2, tc, B3, dB3, u3, du3, sWa, nb, L, d, l, o);
+    const float* hj = h + (long long)ej[te2[t]] * d;
+    float Z[VPL];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) Z[v] = o.z[v] * hj[v * 64 + l];
+    for (int c = 0; c < k3; ++c) {
+      float* out = Zs + (long long)pos3[t * k3 + c] * d;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) out[v * 64 + l] = Z[v];
+    }
+  }
+}
+
+// Q_e = sum_{tau in tseg(e)} sum_c Y3g[pos3[tau, c]]  (gated triplet messages).
+template <int VPL>
+__global__ void tri_combine_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3, int k3,
+                                   const float* __restrict__ Yg, long long Ne, int d, float* __restrict__ Q) {
+  JANUS_WAVE_LOOP(e, Ne) {
+    float acc[VPL];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) acc[v] = 0.f;
+    for (int t = trowptr[e]; t < trowptr[e + 1]; ++t)
+      for (int c = 0; c < k3; ++c) {
+        const float* y = Yg + (long long)pos3[(long long)t * k3 + c] * d;
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) acc[v] += y[v * 64 + l];
+      }
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) Q[e * d + v * 64 + l] = acc[v];
+  }
+}
+
+// Slot rows of an edge adjoint for the triplets of the edge:
+// out[pos3[tau, c]] = (g3_tau,c) * src[e],  tau in tseg(e).
+template <int VPL>
+__global__ void tri_gather_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3, int k3,
+                                  const float* __restrict__ gate3, const float* __restrict__ src, long long Ne, int d,
+                                  float* __restrict__ out) {
+  JANUS_WAVE_LOOP(e, Ne) {
+    const int t0 = trowptr[e], t1 = trowptr[e + 1];
+    if (t0 == t1) continue;
+    float s[VPL];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) s[v] = src[e * d + v * 64 + l];
+    for (int t = t0; t < t1; ++t)
+      for (int c = 0; c < k3; ++c) {
+        const long long f = (long long)t * k3 + c;
+        const float g = gate3 ? gate3[f] : 1.f;
+        float* o = out + (long long)pos3[f] * d;
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) o[v * 64 + l] = g * s[v];
+      }
+  }
+}
+
+// ---------------------------------------------------------------- phase 2
+
+// Per triplet: Zbar = sum_c Zbar_slot; keep it; PT = Zbar * (G W_a) (routed to
+// h_{j(e2)}); accumulate the feature-geometry adjoints
+//   acc += (Zbar * h_j2) . (dG/dc W_a, dG/dr1 W_a, dG/dr2 W_a).
+template <int VPL>
+__global__ void tri_p2_kernel(const int* __restrict__ te, const int* __restrict__ te2, const float* __restrict__ tc,
+                              const float* __restrict__ B3, const float* __restrict__ dB3,
+                              const float* __restrict__ u3, const float* __restrict__ du3,
+                              const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
+                              const float* __restrict__ h, const int* __restrict__ pos3, int k3, long long Nt, int d,
+                              const float* __restrict__ Zbs, float* __restrict__ Zbar, float* __restrict__ PT,
+                              float4* __restrict__ acc) {
+  extern __shared__ float sWa[];
+  load_lds(sWa, Wa, L * nb * d);
+  JANUS_WAVE_LOOP(t, Nt) {
+    float zb[VPL];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) zb[v] = 0.f;
+    for (int c = 0; c < k3; ++c) {
+      const float* y = Zbs + (long long)pos3[t * k3 + c] * d;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) zb[v] += y[v * 64 + l];
+    }
+    TriRows<VPL> o;
+    tri_rows<VPL, true>(t, te, te2, tc, B3, dB3, u3, du3, sWa, nb, L, d, l, o);
+    const float* hj = h + (long long)ej[te2[t]] * d;
+    float ac = 0.f, a1 = 0.f, a2 = 0.f;
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      const long long q = t * d + v * 64 + l;
+      Zbar[q] = zb[v];
+      PT[q] = zb[v] * o.z[v];
+      const float w = zb[v] * hj[v * 64 + l];
+      ac += w * o.wc[v];
+      a1 += w * o.w1[v];
+      a2 += w * o.w2[v];
+    }
+    ac = wave_sum(ac);
+    a1 = wave_sum(a1);
+    a2 = wave_sum(a2);
+    if (l == 0) {
+      float4 s = acc[t];
+      s.x += ac;
+      s.y += a1;
+      s.z += a2;
+      acc[t] = s;
+    }
+  }
+}
+
+// P[e] += sum over the triplets whose second edge is e of PT:
+// sum_{tau' in tseg(e)} PT[trev[tau']].
+template <int VPL>
+__global__ void tri_second_sum_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
+                                      const float* __restrict__ PT, long long Ne, int d, float* __restrict__ P) {
+  JANUS_WAVE_LOOP(e, Ne) {
+    const int t0 = trowptr[e], t1 = trowptr[e + 1];
+    if (t0 == t1) continue;
+    float acc[VPL];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) acc[v] = P[e * d + v * 64 + l];
+    for (int t = t0; t < t1; ++t) {
+      const float* p = PT + (long long)trev[t] * d;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) acc[v] += p[v * 64 + l];
+    }
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) P[e * d + v * 64 + l] = acc[v];
+  }
+}
+
+// Displacement adjoint of every edge from the triplet geometry adjoints
+// (ac, a1, a2) of the triplets it belongs to:
+//   first edge:  ac (u2 - c u1) / r1 + a1 u1;   second edge: ac (u1 - c u2) / r2 + a2 u2.
+__global__ void tri_edge_vec_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
+                                    const int* __restrict__ te2, const float* __restrict__ tc,
+                                    const float4* __restrict__ geo, const float4* __restrict__ acc, long long Ne,
+                                    float4* __restrict__ gvec) {
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  const float4 ue = geo[e];
+  double gx = 0, gy = 0, gz = 0;
+  for (int t = trowptr[e]; t < trowptr[e + 1]; ++t) {
+    // tau = (e, e2): e is the first edge
+    const float4 u2 = geo[te2[t]];
+    const float c = tc[t];
+    const float4 a = acc[t];
+    const double f = a.x / ue.w;
+    gx += f * (u2.x - c * ue.x) + a.y * ue.x;
+    gy += f * (u2.y - c * ue.y) + a.y * ue.y;
+    gz += f * (u2.z - c * ue.z) + a.y * ue.z;
+    // tau' = (e2, e): e is the second edge
+    const int tr = trev[t];
+    const float cr = tc[tr];
+    const float4 ar = acc[tr];
+    const double fr = ar.x / ue.w;
+    gx += fr * (u2.x - cr * ue.x) + ar.z * ue.x;
+    gy += fr * (u2.y - cr * ue.y) + ar.z * ue.y;
+    gz += fr * (u2.z - cr * ue.z) + ar.z * ue.z;
+  }
+  gvec[e] = make_float4((float)gx, (float)gy, (float)gz, 0.f);
+}
+
+// ---------------------------------------------------------------- phase 3
+
+// Per triplet, once per step: the loss adjoints of the feature-geometry
+// adjoints, ct = (ac~, a1~, a2~), from Gt_e = phi_i(e) - phi_j(e):
+//   ac~ = Gt_e . (u2 - c u1) / r1 + Gt_e2 . (u1 - c u2) / r2,  a1~ = rt_e,  a2~ = rt_e2.
+__global__ void tri_ctilde_kernel(const int* __restrict__ te, const int* __restrict__ te2,
+                                  const float* __restrict__ tc, const float4* __restrict__ geo,
+                                  const int* __restrict__ ei, const int* __restrict__ ej,
+                                  const float* __restrict__ phi, const float* __restrict__ rt, long long Nt,
+                                  float4* __restrict__ ct) {
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Nt) return;
+  const int e = te[t], e2 = te2[t];
+  const float4 u1 = geo[e], u2 = geo[e2];
+  const float c = tc[t];
+  const int i = ei[e], j1 = ej[e], j2 = ej[e2];
+  const float g1x = phi[3 * i] - phi[3 * j1], g1y = phi[3 * i + 1] - phi[3 * j1 + 1],
+              g1z = phi[3 * i + 2] - phi[3 * j1 + 2];
+  const float g2x = phi[3 * i] - phi[3 * j2], g2y = phi[3 * i + 1] - phi[3 * j2 + 1],
+              g2z = phi[3 * i + 2] - phi[3 * j2 + 2];
+  const float acx = (g1x * (u2.x - c * u1.x) + g1y * (u2.y - c * u1.y) + g1z * (u2.z - c * u1.z)) / u1.w +
+                    (g2x * (u1.x - c * u2.x) + g2y * (u1.y - c * u2.y) + g2z * (u1.z - c * u2.z)) / u2.w;
+  ct[t] = make_float4(acx, rt[e], rt[e2], 0.f);
+}
+
+// Double backward per triplet (Q = loss adjoint of hbar^t at j(e2), may be null):
+//   vt   = ct . (dG W_a)            (adjoint of Zbar * h_j2)
+//   Zbt  = vt * h_j2 + Q * (G W_a)  -> slots of the triplet
+//   V    = Zbar * h_j2              (dW_a += Gt^T V)
+//   PT   = vt * Zbar                (routed to h_{j(e2)})
+template <int VPL>
+__global__ void tri_p3_kernel(const int* __restrict__ te, const int* __restrict__ te2, const float* __restrict__ tc,
+                              const float* __restrict__ B3, const float* __restrict__ dB3,
+                              const float* __restrict__ u3, const float* __restrict__ du3,
+                              const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
+                              const float* __restrict__ h, const float* __restrict__ hht,
+                              const float4* __restrict__ ct, const float* __restrict__ Zbar,
+                              const int* __restrict__ pos3, int k3, long long Nt, int d, float* __restrict__ Zbts,
+                              float* __restrict__ V, float* __restrict__ PT) {
+  extern __shared__ float sWa[];
+  load_lds(sWa, Wa, L * nb * d);
+  JANUS_WAVE_LOOP(t, Nt) {
+    TriRows<VPL> o;
+    tri_rows<VPL, true>(t, te, te2, tc, B3, dB3, u3, du3, sWa, nb, L, d, l, o);
+    const long long j2 = ej[te2[t]];
+    const float4 cf = ct[t];
+    float Zb[VPL];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      const int col = v * 64 + l;
+      const float zb = Zbar[t * d + col], hj = h[j2 * d + col];
+      const float q = hht ? hht[j2 * d + col] : 0.f;
+      const float vt = cf.x * o.wc[v] + cf.y * o.w1[v] + cf.z * o.w2[v];
+      Zb[v] = vt * hj + q * o.z[v];
+      V[t * d + col] = zb * hj;
+      PT[t * d + col] = vt * zb;
+    }
+    for (int c = 0; c < k3; ++c) {
+      float* out = Zbts + (long long)pos3[t * k3 + c] * d;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) out[v * 64 + l] = Zb[v];
+    }
+  }
+}
+
+// Per edge, double backward of the triplet gather: gate adjoints
+// g3t[tau, c] = Ybt3[pos3] . Xbar_e and QX_e = sum_tau sum_c g3 Ybt3[pos3].
+template <int VPL>
+__global__ void tri_combine_p3_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3, int k3,
+                                      const float* __restrict__ gate3, const float* __restrict__ Ybt3,
+                                      const float* __restrict__ Xbar, long long Ne, int d, float* __restrict__ g3t,
+                                      float* __restrict__ QX) {
+  JANUS_WAVE_LOOP(e, Ne) {
+    float xb[VPL], acc[VPL];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      xb[v] = Xbar[e * d + v * 64 + l];
+      acc[v] = 0.f;
+    }
+    for (int t = trowptr[e]; t < trowptr[e + 1]; ++t)
+      for (int c = 0; c < k3; ++c) {
+        const long long f = (long long)t * k3 + c;
+        const float* y = Ybt3 + (long long)pos3[f] * d;
+        const float g = gate3[f];
+        float s = 0.f;
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          const float yv = y[v * 64 + l];
+          s += yv * xb[v];
+          acc[v] += g * yv;
+        }
+        s = wave_sum(s);
+        if (l == 0) g3t[f] = s;
+      }
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) QX[e * d + v * 64 + l] = acc[v];
+  }
+}
+
+// ---------------------------------------------------------------- phase 4
+
+// Per triplet, final backward: Zt = sum_c Zt_slot;
+//   ZP = Zt * h_j2 + Q * Zbar   (loss adjoint of G W_a; dW_a += G^T ZP)
+//   PT = Zt * (G W_a)            (routed to h_{j(e2)})
+template <int VPL>
+__global__ void tri_p4_kernel(const int* __restrict__ te, const int* __restrict__ te2, const float* __restrict__ tc,
+                              const float* __restrict__ B3, const float* __restrict__ dB3,
+                              const float* __restrict__ u3, const float* __restrict__ du3,
+                              const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
+                              const float* __restrict__ h, const float* __restrict__ hht,
+                              const float* __restrict__ Zbar, const int* __restrict__ pos3, int k3, long long Nt,
+                              int d, const float* __restrict__ Zts, float* __restrict__ ZP, float* __restrict__ PT) {
+  extern __shared__ float sWa[];
+  load_lds(sWa, Wa, L * nb * d);
+  JANUS_WAVE_LOOP(t, Nt) {
+    float zt[VPL];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) zt[v] = 0.f;
+    for (int c = 0; c < k3; ++c) {
+      const float* y = Zts + (long long)pos3[t * k3 + c] * d;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) zt[v] += y[v * 64 + l];
+    }
+    TriRows<VPL> o;
+    tri_rows<VPL, false>(t, te, te2, tc, B3, dB3, u3, du3, sWa, nb, L, d, l, o);
+    const long long j2 = ej[te2[t]];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      const int col = v * 64 + l;
+      const float q = hht ? hht[j2 * d + col] : 0.f;
+      ZP[t * d + col] = zt[v] * h[j2 * d + col] + q * Zbar[t * d + col];
+      PT[t * d + col] = zt[v] * o.z[v];
+    }
+  }
+}
+
+// Loss adjoint of the triplet router logits (lane x = expert x), recomputed
+// from the tables: lt[x] = p[x] (pt[x] - sum_y p[y] pt[y]).
+__device__ __forceinline__ float tri_logit_adjoint(long long t, int lane, int E, int k,
+                                                   const int* __restrict__ species, const int* __restrict__ ei,
+                                                   const int* __restrict__ ej, const int* __restrict__ te,
+                                                   const int* __restrict__ te2, const float* __restrict__ Pa,
+                                                   const float* __restrict__ Pb, const float* __restrict__ Pc,
+                                                   const float* __restrict__ beta, const int* __restrict__ eid,
+                                                   const float* __restrict__ gt) {
+  const int za = species[ei[te[t]]], zb = species[ej[te[t]]], zc = species[ej[te2[t]]];
+  double lg = -1e300;
+  if (lane < E)
+    lg = (((double)Pa[za * E + lane] + (double)Pb[zb * E + lane]) + (double)Pc[zc * E + lane]) + (double)beta[lane];
+  double mx = lg;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
+  const double ex = lane < E ? exp(lg - mx) : 0.0;
+  const double den = wave_sum_d(ex);
+  const float p = (float)(ex / den);
+  float pt = 0.f;
+  for (int c = 0; c < k; ++c)
+    if (eid[t * k + c] == lane) pt += gt[t * k + c];
+  const float s = wave_sum(p * pt);
+  return p * (pt - s);
+}
+
+// Per edge e (lane = expert): LB[e] = sum over tseg(e) of the logit adjoint,
+// LC[e] = sum over the triplets whose second edge is e.
+__global__ void tri_router_edge_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev, int E, int k,
+                                       const int* __restrict__ species, const int* __restrict__ ei,
+                                       const int* __restrict__ ej, const int* __restrict__ te,
+                                       const int* __restrict__ te2, const float* __restrict__ Pa,
+                                       const float* __restrict__ Pb, const float* __restrict__ Pc,
+                                       const float* __restrict__ beta, const int* __restrict__ eid,
+                                       const float* __restrict__ gt, long long Ne, float* __restrict__ LB,
+                                       float* __restrict__ LC) {
+  JANUS_WAVE_LOOP(e, Ne) {
+    float b = 0.f, c = 0.f;
+    for (int t = trowptr[e]; t < trowptr[e + 1]; ++t) {
+      b += tri_logit_adjoint(t, l, E, k, species, ei, ej, te, te2, Pa, Pb, Pc, beta, eid, gt);
+      c += tri_logit_adjoint(trev[t], l, E, k, species, ei, ej, te, te2, Pa, Pb, Pc, beta, eid, gt);
+    }
+    if (l < E) {
+      LB[e * E + l] = b;
+      LC[e * E + l] = c;
+    }
+  }
+}
+
+// Per atom: pa = sum over own edges of LB (vertex species), pb = sum over
+// incoming edges of LB (species of j(e)), pc = sum over incoming edges of LC.
+__global__ void tri_router_atom_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev, int E,
+                                       const float* __restrict__ LB, const float* __restrict__ LC, int N,
+                                       float* __restrict__ pa, float* __restrict__ pb, float* __restrict__ pc) {
+  JANUS_WAVE_LOOP(i, N) {
+    float a = 0.f, b = 0.f, c = 0.f;
+    if (l < E)
+      for (int e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+        a += LB[(long long)e * E + l];
+        b += LB[(long long)rev[e] * E + l];
+        c += LC[(long long)rev[e] * E + l];
+      }
+    if (l < E) {
+      pa[i * E + l] = a;
+      pb[i * E + l] = b;
+      pc[i * E + l] = c;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- loaders
+
+// Rows of the triplet features for weight-gradient products:
+// plain: G[t, f]; with coefficients ct: ac~ dG/dc + a1~ dG/dr1 + a2~ dG/dr2.
+struct LoadTriFeat {
+  const int* te;
+  const int* te2;
+  const float* tc;
+  const float* B3;
+  const float* dB3;
+  const float* u3;
+  const float* du3;
+  const float4* ct;   // null: plain features
+  int nb;
+  using Raw = float4;
+  __device__ __forceinline__ Raw load(long long t, int f) const {
+    const int q = f / nb, n = f - q * nb;
+    float P[kMaxL], dP[kMaxL];
+    legendre_d(tc[t], q + 1, P, dP);
+    const int e1 = te[t], e2 = te2[t];
+    const float4 b = ld4(B3 + (long long)e2 * nb + n);
+    const float u = u3[e1];
+    if (!ct) {
+      const float s = P[q] * u;
+      return make_float4(s * b.x, s * b.y, s * b.z, s * b.w);
+    }
+    const float4 db = ld4(dB3 + (long long)e2 * nb + n);
+    const float4 cf = ct[t];
+    const float du = du3[e1];
+    const float kb = cf.x * dP[q] * u + cf.y * P[q] * du, kd = cf.z * P[q] * u;
+    return make_float4(kb * b.x + kd * db.x, kb * b.y + kd * db.y, kb * b.z + kd * db.z, kb * b.w + kd * db.w);
+  }
+  __device__ __forceinline__ float4 apply(const Raw& v, int) const { return v; }
+};
+
+}  // namespace janus

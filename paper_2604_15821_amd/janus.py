@@ -51,7 +51,10 @@ class ProfileEntry(C.Structure):
 
 class Debug(C.Structure):
     _fields_ = [("eid", C.c_void_p), ("gate", C.c_void_p), ("counts", C.c_void_p), ("pos", C.c_void_p),
-                ("basis", C.c_void_p)]
+                ("basis", C.c_void_p), ("tri_e", C.c_void_p), ("tri_e2", C.c_void_p), ("eid3", C.c_void_p),
+                ("gate3", C.c_void_p)]
+
+    KEYS = ("eid", "gate", "counts", "pos", "basis", "tri_e", "tri_e2", "eid3", "gate3")
 
 
 _LIB = None
@@ -237,7 +240,7 @@ class Context:
         edges = nl.as_struct()
         dbg = None
         if debug is not None:
-            dbg = Debug(*[_ptr(debug.get(k)).value for k in ("eid", "gate", "counts", "pos", "basis")])
+            dbg = Debug(*[_ptr(debug.get(k)).value for k in Debug.KEYS])
         rc = _lib().janus_step(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S, C.byref(edges),
                                _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(loss), _ptr(E), _ptr(F), _ptr(dW),
                                C.byref(dbg) if dbg is not None else None, _stream())

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_entry_point():
         assert hasattr(lib, n), n
 
 
-@pytest.mark.parametrize("name", [n for n, w in WORKLOADS.items() if not w.model.three_body])
+@pytest.mark.parametrize("name", list(WORKLOADS))
 def test_weight_layout_matches_generator(name):
     m = WORKLOADS[name].model
     layout, total = janus.weight_layout(m)

@@ -20,7 +20,7 @@ from helpers import TOL_E, TOL_F, TOL_W, banner, energy_error, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["small", "shard", "irregular"]
+FULL = ["small", "threebody", "shard", "irregular"]
 
 
 def _gpu_step(b, model=None):
@@ -81,7 +81,7 @@ def test_loss_matches_returned_energies_and_forces(full):
 
 
 def test_sampled_structures_energy_and_forces(full):
-    from oracle.model import Params, build_graph, forces, forward_energy, route_all
+    from oracle.model import Params, build_graph_for, forces, forward_energy, route_all
     from paper_2604_15821_amd.synth import subset
     name, b, out = full
     sizes = np.diff(b.offsets)
@@ -93,7 +93,7 @@ def test_sampled_structures_energy_and_forces(full):
         sb = subset(b, [s])
         m = sb.model
         P = Params.from_weights(sb.weights, m)
-        g = build_graph(sb.pos, sb.cell, sb.offsets, m.r_cut, m.n_rbf)
+        g = build_graph_for(sb)
         rt = route_all(sb.species, g, P)
         E, cache = forward_energy(sb.species, g, P, rt)
         F = forces(sb.species, g, P, rt, cache)

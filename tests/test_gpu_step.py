@@ -8,7 +8,7 @@ from helpers import TOL_E, TOL_F, TOL_LOSS, TOL_W, banner, energy_error, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-STEP_CASES = [("tiny", None), ("small", 4)]
+STEP_CASES = [("tiny", None), ("small", 4), ("threebody", 2)]
 
 
 def _batch(name, n):
@@ -17,7 +17,7 @@ def _batch(name, n):
     return b if n is None else subset(b, range(n))
 
 
-def _run(b, debug=True, reps=1):
+def _run(b, debug=True, reps=1, n_triplets=0):
     import torch
     from paper_2604_15821_amd import janus
     d = janus.upload(b)
@@ -31,6 +31,12 @@ def _run(b, debug=True, reps=1):
                "gate": torch.empty(T * Ne * k, device="cuda:0"),
                "counts": torch.empty(T * m.n_experts, dtype=torch.int32, device="cuda:0"),
                "pos": torch.empty(T * Ne * k, dtype=torch.int32, device="cuda:0")}
+        if n_triplets:
+            n3 = T * n_triplets * m.top_k3
+            dbg.update({"tri_e": torch.empty(n_triplets, dtype=torch.int32, device="cuda:0"),
+                        "tri_e2": torch.empty(n_triplets, dtype=torch.int32, device="cuda:0"),
+                        "eid3": torch.empty(n3, dtype=torch.int32, device="cuda:0"),
+                        "gate3": torch.empty(n3, device="cuda:0")})
     outs = []
     for _ in range(reps):
         loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"],
@@ -47,10 +53,26 @@ def case(request):
     from oracle.model import training_step
     name, n = request.param
     b = _batch(name, n)
-    banner("step", name, n, b.n_atoms)
-    outs, dbg, Ne = _run(b, reps=2)
     loss, E, F, grad, aux = training_step(b, return_aux=True)
+    nt = aux["graph"].tri.te.size if aux["graph"].tri is not None else 0
+    banner("step", name, n, b.n_atoms, "atoms", nt, "triplets")
+    outs, dbg, Ne = _run(b, reps=2, n_triplets=nt)
     return b, outs, dbg, Ne, (loss, E, F, grad, aux)
+
+
+def test_triplets_and_their_routing_are_bit_exact(case):
+    b, outs, dbg, Ne, (loss, E, F, grad, aux) = case
+    tri = aux["graph"].tri
+    if tri is None:
+        pytest.skip("workload without the three-body term")
+    m = b.model
+    nt, k3 = tri.te.size, m.top_k3
+    assert nt > 1000
+    assert (dbg["tri_e"] == tri.te).all() and (dbg["tri_e2"] == tri.te2).all()
+    for t, rt in enumerate(aux["routing"]):
+        sl = slice(t * nt * k3, (t + 1) * nt * k3)
+        assert (dbg["eid3"][sl].reshape(nt, k3) == rt.tri.eid).all()
+        assert np.abs(dbg["gate3"][sl].reshape(nt, k3) - rt.tri.gate).max() <= 1e-6
 
 
 def test_routing_is_bit_exact(case):
