@@ -29,7 +29,8 @@
 //
 // Epilogue: the accumulators are staged through LDS, 64 rows at a time, and
 // then visited row-major as float4, so every epilogue read and write of
-// global memory is a coalesced 512-byte row segment.
+// global memory is a coalesced 512-byte row segment; a thread issues all of
+// its epilogue reads before it uses any of them.
 #pragma once
 
 #include "common.h"
@@ -108,14 +109,20 @@ struct LoadSiluD1Scaled {   // SiLU'(z[r, k]) * w[k]
 };
 
 // ---------------------------------------------------------------- epilogues
-// operator()(r, c, v) receives output row r, columns c..c+3 (c % 4 == 0) and
-// returns this piece's contribution to the row sum (used when kRowSum).
+// An epilogue works on output row r, columns c..c+3 (c % 4 == 0) in two
+// steps so that all of a thread's global reads are in flight together:
+// load(r, c) fetches what the piece needs, store(r, c, v, raw) writes the
+// results and returns the piece's contribution to the row sum (kRowSum).
+
+struct NoRaw {};
 
 struct EpiStore {
   float* c;
   long long ld;
   static constexpr bool kRowSum = false;
-  __device__ __forceinline__ float operator()(long long r, int col, float4 v) const {
+  using Raw = NoRaw;
+  __device__ __forceinline__ Raw load(long long, int) const { return Raw{}; }
+  __device__ __forceinline__ float store(long long r, int col, float4 v, const Raw&) const {
     st4(c + r * ld + col, v);
     return 0.f;
   }
@@ -130,8 +137,9 @@ struct EpiRowScale {   // c = s[r] * v
   const float* s;
   long long ld;
   static constexpr bool kRowSum = false;
-  __device__ __forceinline__ float operator()(long long r, int col, float4 v) const {
-    const float a = s[r];
+  using Raw = float;
+  __device__ __forceinline__ Raw load(long long r, int) const { return s[r]; }
+  __device__ __forceinline__ float store(long long r, int col, float4 v, const Raw& a) const {
     st4(c + r * ld + col, make_float4(a * v.x, a * v.y, a * v.z, a * v.w));
     return 0.f;
   }
@@ -144,13 +152,18 @@ struct EpiP2 {
   float* Ab;
   long long ld;
   static constexpr bool kRowSum = false;
-  __device__ __forceinline__ float operator()(long long r, int c, float4 v) const {
+  using Raw = float4;
+  __device__ __forceinline__ Raw load(long long r, int c) const { return ld4(A + r * ld + c); }
+  __device__ __forceinline__ float store(long long r, int c, float4 v, const Raw& a) const {
     const long long i = r * ld + c;
-    const float4 a = ld4(A + i);
     st4(Sb + i, v);
     st4(Ab + i, make_float4(silu_d1(a.x) * v.x, silu_d1(a.y) * v.y, silu_d1(a.z) * v.z, silu_d1(a.w) * v.w));
     return 0.f;
   }
+};
+
+struct Float4x2 {
+  float4 a, b;
 };
 
 // Double backward, after Abt = Xbt W1:
@@ -162,14 +175,19 @@ struct EpiP3 {
   float* Ab;
   long long ld;
   static constexpr bool kRowSum = false;
+  using Raw = Float4x2;
   __device__ __forceinline__ static void d12(float a, float& d1, float& d2) {
     const float s = sig(a);
     d1 = s + a * s * (1.f - s);
     d2 = s * (1.f - s) * (2.f + a * (1.f - 2.f * s));
   }
-  __device__ __forceinline__ float operator()(long long r, int c, float4 v) const {
+  __device__ __forceinline__ Raw load(long long r, int c) const {
     const long long i = r * ld + c;
-    const float4 a = ld4(A + i), sb = ld4(Sb + i);
+    return Raw{ld4(A + i), ld4(Sb + i)};
+  }
+  __device__ __forceinline__ float store(long long r, int c, float4 v, const Raw& x) const {
+    const long long i = r * ld + c;
+    const float4 a = x.a, sb = x.b;
     float4 o1, o2;
     float d1, d2;
     d12(a.x, d1, d2); o1.x = d1 * v.x; o2.x = d2 * sb.x * v.x;
@@ -190,27 +208,38 @@ struct EpiP4 {
   const float* gate;
   long long ld;
   static constexpr bool kRowSum = true;
+  struct Raw {
+    float4 a, c;
+    float g;
+  };
   __device__ __forceinline__ static float one(float a, float v, float c, float g, float& sum) {
     const float s = sig(a);
     sum += v * a * s;
     return g * (s + a * s * (1.f - s)) * v + c;
   }
-  __device__ __forceinline__ float operator()(long long r, int c, float4 v) const {
+  __device__ __forceinline__ Raw load(long long r, int c) const {
     const long long i = r * ld + c;
-    const float4 a = ld4(A + i), cc = ld4(Sb + i);
-    const float g = gate[r];
+    return Raw{ld4(A + i), ld4(Sb + i), gate[r]};
+  }
+  __device__ __forceinline__ float store(long long r, int c, float4 v, const Raw& x) const {
     float sum = 0.f;
     float4 o;
-    o.x = one(a.x, v.x, cc.x, g, sum);
-    o.y = one(a.y, v.y, cc.y, g, sum);
-    o.z = one(a.z, v.z, cc.z, g, sum);
-    o.w = one(a.w, v.w, cc.w, g, sum);
-    st4(Sb + i, o);
+    o.x = one(x.a.x, v.x, x.c.x, x.g, sum);
+    o.y = one(x.a.y, v.y, x.c.y, x.g, sum);
+    o.z = one(x.a.z, v.z, x.c.z, x.g, sum);
+    o.w = one(x.a.w, v.w, x.c.w, x.g, sum);
+    st4(Sb + r * ld + c, o);
     return sum;
   }
 };
 
 // ------------------------------------------------------------ LDS staging
+// The loads are unconditional: rows (and columns) past the end of the range
+// read the last valid one and are replaced by zeros when stored to LDS.  A
+// conditional load would put a branch around every load, and at the join
+// the compiler waits for all earlier loads, which serialises them.  Ranges
+// are never empty (tiles and chunks are built only over rows that exist;
+// widths are multiples of 4).
 
 // [m][k] tile from a k-contiguous operand: thread q loads row q/4, k-quad q%4.
 template <class L>
@@ -223,7 +252,7 @@ struct StageMK {
       const int q = tid + 256 * i;
       const long long r = (long long)r0 + (q >> 2);
       ok[i] = r < r1;
-      if (ok[i]) raw[i] = ld.load(r, k0 + 4 * (q & 3));
+      raw[i] = ld.load(ok[i] ? r : (long long)r1 - 1, k0 + 4 * (q & 3));
     }
   }
   __device__ __forceinline__ void store(const L& ld, float* s, int k0, int tid) const {
@@ -247,7 +276,7 @@ struct StageKM {
       const long long r = rk + (q >> 5);
       const int m = m0 + 4 * (q & 31);
       ok[i] = r < rk_end && m < m_end;
-      if (ok[i]) raw[i] = ld.load(r, m);
+      raw[i] = ld.load(r < rk_end ? r : rk_end - 1, m < m_end ? m : m_end - 4);
     }
   }
   __device__ __forceinline__ void store(const L& ld, float* s, int m0, int tid) const {
@@ -365,7 +394,8 @@ __global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float
 
   // Epilogue in two halves of 64 rows: the waves of row half `half` stage
   // their accumulators (lane l of block (bi, bj) holds column lr and rows
-  // 8 (v / 4) + 4 hf + v % 4), then every thread visits float4 pieces.
+  // 8 (v / 4) + 4 hf + v % 4), then every thread visits 8 float4 pieces:
+  // first all the epilogue's global reads, then the arithmetic and stores.
   float* sC = smem;
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
@@ -378,15 +408,21 @@ __global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float
           for (int v = 0; v < 16; ++v)
             sC[(bi * 32 + 8 * (v >> 2) + 4 * hf + (v & 3)) * LD_C + wn * 64 + bj * 32 + lr] = acc[bi][bj][v];
     }
+    typename Epi::Raw raw[8];
+    const int c4 = tid & 31;
+    const int col = n0 + 4 * c4;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const long long row = (long long)r0 + half * 64 + (tid >> 5) + 8 * i;
+      if (row < r1 && col < N) raw[i] = epi.load(row, col);
+    }
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int idx = tid + 256 * i;
-      const int rl = idx >> 5, c4 = idx & 31;
+      const int rl = (tid >> 5) + 8 * i;
       const long long row = (long long)r0 + half * 64 + rl;
-      const int col = n0 + 4 * c4;
       float part = 0.f;
-      if (row < r1 && col < N) part = epi(row, col, ld4(sC + rl * LD_C + 4 * c4));
+      if (row < r1 && col < N) part = epi.store(row, col, ld4(sC + rl * LD_C + 4 * c4), raw[i]);
       if (Epi::kRowSum) {
 #pragma unroll
         for (int o = 16; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
