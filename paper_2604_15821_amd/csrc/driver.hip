@@ -314,8 +314,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_dispatch);
-      LAUNCH_VPL(dispatch_x_kernel, d, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
-                 POS(t), k, Ne, d, Xs(t), (const float*)(three && Nt > 0 ? p.Q : nullptr));
+      LAUNCH_VPL_K(dispatch_x_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
+                 POS(t), Ne, d, Xs(t), (const float*)(three && Nt > 0 ? p.Q : nullptr));
     }
     {
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
@@ -327,7 +327,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     {
       PROF(PROF_ATOM, 0, by_combine);
-      LAUNCH_VPL(combine_fwd_kernel, d, gN, b256, 0, st, rowptr, POS(t), k, (const float*)p.T1,
+      LAUNCH_VPL_K(combine_fwd_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)p.T1,
                  (const float*)HV(p.h, t), N, d, HV(p.h, t + 1));
     }
   }
@@ -358,7 +358,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     const float* W2 = Wp(blk(t, "W2"));
     {
       PROF(PROF_ATOM, 0, by_gather);
-      LAUNCH_VPL(gather_atom_kernel, d, gN, b256, 0, st, rowptr, POS(t), k, GATE(t), (const float*)HV(p.hh, t + 1),
+      LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), (const float*)HV(p.hh, t + 1),
                  N, d, Ybs(t));
     }
     {
@@ -372,8 +372,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_p2);
-      LAUNCH_VPL(edge_p2_kernel, d, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
-                 (const float*)HV(p.h, t), ej, POS(t), k, Ne, d, (const float*)p.T1, Xbar(t), Fbar(t), p.rbar, p.Pe);
+      LAUNCH_VPL_K(edge_p2_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
+                 (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)p.T1, Xbar(t), Fbar(t), p.rbar, p.Pe);
     }
     if (three && Nt > 0) {
       // triplet messages' backward: Ybar3 = g3 Xbar_e -> experts -> Zbar; feature-geometry adjoints
@@ -479,8 +479,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_p3);
-      LAUNCH_VPL(edge_p3_kernel, d, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
-                 (const float*)HV(p.h, t), ej, POS(t), k, Ne, d, (const float*)Xbar(t), hht_t, (const float*)p.rt,
+      LAUNCH_VPL_K(edge_p3_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
+                 (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)Xbar(t), hht_t, (const float*)p.rt,
                  p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr));
     }
     if (tri_t) {
@@ -524,7 +524,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     {
       PROF(PROF_ATOM, 0, by_cp3);
-      LAUNCH_VPL(combine_p3_kernel, d, gN, b256, 0, st, rowptr, POS(t), k, GATE(t), (const float*)p.T2,
+      LAUNCH_VPL_K(combine_p3_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), (const float*)p.T2,
                  (const float*)HV(p.hh, t + 1), hht_t, N, d, p.g3 + t * M, HV(p.hht, t + 1));
     }
   }
@@ -562,7 +562,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     {
       // message adjoint, ungated, into the slots
       PROF(PROF_ATOM, 0, by_gather);
-      LAUNCH_VPL(gather_atom_kernel, d, gN, b256, 0, st, rowptr, POS(t), k, (const float*)nullptr,
+      LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)nullptr,
                  (const float*)HV(p.hh, t + 1), N, d, p.T1);
     }
     {
@@ -591,8 +591,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     if (Ne > 0) {
       {
         PROF(PROF_EDGE, 0, by_p4);
-        LAUNCH_VPL(edge_p4_kernel, d, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
-                   POS(t), k, Ne, d, (const float*)p.T2, (const float*)Xbar(t), hht_t, p.Ft, p.Pe,
+        LAUNCH_VPL_K(edge_p4_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
+                   POS(t), Ne, d, (const float*)p.T2, (const float*)Xbar(t), hht_t, p.Ft, p.Pe,
                    three ? p.Q : (float*)nullptr);
       }
       {

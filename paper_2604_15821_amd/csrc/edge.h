@@ -1,5 +1,5 @@
 // Edge- and atom-level kernels of the training step (wave64, one wave per
-// edge or per atom; lane l owns feature columns l, l + 64, ...).
+// edge or per atom).
 //
 // Notation (per interaction block t, edge e = (i, j, n), choice c):
 //   F_e  = B(r_e) W_b          radial filter,   F'_e = B'(r_e) W_b
@@ -11,21 +11,93 @@
 // Every sum over the edges of an atom walks its CSR segment in order; sums
 // over the edges that point *to* an atom walk the segment through the
 // reverse-edge map.  No kernel uses floating-point atomics.
+//
+// Memory access: the wave's item index is wave-uniform (readfirstlane), so
+// per-item indices (pos, ej, rev, gates, segment bounds) are scalar loads;
+// a feature row of d = 64 VPL floats is read or written by the whole wave in
+// VPL / W accesses of W = min(VPL, 4) consecutive floats per lane (Lanes),
+// each covering one contiguous 256 W-byte segment.  The k slot rows of an
+// edge (k is a template argument, 1..4) and, in the per-atom sums, the rows
+// of two edges are loaded before any of them is used.
 #pragma once
 
 #include "common.h"
 
 namespace janus {
 
+constexpr int kMaxTopK = 4;
+
 template <int VPL>
-__device__ __forceinline__ void filter_row(const float* __restrict__ Bv, const float* sW, int nb, int d, int l,
-                                           float (&F)[VPL]) {
+struct Lanes {
+  static constexpr int W = VPL < 4 ? VPL : 4;   // floats per lane per access
+  static constexpr int Q = VPL / W;             // accesses per row
+  // column of x[q * W + w] for lane l: 64 W q + W l + w
+  __device__ static __forceinline__ int col(int l, int q) { return 64 * W * q + W * l; }
+};
+
+template <int VPL>
+__device__ __forceinline__ void ld_row(const float* __restrict__ p, int l, float (&x)[VPL]) {
+  constexpr int W = Lanes<VPL>::W;
 #pragma unroll
-  for (int v = 0; v < VPL; ++v) F[v] = 0.f;
+  for (int q = 0; q < Lanes<VPL>::Q; ++q) {
+    const float* s = p + Lanes<VPL>::col(l, q);
+    if constexpr (W == 4) {
+      const float4 v = *reinterpret_cast<const float4*>(s);
+      x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+    } else if constexpr (W == 2) {
+      const float2 v = *reinterpret_cast<const float2*>(s);
+      x[2 * q] = v.x; x[2 * q + 1] = v.y;
+    } else {
+      x[q] = *s;
+    }
+  }
+}
+
+template <int VPL>
+__device__ __forceinline__ void st_row(float* __restrict__ p, int l, const float (&x)[VPL]) {
+  constexpr int W = Lanes<VPL>::W;
+#pragma unroll
+  for (int q = 0; q < Lanes<VPL>::Q; ++q) {
+    float* s = p + Lanes<VPL>::col(l, q);
+    if constexpr (W == 4) {
+      *reinterpret_cast<float4*>(s) = make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]);
+    } else if constexpr (W == 2) {
+      *reinterpret_cast<float2*>(s) = make_float2(x[2 * q], x[2 * q + 1]);
+    } else {
+      *s = x[q];
+    }
+  }
+}
+
+template <int VPL>
+__device__ __forceinline__ void zero_row(float (&x)[VPL]) {
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) x[v] = 0.f;
+}
+
+template <int VPL>
+__device__ __forceinline__ void add_row(float (&x)[VPL], const float (&y)[VPL]) {
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) x[v] += y[v];
+}
+
+// One basis row of an edge, one value per lane (lane n < nb holds b_n);
+// nb <= 32, so a single coalesced load.
+__device__ __forceinline__ float basis_lane(const float* __restrict__ B, long long e, int nb, int l) {
+  return B[e * nb + (l < nb ? l : nb - 1)];
+}
+
+// F = b W_b for one edge, W_b [nb, d] staged in LDS; b is held one value per lane.
+template <int VPL>
+__device__ __forceinline__ void filter_row(float b_lane, const float* sW, int nb, int d, int l, float (&F)[VPL]) {
+  zero_row<VPL>(F);
+#pragma unroll 4
   for (int n = 0; n < nb; ++n) {
-    const float b = Bv[n];
+    const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(b_lane), n));
+    float w[VPL];
+    ld_row<VPL>(sW + n * d, l, w);
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) F[v] += b * sW[n * d + v * 64 + l];
+    for (int v = 0; v < VPL; ++v) F[v] += b * w[v];
   }
 }
 
@@ -34,111 +106,127 @@ __device__ __forceinline__ void load_lds(float* s, const float* g, int n) {
   __syncthreads();
 }
 
-#define JANUS_WAVE_LOOP(var, count)                                                     \
-  const int l = threadIdx.x & 63;                                                       \
-  const long long nw_ = (long long)gridDim.x * (blockDim.x >> 6);                       \
-  for (long long var = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); \
+// Grid-stride loop of waves over items; the item index is wave-uniform.
+#define JANUS_WAVE_LOOP(var, count)                                                                        \
+  const int l = threadIdx.x & 63;                                                                          \
+  const long long nw_ = (long long)gridDim.x * (blockDim.x >> 6);                                          \
+  for (long long var = (long long)blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); \
        var < (count); var += nw_)
+
+// y = sum_c rows[pos[e, c]]  (the k slot rows of edge e)
+template <int VPL, int KC>
+__device__ __forceinline__ void sum_slots(const float* __restrict__ rows, const int* __restrict__ pos, long long e,
+                                          int d, int l, float (&y)[VPL]) {
+  float r[KC][VPL];
+#pragma unroll
+  for (int c = 0; c < KC; ++c) ld_row<VPL>(rows + (long long)pos[e * KC + c] * d, l, r[c]);
+  zero_row<VPL>(y);
+#pragma unroll
+  for (int c = 0; c < KC; ++c) add_row<VPL>(y, r[c]);
+}
 
 // Phase 1: X_e = F_e * h_j (+ Q_e, the triplet messages of e when present),
 // written to the slots of its k experts.
-template <int VPL>
+template <int VPL, int KC>
 __global__ void dispatch_x_kernel(const float* __restrict__ B, int nb, const float* __restrict__ Wb,
                                   const float* __restrict__ h, const int* __restrict__ ej,
-                                  const int* __restrict__ pos, int k, long long Ne, int d, float* __restrict__ Xs,
+                                  const int* __restrict__ pos, long long Ne, int d, float* __restrict__ Xs,
                                   const float* __restrict__ Q) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
+    const float bl = basis_lane(B, e, nb, l);
+    float hj[VPL], q[VPL];
+    ld_row<VPL>(h + (long long)ej[e] * d, l, hj);
+    if (Q) ld_row<VPL>(Q + e * d, l, q); else zero_row<VPL>(q);
     float F[VPL];
-    filter_row<VPL>(B + e * nb, sW, nb, d, l, F);
-    const float* hj = h + (long long)ej[e] * d;
+    filter_row<VPL>(bl, sW, nb, d, l, F);
     float X[VPL];
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) X[v] = F[v] * hj[v * 64 + l] + (Q ? Q[e * d + v * 64 + l] : 0.f);
-    for (int c = 0; c < k; ++c) {
-      float* o = Xs + (long long)pos[e * k + c] * d;
+    for (int v = 0; v < VPL; ++v) X[v] = F[v] * hj[v] + q[v];
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) o[v * 64 + l] = X[v];
-    }
+    for (int c = 0; c < KC; ++c) st_row<VPL>(Xs + (long long)pos[e * KC + c] * d, l, X);
   }
 }
 
 // Phase 1: h'_i = h_i + sum_{e in seg(i)} sum_c Yg[pos[e, c]]  (Yg already gated).
-template <int VPL>
-__global__ void combine_fwd_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos, int k,
+template <int VPL, int KC>
+__global__ void combine_fwd_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos,
                                    const float* __restrict__ Yg, const float* __restrict__ h, int N, int d,
                                    float* __restrict__ hn) {
   JANUS_WAVE_LOOP(i, N) {
     float acc[VPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) acc[v] = h[i * d + v * 64 + l];
+    ld_row<VPL>(h + i * d, l, acc);
     const int e0 = rowptr[i], e1 = rowptr[i + 1];
-    for (int e = e0; e < e1; ++e)
-      for (int c = 0; c < k; ++c) {
-        const float* y = Yg + (long long)pos[(long long)e * k + c] * d;
-#pragma unroll
-        for (int v = 0; v < VPL; ++v) acc[v] += y[v * 64 + l];
-      }
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) hn[i * d + v * 64 + l] = acc[v];
+    int e = e0;
+    for (; e + 2 <= e1; e += 2) {
+      float y0[VPL], y1[VPL];
+      sum_slots<VPL, KC>(Yg, pos, e, d, l, y0);
+      sum_slots<VPL, KC>(Yg, pos, e + 1, d, l, y1);
+      add_row<VPL>(acc, y0);
+      add_row<VPL>(acc, y1);
+    }
+    if (e < e1) {
+      float y0[VPL];
+      sum_slots<VPL, KC>(Yg, pos, e, d, l, y0);
+      add_row<VPL>(acc, y0);
+    }
+    st_row<VPL>(hn + i * d, l, acc);
   }
 }
 
 // Slot rows of the adjoint arriving at the messages: out[pos[e, c]] = (g_ec) * src[i(e)].
-template <int VPL>
-__global__ void gather_atom_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos, int k,
+template <int VPL, int KC>
+__global__ void gather_atom_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos,
                                    const float* __restrict__ gate, const float* __restrict__ src, int N, int d,
                                    float* __restrict__ out) {
   JANUS_WAVE_LOOP(i, N) {
     float s[VPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) s[v] = src[i * d + v * 64 + l];
+    ld_row<VPL>(src + i * d, l, s);
     const int e0 = rowptr[i], e1 = rowptr[i + 1];
-    for (int e = e0; e < e1; ++e)
-      for (int c = 0; c < k; ++c) {
-        const long long f = (long long)e * k + c;
-        const float g = gate ? gate[f] : 1.f;
-        float* o = out + (long long)pos[f] * d;
+    for (int e = e0; e < e1; ++e) {
 #pragma unroll
-        for (int v = 0; v < VPL; ++v) o[v * 64 + l] = g * s[v];
+      for (int c = 0; c < KC; ++c) {
+        const long long f = (long long)e * KC + c;
+        const float g = gate ? gate[f] : 1.f;
+        float o[VPL];
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) o[v] = g * s[v];
+        st_row<VPL>(out + (long long)pos[f] * d, l, o);
       }
+    }
   }
 }
 
 // Phase 2 per edge: Xbar_e = sum_c Xbar_slot; Fbar = Xbar * h_j;
 // rbar_e += Fbar . F'_e; P_e = Xbar * F_e (routed to h_j by scatter_rev).
-template <int VPL>
+template <int VPL, int KC>
 __global__ void edge_p2_kernel(const float* __restrict__ B, const float* __restrict__ dB, int nb,
                                const float* __restrict__ Wb, const float* __restrict__ h, const int* __restrict__ ej,
-                               const int* __restrict__ pos, int k, long long Ne, int d,
-                               const float* __restrict__ Xbs, float* __restrict__ Xbar, float* __restrict__ Fbar,
-                               float* __restrict__ rbar, float* __restrict__ P) {
+                               const int* __restrict__ pos, long long Ne, int d, const float* __restrict__ Xbs,
+                               float* __restrict__ Xbar, float* __restrict__ Fbar, float* __restrict__ rbar,
+                               float* __restrict__ P) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
-    float xb[VPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) xb[v] = 0.f;
-    for (int c = 0; c < k; ++c) {
-      const float* y = Xbs + (long long)pos[e * k + c] * d;
-#pragma unroll
-      for (int v = 0; v < VPL; ++v) xb[v] += y[v * 64 + l];
-    }
+    const float bl = basis_lane(B, e, nb, l), dbl = basis_lane(dB, e, nb, l);
+    float xb[VPL], hj[VPL];
+    sum_slots<VPL, KC>(Xbs, pos, e, d, l, xb);
+    ld_row<VPL>(h + (long long)ej[e] * d, l, hj);
     float F[VPL], Fp[VPL];
-    filter_row<VPL>(B + e * nb, sW, nb, d, l, F);
-    filter_row<VPL>(dB + e * nb, sW, nb, d, l, Fp);
-    const float* hj = h + (long long)ej[e] * d;
+    filter_row<VPL>(bl, sW, nb, d, l, F);
+    filter_row<VPL>(dbl, sW, nb, d, l, Fp);
+    float fb[VPL], p[VPL];
     float s = 0.f;
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
-      const long long o = e * d + v * 64 + l;
-      const float fb = xb[v] * hj[v * 64 + l];
-      Xbar[o] = xb[v];
-      Fbar[o] = fb;
-      P[o] = xb[v] * F[v];
-      s += fb * Fp[v];
+      fb[v] = xb[v] * hj[v];
+      p[v] = xb[v] * F[v];
+      s += fb[v] * Fp[v];
     }
+    st_row<VPL>(Xbar + e * d, l, xb);
+    st_row<VPL>(Fbar + e * d, l, fb);
+    st_row<VPL>(P + e * d, l, p);
     s = wave_sum(s);
     if (l == 0) rbar[e] += s;
   }
@@ -151,121 +239,137 @@ __global__ void scatter_rev_kernel(const int* __restrict__ rowptr, const int* __
                                    const float* __restrict__ base1, int N, int d, float* __restrict__ out) {
   JANUS_WAVE_LOOP(a, N) {
     float acc[VPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      acc[v] = base0 ? base0[a * d + v * 64 + l] : 0.f;
-      if (base1) acc[v] += base1[a * d + v * 64 + l];
+    if (base0) ld_row<VPL>(base0 + a * d, l, acc); else zero_row<VPL>(acc);
+    if (base1) {
+      float b[VPL];
+      ld_row<VPL>(base1 + a * d, l, b);
+      add_row<VPL>(acc, b);
     }
     const int e0 = rowptr[a], e1 = rowptr[a + 1];
-    for (int e = e0; e < e1; ++e) {
-      const float* p = P + (long long)rev[e] * d;
-#pragma unroll
-      for (int v = 0; v < VPL; ++v) acc[v] += p[v * 64 + l];
+    int e = e0;
+    for (; e + 4 <= e1; e += 4) {
+      float p0[VPL], p1[VPL], p2[VPL], p3[VPL];
+      ld_row<VPL>(P + (long long)rev[e] * d, l, p0);
+      ld_row<VPL>(P + (long long)rev[e + 1] * d, l, p1);
+      ld_row<VPL>(P + (long long)rev[e + 2] * d, l, p2);
+      ld_row<VPL>(P + (long long)rev[e + 3] * d, l, p3);
+      add_row<VPL>(acc, p0);
+      add_row<VPL>(acc, p1);
+      add_row<VPL>(acc, p2);
+      add_row<VPL>(acc, p3);
     }
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) out[a * d + v * 64 + l] = acc[v];
+    for (; e < e1; ++e) {
+      float p0[VPL];
+      ld_row<VPL>(P + (long long)rev[e] * d, l, p0);
+      add_row<VPL>(acc, p0);
+    }
+    st_row<VPL>(out + a * d, l, acc);
   }
 }
 
 // Phase 3 per edge (adjoints of the force backward):
 //   Fbt = rt_e F'_e,  Xbt = Q_e * F_e + Fbt * h_j  (Q_e = adjoint of hbar^t at j),
 //   Xbt copied to the k slots; P_e = Fbt * Xbar_e  (routed to h_j).
-template <int VPL>
+template <int VPL, int KC>
 __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restrict__ dB, int nb,
                                const float* __restrict__ Wb, const float* __restrict__ h, const int* __restrict__ ej,
-                               const int* __restrict__ pos, int k, long long Ne, int d, const float* __restrict__ Xbar,
+                               const int* __restrict__ pos, long long Ne, int d, const float* __restrict__ Xbar,
                                const float* __restrict__ hht, const float* __restrict__ rt, float* __restrict__ Xbts,
                                float* __restrict__ P, const float* __restrict__ QX) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
-    float F[VPL], Fp[VPL];
-    filter_row<VPL>(B + e * nb, sW, nb, d, l, F);
-    filter_row<VPL>(dB + e * nb, sW, nb, d, l, Fp);
+    const float bl = basis_lane(B, e, nb, l), dbl = basis_lane(dB, e, nb, l);
     const long long j = ej[e];
     const float r = rt[e];
-    float X[VPL];
+    float q[VPL], hj[VPL], xb[VPL], qx[VPL];
+    if (hht) ld_row<VPL>(hht + j * d, l, q); else zero_row<VPL>(q);
+    ld_row<VPL>(h + j * d, l, hj);
+    ld_row<VPL>(Xbar + e * d, l, xb);
+    if (QX) ld_row<VPL>(QX + e * d, l, qx); else zero_row<VPL>(qx);
+    float F[VPL], Fp[VPL];
+    filter_row<VPL>(bl, sW, nb, d, l, F);
+    filter_row<VPL>(dbl, sW, nb, d, l, Fp);
+    float X[VPL], p[VPL];
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
-      const int col = v * 64 + l;
       const float fbt = r * Fp[v];
-      const float q = hht ? hht[j * d + col] : 0.f;
-      X[v] = q * F[v] + fbt * h[j * d + col] + (QX ? QX[e * d + col] : 0.f);
-      P[e * d + col] = fbt * Xbar[e * d + col];
+      X[v] = q[v] * F[v] + fbt * hj[v] + qx[v];
+      p[v] = fbt * xb[v];
     }
-    for (int c = 0; c < k; ++c) {
-      float* o = Xbts + (long long)pos[e * k + c] * d;
+    st_row<VPL>(P + e * d, l, p);
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) o[v * 64 + l] = X[v];
-    }
+    for (int c = 0; c < KC; ++c) st_row<VPL>(Xbts + (long long)pos[e * KC + c] * d, l, X);
   }
 }
 
 // Phase 3 per atom: gate adjoints g3_ec = Ybt[pos] . hbar^{t+1}_i and
 // hht^{t+1}_i = hht^t_i + sum_{e in seg(i)} sum_c g_ec Ybt[pos[e, c]].
-template <int VPL>
-__global__ void combine_p3_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos, int k,
+template <int VPL, int KC>
+__global__ void combine_p3_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos,
                                   const float* __restrict__ gate, const float* __restrict__ Ybt,
                                   const float* __restrict__ hbar_next, const float* __restrict__ hht, int N, int d,
                                   float* __restrict__ g3, float* __restrict__ hht_next) {
   JANUS_WAVE_LOOP(i, N) {
     float mb[VPL], acc[VPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      mb[v] = hbar_next[i * d + v * 64 + l];
-      acc[v] = hht ? hht[i * d + v * 64 + l] : 0.f;
-    }
+    ld_row<VPL>(hbar_next + i * d, l, mb);
+    if (hht) ld_row<VPL>(hht + i * d, l, acc); else zero_row<VPL>(acc);
     const int e0 = rowptr[i], e1 = rowptr[i + 1];
-    for (int e = e0; e < e1; ++e)
-      for (int c = 0; c < k; ++c) {
-        const long long f = (long long)e * k + c;
-        const float* y = Ybt + (long long)pos[f] * d;
-        const float g = gate[f];
-        float s = 0.f;
+    for (int e = e0; e < e1; ++e) {
+      float y[KC][VPL];
+#pragma unroll
+      for (int c = 0; c < KC; ++c) ld_row<VPL>(Ybt + (long long)pos[(long long)e * KC + c] * d, l, y[c]);
+      float s[KC];
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        const float g = gate[(long long)e * KC + c];
+        s[c] = 0.f;
 #pragma unroll
         for (int v = 0; v < VPL; ++v) {
-          const float yv = y[v * 64 + l];
-          s += yv * mb[v];
-          acc[v] += g * yv;
+          s[c] += y[c][v] * mb[v];
+          acc[v] += g * y[c][v];
         }
-        s = wave_sum(s);
-        if (l == 0) g3[f] = s;
       }
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) hht_next[i * d + v * 64 + l] = acc[v];
+      for (int c = 0; c < KC; ++c) s[c] = wave_sum(s[c]);
+      if (l == 0) {
+#pragma unroll
+        for (int c = 0; c < KC; ++c) g3[(long long)e * KC + c] = s[c];
+      }
+    }
+    st_row<VPL>(hht_next + i * d, l, acc);
   }
 }
 
 // Phase 4 per edge: Xt_e = sum_c Xt_slot; Ft_e = Xt * h_j + Q_e * Xbar_e
 // (Q_e from the double backward); P_e = Xt * F_e (routed to h_j).
-template <int VPL>
+template <int VPL, int KC>
 __global__ void edge_p4_kernel(const float* __restrict__ B, int nb, const float* __restrict__ Wb,
                                const float* __restrict__ h, const int* __restrict__ ej, const int* __restrict__ pos,
-                               int k, long long Ne, int d, const float* __restrict__ Xts,
-                               const float* __restrict__ Xbar, const float* __restrict__ hht,
-                               float* __restrict__ Ft, float* __restrict__ P, float* __restrict__ XT) {
+                               long long Ne, int d, const float* __restrict__ Xts, const float* __restrict__ Xbar,
+                               const float* __restrict__ hht, float* __restrict__ Ft, float* __restrict__ P,
+                               float* __restrict__ XT) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
-    float xt[VPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) xt[v] = 0.f;
-    for (int c = 0; c < k; ++c) {
-      const float* y = Xts + (long long)pos[e * k + c] * d;
-#pragma unroll
-      for (int v = 0; v < VPL; ++v) xt[v] += y[v * 64 + l];
-    }
-    float F[VPL];
-    filter_row<VPL>(B + e * nb, sW, nb, d, l, F);
+    const float bl = basis_lane(B, e, nb, l);
     const long long j = ej[e];
+    float xt[VPL], hj[VPL], q[VPL], xb[VPL];
+    sum_slots<VPL, KC>(Xts, pos, e, d, l, xt);
+    ld_row<VPL>(h + j * d, l, hj);
+    if (hht) ld_row<VPL>(hht + j * d, l, q); else zero_row<VPL>(q);
+    ld_row<VPL>(Xbar + e * d, l, xb);
+    float F[VPL];
+    filter_row<VPL>(bl, sW, nb, d, l, F);
+    float ft[VPL], p[VPL];
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
-      const int col = v * 64 + l;
-      const float q = hht ? hht[j * d + col] : 0.f;
-      Ft[e * d + col] = xt[v] * h[j * d + col] + q * Xbar[e * d + col];
-      P[e * d + col] = xt[v] * F[v];
-      if (XT) XT[e * d + col] = xt[v];
+      ft[v] = xt[v] * hj[v] + q[v] * xb[v];
+      p[v] = xt[v] * F[v];
     }
+    st_row<VPL>(Ft + e * d, l, ft);
+    st_row<VPL>(P + e * d, l, p);
+    if (XT) st_row<VPL>(XT + e * d, l, xt);
   }
 }
 

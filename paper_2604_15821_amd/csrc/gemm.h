@@ -29,8 +29,8 @@
 //
 // Epilogue: the accumulators are staged through LDS, 64 rows at a time, and
 // then visited row-major as float4, so every epilogue read and write of
-// global memory is a coalesced 512-byte row segment; a thread issues all of
-// its epilogue reads before it uses any of them.
+// global memory is a coalesced 512-byte row segment; a thread issues the
+// epilogue reads of four pieces before it uses any of them.
 #pragma once
 
 #include "common.h"
@@ -394,8 +394,8 @@ __global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float
 
   // Epilogue in two halves of 64 rows: the waves of row half `half` stage
   // their accumulators (lane l of block (bi, bj) holds column lr and rows
-  // 8 (v / 4) + 4 hf + v % 4), then every thread visits 8 float4 pieces:
-  // first all the epilogue's global reads, then the arithmetic and stores.
+  // 8 (v / 4) + 4 hf + v % 4), then every thread visits 8 float4 pieces in
+  // two batches: first the batch's global reads, then arithmetic and stores.
   float* sC = smem;
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
@@ -408,25 +408,30 @@ __global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float
           for (int v = 0; v < 16; ++v)
             sC[(bi * 32 + 8 * (v >> 2) + 4 * hf + (v & 3)) * LD_C + wn * 64 + bj * 32 + lr] = acc[bi][bj][v];
     }
-    typename Epi::Raw raw[8];
+    // 4 pieces per batch; loads past the range read the last valid row.
     const int c4 = tid & 31;
     const int col = n0 + 4 * c4;
+    const int colc = col < N ? col : N - 4;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const long long row = (long long)r0 + half * 64 + (tid >> 5) + 8 * i;
-      if (row < r1 && col < N) raw[i] = epi.load(row, col);
-    }
-    __syncthreads();
+    for (int i0 = 0; i0 < 8; i0 += 4) {
+      typename Epi::Raw raw[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int rl = (tid >> 5) + 8 * i;
-      const long long row = (long long)r0 + half * 64 + rl;
-      float part = 0.f;
-      if (row < r1 && col < N) part = epi.store(row, col, ld4(sC + rl * LD_C + 4 * c4), raw[i]);
-      if (Epi::kRowSum) {
+      for (int j = 0; j < 4; ++j) {
+        const long long row = (long long)r0 + half * 64 + (tid >> 5) + 8 * (i0 + j);
+        raw[j] = epi.load(row < r1 ? row : (long long)r1 - 1, colc);
+      }
+      if (i0 == 0) __syncthreads();
 #pragma unroll
-        for (int o = 16; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
-        if (c4 == 0 && row < r1) rowsum_out[row * gridDim.y + blockIdx.y] = part;
+      for (int j = 0; j < 4; ++j) {
+        const int rl = (tid >> 5) + 8 * (i0 + j);
+        const long long row = (long long)r0 + half * 64 + rl;
+        float part = 0.f;
+        if (row < r1 && col < N) part = epi.store(row, col, ld4(sC + rl * LD_C + 4 * c4), raw[j]);
+        if (Epi::kRowSum) {
+#pragma unroll
+          for (int o = 16; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+          if (c4 == 0 && row < r1) rowsum_out[row * gridDim.y + blockIdx.y] = part;
+        }
       }
     }
     __syncthreads();

@@ -328,6 +328,28 @@ __global__ void species_write_kernel(const int* __restrict__ species, int N, con
     }                                                                           \
   } while (0)
 
+// Same, for kernels that also take the number of choices per token (1..4).
+#define JANUS_LAUNCH_VK_(kern, V, K, grid, block, lds, st, ...) \
+  hipLaunchKernelGGL((kern<V, K>), grid, block, lds, st, __VA_ARGS__)
+#define JANUS_LAUNCH_K_(kern, V, k, grid, block, lds, st, ...)                           \
+  switch (k) {                                                                         \
+    case 1: JANUS_LAUNCH_VK_(kern, V, 1, grid, block, lds, st, __VA_ARGS__); break;      \
+    case 2: JANUS_LAUNCH_VK_(kern, V, 2, grid, block, lds, st, __VA_ARGS__); break;      \
+    case 3: JANUS_LAUNCH_VK_(kern, V, 3, grid, block, lds, st, __VA_ARGS__); break;      \
+    case 4: JANUS_LAUNCH_VK_(kern, V, 4, grid, block, lds, st, __VA_ARGS__); break;      \
+    default: break;                                                                    \
+  }
+#define LAUNCH_VPL_K(kern, d, k, grid, block, lds, st, ...)                              \
+  do {                                                                                 \
+    switch ((d) / 64) {                                                                \
+      case 1: JANUS_LAUNCH_K_(kern, 1, k, grid, block, lds, st, __VA_ARGS__); break;     \
+      case 2: JANUS_LAUNCH_K_(kern, 2, k, grid, block, lds, st, __VA_ARGS__); break;     \
+      case 4: JANUS_LAUNCH_K_(kern, 4, k, grid, block, lds, st, __VA_ARGS__); break;     \
+      case 8: JANUS_LAUNCH_K_(kern, 8, k, grid, block, lds, st, __VA_ARGS__); break;     \
+      default: break;                                                                  \
+    }                                                                                  \
+  } while (0)
+
 // h0_i = A[Z_i]
 __global__ void species_rows_gather_kernel(const float* __restrict__ A, const int* __restrict__ species, int N, int d,
                                            float* __restrict__ h) {
