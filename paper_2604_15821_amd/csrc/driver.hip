@@ -165,7 +165,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   const double by_gather = N * 4.0 * d + Ne * k * (8.0 + 4.0 * d);
   const double by_p2 = Ne * (4.0 * k * d + 4.0 * k + 8.0 * nb + 16.0 * d + 12.0);
   const double by_scatter = N * 12.0 * d + Ne * (4.0 + 4.0 * d);
-  const double by_p3 = Ne * (8.0 * nb + 16.0 * d + 8.0 + 4.0 * k + 4.0 * k * d);
+  const double by_p3 = Ne * (8.0 * nb + 16.0 * d + 8.0 + 4.0 * k + 4.0 * k * d) + (p.three ? Ne * 8.0 * d : 0.0);
   const double by_cp3 = N * 12.0 * d + Ne * k * (16.0 + 4.0 * d);
   const double by_p4 = Ne * (4.0 * k * d + 4.0 * k + 4.0 * nb + 20.0 * d);
 
@@ -257,10 +257,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   auto Y3bs = [&](int t) { return p.Y3bs + t * M3 * d; };
   auto Zbar3 = [&](int t) { return p.Zbar3 + t * Nt * d; };
   const size_t ldsWa = (size_t)nf * d * sizeof(float);
-  const dim3 gT = wave_grid(Nt);
   const double f_tri = 2.0 * M3 * d * h3;
   const double f_wa = 2.0 * Nt * nf * d;
-  const double by_tri = Nt * (8.0 * d + 4.0 * k3 * d + 24.0);
+  // per triplet: indices, cosine, u3, slot positions; per edge e2: segment, basis rows, h_j2
+  const double by_tri_idx = Nt * (16.0 + 4.0 * k3) + Ne * (8.0 + 4.0 * nb + 4.0 * d);
 
   // per-block views
   auto Xs = [&](int t) { return p.Xs + t * M * d; };
@@ -290,11 +290,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     if (three && Nt > 0) {
       // triplet tokens -> triplet experts -> messages Q_e of each edge's triplets
       {
-        PROF(PROF_EDGE, 0, by_tri);
-        LAUNCH_VPL(tri_dispatch_kernel, d, gT, b256, ldsWa, st, (const int*)p.te, (const int*)p.te2,
-                   (const float*)p.tc, (const float*)p.B3, (const float*)p.dB3, (const float*)p.u3,
-                   (const float*)p.du3, Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), POS3(t), k3, Nt, d,
-                   Z3s(t));
+        PROF(PROF_EDGE, 0, by_tri_idx + Nt * 4.0 * k3 * d);
+        LAUNCH_VPL_K(tri_dispatch_kernel, d, k3, gE, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+                     (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.u3,
+                     Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), POS3(t), Ne, d, Z3s(t));
       }
       {
         PROF(PROF_EXPERT_GEMM, f_tri, 0);
@@ -308,8 +307,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_EDGE, 0, Ne * 8.0 * d + M3 * 4.0 * d);
-        LAUNCH_VPL(tri_combine_kernel, d, gE, b256, 0, st, (const int*)p.trow, POS3(t), k3, (const float*)p.T3a, Ne,
-                   d, p.Q);
+        LAUNCH_VPL_K(tri_combine_kernel, d, k3, gE, b256, 0, st, (const int*)p.trow, POS3(t), (const float*)p.T3a,
+                     Ne, d, p.Q);
       }
     }
     if (Ne > 0) {
@@ -379,7 +378,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       // triplet messages' backward: Ybar3 = g3 Xbar_e -> experts -> Zbar; feature-geometry adjoints
       {
         PROF(PROF_EDGE, 0, Ne * 4.0 * d + M3 * 4.0 * d);
-        LAUNCH_VPL(tri_gather_kernel, d, gE, b256, 0, st, (const int*)p.trow, POS3(t), k3, GATE3(t),
+        LAUNCH_VPL_K(tri_gather_kernel, d, k3, gE, b256, 0, st, (const int*)p.trow, POS3(t), GATE3(t),
                    (const float*)Xbar(t), Ne, d, Y3bs(t));
       }
       {
@@ -393,13 +392,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                           EpiStore{p.T3a, d});
       }
       {
-        PROF(PROF_EDGE, 0, by_tri + Nt * 8.0 * d);
-        LAUNCH_VPL(tri_p2_kernel, d, gT, b256, ldsWa, st, (const int*)p.te, (const int*)p.te2, (const float*)p.tc,
-                   (const float*)p.B3, (const float*)p.dB3, (const float*)p.u3, (const float*)p.du3,
-                   Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), POS3(t), k3, Nt, d,
-                   (const float*)p.T3a, Zbar3(t), p.PT, p.tacc);
-        LAUNCH_VPL(tri_second_sum_kernel, d, gE, b256, 0, st, (const int*)p.trow, (const int*)p.trev,
-                   (const float*)p.PT, Ne, d, p.Pe);
+        PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 4.0 * d + 32.0) + Ne * (4.0 * nb + 8.0 * d));
+        LAUNCH_VPL_K(tri_p2_kernel, d, k3, gE, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+                     (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.dB3,
+                     (const float*)p.u3, (const float*)p.du3, Wp(blk(t, "W_a")), nb, L3, ej,
+                     (const float*)HV(p.h, t), POS3(t), Ne, d, (const float*)p.T3a, Zbar3(t), p.tacc, p.Pe);
       }
     }
     {
@@ -440,11 +437,12 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       const float* W1a = Wp(blk(t, "W1a"));
       const float* W2a = Wp(blk(t, "W2a"));
       {
-        PROF(PROF_EDGE, 0, by_tri + Nt * 12.0 * d);
-        LAUNCH_VPL(tri_p3_kernel, d, gT, b256, ldsWa, st, (const int*)p.te, (const int*)p.te2, (const float*)p.tc,
-                   (const float*)p.B3, (const float*)p.dB3, (const float*)p.u3, (const float*)p.du3,
-                   Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), hht_t, (const float4*)p.tct,
-                   (const float*)Zbar3(t), POS3(t), k3, Nt, d, p.T3a, p.VT, p.PT);
+        PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 8.0 * d + 20.0) + Ne * (4.0 * nb + 8.0 * d));
+        LAUNCH_VPL_K(tri_p3_kernel, d, k3, gE, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+                     (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.dB3,
+                     (const float*)p.u3, (const float*)p.du3, Wp(blk(t, "W_a")), nb, L3, ej,
+                     (const float*)HV(p.h, t), hht_t, (const float4*)p.tct, (const float*)Zbar3(t), POS3(t), Ne, d,
+                     p.T3a, p.VT, p.Pe);
       }
       {
         // dW_a (part 1): Gt^T (Zbar * h_j2)
@@ -473,20 +471,16 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_EDGE, 0, Ne * 8.0 * d + M3 * (8.0 + 4.0 * d));
-        LAUNCH_VPL(tri_combine_p3_kernel, d, gE, b256, 0, st, (const int*)p.trow, POS3(t), k3, GATE3(t),
+        LAUNCH_VPL_K(tri_combine_p3_kernel, d, k3, gE, b256, 0, st, (const int*)p.trow, POS3(t), GATE3(t),
                    (const float*)p.T3b, (const float*)Xbar(t), Ne, d, p.g3t + t * M3, p.Q);
       }
     }
     if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_p3);
+      // with triplets, P_e already holds the triplet part written by tri_p3
       LAUNCH_VPL_K(edge_p3_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
-                 (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)Xbar(t), hht_t, (const float*)p.rt,
-                 p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr));
-    }
-    if (tri_t) {
-      PROF(PROF_EDGE, 0, Ne * 8.0 * d + Nt * 4.0 * d);
-      LAUNCH_VPL(tri_second_sum_kernel, d, gE, b256, 0, st, (const int*)p.trow, (const int*)p.trev,
-                 (const float*)p.PT, Ne, d, p.Pe);
+                   (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)Xbar(t), hht_t, (const float*)p.rt,
+                   p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr), (int)tri_t);
     }
     {
       // dW_b (part 1): (rt B')^T Fbar
@@ -620,7 +614,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       const float* W2a = Wp(blk(t, "W2a"));
       {
         PROF(PROF_EDGE, 0, Ne * 4.0 * d + M3 * 4.0 * d);
-        LAUNCH_VPL(tri_gather_kernel, d, gE, b256, 0, st, (const int*)p.trow, POS3(t), k3, (const float*)nullptr,
+        LAUNCH_VPL_K(tri_gather_kernel, d, k3, gE, b256, 0, st, (const int*)p.trow, POS3(t), (const float*)nullptr,
                    (const float*)p.Q, Ne, d, p.T3a);
       }
       {
@@ -643,13 +637,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                      p.mc3, E3, p.partial, Gp(blk(t, "W2a")), 1);
       }
       {
-        PROF(PROF_EDGE, 0, by_tri + Nt * 8.0 * d);
-        LAUNCH_VPL(tri_p4_kernel, d, gT, b256, ldsWa, st, (const int*)p.te, (const int*)p.te2, (const float*)p.tc,
-                   (const float*)p.B3, (const float*)p.dB3, (const float*)p.u3, (const float*)p.du3,
-                   Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), hht_t, (const float*)Zbar3(t), POS3(t),
-                   k3, Nt, d, (const float*)p.T3b, p.VT, p.PT);
-        LAUNCH_VPL(tri_second_sum_kernel, d, gE, b256, 0, st, (const int*)p.trow, (const int*)p.trev,
-                   (const float*)p.PT, Ne, d, p.Pe);
+        PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 8.0 * d) + Ne * 12.0 * d);
+        LAUNCH_VPL_K(tri_p4_kernel, d, k3, gE, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+                     (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.u3,
+                     Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), hht_t, (const float*)Zbar3(t),
+                     POS3(t), Ne, d, (const float*)p.T3b, p.VT, p.Pe);
       }
       {
         // dW_a (part 2): G^T (Zt * h_j2 + Q * Zbar)
@@ -662,10 +654,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_OTHER, 0, 0);
         hipLaunchKernelGGL(gate_total_kernel, dim3(cdiv(M3, 256)), b256, 0, st, (const float*)(p.g3t + t * M3),
                            (const float*)p.gpart3, POS3(t), M3, p.ntile3, p.gt3);
-        hipLaunchKernelGGL(tri_router_edge_kernel, gE, b256, 0, st, (const int*)p.trow, (const int*)p.trev, E3, k3,
-                           species, ei, ej, (const int*)p.te, (const int*)p.te2, Wp(blk(t, "P3a")),
-                           Wp(blk(t, "P3b")), Wp(blk(t, "P3c")), Wp(blk(t, "beta3")),
-                           (const int*)(p.eid3 + t * M3), (const float*)p.gt3, Ne, p.LB, p.LC);
+        hipLaunchKernelGGL(tri_logit_kernel, dim3(cdiv(Nt, 256)), b256, 0, st, species, ei, ej, (const int*)p.te,
+                           (const int*)p.te2, Nt, Wp(blk(t, "P3a")), Wp(blk(t, "P3b")), Wp(blk(t, "P3c")),
+                           Wp(blk(t, "beta3")), E3, k3, (const int*)(p.eid3 + t * M3), (const float*)p.gt3, p.LT3);
+        hipLaunchKernelGGL(tri_router_edge_kernel, dim3(cdiv(Ne * E3, 256)), b256, 0, st, (const int*)p.trow,
+                           (const int*)p.trev, E3, (const float*)p.LT3, Ne, p.LB, p.LC);
         hipLaunchKernelGGL(tri_router_atom_kernel, gN, b256, 0, st, rowptr, rev, E3, (const float*)p.LB,
                            (const float*)p.LC, N, p.pa, p.pb, p.pc);
         hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,

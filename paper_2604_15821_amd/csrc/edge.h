@@ -13,8 +13,8 @@
 // reverse-edge map.  No kernel uses floating-point atomics.
 //
 // Memory access: the wave's item index is wave-uniform (readfirstlane), so
-// per-item indices (pos, ej, rev, gates, segment bounds) are scalar loads;
-// a feature row of d = 64 VPL floats is read or written by the whole wave in
+// per-item indices (pos, ej, rev, gates, segment bounds) are one address for
+// the whole wave; a feature row of d = 64 VPL floats is read or written by the whole wave in
 // VPL / W accesses of W = min(VPL, 4) consecutive floats per lane (Lanes),
 // each covering one contiguous 256 W-byte segment.  The k slot rows of an
 // edge (k is a template argument, 1..4) and, in the per-atom sums, the rows
@@ -268,14 +268,15 @@ __global__ void scatter_rev_kernel(const int* __restrict__ rowptr, const int* __
 }
 
 // Phase 3 per edge (adjoints of the force backward):
-//   Fbt = rt_e F'_e,  Xbt = Q_e * F_e + Fbt * h_j  (Q_e = adjoint of hbar^t at j),
-//   Xbt copied to the k slots; P_e = Fbt * Xbar_e  (routed to h_j).
+//   Fbt = rt_e F'_e,  Xbt = Q_e * F_e + Fbt * h_j (+ QX_e)  (Q_e = adjoint of hbar^t at j),
+//   Xbt copied to the k slots; P_e = Fbt * Xbar_e  (routed to h_j), added to
+//   the P_e already stored when accP is set.
 template <int VPL, int KC>
 __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restrict__ dB, int nb,
                                const float* __restrict__ Wb, const float* __restrict__ h, const int* __restrict__ ej,
                                const int* __restrict__ pos, long long Ne, int d, const float* __restrict__ Xbar,
                                const float* __restrict__ hht, const float* __restrict__ rt, float* __restrict__ Xbts,
-                               float* __restrict__ P, const float* __restrict__ QX) {
+                               float* __restrict__ P, const float* __restrict__ QX, int accP) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
@@ -291,11 +292,12 @@ __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restr
     filter_row<VPL>(bl, sW, nb, d, l, F);
     filter_row<VPL>(dbl, sW, nb, d, l, Fp);
     float X[VPL], p[VPL];
+    if (accP) ld_row<VPL>(P + e * d, l, p); else zero_row<VPL>(p);
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
       const float fbt = r * Fp[v];
       X[v] = q[v] * F[v] + fbt * hj[v] + qx[v];
-      p[v] = fbt * xb[v];
+      p[v] += fbt * xb[v];
     }
     st_row<VPL>(P + e * d, l, p);
 #pragma unroll

@@ -164,203 +164,261 @@ __global__ void tri_route_kernel(const int* __restrict__ species, const int* __r
 }
 
 // ---------------------------------------------------------------- feature rows
+//
+// The expert-token kernels run one wave per second edge e2: the sums
+//   s_l = sum_n B3_n(r_e2) W_a[l Nb + n, :]   (and s'_l with B3')
+// depend on e2 only, so they are formed once per edge; each triplet
+// tau = (e, e2) then needs only its Legendre values P_l(c_tau) and u3(r_e).
+// The triplets whose second edge is e2 are trev[tseg(e2)]; their indices,
+// cosines, u3 values and slot positions are loaded one triplet per lane, 64
+// at a time, and broadcast with readlane.
 
-// Per lane (columns v*64 + l): the four products of the features with W_a
-// (shared memory sWa [L*Nb, d]) for one triplet.
+__device__ __forceinline__ float bcast(float x, int q) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), q));
+}
+__device__ __forceinline__ int bcast(int x, int q) { return __builtin_amdgcn_readlane(x, q); }
+
+// Legendre values and derivatives P_q(c), P'_q(c) for q < kMaxL (Bonnet's recursion).
+__device__ __forceinline__ void legendre_all(float c, float (&P)[kMaxL], float (&dP)[kMaxL]) {
+  P[0] = 1.f;
+  dP[0] = 0.f;
+  P[1] = c;
+  dP[1] = 1.f;
+#pragma unroll
+  for (int q = 1; q + 1 < kMaxL; ++q) {
+    P[q + 1] = ((2 * q + 1) * c * P[q] - q * P[q - 1]) / (q + 1);
+    dP[q + 1] = (q + 1) * P[q] + c * dP[q];
+  }
+}
+
+// s[q] = sum_n b_n sWa[(q Nb + n), cols of lane l] for q < L; b held one value per lane.
 template <int VPL>
-struct TriRows {
-  float z[VPL];    // G W_a
-  float wc[VPL];   // dG/dc W_a
-  float w1[VPL];   // dG/dr1 W_a
-  float w2[VPL];   // dG/dr2 W_a
-};
-
-template <int VPL, bool DERIV>
-__device__ __forceinline__ void tri_rows(long long t, const int* __restrict__ te, const int* __restrict__ te2,
-                                         const float* __restrict__ tc, const float* __restrict__ B3,
-                                         const float* __restrict__ dB3, const float* __restrict__ u3,
-                                         const float* __restrict__ du3, const float* sWa, int nb, int L, int d, int l,
-                                         TriRows<VPL>& o) {
-  const int e1 = te[t], e2 = te2[t];
-  float P[kMaxL], dP[kMaxL];
-  legendre_d(tc[t], L, P, dP);
-  const float* b3 = B3 + (long long)e2 * nb;
-  const float* db3 = dB3 + (long long)e2 * nb;
-  float s[VPL], sp[VPL];
+__device__ __forceinline__ void feat_sums(float b_lane, const float* sWa, int nb, int L, int d, int l,
+                                          float (&s)[kMaxL][VPL]) {
 #pragma unroll
-  for (int v = 0; v < VPL; ++v) o.z[v] = o.wc[v] = o.w1[v] = o.w2[v] = 0.f;
-  for (int q = 0; q < L; ++q) {
+  for (int q = 0; q < kMaxL; ++q) zero_row<VPL>(s[q]);
+  for (int n = 0; n < nb; ++n) {
+    const float b = bcast(b_lane, n);
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) s[v] = sp[v] = 0.f;
-    for (int n = 0; n < nb; ++n) {
-      const float bn = b3[n], dbn = DERIV ? db3[n] : 0.f;
+    for (int q = 0; q < kMaxL; ++q) {
+      if (q < L) {
+        float w[VPL];
+        ld_row<VPL>(sWa + (q * nb + n) * d, l, w);
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) {
-        const float w = sWa[(q * nb + n) * d + v * 64 + l];
-        s[v] += bn * w;
-        if (DERIV) sp[v] += dbn * w;
-      }
-    }
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      o.z[v] += P[q] * s[v];
-      if (DERIV) {
-        o.wc[v] += dP[q] * s[v];
-        o.w2[v] += P[q] * sp[v];
+        for (int v = 0; v < VPL; ++v) s[q][v] += b * w[v];
       }
     }
   }
-  const float u = u3[e1], du = du3[e1];
+}
+
+// Per-triplet scalars of up to 64 triplets trev[tb + lane] (tb + lane < t1),
+// one triplet per lane.
+template <int KC>
+struct TriLane {
+  int tau;
+  float c, u, du;
+  int pos[KC];
+  __device__ __forceinline__ void load(const int* __restrict__ trev, const int* __restrict__ te,
+                                       const float* __restrict__ tc, const float* __restrict__ u3,
+                                       const float* __restrict__ du3, const int* __restrict__ pos3, int tb, int t1,
+                                       int l) {
+    const int tl = tb + l < t1 ? tb + l : t1 - 1;
+    tau = trev[tl];
+    c = tc[tau];
+    const int e1 = te[tau];
+    u = u3[e1];
+    du = du3 ? du3[e1] : 0.f;
+#pragma unroll
+    for (int k = 0; k < KC; ++k) pos[k] = pos3[(long long)tau * KC + k];
+  }
+};
+
+// (G W_a) row of one triplet and, with DERIV, (dG/dc W_a), (dG/dr1 W_a), (dG/dr2 W_a).
+template <int VPL, bool DERIV>
+__device__ __forceinline__ void tri_feat(float c, float u, float du, int L, const float (&s)[kMaxL][VPL],
+                                         const float (&sp)[kMaxL][VPL], float (&z)[VPL], float (&wc)[VPL],
+                                         float (&w1)[VPL], float (&w2)[VPL]) {
+  float P[kMaxL], dP[kMaxL];
+  legendre_all(c, P, dP);
+  zero_row<VPL>(z);
+  if (DERIV) {
+    zero_row<VPL>(wc);
+    zero_row<VPL>(w2);
+  }
+#pragma unroll
+  for (int q = 0; q < kMaxL; ++q) {
+    if (q < L) {
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) {
+        z[v] += P[q] * s[q][v];
+        if (DERIV) {
+          wc[v] += dP[q] * s[q][v];
+          w2[v] += P[q] * sp[q][v];
+        }
+      }
+    }
+  }
 #pragma unroll
   for (int v = 0; v < VPL; ++v) {
     if (DERIV) {
-      o.w1[v] = du * o.z[v];
-      o.wc[v] *= u;
-      o.w2[v] *= u;
+      w1[v] = du * z[v];
+      wc[v] *= u;
+      w2[v] *= u;
     }
-    o.z[v] *= u;
+    z[v] *= u;
   }
 }
 
 // ---------------------------------------------------------------- phase 1
 
-// Z = (G W_a) * h_{j(e2)} into the triplet expert slots.
-template <int VPL>
-__global__ void tri_dispatch_kernel(const int* __restrict__ te, const int* __restrict__ te2,
-                                    const float* __restrict__ tc, const float* __restrict__ B3,
-                                    const float* __restrict__ dB3, const float* __restrict__ u3,
-                                    const float* __restrict__ du3, const float* __restrict__ Wa, int nb, int L,
-                                    const int* __restrict__ ej, const float* __restrict__ h,
-                                    const int* __restrict__ pos3, int k3, long long Nt, int d,
+// Z_tau = (G W_a) * h_{j(e2)} into the triplet expert slots.
+template <int VPL, int KC>
+__global__ void tri_dispatch_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
+                                    const int* __restrict__ te, const float* __restrict__ tc,
+                                    const float* __restrict__ B3, const float* __restrict__ u3,
+                                    const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
+                                    const float* __restrict__ h, const int* __restrict__ pos3, long long Ne, int d,
                                     float* __restrict__ Zs) {
   extern __shared__ float sWa[];
   load_lds(sWa, Wa, L * nb * d);
-  JANUS_WAVE_LOOP(t, Nt) {
-    TriRows<VPL> o;
-    tri_rows<VPL, false>(t, te, te2, tc, B3, dB3, u3, du3, sWa, nb, L, d, l, o);
-    const float* hj = h + (long long)ej[te2[t]] * d;
-    float Z[VPL];
+  JANUS_WAVE_LOOP(e2, Ne) {
+    const int t0 = trowptr[e2], t1 = trowptr[e2 + 1];
+    if (t0 == t1) continue;
+    float s[kMaxL][VPL], hj[VPL];
+    feat_sums<VPL>(basis_lane(B3, e2, nb, l), sWa, nb, L, d, l, s);
+    ld_row<VPL>(h + (long long)ej[e2] * d, l, hj);
+    for (int tb = t0; tb < t1; tb += 64) {
+      TriLane<KC> tl;
+      tl.load(trev, te, tc, u3, nullptr, pos3, tb, t1, l);
+      const int n = t1 - tb < 64 ? t1 - tb : 64;
+      for (int q = 0; q < n; ++q) {
+        float z[VPL], wc[VPL], w1[VPL], w2[VPL];
+        tri_feat<VPL, false>(bcast(tl.c, q), bcast(tl.u, q), 0.f, L, s, s, z, wc, w1, w2);
+        float Z[VPL];
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) Z[v] = o.z[v] * hj[v * 64 + l];
-    for (int c = 0; c < k3; ++c) {
-      float* out = Zs + (long long)pos3[t * k3 + c] * d;
+        for (int v = 0; v < VPL; ++v) Z[v] = z[v] * hj[v];
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) out[v * 64 + l] = Z[v];
+        for (int k = 0; k < KC; ++k) st_row<VPL>(Zs + (long long)bcast(tl.pos[k], q) * d, l, Z);
+      }
     }
   }
 }
 
 // Q_e = sum_{tau in tseg(e)} sum_c Y3g[pos3[tau, c]]  (gated triplet messages).
-template <int VPL>
-__global__ void tri_combine_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3, int k3,
+template <int VPL, int KC>
+__global__ void tri_combine_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3,
                                    const float* __restrict__ Yg, long long Ne, int d, float* __restrict__ Q) {
   JANUS_WAVE_LOOP(e, Ne) {
     float acc[VPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) acc[v] = 0.f;
-    for (int t = trowptr[e]; t < trowptr[e + 1]; ++t)
-      for (int c = 0; c < k3; ++c) {
-        const float* y = Yg + (long long)pos3[(long long)t * k3 + c] * d;
-#pragma unroll
-        for (int v = 0; v < VPL; ++v) acc[v] += y[v * 64 + l];
-      }
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) Q[e * d + v * 64 + l] = acc[v];
+    zero_row<VPL>(acc);
+    const int t0 = trowptr[e], t1 = trowptr[e + 1];
+    int t = t0;
+    for (; t + 2 <= t1; t += 2) {
+      float y0[VPL], y1[VPL];
+      sum_slots<VPL, KC>(Yg, pos3, t, d, l, y0);
+      sum_slots<VPL, KC>(Yg, pos3, t + 1, d, l, y1);
+      add_row<VPL>(acc, y0);
+      add_row<VPL>(acc, y1);
+    }
+    if (t < t1) {
+      float y0[VPL];
+      sum_slots<VPL, KC>(Yg, pos3, t, d, l, y0);
+      add_row<VPL>(acc, y0);
+    }
+    st_row<VPL>(Q + e * d, l, acc);
   }
 }
 
 // Slot rows of an edge adjoint for the triplets of the edge:
 // out[pos3[tau, c]] = (g3_tau,c) * src[e],  tau in tseg(e).
-template <int VPL>
-__global__ void tri_gather_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3, int k3,
+template <int VPL, int KC>
+__global__ void tri_gather_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3,
                                   const float* __restrict__ gate3, const float* __restrict__ src, long long Ne, int d,
                                   float* __restrict__ out) {
   JANUS_WAVE_LOOP(e, Ne) {
     const int t0 = trowptr[e], t1 = trowptr[e + 1];
     if (t0 == t1) continue;
     float s[VPL];
+    ld_row<VPL>(src + e * d, l, s);
+    for (int t = t0; t < t1; ++t) {
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) s[v] = src[e * d + v * 64 + l];
-    for (int t = t0; t < t1; ++t)
-      for (int c = 0; c < k3; ++c) {
-        const long long f = (long long)t * k3 + c;
+      for (int k = 0; k < KC; ++k) {
+        const long long f = (long long)t * KC + k;
         const float g = gate3 ? gate3[f] : 1.f;
-        float* o = out + (long long)pos3[f] * d;
+        float o[VPL];
 #pragma unroll
-        for (int v = 0; v < VPL; ++v) o[v * 64 + l] = g * s[v];
+        for (int v = 0; v < VPL; ++v) o[v] = g * s[v];
+        st_row<VPL>(out + (long long)pos3[f] * d, l, o);
       }
+    }
   }
 }
 
 // ---------------------------------------------------------------- phase 2
 
-// Per triplet: Zbar = sum_c Zbar_slot; keep it; PT = Zbar * (G W_a) (routed to
-// h_{j(e2)}); accumulate the feature-geometry adjoints
-//   acc += (Zbar * h_j2) . (dG/dc W_a, dG/dr1 W_a, dG/dr2 W_a).
-template <int VPL>
-__global__ void tri_p2_kernel(const int* __restrict__ te, const int* __restrict__ te2, const float* __restrict__ tc,
+// Per triplet tau = (e, e2): Zbar = sum_c Zbar_slot (kept); the feature-
+// geometry adjoints acc[tau] += (Zbar * h_j2) . (dG/dc W_a, dG/dr1 W_a, dG/dr2 W_a);
+// and P[e2] += sum over the triplets of e2 of Zbar * (G W_a) (routed to h_j2),
+// added in trev[tseg(e2)] order.
+template <int VPL, int KC>
+__global__ void tri_p2_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
+                              const int* __restrict__ te, const float* __restrict__ tc,
                               const float* __restrict__ B3, const float* __restrict__ dB3,
                               const float* __restrict__ u3, const float* __restrict__ du3,
                               const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
-                              const float* __restrict__ h, const int* __restrict__ pos3, int k3, long long Nt, int d,
-                              const float* __restrict__ Zbs, float* __restrict__ Zbar, float* __restrict__ PT,
-                              float4* __restrict__ acc) {
+                              const float* __restrict__ h, const int* __restrict__ pos3, long long Ne, int d,
+                              const float* __restrict__ Zbs, float* __restrict__ Zbar, float4* __restrict__ acc,
+                              float* __restrict__ P) {
   extern __shared__ float sWa[];
   load_lds(sWa, Wa, L * nb * d);
-  JANUS_WAVE_LOOP(t, Nt) {
-    float zb[VPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) zb[v] = 0.f;
-    for (int c = 0; c < k3; ++c) {
-      const float* y = Zbs + (long long)pos3[t * k3 + c] * d;
-#pragma unroll
-      for (int v = 0; v < VPL; ++v) zb[v] += y[v * 64 + l];
-    }
-    TriRows<VPL> o;
-    tri_rows<VPL, true>(t, te, te2, tc, B3, dB3, u3, du3, sWa, nb, L, d, l, o);
-    const float* hj = h + (long long)ej[te2[t]] * d;
-    float ac = 0.f, a1 = 0.f, a2 = 0.f;
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      const long long q = t * d + v * 64 + l;
-      Zbar[q] = zb[v];
-      PT[q] = zb[v] * o.z[v];
-      const float w = zb[v] * hj[v * 64 + l];
-      ac += w * o.wc[v];
-      a1 += w * o.w1[v];
-      a2 += w * o.w2[v];
-    }
-    ac = wave_sum(ac);
-    a1 = wave_sum(a1);
-    a2 = wave_sum(a2);
-    if (l == 0) {
-      float4 s = acc[t];
-      s.x += ac;
-      s.y += a1;
-      s.z += a2;
-      acc[t] = s;
-    }
-  }
-}
-
-// P[e] += sum over the triplets whose second edge is e of PT:
-// sum_{tau' in tseg(e)} PT[trev[tau']].
-template <int VPL>
-__global__ void tri_second_sum_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
-                                      const float* __restrict__ PT, long long Ne, int d, float* __restrict__ P) {
-  JANUS_WAVE_LOOP(e, Ne) {
-    const int t0 = trowptr[e], t1 = trowptr[e + 1];
+  JANUS_WAVE_LOOP(e2, Ne) {
+    const int t0 = trowptr[e2], t1 = trowptr[e2 + 1];
     if (t0 == t1) continue;
-    float acc[VPL];
+    float s[kMaxL][VPL], sp[kMaxL][VPL], hj[VPL], pr[VPL];
+    feat_sums<VPL>(basis_lane(B3, e2, nb, l), sWa, nb, L, d, l, s);
+    feat_sums<VPL>(basis_lane(dB3, e2, nb, l), sWa, nb, L, d, l, sp);
+    ld_row<VPL>(h + (long long)ej[e2] * d, l, hj);
+    ld_row<VPL>(P + e2 * d, l, pr);
+    for (int tb = t0; tb < t1; tb += 64) {
+      TriLane<KC> tl;
+      tl.load(trev, te, tc, u3, du3, pos3, tb, t1, l);
+      const int n = t1 - tb < 64 ? t1 - tb : 64;
+      for (int q = 0; q < n; ++q) {
+        const long long t = bcast(tl.tau, q);
+        float zb[VPL];
+        {
+          float r[KC][VPL];
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) acc[v] = P[e * d + v * 64 + l];
-    for (int t = t0; t < t1; ++t) {
-      const float* p = PT + (long long)trev[t] * d;
+          for (int k = 0; k < KC; ++k) ld_row<VPL>(Zbs + (long long)bcast(tl.pos[k], q) * d, l, r[k]);
+          zero_row<VPL>(zb);
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) acc[v] += p[v * 64 + l];
+          for (int k = 0; k < KC; ++k) add_row<VPL>(zb, r[k]);
+        }
+        float z[VPL], wc[VPL], w1[VPL], w2[VPL];
+        tri_feat<VPL, true>(bcast(tl.c, q), bcast(tl.u, q), bcast(tl.du, q), L, s, sp, z, wc, w1, w2);
+        st_row<VPL>(Zbar + t * d, l, zb);
+        float ac = 0.f, a1 = 0.f, a2 = 0.f;
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          pr[v] += zb[v] * z[v];
+          const float w = zb[v] * hj[v];
+          ac += w * wc[v];
+          a1 += w * w1[v];
+          a2 += w * w2[v];
+        }
+        ac = wave_sum(ac);
+        a1 = wave_sum(a1);
+        a2 = wave_sum(a2);
+        if (l == 0) {
+          float4 g = acc[t];
+          g.x += ac;
+          g.y += a1;
+          g.z += a2;
+          acc[t] = g;
+        }
+      }
     }
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) P[e * d + v * 64 + l] = acc[v];
+    st_row<VPL>(P + e2 * d, l, pr);
   }
 }
 
@@ -421,164 +479,204 @@ __global__ void tri_ctilde_kernel(const int* __restrict__ te, const int* __restr
   ct[t] = make_float4(acx, rt[e], rt[e2], 0.f);
 }
 
-// Double backward per triplet (Q = loss adjoint of hbar^t at j(e2), may be null):
+// Double backward per triplet tau = (e, e2) (Q = loss adjoint of hbar^t at
+// j(e2), may be null):
 //   vt   = ct . (dG W_a)            (adjoint of Zbar * h_j2)
 //   Zbt  = vt * h_j2 + Q * (G W_a)  -> slots of the triplet
 //   V    = Zbar * h_j2              (dW_a += Gt^T V)
-//   PT   = vt * Zbar                (routed to h_{j(e2)})
-template <int VPL>
-__global__ void tri_p3_kernel(const int* __restrict__ te, const int* __restrict__ te2, const float* __restrict__ tc,
+// and P[e2] = sum over the triplets of e2 of vt * Zbar (routed to h_j2),
+// written for every edge (zero without triplets).
+template <int VPL, int KC>
+__global__ void tri_p3_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
+                              const int* __restrict__ te, const float* __restrict__ tc,
                               const float* __restrict__ B3, const float* __restrict__ dB3,
                               const float* __restrict__ u3, const float* __restrict__ du3,
                               const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
                               const float* __restrict__ h, const float* __restrict__ hht,
                               const float4* __restrict__ ct, const float* __restrict__ Zbar,
-                              const int* __restrict__ pos3, int k3, long long Nt, int d, float* __restrict__ Zbts,
-                              float* __restrict__ V, float* __restrict__ PT) {
+                              const int* __restrict__ pos3, long long Ne, int d, float* __restrict__ Zbts,
+                              float* __restrict__ V, float* __restrict__ P) {
   extern __shared__ float sWa[];
   load_lds(sWa, Wa, L * nb * d);
-  JANUS_WAVE_LOOP(t, Nt) {
-    TriRows<VPL> o;
-    tri_rows<VPL, true>(t, te, te2, tc, B3, dB3, u3, du3, sWa, nb, L, d, l, o);
-    const long long j2 = ej[te2[t]];
-    const float4 cf = ct[t];
-    float Zb[VPL];
+  JANUS_WAVE_LOOP(e2, Ne) {
+    const int t0 = trowptr[e2], t1 = trowptr[e2 + 1];
+    float pr[VPL];
+    zero_row<VPL>(pr);
+    if (t0 < t1) {
+      float s[kMaxL][VPL], sp[kMaxL][VPL], hj[VPL], qh[VPL];
+      feat_sums<VPL>(basis_lane(B3, e2, nb, l), sWa, nb, L, d, l, s);
+      feat_sums<VPL>(basis_lane(dB3, e2, nb, l), sWa, nb, L, d, l, sp);
+      const long long j2 = ej[e2];
+      ld_row<VPL>(h + j2 * d, l, hj);
+      if (hht) ld_row<VPL>(hht + j2 * d, l, qh); else zero_row<VPL>(qh);
+      for (int tb = t0; tb < t1; tb += 64) {
+        TriLane<KC> tl;
+        tl.load(trev, te, tc, u3, du3, pos3, tb, t1, l);
+        const float4 cl = ct[tl.tau];
+        const int n = t1 - tb < 64 ? t1 - tb : 64;
+        for (int q = 0; q < n; ++q) {
+          const long long t = bcast(tl.tau, q);
+          float zb[VPL];
+          ld_row<VPL>(Zbar + t * d, l, zb);
+          float z[VPL], wc[VPL], w1[VPL], w2[VPL];
+          tri_feat<VPL, true>(bcast(tl.c, q), bcast(tl.u, q), bcast(tl.du, q), L, s, sp, z, wc, w1, w2);
+          const float cx = bcast(cl.x, q), cy = bcast(cl.y, q), cz = bcast(cl.z, q);
+          float Zb[VPL], vv[VPL];
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      const int col = v * 64 + l;
-      const float zb = Zbar[t * d + col], hj = h[j2 * d + col];
-      const float q = hht ? hht[j2 * d + col] : 0.f;
-      const float vt = cf.x * o.wc[v] + cf.y * o.w1[v] + cf.z * o.w2[v];
-      Zb[v] = vt * hj + q * o.z[v];
-      V[t * d + col] = zb * hj;
-      PT[t * d + col] = vt * zb;
-    }
-    for (int c = 0; c < k3; ++c) {
-      float* out = Zbts + (long long)pos3[t * k3 + c] * d;
+          for (int v = 0; v < VPL; ++v) {
+            const float vt = cx * wc[v] + cy * w1[v] + cz * w2[v];
+            Zb[v] = vt * hj[v] + qh[v] * z[v];
+            vv[v] = zb[v] * hj[v];
+            pr[v] += vt * zb[v];
+          }
+          st_row<VPL>(V + t * d, l, vv);
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) out[v * 64 + l] = Zb[v];
+          for (int k = 0; k < KC; ++k) st_row<VPL>(Zbts + (long long)bcast(tl.pos[k], q) * d, l, Zb);
+        }
+      }
     }
+    st_row<VPL>(P + e2 * d, l, pr);
   }
 }
 
 // Per edge, double backward of the triplet gather: gate adjoints
 // g3t[tau, c] = Ybt3[pos3] . Xbar_e and QX_e = sum_tau sum_c g3 Ybt3[pos3].
-template <int VPL>
-__global__ void tri_combine_p3_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3, int k3,
+template <int VPL, int KC>
+__global__ void tri_combine_p3_kernel(const int* __restrict__ trowptr, const int* __restrict__ pos3,
                                       const float* __restrict__ gate3, const float* __restrict__ Ybt3,
                                       const float* __restrict__ Xbar, long long Ne, int d, float* __restrict__ g3t,
                                       float* __restrict__ QX) {
   JANUS_WAVE_LOOP(e, Ne) {
     float xb[VPL], acc[VPL];
+    ld_row<VPL>(Xbar + e * d, l, xb);
+    zero_row<VPL>(acc);
+    const int t0 = trowptr[e], t1 = trowptr[e + 1];
+    for (int t = t0; t < t1; ++t) {
+      float y[KC][VPL];
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      xb[v] = Xbar[e * d + v * 64 + l];
-      acc[v] = 0.f;
-    }
-    for (int t = trowptr[e]; t < trowptr[e + 1]; ++t)
-      for (int c = 0; c < k3; ++c) {
-        const long long f = (long long)t * k3 + c;
-        const float* y = Ybt3 + (long long)pos3[f] * d;
-        const float g = gate3[f];
-        float s = 0.f;
+      for (int k = 0; k < KC; ++k) ld_row<VPL>(Ybt3 + (long long)pos3[(long long)t * KC + k] * d, l, y[k]);
+      float s[KC];
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const float g = gate3[(long long)t * KC + k];
+        s[k] = 0.f;
 #pragma unroll
         for (int v = 0; v < VPL; ++v) {
-          const float yv = y[v * 64 + l];
-          s += yv * xb[v];
-          acc[v] += g * yv;
+          s[k] += y[k][v] * xb[v];
+          acc[v] += g * y[k][v];
         }
-        s = wave_sum(s);
-        if (l == 0) g3t[f] = s;
       }
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) QX[e * d + v * 64 + l] = acc[v];
+      for (int k = 0; k < KC; ++k) s[k] = wave_sum(s[k]);
+      if (l == 0) {
+#pragma unroll
+        for (int k = 0; k < KC; ++k) g3t[(long long)t * KC + k] = s[k];
+      }
+    }
+    st_row<VPL>(QX + e * d, l, acc);
   }
 }
 
 // ---------------------------------------------------------------- phase 4
 
-// Per triplet, final backward: Zt = sum_c Zt_slot;
+// Per triplet tau = (e, e2), final backward: Zt = sum_c Zt_slot;
 //   ZP = Zt * h_j2 + Q * Zbar   (loss adjoint of G W_a; dW_a += G^T ZP)
-//   PT = Zt * (G W_a)            (routed to h_{j(e2)})
-template <int VPL>
-__global__ void tri_p4_kernel(const int* __restrict__ te, const int* __restrict__ te2, const float* __restrict__ tc,
-                              const float* __restrict__ B3, const float* __restrict__ dB3,
-                              const float* __restrict__ u3, const float* __restrict__ du3,
+// and P[e2] += sum over the triplets of e2 of Zt * (G W_a) (routed to h_j2).
+template <int VPL, int KC>
+__global__ void tri_p4_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
+                              const int* __restrict__ te, const float* __restrict__ tc,
+                              const float* __restrict__ B3, const float* __restrict__ u3,
                               const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
                               const float* __restrict__ h, const float* __restrict__ hht,
-                              const float* __restrict__ Zbar, const int* __restrict__ pos3, int k3, long long Nt,
-                              int d, const float* __restrict__ Zts, float* __restrict__ ZP, float* __restrict__ PT) {
+                              const float* __restrict__ Zbar, const int* __restrict__ pos3, long long Ne, int d,
+                              const float* __restrict__ Zts, float* __restrict__ ZP, float* __restrict__ P) {
   extern __shared__ float sWa[];
   load_lds(sWa, Wa, L * nb * d);
-  JANUS_WAVE_LOOP(t, Nt) {
-    float zt[VPL];
+  JANUS_WAVE_LOOP(e2, Ne) {
+    const int t0 = trowptr[e2], t1 = trowptr[e2 + 1];
+    if (t0 == t1) continue;
+    float s[kMaxL][VPL], hj[VPL], qh[VPL], pr[VPL];
+    feat_sums<VPL>(basis_lane(B3, e2, nb, l), sWa, nb, L, d, l, s);
+    const long long j2 = ej[e2];
+    ld_row<VPL>(h + j2 * d, l, hj);
+    if (hht) ld_row<VPL>(hht + j2 * d, l, qh); else zero_row<VPL>(qh);
+    ld_row<VPL>(P + e2 * d, l, pr);
+    for (int tb = t0; tb < t1; tb += 64) {
+      TriLane<KC> tl;
+      tl.load(trev, te, tc, u3, nullptr, pos3, tb, t1, l);
+      const int n = t1 - tb < 64 ? t1 - tb : 64;
+      for (int q = 0; q < n; ++q) {
+        const long long t = bcast(tl.tau, q);
+        float zt[VPL], zb[VPL];
+        {
+          float r[KC][VPL];
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) zt[v] = 0.f;
-    for (int c = 0; c < k3; ++c) {
-      const float* y = Zts + (long long)pos3[t * k3 + c] * d;
+          for (int k = 0; k < KC; ++k) ld_row<VPL>(Zts + (long long)bcast(tl.pos[k], q) * d, l, r[k]);
+          ld_row<VPL>(Zbar + t * d, l, zb);
+          zero_row<VPL>(zt);
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) zt[v] += y[v * 64 + l];
+          for (int k = 0; k < KC; ++k) add_row<VPL>(zt, r[k]);
+        }
+        float z[VPL], wc[VPL], w1[VPL], w2[VPL];
+        tri_feat<VPL, false>(bcast(tl.c, q), bcast(tl.u, q), 0.f, L, s, s, z, wc, w1, w2);
+        float zp[VPL];
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          zp[v] = zt[v] * hj[v] + qh[v] * zb[v];
+          pr[v] += zt[v] * z[v];
+        }
+        st_row<VPL>(ZP + t * d, l, zp);
+      }
     }
-    TriRows<VPL> o;
-    tri_rows<VPL, false>(t, te, te2, tc, B3, dB3, u3, du3, sWa, nb, L, d, l, o);
-    const long long j2 = ej[te2[t]];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      const int col = v * 64 + l;
-      const float q = hht ? hht[j2 * d + col] : 0.f;
-      ZP[t * d + col] = zt[v] * h[j2 * d + col] + q * Zbar[t * d + col];
-      PT[t * d + col] = zt[v] * o.z[v];
-    }
+    st_row<VPL>(P + e2 * d, l, pr);
   }
 }
 
-// Loss adjoint of the triplet router logits (lane x = expert x), recomputed
-// from the tables: lt[x] = p[x] (pt[x] - sum_y p[y] pt[y]).
-__device__ __forceinline__ float tri_logit_adjoint(long long t, int lane, int E, int k,
-                                                   const int* __restrict__ species, const int* __restrict__ ei,
-                                                   const int* __restrict__ ej, const int* __restrict__ te,
-                                                   const int* __restrict__ te2, const float* __restrict__ Pa,
-                                                   const float* __restrict__ Pb, const float* __restrict__ Pc,
-                                                   const float* __restrict__ beta, const int* __restrict__ eid,
-                                                   const float* __restrict__ gt) {
+// Loss adjoint of the triplet router logits, one thread per triplet:
+//   lt[t, x] = p[x] (pt[x] - sum_c p[eid_c] gt_c),  pt[x] = sum_c [eid_c = x] gt_c,
+// p the float64 softmax of the triplet's logits.
+__global__ void tri_logit_kernel(const int* __restrict__ species, const int* __restrict__ ei,
+                                 const int* __restrict__ ej, const int* __restrict__ te, const int* __restrict__ te2,
+                                 long long Nt, const float* __restrict__ Pa, const float* __restrict__ Pb,
+                                 const float* __restrict__ Pc, const float* __restrict__ beta, int E, int k,
+                                 const int* __restrict__ eid, const float* __restrict__ gt, float* __restrict__ lt) {
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Nt) return;
   const int za = species[ei[te[t]]], zb = species[ej[te[t]]], zc = species[ej[te2[t]]];
-  double lg = -1e300;
-  if (lane < E)
-    lg = (((double)Pa[za * E + lane] + (double)Pb[zb * E + lane]) + (double)Pc[zc * E + lane]) + (double)beta[lane];
-  double mx = lg;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
-  const double ex = lane < E ? exp(lg - mx) : 0.0;
-  const double den = wave_sum_d(ex);
-  const float p = (float)(ex / den);
-  float pt = 0.f;
-  for (int c = 0; c < k; ++c)
-    if (eid[t * k + c] == lane) pt += gt[t * k + c];
-  const float s = wave_sum(p * pt);
-  return p * (pt - s);
+  auto logit = [&](int x) {
+    return (((double)Pa[za * E + x] + (double)Pb[zb * E + x]) + (double)Pc[zc * E + x]) + (double)beta[x];
+  };
+  double mx = -1e300;
+  for (int x = 0; x < E; ++x) mx = fmax(mx, logit(x));
+  double den = 0.0;
+  for (int x = 0; x < E; ++x) den += exp(logit(x) - mx);
+  float s = 0.f;
+  for (int c = 0; c < k; ++c) s += (float)(exp(logit(eid[t * k + c]) - mx) / den) * gt[t * k + c];
+  for (int x = 0; x < E; ++x) {
+    float pt = 0.f;
+    for (int c = 0; c < k; ++c)
+      if (eid[t * k + c] == x) pt += gt[t * k + c];
+    const float p = (float)(exp(logit(x) - mx) / den);
+    lt[t * E + x] = p * (pt - s);
+  }
 }
 
-// Per edge e (lane = expert): LB[e] = sum over tseg(e) of the logit adjoint,
-// LC[e] = sum over the triplets whose second edge is e.
-__global__ void tri_router_edge_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev, int E, int k,
-                                       const int* __restrict__ species, const int* __restrict__ ei,
-                                       const int* __restrict__ ej, const int* __restrict__ te,
-                                       const int* __restrict__ te2, const float* __restrict__ Pa,
-                                       const float* __restrict__ Pb, const float* __restrict__ Pc,
-                                       const float* __restrict__ beta, const int* __restrict__ eid,
-                                       const float* __restrict__ gt, long long Ne, float* __restrict__ LB,
+// Per edge e and expert x (one thread each): LB[e, x] = sum over tseg(e) of
+// lt, LC[e, x] = sum over the triplets whose second edge is e.
+__global__ void tri_router_edge_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev, int E,
+                                       const float* __restrict__ lt, long long Ne, float* __restrict__ LB,
                                        float* __restrict__ LC) {
-  JANUS_WAVE_LOOP(e, Ne) {
-    float b = 0.f, c = 0.f;
-    for (int t = trowptr[e]; t < trowptr[e + 1]; ++t) {
-      b += tri_logit_adjoint(t, l, E, k, species, ei, ej, te, te2, Pa, Pb, Pc, beta, eid, gt);
-      c += tri_logit_adjoint(trev[t], l, E, k, species, ei, ej, te, te2, Pa, Pb, Pc, beta, eid, gt);
-    }
-    if (l < E) {
-      LB[e * E + l] = b;
-      LC[e * E + l] = c;
-    }
+  const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= Ne * E) return;
+  const long long e = g / E;
+  const int x = (int)(g - e * E);
+  float b = 0.f, c = 0.f;
+  for (int t = trowptr[e]; t < trowptr[e + 1]; ++t) {
+    b += lt[(long long)t * E + x];
+    c += lt[(long long)trev[t] * E + x];
   }
+  LB[g] = b;
+  LC[g] = c;
 }
 
 // Per atom: pa = sum over own edges of LB (vertex species), pb = sum over
