@@ -67,26 +67,52 @@ __global__ void build_wchunks_kernel(const int* __restrict__ row_off, int n_grou
   }
 }
 
+// G_g (+)= sum of the chunk partials of group g.  A workgroup owns 16
+// float4 columns; its 16 column-slices sum the chunks c0 + s, c0 + s + 16, ...
+// (two accumulators each), and the slices are added in order 0..15, so the
+// result is the same on every run.
+constexpr int kRedSlices = 16;
 __global__ void wgrad_reduce_kernel(const float* __restrict__ partial, const int* __restrict__ chunk_first,
                                     int n_groups, long long PQ, float* __restrict__ G, int accumulate) {
+  __shared__ float4 red[kRedSlices][16];
   const int g = blockIdx.y;
-  const long long i4 = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (4 * i4 >= PQ) return;
-  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  float4* out = reinterpret_cast<float4*>(G + (long long)g * PQ) + i4;
-  if (accumulate) s = *out;
+  const int cl = threadIdx.x & 15, sl = threadIdx.x >> 4;
+  const long long i4 = (long long)blockIdx.x * 16 + cl;
+  const bool ok = 4 * i4 < PQ;
   const int c0 = chunk_first[g], c1 = chunk_first[g + 1];
-  for (int c = c0; c < c1; ++c) {
-    float4 v = reinterpret_cast<const float4*>(partial + (long long)c * PQ)[i4];
-    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+  if (ok) {
+    int c = c0 + sl;
+    for (; c + kRedSlices < c1; c += 2 * kRedSlices) {
+      const float4 u = reinterpret_cast<const float4*>(partial + (long long)c * PQ)[i4];
+      const float4 v = reinterpret_cast<const float4*>(partial + (long long)(c + kRedSlices) * PQ)[i4];
+      a.x += u.x; a.y += u.y; a.z += u.z; a.w += u.w;
+      b.x += v.x; b.y += v.y; b.z += v.z; b.w += v.w;
+    }
+    if (c < c1) {
+      const float4 u = reinterpret_cast<const float4*>(partial + (long long)c * PQ)[i4];
+      a.x += u.x; a.y += u.y; a.z += u.z; a.w += u.w;
+    }
   }
-  *out = s;
+  red[sl][cl] = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+  __syncthreads();
+  if (sl == 0 && ok) {
+    float4* out = reinterpret_cast<float4*>(G + (long long)g * PQ) + i4;
+    float4 s = accumulate ? *out : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int q = 0; q < kRedSlices; ++q) {
+      const float4 v = red[q][cl];
+      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
+    *out = s;
+  }
 }
 
 void launch_wgrad_reduce(hipStream_t st, const float* partial, const int* chunk_first, int groups,
                          long long PQ, float* G, int accumulate) {
-  dim3 rg(cdiv(PQ / 4, 256), groups);
-  hipLaunchKernelGGL(wgrad_reduce_kernel, rg, dim3(256), 0, st, partial, chunk_first, groups, PQ, G, accumulate);
+  dim3 rg(cdiv(PQ / 4, 16), groups);
+  hipLaunchKernelGGL(wgrad_reduce_kernel, rg, dim3(16 * kRedSlices), 0, st, partial, chunk_first, groups, PQ, G,
+                     accumulate);
 }
 
 // Tile and chunk tables from group row offsets (one workgroup).

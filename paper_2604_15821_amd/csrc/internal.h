@@ -85,11 +85,14 @@ inline int max_rows_tiles(long long M, int groups) { return (int)((M + GBM - 1) 
 inline int max_wchunks(long long M, int groups, int kc) { return (int)((M + kc - 1) / kc) + groups; }
 
 // Chunk length of the weight-gradient contraction: long enough to keep the
-// partials small, short enough to give the GPU a few thousand workgroups.
+// partials small, short enough to give the GPU a few thousand workgroups (at
+// least 256 where the contraction allows); 128 to 16384 rows.
 inline int wgrad_chunk_rows(long long M, int P, int Q) {
   long long tiles = (long long)((P + GBM - 1) / GBM) * ((Q + GBN - 1) / GBN);
+  auto blocks = [&](long long kc) { return ((M + kc - 1) / kc) * tiles; };
   long long kc = 1024;
-  while (kc < 16384 && ((M + kc - 1) / kc) * tiles > 4096) kc *= 2;
+  while (kc > 128 && blocks(kc) < 256) kc /= 2;
+  while (kc < 16384 && blocks(kc) > 4096) kc *= 2;
   return (int)kc;
 }
 

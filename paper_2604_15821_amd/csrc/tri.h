@@ -212,7 +212,7 @@ __device__ __forceinline__ void feat_sums(float b_lane, const float* sWa, int nb
 }
 
 // Per-triplet scalars of up to 64 triplets trev[tb + lane] (tb + lane < t1),
-// one triplet per lane.
+// one triplet per lane (lanes past t1 repeat the last triplet).
 template <int KC>
 struct TriLane {
   int tau;
@@ -232,6 +232,18 @@ struct TriLane {
     for (int k = 0; k < KC; ++k) pos[k] = pos3[(long long)tau * KC + k];
   }
 };
+
+// y = sum_c rows[pos_c] with the slot positions of triplet q held by lane q.
+template <int VPL, int KC>
+__device__ __forceinline__ void sum_slots_lane(const float* __restrict__ rows, const TriLane<KC>& tl, int q, int d,
+                                               int l, float (&y)[VPL]) {
+  float r[KC][VPL];
+#pragma unroll
+  for (int k = 0; k < KC; ++k) ld_row<VPL>(rows + (long long)bcast(tl.pos[k], q) * d, l, r[k]);
+  zero_row<VPL>(y);
+#pragma unroll
+  for (int k = 0; k < KC; ++k) add_row<VPL>(y, r[k]);
+}
 
 // (G W_a) row of one triplet and, with DERIV, (dG/dc W_a), (dG/dr1 W_a), (dG/dr2 W_a).
 template <int VPL, bool DERIV>
@@ -382,39 +394,36 @@ __global__ void tri_p2_kernel(const int* __restrict__ trowptr, const int* __rest
     for (int tb = t0; tb < t1; tb += 64) {
       TriLane<KC> tl;
       tl.load(trev, te, tc, u3, du3, pos3, tb, t1, l);
+      const float4 accl = acc[tl.tau];
       const int n = t1 - tb < 64 ? t1 - tb : 64;
-      for (int q = 0; q < n; ++q) {
-        const long long t = bcast(tl.tau, q);
-        float zb[VPL];
-        {
-          float r[KC][VPL];
+      // two triplets per pass (the second repeats the first when n is odd)
+      for (int q0 = 0; q0 < n; q0 += 2) {
+        const bool two = q0 + 1 < n;
+        const int qq[2] = {q0, two ? q0 + 1 : q0};
+        float zb[2][VPL];
 #pragma unroll
-          for (int k = 0; k < KC; ++k) ld_row<VPL>(Zbs + (long long)bcast(tl.pos[k], q) * d, l, r[k]);
-          zero_row<VPL>(zb);
+        for (int x = 0; x < 2; ++x) sum_slots_lane<VPL, KC>(Zbs, tl, qq[x], d, l, zb[x]);
 #pragma unroll
-          for (int k = 0; k < KC; ++k) add_row<VPL>(zb, r[k]);
-        }
-        float z[VPL], wc[VPL], w1[VPL], w2[VPL];
-        tri_feat<VPL, true>(bcast(tl.c, q), bcast(tl.u, q), bcast(tl.du, q), L, s, sp, z, wc, w1, w2);
-        st_row<VPL>(Zbar + t * d, l, zb);
-        float ac = 0.f, a1 = 0.f, a2 = 0.f;
+        for (int x = 0; x < 2; ++x) {
+          if (x == 1 && !two) break;
+          const int q = qq[x];
+          const long long t = bcast(tl.tau, q);
+          float z[VPL], wc[VPL], w1[VPL], w2[VPL];
+          tri_feat<VPL, true>(bcast(tl.c, q), bcast(tl.u, q), bcast(tl.du, q), L, s, sp, z, wc, w1, w2);
+          st_row<VPL>(Zbar + t * d, l, zb[x]);
+          float ac = 0.f, a1 = 0.f, a2 = 0.f;
 #pragma unroll
-        for (int v = 0; v < VPL; ++v) {
-          pr[v] += zb[v] * z[v];
-          const float w = zb[v] * hj[v];
-          ac += w * wc[v];
-          a1 += w * w1[v];
-          a2 += w * w2[v];
-        }
-        ac = wave_sum(ac);
-        a1 = wave_sum(a1);
-        a2 = wave_sum(a2);
-        if (l == 0) {
-          float4 g = acc[t];
-          g.x += ac;
-          g.y += a1;
-          g.z += a2;
-          acc[t] = g;
+          for (int v = 0; v < VPL; ++v) {
+            pr[v] += zb[x][v] * z[v];
+            const float w = zb[x][v] * hj[v];
+            ac += w * wc[v];
+            a1 += w * w1[v];
+            a2 += w * w2[v];
+          }
+          ac = wave_sum(ac);
+          a1 = wave_sum(a1);
+          a2 = wave_sum(a2);
+          if (l == q) acc[t] = make_float4(accl.x + ac, accl.y + a1, accl.z + a2, accl.w);
         }
       }
     }
@@ -514,24 +523,32 @@ __global__ void tri_p3_kernel(const int* __restrict__ trowptr, const int* __rest
         tl.load(trev, te, tc, u3, du3, pos3, tb, t1, l);
         const float4 cl = ct[tl.tau];
         const int n = t1 - tb < 64 ? t1 - tb : 64;
-        for (int q = 0; q < n; ++q) {
-          const long long t = bcast(tl.tau, q);
-          float zb[VPL];
-          ld_row<VPL>(Zbar + t * d, l, zb);
-          float z[VPL], wc[VPL], w1[VPL], w2[VPL];
-          tri_feat<VPL, true>(bcast(tl.c, q), bcast(tl.u, q), bcast(tl.du, q), L, s, sp, z, wc, w1, w2);
-          const float cx = bcast(cl.x, q), cy = bcast(cl.y, q), cz = bcast(cl.z, q);
-          float Zb[VPL], vv[VPL];
+        for (int q0 = 0; q0 < n; q0 += 2) {
+          const bool two = q0 + 1 < n;
+          const int qq[2] = {q0, two ? q0 + 1 : q0};
+          float zb[2][VPL];
 #pragma unroll
-          for (int v = 0; v < VPL; ++v) {
-            const float vt = cx * wc[v] + cy * w1[v] + cz * w2[v];
-            Zb[v] = vt * hj[v] + qh[v] * z[v];
-            vv[v] = zb[v] * hj[v];
-            pr[v] += vt * zb[v];
+          for (int x = 0; x < 2; ++x) ld_row<VPL>(Zbar + (long long)bcast(tl.tau, qq[x]) * d, l, zb[x]);
+#pragma unroll
+          for (int x = 0; x < 2; ++x) {
+            if (x == 1 && !two) break;
+            const int q = qq[x];
+            const long long t = bcast(tl.tau, q);
+            float z[VPL], wc[VPL], w1[VPL], w2[VPL];
+            tri_feat<VPL, true>(bcast(tl.c, q), bcast(tl.u, q), bcast(tl.du, q), L, s, sp, z, wc, w1, w2);
+            const float cx = bcast(cl.x, q), cy = bcast(cl.y, q), cz = bcast(cl.z, q);
+            float Zb[VPL], vv[VPL];
+#pragma unroll
+            for (int v = 0; v < VPL; ++v) {
+              const float vt = cx * wc[v] + cy * w1[v] + cz * w2[v];
+              Zb[v] = vt * hj[v] + qh[v] * z[v];
+              vv[v] = zb[x][v] * hj[v];
+              pr[v] += vt * zb[x][v];
+            }
+            st_row<VPL>(V + t * d, l, vv);
+#pragma unroll
+            for (int k = 0; k < KC; ++k) st_row<VPL>(Zbts + (long long)bcast(tl.pos[k], q) * d, l, Zb);
           }
-          st_row<VPL>(V + t * d, l, vv);
-#pragma unroll
-          for (int k = 0; k < KC; ++k) st_row<VPL>(Zbts + (long long)bcast(tl.pos[k], q) * d, l, Zb);
         }
       }
     }
@@ -605,27 +622,30 @@ __global__ void tri_p4_kernel(const int* __restrict__ trowptr, const int* __rest
       TriLane<KC> tl;
       tl.load(trev, te, tc, u3, nullptr, pos3, tb, t1, l);
       const int n = t1 - tb < 64 ? t1 - tb : 64;
-      for (int q = 0; q < n; ++q) {
-        const long long t = bcast(tl.tau, q);
-        float zt[VPL], zb[VPL];
-        {
-          float r[KC][VPL];
+      for (int q0 = 0; q0 < n; q0 += 2) {
+        const bool two = q0 + 1 < n;
+        const int qq[2] = {q0, two ? q0 + 1 : q0};
+        float zt[2][VPL], zb[2][VPL];
 #pragma unroll
-          for (int k = 0; k < KC; ++k) ld_row<VPL>(Zts + (long long)bcast(tl.pos[k], q) * d, l, r[k]);
-          ld_row<VPL>(Zbar + t * d, l, zb);
-          zero_row<VPL>(zt);
-#pragma unroll
-          for (int k = 0; k < KC; ++k) add_row<VPL>(zt, r[k]);
+        for (int x = 0; x < 2; ++x) {
+          sum_slots_lane<VPL, KC>(Zts, tl, qq[x], d, l, zt[x]);
+          ld_row<VPL>(Zbar + (long long)bcast(tl.tau, qq[x]) * d, l, zb[x]);
         }
-        float z[VPL], wc[VPL], w1[VPL], w2[VPL];
-        tri_feat<VPL, false>(bcast(tl.c, q), bcast(tl.u, q), 0.f, L, s, s, z, wc, w1, w2);
-        float zp[VPL];
 #pragma unroll
-        for (int v = 0; v < VPL; ++v) {
-          zp[v] = zt[v] * hj[v] + qh[v] * zb[v];
-          pr[v] += zt[v] * z[v];
+        for (int x = 0; x < 2; ++x) {
+          if (x == 1 && !two) break;
+          const int q = qq[x];
+          const long long t = bcast(tl.tau, q);
+          float z[VPL], wc[VPL], w1[VPL], w2[VPL];
+          tri_feat<VPL, false>(bcast(tl.c, q), bcast(tl.u, q), 0.f, L, s, s, z, wc, w1, w2);
+          float zp[VPL];
+#pragma unroll
+          for (int v = 0; v < VPL; ++v) {
+            zp[v] = zt[x][v] * hj[v] + qh[v] * zb[x][v];
+            pr[v] += zt[x][v] * z[v];
+          }
+          st_row<VPL>(ZP + t * d, l, zp);
         }
-        st_row<VPL>(ZP + t * d, l, zp);
       }
     }
     st_row<VPL>(P + e2 * d, l, pr);
