@@ -22,6 +22,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA = 157.3e12      # dense fp32 matrix peak of MI355X, FLOP/s
 PEAK_HBM = 8.0e12              # HBM3E bandwidth, B/s
+CSRC = os.path.join(ROOT, "paper_2604_15821_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def log(*a):
@@ -51,16 +53,44 @@ def cpu_baseline(workload: str, n_struct: int):
                       f"{dt:.1f} s; float64 NumPy, BLAS threads {blas}, affinity {aff}"}
 
 
+def kernel_sources_sha256() -> str:
+    """Hash of the library's kernel sources: measured counters are valid only for these."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".h", ".hip")):
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, family: str):
+    """HBM bytes per launch of a kernel family from the committed rocprofv3 counter summary
+    (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy kernel of known size), or None
+    when no summary matches this workload or the kernel sources changed since it was taken."""
+    path = os.path.join(PROFILES, f"{family}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-json:"):
+                rec = json.loads(line.split(":", 1)[1])
+                if rec.get("sources_sha256") != kernel_sources_sha256():
+                    return None
+                return rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
+    return None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="small")
-    ap.add_argument("--cpu-structs", type=int, default=12)
+    ap.add_argument("--cpu-structs", type=int, default=40)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=0,
-                    help="one device-to-device copy of this many MiB before the run (calibrates HBM counters)")
+                    help="one elementwise copy kernel over this many MiB before the run (calibrates HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path",
@@ -74,9 +104,11 @@ def main():
     from paper_2604_15821_amd.synth import WORKLOADS, make_batch
 
     if args.copy_mib > 0:
+        # one elementwise kernel that reads and writes copy_mib MiB each
         src = torch.ones(args.copy_mib << 18, device="cuda:0")
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.cuda.synchronize()
+        torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         log(f"calibration copy: {args.copy_mib} MiB read + {args.copy_mib} MiB written")
         del src, dst
@@ -112,6 +144,7 @@ def main():
     t1 = time.perf_counter()
     prof = ctx.profile_read()
     ctx.profile(False)
+    Nt = ctx.last_triplets()
     ms = (t1 - t0) * 1e3 / args.steps
     log(f"{ms:.3f} ms/step, loss {float(out[0].cpu()[0]):.6g}")
 
@@ -137,12 +170,12 @@ def main():
     if r["flops"] > 0:
         ach = r["flops"] / r["launches"] / (r["ms"] / r["launches"] * 1e-3) / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": ach, "peak": PEAK_FP32_MFMA / 1e12, "unit": "TFLOP/s",
-                "frac": ach * 1e12 / PEAK_FP32_MFMA, "traffic": None,
+                "frac": ach * 1e12 / PEAK_FP32_MFMA, "traffic": measured_traffic(args.workload, dom),
                 "flops_per_launch": r["flops"] / r["launches"], "avg_launch_ms": r["ms"] / r["launches"]}
     else:
         ach = r["bytes"] / r["launches"] / (r["ms"] / r["launches"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-                "frac": ach * 1e9 / PEAK_HBM, "traffic": None,
+                "frac": ach * 1e9 / PEAK_HBM, "traffic": measured_traffic(args.workload, dom),
                 "bytes_per_launch": r["bytes"] / r["launches"], "avg_launch_ms": r["ms"] / r["launches"]}
 
     res = {
@@ -162,6 +195,8 @@ def main():
                    "d_hidden": m.d_hidden, "experts": m.n_experts, "top_k": m.top_k, "blocks": m.n_blocks,
                    "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none"},
         "edges_per_s": Ne / (ms * 1e-3),
+        "triplets": Nt,
+        "triplets_per_s": Nt / (ms * 1e-3),
         "expert_gemm_flops_per_step": 24.0 * m.top_k * m.d * m.d_hidden * Ne * m.n_blocks,
         "roofline": roof,
         "kernels": kernels,

@@ -231,10 +231,13 @@ int janus_step(janus_ctx* ctx, const float* pos, const float* cell, const int32_
  * chunking except through floating-point summation order of the weight
  * gradients and loss, which is fixed for a given chunking.  A structure too
  * large for the cap makes janus_step return JANUS_ENOMEM.
- * janus_last_chunks returns how many chunks the last janus_step used.
+ * janus_last_chunks returns how many chunks the last janus_step used, and
+ * janus_last_triplets how many bond triplets it formed over the whole batch
+ * (0 without the three-body term).
  */
 int janus_set_workspace_limit(janus_ctx* ctx, int64_t bytes);
 int janus_last_chunks(const janus_ctx* ctx);
+int64_t janus_last_triplets(const janus_ctx* ctx);
 
 /*
  * Grouped fp32 GEMM on the matrix cores, the building block of the expert

@@ -69,6 +69,7 @@ extern "C" int janus_set_workspace_limit(janus_ctx* ctx, int64_t bytes) {
 }
 
 extern "C" int janus_last_chunks(const janus_ctx* ctx) { return ctx ? ctx->last_chunks : 0; }
+extern "C" int64_t janus_last_triplets(const janus_ctx* ctx) { return ctx ? ctx->last_triplets : 0; }
 
 extern "C" int janus_weight_layout(const janus_config* cfg, janus_tensor_desc* out, int32_t* n_tensors,
                                    int64_t* n_floats) {
@@ -863,6 +864,7 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
   rc = ensure(ctx->ws, need);
   if (rc) return rc;
   ctx->last_chunks = (int)chunks.size();
+  ctx->last_triplets = tpre[S];
 
   JANUS_HIP_TRY(hipMemsetAsync(dLdW, 0, sizeof(float) * L.total, st));
   if (dbg && dbg->counts) JANUS_HIP_TRY(hipMemsetAsync(dbg->counts, 0, sizeof(int) * cfg.n_blocks * cfg.n_experts, st));

@@ -60,6 +60,19 @@ __device__ __forceinline__ float4 f4zero() { return make_float4(0.f, 0.f, 0.f, 0
 __device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 __device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
 
+// XCD-aware block order.  Workgroups are handed to the 8 XCDs round-robin
+// by linear id, and each XCD has its own L2.  Block b runs on XCD b % 8 as
+// that XCD's (b / 8)-th block, so the ntile output tiles that share one row
+// range (or one weight-gradient chunk) are given to consecutive blocks of
+// one XCD: row range r = (slot / ntile) * 8 + xcd, tile = slot % ntile.
+// The grid is rows8(nrange) * ntile blocks; ids past the last range exit.
+__device__ __forceinline__ void xcd_map(int b, int ntile, int& range, int& tile) {
+  const int xcd = b & 7, slot = b >> 3;
+  tile = slot % ntile;
+  range = (slot / ntile) * 8 + xcd;
+}
+inline unsigned xcd_grid(long long nrange, int ntile) { return (unsigned)(((nrange + 7) / 8) * 8 * ntile); }
+
 // ---------------------------------------------------------------- loaders
 // load(r, k) fetches what element (r, k..k+3) needs from global memory;
 // apply(raw, k) turns it into the 4 operand values (only for valid rows).
@@ -343,10 +356,12 @@ __global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float
                                                            const RowsTile* __restrict__ tiles,
                                                            const int* __restrict__ n_tiles, Epi epi,
                                                            float* __restrict__ rowsum_out) {
-  const int t = blockIdx.x;
+  const int ncol = (N + GBN - 1) / GBN;
+  int t, ctile;
+  xcd_map(blockIdx.x, ncol, t, ctile);
   if (t >= *n_tiles) return;
   const RowsTile tile = tiles[t];
-  const int n0 = blockIdx.y * GBN;
+  const int n0 = ctile * GBN;
   const int r0 = tile.r0, r1 = tile.r1;
   const float* Bg = B + (long long)tile.group * K * N;
 
@@ -430,7 +445,7 @@ __global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float
         if (Epi::kRowSum) {
 #pragma unroll
           for (int o = 16; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
-          if (c4 == 0 && row < r1) rowsum_out[row * gridDim.y + blockIdx.y] = part;
+          if (c4 == 0 && row < r1) rowsum_out[row * ncol + ctile] = part;
         }
       }
     }
@@ -453,12 +468,13 @@ __global__ __launch_bounds__(256, 2) void gemm_wgrad_kernel(ALoad al, BLoad bl, 
                                                             const WChunk* __restrict__ chunks,
                                                             const int* __restrict__ n_chunks,
                                                             float* __restrict__ partial) {
-  const int c = blockIdx.x;
+  const int ntq = (Q + GBN - 1) / GBN;
+  int c, pq;
+  xcd_map(blockIdx.x, ((P + GBM - 1) / GBM) * ntq, c, pq);
   if (c >= *n_chunks) return;
   const WChunk ch = chunks[c];
-  const int ntq = (Q + GBN - 1) / GBN;
-  const int p0 = (blockIdx.y / ntq) * GBM;
-  const int q0 = (blockIdx.y % ntq) * GBN;
+  const int p0 = (pq / ntq) * GBM;
+  const int q0 = (pq % ntq) * GBN;
 
   __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
   auto sA = [&](int b) { return smem + b * (GBK * LD_KM); };

@@ -43,6 +43,7 @@ struct janus_ctx {
   size_t host_plan_n = 0;
   long long ws_limit = 0;     // workspace cap in bytes (0: from free device memory)
   int last_chunks = 0;        // chunks used by the last janus_step
+  long long last_triplets = 0; // triplets of the last janus_step's batch
   // profiler: event pairs recorded around kernel families while enabled
   bool prof_on = false;
   std::vector<janus_prof_rec> prof_recs;
@@ -104,7 +105,7 @@ template <bool NT, class ALoad, class Epi>
 void launch_rows(hipStream_t st, const ALoad& al, const float* B, int K, int N, const RowsTile* tiles,
                  const int* n_tiles, int max_tiles, const Epi& epi, float* rowsum = nullptr) {
   if (max_tiles <= 0) return;
-  dim3 grid(max_tiles, (N + GBN - 1) / GBN);
+  dim3 grid(xcd_grid(max_tiles, (N + GBN - 1) / GBN));
   hipLaunchKernelGGL((gemm_rows_kernel<NT, ALoad, Epi>), grid, dim3(256), 0, st, al, B, K, N, tiles,
                      n_tiles, epi, rowsum);
 }
@@ -114,7 +115,7 @@ void launch_wgrad(hipStream_t st, const ALoad& al, const BLoad& bl, int P, int Q
                   const int* n_chunks, const int* chunk_first, int max_chunks, int groups,
                   float* partial, float* G, int accumulate) {
   if (max_chunks > 0) {
-    dim3 grid(max_chunks, ((P + GBM - 1) / GBM) * ((Q + GBN - 1) / GBN));
+    dim3 grid(xcd_grid(max_chunks, ((P + GBM - 1) / GBM) * ((Q + GBN - 1) / GBN)));
     hipLaunchKernelGGL((gemm_wgrad_kernel<ALoad, BLoad>), grid, dim3(256), 0, st, al, bl, P, Q, chunks,
                        n_chunks, partial);
   }

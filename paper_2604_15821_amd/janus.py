@@ -80,6 +80,8 @@ def _lib():
         lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
         lib.janus_set_workspace_limit.argtypes = [vp, i64]
         lib.janus_last_chunks.argtypes = [vp]
+        lib.janus_last_triplets.argtypes = [vp]
+        lib.janus_last_triplets.restype = i64
         lib.janus_profile_enable.argtypes = [vp, C.c_int]
         lib.janus_profile_read.argtypes = [vp, C.POINTER(ProfileEntry), i32]
         _LIB = lib
@@ -91,7 +93,7 @@ def exported_symbols():
     lib = _lib()
     names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
              "janus_grouped_gemm", "janus_grouped_wgrad", "janus_profile_enable", "janus_profile_read",
-             "janus_set_workspace_limit", "janus_last_chunks", "janus_strerror"]
+             "janus_set_workspace_limit", "janus_last_chunks", "janus_last_triplets", "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
 
@@ -256,6 +258,9 @@ class Context:
 
     def last_chunks(self) -> int:
         return int(_lib().janus_last_chunks(self.h))
+
+    def last_triplets(self) -> int:
+        return int(_lib().janus_last_triplets(self.h))
 
     # ------------------------------------------------------------- profiler
     def profile(self, on: bool):
