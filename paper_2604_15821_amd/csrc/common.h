@@ -18,12 +18,15 @@ namespace janus {
 
 constexpr int kWave = 64;
 
-__device__ __forceinline__ float sigmoidf_(float a) { return 1.0f / (1.0f + __expf(-a)); }
-
 // SiLU(a) = a * s, SiLU'(a) = s + a s (1 - s), SiLU''(a) = s (1 - s) (2 + a (1 - 2 s)),
-// s = 1 / (1 + exp(-a)).  Evaluated with the accurate expf: the training step
-// is checked against a float64 reference.
-__device__ __forceinline__ float sig(float a) { return 1.0f / (1.0f + expf(-a)); }
+// s = 1 / (1 + exp(-a)), with the hardware exponential (v_exp_f32 on a * log2 e)
+// and reciprocal (v_rcp_f32): relative error of s about 1e-6 at |a| = 20 and a few
+// 1e-7 for |a| < 5, against the 1e-5 energy and 1e-3 gradient tolerances of the
+// float64 comparison.  The GEMMs that apply these per element (SiLU of stored
+// pre-activations, the SiLU' / SiLU'' epilogues) run 10-20 % faster than with the
+// correctly rounded exp and division.  exp(-a) overflows to inf for a < -88 and
+// rcp(inf) = 0, so s saturates cleanly at both ends.
+__device__ __forceinline__ float sig(float a) { return __builtin_amdgcn_rcpf(1.0f + __expf(-a)); }
 __device__ __forceinline__ float silu(float a) { return a * sig(a); }
 __device__ __forceinline__ float silu_d1(float a) {
   float s = sig(a);
