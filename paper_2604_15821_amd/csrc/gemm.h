@@ -351,21 +351,22 @@ __device__ __forceinline__ void mfma_stage(const float* a_s, const float* b_s, i
 
 // ---------------------------------------------------------------- gemm_rows
 
+// One output tile of gemm_rows for (XCD-mapped) block number vb; smem holds
+// SMEM_FLOATS floats of LDS.
 template <bool NT, class ALoad, class Epi>
-__global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float* __restrict__ B, int K, int N,
-                                                           const RowsTile* __restrict__ tiles,
-                                                           const int* __restrict__ n_tiles, Epi epi,
-                                                           float* __restrict__ rowsum_out) {
+__device__ __forceinline__ void gemm_rows_block(int vb, float* smem, const ALoad& al, const float* __restrict__ B,
+                                                int K, int N, const RowsTile* __restrict__ tiles,
+                                                const int* __restrict__ n_tiles, const Epi& epi,
+                                                float* __restrict__ rowsum_out) {
   const int ncol = (N + GBN - 1) / GBN;
   int t, ctile;
-  xcd_map(blockIdx.x, ncol, t, ctile);
+  xcd_map(vb, ncol, t, ctile);
   if (t >= *n_tiles) return;
   const RowsTile tile = tiles[t];
   const int n0 = ctile * GBN;
   const int r0 = tile.r0, r1 = tile.r1;
   const float* Bg = B + (long long)tile.group * K * N;
 
-  __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
   // double buffers: A at smem + b * GBM * LD_MK, B after both A buffers
   auto sA = [&](int b) { return smem + b * (GBM * LD_MK); };
   auto sB = [&](int b) { return smem + 2 * GBM * LD_MK + b * (GBN * LD_MK); };
@@ -453,6 +454,15 @@ __global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float
   }
 }
 
+template <bool NT, class ALoad, class Epi>
+__global__ __launch_bounds__(256, 2) void gemm_rows_kernel(ALoad al, const float* __restrict__ B, int K, int N,
+                                                           const RowsTile* __restrict__ tiles,
+                                                           const int* __restrict__ n_tiles, Epi epi,
+                                                           float* __restrict__ rowsum_out) {
+  __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
+  gemm_rows_block<NT, ALoad, Epi>(blockIdx.x, smem, al, B, K, N, tiles, n_tiles, epi, rowsum_out);
+}
+
 // --------------------------------------------------------------- gemm_wgrad
 // Both operands are row-major over the contraction index r: A [M, P], B [M, Q].
 
@@ -463,20 +473,19 @@ struct WChunk {
   int pad;
 };
 
+// One partial tile of gemm_wgrad for (XCD-mapped) block number vb.
 template <class ALoad, class BLoad>
-__global__ __launch_bounds__(256, 2) void gemm_wgrad_kernel(ALoad al, BLoad bl, int P, int Q,
-                                                            const WChunk* __restrict__ chunks,
-                                                            const int* __restrict__ n_chunks,
-                                                            float* __restrict__ partial) {
+__device__ __forceinline__ void gemm_wgrad_block(int vb, float* smem, const ALoad& al, const BLoad& bl, int P, int Q,
+                                                 const WChunk* __restrict__ chunks,
+                                                 const int* __restrict__ n_chunks, float* __restrict__ partial) {
   const int ntq = (Q + GBN - 1) / GBN;
   int c, pq;
-  xcd_map(blockIdx.x, ((P + GBM - 1) / GBM) * ntq, c, pq);
+  xcd_map(vb, ((P + GBM - 1) / GBM) * ntq, c, pq);
   if (c >= *n_chunks) return;
   const WChunk ch = chunks[c];
   const int p0 = (pq / ntq) * GBM;
   const int q0 = (pq % ntq) * GBN;
 
-  __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
   auto sA = [&](int b) { return smem + b * (GBK * LD_KM); };
   auto sB = [&](int b) { return smem + (2 + b) * (GBK * LD_KM); };
 
@@ -526,6 +535,15 @@ __global__ __launch_bounds__(256, 2) void gemm_wgrad_kernel(ALoad al, BLoad bl, 
         if (pr < P && qc < Q) out[(long long)pr * Q + qc] = acc[bi][bj][v];
       }
     }
+}
+
+template <class ALoad, class BLoad>
+__global__ __launch_bounds__(256, 2) void gemm_wgrad_kernel(ALoad al, BLoad bl, int P, int Q,
+                                                            const WChunk* __restrict__ chunks,
+                                                            const int* __restrict__ n_chunks,
+                                                            float* __restrict__ partial) {
+  __shared__ __attribute__((aligned(16))) float smem[SMEM_FLOATS];
+  gemm_wgrad_block<ALoad, BLoad>(blockIdx.x, smem, al, bl, P, Q, chunks, n_chunks, partial);
 }
 
 }  // namespace janus
