@@ -155,6 +155,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   auto blk = [](int t, const char* n) { return "blocks." + std::to_string(t) + "." + n; };
   const size_t ldsW = (size_t)nb * d * sizeof(float);
   const dim3 gE = wave_grid(Ne), gN = wave_grid(N), b256(256);
+  // kernels that stage W_a (up to 64 KB) in LDS: at most 4 workgroups per CU
+  // fit, so a larger grid would only reload W_a
+  const dim3 gEa(std::min(gE.x, 1024u));
 
   // algorithmic work of one launch of each kernel (matrix products: 2 M N K;
   // memory-bound kernels: bytes that must cross HBM once)
@@ -181,7 +184,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   }
   if (three) {
     // triplets of the chunk: CSR by first edge, reverse map, cosines
-    PROF(PROF_GRAPH, 0, Ne * 8.0 + Nt * 16.0);
+    PROF(PROF_GRAPH, 0, Ne * 8.0 + Nt * (16.0 + 4.0 * nf));
     const unsigned char* tsh = ca.tshort + ca.e0;
     hipLaunchKernelGGL(tri_count_kernel, dim3(cdiv(N, 256)), dim3(256), 0, st, rowptr, tsh, N, p.tcount);
     launch_exclusive_scan(st, p.tcount, (int)Ne, p.trow, nullptr);
@@ -190,6 +193,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                          (const int*)p.trow, Ne, p.te, p.te2);
       hipLaunchKernelGGL(tri_rev_kernel, dim3(cdiv(Nt, 256)), dim3(256), 0, st, (const int*)p.te,
                          (const int*)p.te2, (const int*)p.trow, (const float4*)p.geo, Nt, p.trev, p.tc);
+      // feature rows G of every triplet, for dW_a of the final backward
+      hipLaunchKernelGGL(tri_features_kernel, dim3(cdiv(Nt * (nf / 4), 256)), dim3(256), 0, st,
+                         LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, nullptr, nb}, Nt, nf, p.G3f);
     }
     hipLaunchKernelGGL(set_rows_kernel, dim3(1), dim3(64), 0, st, p.rowT, (int)Nt, p.rowT, Nt);
     build_tables(st, p.rowT, 1, p.kcT, nullptr, nullptr, p.chunksT, p.ncT, p.cfT);
@@ -292,7 +298,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       // triplet tokens -> triplet experts -> messages Q_e of each edge's triplets
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * 4.0 * k3 * d);
-        LAUNCH_VPL_K(tri_dispatch_kernel, d, k3, gE, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+        LAUNCH_VPL_K(tri_dispatch_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
                      (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.u3,
                      Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), POS3(t), Ne, d, Z3s(t));
       }
@@ -394,7 +400,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 4.0 * d + 32.0) + Ne * (4.0 * nb + 8.0 * d));
-        LAUNCH_VPL_K(tri_p2_kernel, d, k3, gE, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+        LAUNCH_VPL_K(tri_p2_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
                      (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.dB3,
                      (const float*)p.u3, (const float*)p.du3, Wp(blk(t, "W_a")), nb, L3, ej,
                      (const float*)HV(p.h, t), POS3(t), Ne, d, (const float*)p.T3a, Zbar3(t), p.tacc, p.Pe);
@@ -419,10 +425,14 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     if (Ne > 0)
       hipLaunchKernelGGL(rtilde_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, ei, ej, (const float4*)p.geo,
                          (const float*)p.phi, Ne, p.rt);
-    if (three && Nt > 0)
+    if (three && Nt > 0) {
       hipLaunchKernelGGL(tri_ctilde_kernel, dim3(cdiv(Nt, 256)), b256, 0, st, (const int*)p.te, (const int*)p.te2,
                          (const float*)p.tc, (const float4*)p.geo, ei, ej, (const float*)p.phi, (const float*)p.rt,
                          Nt, p.tct);
+      // ct-weighted feature derivatives of every triplet, for dW_a of the double backward
+      hipLaunchKernelGGL(tri_features_kernel, dim3(cdiv(Nt * (nf / 4), 256)), b256, 0, st,
+                         LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, p.tct, nb}, Nt, nf, p.G3t);
+    }
   }
   JANUS_HIP_TRY(hipGetLastError());
 
@@ -439,7 +449,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       const float* W2a = Wp(blk(t, "W2a"));
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 8.0 * d + 20.0) + Ne * (4.0 * nb + 8.0 * d));
-        LAUNCH_VPL_K(tri_p3_kernel, d, k3, gE, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+        LAUNCH_VPL_K(tri_p3_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
                      (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.dB3,
                      (const float*)p.u3, (const float*)p.du3, Wp(blk(t, "W_a")), nb, L3, ej,
                      (const float*)HV(p.h, t), hht_t, (const float4*)p.tct, (const float*)Zbar3(t), POS3(t), Ne, d,
@@ -448,8 +458,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       {
         // dW_a (part 1): Gt^T (Zbar * h_j2)
         PROF(PROF_DENSE_GEMM, f_wa, 0);
-        launch_wgrad(st, LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, p.tct, nb}, LoadPlain{p.VT, d}, nf,
-                     d, p.chunksT, p.ncT, p.cfT, p.mcT, 1, p.partial, Gp(blk(t, "W_a")), 1);
+        launch_wgrad(st, LoadPlain{p.G3t, nf}, LoadPlain{p.VT, d}, nf, d, p.chunksT, p.ncT, p.cfT, p.mcT, 1,
+                     p.partial, Gp(blk(t, "W_a")), 1);
       }
       {
         PROF(PROF_EXPERT_WGRAD, f_tri, 0);
@@ -639,7 +649,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 8.0 * d) + Ne * 12.0 * d);
-        LAUNCH_VPL_K(tri_p4_kernel, d, k3, gE, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+        LAUNCH_VPL_K(tri_p4_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
                      (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.u3,
                      Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), hht_t, (const float*)Zbar3(t),
                      POS3(t), Ne, d, (const float*)p.T3b, p.VT, p.Pe);
@@ -647,8 +657,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       {
         // dW_a (part 2): G^T (Zt * h_j2 + Q * Zbar)
         PROF(PROF_DENSE_GEMM, f_wa, 0);
-        launch_wgrad(st, LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, nullptr, nb}, LoadPlain{p.VT, d},
-                     nf, d, p.chunksT, p.ncT, p.cfT, p.mcT, 1, p.partial, Gp(blk(t, "W_a")), 1);
+        launch_wgrad(st, LoadPlain{p.G3f, nf}, LoadPlain{p.VT, d}, nf, d, p.chunksT, p.ncT, p.cfT, p.mcT, 1,
+                     p.partial, Gp(blk(t, "W_a")), 1);
       }
       {
         // triplet router tables: logit adjoints summed per vertex / neighbour species

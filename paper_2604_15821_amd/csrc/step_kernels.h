@@ -493,7 +493,7 @@ struct Plan {
   WChunk* chunksT;
   int *ncT, *cfT;
   float *Z3s, *A3, *S3b, *A3b, *Y3bs, *Zbar3;
-  float *Q, *LT3, *VT, *T3a, *T3b, *gpart3, *gt3, *LB, *LC, *pa, *pb, *pc;
+  float *Q, *LT3, *VT, *G3f, *G3t, *T3a, *T3b, *gpart3, *gt3, *LB, *LC, *pa, *pb, *pc;
   // sizes
   int T, E, k, d, hdim, nb, nsp, N, S;
   long long Ne, M;
@@ -674,6 +674,8 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.Q = cv.take<float>(Ne * d + 4);
     p.LT3 = cv.take<float>(Ntt * E3 + 4);
     p.VT = cv.take<float>(Ntt * d + 4);
+    p.G3f = cv.take<float>(Ntt * p.nf + 4);
+    p.G3t = cv.take<float>(Ntt * p.nf + 4);
     p.T3a = cv.take<float>(M3 * d + 4);
     p.T3b = cv.take<float>(M3 * d + 4);
     p.gpart3 = cv.take<float>(M3 * p.ntile3 + 4);

@@ -211,6 +211,32 @@ __device__ __forceinline__ void feat_sums(float b_lane, const float* sWa, int nb
   }
 }
 
+// The same sums for two basis rows (B3 and B3') in one pass over W_a.
+template <int VPL>
+__device__ __forceinline__ void feat_sums2(float b_lane, float db_lane, const float* sWa, int nb, int L, int d, int l,
+                                           float (&s)[kMaxL][VPL], float (&sp)[kMaxL][VPL]) {
+#pragma unroll
+  for (int q = 0; q < kMaxL; ++q) {
+    zero_row<VPL>(s[q]);
+    zero_row<VPL>(sp[q]);
+  }
+  for (int n = 0; n < nb; ++n) {
+    const float b = bcast(b_lane, n), db = bcast(db_lane, n);
+#pragma unroll
+    for (int q = 0; q < kMaxL; ++q) {
+      if (q < L) {
+        float w[VPL];
+        ld_row<VPL>(sWa + (q * nb + n) * d, l, w);
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          s[q][v] += b * w[v];
+          sp[q][v] += db * w[v];
+        }
+      }
+    }
+  }
+}
+
 // Per-triplet scalars of up to 64 triplets trev[tb + lane] (tb + lane < t1),
 // one triplet per lane (lanes past t1 repeat the last triplet).
 template <int KC>
@@ -387,8 +413,7 @@ __global__ void tri_p2_kernel(const int* __restrict__ trowptr, const int* __rest
     const int t0 = trowptr[e2], t1 = trowptr[e2 + 1];
     if (t0 == t1) continue;
     float s[kMaxL][VPL], sp[kMaxL][VPL], hj[VPL], pr[VPL];
-    feat_sums<VPL>(basis_lane(B3, e2, nb, l), sWa, nb, L, d, l, s);
-    feat_sums<VPL>(basis_lane(dB3, e2, nb, l), sWa, nb, L, d, l, sp);
+    feat_sums2<VPL>(basis_lane(B3, e2, nb, l), basis_lane(dB3, e2, nb, l), sWa, nb, L, d, l, s, sp);
     ld_row<VPL>(h + (long long)ej[e2] * d, l, hj);
     ld_row<VPL>(P + e2 * d, l, pr);
     for (int tb = t0; tb < t1; tb += 64) {
@@ -513,8 +538,7 @@ __global__ void tri_p3_kernel(const int* __restrict__ trowptr, const int* __rest
     zero_row<VPL>(pr);
     if (t0 < t1) {
       float s[kMaxL][VPL], sp[kMaxL][VPL], hj[VPL], qh[VPL];
-      feat_sums<VPL>(basis_lane(B3, e2, nb, l), sWa, nb, L, d, l, s);
-      feat_sums<VPL>(basis_lane(dB3, e2, nb, l), sWa, nb, L, d, l, sp);
+      feat_sums2<VPL>(basis_lane(B3, e2, nb, l), basis_lane(dB3, e2, nb, l), sWa, nb, L, d, l, s, sp);
       const long long j2 = ej[e2];
       ld_row<VPL>(h + j2 * d, l, hj);
       if (hht) ld_row<VPL>(hht + j2 * d, l, qh); else zero_row<VPL>(qh);
@@ -754,5 +778,17 @@ struct LoadTriFeat {
   }
   __device__ __forceinline__ float4 apply(const Raw& v, int) const { return v; }
 };
+
+// Feature rows of every triplet, out[t, f] = ld.load(t, f), written once per
+// step for the weight-gradient products of all blocks (the features do not
+// depend on the block).  One thread per 4 consecutive features.
+__global__ void tri_features_kernel(LoadTriFeat ld, long long Nt, int nf, float* __restrict__ out) {
+  const int nq = nf / 4;
+  const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= Nt * nq) return;
+  const long long t = g / nq;
+  const int f = 4 * (int)(g - t * nq);
+  *reinterpret_cast<float4*>(out + t * nf + f) = ld.load(t, f);
+}
 
 }  // namespace janus
