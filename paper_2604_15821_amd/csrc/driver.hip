@@ -187,7 +187,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     PROF(PROF_GRAPH, 0, Ne * 8.0 + Nt * (16.0 + 4.0 * nf));
     const unsigned char* tsh = ca.tshort + ca.e0;
     hipLaunchKernelGGL(tri_count_kernel, dim3(cdiv(N, 256)), dim3(256), 0, st, rowptr, tsh, N, p.tcount);
-    launch_exclusive_scan(st, p.tcount, (int)Ne, p.trow, nullptr);
+    launch_exclusive_scan(st, p.tcount, (int)Ne, p.trow, nullptr, p.scan);
     if (Nt > 0) {
       hipLaunchKernelGGL(tri_write_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, ei, rowptr, tsh,
                          (const int*)p.trow, Ne, p.te, p.te2);
@@ -204,7 +204,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   {
     PROF(PROF_ROUTE, 0, T * (Ne * (8.0 + 24.0 * k)));
     hipLaunchKernelGGL(species_count_kernel, dim3(nsp), dim3(64), 0, st, species, N, nsp, p.sp_cnt);
-    launch_exclusive_scan(st, p.sp_cnt, nsp, p.sp_off, nullptr);
+    launch_exclusive_scan(st, p.sp_cnt, nsp, p.sp_off, nullptr, p.scan);
     hipLaunchKernelGGL(species_write_kernel, dim3(nsp), dim3(64), 0, st, species, N, p.sp_off, p.sp_atoms);
     hipLaunchKernelGGL(set_rows_kernel, dim3(1), dim3(64), 0, st, p.rowN, N, p.rowE, Ne);
     build_tables(st, p.rowN, 1, p.kcN, p.tilesN, p.ntN, p.chunksN, p.ncN, p.cfN);
@@ -610,9 +610,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_OTHER, 0, 0);
         hipLaunchKernelGGL(gate_total_kernel, dim3(cdiv(M, 256)), b256, 0, st, (const float*)(p.g3 + t * M),
                            (const float*)p.gpart, POS(t), M, p.ntile, p.gt);
-        hipLaunchKernelGGL(router_atom_kernel, gN, b256, 0, st, rowptr, rev, k, Ee, (const int*)(p.pair + t * Ne),
-                           (const float*)(p.pprob + t * np * Ee), (const int*)(p.eid + t * M), (const float*)p.gt, N,
-                           p.partC, p.partN);
+        hipLaunchKernelGGL(edge_logit_kernel, dim3(cdiv(Ne * Ee, 256)), b256, 0, st, (const int*)(p.pair + t * Ne),
+                           (const float*)(p.pprob + t * np * Ee), (const int*)(p.eid + t * M), (const float*)p.gt, Ne,
+                           k, Ee, p.lte);
+        hipLaunchKernelGGL(router_atom_kernel, dim3(cdiv((long long)N * Ee, 256)), b256, 0, st, rowptr, rev, Ee,
+                           (const float*)p.lte, N, p.partC, p.partN);
         hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
                            (const int*)p.sp_atoms, (const float*)p.partC, Ee, nsp, Gp(blk(t, "Pc")));
         hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,

@@ -104,32 +104,77 @@ __global__ void nl_kernel(const float* __restrict__ pos, const float* __restrict
   if (!WRITE && lane == 0) count[i] = cnt;
 }
 
-// Exclusive scan of n int32 values into out[0..n] (one workgroup of 1024).
-// out[n] is the total; totals that do not fit int32 raise flag bit 4.
-__global__ void exclusive_scan_kernel(const int* __restrict__ in, int n, int* __restrict__ out,
-                                      int* __restrict__ flag) {
-  __shared__ long long part[1024];
+// Exclusive scan of n int32 values into out[0..n]; out[n] is the total and
+// totals that do not fit int32 raise flag bit 4.  Three passes over tiles of
+// kScanTile values: tile sums, an exclusive scan of the tile sums (one
+// workgroup), and the scan of every tile from its offset.  Sums are int64.
+constexpr int kScanThreads = 256, kScanPer = 16, kScanTile = kScanThreads * kScanPer;
+
+__device__ __forceinline__ long long block_exclusive_scan(long long v, long long* part, long long& total) {
   const int t = threadIdx.x;
-  const int per = (n + 1023) / 1024;
-  const int lo = min(n, t * per), hi = min(n, lo + per);
-  long long s = 0;
-  for (int k = lo; k < hi; ++k) s += in[k];
-  part[t] = s;
+  part[t] = v;
   __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {
-    long long v = t >= o ? part[t - o] : 0;
+  for (int o = 1; o < kScanThreads; o <<= 1) {
+    const long long w = t >= o ? part[t - o] : 0;
     __syncthreads();
-    part[t] += v;
+    part[t] += w;
     __syncthreads();
   }
-  long long run = part[t] - s;
+  total = part[kScanThreads - 1];
+  const long long r = part[t] - v;
+  __syncthreads();
+  return r;
+}
+
+__global__ void scan_tile_sums_kernel(const int* __restrict__ in, int n, long long* __restrict__ sums) {
+  __shared__ long long part[kScanThreads];
+  const long long lo = (long long)blockIdx.x * kScanTile + (long long)threadIdx.x * kScanPer;
+  long long s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; ++k)
+    if (lo + k < n) s += in[lo + k];
+  long long total;
+  block_exclusive_scan(s, part, total);
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ void scan_sums_kernel(long long* __restrict__ sums, int ntiles, int n, int* __restrict__ out,
+                                 int* __restrict__ flag) {
+  __shared__ long long part[kScanThreads];
+  const int per = (ntiles + kScanThreads - 1) / kScanThreads;
+  const int lo = min(ntiles, (int)threadIdx.x * per), hi = min(ntiles, lo + per);
+  long long s = 0;
+  for (int k = lo; k < hi; ++k) s += sums[k];
+  long long total;
+  long long run = block_exclusive_scan(s, part, total);
   for (int k = lo; k < hi; ++k) {
-    out[k] = (int)run;
-    run += in[k];
+    const long long v = sums[k];
+    sums[k] = run;
+    run += v;
   }
-  if (t == 1023) {
-    out[n] = (int)part[1023];
-    if (part[1023] > 0x7fffffffLL && flag) atomicOr(flag, 16);
+  if (threadIdx.x == 0) {
+    out[n] = (int)total;
+    if (total > 0x7fffffffLL && flag) atomicOr(flag, 16);
+  }
+}
+
+__global__ void scan_tile_kernel(const int* __restrict__ in, int n, const long long* __restrict__ offs,
+                                 int* __restrict__ out) {
+  __shared__ long long part[kScanThreads];
+  const long long lo = (long long)blockIdx.x * kScanTile + (long long)threadIdx.x * kScanPer;
+  int v[kScanPer];
+  long long s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; ++k) {
+    v[k] = lo + k < n ? in[lo + k] : 0;
+    s += v[k];
+  }
+  long long total;
+  long long run = offs[blockIdx.x] + block_exclusive_scan(s, part, total);
+#pragma unroll
+  for (int k = 0; k < kScanPer; ++k) {
+    if (lo + k < n) out[lo + k] = (int)run;
+    run += v[k];
   }
 }
 
@@ -236,8 +281,19 @@ void launch_atom_struct(hipStream_t st, const int* offsets, int S, int N, int* s
   hipLaunchKernelGGL(atom_struct_kernel, dim3(S), dim3(256), 0, st, offsets, S, N, sid);
 }
 
-void launch_exclusive_scan(hipStream_t st, const int* in, int n, int* out, int* flag) {
-  hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, st, in, n, out, flag);
+// scratch: cdiv(n, kScanTile) int64 values (scan_scratch_bytes)
+size_t scan_scratch_bytes(long long n) { return sizeof(long long) * (size_t)((n + kScanTile - 1) / kScanTile + 1); }
+
+void launch_exclusive_scan(hipStream_t st, const int* in, int n, int* out, int* flag, long long* scratch) {
+  const int ntiles = (int)cdiv(n, kScanTile);
+  if (ntiles > 0) {
+    hipLaunchKernelGGL(scan_tile_sums_kernel, dim3(ntiles), dim3(kScanThreads), 0, st, in, n, scratch);
+  }
+  hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(kScanThreads), 0, st, scratch, ntiles, n, out, flag);
+  if (ntiles > 0) {
+    hipLaunchKernelGGL(scan_tile_kernel, dim3(ntiles), dim3(kScanThreads), 0, st, in, n, (const long long*)scratch,
+                       out);
+  }
 }
 
 void launch_geometry(hipStream_t st, const float* pos, const float* cell, const int* sid, const int* ei,
@@ -265,6 +321,7 @@ extern "C" int janus_build_edges(janus_ctx* ctx, const float* pos, const float* 
   cv.take<int>(N);
   cv.take<int>(N);
   cv.take<int>(N + 1);
+  cv.take<long long>(scan_scratch_bytes(N) / sizeof(long long));
   int rc = ensure(ctx->nl, cv.size());
   if (rc) return rc;
   Carver c2(ctx->nl.ptr);
@@ -272,6 +329,7 @@ extern "C" int janus_build_edges(janus_ctx* ctx, const float* pos, const float* 
   int* sid = c2.take<int>(N);
   int* count = c2.take<int>(N);
   int* rp = c2.take<int>(N + 1);
+  long long* scan = c2.take<long long>(scan_scratch_bytes(N) / sizeof(long long));
   int* hw = ctx->host_word;
 
   JANUS_HIP_TRY(hipMemsetAsync(flag, 0, sizeof(int), st));
@@ -288,7 +346,7 @@ extern "C" int janus_build_edges(janus_ctx* ctx, const float* pos, const float* 
     ProfScope ps(ctx, st, PROF_GRAPH, 0.0, 16.0 * N);
     hipLaunchKernelGGL((nl_kernel<false>), dim3(cdiv((long long)N * 64, 256)), dim3(256), 0, st, pos, cell,
                        offsets, sid, r_cut, N, count, nullptr, nullptr, nullptr, nullptr);
-    launch_exclusive_scan(st, count, N, rp, flag);
+    launch_exclusive_scan(st, count, N, rp, flag, scan);
   }
   JANUS_HIP_TRY(hipGetLastError());
   JANUS_HIP_TRY(hipMemcpyAsync(hw, rp + N, sizeof(int), hipMemcpyDeviceToHost, st));

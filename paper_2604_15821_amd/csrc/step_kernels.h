@@ -247,35 +247,42 @@ __global__ void gate_total_kernel(const float* __restrict__ g3, const float* __r
   gt[f] = s;
 }
 
-// Router logit adjoints summed per atom (lane x = expert x):
-//   lt_e[x] = p_e[x] (pt_e[x] - sum_y p_e[y] pt_e[y]),  pt_e[x] = sum_c [eid_ec = x] gt_ec
-// partC[i] = sum over edges out of i, partN[i] = sum over edges into i.
-__device__ __forceinline__ float logit_adjoint(long long e, int k, int lane, int E, const int* __restrict__ pair,
-                                               const float* __restrict__ pprob, const int* __restrict__ eid,
-                                               const float* __restrict__ gt) {
-  const float px = lane < E ? pprob[(long long)pair[e] * E + lane] : 0.f;
-  float pt = 0.f;
-  for (int c = 0; c < k; ++c)
-    if (eid[e * k + c] == lane) pt += gt[e * k + c];
-  const float s = wave_sum(px * pt);
-  return px * (pt - s);
+// Router logit adjoint of every edge, one thread per (edge, expert x):
+//   lt[e, x] = p_e[x] (pt_e[x] - sum_c p_e[eid_ec] gt_ec),  pt_e[x] = sum_c [eid_ec = x] gt_ec,
+// with p_e the softmax of the edge's species pair.
+__global__ void edge_logit_kernel(const int* __restrict__ pair, const float* __restrict__ pprob,
+                                  const int* __restrict__ eid, const float* __restrict__ gt, long long Ne, int k,
+                                  int E, float* __restrict__ lt) {
+  const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= Ne * E) return;
+  const long long e = g / E;
+  const int x = (int)(g - e * E);
+  const float* p = pprob + (long long)pair[e] * E;
+  float s = 0.f, pt = 0.f;
+  for (int c = 0; c < k; ++c) {
+    const int y = eid[e * k + c];
+    const float gc = gt[e * k + c];
+    s += p[y] * gc;
+    if (y == x) pt += gc;
+  }
+  lt[g] = p[x] * (pt - s);
 }
 
-__global__ void router_atom_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev, int k, int E,
-                                   const int* __restrict__ pair, const float* __restrict__ pprob,
-                                   const int* __restrict__ eid, const float* __restrict__ gt, int N,
-                                   float* __restrict__ partC, float* __restrict__ partN) {
-  JANUS_WAVE_LOOP(i, N) {
-    float ac = 0.f, an = 0.f;
-    for (int e = rowptr[i]; e < rowptr[i + 1]; ++e) {
-      ac += logit_adjoint(e, k, l, E, pair, pprob, eid, gt);
-      an += logit_adjoint(rev[e], k, l, E, pair, pprob, eid, gt);
-    }
-    if (l < E) {
-      partC[i * E + l] = ac;
-      partN[i * E + l] = an;
-    }
+// Per atom i and expert x (one thread each): partC = sum over the edges out
+// of i of lt, partN = sum over the edges into i (through rev), in segment order.
+__global__ void router_atom_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev, int E,
+                                   const float* __restrict__ lt, int N, float* __restrict__ partC,
+                                   float* __restrict__ partN) {
+  const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= (long long)N * E) return;
+  const int i = (int)(g / E), x = (int)(g - (long long)i * E);
+  float ac = 0.f, an = 0.f;
+  for (int e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+    ac += lt[(long long)e * E + x];
+    an += lt[(long long)rev[e] * E + x];
   }
+  partC[g] = ac;
+  partN[g] = an;
 }
 
 // out[s] = sum over the atoms of species s (in atom order) of rows of M [N, w]; w <= 64 * VPLW.
@@ -475,9 +482,10 @@ struct Plan {
   // per block activations
   float *Xs, *A, *Sb, *Ab, *Ybs, *Xbar, *Fbar, *g3;
   // temporaries
-  float *T1, *T2, *Pe, *Ft, *gpart, *gt, *partC, *partN, *partial;
+  float *T1, *T2, *Pe, *Ft, *gpart, *gt, *partC, *partN, *lte, *partial;
   // chunk-local neighbour list (indices relative to the chunk)
   int *cei, *cej, *crev, *crow, *coff;
+  long long* scan;   // scratch of the exclusive scans (triplet CSR, species groups)
   // three-body term: triplets (CSR by first edge), per-edge basis at r3,
   // per-block triplet routing, activations and adjoints
   int *tcount, *trow, *te, *te2, *trev;
@@ -538,6 +546,7 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.rt = cv.take<float>(Ne);
   p.rbar = cv.take<float>(Ne);
   p.sp_cnt = cv.take<int>(p.nsp);
+  p.scan = cv.take<long long>(scan_scratch_bytes(std::max<long long>(Ne, p.nsp)) / sizeof(long long));
   p.sp_off = cv.take<int>(p.nsp + 1);
   p.sp_atoms = cv.take<int>(N);
   p.z = cv.take<float>(Nd);
@@ -600,6 +609,7 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.gt = cv.take<float>(M);
   p.partC = cv.take<float>((long long)N * E);
   p.partN = cv.take<float>((long long)N * E);
+  p.lte = cv.take<float>(Ne * E + 1);
   long long part = (long long)p.mc * d * h;
   part = std::max(part, (long long)p.mcN * d * d);
   part = std::max(part, (long long)p.mcE * p.nb * d);
