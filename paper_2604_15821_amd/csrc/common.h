@@ -37,10 +37,23 @@ __device__ __forceinline__ float silu_d2(float a) {
   return s * (1.0f - s) * (2.0f + a * (1.0f - 2.0f * s));
 }
 
+// Sum over the 64 lanes, returned (wave-uniform) in every lane: DPP steps
+// inside each row of 16 lanes (quad_perm 1032, quad_perm 2301, half-row
+// mirror, row mirror), then the four row sums read from lanes 0, 16, 32, 48
+// and added in that order.
+template <int CTRL>
+__device__ __forceinline__ float dpp_step(float v) {
+  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v = dpp_step<0xB1>(v);    // quad_perm(1, 0, 3, 2)
+  v = dpp_step<0x4E>(v);    // quad_perm(2, 3, 0, 1)
+  v = dpp_step<0x141>(v);   // row_half_mirror
+  v = dpp_step<0x140>(v);   // row_mirror
+  const int b = __float_as_int(v);
+  return ((__int_as_float(__builtin_amdgcn_readlane(b, 0)) + __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
+          __int_as_float(__builtin_amdgcn_readlane(b, 32))) +
+         __int_as_float(__builtin_amdgcn_readlane(b, 48));
 }
 
 __device__ __forceinline__ double wave_sum_d(double v) {
