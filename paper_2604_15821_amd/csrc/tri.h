@@ -178,7 +178,8 @@ __device__ __forceinline__ float bcast(float x, int q) {
 }
 __device__ __forceinline__ int bcast(int x, int q) { return __builtin_amdgcn_readlane(x, q); }
 
-// Legendre values and derivatives P_q(c), P'_q(c) for q < kMaxL (Bonnet's recursion).
+// Legendre values and derivatives P_q(c), P'_q(c) for q < kMaxL (Bonnet's
+// recursion, the division by q + 1 taken as a product with its reciprocal).
 __device__ __forceinline__ void legendre_all(float c, float (&P)[kMaxL], float (&dP)[kMaxL]) {
   P[0] = 1.f;
   dP[0] = 0.f;
@@ -186,7 +187,8 @@ __device__ __forceinline__ void legendre_all(float c, float (&P)[kMaxL], float (
   dP[1] = 1.f;
 #pragma unroll
   for (int q = 1; q + 1 < kMaxL; ++q) {
-    P[q + 1] = ((2 * q + 1) * c * P[q] - q * P[q - 1]) / (q + 1);
+    constexpr float one = 1.f;
+    P[q + 1] = ((2 * q + 1) * c * P[q] - q * P[q - 1]) * (one / (q + 1));
     dP[q + 1] = (q + 1) * P[q] + c * dP[q];
   }
 }
@@ -259,17 +261,40 @@ struct TriLane {
   }
 };
 
-// y = sum_c rows[pos_c] with the slot positions of triplet q held by lane q.
+// Raw slot rows of the two triplets of a pass starting at q0 (indices clamped
+// to n - 1, so a pass past the end re-reads valid rows and is never used).
 template <int VPL, int KC>
-__device__ __forceinline__ void sum_slots_lane(const float* __restrict__ rows, const TriLane<KC>& tl, int q, int d,
-                                               int l, float (&y)[VPL]) {
-  float r[KC][VPL];
+struct PassRows {
+  float r[2][KC][VPL];
+  __device__ __forceinline__ void load(const float* __restrict__ rows, const TriLane<KC>& tl, int q0, int n, int d,
+                                       int l) {
 #pragma unroll
-  for (int k = 0; k < KC; ++k) ld_row<VPL>(rows + (long long)bcast(tl.pos[k], q) * d, l, r[k]);
-  zero_row<VPL>(y);
+    for (int x = 0; x < 2; ++x) {
+      const int q = q0 + x < n ? q0 + x : n - 1;
 #pragma unroll
-  for (int k = 0; k < KC; ++k) add_row<VPL>(y, r[k]);
-}
+      for (int k = 0; k < KC; ++k) ld_row<VPL>(rows + (long long)bcast(tl.pos[k], q) * d, l, r[x][k]);
+    }
+  }
+  __device__ __forceinline__ void sum(int x, float (&y)[VPL]) const {
+    zero_row<VPL>(y);
+#pragma unroll
+    for (int k = 0; k < KC; ++k) add_row<VPL>(y, r[x][k]);
+  }
+};
+
+// Rows of a per-triplet array (row = triplet index) for the two triplets of a pass.
+template <int VPL, int KC>
+struct PassTri {
+  float r[2][VPL];
+  __device__ __forceinline__ void load(const float* __restrict__ rows, const TriLane<KC>& tl, int q0, int n, int d,
+                                       int l) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      const int q = q0 + x < n ? q0 + x : n - 1;
+      ld_row<VPL>(rows + (long long)bcast(tl.tau, q) * d, l, r[x]);
+    }
+  }
+};
 
 // (G W_a) row of one triplet and, with DERIV, (dG/dc W_a), (dG/dr1 W_a), (dG/dr2 W_a).
 template <int VPL, bool DERIV>
@@ -419,19 +444,23 @@ __global__ void tri_p2_kernel(const int* __restrict__ trowptr, const int* __rest
     for (int tb = t0; tb < t1; tb += 64) {
       TriLane<KC> tl;
       tl.load(trev, te, tc, u3, du3, pos3, tb, t1, l);
-      const float4 accl = acc[tl.tau];
       const int n = t1 - tb < 64 ? t1 - tb : 64;
-      // two triplets per pass (the second repeats the first when n is odd)
-      for (int q0 = 0; q0 < n; q0 += 2) {
-        const bool two = q0 + 1 < n;
-        const int qq[2] = {q0, two ? q0 + 1 : q0};
+      // lane q keeps the geometry adjoints of triplet q of the batch
+      float my_ac = 0.f, my_a1 = 0.f, my_a2 = 0.f;
+      // two triplets per pass, with the rows of the following pass loaded
+      // before a pass is computed (buffers A and B alternate).  Every pass does
+      // the same memory operations (a pass past the end repeats the last
+      // triplet with identical stores and zero weight in the sums), so the
+      // compiler's waits stay exact.
+      auto pass = [&](const PassRows<VPL, KC>& cur, int q0) {
         float zb[2][VPL];
 #pragma unroll
-        for (int x = 0; x < 2; ++x) sum_slots_lane<VPL, KC>(Zbs, tl, qq[x], d, l, zb[x]);
+        for (int x = 0; x < 2; ++x) cur.sum(x, zb[x]);
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
-          if (x == 1 && !two) break;
-          const int q = qq[x];
+          const bool real = q0 + x < n;
+          const int q = real ? q0 + x : n - 1;
+          const float wgt = real ? 1.f : 0.f;
           const long long t = bcast(tl.tau, q);
           float z[VPL], wc[VPL], w1[VPL], w2[VPL];
           tri_feat<VPL, true>(bcast(tl.c, q), bcast(tl.u, q), bcast(tl.du, q), L, s, sp, z, wc, w1, w2);
@@ -439,7 +468,7 @@ __global__ void tri_p2_kernel(const int* __restrict__ trowptr, const int* __rest
           float ac = 0.f, a1 = 0.f, a2 = 0.f;
 #pragma unroll
           for (int v = 0; v < VPL; ++v) {
-            pr[v] += zb[x][v] * z[v];
+            pr[v] += wgt * (zb[x][v] * z[v]);
             const float w = zb[x][v] * hj[v];
             ac += w * wc[v];
             a1 += w * w1[v];
@@ -448,8 +477,24 @@ __global__ void tri_p2_kernel(const int* __restrict__ trowptr, const int* __rest
           ac = wave_sum(ac);
           a1 = wave_sum(a1);
           a2 = wave_sum(a2);
-          if (l == q) acc[t] = make_float4(accl.x + ac, accl.y + a1, accl.z + a2, accl.w);
+          my_ac = l == q ? ac : my_ac;
+          my_a1 = l == q ? a1 : my_a1;
+          my_a2 = l == q ? a2 : my_a2;
         }
+      };
+      PassRows<VPL, KC> A, B;
+      A.load(Zbs, tl, 0, n, d, l);
+      for (int q0 = 0; q0 < n; q0 += 4) {
+        B.load(Zbs, tl, q0 + 2, n, d, l);
+        __builtin_amdgcn_sched_barrier(0);
+        pass(A, q0);
+        A.load(Zbs, tl, q0 + 4, n, d, l);
+        __builtin_amdgcn_sched_barrier(0);
+        pass(B, q0 + 2);
+      }
+      if (l < n) {
+        const float4 g = acc[tl.tau];
+        acc[tl.tau] = make_float4(g.x + my_ac, g.y + my_a1, g.z + my_a2, g.w);
       }
     }
     st_row<VPL>(P + e2 * d, l, pr);
@@ -547,16 +592,12 @@ __global__ void tri_p3_kernel(const int* __restrict__ trowptr, const int* __rest
         tl.load(trev, te, tc, u3, du3, pos3, tb, t1, l);
         const float4 cl = ct[tl.tau];
         const int n = t1 - tb < 64 ? t1 - tb : 64;
-        for (int q0 = 0; q0 < n; q0 += 2) {
-          const bool two = q0 + 1 < n;
-          const int qq[2] = {q0, two ? q0 + 1 : q0};
-          float zb[2][VPL];
-#pragma unroll
-          for (int x = 0; x < 2; ++x) ld_row<VPL>(Zbar + (long long)bcast(tl.tau, qq[x]) * d, l, zb[x]);
+        auto pass = [&](const PassTri<VPL, KC>& cur, int q0) {
 #pragma unroll
           for (int x = 0; x < 2; ++x) {
-            if (x == 1 && !two) break;
-            const int q = qq[x];
+            const bool real = q0 + x < n;
+            const int q = real ? q0 + x : n - 1;
+            const float wgt = real ? 1.f : 0.f;
             const long long t = bcast(tl.tau, q);
             float z[VPL], wc[VPL], w1[VPL], w2[VPL];
             tri_feat<VPL, true>(bcast(tl.c, q), bcast(tl.u, q), bcast(tl.du, q), L, s, sp, z, wc, w1, w2);
@@ -566,13 +607,23 @@ __global__ void tri_p3_kernel(const int* __restrict__ trowptr, const int* __rest
             for (int v = 0; v < VPL; ++v) {
               const float vt = cx * wc[v] + cy * w1[v] + cz * w2[v];
               Zb[v] = vt * hj[v] + qh[v] * z[v];
-              vv[v] = zb[x][v] * hj[v];
-              pr[v] += vt * zb[x][v];
+              vv[v] = cur.r[x][v] * hj[v];
+              pr[v] += wgt * (vt * cur.r[x][v]);
             }
             st_row<VPL>(V + t * d, l, vv);
 #pragma unroll
             for (int k = 0; k < KC; ++k) st_row<VPL>(Zbts + (long long)bcast(tl.pos[k], q) * d, l, Zb);
           }
+        };
+        PassTri<VPL, KC> A, B;
+        A.load(Zbar, tl, 0, n, d, l);
+        for (int q0 = 0; q0 < n; q0 += 4) {
+          B.load(Zbar, tl, q0 + 2, n, d, l);
+          __builtin_amdgcn_sched_barrier(0);
+          pass(A, q0);
+          A.load(Zbar, tl, q0 + 4, n, d, l);
+          __builtin_amdgcn_sched_barrier(0);
+          pass(B, q0 + 2);
         }
       }
     }
@@ -646,30 +697,40 @@ __global__ void tri_p4_kernel(const int* __restrict__ trowptr, const int* __rest
       TriLane<KC> tl;
       tl.load(trev, te, tc, u3, nullptr, pos3, tb, t1, l);
       const int n = t1 - tb < 64 ? t1 - tb : 64;
-      for (int q0 = 0; q0 < n; q0 += 2) {
-        const bool two = q0 + 1 < n;
-        const int qq[2] = {q0, two ? q0 + 1 : q0};
-        float zt[2][VPL], zb[2][VPL];
+      auto pass = [&](const PassRows<VPL, KC>& cur, const PassTri<VPL, KC>& curb, int q0) {
+        float zt[2][VPL];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) cur.sum(x, zt[x]);
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
-          sum_slots_lane<VPL, KC>(Zts, tl, qq[x], d, l, zt[x]);
-          ld_row<VPL>(Zbar + (long long)bcast(tl.tau, qq[x]) * d, l, zb[x]);
-        }
-#pragma unroll
-        for (int x = 0; x < 2; ++x) {
-          if (x == 1 && !two) break;
-          const int q = qq[x];
+          const bool real = q0 + x < n;
+          const int q = real ? q0 + x : n - 1;
+          const float wgt = real ? 1.f : 0.f;
           const long long t = bcast(tl.tau, q);
           float z[VPL], wc[VPL], w1[VPL], w2[VPL];
           tri_feat<VPL, false>(bcast(tl.c, q), bcast(tl.u, q), 0.f, L, s, s, z, wc, w1, w2);
           float zp[VPL];
 #pragma unroll
           for (int v = 0; v < VPL; ++v) {
-            zp[v] = zt[x][v] * hj[v] + qh[v] * zb[x][v];
-            pr[v] += zt[x][v] * z[v];
+            zp[v] = zt[x][v] * hj[v] + qh[v] * curb.r[x][v];
+            pr[v] += wgt * (zt[x][v] * z[v]);
           }
           st_row<VPL>(ZP + t * d, l, zp);
         }
+      };
+      PassRows<VPL, KC> A, B;
+      PassTri<VPL, KC> Ab, Bb;
+      A.load(Zts, tl, 0, n, d, l);
+      Ab.load(Zbar, tl, 0, n, d, l);
+      for (int q0 = 0; q0 < n; q0 += 4) {
+        B.load(Zts, tl, q0 + 2, n, d, l);
+        Bb.load(Zbar, tl, q0 + 2, n, d, l);
+        __builtin_amdgcn_sched_barrier(0);
+        pass(A, Ab, q0);
+        A.load(Zts, tl, q0 + 4, n, d, l);
+        Ab.load(Zbar, tl, q0 + 4, n, d, l);
+        __builtin_amdgcn_sched_barrier(0);
+        pass(B, Bb, q0 + 2);
       }
     }
     st_row<VPL>(P + e2 * d, l, pr);
