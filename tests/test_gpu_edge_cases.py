@@ -164,3 +164,34 @@ def test_three_body_chunked_matches_single_pass_and_oracle():
     assert abs(o1["loss"] - o2["loss"]) <= 1e-6 * abs(o1["loss"])
     assert rel_l2(o2["dW"], o1["dW"]) <= 1e-6
     _check_against_oracle(b, o2)
+
+
+@pytest.mark.parametrize("what", ["species", "edge_index", "reverse_map", "offsets"])
+def test_step_rejects_invalid_inputs(what):
+    """Invalid species, neighbour lists or offsets are refused before any compute
+    (the validation kernels read only in-range indices)."""
+    import torch
+    from paper_2604_15821_amd import janus
+    from paper_2604_15821_amd.synth import make_batch, subset
+    b = subset(make_batch("tiny"), range(2))
+    banner("edge cases: invalid", what)
+    d = janus.upload(b)
+    ctx = janus.Context(b.model)
+    try:
+        nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+        offsets = d["offsets"]
+        if what == "species":
+            d["species"][3] = b.model.n_species
+        elif what == "edge_index":
+            nl.ej[0] = b.n_atoms + 5
+        elif what == "reverse_map":
+            nl.rev[0] = nl.rev[1]
+        else:
+            offsets = offsets.clone()
+            offsets[-1] = b.n_atoms - 1
+        torch.cuda.synchronize()
+        with pytest.raises(janus.JanusError) as ex:
+            ctx.step(d["pos"], d["cell"], d["species"], offsets, nl, d["W"], d["E_ref"], d["F_ref"])
+        assert ex.value.code == janus.JANUS_EINVAL
+    finally:
+        ctx.close()
