@@ -269,8 +269,12 @@ int janus_grouped_wgrad(janus_ctx* ctx, const float* A, const float* B, float* G
  * Optional profiler of the kernel families of janus_build_edges and
  * janus_step (host-side bookkeeping; HIP events recorded on the caller's
  * stream around each family of launches).
- * janus_profile_enable(ctx, 1) starts recording (and clears earlier
- * records); 0 stops it.  janus_profile_read synchronises the recorded
+ * janus_profile_enable(ctx, mask) starts recording the families whose bit
+ * is set in `mask` (bit 0 expert_gemm, 1 expert_wgrad, 2 dense_gemm, 3 edge,
+ * 4 atom, 5 route, 6 graph, 7 other; -1 records all) and clears earlier
+ * records; 0 stops it.  Each recorded launch group costs two events on the
+ * stream (a few microseconds), so timing one family perturbs the step less
+ * than timing all of them.  janus_profile_read synchronises the recorded
  * events, fills up to `cap` entries of `out` (host array) with one line per
  * family that ran, returns the number of entries (or a negative code), and
  * clears the records.  `flops` and `bytes` are the algorithmic work of the
@@ -285,7 +289,7 @@ typedef struct janus_profile_entry {
   double bytes;
 } janus_profile_entry;
 
-int janus_profile_enable(janus_ctx* ctx, int on);
+int janus_profile_enable(janus_ctx* ctx, int mask);
 int janus_profile_read(janus_ctx* ctx, janus_profile_entry* out /* host */, int32_t cap);
 
 /* Static message for a return code. */

@@ -46,6 +46,7 @@ struct janus_ctx {
   long long last_triplets = 0; // triplets of the last janus_step's batch
   // profiler: event pairs recorded around kernel families while enabled
   bool prof_on = false;
+  unsigned prof_mask = 0;     // families recorded (bit = JanusProfClass)
   std::vector<janus_prof_rec> prof_recs;
   std::vector<hipEvent_t> prof_pool;
   size_t prof_used = 0;

@@ -18,7 +18,7 @@ static hipEvent_t take_event(janus_ctx* c) {
 }
 
 ProfScope::ProfScope(janus_ctx* ctx, hipStream_t s, int cls, double flops, double bytes)
-    : c(ctx), st(s), on(ctx && ctx->prof_on) {
+    : c(ctx), st(s), on(ctx && ctx->prof_on && (ctx->prof_mask >> cls & 1u)) {
   if (!on) return;
   rec.cls = cls;
   rec.flops = flops;
@@ -42,10 +42,11 @@ ProfScope::~ProfScope() {
 
 using namespace janus;
 
-extern "C" int janus_profile_enable(janus_ctx* ctx, int on) {
+extern "C" int janus_profile_enable(janus_ctx* ctx, int mask) {
   if (!ctx) return JANUS_EINVAL;
-  ctx->prof_on = on != 0;
-  if (on) {
+  ctx->prof_on = mask != 0;
+  ctx->prof_mask = (unsigned)mask;
+  if (mask) {
     ctx->prof_recs.clear();
     ctx->prof_used = 0;
   }

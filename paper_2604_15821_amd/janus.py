@@ -263,8 +263,14 @@ class Context:
         return int(_lib().janus_last_triplets(self.h))
 
     # ------------------------------------------------------------- profiler
-    def profile(self, on: bool):
-        rc = _lib().janus_profile_enable(self.h, int(on))
+    PROFILE_FAMILIES = ["expert_gemm", "expert_wgrad", "dense_gemm", "edge", "atom", "route", "graph", "other"]
+
+    def profile(self, on: bool, families=None):
+        """Start (on) or stop the event profiler; `families` restricts it to some kernel families."""
+        mask = 0
+        if on:
+            mask = -1 if families is None else sum(1 << self.PROFILE_FAMILIES.index(f) for f in families)
+        rc = _lib().janus_profile_enable(self.h, mask)
         if rc:
             raise JanusError(rc, "janus_profile_enable")
 
