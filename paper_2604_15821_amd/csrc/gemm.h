@@ -42,10 +42,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int GBM = 128;            // tile rows
 constexpr int GBN = 128;            // tile cols
 constexpr int GBK = 16;             // k per LDS stage
-constexpr int LD_MK = GBK + 4;      // row stride of an [m][k] LDS tile (floats)
+constexpr int LD_MK = GBK;          // row stride of an [m][k] LDS tile (floats; float4 columns swizzled)
 constexpr int LD_KM = GBM + 8;      // row stride of a [k][m] LDS tile (floats)
 constexpr int LD_C = GBN + 8;       // row stride of the staged output (floats)
-constexpr int SMEM_MAIN = 2 * GBM * LD_MK + 2 * GBN * LD_MK;   // floats, >= the NN and wgrad layouts
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int B_BUF = cmax(GBN * LD_MK, GBK * LD_KM);             // one B stage, [n][k] or [k][n]
+constexpr int SMEM_MAIN = cmax(2 * GBM * LD_MK + 2 * B_BUF,       // gemm_rows
+                               4 * GBK * LD_KM);                   // gemm_wgrad
 constexpr int SMEM_EPI = 64 * LD_C;
 constexpr int SMEM_FLOATS = SMEM_MAIN > SMEM_EPI ? SMEM_MAIN : SMEM_EPI;
 
@@ -247,6 +250,12 @@ struct EpiP4 {
 };
 
 // ------------------------------------------------------------ LDS staging
+// [m][k] tiles hold the 4 float4 columns of row m in the order
+// kq ^ ((m / 4) % 4): a 16-lane group then touches 64 distinct banks both
+// when it stores 4 rows x 4 columns and when it reads one column of 16 rows.
+static_assert(GBK == 16, "the [m][k] swizzle assumes 4 float4 columns per row");
+__device__ __forceinline__ int mk_off(int m, int kq) { return m * LD_MK + 4 * (kq ^ ((m >> 2) & 3)); }
+
 // The loads are unconditional: rows (and columns) past the end of the range
 // read the last valid one and are replaced by zeros when stored to LDS.  A
 // conditional load would put a branch around every load, and at the join
@@ -272,7 +281,7 @@ struct StageMK {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int q = tid + 256 * i;
-      st4(s + (q >> 2) * LD_MK + 4 * (q & 3), ok[i] ? ld.apply(raw[i], k0 + 4 * (q & 3)) : f4zero());
+      st4(s + mk_off(q >> 2, q & 3), ok[i] ? ld.apply(raw[i], k0 + 4 * (q & 3)) : f4zero());
     }
   }
 };
@@ -321,7 +330,7 @@ __device__ __forceinline__ void mfma_stage(const float* a_s, const float* b_s, i
     for (int bi = 0; bi < 2; ++bi) {
       const int m = wm * 64 + bi * 32 + lr;
       if (AMK) {
-        const float4 v = ld4(a_s + m * LD_MK + 8 * g + 4 * hf);
+        const float4 v = ld4(a_s + mk_off(m, 2 * g + hf));
         af[bi][0] = v.x; af[bi][1] = v.y; af[bi][2] = v.z; af[bi][3] = v.w;
       } else {
 #pragma unroll
@@ -332,7 +341,7 @@ __device__ __forceinline__ void mfma_stage(const float* a_s, const float* b_s, i
     for (int bj = 0; bj < 2; ++bj) {
       const int n = wn * 64 + bj * 32 + lr;
       if (BMK) {
-        const float4 v = ld4(b_s + n * LD_MK + 8 * g + 4 * hf);
+        const float4 v = ld4(b_s + mk_off(n, 2 * g + hf));
         bf[bj][0] = v.x; bf[bj][1] = v.y; bf[bj][2] = v.z; bf[bj][3] = v.w;
       } else {
 #pragma unroll
@@ -369,7 +378,7 @@ __device__ __forceinline__ void gemm_rows_block(int vb, float* smem, const ALoad
 
   // double buffers: A at smem + b * GBM * LD_MK, B after both A buffers
   auto sA = [&](int b) { return smem + b * (GBM * LD_MK); };
-  auto sB = [&](int b) { return smem + 2 * GBM * LD_MK + b * (GBN * LD_MK); };
+  auto sB = [&](int b) { return smem + 2 * GBM * LD_MK + b * B_BUF; };
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, l = tid & 63;
