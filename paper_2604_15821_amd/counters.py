@@ -1,0 +1,160 @@
+"""Summary of the rocprofv3 runs behind bench.py's roofline figures.
+
+Three runs of ``bench.py`` on the GPU (see ``commands``): a kernel trace with
+statistics, then one counter pass with FETCH_SIZE and one with WRITE_SIZE
+(each counter in KiB per dispatch).  The counter passes start with
+``--copy-mib 1024``: one elementwise kernel that reads 1 GiB and writes 1 GiB,
+whose counter values scale every other dispatch to bytes.  This module turns
+the CSV output of those runs into ``profiles/expert_gemm_<workload>_traffic.md``,
+including the machine-readable record that ``bench.py`` reads back while the
+kernel sources still hash to the recorded value.
+
+    python -m paper_2604_15821_amd.counters <workload> <directory with the run outputs>
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import json
+import os
+import re
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def commands(workload: str, out: str = "$R/gpurun_out") -> list[str]:
+    """The three rocprofv3 command lines (run from /tmp with TMPDIR=/tmp, repo at $R)."""
+    bench = "python3 $R/bench.py"
+    return [
+        f"rocprofv3 --kernel-trace --stats --output-format csv -d {out}/tr_k_{workload} -o run -- "
+        f"{bench} --workload {workload} --steps 10 --warmup 2 --no-cpu-baseline",
+        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {out}/tr_f_{workload} -o run -- "
+        f"{bench} --workload {workload} --steps 2 --warmup 0 --no-cpu-baseline --copy-mib 1024",
+        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {out}/tr_w_{workload} -o run -- "
+        f"{bench} --workload {workload} --steps 2 --warmup 0 --no-cpu-baseline --copy-mib 1024",
+    ]
+
+
+def family(kernel_name: str) -> str:
+    """Kernel family of a dispatch, as bench.py's profiler groups launches."""
+    n = kernel_name
+    if "gemm_rows_kernel" in n:
+        return "dense_gemm" if "EpiDense" in n else "expert_gemm"
+    if "gemm_wgrad_kernel" in n or "wgrad_reduce" in n:
+        return "wgrad"
+    if re.search(r"(dispatch_x|edge_p[234]|tri_(dispatch|p[234]|combine|gather|combine_p3))_kernel", n):
+        return "edge"
+    if re.search(r"(combine_fwd|gather_atom|scatter_rev|combine_p3)_kernel", n):
+        return "atom"
+    if "elementwise_kernel" in n or "vectorized" in n:
+        return "copy"
+    return "other"
+
+
+def _counter(path: str, name: str):
+    per, names = collections.defaultdict(float), {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != name:
+                continue
+            k = int(r["Dispatch_Id"])
+            per[k] += float(r["Counter_Value"])
+            names[k] = r["Kernel_Name"]
+    return per, names
+
+
+def summarize(workload: str, runs: str) -> str:
+    """Markdown summary of the three runs found under `runs`."""
+    sys.path.insert(0, ROOT)
+    import bench  # noqa: E402  (the source hash and the record format are bench.py's)
+
+    fetch, fnames = _counter(f"{runs}/tr_f_{workload}/run_counter_collection.csv", "FETCH_SIZE")
+    write, wnames = _counter(f"{runs}/tr_w_{workload}/run_counter_collection.csv", "WRITE_SIZE")
+    copy_f = [fetch[k] for k in fetch if family(fnames[k]) == "copy" and fetch[k] > 5e5]
+    copy_w = [write[k] for k in write if family(wnames[k]) == "copy" and write[k] > 5e5]
+    kf, kw = 1048576.0 / copy_f[0], 1048576.0 / copy_w[0]
+    agg = collections.defaultdict(lambda: [0, 0.0, 0.0])
+    for k in fetch:
+        a = agg[family(fnames[k])]
+        a[0] += 1
+        a[1] += fetch[k] * 1024 * kf
+    for k in write:
+        agg[family(wnames[k])][2] += write[k] * 1024 * kw
+    dur = collections.defaultdict(list)
+    with open(f"{runs}/tr_k_{workload}/run_kernel_trace.csv") as f:
+        for r in csv.DictReader(f):
+            dur[family(r["Kernel_Name"])].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    with open(f"{runs}/tr_k_{workload}/run_kernel_stats.csv") as f:
+        stats = list(csv.DictReader(f))
+    bench_line = None
+    log = f"{runs}/tr_k_{workload}.log"
+    if os.path.exists(log):
+        lines = [x for x in open(log) if x.startswith("{")]
+        bench_line = json.loads(lines[-1]) if lines else None
+    ex = agg["expert_gemm"]
+    rec = {"workload": workload, "family": "expert_gemm", "sources_sha256": bench.kernel_sources_sha256(),
+           "launches_counted": ex[0], "fetch_bytes_per_launch": ex[1] / ex[0], "write_bytes_per_launch": ex[2] / ex[0],
+           "fetch_scale": kf, "write_scale": kw}
+    L = [f"# Kernel time and HBM traffic, training step, workload `{workload}`", "",
+         "Commands (run from /tmp on the MI355X box with `TMPDIR=/tmp`, repo at `$R`), three separate runs:", "",
+         "```", *commands(workload), "```", "",
+         f"Summarised by `python -m paper_2604_15821_amd.counters {workload} $R/gpurun_out`.", "",
+         "FETCH_SIZE and WRITE_SIZE are KiB per dispatch. Each is scaled by what the same counter reads for the",
+         "calibration kernel of the `--copy-mib 1024` runs: one elementwise kernel that reads 1 GiB and writes 1 GiB.",
+         f"The scale factors are fetch x{kf:.3f} and write x{kw:.3f}. Traffic is counted over every step of the",
+         "counter runs (3 untimed + 2 timed steps, so 5x the per-step launches).", "",
+         "| family | launches | avg us (kernel trace) | HBM read MB/launch | HBM write MB/launch |",
+         "|---|---:|---:|---:|---:|"]
+    for fam in ["expert_gemm", "wgrad", "dense_gemm", "edge", "atom", "other"]:
+        if agg[fam][0]:
+            d, a = dur.get(fam, [0.0]), agg[fam]
+            L.append(f"| {fam} | {a[0]} | {sum(d) / max(len(d), 1):.1f} | {a[1] / a[0] / 1e6:.1f} | "
+                     f"{a[2] / a[0] / 1e6:.1f} |")
+    L += ["", "Kernel statistics of the kernel-trace run (rocprofv3 --stats, all dispatches including warm-up):", "",
+          "| kernel | calls | avg us | total ms | % |", "|---|---:|---:|---:|---:|"]
+    for r in stats[:30]:
+        n = re.sub(r"\(.*", "", r["Name"].replace("janus::", ""))
+        L.append(f"| `{n}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                 f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f} |")
+    if bench_line:
+        roof = {k: v for k, v in bench_line["roofline"].items() if k != "traffic"}
+        L += ["", "bench.py line of the kernel-trace run (its own HIP-event timing on the library's stream):", "",
+              "```", json.dumps({k: bench_line[k] for k in ("value", "unit", "ms_per_step")}), json.dumps(roof), "```",
+              "", f"expert_gemm average launch: bench HIP events in the timed region {roof['avg_launch_ms'] * 1e3:.1f} us; "
+              f"kernel trace {sum(dur['expert_gemm']) / len(dur['expert_gemm']):.1f} us (all dispatches of the run)."]
+    algorithmic = algorithmic_bytes(bench_line)
+    if algorithmic:
+        ar, aw = algorithmic
+        L += ["", "Algorithmic bytes per expert-GEMM launch (average over the 8 products of a block):",
+              f"read {ar / 1e6:.0f} MB, write {aw / 1e6:.0f} MB; measured read / algorithmic = "
+              f"{rec['fetch_bytes_per_launch'] / ar:.2f}, write = {rec['write_bytes_per_launch'] / aw:.2f}."]
+    L += ["", "Machine-readable record read by bench.py (valid while the kernel sources hash to `sources_sha256`):", "",
+          "traffic-json: " + json.dumps(rec)]
+    return "\n".join(L) + "\n"
+
+
+def algorithmic_bytes(bench_line: dict):
+    """Average algorithmic HBM bytes (read, write) per expert-GEMM launch of a block of the
+    edge MoE, from the workload of a bench.py line: the 8 products G1-G6, G9, G10 over
+    M = k Ne slot rows with [M, h] and [M, d] fp32 tensors (operands, stored
+    pre-activations and adjoints read once, outputs written once).  None with triplets
+    (their products join the family)."""
+    if not bench_line or bench_line.get("triplets", 0):
+        return None
+    c = bench_line["config"]
+    M = c["top_k"] * c["edges"]
+    H, D = 4.0 * M * c["d_hidden"], 4.0 * M * c["d"]
+    reads = D + H + (D + H) + H + (D + 2 * H) + H + (D + 2 * H) + H      # G1 G2 G3 G4 G5 G6 G9 G10
+    writes = H + D + 2 * H + D + 2 * H + D + H + D
+    return reads / 8, writes / 8
+
+
+if __name__ == "__main__":
+    wl = sys.argv[1] if len(sys.argv) > 1 else "small"
+    runs = sys.argv[2] if len(sys.argv) > 2 else os.path.join(ROOT, "gpurun_out")
+    text = summarize(wl, runs)
+    out = os.path.join(ROOT, "profiles", f"expert_gemm_{wl}_traffic.md")
+    with open(out, "w") as f:
+        f.write(text)
+    print(out)
