@@ -72,6 +72,14 @@ enum {
  *              d_hidden3 (multiple of 64); n_legendre * n_rbf * d * 4 bytes
  *              must fit 64 KB
  *   w_E, w_F   loss weights of the energy and force terms
+ *   atom_moe   non-zero adds the feature-update MoE to every block (paper
+ *              Sec. "Sparse MoE routing": a second expert layer per block
+ *              that refines atom features, routed by element type):
+ *              u_i = h_i + sum of the block's messages, then
+ *              h'_i = u_i + sum_c g_ic W2f_x^T SiLU(W1f_x^T u_i) over the
+ *              top_k_f (1..4) of n_experts_f (1..64) experts chosen by the
+ *              logits Pf[Z_i] + betaf; each expert d -> d_hidden_f -> d
+ *              (d_hidden_f a multiple of 64)
  */
 typedef struct janus_config {
   int32_t n_species;
@@ -91,6 +99,10 @@ typedef struct janus_config {
   int32_t n_legendre;
   float w_E;
   float w_F;
+  int32_t atom_moe;
+  int32_t n_experts_f;
+  int32_t top_k_f;
+  int32_t d_hidden_f;
 } janus_config;
 
 typedef struct janus_ctx janus_ctx;
@@ -138,6 +150,9 @@ typedef struct janus_edges {
  *                               (e, e2) order
  *   eid3   [T*Nt*top_k3] int32 chosen triplet experts
  *   gate3  [T*Nt*top_k3] fp32  their gates
+ * With the feature-update MoE:
+ *   eidf   [T*N*top_k_f] int32 chosen experts of every atom
+ *   gatef  [T*N*top_k_f] fp32  their gates
  */
 typedef struct janus_debug {
   int32_t* eid;
@@ -149,6 +164,8 @@ typedef struct janus_debug {
   int32_t* tri_e2;
   int32_t* eid3;
   float* gate3;
+  int32_t* eidf;
+  float* gatef;
 } janus_debug;
 
 /* Create a context for `cfg` on the current device.  The context owns its
@@ -165,8 +182,9 @@ void janus_destroy(janus_ctx* ctx);
  * each block t: W_b [n_rbf, d], Pc [n_species, E], Pn [n_species, E],
  * beta [E], W1 [E, d, d_hidden], W2 [E, d_hidden, d], and with the
  * three-body term W_a [n_legendre*n_rbf, d], P3a, P3b, P3c [n_species, E3],
- * beta3 [E3], W1a [E3, d, d_hidden3], W2a [E3, d_hidden3, d]; then
- * W_o1 [d, d], w_o2 [d].  If `out` is NULL only the counts are written.  *n_tensors (in:
+ * beta3 [E3], W1a [E3, d, d_hidden3], W2a [E3, d_hidden3, d], and with
+ * the feature-update MoE Pf [n_species, Ef], betaf [Ef], W1f [Ef, d,
+ * d_hidden_f], W2f [Ef, d_hidden_f, d]; then W_o1 [d, d], w_o2 [d].  If `out` is NULL only the counts are written.  *n_tensors (in:
  * capacity of out, out: number of tensors) and *n_floats (total blob size)
  * are host pointers.  Errors: JANUS_EINVAL (capacity too small). */
 int janus_weight_layout(const janus_config* cfg, janus_tensor_desc* out, int32_t* n_tensors,
@@ -211,7 +229,7 @@ int janus_build_edges(janus_ctx* ctx, const float* pos, const float* cell, const
  *   E [S]      per-structure energies
  *   F [N*3]    forces -dE/dR
  *   dLdW       gradient of loss with respect to W, same layout as W; the
- *              routing biases beta receive exactly zero
+ *              routing biases (beta, beta3, betaf) receive exactly zero
  *   dbg        optional debug outputs (may be NULL)
  * Inputs are validated on the device first (species range, offsets, edge
  * indices, CSR and reverse map); a failure returns JANUS_EINVAL and writes

@@ -29,6 +29,14 @@ the messages of the bond triplets whose first bond is e:
     X_e   = F_e * h_{j(e)} + q_e,   q_e = sum_{tau = (e, .)} MoE3(Z_tau)
 and the forces and second-order sweeps carry the angle derivatives.
 
+With the feature-update MoE (paper Sec. "Sparse MoE routing": a second MoE
+per block that refines atom features, routed by element type) the block
+update becomes
+    u_i       = h^t_i + sum_{e : i(e) = i} m_e
+    lf_i      = Pf[Z_i] + betaf                      (float32 decision)
+    h^{t+1}_i = u_i + sum_c gf_ic W2f_x^T SiLU(W1f_x^T u_i),  x = Kf_i[c]
+with the same gating rule as the edge MoE; betaf is fixed like beta.
+
 Second order (paper Sec. "Runtime for multi-phase double-backward
 execution": the force loss needs derivatives of F with respect to the
 weights).  With lam_s = dL/dE_s and phi_a = dL/dF_a held fixed,
@@ -74,12 +82,16 @@ class Params:
     three: bool = False
     k3: int = 0
     E3: int = 0
+    atom: bool = False
+    kf: int = 0
+    Ef: int = 0
 
     @classmethod
     def from_weights(cls, weights, model):
         w = {n: np.asarray(v, np.float64) for n, v in weights.items()}
         return cls(w=w, T=model.n_blocks, k=model.top_k, E=model.n_experts, three=bool(model.three_body),
-                   k3=model.top_k3, E3=model.n_experts3)
+                   k3=model.top_k3, E3=model.n_experts3, atom=bool(model.atom_moe),
+                   kf=model.top_k_f, Ef=model.n_experts_f)
 
     def blk(self, t, name):
         return self.w[f"blocks.{t}.{name}"]
@@ -155,6 +167,7 @@ class Routing:
     pos: np.ndarray      # [Ne, k] int32 slot of (e, c) in the expert-grouped order
     inv: np.ndarray      # [Ne*k] int32 flattened (e*k + c) held by each slot
     tri: object = None   # routing of the triplet tokens of the same block (three-body term)
+    atom: object = None  # routing of the atom tokens of the feature-update MoE
 
 
 def route(species, ei, ej, Pc, Pn, beta, k):
@@ -182,6 +195,14 @@ def route_triplets(species, g, P3a, P3b, P3c, beta3, k3):
     return _route_logits(l32, l64, k3)
 
 
+def route_atoms(species, Pf, betaf, kf):
+    """Routing of the feature-update MoE: one token per atom, logits Pf[Z_i] + betaf,
+    decided in float32 (the element type alone selects the experts)."""
+    l32 = np.asarray(Pf, np.float32)[species] + np.asarray(betaf, np.float32)[None, :]
+    l64 = np.asarray(Pf, np.float64)[species] + np.asarray(betaf, np.float64)[None, :]
+    return _route_logits(l32, l64, kf)
+
+
 def _route_logits(l32, l64, k):
     """Top-k on float32 logits (lower index first on ties), gates from the float64 softmax."""
     eid = np.argsort(-l32, axis=1, kind="stable")[:, :k].astype(np.int32)
@@ -206,6 +227,8 @@ def route_all(species, g: Graph, P: Params):
         if g.tri is not None:
             rt.tri = route_triplets(species, g, P.blk(t, "P3a"), P.blk(t, "P3b"), P.blk(t, "P3c"),
                                     P.blk(t, "beta3"), P.k3)
+        if P.atom:
+            rt.atom = route_atoms(species, P.blk(t, "Pf"), P.blk(t, "betaf"), P.kf)
         out.append(rt)
     return out
 
@@ -248,12 +271,20 @@ def _tri_tokens(g, P, t, h):
     return Zpre, hj2, Zpre * hj2
 
 
+def _atom_moe(P, t, routing, u):
+    """Feature-update MoE output for the atom features u (zero without it)."""
+    if not P.atom:
+        return np.zeros_like(u)
+    return _moe(routing[t].atom, P.Ef, P.blk(t, "W1f"), P.blk(t, "W2f"), u)
+
+
 def forward_energy(species, g: Graph, P: Params, routing):
-    """Forward pass: per-structure energies and the stored atom features h^t."""
+    """Forward pass: per-structure energies, the stored atom features h^t and
+    the message-updated features u^t of every block."""
     N = species.shape[0]
     Ne = g.ei.shape[0]
     h = P.w["A"][species]
-    hs = [h]
+    hs, us = [h], []
     for t in range(P.T):
         F = g.B @ P.blk(t, "W_b")
         X = F * h[g.ej]
@@ -262,12 +293,14 @@ def forward_energy(species, g: Graph, P: Params, routing):
             y = _moe(routing[t].tri, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z)
             X = X + _seg(g.tri.te, Ne, y)
         m = _moe(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X)
-        h = h + _seg(g.ei, N, m)
+        u = h + _seg(g.ei, N, m)
+        h = u + _atom_moe(P, t, routing, u)
+        us.append(u)
         hs.append(h)
     z = h @ P.w["W_o1"]
     eps = silu(z) @ P.w["w_o2"]
     E = _seg(g.struct_of_atom, g.n_atoms_struct.size, eps)
-    return E, {"h": hs, "z": z, "eps": eps}
+    return E, {"h": hs, "u": us, "z": z, "eps": eps}
 
 
 def _block_tokens(g, P, t, h, routing):
@@ -285,12 +318,14 @@ def forces(species, g: Graph, P: Params, routing, cache):
     """Conservative forces F = -dE/dR by one hand-derived reverse sweep."""
     N = species.shape[0]
     Ne = g.ei.shape[0]
-    hs, z = cache["h"], cache["z"]
+    hs, us, z = cache["h"], cache["u"], cache["z"]
     hbar = (silu_d1(z) * P.w["w_o2"][None, :]) @ P.w["W_o1"].T      # dE/dh^T
     rbar = np.zeros(Ne)                                               # dE/dr_e (radial filter)
     Gvec = np.zeros((Ne, 3))                                          # dE/dd_e (triplet features)
     for t in reversed(range(P.T)):
         h = hs[t]
+        if P.atom:                                                    # h^{t+1} = u + MoE_f(u)
+            hbar = hbar + _moe_backward(routing[t].atom, P.Ef, P.blk(t, "W1f"), P.blk(t, "W2f"), us[t], hbar)
         F, X = _block_tokens(g, P, t, h, routing)
         Xbar = _moe_backward(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, hbar[g.ei])
         hbar_next = hbar + _seg(g.ej, N, Xbar * F)
@@ -377,16 +412,22 @@ def energy_tangent(species, g: Graph, P: Params, routing, phi):
     Gd = tb.feature_tangent(g.tri, g.r, g.u, ddot) if g.tri is not None else None
     h = P.w["A"][species]
     hd = np.zeros_like(h)
-    hs, hds = [h], [hd]
+    hs, hds, us, uds = [h], [hd], [], []
     for t in range(P.T):
         F, Fd, X, Xd = _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing)
         m, md = _moe_tangent(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd)
-        h = h + _seg(g.ei, N, m)
-        hd = hd + _seg(g.ei, N, md)
+        u = h + _seg(g.ei, N, m)
+        ud = hd + _seg(g.ei, N, md)
+        h, hd = u, ud
+        if P.atom:
+            f, fd = _moe_tangent(routing[t].atom, P.Ef, P.blk(t, "W1f"), P.blk(t, "W2f"), u, ud)
+            h, hd = u + f, ud + fd
+        us.append(u); uds.append(ud)
         hs.append(h); hds.append(hd)
     z, zd = h @ P.w["W_o1"], hd @ P.w["W_o1"]
     epsd = (silu_d1(z) * zd) @ P.w["w_o2"]
-    return epsd.sum(), {"h": hs, "hd": hds, "z": z, "zd": zd, "rdot": rdot, "Bdot": Bdot, "Gd": Gd}
+    return epsd.sum(), {"h": hs, "hd": hds, "u": us, "ud": uds, "z": z, "zd": zd, "rdot": rdot, "Bdot": Bdot,
+                        "Gd": Gd}
 
 
 def _moe_reverse(rt, E, W1, W2, X, Xd, Pm, Tm):
@@ -449,8 +490,16 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi):
 
     for t in reversed(range(P.T)):
         h, hd = hs[t], hds[t]
-        F, Fd, X, Xd = _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing)
         rt = routing[t]
+        if P.atom:
+            # h^{t+1} = u + MoE_f(u), hd^{t+1} = ud + D MoE_f(u) ud: adjoints of u, ud
+            u, ud = tc["u"][t], tc["ud"][t]
+            PU, TU, dW1f, dW2f, Pgf = _moe_reverse(rt.atom, P.Ef, P.blk(t, "W1f"), P.blk(t, "W2f"), u, ud, Ph, Th)
+            grad[f"blocks.{t}.W1f"] = dW1f
+            grad[f"blocks.{t}.W2f"] = dW2f
+            grad[f"blocks.{t}.Pf"] = _seg(species, S_, _logit_adjoint(rt.atom, Pgf))
+            Ph, Th = Ph + PU, Th + TU
+        F, Fd, X, Xd = _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing)
         PX, TX, dW1, dW2, Pg = _moe_reverse(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd, Ph[g.ei], Th[g.ei])
         grad[f"blocks.{t}.W1"] = dW1
         grad[f"blocks.{t}.W2"] = dW2

@@ -428,6 +428,13 @@ Layout make_layout(const janus_config& c) {
       L.add(p + "W1a", {E3, d, h3});
       L.add(p + "W2a", {E3, h3, d});
     }
+    if (c.atom_moe) {
+      const long long Ef = c.n_experts_f, hf = c.d_hidden_f;
+      L.add(p + "Pf", {S, Ef});
+      L.add(p + "betaf", {Ef});
+      L.add(p + "W1f", {Ef, d, hf});
+      L.add(p + "W2f", {Ef, hf, d});
+    }
   }
   L.add("W_o1", {d, d});
   L.add("w_o2", {d});
@@ -450,6 +457,10 @@ int check_config(const janus_config* c) {
     // the feature-to-width matrix W_a is staged in LDS (at most 64 KB)
     if (c->d_hidden3 % 64 || c->n_legendre > 8 || (size_t)c->n_legendre * c->n_rbf * c->d * 4 > 65536)
       return JANUS_EUNSUPPORTED;
+  }
+  if (c->atom_moe) {
+    // the step does not run the feature-update MoE yet
+    return JANUS_EUNSUPPORTED;
   }
   return JANUS_OK;
 }

@@ -31,7 +31,8 @@ class Config(C.Structure):
         ("n_experts", C.c_int32), ("top_k", C.c_int32), ("d_hidden", C.c_int32), ("env_p", C.c_int32),
         ("r_cut", C.c_float), ("three_body", C.c_int32), ("r_cut3", C.c_float), ("n_experts3", C.c_int32),
         ("top_k3", C.c_int32), ("d_hidden3", C.c_int32), ("n_legendre", C.c_int32), ("w_E", C.c_float),
-        ("w_F", C.c_float),
+        ("w_F", C.c_float), ("atom_moe", C.c_int32), ("n_experts_f", C.c_int32), ("top_k_f", C.c_int32),
+        ("d_hidden_f", C.c_int32),
     ]
 
 
@@ -52,9 +53,9 @@ class ProfileEntry(C.Structure):
 class Debug(C.Structure):
     _fields_ = [("eid", C.c_void_p), ("gate", C.c_void_p), ("counts", C.c_void_p), ("pos", C.c_void_p),
                 ("basis", C.c_void_p), ("tri_e", C.c_void_p), ("tri_e2", C.c_void_p), ("eid3", C.c_void_p),
-                ("gate3", C.c_void_p)]
+                ("gate3", C.c_void_p), ("eidf", C.c_void_p), ("gatef", C.c_void_p)]
 
-    KEYS = ("eid", "gate", "counts", "pos", "basis", "tri_e", "tri_e2", "eid3", "gate3")
+    KEYS = ("eid", "gate", "counts", "pos", "basis", "tri_e", "tri_e2", "eid3", "gate3", "eidf", "gatef")
 
 
 _LIB = None

@@ -33,7 +33,9 @@ class ModelConfig:
     d: embedding width; n_rbf: Bessel functions; n_blocks: interaction blocks;
     n_experts / top_k / d_hidden: edge-MoE size (each expert d -> d_hidden -> d);
     r_cut: neighbour cutoff in Angstrom.  The three-body fields describe the
-    optional angular term (triplets of bonds shorter than r_cut3).
+    optional angular term (triplets of bonds shorter than r_cut3).  The
+    atom_moe fields describe the optional feature-update MoE of every block
+    (atom tokens routed by element type; each expert d -> d_hidden_f -> d).
     """
 
     d: int
@@ -53,6 +55,10 @@ class ModelConfig:
     n_legendre: int = 5
     w_E: float = 1.0
     w_F: float = 1.0
+    atom_moe: bool = False
+    n_experts_f: int = 0
+    top_k_f: int = 0
+    d_hidden_f: int = 0
 
     def weight_shapes(self):
         """Named weight tensors in blob order, with the fan-in used at init.
@@ -83,6 +89,14 @@ class ModelConfig:
                     (p + "beta3", (E3,), "zero"),
                     (p + "W1a", (E3, d, h3), d),
                     (p + "W2a", (E3, h3, d), h3),
+                ]
+            if self.atom_moe:
+                Ef, hf = self.n_experts_f, self.d_hidden_f
+                out += [
+                    (p + "Pf", (S, Ef), None),
+                    (p + "betaf", (Ef,), "zero"),
+                    (p + "W1f", (Ef, d, hf), d),
+                    (p + "W2f", (Ef, hf, d), hf),
                 ]
         out += [("W_o1", (d, d), d), ("w_o2", (d,), d)]
         return out
@@ -122,12 +136,14 @@ class Workload:
 _M_TINY = ModelConfig(d=64, n_rbf=8, n_blocks=2, n_experts=4, top_k=1, d_hidden=128, r_cut=4.0)
 _M_SMALL = ModelConfig(d=128, n_rbf=16, n_blocks=3, n_experts=8, top_k=2, d_hidden=512, r_cut=5.0)
 _M_3B = dataclasses.replace(_M_SMALL, three_body=True, r_cut3=3.5, n_experts3=8, top_k3=2, d_hidden3=256)
+_M_ATOM = dataclasses.replace(_M_SMALL, atom_moe=True, n_experts_f=8, top_k_f=2, d_hidden_f=512)
 _M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
 
 WORKLOADS = {
     "tiny": Workload("tiny", "cubic", 8, 32, 0.08, _M_TINY),
     "small": Workload("small", "ortho", 64, 64, 0.08, _M_SMALL),
     "threebody": Workload("threebody", "ortho", 64, 64, 0.08, _M_3B),
+    "atom_moe": Workload("atom_moe", "ortho", 64, 64, 0.08, _M_ATOM),
     "shard": Workload("shard", "cubic", 256, 128, 0.1, _M_BIG),
     "irregular": Workload("irregular", "mixed", 512, 0, 0.1, _M_BIG, zipf_s=1.2),
 }

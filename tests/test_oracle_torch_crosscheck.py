@@ -152,3 +152,74 @@ def test_oracle_matches_torch_double_backward_with_three_body_term():
     for k, v in tg.items():
         scale = np.abs(v).max()
         np.testing.assert_allclose(grad[k], v, rtol=0, atol=1e-9 * scale + 1e-15, err_msg=k)
+
+
+def _torch_step_atom_moe(b, aux):
+    """Edge MoE plus the feature-update MoE, written with torch ops; forces and weight
+    gradients from autograd (routing decisions taken from the oracle)."""
+    g, rts = aux["graph"], aux["routing"]
+    m = b.model
+    dt = torch.float64
+    fixed = lambda k: k.rsplit(".", 1)[-1] in ("beta", "betaf")
+    pos = torch.tensor(b.pos, dtype=dt, requires_grad=True)
+    cell = torch.tensor(b.cell, dtype=dt)
+    W = {k: torch.tensor(v, dtype=dt, requires_grad=not fixed(k)) for k, v in b.weights.items()}
+    Z = torch.tensor(b.species, dtype=torch.long)
+    ei = torch.tensor(g.ei, dtype=torch.long)
+    ej = torch.tensor(g.ej, dtype=torch.long)
+    sid = torch.tensor(g.struct_of_atom, dtype=torch.long)
+    shift = torch.tensor(g.shift, dtype=dt)
+    d = pos[ej] - pos[ei] + torch.einsum("ek,ekc->ec", shift, cell[sid[ei]])
+    r = torch.sqrt((d * d).sum(1))
+    n = torch.arange(1, m.n_rbf + 1, dtype=dt)
+    x = r / m.r_cut
+    u = 1 - 28 * x ** 6 + 48 * x ** 7 - 21 * x ** 8
+    B = (2.0 / m.r_cut) ** 0.5 * torch.sin(n[None] * np.pi * r[:, None] / m.r_cut) / r[:, None] * u[:, None]
+
+    def moe(X, prob, eid, E, k, W1, W2):
+        out = torch.zeros(X.shape[0], W2.shape[2], dtype=dt)
+        for cc in range(k):
+            for xx in range(E):
+                rows = torch.nonzero(eid[:, cc] == xx).flatten()
+                if rows.numel():
+                    y = torch.nn.functional.silu(X[rows] @ W1[xx]) @ W2[xx]
+                    out = out.index_add(0, rows, prob[rows, xx][:, None] * y)
+        return out
+
+    h = W["A"][Z]
+    N = pos.shape[0]
+    for t in range(m.n_blocks):
+        p = f"blocks.{t}."
+        X = (B @ W[p + "W_b"]) * h[ej]
+        prob = torch.softmax(W[p + "Pc"][Z[ei]] + W[p + "Pn"][Z[ej]] + W[p + "beta"], dim=1)
+        msg = moe(X, prob, torch.tensor(rts[t].eid, dtype=torch.long), m.n_experts, m.top_k, W[p + "W1"], W[p + "W2"])
+        uu = h.index_add(0, ei, msg)
+        probf = torch.softmax(W[p + "Pf"][Z] + W[p + "betaf"], dim=1)
+        h = uu + moe(uu, probf, torch.tensor(rts[t].atom.eid, dtype=torch.long), m.n_experts_f, m.top_k_f,
+                     W[p + "W1f"], W[p + "W2f"])
+    eps = torch.nn.functional.silu(h @ W["W_o1"]) @ W["w_o2"]
+    E = torch.zeros(b.n_struct, dtype=dt).index_add(0, sid, eps)
+    F = -torch.autograd.grad(E.sum(), pos, create_graph=True)[0]
+    nat = torch.tensor(np.diff(b.offsets), dtype=dt)
+    loss = ((E / nat - torch.tensor(b.E_ref, dtype=dt)) ** 2).mean() \
+        + ((F - torch.tensor(b.F_ref, dtype=dt)) ** 2).sum() / (3 * N)
+    names = [k for k in W if W[k].requires_grad]
+    grads = torch.autograd.grad(loss, [W[k] for k in names])
+    return loss.item(), E.detach().numpy(), F.detach().numpy(), dict(zip(names, [x.numpy() for x in grads]))
+
+
+def test_oracle_matches_torch_double_backward_with_feature_update_moe():
+    import dataclasses
+    from paper_2604_15821_amd.synth import _draw_weights
+    b = make_batch("tiny", n_struct=3)
+    m = dataclasses.replace(b.model, atom_moe=True, n_experts_f=4, top_k_f=2, d_hidden_f=96)
+    b = dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(5), m, 0.0))
+    loss, E, F, grad, aux = training_step(b, return_aux=True)
+    tl, tE, tF, tg = _torch_step_atom_moe(b, aux)
+    assert loss == pytest.approx(tl, rel=1e-12)
+    np.testing.assert_allclose(E, tE, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(F, tF, rtol=1e-9, atol=1e-12)
+    assert any(k.endswith("W1f") for k in tg)
+    for k, v in tg.items():
+        scale = np.abs(v).max()
+        np.testing.assert_allclose(grad[k], v, rtol=0, atol=1e-9 * scale + 1e-15, err_msg=k)
