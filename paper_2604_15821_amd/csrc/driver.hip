@@ -177,6 +177,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   const bool three = p.three != 0;
   const long long Nt = p.Nt, M3 = p.M3;
   const int E3 = p.E3, k3 = p.k3, h3 = p.hd3, L3 = p.L3, nf = p.nf;
+  const bool atom = p.atom != 0;
+  const long long Mf = p.Mf;
+  const int Ef = p.Ef, kf = p.kf, hf = p.hdf;
+  if (atom) hipLaunchKernelGGL(iota_kernel, dim3(cdiv(N + 1, 256)), dim3(256), 0, st, p.iota, N);
   {
     PROF(PROF_GRAPH, 0, Ne * (12.0 + 3.0 + 16.0 + 8.0 * nb));
     launch_geometry(st, pos, cell, p.sid, ei, ej, shift, (int)Ne, cfg.r_cut, nb, p.geo, p.B, p.dB,
@@ -246,6 +250,30 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         build_tables(st, p.off3 + t * (E3 + 1), E3, p.kc3, p.tiles3 + (long long)t * p.mt3, p.ntiles3 + t,
                      p.chunks3 + (long long)t * p.mc3, p.nchunks3 + t, p.cfirst3 + t * (E3 + 1));
       }
+      if (atom) {
+        AtomRouteArgs fa;
+        fa.Pf = Wp(blk(t, "Pf"));
+        fa.beta = Wp(blk(t, "betaf"));
+        fa.species = species;
+        fa.N = N;
+        fa.nsp = nsp;
+        fa.E = Ef;
+        fa.k = kf;
+        fa.seid = p.seid + (long long)t * nsp * kf;
+        fa.sgate = p.sgate + (long long)t * nsp * kf;
+        fa.sprob = p.sprob + (long long)t * nsp * Ef;
+        fa.eid = p.eidf + t * Mf;
+        fa.gate = p.gatef + t * Mf;
+        fa.cnt = p.cntf;
+        fa.colpre = p.colpref;
+        fa.total = p.totalf + t * Ef;
+        fa.off = p.offf + t * (Ef + 1);
+        fa.pos = p.posf + t * Mf;
+        fa.slot_gate = p.slot_gatef + t * Mf;
+        route_atoms(st, fa);
+        build_tables(st, fa.off, Ef, p.kcf, p.tilesf + (long long)t * p.mtf, p.ntilesf + t,
+                     p.chunksf + (long long)t * p.mcf, p.nchunksf + t, p.cfirstf + t * (Ef + 1));
+      }
     }
   }
   JANUS_HIP_TRY(hipGetLastError());
@@ -284,6 +312,25 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   auto CH = [&](int t) { return (const WChunk*)(p.chunks + (long long)t * p.mc); };
   auto CF = [&](int t) { return (const int*)(p.cfirst + t * (Ee + 1)); };
   auto HV = [&](float* base, int t) { return base + t * Nd; };
+
+  // feature-update MoE views of block t (atom tokens; the identity CSR p.iota
+  // lets the per-atom gather / combine kernels serve one token per atom)
+  auto POSF = [&](int t) { return (const int*)(p.posf + t * Mf); };
+  auto GATEF = [&](int t) { return (const float*)(p.gatef + t * Mf); };
+  auto SGF = [&](int t) { return (const float*)(p.slot_gatef + t * Mf); };
+  auto TLF = [&](int t) { return (const RowsTile*)(p.tilesf + (long long)t * p.mtf); };
+  auto CHF = [&](int t) { return (const WChunk*)(p.chunksf + (long long)t * p.mcf); };
+  auto CFF = [&](int t) { return (const int*)(p.cfirstf + t * (Ef + 1)); };
+  auto Xsf = [&](int t) { return p.Xsf + t * Mf * d; };
+  auto Af = [&](int t) { return p.Af + t * Mf * hf; };
+  auto Sbf = [&](int t) { return p.Sbf + t * Mf * hf; };
+  auto Abf = [&](int t) { return p.Abf + t * Mf * hf; };
+  auto Ybf = [&](int t) { return p.Ybf + t * Mf * d; };
+  auto UU = [&](int t) { return p.uu + t * Nd; };
+  const int* iota = p.iota;
+  const double f_atm = 2.0 * Mf * d * hf;
+  const double by_fgather = N * 4.0 * d + Mf * (8.0 + 4.0 * d);
+  const double by_fcombine = N * 8.0 * d + Mf * (4.0 + 4.0 * d);
 
   // ---- phase 1: forward
   {
@@ -332,9 +379,34 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       launch_rows<false>(st, LoadSilu{Aa(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiRowScale{p.T1, SG(t), d});
     }
     {
+      // u = h + messages (h^{t+1} itself without the feature-update MoE)
       PROF(PROF_ATOM, 0, by_combine);
       LAUNCH_VPL_K(combine_fwd_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)p.T1,
-                 (const float*)HV(p.h, t), N, d, HV(p.h, t + 1));
+                 (const float*)HV(p.h, t), N, d, atom ? p.ut : HV(p.h, t + 1));
+    }
+    if (atom) {
+      // feature-update MoE: h^{t+1} = u + sum_c g W2f^T SiLU(W1f^T u)
+      const float* W1f = Wp(blk(t, "W1f"));
+      const float* W2f = Wp(blk(t, "W2f"));
+      {
+        PROF(PROF_ATOM, 0, by_fgather);
+        LAUNCH_VPL_K(gather_atom_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), (const float*)nullptr,
+                     (const float*)p.ut, N, d, Xsf(t));
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_atm, 0);
+        launch_rows<false>(st, LoadPlain{Xsf(t), d}, W1f, d, hf, TLF(t), p.ntilesf + t, p.mtf, EpiStore{Af(t), hf});
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_atm, 0);
+        launch_rows<false>(st, LoadSilu{Af(t), hf}, W2f, hf, d, TLF(t), p.ntilesf + t, p.mtf,
+                           EpiRowScale{p.T1f, SGF(t), d});
+      }
+      {
+        PROF(PROF_ATOM, 0, by_fcombine);
+        LAUNCH_VPL_K(combine_fwd_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), (const float*)p.T1f,
+                     (const float*)p.ut, N, d, HV(p.h, t + 1));
+      }
     }
   }
   const float* Wo1 = Wp("W_o1");
@@ -362,10 +434,35 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     const float* Wb = Wp(blk(t, "W_b"));
     const float* W1 = Wp(blk(t, "W1"));
     const float* W2 = Wp(blk(t, "W2"));
+    // dE/du of the message update (dE/dh^{t+1} without the feature-update MoE)
+    const float* hbar_u = HV(p.hh, t + 1);
+    if (atom) {
+      const float* W1f = Wp(blk(t, "W1f"));
+      const float* W2f = Wp(blk(t, "W2f"));
+      {
+        PROF(PROF_ATOM, 0, by_fgather);
+        LAUNCH_VPL_K(gather_atom_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), GATEF(t),
+                     (const float*)HV(p.hh, t + 1), N, d, Ybf(t));
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_atm, 0);
+        launch_rows<true>(st, LoadPlain{Ybf(t), d}, W2f, d, hf, TLF(t), p.ntilesf + t, p.mtf,
+                          EpiP2{Af(t), Sbf(t), Abf(t), hf});
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_atm, 0);
+        launch_rows<true>(st, LoadPlain{Abf(t), hf}, W1f, hf, d, TLF(t), p.ntilesf + t, p.mtf, EpiStore{p.T1f, d});
+      }
+      {
+        PROF(PROF_ATOM, 0, by_fcombine);
+        LAUNCH_VPL_K(combine_fwd_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), (const float*)p.T1f,
+                     (const float*)HV(p.hh, t + 1), N, d, UU(t));
+      }
+      hbar_u = UU(t);
+    }
     {
       PROF(PROF_ATOM, 0, by_gather);
-      LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), (const float*)HV(p.hh, t + 1),
-                 N, d, Ybs(t));
+      LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), hbar_u, N, d, Ybs(t));
     }
     {
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
@@ -408,8 +505,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     {
       PROF(PROF_ATOM, 0, by_scatter);
-      LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe,
-                 (const float*)HV(p.hh, t + 1), (const float*)nullptr, N, d, HV(p.hh, t));
+      LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe, hbar_u,
+                 (const float*)nullptr, N, d, HV(p.hh, t));
     }
   }
   {
@@ -528,9 +625,45 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                    p.partial, Gp(blk(t, "W2")), 1);
     }
     {
+      // adjoint of the gathered dE/du (of hh^{t+1} without the feature-update MoE)
       PROF(PROF_ATOM, 0, by_cp3);
       LAUNCH_VPL_K(combine_p3_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), (const float*)p.T2,
-                 (const float*)HV(p.hh, t + 1), hht_t, N, d, p.g3 + t * M, HV(p.hht, t + 1));
+                   (const float*)(atom ? UU(t) : HV(p.hh, t + 1)), hht_t, N, d, p.g3 + t * M,
+                   atom ? p.ut : HV(p.hht, t + 1));
+    }
+    if (atom) {
+      // double backward of the feature-update MoE's force backward (same products as G5-G8)
+      const float* W1f = Wp(blk(t, "W1f"));
+      const float* W2f = Wp(blk(t, "W2f"));
+      {
+        PROF(PROF_ATOM, 0, by_fgather);
+        LAUNCH_VPL_K(gather_atom_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), (const float*)nullptr,
+                     (const float*)p.ut, N, d, p.T1f);
+      }
+      {
+        PROF(PROF_EXPERT_WGRAD, f_atm, 0);
+        launch_wgrad(st, LoadPlain{p.T1f, d}, LoadPlain{Abf(t), hf}, d, hf, CHF(t), p.nchunksf + t, CFF(t), p.mcf,
+                     Ef, p.partial, Gp(blk(t, "W1f")), 1);
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_atm, 0);
+        launch_rows<false>(st, LoadPlain{p.T1f, d}, W1f, d, hf, TLF(t), p.ntilesf + t, p.mtf,
+                           EpiP3{Af(t), Sbf(t), Abf(t), hf});
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_atm, 0);
+        launch_rows<false>(st, LoadPlain{Abf(t), hf}, W2f, hf, d, TLF(t), p.ntilesf + t, p.mtf, EpiStore{p.T2f, d});
+      }
+      {
+        PROF(PROF_EXPERT_WGRAD, f_atm, 0);
+        launch_wgrad(st, LoadPlain{Abf(t), hf}, LoadPlain{Ybf(t), d}, hf, d, CHF(t), p.nchunksf + t, CFF(t), p.mcf,
+                     Ef, p.partial, Gp(blk(t, "W2f")), 1);
+      }
+      {
+        PROF(PROF_ATOM, 0, by_fcombine + Mf * 8.0 + N * 4.0 * d);
+        LAUNCH_VPL_K(combine_p3_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), GATEF(t), (const float*)p.T2f,
+                     (const float*)HV(p.hh, t + 1), (const float*)p.ut, N, d, p.g3f + t * Mf, HV(p.hht, t + 1));
+      }
     }
   }
   {
@@ -564,11 +697,58 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     const float* W1 = Wp(blk(t, "W1"));
     const float* W2 = Wp(blk(t, "W2"));
     const float* hht_t = t == 0 ? nullptr : HV(p.hht, t);
+    // loss adjoint of u (of h^{t+1} without the feature-update MoE)
+    const float* a_u = HV(p.hh, t + 1);
+    if (atom) {
+      const float* W1f = Wp(blk(t, "W1f"));
+      const float* W2f = Wp(blk(t, "W2f"));
+      {
+        PROF(PROF_ATOM, 0, by_fgather);
+        LAUNCH_VPL_K(gather_atom_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), (const float*)nullptr,
+                     (const float*)HV(p.hh, t + 1), N, d, p.T1f);
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_atm, 0);
+        launch_rows<true>(st, LoadPlain{p.T1f, d}, W2f, d, hf, TLF(t), p.ntilesf + t, p.mtf,
+                          EpiP4{Af(t), Sbf(t), SGF(t), hf}, p.gpartf);
+      }
+      {
+        PROF(PROF_EXPERT_GEMM, f_atm, 0);
+        launch_rows<true>(st, LoadPlain{Sbf(t), hf}, W1f, hf, d, TLF(t), p.ntilesf + t, p.mtf, EpiStore{p.T2f, d});
+      }
+      {
+        PROF(PROF_EXPERT_WGRAD, f_atm, 0);
+        launch_wgrad(st, LoadPlain{Xsf(t), d}, LoadPlain{Sbf(t), hf}, d, hf, CHF(t), p.nchunksf + t, CFF(t), p.mcf,
+                     Ef, p.partial, Gp(blk(t, "W1f")), 1);
+      }
+      {
+        PROF(PROF_EXPERT_WGRAD, f_atm, 0);
+        launch_wgrad(st, LoadSilu{Af(t), hf}, LoadRowScale{p.T1f, SGF(t), d}, hf, d, CHF(t), p.nchunksf + t, CFF(t),
+                     p.mcf, Ef, p.partial, Gp(blk(t, "W2f")), 1);
+      }
+      {
+        PROF(PROF_ATOM, 0, by_fcombine);
+        LAUNCH_VPL_K(combine_fwd_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), (const float*)p.T2f,
+                     (const float*)HV(p.hh, t + 1), N, d, p.ut);
+      }
+      {
+        // feature router: gate adjoints -> logit adjoints per atom -> sums per species
+        PROF(PROF_OTHER, 0, 0);
+        hipLaunchKernelGGL(gate_total_kernel, dim3(cdiv(Mf, 256)), b256, 0, st, (const float*)(p.g3f + t * Mf),
+                           (const float*)p.gpartf, POSF(t), Mf, p.ntilef, p.gtf);
+        hipLaunchKernelGGL(edge_logit_kernel, dim3(cdiv((long long)N * Ef, 256)), b256, 0, st, species,
+                           (const float*)(p.sprob + (long long)t * nsp * Ef), (const int*)(p.eidf + t * Mf),
+                           (const float*)p.gtf, (long long)N, kf, Ef, p.ltf);
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+                           (const int*)p.sp_atoms, (const float*)p.ltf, Ef, nsp, Gp(blk(t, "Pf")));
+      }
+      a_u = p.ut;
+    }
     {
       // message adjoint, ungated, into the slots
       PROF(PROF_ATOM, 0, by_gather);
-      LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)nullptr,
-                 (const float*)HV(p.hh, t + 1), N, d, p.T1);
+      LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)nullptr, a_u, N, d,
+                   p.T1);
     }
     {
       // G9: St = mt W2^T -> At = g SiLU'(A) St + C (into Sb); row sums for the gate adjoint
@@ -684,8 +864,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     {
       PROF(PROF_ATOM, 0, by_scatter + 4.0 * Nd);
-      LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe,
-                 (const float*)HV(p.hh, t + 1), (const float*)HV(p.h3, t), N, d, HV(p.hh, t));
+      LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe, a_u,
+                 (const float*)HV(p.h3, t), N, d, HV(p.hh, t));
     }
   }
   {
@@ -729,6 +909,17 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                                        hipMemcpyDeviceToDevice, st));
         if (dbg->gate3)
           JANUS_HIP_TRY(hipMemcpyAsync(dbg->gate3 + t * Mt3 + f3, p.gate3 + t * M3, sizeof(float) * M3,
+                                       hipMemcpyDeviceToDevice, st));
+      }
+    }
+    if (atom && Mf > 0) {
+      const long long Mtf = (long long)ca.N_tot * kf, ff = (long long)ca.a0 * kf;
+      for (int t = 0; t < T; ++t) {
+        if (dbg->eidf)
+          JANUS_HIP_TRY(hipMemcpyAsync(dbg->eidf + t * Mtf + ff, p.eidf + t * Mf, sizeof(int) * Mf,
+                                       hipMemcpyDeviceToDevice, st));
+        if (dbg->gatef)
+          JANUS_HIP_TRY(hipMemcpyAsync(dbg->gatef + t * Mtf + ff, p.gatef + t * Mf, sizeof(float) * Mf,
                                        hipMemcpyDeviceToDevice, st));
       }
     }

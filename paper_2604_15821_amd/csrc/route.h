@@ -27,7 +27,27 @@ struct RouteArgs {
   float* slot_gate;       // [Ne*k]        gate of the token in each slot
 };
 
+// Routing of the atom tokens of the feature-update MoE (logits Pf[Z_i] + beta).
+struct AtomRouteArgs {
+  const float* Pf;        // [nsp, E]
+  const float* beta;      // [E]
+  const int* species;     // [N]
+  int N, nsp, E, k;
+  int* seid;              // [nsp, k]      chosen experts per species
+  float* sgate;           // [nsp, k]      their gates
+  float* sprob;           // [nsp, E]      full softmax per species
+  int* eid;               // [N, k]
+  float* gate;            // [N, k]
+  int* cnt;               // [sort_chunks(N*k), E] scratch
+  int* colpre;            // [sort_chunks(N*k), E] scratch
+  int* total;             // [E]
+  int* off;               // [E+1]
+  int* pos;               // [N, k]        slot of (atom, choice)
+  float* slot_gate;       // [N*k]
+};
+
 __global__ void zero_ints_kernel(int* p, int n);
+void route_atoms(hipStream_t st, const AtomRouteArgs& a);
 void route_block(hipStream_t st, const RouteArgs& a);
 // Stable counting sort of M tokens (flattened (token, choice) entries with
 // expert ids eid) into expert-grouped slots: total[E], off[E+1], pos[M],

@@ -8,7 +8,9 @@
 // taken in descending logit order with the lower index first on ties; the
 // gate of a chosen expert is its probability under the softmax over all
 // experts.  Because the logits depend only on the species pair, the decision
-// is made once per pair and looked up per edge.  Tokens are then grouped by
+// is made once per pair and looked up per edge.  The feature-update MoE
+// routes atom tokens the same way with logits Pf[Z_i] + betaf, decided once
+// per species.  Tokens are then grouped by
 // expert with a stable counting sort on (expert, edge, choice), which fixes
 // the slot of every (edge, choice) pair exactly.
 #include "internal.h"
@@ -18,25 +20,22 @@ namespace janus {
 
 constexpr int kSortChunk = 4096;
 
-// One thread per species pair p = a * n_species + b.
-__global__ void route_pairs_kernel(const float* __restrict__ Pc, const float* __restrict__ Pn,
-                                   const float* __restrict__ beta, int nsp, int E, int k,
-                                   int* __restrict__ peid, float* __restrict__ pgate, float* __restrict__ pprob) {
-  const int p = blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= nsp * nsp) return;
-  const int a = p / nsp, b = p % nsp;
+// Top-k (descending fp32 logit, lower index first on ties) and gates (softmax
+// over all E experts, evaluated in fp64) of one logit row; l32(x) and l64(x)
+// give the logit of expert x in fp32 and fp64.
+template <class L32, class L64>
+__device__ void topk_softmax(L32 l32, L64 l64, int E, int k, int* __restrict__ eid, float* __restrict__ gate,
+                             float* __restrict__ prob) {
   float l[64];
   double mx = -1e300;
   for (int x = 0; x < E; ++x) {
-    l[x] = __fadd_rn(__fadd_rn(Pc[a * E + x], Pn[b * E + x]), beta[x]);
-    double ld = ((double)Pc[a * E + x] + (double)Pn[b * E + x]) + (double)beta[x];
+    l[x] = l32(x);
+    const double ld = l64(x);
     mx = ld > mx ? ld : mx;
   }
   double den = 0.0;
-  for (int x = 0; x < E; ++x) den += exp((((double)Pc[a * E + x] + (double)Pn[b * E + x]) + (double)beta[x]) - mx);
-  for (int x = 0; x < E; ++x)
-    pprob[(long long)p * E + x] =
-        (float)(exp((((double)Pc[a * E + x] + (double)Pn[b * E + x]) + (double)beta[x]) - mx) / den);
+  for (int x = 0; x < E; ++x) den += exp(l64(x) - mx);
+  for (int x = 0; x < E; ++x) prob[x] = (float)(exp(l64(x) - mx) / den);
   unsigned long long taken = 0;
   for (int c = 0; c < k; ++c) {
     int best = -1;
@@ -45,9 +44,45 @@ __global__ void route_pairs_kernel(const float* __restrict__ Pc, const float* __
       if (best < 0 || l[x] > l[best]) best = x;
     }
     taken |= 1ull << best;
-    peid[p * k + c] = best;
-    pgate[p * k + c] =
-        (float)(exp((((double)Pc[a * E + best] + (double)Pn[b * E + best]) + (double)beta[best]) - mx) / den);
+    eid[c] = best;
+    gate[c] = (float)(exp(l64(best) - mx) / den);
+  }
+}
+
+// One thread per species pair p = a * n_species + b.
+__global__ void route_pairs_kernel(const float* __restrict__ Pc, const float* __restrict__ Pn,
+                                   const float* __restrict__ beta, int nsp, int E, int k,
+                                   int* __restrict__ peid, float* __restrict__ pgate, float* __restrict__ pprob) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= nsp * nsp) return;
+  const float* pa = Pc + (long long)(p / nsp) * E;
+  const float* pb = Pn + (long long)(p % nsp) * E;
+  topk_softmax([&](int x) { return __fadd_rn(__fadd_rn(pa[x], pb[x]), beta[x]); },
+               [&](int x) { return ((double)pa[x] + (double)pb[x]) + (double)beta[x]; }, E, k, peid + p * k,
+               pgate + p * k, pprob + (long long)p * E);
+}
+
+// Feature-update MoE, one thread per species a: logits Pf[a] + betaf.
+__global__ void route_species_kernel(const float* __restrict__ Pf, const float* __restrict__ beta, int nsp, int E,
+                                     int k, int* __restrict__ seid, float* __restrict__ sgate,
+                                     float* __restrict__ sprob) {
+  const int a = blockIdx.x * blockDim.x + threadIdx.x;
+  if (a >= nsp) return;
+  const float* pa = Pf + (long long)a * E;
+  topk_softmax([&](int x) { return __fadd_rn(pa[x], beta[x]); },
+               [&](int x) { return (double)pa[x] + (double)beta[x]; }, E, k, seid + a * k, sgate + a * k,
+               sprob + (long long)a * E);
+}
+
+// Per atom: chosen experts and gates of its species.
+__global__ void route_atoms_kernel(const int* __restrict__ species, int N, int k, const int* __restrict__ seid,
+                                   const float* __restrict__ sgate, int* __restrict__ eid, float* __restrict__ gate) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const int z = species[i];
+  for (int c = 0; c < k; ++c) {
+    eid[(long long)i * k + c] = seid[z * k + c];
+    gate[(long long)i * k + c] = sgate[z * k + c];
   }
 }
 
@@ -159,6 +194,15 @@ void route_block(hipStream_t st, const RouteArgs& a) {
     hipLaunchKernelGGL(route_edges_kernel, dim3(cdiv(a.Ne, 256)), dim3(256), 0, st, a.species, a.ei, a.ej, a.Ne,
                        a.nsp, a.k, a.peid, a.pgate, a.pair, a.eid, a.gate);
   sort_tokens(st, a.eid, a.gate, (long long)a.Ne * a.k, a.E, a.cnt, a.colpre, a.total, a.off, a.pos, a.slot_gate);
+}
+
+void route_atoms(hipStream_t st, const AtomRouteArgs& a) {
+  hipLaunchKernelGGL(route_species_kernel, dim3(cdiv(a.nsp, 64)), dim3(64), 0, st, a.Pf, a.beta, a.nsp, a.E, a.k,
+                     a.seid, a.sgate, a.sprob);
+  if (a.N > 0)
+    hipLaunchKernelGGL(route_atoms_kernel, dim3(cdiv(a.N, 256)), dim3(256), 0, st, a.species, a.N, a.k, a.seid,
+                       a.sgate, a.eid, a.gate);
+  sort_tokens(st, a.eid, a.gate, (long long)a.N * a.k, a.E, a.cnt, a.colpre, a.total, a.off, a.pos, a.slot_gate);
 }
 
 void sort_tokens(hipStream_t st, const int* eid, const float* gate, long long M, int E, int* cnt, int* colpre,

@@ -459,8 +459,10 @@ int check_config(const janus_config* c) {
       return JANUS_EUNSUPPORTED;
   }
   if (c->atom_moe) {
-    // the step does not run the feature-update MoE yet
-    return JANUS_EUNSUPPORTED;
+    if (c->n_experts_f < 1 || c->n_experts_f > 64 || c->top_k_f < 1 || c->top_k_f > 4 ||
+        c->top_k_f > c->n_experts_f || c->d_hidden_f < 64)
+      return JANUS_EINVAL;
+    if (c->d_hidden_f % 64) return JANUS_EUNSUPPORTED;
   }
   return JANUS_OK;
 }
@@ -513,6 +515,16 @@ struct Plan {
   int *ncT, *cfT;
   float *Z3s, *A3, *S3b, *A3b, *Y3bs, *Zbar3;
   float *Q, *LT3, *VT, *G3f, *G3t, *T3a, *T3b, *gpart3, *gt3, *LB, *LC, *pa, *pb, *pc;
+  // feature-update MoE: atom tokens (one row per atom in an identity CSR),
+  // per-block routing by species, GEMM tables, activations and adjoints
+  int* iota;
+  int *seid, *eidf, *posf, *totalf, *offf, *cntf, *colpref;
+  float *sgate, *sprob, *gatef, *slot_gatef, *g3f;
+  RowsTile* tilesf;
+  int* ntilesf;
+  WChunk* chunksf;
+  int *nchunksf, *cfirstf;
+  float *Xsf, *Af, *Sbf, *Abf, *Ybf, *uu, *T1f, *T2f, *ut, *gpartf, *gtf, *ltf;
   // sizes
   int T, E, k, d, hdim, nb, nsp, N, S;
   long long Ne, M;
@@ -520,6 +532,9 @@ struct Plan {
   int three, E3, k3, hd3, L3, nf;
   long long Nt, M3;
   int mt3, mc3, kc3, kcT, mcT, nch3, ntile3;
+  int atom, Ef, kf, hdf;
+  long long Mf;
+  int mtf, kcf, mcf, nchf, ntilef;
 };
 
 size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, long long Ne, long long Nt = 0) {
@@ -631,6 +646,19 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
                               c.d_hidden3);
     part = std::max(part, (long long)max_wchunks(Nt, 1, wgrad_chunk_rows(Nt, nf, d)) * nf * d);
   }
+  p.atom = c.atom_moe ? 1 : 0;
+  p.Ef = c.n_experts_f;
+  p.kf = c.top_k_f;
+  p.hdf = c.d_hidden_f;
+  p.Mf = p.atom ? (long long)N * c.top_k_f : 0;
+  if (p.atom) {
+    p.mtf = max_rows_tiles(p.Mf, p.Ef);
+    p.kcf = wgrad_chunk_rows(p.Mf, d, p.hdf);
+    p.mcf = max_wchunks(p.Mf, p.Ef, p.kcf);
+    p.nchf = sort_chunks(p.Mf);
+    p.ntilef = (p.hdf + GBN - 1) / GBN;
+    part = std::max(part, (long long)p.mcf * d * p.hdf);
+  }
   p.partial = cv.take<float>(part);
   p.cei = cv.take<int>(Ne + 1);
   p.cej = cv.take<int>(Ne + 1);
@@ -707,7 +735,46 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.pb = cv.take<float>((long long)N * E3 + 1);
     p.pc = cv.take<float>((long long)N * E3 + 1);
   }
+  if (p.atom) {
+    const long long Mf = p.Mf, Ef = p.Ef, kf = p.kf, hf = p.hdf;
+    p.iota = cv.take<int>(N + 1);
+    p.seid = cv.take<int>(T * p.nsp * kf);
+    p.sgate = cv.take<float>(T * p.nsp * kf);
+    p.sprob = cv.take<float>(T * p.nsp * Ef);
+    p.eidf = cv.take<int>(T * Mf + 1);
+    p.gatef = cv.take<float>(T * Mf + 1);
+    p.posf = cv.take<int>(T * Mf + 1);
+    p.slot_gatef = cv.take<float>(T * Mf + 1);
+    p.g3f = cv.take<float>(T * Mf + 1);
+    p.totalf = cv.take<int>(T * Ef);
+    p.offf = cv.take<int>(T * (Ef + 1));
+    p.cntf = cv.take<int>((long long)p.nchf * Ef + 1);
+    p.colpref = cv.take<int>((long long)p.nchf * Ef + 1);
+    p.tilesf = cv.take<RowsTile>((long long)T * p.mtf);
+    p.ntilesf = cv.take<int>(T + 1);
+    p.chunksf = cv.take<WChunk>((long long)T * p.mcf);
+    p.nchunksf = cv.take<int>(T + 1);
+    p.cfirstf = cv.take<int>(T * (Ef + 1) + 1);
+    p.Xsf = cv.take<float>(T * Mf * d + 4);
+    p.Af = cv.take<float>(T * Mf * hf + 4);
+    p.Sbf = cv.take<float>(T * Mf * hf + 4);
+    p.Abf = cv.take<float>(T * Mf * hf + 4);
+    p.Ybf = cv.take<float>(T * Mf * d + 4);
+    p.uu = cv.take<float>(T * Nd + 4);
+    p.T1f = cv.take<float>(Mf * d + 4);
+    p.T2f = cv.take<float>(Mf * d + 4);
+    p.ut = cv.take<float>(Nd + 4);
+    p.gpartf = cv.take<float>(Mf * p.ntilef + 4);
+    p.gtf = cv.take<float>(Mf + 1);
+    p.ltf = cv.take<float>((long long)N * Ef + 1);
+  }
   return cv.size();
+}
+
+// Identity CSR [0, 1, ..., N]: every atom is one token of the feature-update MoE.
+__global__ void iota_kernel(int* __restrict__ out, int n) {
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q <= n) out[q] = q;
 }
 
 __global__ void set_rows_kernel(int* rowN, int N, int* rowE, long long Ne) {

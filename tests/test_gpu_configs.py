@@ -2,7 +2,9 @@
 embedding width 256 and 512 with the three-body term, top-k of 3 and 4,
 expert counts that are not powers of two, hidden widths that leave a partial
 64-column GEMM tile (192, 320), few Legendre orders and basis functions,
-and Zipf-skewed routing on a crystal/molecule mix (empty experts)."""
+Zipf-skewed routing on a crystal/molecule mix (empty experts), and the
+feature-update MoE at top-k 1, 3 and 4 (alone, with the three-body term,
+and with every expert chosen)."""
 import numpy as np
 import pytest
 
@@ -29,6 +31,19 @@ def _configs():
             "3b-d512", "cubic", 1, 32, 0.08,
             ModelConfig(d=512, n_rbf=8, n_blocks=1, n_experts=2, top_k=2, d_hidden=64, r_cut=5.0, three_body=True,
                         r_cut3=3.5, n_experts3=4, top_k3=4, d_hidden3=64, n_legendre=4), seed=11),
+        "atom-d64-kf1-Ef5-hf192": Workload(
+            "atom-d64", "cubic", 4, 20, 0.08,
+            ModelConfig(d=64, n_rbf=8, n_blocks=2, n_experts=3, top_k=2, d_hidden=128, r_cut=4.5, atom_moe=True,
+                        n_experts_f=5, top_k_f=1, d_hidden_f=192), seed=13),
+        "3b-atom-d128-kf3-Ef6": Workload(
+            "3b-atom", "cubic", 2, 24, 0.08,
+            ModelConfig(d=128, n_rbf=8, n_blocks=2, n_experts=4, top_k=2, d_hidden=128, r_cut=4.5, three_body=True,
+                        r_cut3=3.5, n_experts3=3, top_k3=2, d_hidden3=64, n_legendre=3, atom_moe=True,
+                        n_experts_f=6, top_k_f=3, d_hidden_f=128), seed=17),
+        "atom-d256-kf4-Ef4-hf320-zipf": Workload(
+            "atom-zipf", "mixed", 5, 0, 0.1,
+            ModelConfig(d=256, n_rbf=8, n_blocks=1, n_experts=6, top_k=2, d_hidden=64, r_cut=4.0, atom_moe=True,
+                        n_experts_f=4, top_k_f=4, d_hidden_f=320), seed=19, size_lo=6, size_hi=30, zipf_s=1.2),
     }
 
 
@@ -83,7 +98,7 @@ def test_weight_gradients(case):
     got = janus.unpack(out["dW"], b.model)
     worst = 0.0
     for name, ref in grad.items():
-        if name.endswith("beta") or name.endswith("beta3"):
+        if name.rsplit(".", 1)[-1] in ("beta", "beta3", "betaf"):
             assert not got[name].any(), name
             continue
         if not ref.any():

@@ -8,7 +8,8 @@ from helpers import TOL_E, TOL_F, TOL_LOSS, TOL_W, banner, energy_error, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-STEP_CASES = [("tiny", None), ("small", 4), ("threebody", 2)]
+STEP_CASES = [("tiny", None), ("small", 4), ("threebody", 2), ("atom_moe", 4)]
+FIXED = ("beta", "beta3", "betaf")
 
 
 def _batch(name, n):
@@ -31,6 +32,10 @@ def _run(b, debug=True, reps=1, n_triplets=0):
                "gate": torch.empty(T * Ne * k, device="cuda:0"),
                "counts": torch.empty(T * m.n_experts, dtype=torch.int32, device="cuda:0"),
                "pos": torch.empty(T * Ne * k, dtype=torch.int32, device="cuda:0")}
+        if m.atom_moe:
+            nf = T * b.n_atoms * m.top_k_f
+            dbg.update({"eidf": torch.empty(nf, dtype=torch.int32, device="cuda:0"),
+                        "gatef": torch.empty(nf, device="cuda:0")})
         if n_triplets:
             n3 = T * n_triplets * m.top_k3
             dbg.update({"tri_e": torch.empty(n_triplets, dtype=torch.int32, device="cuda:0"),
@@ -75,6 +80,18 @@ def test_triplets_and_their_routing_are_bit_exact(case):
         assert np.abs(dbg["gate3"][sl].reshape(nt, k3) - rt.tri.gate).max() <= 1e-6
 
 
+def test_atom_routing_is_bit_exact(case):
+    b, outs, dbg, Ne, (loss, E, F, grad, aux) = case
+    m = b.model
+    if not m.atom_moe:
+        pytest.skip("workload without the feature-update MoE")
+    N, kf = b.n_atoms, m.top_k_f
+    for t, rt in enumerate(aux["routing"]):
+        sl = slice(t * N * kf, (t + 1) * N * kf)
+        assert (dbg["eidf"][sl].reshape(N, kf) == rt.atom.eid).all()
+        assert np.abs(dbg["gatef"][sl].reshape(N, kf) - rt.atom.gate).max() <= 1e-6
+
+
 def test_routing_is_bit_exact(case):
     b, outs, dbg, Ne, (loss, E, F, grad, aux) = case
     m = b.model
@@ -111,7 +128,7 @@ def test_weight_gradients(case):
     got = janus.unpack(outs[0][3], b.model)
     worst = {}
     for name, ref in grad.items():
-        if name.endswith("beta"):
+        if name.rsplit(".", 1)[-1] in FIXED:
             assert (got[name] == 0).all()
             continue
         worst[name] = rel_l2(got[name], ref)
