@@ -208,11 +208,14 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "structures": S, "atoms": N, "edges": Ne, "d": m.d,
                    "d_hidden": m.d_hidden, "experts": m.n_experts, "top_k": m.top_k, "blocks": m.n_blocks,
-                   "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none"},
+                   "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none",
+                   **({"atom_moe": {"experts": m.n_experts_f, "top_k": m.top_k_f, "d_hidden": m.d_hidden_f}}
+                      if m.atom_moe else {})},
         "edges_per_s": Ne / (ms * 1e-3),
         "triplets": Nt,
         "triplets_per_s": Nt / (ms * 1e-3),
-        "expert_gemm_flops_per_step": 24.0 * m.top_k * m.d * m.d_hidden * Ne * m.n_blocks,
+        "expert_gemm_flops_per_step": 24.0 * m.top_k * m.d * m.d_hidden * Ne * m.n_blocks
+        + (24.0 * m.top_k_f * m.d * m.d_hidden_f * N * m.n_blocks if m.atom_moe else 0.0),
         "roofline": roof,
         "kernels": kernels,
     }
