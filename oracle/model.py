@@ -317,6 +317,26 @@ def _block_tokens(g, P, t, h, routing):
 def forces(species, g: Graph, P: Params, routing, cache):
     """Conservative forces F = -dE/dR by one hand-derived reverse sweep."""
     N = species.shape[0]
+    G = energy_displacement_gradient(species, g, P, routing, cache)
+    dEdR = _seg(g.ej, N, G) - _seg(g.ei, N, G)
+    return -dEdR
+
+
+def stress(g: Graph, G, cell):
+    """Stress of every structure from G_e = dE/dd_e (paper Sec. "MatRIS": the stress is
+    the strain derivative of the energy over the cell volume).  A strain eps maps every
+    displacement d_e to (I + eps) d_e, so dE/deps_ab = sum_e G_e,a d_e,b and
+    sigma_s = (1/V_s) sum_{e in s} G_e d_e^T, V_s = |det L_s|."""
+    S = g.n_atoms_struct.size
+    W = np.zeros((S, 3, 3))
+    np.add.at(W, g.struct_of_atom[g.ei], G[:, :, None] * g.d[:, None, :])
+    V = np.abs(np.linalg.det(np.asarray(cell, np.float64)))
+    return W / V[:, None, None]
+
+
+def energy_displacement_gradient(species, g: Graph, P: Params, routing, cache):
+    """G_e = dE/dd_e of every edge, by one hand-derived reverse sweep."""
+    N = species.shape[0]
     Ne = g.ei.shape[0]
     hs, us, z = cache["h"], cache["u"], cache["z"]
     hbar = (silu_d1(z) * P.w["w_o2"][None, :]) @ P.w["W_o1"].T      # dE/dh^T
@@ -338,9 +358,7 @@ def forces(species, g: Graph, P: Params, routing, cache):
         Fbar = Xbar * h[g.ej]
         rbar += ((Fbar @ P.blk(t, "W_b").T) * g.dB).sum(1)
         hbar = hbar_next
-    G = rbar[:, None] * g.u + Gvec                                    # dE/dd_e
-    dEdR = _seg(g.ej, N, G) - _seg(g.ei, N, G)
-    return -dEdR
+    return rbar[:, None] * g.u + Gvec                                 # dE/dd_e
 
 
 def loss_and_seeds(E, F, E_ref, F_ref, n_atoms_struct, w_E=1.0, w_F=1.0):
@@ -399,14 +417,34 @@ def _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing):
     return F, Fd, X, Xd
 
 
-def energy_tangent(species, g: Graph, P: Params, routing, phi):
-    """Tangent forward sweep along positions R + e*phi.
+def stress_loss_and_seed(sigma, S_ref, n_struct_total, w_S):
+    """Stress term of the loss, w_S/(9S) sum_s |sigma_s - S_ref,s|_F^2, and its seed
+    psi_s = dL/dsigma_s (paper Sec. "Multi-task training strategies" names stress among
+    the errors of the base loss; reading: mean-squared error like the other terms)."""
+    ds = sigma - np.asarray(S_ref, np.float64)
+    return w_S * (ds * ds).sum() / (9.0 * n_struct_total), 2.0 * w_S * ds / (9.0 * n_struct_total)
 
-    Returns (D_phi E_tot, cache) where cache holds per-block primal and
+
+def displacement_tangent(g: Graph, phi, Psi=None):
+    """Tangent of every displacement along the combined direction of the force and
+    stress seeds: phi_j - phi_i - Psi_s d_e with Psi_s = psi_s / V_s.  Along it,
+    -D E = -D_phi E + sum_s (1/V_s) psi_s : dE/deps_s, so the weight gradient of
+    sum_s lam_s E_s - D E is that of the energy + force + stress loss."""
+    ddot = phi[g.ej] - phi[g.ei]
+    if Psi is not None:
+        ddot = ddot - np.einsum("eab,eb->ea", Psi[g.struct_of_atom[g.ei]], g.d)
+    return ddot
+
+
+def energy_tangent(species, g: Graph, P: Params, routing, phi, Psi=None):
+    """Tangent forward sweep along positions R + e*phi (and, with Psi, the strain
+    direction of the stress seeds).
+
+    Returns (D E_tot, cache) where cache holds per-block primal and
     tangent atom features for the reverse sweep.
     """
     N = species.shape[0]
-    ddot = phi[g.ej] - phi[g.ei]                                       # d(d_e)/de
+    ddot = displacement_tangent(g, phi, Psi)                          # d(d_e)/de
     rdot = (ddot * g.u).sum(1)                                         # dr_e/de
     Bdot = g.dB * rdot[:, None]
     Gd = tb.feature_tangent(g.tri, g.r, g.u, ddot) if g.tri is not None else None
@@ -467,14 +505,15 @@ def _logit_adjoint(rt, Pg):
     return rt.prob * (Pp - (rt.prob * Pp).sum(1, keepdims=True))
 
 
-def weight_gradient(species, g: Graph, P: Params, routing, lam, phi):
-    """dL/dtheta = d/dtheta [sum_s lam_s E_s - D_phi E] by reverse over the tangent sweep.
+def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
+    """dL/dtheta = d/dtheta [sum_s lam_s E_s - D_phi E] by reverse over the tangent sweep
+    (with Psi, the tangent also carries the strain direction of the stress seeds).
 
     Adjoint names: Pq is the adjoint of primal q, Tq the adjoint of tangent q.
     """
     N = species.shape[0]
     Ne = g.ei.shape[0]
-    _, tc = energy_tangent(species, g, P, routing, phi)
+    _, tc = energy_tangent(species, g, P, routing, phi, Psi)
     hs, hds, z, zd, Bdot, Gd = tc["h"], tc["hd"], tc["z"], tc["zd"], tc["Bdot"], tc["Gd"]
     wo1, wo2 = P.w["W_o1"], P.w["w_o2"]
     grad = {n: np.zeros_like(v) for n, v in P.w.items()}
@@ -543,18 +582,28 @@ def training_step(batch, edges=None, return_aux=False):
     """One full training step on a synthetic batch.
 
     Returns loss, E [S], F [N,3], grad (dict name -> float64 array with the
-    weight's shape).  With return_aux, also the graph and routing.
+    weight's shape).  With return_aux, also the graph, the routing and the
+    stress [S,3,3].  With w_S > 0 the loss has the stress term.
     """
     m = batch.model
     P = Params.from_weights(batch.weights, m)
     g = build_graph_for(batch, edges)
     routing = route_all(batch.species, g, P)
     E, cache = forward_energy(batch.species, g, P, routing)
-    F = forces(batch.species, g, P, routing, cache)
+    G = energy_displacement_gradient(batch.species, g, P, routing, cache)
+    N = batch.species.shape[0]
+    F = _seg(g.ei, N, G) - _seg(g.ej, N, G)
+    sigma = stress(g, G, batch.cell)
     loss, lam, phi = loss_and_seeds(E, F, batch.E_ref, batch.F_ref, g.n_atoms_struct, m.w_E, m.w_F)
-    grad = weight_gradient(batch.species, g, P, routing, lam, phi)
+    Psi = None
+    if m.w_S:
+        loss_S, psi = stress_loss_and_seed(sigma, batch.S_ref, E.shape[0], m.w_S)
+        loss = loss + loss_S
+        Psi = psi / np.abs(np.linalg.det(np.asarray(batch.cell, np.float64)))[:, None, None]
+    grad = weight_gradient(batch.species, g, P, routing, lam, phi, Psi)
     if return_aux:
-        return loss, E, F, grad, {"graph": g, "routing": routing, "lam": lam, "phi": phi}
+        return loss, E, F, grad, {"graph": g, "routing": routing, "lam": lam, "phi": phi, "stress": sigma,
+                                  "Psi": Psi}
     return loss, E, F, grad
 
 

@@ -36,6 +36,8 @@ class ModelConfig:
     optional angular term (triplets of bonds shorter than r_cut3).  The
     atom_moe fields describe the optional feature-update MoE of every block
     (atom tokens routed by element type; each expert d -> d_hidden_f -> d).
+    w_E, w_F, w_S weigh the energy, force and stress terms of the loss (stress
+    in eV/A^3; w_S = 0 leaves it out).
     """
 
     d: int
@@ -59,6 +61,7 @@ class ModelConfig:
     n_experts_f: int = 0
     top_k_f: int = 0
     d_hidden_f: int = 0
+    w_S: float = 0.0
 
     def weight_shapes(self):
         """Named weight tensors in blob order, with the fan-in used at init.
@@ -137,6 +140,8 @@ _M_TINY = ModelConfig(d=64, n_rbf=8, n_blocks=2, n_experts=4, top_k=1, d_hidden=
 _M_SMALL = ModelConfig(d=128, n_rbf=16, n_blocks=3, n_experts=8, top_k=2, d_hidden=512, r_cut=5.0)
 _M_3B = dataclasses.replace(_M_SMALL, three_body=True, r_cut3=3.5, n_experts3=8, top_k3=2, d_hidden3=256)
 _M_ATOM = dataclasses.replace(_M_SMALL, atom_moe=True, n_experts_f=8, top_k_f=2, d_hidden_f=512)
+# stress weight 0.1 on stresses measured in GPa (1 eV/A^3 = 160.2177 GPa)
+_M_STRESS = dataclasses.replace(_M_SMALL, w_S=0.1 * 160.2177 ** 2)
 _M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
 
 WORKLOADS = {
@@ -144,6 +149,7 @@ WORKLOADS = {
     "small": Workload("small", "ortho", 64, 64, 0.08, _M_SMALL),
     "threebody": Workload("threebody", "ortho", 64, 64, 0.08, _M_3B),
     "atom_moe": Workload("atom_moe", "ortho", 64, 64, 0.08, _M_ATOM),
+    "stress": Workload("stress", "ortho", 64, 64, 0.08, _M_STRESS),
     "shard": Workload("shard", "cubic", 256, 128, 0.1, _M_BIG),
     "irregular": Workload("irregular", "mixed", 512, 0, 0.1, _M_BIG, zipf_s=1.2),
 }
@@ -160,6 +166,7 @@ class Batch:
     E_ref: np.ndarray        # [S] per-atom reference energy of each structure
     F_ref: np.ndarray        # [N, 3]
     weights: dict = field(default_factory=dict)   # name -> float32 array
+    S_ref: np.ndarray | None = None   # [S, 3, 3] reference stress (eV/A^3), symmetric
     model: ModelConfig | None = None
     name: str = ""
 
@@ -252,6 +259,10 @@ def make_batch(wl: Workload | str, seed: int | None = None, n_struct: int | None
     weights = _draw_weights(rng, m, wl.zipf_s)
     E_ref = rng.standard_normal(S).astype(np.float32)
     F_ref = rng.standard_normal((N, 3)).astype(np.float32)
+    # 7. reference stresses: (a + a^T)/sqrt(2) GPa for a standard Gaussian a
+    #    (off-diagonal variance 1 GPa^2, diagonal 2 GPa^2), stored in eV/A^3
+    a = rng.standard_normal((S, 3, 3))
+    S_ref = ((a + a.transpose(0, 2, 1)) / np.sqrt(2.0) / 160.2177).astype(np.float32)
 
     cell = np.zeros((S, 3, 3), np.float32)
     for s in range(S):
@@ -259,7 +270,7 @@ def make_batch(wl: Workload | str, seed: int | None = None, n_struct: int | None
     offsets = np.zeros(S + 1, np.int32)
     offsets[1:] = np.cumsum(sizes)
     return Batch(pos=pos, cell=cell, species=species, offsets=offsets, E_ref=E_ref,
-                 F_ref=F_ref, weights=weights, model=m, name=wl.name)
+                 F_ref=F_ref, weights=weights, model=m, name=wl.name, S_ref=S_ref)
 
 
 def subset(batch: Batch, structs) -> Batch:
@@ -275,4 +286,5 @@ def subset(batch: Batch, structs) -> Batch:
     return Batch(pos=np.concatenate(pos, 0), cell=batch.cell[structs].copy(),
                  species=np.concatenate(spc, 0), offsets=off, E_ref=batch.E_ref[structs].copy(),
                  F_ref=np.concatenate(fref, 0), weights=batch.weights, model=batch.model,
-                 name=batch.name + "[sub]")
+                 name=batch.name + "[sub]",
+                 S_ref=None if batch.S_ref is None else batch.S_ref[structs].copy())
