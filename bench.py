@@ -128,11 +128,14 @@ def main():
     N, S = b.n_atoms, b.n_struct
     out = (torch.empty(1, device="cuda:0"), torch.empty(S, device="cuda:0"), torch.empty(N, 3, device="cuda:0"),
            torch.empty_like(d["W"]))
+    # with a stress weight the step also returns the stress and trains on it
+    stress = dict(S_ref=d["S_ref"], stress=torch.empty(S, 3, 3, device="cuda:0")) if m.w_S else {}
 
     def step():
         ne = ctx.build_edges_into(d["pos"], d["cell"], d["offsets"], nl)
         assert ne == Ne
-        ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"], out=out)
+        ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"], out=out,
+                 **stress)
 
     log(f"workload {args.workload}: {S} structures, {N} atoms, {Ne} edges, d={m.d} h={m.d_hidden} "
         f"E={m.n_experts} k={m.top_k} T={m.n_blocks}")
@@ -194,7 +197,8 @@ def main():
                 "bytes_per_launch": r["bytes"] / r["launches"], "avg_launch_ms": r["ms"] / r["launches"]}
 
     res = {
-        "metric": "atoms/s per training step (E+F+2nd-order dL/dW) on 1 MI355X",
+        "metric": "atoms/s per training step (E+F+2nd-order dL/dW) on 1 MI355X"
+        + (" with the stress term" if m.w_S else ""),
         "value": N / (ms * 1e-3),
         "unit": "atoms/s",
         "n_gpus": 1,
@@ -210,7 +214,8 @@ def main():
                    "d_hidden": m.d_hidden, "experts": m.n_experts, "top_k": m.top_k, "blocks": m.n_blocks,
                    "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none",
                    **({"atom_moe": {"experts": m.n_experts_f, "top_k": m.top_k_f, "d_hidden": m.d_hidden_f}}
-                      if m.atom_moe else {})},
+                      if m.atom_moe else {}),
+                   **({"stress_weight": m.w_S} if m.w_S else {})},
         "edges_per_s": Ne / (ms * 1e-3),
         "triplets": Nt,
         "triplets_per_s": Nt / (ms * 1e-3),

@@ -80,6 +80,8 @@ enum {
  *              top_k_f (1..4) of n_experts_f (1..64) experts chosen by the
  *              logits Pf[Z_i] + betaf; each expert d -> d_hidden_f -> d
  *              (d_hidden_f a multiple of 64)
+ *   w_S        loss weight of the stress term (>= 0; 0 leaves it out; used by
+ *              janus_step_stress, stresses in energy / length^3)
  */
 typedef struct janus_config {
   int32_t n_species;
@@ -103,6 +105,7 @@ typedef struct janus_config {
   int32_t n_experts_f;
   int32_t top_k_f;
   int32_t d_hidden_f;
+  float w_S;
 } janus_config;
 
 typedef struct janus_ctx janus_ctx;
@@ -239,6 +242,27 @@ int janus_step(janus_ctx* ctx, const float* pos, const float* cell, const int32_
                const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
                const float* W, const float* E_ref, const float* F_ref, float* loss, float* E,
                float* F, float* dLdW, const janus_debug* dbg, void* stream);
+
+/*
+ * janus_step with stress (paper Sec. "MatRIS": the stress is the strain
+ * derivative of the energy over the cell volume, sigma = (1/V) dE/deps; Sec.
+ * "Multi-task training strategies": stress is one of the errors of the base
+ * loss).  A strain eps maps every displacement d_e to (I + eps) d_e, so
+ *     sigma_s[a][b] = (1/V_s) sum over the edges of s of (dE/dd_e)_a (d_e)_b,
+ * V_s = |det| of the cell rows.  With cfg.w_S > 0 the loss gains
+ *     w_S/(9S) * sum_s sum_ab (sigma_s[a][b] - S_ref_s[a][b])^2
+ * and dLdW includes its second-order gradient.
+ *   S_ref  [S*9] reference stress per structure, row-major 3x3; required when
+ *          cfg.w_S > 0 (JANUS_EINVAL otherwise), ignored when cfg.w_S = 0
+ *   stress [S*9] output stress per structure, row-major 3x3; may be NULL
+ * Every other argument, output and error is as for janus_step, which is this
+ * call with S_ref = stress = NULL.
+ */
+int janus_step_stress(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
+                      const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
+                      const float* W, const float* E_ref, const float* F_ref, const float* S_ref,
+                      float* loss, float* E, float* F, float* stress, float* dLdW,
+                      const janus_debug* dbg, void* stream);
 
 /*
  * Workspace of janus_step.  Structures are independent apart from the loss

@@ -121,8 +121,8 @@ __global__ void copy_add_kernel(int* __restrict__ dst, const int* __restrict__ s
 
 int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const ChunkArgs& ca, const float* pos_g,
               const float* cell_g, const int32_t* species_g, const int32_t* offsets_g, const janus_edges* nl,
-              const float* W, const float* E_ref_g, const float* F_ref_g, double* loss_part, float* E_g, float* F_g,
-              float* dLdW, const janus_debug* dbg) {
+              const float* W, const float* E_ref_g, const float* F_ref_g, const float* S_ref_g, double* loss_part,
+              float* E_g, float* F_g, float* stress_g, float* dLdW, const janus_debug* dbg) {
   const janus_config& cfg = ctx->cfg;
   const int T = p.T, Ee = p.E, k = p.k, d = p.d, h = p.hdim, nb = p.nb, nsp = p.nsp;
   const int N = ca.N, S = ca.S;
@@ -137,6 +137,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   const float* F_ref = F_ref_g + 3LL * ca.a0;
   float* E = E_g + ca.s0;
   float* F = F_g + 3LL * ca.a0;
+  const float* S_ref = S_ref_g ? S_ref_g + 9LL * ca.s0 : nullptr;
+  float* stress_out = stress_g ? stress_g + 9LL * ca.s0 : nullptr;
   {
     PROF(PROF_OTHER, 0, Ne * 24.0);
     const long long nthr = std::max<long long>(Ne, std::max(N, S) + 1);
@@ -517,15 +519,20 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                          (const float4*)p.tacc, Ne, p.gvec);
     hipLaunchKernelGGL(force_kernel, dim3(cdiv(N, 256)), b256, 0, st, rowptr, rev, (const float*)p.rbar,
                        (const float4*)p.geo, (const float4*)(three ? p.gvec : nullptr), N, F);
+    if (S_ref || stress_out)
+      hipLaunchKernelGGL(stress_kernel, wave_grid(S), b256, 0, st, rowptr, offsets, cell, (const float*)p.rbar,
+                         (const float4*)p.geo, (const float4*)(three ? p.gvec : nullptr), S, p.sig, stress_out);
     hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
-                       (const float*)F, F_ref, N, ca.S_tot, ca.N_tot, cfg.w_E, cfg.w_F, loss_part, p.lam, p.phi);
+                       (const float*)F, F_ref, N, ca.S_tot, ca.N_tot, cfg.w_E, cfg.w_F, (const float*)p.sig, S_ref,
+                       cfg.w_S, cell, loss_part, p.lam, p.phi, p.Psi);
     if (Ne > 0)
       hipLaunchKernelGGL(rtilde_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, ei, ej, (const float4*)p.geo,
-                         (const float*)p.phi, Ne, p.rt);
+                         (const float*)p.phi, (const int*)p.sid, (const float*)(S_ref ? p.Psi : nullptr), Ne, p.rt,
+                         three ? p.gtan : (float4*)nullptr);
     if (three && Nt > 0) {
       hipLaunchKernelGGL(tri_ctilde_kernel, dim3(cdiv(Nt, 256)), b256, 0, st, (const int*)p.te, (const int*)p.te2,
-                         (const float*)p.tc, (const float4*)p.geo, ei, ej, (const float*)p.phi, (const float*)p.rt,
-                         Nt, p.tct);
+                         (const float*)p.tc, (const float4*)p.geo, (const float4*)p.gtan, (const float*)p.rt, Nt,
+                         p.tct);
       // ct-weighted feature derivatives of every triplet, for dW_a of the double backward
       hipLaunchKernelGGL(tri_features_kernel, dim3(cdiv(Nt * (nf / 4), 256)), b256, 0, st,
                          LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, p.tct, nb}, Nt, nf, p.G3t);
@@ -933,9 +940,21 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
                           const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
                           const float* W, const float* E_ref, const float* F_ref, float* loss, float* E, float* F,
                           float* dLdW, const janus_debug* dbg, void* stream) {
+  return janus_step_stress(ctx, pos, cell, species, offsets, n_atoms, n_struct, nl, W, E_ref, F_ref, nullptr, loss,
+                           E, F, nullptr, dLdW, dbg, stream);
+}
+
+extern "C" int janus_step_stress(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
+                                 const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
+                                 const float* W, const float* E_ref, const float* F_ref, const float* S_ref,
+                                 float* loss, float* E, float* F, float* stress, float* dLdW, const janus_debug* dbg,
+                                 void* stream) {
   if (!ctx || !pos || !cell || !species || !offsets || !nl || !W || !E_ref || !F_ref || !loss || !E || !F ||
       !dLdW || n_atoms < 1 || n_struct < 1 || n_struct > n_atoms)
     return JANUS_EINVAL;
+  // the stress term of the loss needs its reference; without the term no reference is read
+  if (ctx->cfg.w_S != 0.f && !S_ref) return JANUS_EINVAL;
+  if (ctx->cfg.w_S == 0.f) S_ref = nullptr;
   if (nl->n_edges < 0 || nl->n_edges > INT32_MAX / 4 || !nl->rowptr) return JANUS_EINVAL;
   if (nl->n_edges > 0 && (!nl->ei || !nl->ej || !nl->shift || !nl->rev)) return JANUS_EINVAL;
   const janus_config& cfg = ctx->cfg;
@@ -1074,8 +1093,8 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
   for (const ChunkArgs& ca : chunks) {
     Plan p;
     plan_layout(p, ctx->ws.ptr, cfg, ca.N, ca.S, ca.Ne, ca.Nt);
-    rc = run_chunk(ctx, st, p, L, ca, pos, cell, species, offsets, nl, W, E_ref, F_ref, loss_part + ca.index, E, F,
-                   dLdW, dbg);
+    rc = run_chunk(ctx, st, p, L, ca, pos, cell, species, offsets, nl, W, E_ref, F_ref, S_ref, loss_part + ca.index,
+                   E, F, stress, dLdW, dbg);
     if (rc) return rc;
   }
   hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1), 0, st, (const double*)loss_part, (int)chunks.size(), loss);

@@ -114,30 +114,90 @@ __global__ void force_kernel(const int* __restrict__ rowptr, const int* __restri
   F[3 * a + 2] = (float)fz;
 }
 
+// |det| of the lattice rows of one structure (its volume).
+__device__ __forceinline__ double cell_volume(const float* __restrict__ c) {
+  const double a0 = c[0], a1 = c[1], a2 = c[2], b0 = c[3], b1 = c[4], b2 = c[5], c0 = c[6], c1 = c[7], c2 = c[8];
+  return fabs(a0 * (b1 * c2 - b2 * c1) - a1 * (b0 * c2 - b2 * c0) + a2 * (b0 * c1 - b1 * c0));
+}
+
+// Stress of every structure (one wave each), from G_e = dE/dd_e:
+//   sigma_s[a][b] = (1/V_s) sum over the structure's edges of G_e,a d_e,b
+// (a strain (I + eps) maps d_e to (I + eps) d_e).  The edges of a structure are
+// contiguous: [rowptr[offsets[s]], rowptr[offsets[s+1]]).  fp64 accumulation in
+// a fixed lane order.
+__global__ void stress_kernel(const int* __restrict__ rowptr, const int* __restrict__ offsets,
+                              const float* __restrict__ cell, const float* __restrict__ rbar,
+                              const float4* __restrict__ geo, const float4* __restrict__ gvec, int S,
+                              float* __restrict__ sig, float* __restrict__ out) {
+  JANUS_WAVE_LOOP(s, S) {
+    double w[9];
+#pragma unroll
+    for (int q = 0; q < 9; ++q) w[q] = 0.0;
+    const int e1 = rowptr[offsets[s + 1]];
+    for (int e = rowptr[offsets[s]] + l; e < e1; e += 64) {
+      const float4 u = geo[e];
+      double g[3] = {(double)rbar[e] * u.x, (double)rbar[e] * u.y, (double)rbar[e] * u.z};
+      if (gvec) {
+        const float4 v = gvec[e];
+        g[0] += v.x;
+        g[1] += v.y;
+        g[2] += v.z;
+      }
+      const double dv[3] = {(double)u.x * u.w, (double)u.y * u.w, (double)u.z * u.w};
+#pragma unroll
+      for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 3; ++b) w[3 * a + b] += g[a] * dv[b];
+    }
+    const double iv = 1.0 / cell_volume(cell + 9 * s);
+#pragma unroll
+    for (int q = 0; q < 9; ++q) w[q] = wave_sum_d(w[q]);
+    if (l < 9) {
+      double v = 0.0;
+#pragma unroll
+      for (int q = 0; q < 9; ++q) v = q == l ? w[q] : v;
+      sig[9 * s + l] = (float)(v * iv);
+      if (out) out[9 * s + l] = (float)(v * iv);
+    }
+  }
+}
+
 // Loss and adjoint seeds (one workgroup of 1024, fixed reduction order):
 //   loss = w_E/S sum_s (E_s/n_s - Eref_s)^2 + w_F/(3N) sum_a |F_a - Fref_a|^2
-//   lam_s = dloss/dE_s,  phi_a = dloss/dF_a.
+//          [+ w_S/(9S) sum_s |sigma_s - Sref_s|^2]
+//   lam_s = dloss/dE_s,  phi_a = dloss/dF_a,  Psi_s = (dloss/dsigma_s) / V_s.
 // S, N: structures and atoms of this chunk; S_tot, N_tot: of the whole batch
 // (the normalisation).  Writes this chunk's share of the loss to *loss_part.
+// The stress term is skipped when Sref is null.
 __global__ void loss_kernel(const double* __restrict__ Ed, const float* __restrict__ Eref,
                             const int* __restrict__ offsets, int S, const float* __restrict__ F,
                             const float* __restrict__ Fref, int N, int S_tot, int N_tot, float wE, float wF,
-                            double* __restrict__ loss_part, float* __restrict__ lam, float* __restrict__ phi) {
+                            const float* __restrict__ sig, const float* __restrict__ Sref, float wS,
+                            const float* __restrict__ cell, double* __restrict__ loss_part,
+                            float* __restrict__ lam, float* __restrict__ phi, float* __restrict__ Psi) {
   __shared__ double red[1024];
   const int t = threadIdx.x;
-  double se = 0.0, sf = 0.0;
+  double se = 0.0, sf = 0.0, ss = 0.0;
   for (int s = t; s < S; s += 1024) {
     const double n = (double)(offsets[s + 1] - offsets[s]);
     const double de = Ed[s] / n - (double)Eref[s];
     se += de * de;
     lam[s] = (float)(2.0 * wE * de / ((double)S_tot * n));
+    if (Sref) {
+      const double iv = 1.0 / cell_volume(cell + 9 * s);
+      for (int q = 0; q < 9; ++q) {
+        const double ds = (double)sig[9 * s + q] - (double)Sref[9 * s + q];
+        ss += ds * ds;
+        Psi[9 * s + q] = (float)(2.0 * wS * ds / (9.0 * S_tot) * iv);
+      }
+    }
   }
   for (int q = t; q < 3 * N; q += 1024) {
     const double df = (double)F[q] - (double)Fref[q];
     sf += df * df;
     phi[q] = (float)(2.0 * wF * df / (3.0 * N_tot));
   }
-  red[t] = wE * se / S_tot + wF * sf / (3.0 * N_tot);
+  red[t] = wE * se / S_tot + wF * sf / (3.0 * N_tot) + wS * ss / (9.0 * S_tot);
   __syncthreads();
   for (int o = 512; o > 0; o >>= 1) {
     if (t < o) red[t] += red[t + o];
@@ -183,14 +243,28 @@ __global__ void struct_edges_kernel(const int* __restrict__ offsets, const int* 
 }
 
 // rt_e = (phi_i - phi_j) . u_e: the loss adjoint of rbar_e.
+// Displacement tangent of the second-order sweep, per edge:
+//   gt_e = phi_i - phi_j + Psi_s d_e   (Psi null: no stress term)
+//   rt_e = gt_e . u_e
+// gt (float4, may be null) is kept for the bond-angle term.
 __global__ void rtilde_kernel(const int* __restrict__ ei, const int* __restrict__ ej, const float4* __restrict__ geo,
-                              const float* __restrict__ phi, long long Ne, float* __restrict__ rt) {
+                              const float* __restrict__ phi, const int* __restrict__ sid,
+                              const float* __restrict__ Psi, long long Ne, float* __restrict__ rt,
+                              float4* __restrict__ gt) {
   const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= Ne) return;
   const int i = ei[e], j = ej[e];
   const float4 u = geo[e];
-  rt[e] = (phi[3 * i] - phi[3 * j]) * u.x + (phi[3 * i + 1] - phi[3 * j + 1]) * u.y +
-          (phi[3 * i + 2] - phi[3 * j + 2]) * u.z;
+  float gx = phi[3 * i] - phi[3 * j], gy = phi[3 * i + 1] - phi[3 * j + 1], gz = phi[3 * i + 2] - phi[3 * j + 2];
+  if (Psi) {
+    const float* P = Psi + 9 * sid[i];
+    const float dx = u.x * u.w, dy = u.y * u.w, dz = u.z * u.w;
+    gx += P[0] * dx + P[1] * dy + P[2] * dz;
+    gy += P[3] * dx + P[4] * dy + P[5] * dz;
+    gz += P[6] * dx + P[7] * dy + P[8] * dz;
+  }
+  rt[e] = gx * u.x + gy * u.y + gz * u.z;
+  if (gt) gt[e] = make_float4(gx, gy, gz, 0.f);
 }
 
 // Readout of the double + final backward, per atom and column:
@@ -458,6 +532,7 @@ int check_config(const janus_config* c) {
     if (c->d_hidden3 % 64 || c->n_legendre > 8 || (size_t)c->n_legendre * c->n_rbf * c->d * 4 > 65536)
       return JANUS_EUNSUPPORTED;
   }
+  if (!(c->w_S >= 0.f)) return JANUS_EINVAL;
   if (c->atom_moe) {
     if (c->n_experts_f < 1 || c->n_experts_f > 64 || c->top_k_f < 1 || c->top_k_f > 4 ||
         c->top_k_f > c->n_experts_f || c->d_hidden_f < 64)
@@ -476,7 +551,8 @@ struct Plan {
   float4* geo;
   float *B, *dB, *rt, *rbar;
   int *sp_cnt, *sp_off, *sp_atoms;
-  float *z, *eps, *lam, *phi, *vt, *Zr, *Tr, *colpart;
+  float *z, *eps, *lam, *phi, *vt, *Zr, *Tr, *colpart, *sig, *Psi;
+  float4* gtan;
   double* Ed;
   float *h, *hh, *hht, *h3;   // [(T+1) or T][N, d]; the final-backward adjoint reuses hh
   // routing, per block
@@ -579,6 +655,9 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.eps = cv.take<float>(N);
   p.lam = cv.take<float>(S);
   p.phi = cv.take<float>(3LL * N);
+  p.sig = cv.take<float>(9LL * S);
+  p.Psi = cv.take<float>(9LL * S);
+  p.gtan = cv.take<float4>(Ne + 1);
   p.vt = cv.take<float>(Nd);
   p.Zr = cv.take<float>(Nd);
   p.Tr = cv.take<float>(Nd);

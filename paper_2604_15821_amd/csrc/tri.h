@@ -536,23 +536,21 @@ __global__ void tri_edge_vec_kernel(const int* __restrict__ trowptr, const int* 
 // ---------------------------------------------------------------- phase 3
 
 // Per triplet, once per step: the loss adjoints of the feature-geometry
-// adjoints, ct = (ac~, a1~, a2~), from Gt_e = phi_i(e) - phi_j(e):
+// adjoints, ct = (ac~, a1~, a2~), from the displacement tangents Gt_e
+// (phi_i(e) - phi_j(e), plus the strain term of the stress seeds):
 //   ac~ = Gt_e . (u2 - c u1) / r1 + Gt_e2 . (u1 - c u2) / r2,  a1~ = rt_e,  a2~ = rt_e2.
 __global__ void tri_ctilde_kernel(const int* __restrict__ te, const int* __restrict__ te2,
                                   const float* __restrict__ tc, const float4* __restrict__ geo,
-                                  const int* __restrict__ ei, const int* __restrict__ ej,
-                                  const float* __restrict__ phi, const float* __restrict__ rt, long long Nt,
+                                  const float4* __restrict__ gt, const float* __restrict__ rt, long long Nt,
                                   float4* __restrict__ ct) {
   const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= Nt) return;
   const int e = te[t], e2 = te2[t];
   const float4 u1 = geo[e], u2 = geo[e2];
   const float c = tc[t];
-  const int i = ei[e], j1 = ej[e], j2 = ej[e2];
-  const float g1x = phi[3 * i] - phi[3 * j1], g1y = phi[3 * i + 1] - phi[3 * j1 + 1],
-              g1z = phi[3 * i + 2] - phi[3 * j1 + 2];
-  const float g2x = phi[3 * i] - phi[3 * j2], g2y = phi[3 * i + 1] - phi[3 * j2 + 1],
-              g2z = phi[3 * i + 2] - phi[3 * j2 + 2];
+  const float4 G1 = gt[e], G2 = gt[e2];
+  const float g1x = G1.x, g1y = G1.y, g1z = G1.z;
+  const float g2x = G2.x, g2y = G2.y, g2z = G2.z;
   const float acx = (g1x * (u2.x - c * u1.x) + g1y * (u2.y - c * u1.y) + g1z * (u2.z - c * u1.z)) / u1.w +
                     (g2x * (u1.x - c * u2.x) + g2y * (u1.y - c * u2.y) + g2z * (u1.z - c * u2.z)) / u2.w;
   ct[t] = make_float4(acx, rt[e], rt[e2], 0.f);

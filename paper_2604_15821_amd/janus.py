@@ -32,7 +32,7 @@ class Config(C.Structure):
         ("r_cut", C.c_float), ("three_body", C.c_int32), ("r_cut3", C.c_float), ("n_experts3", C.c_int32),
         ("top_k3", C.c_int32), ("d_hidden3", C.c_int32), ("n_legendre", C.c_int32), ("w_E", C.c_float),
         ("w_F", C.c_float), ("atom_moe", C.c_int32), ("n_experts_f", C.c_int32), ("top_k_f", C.c_int32),
-        ("d_hidden_f", C.c_int32),
+        ("d_hidden_f", C.c_int32), ("w_S", C.c_float),
     ]
 
 
@@ -77,6 +77,8 @@ def _lib():
         lib.janus_build_edges.argtypes = [vp, vp, vp, vp, i32, i32, i64, vp, vp, vp, vp, vp, C.POINTER(i64), vp]
         lib.janus_step.argtypes = [vp, vp, vp, vp, vp, i32, i32, C.POINTER(Edges), vp, vp, vp, vp, vp, vp, vp,
                                    C.POINTER(Debug), vp]
+        lib.janus_step_stress.argtypes = [vp, vp, vp, vp, vp, i32, i32, C.POINTER(Edges), vp, vp, vp, vp, vp, vp,
+                                          vp, vp, vp, C.POINTER(Debug), vp]
         lib.janus_grouped_gemm.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
         lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
         lib.janus_set_workspace_limit.argtypes = [vp, i64]
@@ -93,6 +95,7 @@ def exported_symbols():
     """Names the library exports (checked against include/janus.h by the CPU tests)."""
     lib = _lib()
     names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
+             "janus_step_stress",
              "janus_grouped_gemm", "janus_grouped_wgrad", "janus_profile_enable", "janus_profile_read",
              "janus_set_workspace_limit", "janus_last_chunks", "janus_last_triplets", "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
@@ -230,8 +233,12 @@ class Context:
         return int(ne.value)
 
     # ----------------------------------------------------------------- step
-    def step(self, pos, cell, species, offsets, nl: NeighborList, W, E_ref, F_ref, out=None, debug=None):
-        """One training step; returns (loss [1], E [S], F [N,3], dLdW [like W]) device tensors."""
+    def step(self, pos, cell, species, offsets, nl: NeighborList, W, E_ref, F_ref, out=None, debug=None,
+             S_ref=None, stress=None):
+        """One training step; returns (loss [1], E [S], F [N,3], dLdW [like W]) device tensors.
+
+        With S_ref [S,3,3] (needed when the model's w_S > 0) or a stress output
+        tensor [S,3,3], runs janus_step_stress and writes the stress into `stress`."""
         import torch
         dev = pos.device
         N = pos.shape[0]
@@ -244,9 +251,15 @@ class Context:
         dbg = None
         if debug is not None:
             dbg = Debug(*[_ptr(debug.get(k)).value for k in Debug.KEYS])
-        rc = _lib().janus_step(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S, C.byref(edges),
-                               _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(loss), _ptr(E), _ptr(F), _ptr(dW),
-                               C.byref(dbg) if dbg is not None else None, _stream())
+        dbgp = C.byref(dbg) if dbg is not None else None
+        if S_ref is None and stress is None:
+            rc = _lib().janus_step(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S, C.byref(edges),
+                                   _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(loss), _ptr(E), _ptr(F), _ptr(dW), dbgp,
+                                   _stream())
+        else:
+            rc = _lib().janus_step_stress(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S,
+                                          C.byref(edges), _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(S_ref), _ptr(loss),
+                                          _ptr(E), _ptr(F), _ptr(stress), _ptr(dW), dbgp, _stream())
         if rc:
             raise JanusError(rc, "janus_step")
         return loss, E, F, dW
@@ -321,5 +334,6 @@ def upload(batch, device="cuda:0"):
         "offsets": t(batch.offsets, torch.int32),
         "E_ref": t(batch.E_ref, torch.float32),
         "F_ref": t(batch.F_ref, torch.float32),
+        "S_ref": None if batch.S_ref is None else t(batch.S_ref, torch.float32),
         "W": t(pack_weights(batch.weights, batch.model), torch.float32),
     }

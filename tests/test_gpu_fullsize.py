@@ -20,7 +20,7 @@ from helpers import TOL_E, TOL_F, TOL_W, banner, energy_error, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["small", "threebody", "atom_moe", "shard", "irregular"]
+FULL = ["small", "threebody", "atom_moe", "stress", "shard", "irregular"]
 
 
 def _gpu_step(b, model=None):
@@ -30,12 +30,14 @@ def _gpu_step(b, model=None):
     d = janus.upload(b)
     ctx = janus.Context(m)
     nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
-    loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"])
+    st = torch.empty(b.n_struct, 3, 3, device="cuda:0")
+    loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"],
+                              S_ref=d["S_ref"], stress=st)
     torch.cuda.synchronize()
     out = {"loss": float(loss.cpu()[0]), "E": E.cpu().numpy(), "F": F.cpu().numpy(), "dW": dW.cpu().numpy(),
-           "chunks": ctx.last_chunks(), "edges": nl.n_edges}
+           "stress": st.cpu().numpy(), "chunks": ctx.last_chunks(), "edges": nl.n_edges}
     ctx.close()
-    del d, nl, loss, E, F, dW
+    del d, nl, loss, E, F, dW, st
     torch.cuda.empty_cache()
     return out
 
@@ -45,7 +47,7 @@ def _scaled_part(b, structs):
     from paper_2604_15821_amd.synth import subset
     sb = subset(b, structs)
     m = dataclasses.replace(b.model, w_E=b.model.w_E * sb.n_struct / b.n_struct,
-                            w_F=b.model.w_F * sb.n_atoms / b.n_atoms)
+                            w_F=b.model.w_F * sb.n_atoms / b.n_atoms, w_S=b.model.w_S * sb.n_struct / b.n_struct)
     return dataclasses.replace(sb, model=m)
 
 
@@ -77,11 +79,15 @@ def test_loss_matches_returned_energies_and_forces(full):
     de = out["E"].astype(np.float64) / n - b.E_ref.astype(np.float64)
     dF = out["F"].astype(np.float64) - b.F_ref.astype(np.float64)
     loss = m.w_E * (de * de).sum() / b.n_struct + m.w_F * (dF * dF).sum() / (3.0 * b.n_atoms)
+    if m.w_S:
+        dS = out["stress"].astype(np.float64) - b.S_ref.astype(np.float64)
+        loss += m.w_S * (dS * dS).sum() / (9.0 * b.n_struct)
     assert abs(out["loss"] - loss) <= 1e-5 * abs(loss)
 
 
 def test_sampled_structures_energy_and_forces(full):
-    from oracle.model import Params, build_graph_for, forces, forward_energy, route_all
+    from oracle.model import (Params, build_graph_for, energy_displacement_gradient, forces, forward_energy,
+                              route_all, stress)
     from paper_2604_15821_amd.synth import subset
     name, b, out = full
     sizes = np.diff(b.offsets)
@@ -96,8 +102,11 @@ def test_sampled_structures_energy_and_forces(full):
         g = build_graph_for(sb)
         rt = route_all(sb.species, g, P)
         E, cache = forward_energy(sb.species, g, P, rt)
+        G = energy_displacement_gradient(sb.species, g, P, rt, cache)
         F = forces(sb.species, g, P, rt, cache)
         a0, a1 = b.offsets[s], b.offsets[s + 1]
+        serr = rel_l2(out["stress"][s], stress(g, G, sb.cell)[0])
+        assert serr <= 1e-3, serr
         err = energy_error(out["E"][s:s + 1], E, cache["eps"], np.array([0, a1 - a0]))
         ferr = rel_l2(out["F"][a0:a1], F)
         print(f"  structure {s}: energy error {err:.2e}, force rel L2 {ferr:.2e}", flush=True)
