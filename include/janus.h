@@ -82,6 +82,9 @@ enum {
  *              (d_hidden_f a multiple of 64)
  *   w_S        loss weight of the stress term (>= 0; 0 leaves it out; used by
  *              janus_step_stress, stresses in energy / length^3)
+ *   n_heads    0, or the number of heads of the self-attention over every
+ *              atom's edge messages (paper Sec. "Multi-head self-attention");
+ *              must divide d
  */
 typedef struct janus_config {
   int32_t n_species;
@@ -106,6 +109,7 @@ typedef struct janus_config {
   int32_t top_k_f;
   int32_t d_hidden_f;
   float w_S;
+  int32_t n_heads;
 } janus_config;
 
 typedef struct janus_ctx janus_ctx;
@@ -187,7 +191,8 @@ void janus_destroy(janus_ctx* ctx);
  * three-body term W_a [n_legendre*n_rbf, d], P3a, P3b, P3c [n_species, E3],
  * beta3 [E3], W1a [E3, d, d_hidden3], W2a [E3, d_hidden3, d], and with
  * the feature-update MoE Pf [n_species, Ef], betaf [Ef], W1f [Ef, d,
- * d_hidden_f], W2f [Ef, d_hidden_f, d]; then W_o1 [d, d], w_o2 [d].  If `out` is NULL only the counts are written.  *n_tensors (in:
+ * d_hidden_f], W2f [Ef, d_hidden_f, d], and with attention Wqkv [d, 3d]
+ * (query | key | value columns), Wo [d, d]; then W_o1 [d, d], w_o2 [d].  If `out` is NULL only the counts are written.  *n_tensors (in:
  * capacity of out, out: number of tensors) and *n_floats (total blob size)
  * are host pointers.  Errors: JANUS_EINVAL (capacity too small). */
 int janus_weight_layout(const janus_config* cfg, janus_tensor_desc* out, int32_t* n_tensors,

@@ -37,6 +37,15 @@ update becomes
     h^{t+1}_i = u_i + sum_c gf_ic W2f_x^T SiLU(W1f_x^T u_i),  x = Kf_i[c]
 with the same gating rule as the edge MoE; betaf is fixed like beta.
 
+With multi-head self-attention (paper Sec. "Multi-head self-attention",
+``attention.py``) the messages of the edges of atom i attend to each other
+before they reach the atom:
+    u_i = h^t_i + (sum_{e : i(e) = i} u(r_e/r_c) o_e) Wo,
+    o = attention over N(i) of m,
+with queries, keys and values m [Wq | Wk | Wv] = m Wqkv; the edge envelope
+u weighs every edge both as a key (inside the softmax) and as a query (in
+the sum), so an edge entering the cutoff changes E smoothly.
+
 Second order (paper Sec. "Runtime for multi-phase double-backward
 execution": the force loss needs derivatives of F with respect to the
 weights).  With lam_s = dL/dE_s and phi_a = dL/dF_a held fixed,
@@ -57,8 +66,9 @@ from dataclasses import dataclass
 import numpy as np
 import scipy.sparse as sp
 
+from . import attention as attn
 from . import threebody as tb
-from .basis import bessel_basis, silu, silu_d1, silu_d2, silu_family
+from .basis import bessel_basis, envelope, silu, silu_d1, silu_d2, silu_family
 from .neighbors import neighbor_list, reverse_map, triplet_list
 
 
@@ -85,13 +95,15 @@ class Params:
     atom: bool = False
     kf: int = 0
     Ef: int = 0
+    heads: int = 0
+    r_cut: float = 0.0
 
     @classmethod
     def from_weights(cls, weights, model):
         w = {n: np.asarray(v, np.float64) for n, v in weights.items()}
         return cls(w=w, T=model.n_blocks, k=model.top_k, E=model.n_experts, three=bool(model.three_body),
                    k3=model.top_k3, E3=model.n_experts3, atom=bool(model.atom_moe),
-                   kf=model.top_k_f, Ef=model.n_experts_f)
+                   kf=model.top_k_f, Ef=model.n_experts_f, heads=model.n_heads, r_cut=model.r_cut)
 
     def blk(self, t, name):
         return self.w[f"blocks.{t}.{name}"]
@@ -271,6 +283,114 @@ def _tri_tokens(g, P, t, h):
     return Zpre, hj2, Zpre * hj2
 
 
+# --------------------------------------------------------------------------- attention
+
+def _attn_env(g, P):
+    """log u(r_e/r_c) of every edge and its derivative in r_e (attention key weights)."""
+    u, du, _ = envelope(g.r / P.r_cut)
+    return np.log(u), du / (u * P.r_cut)
+
+
+def _attn_heads(g, P, fn, N, *per_edge):
+    """Call fn(i, a, b, cols, slices...) for every (atom, head) neighbourhood; per_edge
+    arrays are [Ne, w] with w a multiple of d (column blocks q|k|v, sliced to the head's
+    columns) or [Ne] (per-key scalars)."""
+    d = P.w["A"].shape[1]
+    dh = d // P.heads
+    for i in range(N):
+        a, b = int(g.rowptr[i]), int(g.rowptr[i + 1])
+        if a == b:
+            continue
+        for hd in range(P.heads):
+            cols = np.arange(hd * dh, (hd + 1) * dh)
+            args = []
+            for x in per_edge:
+                if x.ndim == 1:
+                    args.append(x[a:b])
+                else:
+                    args += [x[a:b, j * d + cols] for j in range(x.shape[1] // d)]
+            fn(i, a, b, cols, *args)
+
+
+def _attn_forward(g, P, t, m, lu, N):
+    """osum [N, d]: per atom, sum over its edges e of u_e o_e (query weight u_e)."""
+    d = m.shape[1]
+    QKV = m @ P.blk(t, "Wqkv")
+    osum = np.zeros((N, d))
+
+    def fn(i, a, b, cols, q, k, v, l):
+        osum[i, cols] = (np.exp(l)[:, None] * attn.forward(q, k, v, l)[0]).sum(0)
+    _attn_heads(g, P, fn, N, QKV, lu)
+    return osum
+
+
+def _attn_backward(g, P, t, m, lu, ubar, N):
+    """Adjoints of the messages and of log u for the adjoint ubar of u = h + osum Wo."""
+    d = m.shape[1]
+    QKV = m @ P.blk(t, "Wqkv")
+    ob = ubar @ P.blk(t, "Wo").T
+    QKVb = np.zeros_like(QKV)
+    lub = np.zeros(m.shape[0])
+
+    def fn(i, a, b, cols, q, k, v, l):
+        uq = np.exp(l)[:, None]
+        o = attn.forward(q, k, v, l)[0]
+        qb, kb, vb, lb = attn.backward(q, k, v, l, uq * ob[i, cols][None, :])
+        QKVb[a:b, cols], QKVb[a:b, d + cols], QKVb[a:b, 2 * d + cols] = qb, kb, vb
+        # log u of an edge enters as key (lb) and through the query weight
+        lub[a:b] += lb + uq[:, 0] * (o @ ob[i, cols])
+    _attn_heads(g, P, fn, N, QKV, lu)
+    return QKVb @ P.blk(t, "Wqkv").T, lub
+
+
+def _attn_tangent(g, P, t, m, md, lu, rho, N):
+    """(osum, osum-dot) for message tangents md and key-weight tangents rho."""
+    d = m.shape[1]
+    Wqkv = P.blk(t, "Wqkv")
+    QKV, QKVd = m @ Wqkv, md @ Wqkv
+    osum, osumd = np.zeros((N, d)), np.zeros((N, d))
+
+    def fn(i, a, b, cols, q, k, v, qd, kd, vd, l, r):
+        uq = np.exp(l)[:, None]
+        o, od = attn.tangent(q, k, v, l, qd, kd, vd, r)
+        osum[i, cols] = (uq * o).sum(0)
+        osumd[i, cols] = (uq * od + uq * r[:, None] * o).sum(0)
+    _attn_heads(g, P, fn, N, QKV, QKVd, lu, rho)
+    return osum, osumd
+
+
+def _attn_reverse(g, P, t, m, md, lu, rho, Pu, Tu, N):
+    """Reverse sweep of u = h + osum Wo, ud = hd + osumd Wo through the attention:
+    returns the adjoints of the messages and of their tangents, dWqkv and dWo."""
+    d = m.shape[1]
+    Wqkv, Wo = P.blk(t, "Wqkv"), P.blk(t, "Wo")
+    QKV, QKVd = m @ Wqkv, md @ Wqkv
+    osum, osumd = _attn_tangent(g, P, t, m, md, lu, rho, N)
+    dWo = osum.T @ Pu + osumd.T @ Tu
+    Po, To = Pu @ Wo.T, Tu @ Wo.T
+    PQ, TQ = np.zeros_like(QKV), np.zeros_like(QKV)
+
+    def fn(i, a, b, cols, q, k, v, qd, kd, vd, l, r):
+        # osum = sum u o, osumd = sum u od + u rho o: adjoints of o and od per query
+        uq = np.exp(l)[:, None]
+        A, B = Po[i, cols][None, :], To[i, cols][None, :]
+        (qb, kb, vb), (qdb, kdb, vdb) = attn.dual_reverse(q, k, v, l, qd, kd, vd, r,
+                                                          uq * (A + r[:, None] * B), uq * B)
+        PQ[a:b, cols], PQ[a:b, d + cols], PQ[a:b, 2 * d + cols] = qb, kb, vb
+        TQ[a:b, cols], TQ[a:b, d + cols], TQ[a:b, 2 * d + cols] = qdb, kdb, vdb
+    _attn_heads(g, P, fn, N, QKV, QKVd, lu, rho)
+    dWqkv = m.T @ PQ + md.T @ TQ
+    return PQ @ Wqkv.T, TQ @ Wqkv.T, dWqkv, dWo
+
+
+def _aggregate(g, P, t, m, N):
+    """Message update of the atoms: sum of the messages, or the attention output."""
+    if not P.heads:
+        return _seg(g.ei, N, m)
+    lu, _ = _attn_env(g, P)
+    return _attn_forward(g, P, t, m, lu, N) @ P.blk(t, "Wo")
+
+
 def _atom_moe(P, t, routing, u):
     """Feature-update MoE output for the atom features u (zero without it)."""
     if not P.atom:
@@ -293,7 +413,7 @@ def forward_energy(species, g: Graph, P: Params, routing):
             y = _moe(routing[t].tri, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z)
             X = X + _seg(g.tri.te, Ne, y)
         m = _moe(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X)
-        u = h + _seg(g.ei, N, m)
+        u = h + _aggregate(g, P, t, m, N)
         h = u + _atom_moe(P, t, routing, u)
         us.append(u)
         hs.append(h)
@@ -347,7 +467,15 @@ def energy_displacement_gradient(species, g: Graph, P: Params, routing, cache):
         if P.atom:                                                    # h^{t+1} = u + MoE_f(u)
             hbar = hbar + _moe_backward(routing[t].atom, P.Ef, P.blk(t, "W1f"), P.blk(t, "W2f"), us[t], hbar)
         F, X = _block_tokens(g, P, t, h, routing)
-        Xbar = _moe_backward(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, hbar[g.ei])
+        if P.heads:
+            # u = h + attention(m): adjoint of the messages; log u(r) feeds dE/dr
+            m = _moe(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X)
+            lu, dlu = _attn_env(g, P)
+            mbar, lub = _attn_backward(g, P, t, m, lu, hbar, N)
+            rbar += lub * dlu
+        else:
+            mbar = hbar[g.ei]
+        Xbar = _moe_backward(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, mbar)
         hbar_next = hbar + _seg(g.ej, N, Xbar * F)
         if g.tri is not None:
             Zpre, hj2, Z = _tri_tokens(g, P, t, h)
@@ -454,8 +582,14 @@ def energy_tangent(species, g: Graph, P: Params, routing, phi, Psi=None):
     for t in range(P.T):
         F, Fd, X, Xd = _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing)
         m, md = _moe_tangent(routing[t], P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd)
-        u = h + _seg(g.ei, N, m)
-        ud = hd + _seg(g.ei, N, md)
+        if P.heads:
+            lu, dlu = _attn_env(g, P)
+            osum, osumd = _attn_tangent(g, P, t, m, md, lu, dlu * rdot, N)
+            u = h + osum @ P.blk(t, "Wo")
+            ud = hd + osumd @ P.blk(t, "Wo")
+        else:
+            u = h + _seg(g.ei, N, m)
+            ud = hd + _seg(g.ei, N, md)
         h, hd = u, ud
         if P.atom:
             f, fd = _moe_tangent(routing[t].atom, P.Ef, P.blk(t, "W1f"), P.blk(t, "W2f"), u, ud)
@@ -539,7 +673,15 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
             grad[f"blocks.{t}.Pf"] = _seg(species, S_, _logit_adjoint(rt.atom, Pgf))
             Ph, Th = Ph + PU, Th + TU
         F, Fd, X, Xd = _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing)
-        PX, TX, dW1, dW2, Pg = _moe_reverse(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd, Ph[g.ei], Th[g.ei])
+        if P.heads:
+            m, md = _moe_tangent(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd)
+            lu, dlu = _attn_env(g, P)
+            Pm, Tm, dWqkv, dWo = _attn_reverse(g, P, t, m, md, lu, dlu * tc["rdot"], Ph, Th, N)
+            grad[f"blocks.{t}.Wqkv"] = dWqkv
+            grad[f"blocks.{t}.Wo"] = dWo
+        else:
+            Pm, Tm = Ph[g.ei], Th[g.ei]
+        PX, TX, dW1, dW2, Pg = _moe_reverse(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd, Pm, Tm)
         grad[f"blocks.{t}.W1"] = dW1
         grad[f"blocks.{t}.W2"] = dW2
         # X = F * h_j (+ q) ;  Xd = Fd * h_j + F * hd_j (+ qd)

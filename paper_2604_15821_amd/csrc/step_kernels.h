@@ -509,6 +509,10 @@ Layout make_layout(const janus_config& c) {
       L.add(p + "W1f", {Ef, d, hf});
       L.add(p + "W2f", {Ef, hf, d});
     }
+    if (c.n_heads) {
+      L.add(p + "Wqkv", {d, 3 * d});
+      L.add(p + "Wo", {d, d});
+    }
   }
   L.add("W_o1", {d, d});
   L.add("w_o2", {d});
@@ -533,6 +537,9 @@ int check_config(const janus_config* c) {
       return JANUS_EUNSUPPORTED;
   }
   if (!(c->w_S >= 0.f)) return JANUS_EINVAL;
+  if (c->n_heads < 0 || (c->n_heads && c->d % c->n_heads)) return JANUS_EINVAL;
+  // the step does not run neighbourhood attention yet
+  if (c->n_heads) return JANUS_EUNSUPPORTED;
   if (c->atom_moe) {
     if (c->n_experts_f < 1 || c->n_experts_f > 64 || c->top_k_f < 1 || c->top_k_f > 4 ||
         c->top_k_f > c->n_experts_f || c->d_hidden_f < 64)

@@ -37,7 +37,8 @@ class ModelConfig:
     atom_moe fields describe the optional feature-update MoE of every block
     (atom tokens routed by element type; each expert d -> d_hidden_f -> d).
     w_E, w_F, w_S weigh the energy, force and stress terms of the loss (stress
-    in eV/A^3; w_S = 0 leaves it out).
+    in eV/A^3; w_S = 0 leaves it out).  n_heads > 0 adds multi-head
+    self-attention over every atom's edge messages (head width d / n_heads).
     """
 
     d: int
@@ -62,6 +63,7 @@ class ModelConfig:
     top_k_f: int = 0
     d_hidden_f: int = 0
     w_S: float = 0.0
+    n_heads: int = 0
 
     def weight_shapes(self):
         """Named weight tensors in blob order, with the fan-in used at init.
@@ -100,6 +102,11 @@ class ModelConfig:
                     (p + "betaf", (Ef,), "zero"),
                     (p + "W1f", (Ef, d, hf), d),
                     (p + "W2f", (Ef, hf, d), hf),
+                ]
+            if self.n_heads:
+                out += [
+                    (p + "Wqkv", (d, 3 * d), d),
+                    (p + "Wo", (d, d), d),
                 ]
         out += [("W_o1", (d, d), d), ("w_o2", (d,), d)]
         return out
@@ -142,6 +149,7 @@ _M_3B = dataclasses.replace(_M_SMALL, three_body=True, r_cut3=3.5, n_experts3=8,
 _M_ATOM = dataclasses.replace(_M_SMALL, atom_moe=True, n_experts_f=8, top_k_f=2, d_hidden_f=512)
 # stress weight 0.1 on stresses measured in GPa (1 eV/A^3 = 160.2177 GPa)
 _M_STRESS = dataclasses.replace(_M_SMALL, w_S=0.1 * 160.2177 ** 2)
+_M_ATTN = dataclasses.replace(_M_SMALL, n_heads=4)
 _M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
 
 WORKLOADS = {
@@ -150,6 +158,7 @@ WORKLOADS = {
     "threebody": Workload("threebody", "ortho", 64, 64, 0.08, _M_3B),
     "atom_moe": Workload("atom_moe", "ortho", 64, 64, 0.08, _M_ATOM),
     "stress": Workload("stress", "ortho", 64, 64, 0.08, _M_STRESS),
+    "attention": Workload("attention", "ortho", 64, 64, 0.08, _M_ATTN),
     "shard": Workload("shard", "cubic", 256, 128, 0.1, _M_BIG),
     "irregular": Workload("irregular", "mixed", 512, 0, 0.1, _M_BIG, zipf_s=1.2),
 }
