@@ -215,7 +215,8 @@ def main():
                    "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none",
                    **({"atom_moe": {"experts": m.n_experts_f, "top_k": m.top_k_f, "d_hidden": m.d_hidden_f}}
                       if m.atom_moe else {}),
-                   **({"stress_weight": m.w_S} if m.w_S else {})},
+                   **({"stress_weight": m.w_S} if m.w_S else {}),
+                   **({"attention_heads": m.n_heads} if m.n_heads else {})},
         "edges_per_s": Ne / (ms * 1e-3),
         "triplets": Nt,
         "triplets_per_s": Nt / (ms * 1e-3),

@@ -47,6 +47,8 @@ def family(kernel_name: str) -> str:
         return "edge"
     if re.search(r"(combine_fwd|gather_atom|scatter_rev|combine_p3)_kernel", n):
         return "atom"
+    if re.search(r"attn_(fwd|bwd|tan|rev)_kernel", n):
+        return "attention"
     if "elementwise_kernel" in n or "vectorized" in n:
         return "copy"
     return "other"

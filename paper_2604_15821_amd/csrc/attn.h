@@ -1,0 +1,509 @@
+// Multi-head self-attention over every atom's edge messages (paper Sec.
+// "Multi-head self-attention": each edge of a neighbourhood attends to every
+// edge of the same neighbourhood, cost m d sum_i |N(i)|^2).
+//
+// Per atom i with edges e in N(i) (contiguous rows rowptr[i] .. rowptr[i+1])
+// and head a (32 columns of q, k, v = m Wqkv, row layout [q | k | v]):
+//   s_el  = q_e . k_l / sqrt(32)
+//   p_el  = u_l exp(s_el) / sum_j u_j exp(s_ej)        (u = edge envelope)
+//   o_e   = sum_l p_el v_l
+//   osum_i = sum_e u_e o_e                              (then u_i = h_i + osum_i Wo)
+// One wave per atom loops over the heads.  Passes with one lane per query
+// keep the query row in registers and read every key row once per 64
+// queries (all lanes the same row); passes with one lane per key do the
+// transpose.  Per-query softmax statistics (max of s, Z = sum u exp(s - max))
+// are stored by the forward and reused by the three backward phases.  Per-edge
+// scalars shared between the passes of one head live in LDS, so a
+// neighbourhood holds at most kAttnMaxN edges (checked before the step).
+#pragma once
+
+#include "edge.h"
+
+namespace janus {
+
+constexpr int kAttnDh = 32;
+constexpr int kAttnMaxN = 256;
+constexpr int kAttnWaves = 4;   // waves per workgroup (256 threads)
+
+__device__ __forceinline__ void ld32(const float* __restrict__ p, float* x) {
+#pragma unroll
+  for (int c = 0; c < kAttnDh; c += 4) {
+    const float4 v = *reinterpret_cast<const float4*>(p + c);
+    x[c] = v.x;
+    x[c + 1] = v.y;
+    x[c + 2] = v.z;
+    x[c + 3] = v.w;
+  }
+}
+
+__device__ __forceinline__ void st32(float* __restrict__ p, const float* x) {
+#pragma unroll
+  for (int c = 0; c < kAttnDh; c += 4)
+    *reinterpret_cast<float4*>(p + c) = make_float4(x[c], x[c + 1], x[c + 2], x[c + 3]);
+}
+
+__device__ __forceinline__ float dot32(const float* a, const float* b) {
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < kAttnDh; ++c) s += a[c] * b[c];
+  return s;
+}
+
+// Row sums of a per-lane 32-vector over the wave, stored by lanes 0..31.
+__device__ __forceinline__ void wave_store32(float* __restrict__ out, const float* x, int l) {
+  float mine = 0.f;
+#pragma unroll
+  for (int c = 0; c < kAttnDh; ++c) {
+    const float s = wave_sum(x[c]);
+    mine = l == c ? s : mine;
+  }
+  if (l < kAttnDh) out[l] = mine;
+}
+
+constexpr float kAttnScale = 0.17677669529663687f;   // 1 / sqrt(32)
+
+// Envelope of every edge: u(r/r_c) and du/dr.
+__global__ void attn_env_kernel(const float4* __restrict__ geo, long long Ne, float rc, float* __restrict__ uu,
+                                float* __restrict__ ud) {
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  const double x = (double)geo[e].w / rc;
+  const double x2 = x * x, x5 = x2 * x2 * x, x6 = x5 * x;
+  const double u = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
+  const double du = -168.0 * x5 * (1.0 - x) * (1.0 - x);
+  uu[e] = (float)u;
+  ud[e] = (float)(du / rc);
+}
+
+// Phase 1: osum_i (one wave per atom; lanes = queries).  stats[(e*H + a)*2 + {0,1}] = (max s, Z).
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu, int N, int d, int H,
+    float* __restrict__ stats, float* __restrict__ osum) {
+  const long long ld = 3LL * d;
+  JANUS_WAVE_LOOP(i, N) {
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    for (int a = 0; a < H; ++a) {
+      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      float acc[kAttnDh];
+#pragma unroll
+      for (int c = 0; c < kAttnDh; ++c) acc[c] = 0.f;
+      for (int q0 = 0; q0 < n; q0 += 64) {
+        const bool valid = q0 + l < n;
+        const long long e = e0 + (valid ? q0 + l : 0);
+        float q[kAttnDh], o[kAttnDh];
+        ld32(QKV + e * ld + cq, q);
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) o[c] = 0.f;
+        float M = -INFINITY, Z = 0.f;
+        for (int j = 0; j < n; ++j) {
+          const long long key = e0 + j;
+          float k[kAttnDh], v[kAttnDh];
+          ld32(QKV + key * ld + ck, k);
+          ld32(QKV + key * ld + cv, v);
+          const float s = dot32(q, k) * kAttnScale;
+          const float Mn = fmaxf(M, s);
+          const float f = __expf(M - Mn), g = uu[key] * __expf(s - Mn);
+          Z = Z * f + g;
+#pragma unroll
+          for (int c = 0; c < kAttnDh; ++c) o[c] = o[c] * f + g * v[c];
+          M = Mn;
+        }
+        const float w = valid ? uu[e] / Z : 0.f;
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) acc[c] += w * o[c];
+        if (valid) {
+          stats[(e * H + a) * 2] = M;
+          stats[(e * H + a) * 2 + 1] = Z;
+        }
+      }
+      wave_store32(osum + (long long)i * d + cq, acc, l);
+    }
+  }
+}
+
+// Phase 2 (force backward), for ob_i = dE/du_i Wo^T (the adjoint of osum_i):
+//   adjoint of o_e = u_e ob,  w_l = ob . v_l,  cw_e = sum_l p_el w_l,
+//   zb_el = u_e p_el (w_l - cw_e)                    (adjoint of s_el and of log u_l)
+//   qb_e = sum_l zb_el k_l / sqrt(32),  kb_l = sum_e zb_el q_e / sqrt(32),
+//   vb_l = (sum_e u_e p_el) ob,
+//   dE/dr_e += u'(r_e) [cw_e (query weight) + sum_j u_j exp(s_je - M_j)/Z_j (w_e - cw_j) (key weight)]
+// summed over heads.  QKVb [Ne, 3d] gets (qb | kb | vb).
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu,
+    const float* __restrict__ ud, const float* __restrict__ stats, const float* __restrict__ ob, int N, int d, int H,
+    float* __restrict__ QKVb, float* __restrict__ rbar) {
+  __shared__ float s_cw[kAttnWaves][kAttnMaxN];
+  __shared__ float s_rb[kAttnWaves][kAttnMaxN];
+  const int wv = threadIdx.x >> 6;
+  float* cw = s_cw[wv];
+  float* rb = s_rb[wv];
+  const long long ld = 3LL * d;
+  JANUS_WAVE_LOOP(i, N) {
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    for (int j = l; j < n; j += 64) rb[j] = 0.f;
+    for (int a = 0; a < H; ++a) {
+      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      float obr[kAttnDh];
+      ld32(ob + (long long)i * d + cq, obr);
+      // queries
+      for (int q0 = 0; q0 < n; q0 += 64) {
+        const bool valid = q0 + l < n;
+        const long long e = e0 + (valid ? q0 + l : 0);
+        float q[kAttnDh], A1[kAttnDh], A2[kAttnDh];
+        ld32(QKV + e * ld + cq, q);
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) A1[c] = A2[c] = 0.f;
+        const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
+        float s1 = 0.f;
+        for (int j = 0; j < n; ++j) {
+          const long long key = e0 + j;
+          float k[kAttnDh], v[kAttnDh];
+          ld32(QKV + key * ld + ck, k);
+          ld32(QKV + key * ld + cv, v);
+          const float p = uu[key] * __expf(dot32(q, k) * kAttnScale - M) * iZ;
+          const float w = dot32(obr, v);
+          s1 += p * w;
+#pragma unroll
+          for (int c = 0; c < kAttnDh; ++c) {
+            A1[c] += p * w * k[c];
+            A2[c] += p * k[c];
+          }
+        }
+        const float ue = uu[e] * kAttnScale;
+        float qb[kAttnDh];
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) qb[c] = ue * (A1[c] - s1 * A2[c]);
+        if (valid) {
+          st32(QKVb + e * ld + cq, qb);
+          cw[q0 + l] = s1;
+          rb[q0 + l] += s1;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      // keys
+      for (int k0 = 0; k0 < n; k0 += 64) {
+        const bool valid = k0 + l < n;
+        const long long key = e0 + (valid ? k0 + l : 0);
+        float k[kAttnDh], v[kAttnDh], kb[kAttnDh];
+        ld32(QKV + key * ld + ck, k);
+        ld32(QKV + key * ld + cv, v);
+        const float w = dot32(obr, v), uk = uu[key];
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) kb[c] = 0.f;
+        float Pu = 0.f, kl = 0.f;
+        for (int jq = 0; jq < n; ++jq) {
+          const long long e = e0 + jq;
+          float q[kAttnDh];
+          ld32(QKV + e * ld + cq, q);
+          const float E = __expf(dot32(q, k) * kAttnScale - stats[(e * H + a) * 2]) / stats[(e * H + a) * 2 + 1];
+          const float ue = uu[e];
+          const float t = ue * E * (w - cw[jq]);
+          kl += t;
+          Pu += ue * uk * E;
+#pragma unroll
+          for (int c = 0; c < kAttnDh; ++c) kb[c] += uk * t * q[c];
+        }
+        float vb[kAttnDh];
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) {
+          kb[c] *= kAttnScale;
+          vb[c] = Pu * obr[c];
+        }
+        if (valid) {
+          st32(QKVb + key * ld + ck, kb);
+          st32(QKVb + key * ld + cv, vb);
+          rb[k0 + l] += kl;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    for (int j = l; j < n; j += 64) rbar[e0 + j] += ud[e0 + j] * rb[j];
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// Phase 3 (double backward as a tangent sweep): tangents qh, kh, vh of q, k, v and
+// uh = u' rt of the envelope.  Per query:
+//   pz_el = p_el sh_el + uh_l exp(s_el - M_e)/Z_e   (p times the tangent of s + log u)
+//   oh_e  = sum_l pz_el v_l - (sum_l pz_el) o_e + sum_l p_el vh_l
+//   osumh_i = sum_e (u_e oh_e + uh_e o_e).
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
+    const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
+    const float* __restrict__ stats, int N, int d, int H, float* __restrict__ osumh) {
+  const long long ld = 3LL * d;
+  JANUS_WAVE_LOOP(i, N) {
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    for (int a = 0; a < H; ++a) {
+      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      float acc[kAttnDh];
+#pragma unroll
+      for (int c = 0; c < kAttnDh; ++c) acc[c] = 0.f;
+      for (int q0 = 0; q0 < n; q0 += 64) {
+        const bool valid = q0 + l < n;
+        const long long e = e0 + (valid ? q0 + l : 0);
+        float q[kAttnDh], qh[kAttnDh], A1[kAttnDh], A2[kAttnDh], A3[kAttnDh];
+        ld32(QKV + e * ld + cq, q);
+        ld32(QKVh + e * ld + cq, qh);
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) A1[c] = A2[c] = A3[c] = 0.f;
+        const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
+        float s1 = 0.f;
+        for (int j = 0; j < n; ++j) {
+          const long long key = e0 + j;
+          float k[kAttnDh], v[kAttnDh];
+          ld32(QKV + key * ld + ck, k);
+          float sh = dot32(qh, k);
+          const float E = __expf(dot32(q, k) * kAttnScale - M) * iZ;
+          ld32(QKVh + key * ld + ck, k);
+          sh = (sh + dot32(q, k)) * kAttnScale;
+          const float p = uu[key] * E;
+          const float pz = p * sh + ud[key] * rt[key] * E;
+          s1 += pz;
+          ld32(QKV + key * ld + cv, v);
+#pragma unroll
+          for (int c = 0; c < kAttnDh; ++c) {
+            A1[c] += pz * v[c];
+            A2[c] += p * v[c];
+          }
+          ld32(QKVh + key * ld + cv, v);
+#pragma unroll
+          for (int c = 0; c < kAttnDh; ++c) A3[c] += p * v[c];
+        }
+        const float ue = valid ? uu[e] : 0.f, uh = valid ? ud[e] * rt[e] : 0.f;
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) acc[c] += ue * (A1[c] - s1 * A2[c] + A3[c]) + uh * A2[c];
+      }
+      wave_store32(osumh + (long long)i * d + cq, acc, l);
+    }
+  }
+}
+
+// Phase 4 (final backward through the forward and its tangent): alpha_i = adjoint of
+// osum_i (times Wo^T), beta_i = adjoint of the tangent osumh_i (= the phase-2 ob_i).
+// Per query the adjoints of o_e and oh_e are u_e alpha + uh_e beta and u_e beta; with
+// a_l = alpha.v_l + beta.vh_l, b_l = beta.v_l and, per query, am = sum p a, bm = sum p b,
+// zm = sum pz, pbz = sum pz b, SP = u_e (am + pbz - 2 zm bm) + uh_e bm:
+//   zb_el  = u_e (p a_l + b_l (pz - p zm) - pz bm) + uh_e p b_l - p SP   (adjoint of s_el)
+//   zhb_el = u_e p (b_l - bm)                                            (adjoint of sh_el)
+//   qb_e = sum_l (zb k_l + zhb kh_l)/sqrt(32),  kb_l = sum_e (zb q_e + zhb qh_e)/sqrt(32),
+//   vb_l = alpha sum_e u_e p + beta sum_e (uh_e p + u_e (pz - p zm)).
+// QKVa [Ne, 3d] gets (qb | kb | vb), the adjoints of the primal q, k, v.
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
+    const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
+    const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
+    int H, float* __restrict__ QKVa) {
+  __shared__ float s_sc[kAttnWaves][7][kAttnMaxN];
+  const int wv = threadIdx.x >> 6;
+  float* sa = s_sc[wv][0];
+  float* sb = s_sc[wv][1];
+  float* am_ = s_sc[wv][2];
+  float* bm_ = s_sc[wv][3];
+  float* zm_ = s_sc[wv][4];
+  float* sp_ = s_sc[wv][5];
+  const long long ld = 3LL * d;
+  JANUS_WAVE_LOOP(i, N) {
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    for (int a = 0; a < H; ++a) {
+      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      // per key: a_l, b_l
+      for (int k0 = 0; k0 < n; k0 += 64) {
+        const bool valid = k0 + l < n;
+        const long long key = e0 + (valid ? k0 + l : 0);
+        float x[kAttnDh], v[kAttnDh];
+        ld32(QKV + key * ld + cv, v);
+        ld32(beta + (long long)i * d + cq, x);
+        const float bj = dot32(x, v);
+        float aj = 0.f;
+        ld32(QKVh + key * ld + cv, v);
+        aj += dot32(x, v);
+        ld32(QKV + key * ld + cv, v);
+        ld32(alpha + (long long)i * d + cq, x);
+        aj += dot32(x, v);
+        if (valid) {
+          sa[k0 + l] = aj;
+          sb[k0 + l] = bj;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      // queries, sweep 1: per-query sums
+      for (int q0 = 0; q0 < n; q0 += 64) {
+        const bool valid = q0 + l < n;
+        const long long e = e0 + (valid ? q0 + l : 0);
+        float q[kAttnDh], qh[kAttnDh];
+        ld32(QKV + e * ld + cq, q);
+        ld32(QKVh + e * ld + cq, qh);
+        const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
+        float am = 0.f, bm = 0.f, zm = 0.f, pbz = 0.f;
+        for (int j = 0; j < n; ++j) {
+          const long long key = e0 + j;
+          float k[kAttnDh], kh[kAttnDh];
+          ld32(QKV + key * ld + ck, k);
+          ld32(QKVh + key * ld + ck, kh);
+          const float E = __expf(dot32(q, k) * kAttnScale - M) * iZ;
+          const float sh = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
+          const float p = uu[key] * E;
+          const float pz = p * sh + ud[key] * rt[key] * E;
+          const float aj = sa[j], bj = sb[j];
+          am += p * aj;
+          bm += p * bj;
+          zm += pz;
+          pbz += pz * bj;
+        }
+        const float ue = uu[e], uh = ud[e] * rt[e];
+        if (valid) {
+          am_[q0 + l] = am;
+          bm_[q0 + l] = bm;
+          zm_[q0 + l] = zm;
+          sp_[q0 + l] = ue * (am + pbz - 2.f * zm * bm) + uh * bm;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      // queries, sweep 2: qb
+      for (int q0 = 0; q0 < n; q0 += 64) {
+        const bool valid = q0 + l < n;
+        const int jq = valid ? q0 + l : 0;
+        const long long e = e0 + jq;
+        float q[kAttnDh], qh[kAttnDh], qb[kAttnDh];
+        ld32(QKV + e * ld + cq, q);
+        ld32(QKVh + e * ld + cq, qh);
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) qb[c] = 0.f;
+        const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
+        const float ue = uu[e], uh = ud[e] * rt[e];
+        const float bm = bm_[jq], zm = zm_[jq], SP = sp_[jq];
+        for (int j = 0; j < n; ++j) {
+          const long long key = e0 + j;
+          float k[kAttnDh], kh[kAttnDh];
+          ld32(QKV + key * ld + ck, k);
+          ld32(QKVh + key * ld + ck, kh);
+          const float E = __expf(dot32(q, k) * kAttnScale - M) * iZ;
+          const float sh = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
+          const float p = uu[key] * E;
+          const float pz = p * sh + ud[key] * rt[key] * E;
+          const float aj = sa[j], bj = sb[j];
+          const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
+          const float zhb = ue * p * (bj - bm);
+#pragma unroll
+          for (int c = 0; c < kAttnDh; ++c) qb[c] += zb * k[c] + zhb * kh[c];
+        }
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) qb[c] *= kAttnScale;
+        if (valid) st32(QKVa + e * ld + cq, qb);
+      }
+      // keys: kb and vb
+      for (int k0 = 0; k0 < n; k0 += 64) {
+        const bool valid = k0 + l < n;
+        const int jk = valid ? k0 + l : 0;
+        const long long key = e0 + jk;
+        float k[kAttnDh], kh[kAttnDh], kb[kAttnDh];
+        ld32(QKV + key * ld + ck, k);
+        ld32(QKVh + key * ld + ck, kh);
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) kb[c] = 0.f;
+        const float uk = uu[key], uhk = ud[key] * rt[key], aj = sa[jk], bj = sb[jk];
+        float S1 = 0.f, S2 = 0.f;
+        for (int jq = 0; jq < n; ++jq) {
+          const long long e = e0 + jq;
+          float q[kAttnDh], qh[kAttnDh];
+          ld32(QKV + e * ld + cq, q);
+          ld32(QKVh + e * ld + cq, qh);
+          const float E = __expf(dot32(q, k) * kAttnScale - stats[(e * H + a) * 2]) / stats[(e * H + a) * 2 + 1];
+          const float sh = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
+          const float p = uk * E;
+          const float pz = p * sh + uhk * E;
+          const float ue = uu[e], uh = ud[e] * rt[e];
+          const float bm = bm_[jq], zm = zm_[jq], SP = sp_[jq];
+          const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
+          const float zhb = ue * p * (bj - bm);
+          S1 += ue * p;
+          S2 += uh * p + ue * (pz - p * zm);
+#pragma unroll
+          for (int c = 0; c < kAttnDh; ++c) kb[c] += zb * q[c] + zhb * qh[c];
+        }
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) kb[c] *= kAttnScale;
+        if (valid) st32(QKVa + key * ld + ck, kb);
+        float al[kAttnDh], be[kAttnDh];
+        ld32(alpha + (long long)i * d + cq, al);
+        ld32(beta + (long long)i * d + cq, be);
+#pragma unroll
+        for (int c = 0; c < kAttnDh; ++c) kb[c] = S1 * al[c] + S2 * be[c];
+        if (valid) st32(QKVa + key * ld + cv, kb);
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+}
+
+// Messages per edge from the expert slots: out_e = sum_c Y[pos[e, c]] (already gated).
+template <int VPL, int KC>
+__global__ void edge_sum_kernel(const int* __restrict__ pos, const float* __restrict__ Y, long long Ne, int d,
+                                float* __restrict__ out) {
+  JANUS_WAVE_LOOP(e, Ne) {
+    float y[VPL];
+    sum_slots<VPL, KC>(Y, pos, e, d, l, y);
+    st_row<VPL>(out + e * d, l, y);
+  }
+}
+
+// Slot rows of a per-edge adjoint: out[pos[e, c]] = (g_ec) src_e.
+template <int VPL, int KC>
+__global__ void edge_gather_kernel(const int* __restrict__ pos, const float* __restrict__ gate,
+                                   const float* __restrict__ src, long long Ne, int d, float* __restrict__ out) {
+  JANUS_WAVE_LOOP(e, Ne) {
+    float s[VPL];
+    ld_row<VPL>(src + e * d, l, s);
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      const long long f = e * KC + c;
+      const float g = gate ? gate[f] : 1.f;
+      float o[VPL];
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) o[v] = g * s[v];
+      st_row<VPL>(out + (long long)pos[f] * d, l, o);
+    }
+  }
+}
+
+// Phase 3 per edge: mh_e = sum_c g_ec Ybt[pos[e, c]] (tangent of the message) and the gate
+// adjoints g3_ec = Ybt[pos[e, c]] . mbar_e (mbar = the phase-2 adjoint of the message).
+template <int VPL, int KC>
+__global__ void edge_combine_p3_kernel(const int* __restrict__ pos, const float* __restrict__ gate,
+                                       const float* __restrict__ Ybt, const float* __restrict__ mbar, long long Ne,
+                                       int d, float* __restrict__ g3, float* __restrict__ mh) {
+  JANUS_WAVE_LOOP(e, Ne) {
+    float mb[VPL], acc[VPL];
+    ld_row<VPL>(mbar + e * d, l, mb);
+    zero_row<VPL>(acc);
+    float s[KC];
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      float y[VPL];
+      ld_row<VPL>(Ybt + (long long)pos[e * KC + c] * d, l, y);
+      const float g = gate[e * KC + c];
+      s[c] = 0.f;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) {
+        s[c] += y[v] * mb[v];
+        acc[v] += g * y[v];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < KC; ++c) s[c] = wave_sum(s[c]);
+    if (l == 0) {
+#pragma unroll
+      for (int c = 0; c < KC; ++c) g3[e * KC + c] = s[c];
+    }
+    st_row<VPL>(mh + e * d, l, acc);
+  }
+}
+
+// Largest neighbourhood: flag[0] |= 2 when an atom has more than kAttnMaxN edges.
+__global__ void attn_degree_check_kernel(const int* __restrict__ rowptr, int N, int* __restrict__ flag) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < N && rowptr[i + 1] - rowptr[i] > kAttnMaxN) atomicOr(flag + 1, 1);
+}
+
+}  // namespace janus

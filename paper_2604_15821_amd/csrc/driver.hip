@@ -183,6 +183,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   const long long Mf = p.Mf;
   const int Ef = p.Ef, kf = p.kf, hf = p.hdf;
   if (atom) hipLaunchKernelGGL(iota_kernel, dim3(cdiv(N + 1, 256)), dim3(256), 0, st, p.iota, N);
+  const bool attn = p.attn != 0;
+  const int H = p.H;
   {
     PROF(PROF_GRAPH, 0, Ne * (12.0 + 3.0 + 16.0 + 8.0 * nb));
     launch_geometry(st, pos, cell, p.sid, ei, ej, shift, (int)Ne, cfg.r_cut, nb, p.geo, p.B, p.dB,
@@ -215,6 +217,12 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     hipLaunchKernelGGL(set_rows_kernel, dim3(1), dim3(64), 0, st, p.rowN, N, p.rowE, Ne);
     build_tables(st, p.rowN, 1, p.kcN, p.tilesN, p.ntN, p.chunksN, p.ncN, p.cfN);
     build_tables(st, p.rowE, 1, p.kcE, nullptr, nullptr, p.chunksE, p.ncE, p.cfE);
+    if (attn) {
+      build_tables(st, p.rowE, 1, p.kcA, p.tilesE, p.ntE, p.chunksA, p.ncA, p.cfA);
+      if (Ne > 0)
+        hipLaunchKernelGGL(attn_env_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, (const float4*)p.geo, Ne,
+                           cfg.r_cut, p.eu, p.eud);
+    }
     for (int t = 0; t < T; ++t) {
       RouteArgs ra;
       ra.Pc = Wp(blk(t, "Pc"));
@@ -330,6 +338,20 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   auto Ybf = [&](int t) { return p.Ybf + t * Mf * d; };
   auto UU = [&](int t) { return p.uu + t * Nd; };
   const int* iota = p.iota;
+
+  // attention views of block t
+  const long long sEd = Ne * d + 4, sE3 = 3 * Ne * d + 4, sNd = Nd + 4, sSt = 2 * Ne * H + 4;
+  auto MM = [&](int t) { return p.Mm + t * sEd; };
+  auto QKVt = [&](int t) { return p.QKV + t * sE3; };
+  auto STt = [&](int t) { return p.stats + t * sSt; };
+  auto OSt = [&](int t) { return p.osum + t * sNd; };
+  auto OBt = [&](int t) { return p.OB + t * sNd; };
+  auto QKVbt = [&](int t) { return p.QKVb + t * sE3; };
+  auto MBt = [&](int t) { return p.MB + t * sEd; };
+  auto MHt = [&](int t) { return p.Mh + t * sEd; };
+  auto QKVht = [&](int t) { return p.QKVh + t * sE3; };
+  const double f_qkv = 6.0 * Ne * d * d;
+  const double by_attn = Ne * (12.0 * d + 8.0 * H + 8.0) + N * 8.0 * d;
   const double f_atm = 2.0 * Mf * d * hf;
   const double by_fgather = N * 4.0 * d + Mf * (8.0 + 4.0 * d);
   const double by_fcombine = N * 8.0 * d + Mf * (4.0 + 4.0 * d);
@@ -380,11 +402,33 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
       launch_rows<false>(st, LoadSilu{Aa(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiRowScale{p.T1, SG(t), d});
     }
-    {
-      // u = h + messages (h^{t+1} itself without the feature-update MoE)
+    // u = h + messages (h^{t+1} itself without the feature-update MoE)
+    float* u_out = atom ? p.ut : HV(p.h, t + 1);
+    if (attn) {
+      // messages per edge -> q|k|v -> attention over each neighbourhood -> u = h + osum Wo
+      {
+        PROF(PROF_EDGE, 0, Ne * (4.0 * k + 4.0 * k * d + 4.0 * d));
+        LAUNCH_VPL_K(edge_sum_kernel, d, k, gE, b256, 0, st, POS(t), (const float*)p.T1, Ne, d, MM(t));
+      }
+      {
+        PROF(PROF_DENSE_GEMM, f_qkv, 0);
+        launch_rows<false>(st, LoadPlain{MM(t), d}, Wp(blk(t, "Wqkv")), d, 3 * d, p.tilesE, p.ntE, p.mtE,
+                           EpiStore{QKVt(t), 3LL * d});
+      }
+      {
+        PROF(PROF_ATTN, 0, by_attn);
+        hipLaunchKernelGGL(attn_fwd_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)p.eu, N,
+                           d, H, STt(t), OSt(t));
+      }
+      {
+        PROF(PROF_DENSE_GEMM, f_dense, 0);
+        launch_rows<false>(st, LoadPlain{OSt(t), d}, Wp(blk(t, "Wo")), d, d, p.tilesN, p.ntN, p.mtN,
+                           EpiAdd{u_out, HV(p.h, t), d});
+      }
+    } else {
       PROF(PROF_ATOM, 0, by_combine);
       LAUNCH_VPL_K(combine_fwd_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)p.T1,
-                 (const float*)HV(p.h, t), N, d, atom ? p.ut : HV(p.h, t + 1));
+                 (const float*)HV(p.h, t), N, d, u_out);
     }
     if (atom) {
       // feature-update MoE: h^{t+1} = u + sum_c g W2f^T SiLU(W1f^T u)
@@ -462,7 +506,29 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       hbar_u = UU(t);
     }
-    {
+    if (attn) {
+      // adjoint of osum (ob = dE/du Wo^T) -> attention backward -> message adjoints -> slots
+      {
+        PROF(PROF_DENSE_GEMM, f_dense, 0);
+        launch_rows<true>(st, LoadPlain{hbar_u, d}, Wp(blk(t, "Wo")), d, d, p.tilesN, p.ntN, p.mtN,
+                          EpiStore{OBt(t), d});
+      }
+      {
+        PROF(PROF_ATTN, 0, by_attn);
+        hipLaunchKernelGGL(attn_bwd_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)p.eu,
+                           (const float*)p.eud, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t),
+                           p.rbar);
+      }
+      {
+        PROF(PROF_DENSE_GEMM, f_qkv, 0);
+        launch_rows<true>(st, LoadPlain{QKVbt(t), 3LL * d}, Wp(blk(t, "Wqkv")), 3 * d, d, p.tilesE, p.ntE, p.mtE,
+                          EpiStore{MBt(t), d});
+      }
+      {
+        PROF(PROF_EDGE, 0, Ne * (4.0 * d + 8.0 * k + 4.0 * k * d));
+        LAUNCH_VPL_K(edge_gather_kernel, d, k, gE, b256, 0, st, POS(t), GATE(t), (const float*)MBt(t), Ne, d, Ybs(t));
+      }
+    } else {
       PROF(PROF_ATOM, 0, by_gather);
       LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), hbar_u, N, d, Ybs(t));
     }
@@ -631,12 +697,40 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       launch_wgrad(st, LoadPlain{Ab(t), h}, LoadPlain{Ybs(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
                    p.partial, Gp(blk(t, "W2")), 1);
     }
-    {
-      // adjoint of the gathered dE/du (of hh^{t+1} without the feature-update MoE)
+    // phase-2 dE/du of this block (hh^{t+1} without the feature-update MoE)
+    const float* hbar_u3 = atom ? UU(t) : HV(p.hh, t + 1);
+    float* uh_out = atom ? p.ut : HV(p.hht, t + 1);
+    if (attn) {
+      // tangent of the messages and gate adjoints -> tangent q|k|v -> attention tangent -> u-tangent
+      {
+        PROF(PROF_EDGE, 0, Ne * (8.0 * d + 12.0 * k + 4.0 * k * d));
+        LAUNCH_VPL_K(edge_combine_p3_kernel, d, k, gE, b256, 0, st, POS(t), GATE(t), (const float*)p.T2,
+                     (const float*)MBt(t), Ne, d, p.g3 + t * M, MHt(t));
+      }
+      {
+        PROF(PROF_DENSE_GEMM, f_qkv, 0);
+        launch_rows<false>(st, LoadPlain{MHt(t), d}, Wp(blk(t, "Wqkv")), d, 3 * d, p.tilesE, p.ntE, p.mtE,
+                           EpiStore{QKVht(t), 3LL * d});
+      }
+      {
+        PROF(PROF_ATTN, 0, by_attn);
+        hipLaunchKernelGGL(attn_tan_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)QKVht(t),
+                           (const float*)p.eu, (const float*)p.eud, (const float*)p.rt, (const float*)STt(t), N, d, H,
+                           p.osh);
+      }
+      {
+        PROF(PROF_DENSE_GEMM, 2 * f_dense, 0);
+        launch_rows<false>(st, LoadPlain{p.osh, d}, Wp(blk(t, "Wo")), d, d, p.tilesN, p.ntN, p.mtN,
+                           EpiAdd{uh_out, hht_t, d});
+        // dWo (tangent part): osumh^T dE/du
+        launch_wgrad(st, LoadPlain{p.osh, d}, LoadPlain{hbar_u3, d}, d, d, p.chunksN, p.ncN, p.cfN, p.mcN, 1,
+                     p.partial, Gp(blk(t, "Wo")), 1);
+      }
+    } else {
+      // adjoint of the gathered dE/du
       PROF(PROF_ATOM, 0, by_cp3);
-      LAUNCH_VPL_K(combine_p3_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), (const float*)p.T2,
-                   (const float*)(atom ? UU(t) : HV(p.hh, t + 1)), hht_t, N, d, p.g3 + t * M,
-                   atom ? p.ut : HV(p.hht, t + 1));
+      LAUNCH_VPL_K(combine_p3_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), (const float*)p.T2, hbar_u3,
+                   hht_t, N, d, p.g3 + t * M, uh_out);
     }
     if (atom) {
       // double backward of the feature-update MoE's force backward (same products as G5-G8)
@@ -751,7 +845,37 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       a_u = p.ut;
     }
-    {
+    if (attn) {
+      // adjoints of osum and of its tangent -> attention reverse -> primal message adjoints
+      const float* Wqkv = Wp(blk(t, "Wqkv"));
+      {
+        PROF(PROF_DENSE_GEMM, 2 * f_dense, 0);
+        launch_rows<true>(st, LoadPlain{a_u, d}, Wp(blk(t, "Wo")), d, d, p.tilesN, p.ntN, p.mtN, EpiStore{p.AO, d});
+        // dWo (primal part): osum^T a_u
+        launch_wgrad(st, LoadPlain{OSt(t), d}, LoadPlain{a_u, d}, d, d, p.chunksN, p.ncN, p.cfN, p.mcN, 1,
+                     p.partial, Gp(blk(t, "Wo")), 1);
+      }
+      {
+        PROF(PROF_ATTN, 0, by_attn);
+        hipLaunchKernelGGL(attn_rev_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)QKVht(t),
+                           (const float*)p.eu, (const float*)p.eud, (const float*)p.rt, (const float*)STt(t),
+                           (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa);
+      }
+      {
+        PROF(PROF_DENSE_GEMM, 3 * f_qkv, 0);
+        launch_rows<true>(st, LoadPlain{p.QKVa, 3LL * d}, Wqkv, 3 * d, d, p.tilesE, p.ntE, p.mtE, EpiStore{p.mta, d});
+        // dWqkv: m^T (q|k|v adjoints) + mh^T (phase-2 q|k|v adjoints = adjoints of the tangents)
+        launch_wgrad(st, LoadPlain{MM(t), d}, LoadPlain{p.QKVa, 3LL * d}, d, 3 * d, p.chunksA, p.ncA, p.cfA, p.mcA, 1,
+                     p.partial, Gp(blk(t, "Wqkv")), 1);
+        launch_wgrad(st, LoadPlain{MHt(t), d}, LoadPlain{QKVbt(t), 3LL * d}, d, 3 * d, p.chunksA, p.ncA, p.cfA,
+                     p.mcA, 1, p.partial, Gp(blk(t, "Wqkv")), 1);
+      }
+      {
+        PROF(PROF_EDGE, 0, Ne * (4.0 * d + 4.0 * k + 4.0 * k * d));
+        LAUNCH_VPL_K(edge_gather_kernel, d, k, gE, b256, 0, st, POS(t), (const float*)nullptr, (const float*)p.mta,
+                     Ne, d, p.T1);
+      }
+    } else {
       // message adjoint, ungated, into the slots
       PROF(PROF_ATOM, 0, by_gather);
       LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)nullptr, a_u, N, d,
@@ -1003,13 +1127,16 @@ extern "C" int janus_step_stress(janus_ctx* ctx, const float* pos, const float* 
                          nl->rev, (const int*)sid, N, Ne, flag);
     hipLaunchKernelGGL(struct_edges_kernel, dim3(cdiv(S + 1, 256)), dim3(256), 0, st, offsets, nl->rowptr, S, N,
                        sedge);
+    if (cfg.n_heads)
+      hipLaunchKernelGGL(attn_degree_check_kernel, dim3(cdiv(N, 256)), dim3(256), 0, st, nl->rowptr, N, flag);
   }
   JANUS_HIP_TRY(hipGetLastError());
   int* hp = ctx->host_plan;
-  JANUS_HIP_TRY(hipMemcpyAsync(hp, flag, sizeof(int), hipMemcpyDeviceToHost, st));
+  JANUS_HIP_TRY(hipMemcpyAsync(hp, flag, 2 * sizeof(int), hipMemcpyDeviceToHost, st));
   JANUS_HIP_TRY(hipMemcpyAsync(hp + 4, sedge, sizeof(int) * 2 * (S + 1), hipMemcpyDeviceToHost, st));
   JANUS_HIP_TRY(hipStreamSynchronize(st));
   if (hp[0]) return JANUS_EINVAL;
+  if (hp[1]) return JANUS_EUNSUPPORTED;   // a neighbourhood larger than the attention kernels hold
   const int* h_erow = hp + 4;            // first edge of structure s
   const int* h_off = hp + 4 + (S + 1);   // first atom of structure s
   // triplets per structure (second read, once the indices are known to be valid)

@@ -161,6 +161,22 @@ struct EpiRowScale {   // c = s[r] * v
   }
 };
 
+// C = A B + R (residual R may be null): the attention output added to the atom features.
+struct EpiAdd {
+  float* c;
+  const float* r;
+  long long ld;
+  static constexpr bool kRowSum = false;
+  using Raw = float4;
+  __device__ __forceinline__ Raw load(long long row, int col) const {
+    return r ? ld4(r + row * ld + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  __device__ __forceinline__ float store(long long row, int col, float4 v, const Raw& x) const {
+    st4(c + row * ld + col, make_float4(v.x + x.x, v.y + x.y, v.z + x.z, v.w + x.w));
+    return 0.f;
+  }
+};
+
 // Force backward, after Sbar = Ybar W2^T: keep Sbar and Abar = SiLU'(A) Sbar.
 struct EpiP2 {
   const float* A;

@@ -22,6 +22,7 @@ enum JanusProfClass {
   PROF_ROUTE,             // routing and the expert permutation
   PROF_GRAPH,             // neighbour list, reverse map, geometry and basis
   PROF_OTHER,             // validation, readout, loss, forces, router and embedding gradients
+  PROF_ATTN,              // neighbourhood self-attention (per-atom query / key passes)
   PROF_NCLASS
 };
 

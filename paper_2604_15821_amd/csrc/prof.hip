@@ -5,8 +5,8 @@
 
 namespace janus {
 
-static const char* kProfNames[PROF_NCLASS] = {"expert_gemm", "expert_wgrad", "dense_gemm", "edge",
-                                              "atom",        "route",        "graph",      "other"};
+static const char* kProfNames[PROF_NCLASS] = {"expert_gemm", "expert_wgrad", "dense_gemm", "edge",     "atom",
+                                              "route",       "graph",        "other",      "attention"};
 
 static hipEvent_t take_event(janus_ctx* c) {
   if (c->prof_used == c->prof_pool.size()) {

@@ -16,6 +16,7 @@
 #include "kernels.h"
 #include "route.h"
 #include "tri.h"
+#include "attn.h"
 
 namespace janus {
 
@@ -538,8 +539,8 @@ int check_config(const janus_config* c) {
   }
   if (!(c->w_S >= 0.f)) return JANUS_EINVAL;
   if (c->n_heads < 0 || (c->n_heads && c->d % c->n_heads)) return JANUS_EINVAL;
-  // the step does not run neighbourhood attention yet
-  if (c->n_heads) return JANUS_EUNSUPPORTED;
+  // heads of 32 columns
+  if (c->n_heads && c->d / c->n_heads != kAttnDh) return JANUS_EUNSUPPORTED;
   if (c->atom_moe) {
     if (c->n_experts_f < 1 || c->n_experts_f > 64 || c->top_k_f < 1 || c->top_k_f > 4 ||
         c->top_k_f > c->n_experts_f || c->d_hidden_f < 64)
@@ -608,6 +609,15 @@ struct Plan {
   WChunk* chunksf;
   int *nchunksf, *cfirstf;
   float *Xsf, *Af, *Sbf, *Abf, *Ybf, *uu, *T1f, *T2f, *ut, *gpartf, *gtf, *ltf;
+  // neighbourhood attention: per block messages, q|k|v, softmax statistics, atom
+  // sums, first-order adjoints, tangents; temporaries; GEMM tables over Ne rows
+  float *eu, *eud;
+  float *Mm, *QKV, *stats, *osum, *OB, *QKVb, *MB, *Mh, *QKVh;
+  float *AO, *QKVa, *mta, *osh;
+  RowsTile* tilesE;
+  int* ntE;
+  WChunk* chunksA;
+  int *ncA, *cfA;
   // sizes
   int T, E, k, d, hdim, nb, nsp, N, S;
   long long Ne, M;
@@ -618,6 +628,7 @@ struct Plan {
   int atom, Ef, kf, hdf;
   long long Mf;
   int mtf, kcf, mcf, nchf, ntilef;
+  int attn, H, mtE, kcA, mcA;
 };
 
 size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, long long Ne, long long Nt = 0) {
@@ -745,6 +756,14 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.ntilef = (p.hdf + GBN - 1) / GBN;
     part = std::max(part, (long long)p.mcf * d * p.hdf);
   }
+  p.attn = c.n_heads ? 1 : 0;
+  p.H = c.n_heads;
+  if (p.attn) {
+    p.mtE = max_rows_tiles(Ne, 1);
+    p.kcA = wgrad_chunk_rows(Ne, d, 3 * d);
+    p.mcA = max_wchunks(Ne, 1, p.kcA);
+    part = std::max(part, (long long)p.mcA * d * 3 * d);
+  }
   p.partial = cv.take<float>(part);
   p.cei = cv.take<int>(Ne + 1);
   p.cej = cv.take<int>(Ne + 1);
@@ -853,6 +872,29 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.gpartf = cv.take<float>(Mf * p.ntilef + 4);
     p.gtf = cv.take<float>(Mf + 1);
     p.ltf = cv.take<float>((long long)N * Ef + 1);
+  }
+  if (p.attn) {
+    const long long Ed = Ne * d + 4, E3d = 3 * Ne * d + 4;
+    p.eu = cv.take<float>(Ne + 1);
+    p.eud = cv.take<float>(Ne + 1);
+    p.Mm = cv.take<float>(T * Ed);
+    p.QKV = cv.take<float>(T * E3d);
+    p.stats = cv.take<float>(T * (2 * Ne * p.H + 4));
+    p.osum = cv.take<float>(T * Nd + 4);
+    p.OB = cv.take<float>(T * Nd + 4);
+    p.QKVb = cv.take<float>(T * E3d);
+    p.MB = cv.take<float>(T * Ed);
+    p.Mh = cv.take<float>(T * Ed);
+    p.QKVh = cv.take<float>(T * E3d);
+    p.AO = cv.take<float>(Nd + 4);
+    p.QKVa = cv.take<float>(E3d);
+    p.mta = cv.take<float>(Ed);
+    p.osh = cv.take<float>(Nd + 4);
+    p.tilesE = cv.take<RowsTile>(p.mtE);
+    p.ntE = cv.take<int>(1);
+    p.chunksA = cv.take<WChunk>(p.mcA);
+    p.ncA = cv.take<int>(1);
+    p.cfA = cv.take<int>(2);
   }
   return cv.size();
 }

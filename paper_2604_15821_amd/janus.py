@@ -277,7 +277,8 @@ class Context:
         return int(_lib().janus_last_triplets(self.h))
 
     # ------------------------------------------------------------- profiler
-    PROFILE_FAMILIES = ["expert_gemm", "expert_wgrad", "dense_gemm", "edge", "atom", "route", "graph", "other"]
+    PROFILE_FAMILIES = ["expert_gemm", "expert_wgrad", "dense_gemm", "edge", "atom", "route", "graph", "other",
+                        "attention"]
 
     def profile(self, on: bool, families=None):
         """Start (on) or stop the event profiler; `families` restricts it to some kernel families."""

@@ -24,7 +24,7 @@ def _step(b, limit=None):
     return out
 
 
-@pytest.mark.parametrize("name", ["small", "atom_moe", "stress"])
+@pytest.mark.parametrize("name", ["small", "atom_moe", "stress", "attention"])
 def test_chunked_step_matches_single_pass_and_oracle(name):
     from oracle.model import Params, forward_energy, training_step
     from paper_2604_15821_amd import janus

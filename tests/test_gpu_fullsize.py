@@ -20,7 +20,7 @@ from helpers import TOL_E, TOL_F, TOL_W, banner, energy_error, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["small", "threebody", "atom_moe", "stress", "shard", "irregular"]
+FULL = ["small", "threebody", "atom_moe", "stress", "attention", "shard", "irregular"]
 
 
 def _gpu_step(b, model=None):
