@@ -11,10 +11,12 @@
 // One wave per atom loops over the heads.  Passes with one lane per query
 // keep the query row in registers and read every key row once per 64
 // queries (all lanes the same row); passes with one lane per key do the
-// transpose.  Per-query softmax statistics (max of s, Z = sum u exp(s - max))
-// are stored by the forward and reused by the three backward phases.  Per-edge
-// scalars shared between the passes of one head live in LDS, so a
-// neighbourhood holds at most kAttnMaxN edges (checked before the step).
+// transpose.  The rows a pass loops over are staged in LDS 32 at a time (each
+// wave its own region) and read back as broadcasts.  Per-query softmax
+// statistics (max of s, Z = sum u exp(s - max)) are stored by the forward and
+// reused by the three backward phases.  Per-edge scalars shared between the
+// passes of one head live in LDS, so a neighbourhood holds at most kAttnMaxN
+// edges (checked before the step).
 #pragma once
 
 #include "edge.h"
@@ -42,11 +44,13 @@ __device__ __forceinline__ void st32(float* __restrict__ p, const float* x) {
     *reinterpret_cast<float4*>(p + c) = make_float4(x[c], x[c + 1], x[c + 2], x[c + 3]);
 }
 
+// Four independent partial sums: a single 32-long chain of dependent multiply-adds
+// leaves the vector unit waiting on each result.
 __device__ __forceinline__ float dot32(const float* a, const float* b) {
-  float s = 0.f;
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int c = 0; c < kAttnDh; ++c) s += a[c] * b[c];
-  return s;
+  for (int c = 0; c < kAttnDh; ++c) s[c & 3] += a[c] * b[c];
+  return (s[0] + s[1]) + (s[2] + s[3]);
 }
 
 // Row sums of a per-lane 32-vector over the wave, stored by lanes 0..31.
@@ -75,15 +79,52 @@ __global__ void attn_env_kernel(const float4* __restrict__ geo, long long Ne, fl
   ud[e] = (float)(du / rc);
 }
 
+constexpr int kAttnChunk = 32;   // key (or query) rows staged in LDS at a time
+
+// Orders one wave's LDS writes before its later reads (and reads before later overwrites).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Up to four 32-column blocks of the rows of one neighbourhood.
+struct AttnCols {
+  const float* p[4];
+};
+
+// Stage rows row0 .. row0+cnt-1 (cnt <= kAttnChunk) into LDS, NM column blocks per
+// row: lds[r * NM*32 + m*32 + c] = src.p[m][(row0 + r) * ld + c].  Two lanes per row.
+template <int NM>
+__device__ __forceinline__ void stage_rows(float* lds, const AttnCols& src, long long ld, long long row0, int cnt,
+                                           int l) {
+  const int r = l >> 1, hf = (l & 1) * 16;
+  if (r < cnt) {
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      const float* g = src.p[m] + (row0 + r) * ld + hf;
+      float* s = lds + r * NM * kAttnDh + m * kAttnDh + hf;
+#pragma unroll
+      for (int c = 0; c < 16; c += 4) *reinterpret_cast<float4*>(s + c) = *reinterpret_cast<const float4*>(g + c);
+    }
+  }
+}
+
 // Phase 1: osum_i (one wave per atom; lanes = queries).  stats[(e*H + a)*2 + {0,1}] = (max s, Z).
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu, int N, int d, int H,
     float* __restrict__ stats, float* __restrict__ osum) {
+  __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
+  __shared__ float s_u[kAttnWaves][kAttnChunk];
+  const int wv = threadIdx.x >> 6;
+  float* rows = s_rows[wv];
+  float* su = s_u[wv];
   const long long ld = 3LL * d;
   JANUS_WAVE_LOOP(i, N) {
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
     for (int a = 0; a < H; ++a) {
       const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      const AttnCols kvc{{QKV + ck, QKV + cv, nullptr, nullptr}};
       float acc[kAttnDh];
 #pragma unroll
       for (int c = 0; c < kAttnDh; ++c) acc[c] = 0.f;
@@ -95,18 +136,24 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_kernel(
 #pragma unroll
         for (int c = 0; c < kAttnDh; ++c) o[c] = 0.f;
         float M = -INFINITY, Z = 0.f;
-        for (int j = 0; j < n; ++j) {
-          const long long key = e0 + j;
-          float k[kAttnDh], v[kAttnDh];
-          ld32(QKV + key * ld + ck, k);
-          ld32(QKV + key * ld + cv, v);
-          const float s = dot32(q, k) * kAttnScale;
-          const float Mn = fmaxf(M, s);
-          const float f = __expf(M - Mn), g = uu[key] * __expf(s - Mn);
-          Z = Z * f + g;
+        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
+          const int cnt = min(kAttnChunk, n - j0);
+          wave_sync();
+          stage_rows<2>(rows, kvc, ld, e0 + j0, cnt, l);
+          if (l < cnt) su[l] = uu[e0 + j0 + l];
+          wave_sync();
+          for (int jj = 0; jj < cnt; ++jj) {
+            float k[kAttnDh], v[kAttnDh];
+            ld32(rows + jj * 2 * kAttnDh, k);
+            const float s = dot32(q, k) * kAttnScale;
+            const float Mn = fmaxf(M, s);
+            const float f = __expf(M - Mn), g = su[jj] * __expf(s - Mn);
+            Z = Z * f + g;
+            ld32(rows + jj * 2 * kAttnDh + kAttnDh, v);
 #pragma unroll
-          for (int c = 0; c < kAttnDh; ++c) o[c] = o[c] * f + g * v[c];
-          M = Mn;
+            for (int c = 0; c < kAttnDh; ++c) o[c] = o[c] * f + g * v[c];
+            M = Mn;
+          }
         }
         const float w = valid ? uu[e] / Z : 0.f;
 #pragma unroll
@@ -132,17 +179,26 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu,
     const float* __restrict__ ud, const float* __restrict__ stats, const float* __restrict__ ob, int N, int d, int H,
     float* __restrict__ QKVb, float* __restrict__ rbar) {
+  __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
+  __shared__ float s_sc[kAttnWaves][3][kAttnChunk];
   __shared__ float s_cw[kAttnWaves][kAttnMaxN];
   __shared__ float s_rb[kAttnWaves][kAttnMaxN];
   const int wv = threadIdx.x >> 6;
+  float* rows = s_rows[wv];
+  float* s0 = s_sc[wv][0];
+  float* s1v = s_sc[wv][1];
+  float* s2 = s_sc[wv][2];
   float* cw = s_cw[wv];
   float* rb = s_rb[wv];
   const long long ld = 3LL * d;
   JANUS_WAVE_LOOP(i, N) {
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    wave_sync();
     for (int j = l; j < n; j += 64) rb[j] = 0.f;
     for (int a = 0; a < H; ++a) {
       const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      const AttnCols kvc{{QKV + ck, QKV + cv, nullptr, nullptr}};
+      const AttnCols qc{{QKV + cq, nullptr, nullptr, nullptr}};
       float obr[kAttnDh];
       ld32(ob + (long long)i * d + cq, obr);
       // queries
@@ -154,32 +210,37 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_kernel(
 #pragma unroll
         for (int c = 0; c < kAttnDh; ++c) A1[c] = A2[c] = 0.f;
         const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
-        float s1 = 0.f;
-        for (int j = 0; j < n; ++j) {
-          const long long key = e0 + j;
-          float k[kAttnDh], v[kAttnDh];
-          ld32(QKV + key * ld + ck, k);
-          ld32(QKV + key * ld + cv, v);
-          const float p = uu[key] * __expf(dot32(q, k) * kAttnScale - M) * iZ;
-          const float w = dot32(obr, v);
-          s1 += p * w;
+        float sw = 0.f;
+        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
+          const int cnt = min(kAttnChunk, n - j0);
+          wave_sync();
+          stage_rows<2>(rows, kvc, ld, e0 + j0, cnt, l);
+          if (l < cnt) s0[l] = uu[e0 + j0 + l];
+          wave_sync();
+          for (int jj = 0; jj < cnt; ++jj) {
+            float k[kAttnDh], v[kAttnDh];
+            ld32(rows + jj * 2 * kAttnDh, k);
+            ld32(rows + jj * 2 * kAttnDh + kAttnDh, v);
+            const float p = s0[jj] * __expf(dot32(q, k) * kAttnScale - M) * iZ;
+            const float w = dot32(obr, v);
+            sw += p * w;
 #pragma unroll
-          for (int c = 0; c < kAttnDh; ++c) {
-            A1[c] += p * w * k[c];
-            A2[c] += p * k[c];
+            for (int c = 0; c < kAttnDh; ++c) {
+              A1[c] += p * w * k[c];
+              A2[c] += p * k[c];
+            }
           }
         }
         const float ue = uu[e] * kAttnScale;
         float qb[kAttnDh];
 #pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) qb[c] = ue * (A1[c] - s1 * A2[c]);
+        for (int c = 0; c < kAttnDh; ++c) qb[c] = ue * (A1[c] - sw * A2[c]);
         if (valid) {
           st32(QKVb + e * ld + cq, qb);
-          cw[q0 + l] = s1;
-          rb[q0 + l] += s1;
+          cw[q0 + l] = sw;
+          rb[q0 + l] += sw;
         }
       }
-      __builtin_amdgcn_wave_barrier();
       // keys
       for (int k0 = 0; k0 < n; k0 += 64) {
         const bool valid = k0 + l < n;
@@ -191,34 +252,43 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_kernel(
 #pragma unroll
         for (int c = 0; c < kAttnDh; ++c) kb[c] = 0.f;
         float Pu = 0.f, kl = 0.f;
-        for (int jq = 0; jq < n; ++jq) {
-          const long long e = e0 + jq;
-          float q[kAttnDh];
-          ld32(QKV + e * ld + cq, q);
-          const float E = __expf(dot32(q, k) * kAttnScale - stats[(e * H + a) * 2]) / stats[(e * H + a) * 2 + 1];
-          const float ue = uu[e];
-          const float t = ue * E * (w - cw[jq]);
-          kl += t;
-          Pu += ue * uk * E;
+        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
+          const int cnt = min(kAttnChunk, n - j0);
+          wave_sync();
+          stage_rows<1>(rows, qc, ld, e0 + j0, cnt, l);
+          if (l < cnt) {
+            const long long e = e0 + j0 + l;
+            s0[l] = stats[(e * H + a) * 2];
+            s1v[l] = 1.f / stats[(e * H + a) * 2 + 1];
+            s2[l] = uu[e];
+          }
+          wave_sync();
+          for (int jj = 0; jj < cnt; ++jj) {
+            float q[kAttnDh];
+            ld32(rows + jj * kAttnDh, q);
+            const float E = __expf(dot32(q, k) * kAttnScale - s0[jj]) * s1v[jj];
+            const float ue = s2[jj];
+            const float t = ue * E * (w - cw[j0 + jj]);
+            kl += t;
+            Pu += ue * uk * E;
 #pragma unroll
-          for (int c = 0; c < kAttnDh; ++c) kb[c] += uk * t * q[c];
+            for (int c = 0; c < kAttnDh; ++c) kb[c] += uk * t * q[c];
+          }
         }
-        float vb[kAttnDh];
 #pragma unroll
         for (int c = 0; c < kAttnDh; ++c) {
           kb[c] *= kAttnScale;
-          vb[c] = Pu * obr[c];
+          v[c] = Pu * obr[c];
         }
         if (valid) {
           st32(QKVb + key * ld + ck, kb);
-          st32(QKVb + key * ld + cv, vb);
+          st32(QKVb + key * ld + cv, v);
           rb[k0 + l] += kl;
         }
       }
-      __builtin_amdgcn_wave_barrier();
     }
+    wave_sync();
     for (int j = l; j < n; j += 64) rbar[e0 + j] += ud[e0 + j] * rb[j];
-    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -231,11 +301,18 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
     const float* __restrict__ stats, int N, int d, int H, float* __restrict__ osumh) {
+  __shared__ float s_rows[kAttnWaves][kAttnChunk * 4 * kAttnDh];
+  __shared__ float s_sc[kAttnWaves][2][kAttnChunk];
+  const int wv = threadIdx.x >> 6;
+  float* rows = s_rows[wv];
+  float* su = s_sc[wv][0];
+  float* sh = s_sc[wv][1];
   const long long ld = 3LL * d;
   JANUS_WAVE_LOOP(i, N) {
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
     for (int a = 0; a < H; ++a) {
       const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      const AttnCols cols{{QKV + ck, QKVh + ck, QKV + cv, QKVh + cv}};
       float acc[kAttnDh];
 #pragma unroll
       for (int c = 0; c < kAttnDh; ++c) acc[c] = 0.f;
@@ -249,26 +326,36 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_kernel(
         for (int c = 0; c < kAttnDh; ++c) A1[c] = A2[c] = A3[c] = 0.f;
         const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
         float s1 = 0.f;
-        for (int j = 0; j < n; ++j) {
-          const long long key = e0 + j;
-          float k[kAttnDh], v[kAttnDh];
-          ld32(QKV + key * ld + ck, k);
-          float sh = dot32(qh, k);
-          const float E = __expf(dot32(q, k) * kAttnScale - M) * iZ;
-          ld32(QKVh + key * ld + ck, k);
-          sh = (sh + dot32(q, k)) * kAttnScale;
-          const float p = uu[key] * E;
-          const float pz = p * sh + ud[key] * rt[key] * E;
-          s1 += pz;
-          ld32(QKV + key * ld + cv, v);
-#pragma unroll
-          for (int c = 0; c < kAttnDh; ++c) {
-            A1[c] += pz * v[c];
-            A2[c] += p * v[c];
+        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
+          const int cnt = min(kAttnChunk, n - j0);
+          wave_sync();
+          stage_rows<4>(rows, cols, ld, e0 + j0, cnt, l);
+          if (l < cnt) {
+            su[l] = uu[e0 + j0 + l];
+            sh[l] = ud[e0 + j0 + l] * rt[e0 + j0 + l];
           }
-          ld32(QKVh + key * ld + cv, v);
+          wave_sync();
+          for (int jj = 0; jj < cnt; ++jj) {
+            const float* r = rows + jj * 4 * kAttnDh;
+            float x[kAttnDh];
+            ld32(r, x);                                   // k
+            float shv = dot32(qh, x);
+            const float E = __expf(dot32(q, x) * kAttnScale - M) * iZ;
+            ld32(r + kAttnDh, x);                         // kh
+            shv = (shv + dot32(q, x)) * kAttnScale;
+            const float p = su[jj] * E;
+            const float pz = p * shv + sh[jj] * E;
+            s1 += pz;
+            ld32(r + 2 * kAttnDh, x);                     // v
 #pragma unroll
-          for (int c = 0; c < kAttnDh; ++c) A3[c] += p * v[c];
+            for (int c = 0; c < kAttnDh; ++c) {
+              A1[c] += pz * x[c];
+              A2[c] += p * x[c];
+            }
+            ld32(r + 3 * kAttnDh, x);                     // vh
+#pragma unroll
+            for (int c = 0; c < kAttnDh; ++c) A3[c] += p * x[c];
+          }
         }
         const float ue = valid ? uu[e] : 0.f, uh = valid ? ud[e] * rt[e] : 0.f;
 #pragma unroll
@@ -294,19 +381,28 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
     const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
     int H, float* __restrict__ QKVa) {
-  __shared__ float s_sc[kAttnWaves][7][kAttnMaxN];
+  __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
+  __shared__ float s_ch[kAttnWaves][4][kAttnChunk];
+  __shared__ float s_sc[kAttnWaves][6][kAttnMaxN];
   const int wv = threadIdx.x >> 6;
+  float* rows = s_rows[wv];
+  float* c0 = s_ch[wv][0];
+  float* c1 = s_ch[wv][1];
+  float* c2 = s_ch[wv][2];
+  float* c3 = s_ch[wv][3];
   float* sa = s_sc[wv][0];
   float* sb = s_sc[wv][1];
-  float* am_ = s_sc[wv][2];
-  float* bm_ = s_sc[wv][3];
-  float* zm_ = s_sc[wv][4];
-  float* sp_ = s_sc[wv][5];
+  float* bm_ = s_sc[wv][2];
+  float* zm_ = s_sc[wv][3];
+  float* sp_ = s_sc[wv][4];
   const long long ld = 3LL * d;
   JANUS_WAVE_LOOP(i, N) {
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
     for (int a = 0; a < H; ++a) {
       const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      const AttnCols kc{{QKV + ck, QKVh + ck, nullptr, nullptr}};
+      const AttnCols qc{{QKV + cq, QKVh + cq, nullptr, nullptr}};
+      wave_sync();
       // per key: a_l, b_l
       for (int k0 = 0; k0 < n; k0 += 64) {
         const bool valid = k0 + l < n;
@@ -326,7 +422,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
           sb[k0 + l] = bj;
         }
       }
-      __builtin_amdgcn_wave_barrier();
       // queries, sweep 1: per-query sums
       for (int q0 = 0; q0 < n; q0 += 64) {
         const bool valid = q0 + l < n;
@@ -336,30 +431,38 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
         ld32(QKVh + e * ld + cq, qh);
         const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
         float am = 0.f, bm = 0.f, zm = 0.f, pbz = 0.f;
-        for (int j = 0; j < n; ++j) {
-          const long long key = e0 + j;
-          float k[kAttnDh], kh[kAttnDh];
-          ld32(QKV + key * ld + ck, k);
-          ld32(QKVh + key * ld + ck, kh);
-          const float E = __expf(dot32(q, k) * kAttnScale - M) * iZ;
-          const float sh = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
-          const float p = uu[key] * E;
-          const float pz = p * sh + ud[key] * rt[key] * E;
-          const float aj = sa[j], bj = sb[j];
-          am += p * aj;
-          bm += p * bj;
-          zm += pz;
-          pbz += pz * bj;
+        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
+          const int cnt = min(kAttnChunk, n - j0);
+          wave_sync();
+          stage_rows<2>(rows, kc, ld, e0 + j0, cnt, l);
+          if (l < cnt) {
+            c0[l] = uu[e0 + j0 + l];
+            c1[l] = ud[e0 + j0 + l] * rt[e0 + j0 + l];
+          }
+          wave_sync();
+          for (int jj = 0; jj < cnt; ++jj) {
+            float x[kAttnDh];
+            ld32(rows + jj * 2 * kAttnDh, x);
+            float shv = dot32(qh, x);
+            const float E = __expf(dot32(q, x) * kAttnScale - M) * iZ;
+            ld32(rows + jj * 2 * kAttnDh + kAttnDh, x);
+            shv = (shv + dot32(q, x)) * kAttnScale;
+            const float p = c0[jj] * E;
+            const float pz = p * shv + c1[jj] * E;
+            const float aj = sa[j0 + jj], bj = sb[j0 + jj];
+            am += p * aj;
+            bm += p * bj;
+            zm += pz;
+            pbz += pz * bj;
+          }
         }
         const float ue = uu[e], uh = ud[e] * rt[e];
         if (valid) {
-          am_[q0 + l] = am;
           bm_[q0 + l] = bm;
           zm_[q0 + l] = zm;
           sp_[q0 + l] = ue * (am + pbz - 2.f * zm * bm) + uh * bm;
         }
       }
-      __builtin_amdgcn_wave_barrier();
       // queries, sweep 2: qb
       for (int q0 = 0; q0 < n; q0 += 64) {
         const bool valid = q0 + l < n;
@@ -372,21 +475,31 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
         for (int c = 0; c < kAttnDh; ++c) qb[c] = 0.f;
         const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
         const float ue = uu[e], uh = ud[e] * rt[e];
+        wave_sync();
         const float bm = bm_[jq], zm = zm_[jq], SP = sp_[jq];
-        for (int j = 0; j < n; ++j) {
-          const long long key = e0 + j;
-          float k[kAttnDh], kh[kAttnDh];
-          ld32(QKV + key * ld + ck, k);
-          ld32(QKVh + key * ld + ck, kh);
-          const float E = __expf(dot32(q, k) * kAttnScale - M) * iZ;
-          const float sh = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
-          const float p = uu[key] * E;
-          const float pz = p * sh + ud[key] * rt[key] * E;
-          const float aj = sa[j], bj = sb[j];
-          const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
-          const float zhb = ue * p * (bj - bm);
+        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
+          const int cnt = min(kAttnChunk, n - j0);
+          wave_sync();
+          stage_rows<2>(rows, kc, ld, e0 + j0, cnt, l);
+          if (l < cnt) {
+            c0[l] = uu[e0 + j0 + l];
+            c1[l] = ud[e0 + j0 + l] * rt[e0 + j0 + l];
+          }
+          wave_sync();
+          for (int jj = 0; jj < cnt; ++jj) {
+            float k[kAttnDh], kh[kAttnDh];
+            ld32(rows + jj * 2 * kAttnDh, k);
+            ld32(rows + jj * 2 * kAttnDh + kAttnDh, kh);
+            const float E = __expf(dot32(q, k) * kAttnScale - M) * iZ;
+            const float shv = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
+            const float p = c0[jj] * E;
+            const float pz = p * shv + c1[jj] * E;
+            const float aj = sa[j0 + jj], bj = sb[j0 + jj];
+            const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
+            const float zhb = ue * p * (bj - bm);
 #pragma unroll
-          for (int c = 0; c < kAttnDh; ++c) qb[c] += zb * k[c] + zhb * kh[c];
+            for (int c = 0; c < kAttnDh; ++c) qb[c] += zb * k[c] + zhb * kh[c];
+          }
         }
 #pragma unroll
         for (int c = 0; c < kAttnDh; ++c) qb[c] *= kAttnScale;
@@ -404,23 +517,36 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
         for (int c = 0; c < kAttnDh; ++c) kb[c] = 0.f;
         const float uk = uu[key], uhk = ud[key] * rt[key], aj = sa[jk], bj = sb[jk];
         float S1 = 0.f, S2 = 0.f;
-        for (int jq = 0; jq < n; ++jq) {
-          const long long e = e0 + jq;
-          float q[kAttnDh], qh[kAttnDh];
-          ld32(QKV + e * ld + cq, q);
-          ld32(QKVh + e * ld + cq, qh);
-          const float E = __expf(dot32(q, k) * kAttnScale - stats[(e * H + a) * 2]) / stats[(e * H + a) * 2 + 1];
-          const float sh = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
-          const float p = uk * E;
-          const float pz = p * sh + uhk * E;
-          const float ue = uu[e], uh = ud[e] * rt[e];
-          const float bm = bm_[jq], zm = zm_[jq], SP = sp_[jq];
-          const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
-          const float zhb = ue * p * (bj - bm);
-          S1 += ue * p;
-          S2 += uh * p + ue * (pz - p * zm);
+        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
+          const int cnt = min(kAttnChunk, n - j0);
+          wave_sync();
+          stage_rows<2>(rows, qc, ld, e0 + j0, cnt, l);
+          if (l < cnt) {
+            const long long e = e0 + j0 + l;
+            c0[l] = stats[(e * H + a) * 2];
+            c1[l] = 1.f / stats[(e * H + a) * 2 + 1];
+            c2[l] = uu[e];
+            c3[l] = ud[e] * rt[e];
+          }
+          wave_sync();
+          for (int jj = 0; jj < cnt; ++jj) {
+            float q[kAttnDh], qh[kAttnDh];
+            ld32(rows + jj * 2 * kAttnDh, q);
+            ld32(rows + jj * 2 * kAttnDh + kAttnDh, qh);
+            const float E = __expf(dot32(q, k) * kAttnScale - c0[jj]) * c1[jj];
+            const float shv = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
+            const float p = uk * E;
+            const float pz = p * shv + uhk * E;
+            const float ue = c2[jj], uh = c3[jj];
+            const int jq = j0 + jj;
+            const float bm = bm_[jq], zm = zm_[jq], SP = sp_[jq];
+            const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
+            const float zhb = ue * p * (bj - bm);
+            S1 += ue * p;
+            S2 += uh * p + ue * (pz - p * zm);
 #pragma unroll
-          for (int c = 0; c < kAttnDh; ++c) kb[c] += zb * q[c] + zhb * qh[c];
+            for (int c = 0; c < kAttnDh; ++c) kb[c] += zb * q[c] + zhb * qh[c];
+          }
         }
 #pragma unroll
         for (int c = 0; c < kAttnDh; ++c) kb[c] *= kAttnScale;
@@ -432,7 +558,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
         for (int c = 0; c < kAttnDh; ++c) kb[c] = S1 * al[c] + S2 * be[c];
         if (valid) st32(QKVa + key * ld + cv, kb);
       }
-      __builtin_amdgcn_wave_barrier();
     }
   }
 }
