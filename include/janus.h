@@ -85,6 +85,10 @@ enum {
  *   n_heads    0, or the number of heads of the self-attention over every
  *              atom's edge messages (paper Sec. "Multi-head self-attention");
  *              must divide d
+ *   n_tasks    0, or the number of tasks of the task-aware embedding (paper
+ *              Sec. "Task-aware feature embedding"); then n_charges and
+ *              n_spins (>= 1) size the charge and spin tables, and every
+ *              structure's labels select rows of them (janus_step_ex)
  */
 typedef struct janus_config {
   int32_t n_species;
@@ -110,6 +114,9 @@ typedef struct janus_config {
   int32_t d_hidden_f;
   float w_S;
   int32_t n_heads;
+  int32_t n_tasks;
+  int32_t n_charges;
+  int32_t n_spins;
 } janus_config;
 
 typedef struct janus_ctx janus_ctx;
@@ -185,7 +192,9 @@ int janus_create(const janus_config* cfg /* host */, janus_ctx** out /* host */)
  * have synchronised every stream the context was used on. */
 void janus_destroy(janus_ctx* ctx);
 
-/* Layout of the flat weight blob for `cfg`.  Order: A [n_species, d]; for
+/* Layout of the flat weight blob for `cfg`.  Order: A [n_species, d], with the
+ * task-aware embedding Tk [n_tasks, d], Qe [n_charges, d], Se [n_spins, d],
+ * Wc [n_species, d]; for
  * each block t: W_b [n_rbf, d], Pc [n_species, E], Pn [n_species, E],
  * beta [E], W1 [E, d, d_hidden], W2 [E, d_hidden, d], and with the
  * three-body term W_a [n_legendre*n_rbf, d], P3a, P3b, P3c [n_species, E3],

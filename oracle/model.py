@@ -37,6 +37,13 @@ update becomes
     h^{t+1}_i = u_i + sum_c gf_ic W2f_x^T SiLU(W1f_x^T u_i),  x = Kf_i[c]
 with the same gating rule as the edge MoE; betaf is fixed like beta.
 
+With the task-aware embedding (paper Sec. "Task-aware feature embedding": a
+task (dataset) embedding, charge and spin embeddings and a global embedding
+of the element composition) every structure s adds one vector to the
+embedding of its atoms:
+    h^0_i = A[Z_i] + Tk[task_s] + Qe[charge_s] + Se[spin_s] + c_s Wc,
+with c_s the element fractions of s (labels are per-structure indices).
+
 With multi-head self-attention (paper Sec. "Multi-head self-attention",
 ``attention.py``) the messages of the edges of atom i attend to each other
 before they reach the atom:
@@ -97,13 +104,15 @@ class Params:
     Ef: int = 0
     heads: int = 0
     r_cut: float = 0.0
+    task: bool = False
 
     @classmethod
     def from_weights(cls, weights, model):
         w = {n: np.asarray(v, np.float64) for n, v in weights.items()}
         return cls(w=w, T=model.n_blocks, k=model.top_k, E=model.n_experts, three=bool(model.three_body),
                    k3=model.top_k3, E3=model.n_experts3, atom=bool(model.atom_moe),
-                   kf=model.top_k_f, Ef=model.n_experts_f, heads=model.n_heads, r_cut=model.r_cut)
+                   kf=model.top_k_f, Ef=model.n_experts_f, heads=model.n_heads, r_cut=model.r_cut,
+                   task=model.n_tasks > 0)
 
     def blk(self, t, name):
         return self.w[f"blocks.{t}.{name}"]
@@ -125,6 +134,7 @@ class Graph:
     struct_of_atom: np.ndarray
     n_atoms_struct: np.ndarray
     tri: object = None  # threebody.Triplets when the model has the angular term
+    labels: object = None  # (task, charge, spin) per structure for the task-aware embedding
 
 
 def edge_geometry(pos, cell, offsets, ei, ej, shift):
@@ -142,10 +152,11 @@ def edge_geometry(pos, cell, offsets, ei, ej, shift):
     return d, r, d / r[:, None], sid
 
 
-def build_graph(batch_pos, cell, offsets, r_cut, n_rbf, edges=None, three=None):
+def build_graph(batch_pos, cell, offsets, r_cut, n_rbf, edges=None, three=None, labels=None):
     """Neighbour list (unless given as (ei, ej, shift, rowptr)) plus geometry and basis.
 
-    three = (r_cut3, n_legendre) adds the bond triplets and their features.
+    three = (r_cut3, n_legendre) adds the bond triplets and their features;
+    labels = (task, charge, spin) per structure feed the task-aware embedding.
     """
     if edges is None:
         edges = neighbor_list(batch_pos, cell, offsets, r_cut)
@@ -159,13 +170,34 @@ def build_graph(batch_pos, cell, offsets, r_cut, n_rbf, edges=None, three=None):
         te, te2, trp = triplet_list(ei, ej, shift, batch_pos, cell, offsets, rowptr, r3)
         tri = tb.triplet_features(te, te2, trp, r, u, r3, n_rbf, n_l)
     return Graph(ei=ei, ej=ej, shift=shift, rowptr=rowptr, d=d, r=r, u=u, B=B, dB=dB,
-                 struct_of_atom=sid, n_atoms_struct=nst, tri=tri)
+                 struct_of_atom=sid, n_atoms_struct=nst, tri=tri, labels=labels)
 
 
 def build_graph_for(batch, edges=None):
     m = batch.model
     three = (m.r_cut3, m.n_legendre) if m.three_body else None
-    return build_graph(batch.pos, batch.cell, batch.offsets, m.r_cut, m.n_rbf, edges, three)
+    labels = (batch.task, batch.charge, batch.spin) if m.n_tasks else None
+    return build_graph(batch.pos, batch.cell, batch.offsets, m.r_cut, m.n_rbf, edges, three, labels)
+
+
+def composition(species, g: Graph, n_species):
+    """c_s: fraction of the atoms of structure s of each element [S, n_species]."""
+    S = g.n_atoms_struct.size
+    counts = np.zeros((S, n_species))
+    np.add.at(counts, (g.struct_of_atom, species), 1.0)
+    return counts / np.maximum(g.n_atoms_struct, 1)[:, None]
+
+
+def embed(species, g: Graph, P):
+    """h^0: the species embedding, plus the per-structure task, charge, spin and
+    composition embeddings when the model has them."""
+    h = P.w["A"][species]
+    if P.task:
+        task, charge, spin = g.labels
+        c = composition(species, g, P.w["A"].shape[0])
+        gs = P.w["Tk"][task] + P.w["Qe"][charge] + P.w["Se"][spin] + c @ P.w["Wc"]
+        h = h + gs[g.struct_of_atom]
+    return h
 
 
 # --------------------------------------------------------------------------- routing
@@ -403,7 +435,7 @@ def forward_energy(species, g: Graph, P: Params, routing):
     the message-updated features u^t of every block."""
     N = species.shape[0]
     Ne = g.ei.shape[0]
-    h = P.w["A"][species]
+    h = embed(species, g, P)
     hs, us = [h], []
     for t in range(P.T):
         F = g.B @ P.blk(t, "W_b")
@@ -576,7 +608,7 @@ def energy_tangent(species, g: Graph, P: Params, routing, phi, Psi=None):
     rdot = (ddot * g.u).sum(1)                                         # dr_e/de
     Bdot = g.dB * rdot[:, None]
     Gd = tb.feature_tangent(g.tri, g.r, g.u, ddot) if g.tri is not None else None
-    h = P.w["A"][species]
+    h = embed(species, g, P)
     hd = np.zeros_like(h)
     hs, hds, us, uds = [h], [hd], [], []
     for t in range(P.T):
@@ -715,6 +747,14 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
             grad[f"blocks.{t}.P3c"] = _seg(species[j2], S_, Pl3)
         Ph, Th = Ph_new, Th_new
     grad["A"] = _seg(species, P.w["A"].shape[0], Ph)
+    if P.task:
+        # h0 gains one vector per structure: its adjoint is the sum over the atoms
+        task, charge, spin = g.labels
+        Pg = _seg(g.struct_of_atom, g.n_atoms_struct.size, Ph)
+        grad["Tk"] = _seg(task, P.w["Tk"].shape[0], Pg)
+        grad["Qe"] = _seg(charge, P.w["Qe"].shape[0], Pg)
+        grad["Se"] = _seg(spin, P.w["Se"].shape[0], Pg)
+        grad["Wc"] = composition(species, g, P.w["A"].shape[0]).T @ Pg
     return grad
 
 

@@ -485,6 +485,12 @@ Layout make_layout(const janus_config& c) {
   Layout L;
   const long long S = c.n_species, d = c.d, E = c.n_experts, h = c.d_hidden, nb = c.n_rbf;
   L.add("A", {S, d});
+  if (c.n_tasks) {
+    L.add("Tk", {(long long)c.n_tasks, d});
+    L.add("Qe", {(long long)c.n_charges, d});
+    L.add("Se", {(long long)c.n_spins, d});
+    L.add("Wc", {S, d});
+  }
   for (int t = 0; t < c.n_blocks; ++t) {
     const std::string p = "blocks." + std::to_string(t) + ".";
     L.add(p + "W_b", {nb, d});
@@ -539,6 +545,9 @@ int check_config(const janus_config* c) {
   }
   if (!(c->w_S >= 0.f)) return JANUS_EINVAL;
   if (c->n_heads < 0 || (c->n_heads && c->d % c->n_heads)) return JANUS_EINVAL;
+  if (c->n_tasks < 0 || (c->n_tasks && (c->n_charges < 1 || c->n_spins < 1))) return JANUS_EINVAL;
+  // the step does not run the task-aware embedding yet
+  if (c->n_tasks) return JANUS_EUNSUPPORTED;
   // heads of 32 columns
   if (c->n_heads && c->d / c->n_heads != kAttnDh) return JANUS_EUNSUPPORTED;
   if (c->atom_moe) {

@@ -39,6 +39,9 @@ class ModelConfig:
     w_E, w_F, w_S weigh the energy, force and stress terms of the loss (stress
     in eV/A^3; w_S = 0 leaves it out).  n_heads > 0 adds multi-head
     self-attention over every atom's edge messages (head width d / n_heads).
+    n_tasks > 0 adds the task-aware embedding: per-structure task, charge and
+    spin labels (indices below n_tasks, n_charges, n_spins) and the element
+    composition each add a vector to the atom embedding.
     """
 
     d: int
@@ -64,6 +67,9 @@ class ModelConfig:
     d_hidden_f: int = 0
     w_S: float = 0.0
     n_heads: int = 0
+    n_tasks: int = 0
+    n_charges: int = 0
+    n_spins: int = 0
 
     def weight_shapes(self):
         """Named weight tensors in blob order, with the fan-in used at init.
@@ -73,6 +79,9 @@ class ModelConfig:
         """
         d, E, h, nb, S = self.d, self.n_experts, self.d_hidden, self.n_rbf, self.n_species
         out = [("A", (S, d), None)]
+        if self.n_tasks:
+            out += [("Tk", (self.n_tasks, d), None), ("Qe", (self.n_charges, d), None),
+                    ("Se", (self.n_spins, d), None), ("Wc", (S, d), None)]
         for t in range(self.n_blocks):
             p = f"blocks.{t}."
             out += [
@@ -150,6 +159,8 @@ _M_ATOM = dataclasses.replace(_M_SMALL, atom_moe=True, n_experts_f=8, top_k_f=2,
 # stress weight 0.1 on stresses measured in GPa (1 eV/A^3 = 160.2177 GPa)
 _M_STRESS = dataclasses.replace(_M_SMALL, w_S=0.1 * 160.2177 ** 2)
 _M_ATTN = dataclasses.replace(_M_SMALL, n_heads=4)
+# task-aware embedding: 4 datasets, total charges -2..2, spin multiplicities 1..4
+_M_TASK = dataclasses.replace(_M_SMALL, n_tasks=4, n_charges=5, n_spins=4)
 _M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
 
 WORKLOADS = {
@@ -159,6 +170,7 @@ WORKLOADS = {
     "atom_moe": Workload("atom_moe", "ortho", 64, 64, 0.08, _M_ATOM),
     "stress": Workload("stress", "ortho", 64, 64, 0.08, _M_STRESS),
     "attention": Workload("attention", "ortho", 64, 64, 0.08, _M_ATTN),
+    "multitask": Workload("multitask", "ortho", 64, 64, 0.08, _M_TASK),
     "shard": Workload("shard", "cubic", 256, 128, 0.1, _M_BIG),
     "irregular": Workload("irregular", "mixed", 512, 0, 0.1, _M_BIG, zipf_s=1.2),
 }
@@ -176,6 +188,9 @@ class Batch:
     F_ref: np.ndarray        # [N, 3]
     weights: dict = field(default_factory=dict)   # name -> float32 array
     S_ref: np.ndarray | None = None   # [S, 3, 3] reference stress (eV/A^3), symmetric
+    task: np.ndarray | None = None    # [S] int32 labels of the task-aware embedding
+    charge: np.ndarray | None = None  # [S] int32 index of the total charge
+    spin: np.ndarray | None = None    # [S] int32 index of the spin multiplicity
     model: ModelConfig | None = None
     name: str = ""
 
@@ -272,6 +287,12 @@ def make_batch(wl: Workload | str, seed: int | None = None, n_struct: int | None
     #    (off-diagonal variance 1 GPa^2, diagonal 2 GPa^2), stored in eV/A^3
     a = rng.standard_normal((S, 3, 3))
     S_ref = ((a + a.transpose(0, 2, 1)) / np.sqrt(2.0) / 160.2177).astype(np.float32)
+    # 8. labels of the task-aware embedding (uniform over each label's range)
+    labels = {}
+    if m.n_tasks:
+        labels = {"task": rng.integers(0, m.n_tasks, S).astype(np.int32),
+                  "charge": rng.integers(0, m.n_charges, S).astype(np.int32),
+                  "spin": rng.integers(0, m.n_spins, S).astype(np.int32)}
 
     cell = np.zeros((S, 3, 3), np.float32)
     for s in range(S):
@@ -279,7 +300,7 @@ def make_batch(wl: Workload | str, seed: int | None = None, n_struct: int | None
     offsets = np.zeros(S + 1, np.int32)
     offsets[1:] = np.cumsum(sizes)
     return Batch(pos=pos, cell=cell, species=species, offsets=offsets, E_ref=E_ref,
-                 F_ref=F_ref, weights=weights, model=m, name=wl.name, S_ref=S_ref)
+                 F_ref=F_ref, weights=weights, model=m, name=wl.name, S_ref=S_ref, **labels)
 
 
 def subset(batch: Batch, structs) -> Batch:
@@ -296,4 +317,6 @@ def subset(batch: Batch, structs) -> Batch:
                  species=np.concatenate(spc, 0), offsets=off, E_ref=batch.E_ref[structs].copy(),
                  F_ref=np.concatenate(fref, 0), weights=batch.weights, model=batch.model,
                  name=batch.name + "[sub]",
-                 S_ref=None if batch.S_ref is None else batch.S_ref[structs].copy())
+                 S_ref=None if batch.S_ref is None else batch.S_ref[structs].copy(),
+                 **{k: None if getattr(batch, k) is None else getattr(batch, k)[structs].copy()
+                    for k in ("task", "charge", "spin")})
