@@ -130,6 +130,8 @@ def main():
            torch.empty_like(d["W"]))
     # with a stress weight the step also returns the stress and trains on it
     stress = dict(S_ref=d["S_ref"], stress=torch.empty(S, 3, 3, device="cuda:0")) if m.w_S else {}
+    if m.n_tasks:
+        stress["labels"] = d["labels"]
 
     def step():
         ne = ctx.build_edges_into(d["pos"], d["cell"], d["offsets"], nl)
@@ -216,7 +218,8 @@ def main():
                    **({"atom_moe": {"experts": m.n_experts_f, "top_k": m.top_k_f, "d_hidden": m.d_hidden_f}}
                       if m.atom_moe else {}),
                    **({"stress_weight": m.w_S} if m.w_S else {}),
-                   **({"attention_heads": m.n_heads} if m.n_heads else {})},
+                   **({"attention_heads": m.n_heads} if m.n_heads else {}),
+                   **({"tasks": m.n_tasks, "charges": m.n_charges, "spins": m.n_spins} if m.n_tasks else {})},
         "edges_per_s": Ne / (ms * 1e-3),
         "triplets": Nt,
         "triplets_per_s": Nt / (ms * 1e-3),

@@ -279,6 +279,35 @@ int janus_step_stress(janus_ctx* ctx, const float* pos, const float* cell, const
                       const janus_debug* dbg, void* stream);
 
 /*
+ * Per-structure labels of the task-aware embedding (paper Sec. "Task-aware
+ * feature embedding": task (dataset), charge and spin embeddings).  Device
+ * arrays of n_struct int32 each: task[s] in [0, n_tasks), charge[s] in
+ * [0, n_charges) (the index of the structure's total charge) and spin[s] in
+ * [0, n_spins) (the index of its spin multiplicity).
+ */
+typedef struct janus_labels {
+  const int32_t* task;
+  const int32_t* charge;
+  const int32_t* spin;
+} janus_labels;
+
+/*
+ * janus_step with stress and the task-aware embedding.  With cfg.n_tasks > 0
+ * every atom's embedding gains
+ *     Tk[task_s] + Qe[charge_s] + Se[spin_s] + c_s Wc
+ * (c_s = the element fractions of its structure s) and dLdW includes the
+ * gradients of the four tables.  labels (host struct of device pointers) is
+ * required then (JANUS_EINVAL otherwise, and for a label out of range) and
+ * ignored otherwise.  Every other argument, output and error is as for
+ * janus_step_stress, which is this call with labels = NULL.
+ */
+int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
+                  const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
+                  const float* W, const float* E_ref, const float* F_ref, const float* S_ref,
+                  const janus_labels* labels, float* loss, float* E, float* F, float* stress,
+                  float* dLdW, const janus_debug* dbg, void* stream);
+
+/*
  * Workspace of janus_step.  Structures are independent apart from the loss
  * normalisation, so janus_step processes the batch in chunks of whole
  * structures, in order, each sized so that its workspace fits `bytes`

@@ -121,8 +121,9 @@ __global__ void copy_add_kernel(int* __restrict__ dst, const int* __restrict__ s
 
 int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const ChunkArgs& ca, const float* pos_g,
               const float* cell_g, const int32_t* species_g, const int32_t* offsets_g, const janus_edges* nl,
-              const float* W, const float* E_ref_g, const float* F_ref_g, const float* S_ref_g, double* loss_part,
-              float* E_g, float* F_g, float* stress_g, float* dLdW, const janus_debug* dbg) {
+              const float* W, const float* E_ref_g, const float* F_ref_g, const float* S_ref_g,
+              const janus_labels* labels, double* loss_part, float* E_g, float* F_g, float* stress_g, float* dLdW,
+              const janus_debug* dbg) {
   const janus_config& cfg = ctx->cfg;
   const int T = p.T, Ee = p.E, k = p.k, d = p.d, h = p.hdim, nb = p.nb, nsp = p.nsp;
   const int N = ca.N, S = ca.S;
@@ -360,6 +361,13 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   {
     PROF(PROF_OTHER, 0, 8.0 * Nd);
     hipLaunchKernelGGL(species_rows_gather_kernel, dim3(cdiv(Nd, 256)), b256, 0, st, Wp("A"), species, N, d, p.h);
+    if (cfg.n_tasks) {
+      // h0 += task, charge, spin and composition embedding of the atom's structure
+      LAUNCH_VPL(struct_embed_kernel, d, wave_grid(S), b256, 0, st, labels->task + ca.s0, labels->charge + ca.s0,
+                 labels->spin + ca.s0, offsets, species, Wp("Tk"), Wp("Qe"), Wp("Se"), Wp("Wc"), S, d, p.gs);
+      hipLaunchKernelGGL(add_struct_rows_kernel, dim3(cdiv(Nd, 256)), b256, 0, st, (const float*)p.gs,
+                         (const int*)p.sid, N, d, p.h);
+    }
   }
   for (int t = 0; t < T; ++t) {
     const float* Wb = Wp(blk(t, "W_b"));
@@ -1003,6 +1011,18 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     PROF(PROF_OTHER, 0, 8.0 * Nd);
     hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(256), 0, st, (const int*)p.sp_off,
                        (const int*)p.sp_atoms, (const float*)HV(p.hh, 0), d, nsp, Gp("A"));
+    if (cfg.n_tasks) {
+      // per-structure sums of dL/dh0, then per label value and per species (composition)
+      LAUNCH_VPL(struct_sum_kernel, d, wave_grid(S), b256, 0, st, offsets, (const float*)HV(p.hh, 0), S, d, p.gsb);
+      hipLaunchKernelGGL(label_rows_kernel, dim3(cfg.n_tasks), b256, 0, st, labels->task + ca.s0, S,
+                         (const float*)p.gsb, d, Gp("Tk"));
+      hipLaunchKernelGGL(label_rows_kernel, dim3(cfg.n_charges), b256, 0, st, labels->charge + ca.s0, S,
+                         (const float*)p.gsb, d, Gp("Qe"));
+      hipLaunchKernelGGL(label_rows_kernel, dim3(cfg.n_spins), b256, 0, st, labels->spin + ca.s0, S,
+                         (const float*)p.gsb, d, Gp("Se"));
+      hipLaunchKernelGGL(comp_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off, (const int*)p.sp_atoms,
+                         (const int*)p.sid, offsets, (const float*)p.gsb, d, nsp, Gp("Wc"));
+    }
   }
   JANUS_HIP_TRY(hipGetLastError());
 
@@ -1064,8 +1084,8 @@ extern "C" int janus_step(janus_ctx* ctx, const float* pos, const float* cell, c
                           const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
                           const float* W, const float* E_ref, const float* F_ref, float* loss, float* E, float* F,
                           float* dLdW, const janus_debug* dbg, void* stream) {
-  return janus_step_stress(ctx, pos, cell, species, offsets, n_atoms, n_struct, nl, W, E_ref, F_ref, nullptr, loss,
-                           E, F, nullptr, dLdW, dbg, stream);
+  return janus_step_ex(ctx, pos, cell, species, offsets, n_atoms, n_struct, nl, W, E_ref, F_ref, nullptr, nullptr,
+                       loss, E, F, nullptr, dLdW, dbg, stream);
 }
 
 extern "C" int janus_step_stress(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
@@ -1073,9 +1093,20 @@ extern "C" int janus_step_stress(janus_ctx* ctx, const float* pos, const float* 
                                  const float* W, const float* E_ref, const float* F_ref, const float* S_ref,
                                  float* loss, float* E, float* F, float* stress, float* dLdW, const janus_debug* dbg,
                                  void* stream) {
+  return janus_step_ex(ctx, pos, cell, species, offsets, n_atoms, n_struct, nl, W, E_ref, F_ref, S_ref, nullptr,
+                       loss, E, F, stress, dLdW, dbg, stream);
+}
+
+extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
+                             const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
+                             const float* W, const float* E_ref, const float* F_ref, const float* S_ref,
+                             const janus_labels* labels, float* loss, float* E, float* F, float* stress, float* dLdW,
+                             const janus_debug* dbg, void* stream) {
   if (!ctx || !pos || !cell || !species || !offsets || !nl || !W || !E_ref || !F_ref || !loss || !E || !F ||
       !dLdW || n_atoms < 1 || n_struct < 1 || n_struct > n_atoms)
     return JANUS_EINVAL;
+  // the task-aware embedding needs every structure's labels
+  if (ctx->cfg.n_tasks && (!labels || !labels->task || !labels->charge || !labels->spin)) return JANUS_EINVAL;
   // the stress term of the loss needs its reference; without the term no reference is read
   if (ctx->cfg.w_S != 0.f && !S_ref) return JANUS_EINVAL;
   if (ctx->cfg.w_S == 0.f) S_ref = nullptr;
@@ -1129,6 +1160,9 @@ extern "C" int janus_step_stress(janus_ctx* ctx, const float* pos, const float* 
                        sedge);
     if (cfg.n_heads)
       hipLaunchKernelGGL(attn_degree_check_kernel, dim3(cdiv(N, 256)), dim3(256), 0, st, nl->rowptr, N, flag);
+    if (cfg.n_tasks)
+      hipLaunchKernelGGL(validate_labels_kernel, dim3(cdiv(S, 256)), dim3(256), 0, st, labels->task, labels->charge,
+                         labels->spin, S, cfg.n_tasks, cfg.n_charges, cfg.n_spins, flag);
   }
   JANUS_HIP_TRY(hipGetLastError());
   int* hp = ctx->host_plan;
@@ -1220,8 +1254,8 @@ extern "C" int janus_step_stress(janus_ctx* ctx, const float* pos, const float* 
   for (const ChunkArgs& ca : chunks) {
     Plan p;
     plan_layout(p, ctx->ws.ptr, cfg, ca.N, ca.S, ca.Ne, ca.Nt);
-    rc = run_chunk(ctx, st, p, L, ca, pos, cell, species, offsets, nl, W, E_ref, F_ref, S_ref, loss_part + ca.index,
-                   E, F, stress, dLdW, dbg);
+    rc = run_chunk(ctx, st, p, L, ca, pos, cell, species, offsets, nl, W, E_ref, F_ref, S_ref, labels,
+                   loss_part + ca.index, E, F, stress, dLdW, dbg);
     if (rc) return rc;
   }
   hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1), 0, st, (const double*)loss_part, (int)chunks.size(), loss);

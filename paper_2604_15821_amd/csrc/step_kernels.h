@@ -432,6 +432,102 @@ __global__ void species_write_kernel(const int* __restrict__ species, int N, con
     }                                                                                  \
   } while (0)
 
+// Task-aware embedding (paper Sec. "Task-aware feature embedding"), one wave per
+// structure s of the chunk:
+//   g_s = Tk[task_s] + Qe[charge_s] + Se[spin_s] + (1/n_s) sum_{i in s} Wc[Z_i]
+// (the last term is the element fractions times Wc), summed in atom order.
+template <int VPL>
+__global__ void struct_embed_kernel(const int* __restrict__ task, const int* __restrict__ charge,
+                                    const int* __restrict__ spin, const int* __restrict__ offsets,
+                                    const int* __restrict__ species, const float* __restrict__ Tk,
+                                    const float* __restrict__ Qe, const float* __restrict__ Se,
+                                    const float* __restrict__ Wc, int S, int d, float* __restrict__ g) {
+  JANUS_WAVE_LOOP(s, S) {
+    float c[VPL], acc[VPL];
+    zero_row<VPL>(c);
+    const int a0 = offsets[s], a1 = offsets[s + 1];
+    for (int i = a0; i < a1; ++i) {
+      float w[VPL];
+      ld_row<VPL>(Wc + (long long)species[i] * d, l, w);
+      add_row<VPL>(c, w);
+    }
+    const float inv = a1 > a0 ? 1.f / (float)(a1 - a0) : 0.f;
+    ld_row<VPL>(Tk + (long long)task[s] * d, l, acc);
+    float w[VPL];
+    ld_row<VPL>(Qe + (long long)charge[s] * d, l, w);
+    add_row<VPL>(acc, w);
+    ld_row<VPL>(Se + (long long)spin[s] * d, l, w);
+    add_row<VPL>(acc, w);
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) acc[v] += c[v] * inv;
+    st_row<VPL>(g + s * d, l, acc);
+  }
+}
+
+// h0_i += g_s(i)
+__global__ void add_struct_rows_kernel(const float* __restrict__ g, const int* __restrict__ sid, int N, int d,
+                                       float* __restrict__ h) {
+  const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= (long long)N * d) return;
+  const long long i = q / d;
+  h[q] += g[(long long)sid[i] * d + (q - i * d)];
+}
+
+// gbar_s = sum over the atoms of s (in order) of hbar_i, one wave per structure.
+template <int VPL>
+__global__ void struct_sum_kernel(const int* __restrict__ offsets, const float* __restrict__ hbar, int S, int d,
+                                  float* __restrict__ gbar) {
+  JANUS_WAVE_LOOP(s, S) {
+    float acc[VPL];
+    zero_row<VPL>(acc);
+    for (int i = offsets[s]; i < offsets[s + 1]; ++i) {
+      float x[VPL];
+      ld_row<VPL>(hbar + (long long)i * d, l, x);
+      add_row<VPL>(acc, x);
+    }
+    st_row<VPL>(gbar + s * d, l, acc);
+  }
+}
+
+// out[t] += sum over the structures s with label[s] == t (in order) of gbar_s;
+// one workgroup per label value.
+__global__ void label_rows_kernel(const int* __restrict__ label, int S, const float* __restrict__ gbar, int d,
+                                  float* __restrict__ out) {
+  const int t = blockIdx.x;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    float acc = 0.f;
+    for (int s = 0; s < S; ++s)
+      if (label[s] == t) acc += gbar[(long long)s * d + c];
+    out[(long long)t * d + c] += acc;
+  }
+}
+
+// dWc[z] += sum over the atoms i of species z (in atom order) of gbar_s(i) / n_s(i).
+__global__ void comp_rows_kernel(const int* __restrict__ sp_off, const int* __restrict__ sp_atoms,
+                                 const int* __restrict__ sid, const int* __restrict__ offsets,
+                                 const float* __restrict__ gbar, int d, int nsp, float* __restrict__ out) {
+  const int z = blockIdx.x;
+  if (z >= nsp) return;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    float acc = 0.f;
+    for (int q = sp_off[z]; q < sp_off[z + 1]; ++q) {
+      const int i = sp_atoms[q], s = sid[i];
+      acc += gbar[(long long)s * d + c] / (float)(offsets[s + 1] - offsets[s]);
+    }
+    out[(long long)z * d + c] += acc;
+  }
+}
+
+// flag[0] = 1 when a structure's label is out of its table's range.
+__global__ void validate_labels_kernel(const int* __restrict__ task, const int* __restrict__ charge,
+                                       const int* __restrict__ spin, int S, int nt, int nc, int ns,
+                                       int* __restrict__ flag) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= S) return;
+  if (task[s] < 0 || task[s] >= nt || charge[s] < 0 || charge[s] >= nc || spin[s] < 0 || spin[s] >= ns)
+    atomicOr(flag, 1);
+}
+
 // h0_i = A[Z_i]
 __global__ void species_rows_gather_kernel(const float* __restrict__ A, const int* __restrict__ species, int N, int d,
                                            float* __restrict__ h) {
@@ -546,8 +642,7 @@ int check_config(const janus_config* c) {
   if (!(c->w_S >= 0.f)) return JANUS_EINVAL;
   if (c->n_heads < 0 || (c->n_heads && c->d % c->n_heads)) return JANUS_EINVAL;
   if (c->n_tasks < 0 || (c->n_tasks && (c->n_charges < 1 || c->n_spins < 1))) return JANUS_EINVAL;
-  // the step does not run the task-aware embedding yet
-  if (c->n_tasks) return JANUS_EUNSUPPORTED;
+
   // heads of 32 columns
   if (c->n_heads && c->d / c->n_heads != kAttnDh) return JANUS_EUNSUPPORTED;
   if (c->atom_moe) {
@@ -568,7 +663,7 @@ struct Plan {
   float4* geo;
   float *B, *dB, *rt, *rbar;
   int *sp_cnt, *sp_off, *sp_atoms;
-  float *z, *eps, *lam, *phi, *vt, *Zr, *Tr, *colpart, *sig, *Psi;
+  float *z, *eps, *lam, *phi, *vt, *Zr, *Tr, *colpart, *sig, *Psi, *gs, *gsb;
   float4* gtan;
   double* Ed;
   float *h, *hh, *hht, *h3;   // [(T+1) or T][N, d]; the final-backward adjoint reuses hh
@@ -683,6 +778,8 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.lam = cv.take<float>(S);
   p.phi = cv.take<float>(3LL * N);
   p.sig = cv.take<float>(9LL * S);
+  p.gs = cv.take<float>((long long)S * d + 4);
+  p.gsb = cv.take<float>((long long)S * d + 4);
   p.Psi = cv.take<float>(9LL * S);
   p.gtan = cv.take<float4>(Ne + 1);
   p.vt = cv.take<float>(Nd);

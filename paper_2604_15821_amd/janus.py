@@ -46,6 +46,10 @@ class Edges(C.Structure):
                 ("rowptr", C.c_void_p), ("rev", C.c_void_p)]
 
 
+class Labels(C.Structure):
+    _fields_ = [("task", C.c_void_p), ("charge", C.c_void_p), ("spin", C.c_void_p)]
+
+
 class ProfileEntry(C.Structure):
     _fields_ = [("name", C.c_char * 32), ("launches", C.c_int64), ("ms", C.c_double), ("flops", C.c_double),
                 ("bytes", C.c_double)]
@@ -80,6 +84,8 @@ def _lib():
                                    C.POINTER(Debug), vp]
         lib.janus_step_stress.argtypes = [vp, vp, vp, vp, vp, i32, i32, C.POINTER(Edges), vp, vp, vp, vp, vp, vp,
                                           vp, vp, vp, C.POINTER(Debug), vp]
+        lib.janus_step_ex.argtypes = [vp, vp, vp, vp, vp, i32, i32, C.POINTER(Edges), vp, vp, vp, vp,
+                                      C.POINTER(Labels), vp, vp, vp, vp, vp, C.POINTER(Debug), vp]
         lib.janus_grouped_gemm.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
         lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
         lib.janus_set_workspace_limit.argtypes = [vp, i64]
@@ -96,7 +102,7 @@ def exported_symbols():
     """Names the library exports (checked against include/janus.h by the CPU tests)."""
     lib = _lib()
     names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
-             "janus_step_stress",
+             "janus_step_stress", "janus_step_ex",
              "janus_grouped_gemm", "janus_grouped_wgrad", "janus_profile_enable", "janus_profile_read",
              "janus_set_workspace_limit", "janus_last_chunks", "janus_last_triplets", "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
@@ -235,11 +241,12 @@ class Context:
 
     # ----------------------------------------------------------------- step
     def step(self, pos, cell, species, offsets, nl: NeighborList, W, E_ref, F_ref, out=None, debug=None,
-             S_ref=None, stress=None):
+             S_ref=None, stress=None, labels=None):
         """One training step; returns (loss [1], E [S], F [N,3], dLdW [like W]) device tensors.
 
         With S_ref [S,3,3] (needed when the model's w_S > 0) or a stress output
-        tensor [S,3,3], runs janus_step_stress and writes the stress into `stress`."""
+        tensor [S,3,3], writes the stress into `stress`; labels = (task, charge,
+        spin) int32 device tensors [S] (needed when the model has n_tasks > 0)."""
         import torch
         dev = pos.device
         N = pos.shape[0]
@@ -253,14 +260,19 @@ class Context:
         if debug is not None:
             dbg = Debug(*[_ptr(debug.get(k)).value for k in Debug.KEYS])
         dbgp = C.byref(dbg) if dbg is not None else None
-        if S_ref is None and stress is None:
+        if S_ref is None and stress is None and labels is None:
             rc = _lib().janus_step(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S, C.byref(edges),
                                    _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(loss), _ptr(E), _ptr(F), _ptr(dW), dbgp,
                                    _stream())
-        else:
+        elif labels is None:
             rc = _lib().janus_step_stress(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S,
                                           C.byref(edges), _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(S_ref), _ptr(loss),
                                           _ptr(E), _ptr(F), _ptr(stress), _ptr(dW), dbgp, _stream())
+        else:
+            lab = Labels(*[_ptr(x).value for x in labels])
+            rc = _lib().janus_step_ex(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S,
+                                      C.byref(edges), _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(S_ref), C.byref(lab),
+                                      _ptr(loss), _ptr(E), _ptr(F), _ptr(stress), _ptr(dW), dbgp, _stream())
         if rc:
             raise JanusError(rc, "janus_step")
         return loss, E, F, dW
@@ -337,5 +349,7 @@ def upload(batch, device="cuda:0"):
         "E_ref": t(batch.E_ref, torch.float32),
         "F_ref": t(batch.F_ref, torch.float32),
         "S_ref": None if batch.S_ref is None else t(batch.S_ref, torch.float32),
+        "labels": None if batch.task is None else tuple(t(getattr(batch, k), torch.int32)
+                                                        for k in ("task", "charge", "spin")),
         "W": t(pack_weights(batch.weights, batch.model), torch.float32),
     }

@@ -17,14 +17,14 @@ def _step(b, limit=None):
         ctx.set_workspace_limit(limit)
     nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
     loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"],
-                              S_ref=d["S_ref"] if b.model.w_S else None)
+                              S_ref=d["S_ref"] if b.model.w_S else None, labels=d["labels"])
     torch.cuda.synchronize()
     out = (float(loss.cpu()[0]), E.cpu().numpy(), F.cpu().numpy(), dW.cpu().numpy(), ctx.last_chunks())
     ctx.close()
     return out
 
 
-@pytest.mark.parametrize("name", ["small", "atom_moe", "stress", "attention"])
+@pytest.mark.parametrize("name", ["small", "atom_moe", "stress", "attention", "multitask"])
 def test_chunked_step_matches_single_pass_and_oracle(name):
     from oracle.model import Params, forward_energy, training_step
     from paper_2604_15821_amd import janus

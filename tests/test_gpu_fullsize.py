@@ -20,7 +20,7 @@ from helpers import TOL_E, TOL_F, TOL_W, banner, energy_error, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["small", "threebody", "atom_moe", "stress", "attention", "shard", "irregular"]
+FULL = ["small", "threebody", "atom_moe", "stress", "attention", "multitask", "shard", "irregular"]
 
 
 def _gpu_step(b, model=None):
@@ -32,7 +32,7 @@ def _gpu_step(b, model=None):
     nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
     st = torch.empty(b.n_struct, 3, 3, device="cuda:0")
     loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"],
-                              S_ref=d["S_ref"], stress=st)
+                              S_ref=d["S_ref"], stress=st, labels=d["labels"])
     torch.cuda.synchronize()
     out = {"loss": float(loss.cpu()[0]), "E": E.cpu().numpy(), "F": F.cpu().numpy(), "dW": dW.cpu().numpy(),
            "stress": st.cpu().numpy(), "chunks": ctx.last_chunks(), "edges": nl.n_edges}
