@@ -10,6 +10,9 @@ including the machine-readable record that ``bench.py`` reads back while the
 kernel sources still hash to the recorded value.
 
     python -m paper_2604_15821_amd.counters <workload> <directory with the run outputs>
+    python -m paper_2604_15821_amd.counters --trace <workload> <steps> <directory>
+
+The second form summarises a kernel-trace run alone into profiles/kernels_<workload>.md.
 """
 from __future__ import annotations
 
@@ -152,7 +155,58 @@ def algorithmic_bytes(bench_line: dict):
     return reads / 8, writes / 8
 
 
+def trace_command(workload: str, steps: int, out: str = "$R/gpurun_out") -> str:
+    """The rocprofv3 kernel-trace command of one workload (run from /tmp with TMPDIR=/tmp)."""
+    return (f"rocprofv3 --kernel-trace --stats --output-format csv -d {out}/trace_{workload} -o run -- "
+            f"python3 $R/bench.py --workload {workload} --steps {steps} --warmup 1 --breakdown-steps 1 "
+            f"--no-cpu-baseline")
+
+
+def trace_summary(workload: str, runs: str, steps: int) -> str:
+    """Markdown summary of one kernel-trace run: per-family and per-kernel time."""
+    with open(f"{runs}/trace_{workload}/run_kernel_stats.csv") as f:
+        stats = list(csv.DictReader(f))
+    fam = collections.defaultdict(lambda: [0, 0.0])
+    for r in stats:
+        a = fam[family(r["Name"])]
+        a[0] += int(r["Calls"])
+        a[1] += float(r["TotalDurationNs"]) / 1e6
+    bench_line = None
+    log = f"{runs}/trace_{workload}.log"
+    if os.path.exists(log):
+        lines = [x for x in open(log) if x.startswith("{")]
+        bench_line = json.loads(lines[-1]) if lines else None
+    L = [f"# Kernel time, training step, workload `{workload}`", "",
+         "Command (run from /tmp on the MI355X box with `TMPDIR=/tmp`, repo at `$R`):", "",
+         "```", trace_command(workload, steps), "```", "",
+         f"Summarised by `python -m paper_2604_15821_amd.counters --trace {workload} {steps} $R/gpurun_out`.",
+         f"All dispatches of the run ({steps} timed + 1 warm-up + 1 breakdown step). Families follow the",
+         "kernel names: products that use the expert GEMM kernels (the attention q|k|v and Wo products",
+         "too) count as expert_gemm here; bench.py's own profiler files those under dense_gemm.", "",
+         "| family | dispatches | total ms | % |", "|---|---:|---:|---:|"]
+    tot = sum(v[1] for v in fam.values()) or 1.0
+    for k, v in sorted(fam.items(), key=lambda kv: -kv[1][1]):
+        L.append(f"| {k} | {v[0]} | {v[1]:.2f} | {100 * v[1] / tot:.1f} |")
+    L += ["", "| kernel | calls | avg us | total ms | % |", "|---|---:|---:|---:|---:|"]
+    for r in stats[:25]:
+        n = re.sub(r"\(.*", "", r["Name"].replace("janus::", ""))
+        L.append(f"| `{n}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                 f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f} |")
+    if bench_line:
+        L += ["", "bench.py line of the same run (its own HIP-event timing):", "", "```",
+              json.dumps({k: bench_line[k] for k in ("value", "unit", "ms_per_step")}), "```"]
+    return "\n".join(L) + "\n"
+
+
 if __name__ == "__main__":
+    if len(sys.argv) > 1 and sys.argv[1] == "--trace":
+        wl, steps = sys.argv[2], int(sys.argv[3])
+        runs = sys.argv[4] if len(sys.argv) > 4 else os.path.join(ROOT, "gpurun_out")
+        out = os.path.join(ROOT, "profiles", f"kernels_{wl}.md")
+        with open(out, "w") as f:
+            f.write(trace_summary(wl, runs, steps))
+        print(out)
+        sys.exit(0)
     wl = sys.argv[1] if len(sys.argv) > 1 else "small"
     runs = sys.argv[2] if len(sys.argv) > 2 else os.path.join(ROOT, "gpurun_out")
     text = summarize(wl, runs)
