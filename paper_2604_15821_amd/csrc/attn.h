@@ -111,9 +111,10 @@ __device__ __forceinline__ void stage_rows(float* lds, const AttnCols& src, long
 }
 
 // Phase 1: osum_i (one wave per atom; lanes = queries).  stats[(e*H + a)*2 + {0,1}] = (max s, Z).
+// Atoms with at most min_n edges are skipped (the matrix-core kernel takes them).
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu, int N, int d, int H,
-    float* __restrict__ stats, float* __restrict__ osum) {
+    float* __restrict__ stats, float* __restrict__ osum, int min_n) {
   __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
   __shared__ float s_u[kAttnWaves][kAttnChunk];
   const int wv = threadIdx.x >> 6;
@@ -122,6 +123,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_kernel(
   const long long ld = 3LL * d;
   JANUS_WAVE_LOOP(i, N) {
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n <= min_n) continue;
     for (int a = 0; a < H; ++a) {
       const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
       const AttnCols kvc{{QKV + ck, QKV + cv, nullptr, nullptr}};
@@ -557,6 +559,175 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
 #pragma unroll
         for (int c = 0; c < kAttnDh; ++c) kb[c] = S1 * al[c] + S2 * be[c];
         if (valid) st32(QKVa + key * ld + cv, kb);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ matrix-core kernels
+// Neighbourhoods of at most kAttnMfmaN edges run on v_mfma_f32_16x16x4_f32, with the
+// edges padded to 16-row tiles.  Lane l works on row i16 = l % 16 of a tile and
+// slot j4 = l / 16 of the contraction; the 32 head columns are contracted in 8 steps
+// with column 8*j4 + s at step s, so each lane reads 8 consecutive floats of a row.
+// Scores are formed transposed (keys x queries): lane l then holds, for each pair of
+// tiles, keys 4*j4 + r (r = 0..3) of one query i16 -- exactly the A operand of the
+// following product with the values, so no data moves between the two products.
+constexpr int kAttnMfmaN = 64;
+constexpr int kAttnTiles = kAttnMfmaN / 16;
+
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4v mfma16(float a, float b, f32x4v c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// 8 floats of row `row` (clamped to the neighbourhood, zero past it) starting at column c0.
+__device__ __forceinline__ void frag8(const float* __restrict__ base, long long ld, int e0, int n, int row, int c0,
+                                      float* x) {
+  const int rr = row < n ? row : n - 1;
+  const float* p = base + (long long)(e0 + rr) * ld + c0;
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  const float z = row < n ? 1.f : 0.f;
+  x[0] = z * a.x; x[1] = z * a.y; x[2] = z * a.z; x[3] = z * a.w;
+  x[4] = z * b.x; x[5] = z * b.y; x[6] = z * b.z; x[7] = z * b.w;
+}
+
+// Sum (or max) over the four lane groups j4 of a value owned by row i16.
+__device__ __forceinline__ float sum_j4(float v) {
+  v += __shfl_xor(v, 16, 64);
+  return v + __shfl_xor(v, 32, 64);
+}
+__device__ __forceinline__ float max_j4(float v) {
+  v = fmaxf(v, __shfl_xor(v, 16, 64));
+  return fmaxf(v, __shfl_xor(v, 32, 64));
+}
+
+// Phase 1 on matrix cores for the atoms whose neighbourhood spans NT 16-row tiles
+// (NT = 1 also takes the atoms without edges); one instance per NT keeps the register
+// use of the small neighbourhoods small.  Same outputs as attn_fwd_kernel.
+template <int NT>
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_mfma_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu, int N, int d, int H,
+    float* __restrict__ stats, float* __restrict__ osum) {
+  const long long ld = 3LL * d;
+  const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
+  // one wave per (atom, head)
+  JANUS_WAVE_LOOP(item, (long long)N * H) {
+    const int i = (int)(item / H), a = (int)(item - (long long)i * H);
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n == 0 && NT == 1) {
+      if ((threadIdx.x & 63) < kAttnDh) osum[(long long)i * d + a * kAttnDh + (threadIdx.x & 63)] = 0.f;
+      continue;
+    }
+    if ((n + 15) >> 4 != NT) continue;
+    constexpr int nt = NT;
+    {
+      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+      // every load of the head first: q and k fragments, the value columns and envelope
+      // weights of the rows kt*16 + 4*j4 + r this lane feeds to the value product (the
+      // same rows give the query weights of the output tile)
+      float qf[NT][8], kf[NT][8], v0[NT][4], v1[NT][4], uk[NT][4];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        if (t >= nt) break;
+        frag8(QKV, ld, e0, n, t * 16 + i16, cq + 8 * j4, qf[t]);
+        frag8(QKV, ld, e0, n, t * 16 + i16, ck + 8 * j4, kf[t]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = t * 16 + 4 * j4 + r;
+          const int kk = key < n ? key : n - 1;
+          const float* vr = QKV + (long long)(e0 + kk) * ld + cv + i16;
+          v0[t][r] = vr[0];
+          v1[t][r] = vr[16];
+          uk[t][r] = key < n ? uu[e0 + kk] : 0.f;
+        }
+      }
+      // transposed scores per (key tile, query tile); the contraction step is outermost so
+      // the tile accumulators are independent
+      f32x4v S[NT][NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int u = 0; u < NT; ++u) S[t][u] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt)
+            if (kt < nt && qt < nt) S[kt][qt] = mfma16(kf[kt][st], qf[qt][st], S[kt][qt]);
+      // softmax over the keys of each query (query = qt*16 + i16; keys kt*16 + 4*j4 + r)
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt) {
+        if (qt >= nt) break;
+        float M = -INFINITY;
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt) {
+          if (kt >= nt) break;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = kt * 16 + 4 * j4 + r;
+            const float sv = key < n ? S[kt][qt][r] * kAttnScale : -INFINITY;
+            S[kt][qt][r] = sv;
+            M = fmaxf(M, sv);
+          }
+        }
+        M = max_j4(M);
+        float Z = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt) {
+          if (kt >= nt) break;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float pv = uk[kt][r] * __expf(S[kt][qt][r] - M);
+            S[kt][qt][r] = pv;
+            Z += pv;
+          }
+        }
+        Z = sum_j4(Z);
+        const float iZ = 1.f / Z;
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt) {
+          if (kt >= nt) break;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) S[kt][qt][r] *= iZ;
+        }
+        const int q = qt * 16 + i16;
+        if (j4 == 0 && q < n) {
+          stats[((long long)(e0 + q) * H + a) * 2] = M;
+          stats[((long long)(e0 + q) * H + a) * 2 + 1] = Z;
+        }
+      }
+      // o = p v for every (query tile, 16-column tile), key steps outermost so the eight
+      // accumulators are independent; osum = sum over queries of u_q o_q
+      f32x4v O[NT][2];
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt) O[qt][0] = O[qt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt)
+            if (kt < nt && qt < nt) {
+              O[qt][0] = mfma16(S[kt][qt][r], v0[kt][r], O[qt][0]);
+              O[qt][1] = mfma16(S[kt][qt][r], v1[kt][r], O[qt][1]);
+            }
+      float col0 = 0.f, col1 = 0.f;
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt) {
+        if (qt >= nt) break;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          col0 += uk[qt][r] * O[qt][0][r];
+          col1 += uk[qt][r] * O[qt][1][r];
+        }
+      }
+      col0 = sum_j4(col0);
+      col1 = sum_j4(col1);
+      if (j4 == 0) {
+        osum[(long long)i * d + cq + i16] = col0;
+        osum[(long long)i * d + cq + 16 + i16] = col1;
       }
     }
   }

@@ -352,6 +352,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   auto MHt = [&](int t) { return p.Mh + t * sEd; };
   auto QKVht = [&](int t) { return p.QKVh + t * sE3; };
   const double f_qkv = 6.0 * Ne * d * d;
+  const dim3 gNH = wave_grid((long long)N * (H > 0 ? H : 1));
   const double by_attn = Ne * (12.0 * d + 8.0 * H + 8.0) + N * 8.0 * d;
   const double f_atm = 2.0 * Mf * d * hf;
   const double by_fgather = N * 4.0 * d + Mf * (8.0 + 4.0 * d);
@@ -425,8 +426,17 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_ATTN, 0, by_attn);
+        // neighbourhoods up to kAttnMfmaN edges on matrix cores, larger ones on the vector units
+        hipLaunchKernelGGL(attn_fwd_mfma_kernel<1>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
+        hipLaunchKernelGGL(attn_fwd_mfma_kernel<2>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
+        hipLaunchKernelGGL(attn_fwd_mfma_kernel<3>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
+        hipLaunchKernelGGL(attn_fwd_mfma_kernel<4>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
         hipLaunchKernelGGL(attn_fwd_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)p.eu, N,
-                           d, H, STt(t), OSt(t));
+                           d, H, STt(t), OSt(t), kAttnMfmaN);
       }
       {
         PROF(PROF_DENSE_GEMM, f_dense, 0);
