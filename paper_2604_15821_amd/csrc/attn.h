@@ -302,7 +302,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_kernel(
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
-    const float* __restrict__ stats, int N, int d, int H, float* __restrict__ osumh) {
+    const float* __restrict__ stats, int N, int d, int H, float* __restrict__ osumh, int min_n) {
   __shared__ float s_rows[kAttnWaves][kAttnChunk * 4 * kAttnDh];
   __shared__ float s_sc[kAttnWaves][2][kAttnChunk];
   const int wv = threadIdx.x >> 6;
@@ -312,6 +312,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_kernel(
   const long long ld = 3LL * d;
   JANUS_WAVE_LOOP(i, N) {
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n <= min_n) continue;
     for (int a = 0; a < H; ++a) {
       const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
       const AttnCols cols{{QKV + ck, QKVh + ck, QKV + cv, QKVh + cv}};
@@ -729,6 +730,141 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_mfma_kernel(
         osum[(long long)i * d + cq + i16] = col0;
         osum[(long long)i * d + cq + 16 + i16] = col1;
       }
+    }
+  }
+}
+
+// Phase 3 on matrix cores for the atoms whose neighbourhood spans NT 16-row tiles
+// (NT = 1 also takes the atoms without edges), one wave per (atom, head); same output as
+// attn_tan_kernel.  Transposed score tiles S = k.q and Sh = k.qh + kh.q give, per
+// (key, query), p = u_k E and pz = p sh + uh_k E with E = exp(s - M_q)/Z_q (stored
+// statistics); then oh = pz v - (sum pz) o + p vh with o = p v, three value products
+// chained on the probability tiles as in the forward.
+template <int NT>
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_mfma_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
+    const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
+    const float* __restrict__ stats, int N, int d, int H, float* __restrict__ osumh) {
+  const long long ld = 3LL * d;
+  const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
+  JANUS_WAVE_LOOP(item, (long long)N * H) {
+    const int i = (int)(item / H), a = (int)(item - (long long)i * H);
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n == 0 && NT == 1) {
+      if ((threadIdx.x & 63) < kAttnDh) osumh[(long long)i * d + a * kAttnDh + (threadIdx.x & 63)] = 0.f;
+      continue;
+    }
+    if ((n + 15) >> 4 != NT) continue;
+    const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    // scores and their tangents, transposed (key tile, query tile)
+    f32x4v S[NT][NT], Sh[NT][NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int u = 0; u < NT; ++u) S[t][u] = Sh[t][u] = f32x4v{0.f, 0.f, 0.f, 0.f};
+    {
+      float qf[NT][8], kf[NT][8];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        frag8(QKV, ld, e0, n, t * 16 + i16, cq + 8 * j4, qf[t]);
+        frag8(QKV, ld, e0, n, t * 16 + i16, ck + 8 * j4, kf[t]);
+      }
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt) S[kt][qt] = mfma16(kf[kt][st], qf[qt][st], S[kt][qt]);
+      float hf[NT][8];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) frag8(QKVh, ld, e0, n, t * 16 + i16, cq + 8 * j4, hf[t]);   // qh
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt) Sh[kt][qt] = mfma16(kf[kt][st], hf[qt][st], Sh[kt][qt]);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) frag8(QKVh, ld, e0, n, t * 16 + i16, ck + 8 * j4, hf[t]);   // kh
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt) Sh[kt][qt] = mfma16(hf[kt][st], qf[qt][st], Sh[kt][qt]);
+    }
+    // per-key weights of the rows kt*16 + 4*j4 + r (also the output rows' query weights)
+    float uk[NT][4], uhk[NT][4];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = t * 16 + 4 * j4 + r;
+        const int kk = key < n ? key : n - 1;
+        uk[t][r] = key < n ? uu[e0 + kk] : 0.f;
+        uhk[t][r] = key < n ? ud[e0 + kk] * rt[e0 + kk] : 0.f;
+      }
+    // p (into S) and pz (into Sh); s1 = sum over keys of pz, per query
+    float s1[NT];
+#pragma unroll
+    for (int qt = 0; qt < NT; ++qt) {
+      const int q = qt * 16 + i16;
+      const long long sq = ((long long)(e0 + (q < n ? q : n - 1)) * H + a) * 2;
+      const float M = stats[sq], iZ = 1.f / stats[sq + 1];
+      float sum = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float E = __expf(S[kt][qt][r] * kAttnScale - M) * iZ;
+          const float p = uk[kt][r] * E;
+          const float pz = p * Sh[kt][qt][r] * kAttnScale + uhk[kt][r] * E;
+          S[kt][qt][r] = p;
+          Sh[kt][qt][r] = pz;
+          sum += pz;
+        }
+      s1[qt] = sum_j4(sum);
+    }
+    // value products: o = p v, oz = pz v, ov = p vh, per (query tile, 16-column tile)
+    f32x4v O[NT][2], OZ[NT][2], OV[NT][2];
+#pragma unroll
+    for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) O[qt][ct] = OZ[qt][ct] = OV[qt][ct] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = kt * 16 + 4 * j4 + r;
+        const long long row = (long long)(e0 + (key < n ? key : n - 1)) * ld;
+        const float v0 = QKV[row + cv + i16], v1 = QKV[row + cv + 16 + i16];
+        const float w0 = QKVh[row + cv + i16], w1 = QKVh[row + cv + 16 + i16];
+#pragma unroll
+        for (int qt = 0; qt < NT; ++qt) {
+          O[qt][0] = mfma16(S[kt][qt][r], v0, O[qt][0]);
+          O[qt][1] = mfma16(S[kt][qt][r], v1, O[qt][1]);
+          OZ[qt][0] = mfma16(Sh[kt][qt][r], v0, OZ[qt][0]);
+          OZ[qt][1] = mfma16(Sh[kt][qt][r], v1, OZ[qt][1]);
+          OV[qt][0] = mfma16(S[kt][qt][r], w0, OV[qt][0]);
+          OV[qt][1] = mfma16(S[kt][qt][r], w1, OV[qt][1]);
+        }
+      }
+    // osumh = sum over queries of u_q oh_q + uh_q o_q, oh = oz - s1 o + ov (rows qt*16 + 4*j4 + r)
+    float col0 = 0.f, col1 = 0.f;
+#pragma unroll
+    for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float s1r = __shfl(s1[qt], 4 * j4 + r, 64);   // s1 of query qt*16 + 4*j4 + r
+        const float u = uk[qt][r], uh = uhk[qt][r];
+        col0 += u * (OZ[qt][0][r] - s1r * O[qt][0][r] + OV[qt][0][r]) + uh * O[qt][0][r];
+        col1 += u * (OZ[qt][1][r] - s1r * O[qt][1][r] + OV[qt][1][r]) + uh * O[qt][1][r];
+      }
+    col0 = sum_j4(col0);
+    col1 = sum_j4(col1);
+    if (j4 == 0) {
+      osumh[(long long)i * d + cq + i16] = col0;
+      osumh[(long long)i * d + cq + 16 + i16] = col1;
     }
   }
 }

@@ -732,9 +732,18 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_ATTN, 0, by_attn);
+#define JANUS_TAN_MFMA(NTV)                                                                                    \
+  hipLaunchKernelGGL(attn_tan_mfma_kernel<NTV>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),                \
+                     (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,         \
+                     (const float*)STt(t), N, d, H, p.osh)
+        JANUS_TAN_MFMA(1);
+        JANUS_TAN_MFMA(2);
+        JANUS_TAN_MFMA(3);
+        JANUS_TAN_MFMA(4);
+#undef JANUS_TAN_MFMA
         hipLaunchKernelGGL(attn_tan_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)QKVht(t),
                            (const float*)p.eu, (const float*)p.eud, (const float*)p.rt, (const float*)STt(t), N, d, H,
-                           p.osh);
+                           p.osh, kAttnMfmaN);
       }
       {
         PROF(PROF_DENSE_GEMM, 2 * f_dense, 0);
