@@ -94,6 +94,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown-steps", type=int, default=3,
                     help="untimed steps with every kernel family's events, for the per-family table")
+    ap.add_argument("--concurrent", action="store_true",
+                    help="expert weight gradients on a second stream, beside the expert products")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="one elementwise copy kernel over this many MiB before the run (calibrates HBM counters)")
     args = ap.parse_args()
@@ -123,6 +125,7 @@ def main():
     b = make_batch(args.workload)
     d = janus.upload(b, "cuda:0")
     ctx = janus.Context(m)
+    ctx.set_concurrency(args.concurrent)
     nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
     Ne = nl.n_edges
     N, S = b.n_atoms, b.n_struct
@@ -215,6 +218,7 @@ def main():
         "config": {"workload": args.workload, "structures": S, "atoms": N, "edges": Ne, "d": m.d,
                    "d_hidden": m.d_hidden, "experts": m.n_experts, "top_k": m.top_k, "blocks": m.n_blocks,
                    "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none",
+                   "streams": 2 if args.concurrent else 1,
                    **({"atom_moe": {"experts": m.n_experts_f, "top_k": m.top_k_f, "d_hidden": m.d_hidden_f}}
                       if m.atom_moe else {}),
                    **({"stress_weight": m.w_S} if m.w_S else {}),

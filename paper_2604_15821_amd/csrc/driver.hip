@@ -59,12 +59,20 @@ extern "C" void janus_destroy(janus_ctx* c) {
   if (c->host_word) (void)hipHostFree(c->host_word);
   if (c->host_plan) (void)hipHostFree(c->host_plan);
   for (hipEvent_t e : c->prof_pool) (void)hipEventDestroy(e);
+  for (hipEvent_t e : c->sync_pool) (void)hipEventDestroy(e);
+  if (c->side) (void)hipStreamDestroy(c->side);
   delete c;
 }
 
 extern "C" int janus_set_workspace_limit(janus_ctx* ctx, int64_t bytes) {
   if (!ctx || bytes < 0) return JANUS_EINVAL;
   ctx->ws_limit = bytes;
+  return JANUS_OK;
+}
+
+extern "C" int janus_set_concurrency(janus_ctx* ctx, int on) {
+  if (!ctx || (on != 0 && on != 1)) return JANUS_EINVAL;
+  ctx->concurrent = on;
   return JANUS_OK;
 }
 
@@ -95,6 +103,7 @@ extern "C" int janus_weight_layout(const janus_config* cfg, janus_tensor_desc* o
 #define JANUS_CAT2(a, b) a##b
 #define JANUS_CAT(a, b) JANUS_CAT2(a, b)
 #define PROF(cls, fl, by) ProfScope JANUS_CAT(ps_, __LINE__)(ctx, st, cls, (double)(fl), (double)(by))
+#define PROFS(strm, cls, fl, by) ProfScope JANUS_CAT(ps_, __LINE__)(ctx, strm, cls, (double)(fl), (double)(by))
 
 namespace {
 
@@ -625,6 +634,15 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   JANUS_HIP_TRY(hipGetLastError());
 
   // ---- phase 3: double backward of the force loss (hht[t] = loss adjoint of hh[t])
+  // The expert weight gradients go to the side stream (ss.sd), where they run
+  // beside the memory-bound products G5/G6 and the edge kernels.  Buffers they
+  // read: p.T1 (G7, until t1_free), Abar of the block (G7), Sbt (G8).  Sbt of
+  // block t is written over Abar of block t-1 (block 0: p.Shat0), which G7 of
+  // block t-1 has finished reading once t1_free of that block has passed.
+  SideSync ss(ctx, st);
+  hipStream_t sd = ss.sd;
+  hipEvent_t t1_free = nullptr;   // side stream done with p.T1 (and with the last Abar it read)
+  auto Shat = [&](int t) { return t == 0 ? p.Shat0 : Ab(t - 1); };
   for (int t = 0; t < T; ++t) {
     const float* Wb = Wp(blk(t, "W_b"));
     const float* W1 = Wp(blk(t, "W1"));
@@ -674,6 +692,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                    (const float*)p.T3b, (const float*)Xbar(t), Ne, d, p.g3t + t * M3, p.Q);
       }
     }
+    ss.wait(t1_free);   // edge_p3 rewrites p.T1; G5 below rewrites Abar of block t-1
     if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_p3);
       // with triplets, P_e already holds the triplet part written by tri_p3
@@ -684,36 +703,39 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     {
       // dW_b (part 1): (rt B')^T Fbar
       PROF(PROF_DENSE_GEMM, f_filt, 0);
-      launch_wgrad(st, LoadRowScale{p.dB, p.rt, nb}, LoadPlain{Fbar(t), d}, nb, d, p.chunksE, p.ncE, p.cfE, p.mcE, 1,
-                   p.partial, Gp(blk(t, "W_b")), 1);
+      launch_wgrad_skinny(st, p.dB, p.rt, Fbar(t), nb, d, p.chunksE, p.ncE, p.cfE, p.mcE, p.partial,
+                          Gp(blk(t, "W_b")), 1);
     }
     {
       PROF(PROF_ATOM, 0, by_scatter);
       LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe, (const float*)nullptr,
                  (const float*)nullptr, N, d, HV(p.h3, t));
     }
+    ss.fork();
     {
-      // G7: dW1 += Xbt^T Abar
-      PROF(PROF_EXPERT_WGRAD, f_exp, 0);
-      launch_wgrad(st, LoadPlain{p.T1, d}, LoadPlain{Ab(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
-                   p.partial, Gp(blk(t, "W1")), 1);
+      // G7: dW1 += Xbt^T Abar (side stream)
+      PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
+      launch_wgrad(sd, LoadPlain{p.T1, d}, LoadPlain{Ab(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
+                   p.partial2, Gp(blk(t, "W1")), 1);
     }
+    t1_free = ss.mark();
     {
-      // G5: Abt = Xbt W1 -> Sbt (into Ab), C (into Sb)
+      // G5: Abt = Xbt W1 -> Sbt (into Shat(t)), C (into Sb)
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
       launch_rows<false>(st, LoadPlain{p.T1, d}, W1, d, h, TL(t), p.ntiles + t, p.mt,
-                         EpiP3{Aa(t), Sb(t), Ab(t), h});
+                         EpiP3{Aa(t), Sb(t), Shat(t), h});
+    }
+    ss.fork();
+    {
+      // G8: dW2 += Sbt^T Ybar (side stream)
+      PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
+      launch_wgrad(sd, LoadPlain{Shat(t), h}, LoadPlain{Ybs(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
+                   p.partial2, Gp(blk(t, "W2")), 1);
     }
     {
       // G6: Ybt = Sbt W2
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
-      launch_rows<false>(st, LoadPlain{Ab(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
-    }
-    {
-      // G8: dW2 += Sbt^T Ybar
-      PROF(PROF_EXPERT_WGRAD, f_exp, 0);
-      launch_wgrad(st, LoadPlain{Ab(t), h}, LoadPlain{Ybs(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
-                   p.partial, Gp(blk(t, "W2")), 1);
+      launch_rows<false>(st, LoadPlain{Shat(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
     }
     // phase-2 dE/du of this block (hh^{t+1} without the feature-update MoE)
     const float* hbar_u3 = atom ? UU(t) : HV(p.hh, t + 1);
@@ -820,11 +842,13 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                  p.mcN, 1, p.partial, Gp("W_o1"), 1);
     launch_rows<true>(st, LoadPlain{p.Zr, d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiDense{HV(p.hh, T), d});
   }
+  // G11 and G12 go to the side stream; G12 reads p.T1 until t1_free.
   for (int t = T - 1; t >= 0; --t) {
     const float* Wb = Wp(blk(t, "W_b"));
     const float* W1 = Wp(blk(t, "W1"));
     const float* W2 = Wp(blk(t, "W2"));
     const float* hht_t = t == 0 ? nullptr : HV(p.hht, t);
+    ss.wait(t1_free);   // p.T1 is rewritten below
     // loss adjoint of u (of h^{t+1} without the feature-update MoE)
     const float* a_u = HV(p.hh, t + 1);
     if (atom) {
@@ -908,28 +932,31 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)nullptr, a_u, N, d,
                    p.T1);
     }
+    ss.fork();
+    {
+      // G12: dW2 += SiLU(A)^T (g mt) (side stream)
+      PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
+      launch_wgrad(sd, LoadSilu{Aa(t), h}, LoadRowScale{p.T1, SG(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc,
+                   Ee, p.partial2, Gp(blk(t, "W2")), 1);
+    }
+    t1_free = ss.mark();
     {
       // G9: St = mt W2^T -> At = g SiLU'(A) St + C (into Sb); row sums for the gate adjoint
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
       launch_rows<true>(st, LoadPlain{p.T1, d}, W2, d, h, TL(t), p.ntiles + t, p.mt, EpiP4{Aa(t), Sb(t), SG(t), h},
                         p.gpart);
     }
+    ss.fork();
+    {
+      // G11: dW1 += X^T At (side stream)
+      PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
+      launch_wgrad(sd, LoadPlain{Xs(t), d}, LoadPlain{Sb(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
+                   p.partial2, Gp(blk(t, "W1")), 1);
+    }
     {
       // G10: Xt = At W1^T
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
       launch_rows<true>(st, LoadPlain{Sb(t), h}, W1, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
-    }
-    {
-      // G11: dW1 += X^T At
-      PROF(PROF_EXPERT_WGRAD, f_exp, 0);
-      launch_wgrad(st, LoadPlain{Xs(t), d}, LoadPlain{Sb(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
-                   p.partial, Gp(blk(t, "W1")), 1);
-    }
-    {
-      // G12: dW2 += SiLU(A)^T (g mt)
-      PROF(PROF_EXPERT_WGRAD, f_exp, 0);
-      launch_wgrad(st, LoadSilu{Aa(t), h}, LoadRowScale{p.T1, SG(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc,
-                   Ee, p.partial, Gp(blk(t, "W2")), 1);
     }
     if (Ne > 0) {
       {
@@ -941,8 +968,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       {
         // dW_b (part 2): B^T Ft
         PROF(PROF_DENSE_GEMM, f_filt, 0);
-        launch_wgrad(st, LoadPlain{p.B, nb}, LoadPlain{p.Ft, d}, nb, d, p.chunksE, p.ncE, p.cfE, p.mcE, 1, p.partial,
-                     Gp(blk(t, "W_b")), 1);
+        launch_wgrad_skinny(st, p.B, nullptr, p.Ft, nb, d, p.chunksE, p.ncE, p.cfE, p.mcE, p.partial,
+                            Gp(blk(t, "W_b")), 1);
       }
       {
         PROF(PROF_OTHER, 0, 0);
@@ -1026,6 +1053,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                  (const float*)HV(p.h3, t), N, d, HV(p.hh, t));
     }
   }
+  // the caller's stream waits for the side stream's weight gradients
+  ss.join();
+  if (ss.err != hipSuccess) return janus_set_hip_error(ss.err);
   {
     PROF(PROF_OTHER, 0, 8.0 * Nd);
     hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(256), 0, st, (const int*)p.sp_off,
@@ -1268,6 +1298,11 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
   ctx->last_chunks = (int)chunks.size();
   ctx->last_triplets = tpre[S];
 
+  if (ctx->concurrent && !ctx->side) {
+    // created on first use on the context's device; default priority
+    JANUS_HIP_TRY(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking));
+  }
+  ctx->sync_used = 0;
   JANUS_HIP_TRY(hipMemsetAsync(dLdW, 0, sizeof(float) * L.total, st));
   if (dbg && dbg->counts) JANUS_HIP_TRY(hipMemsetAsync(dbg->counts, 0, sizeof(int) * cfg.n_blocks * cfg.n_experts, st));
   for (const ChunkArgs& ca : chunks) {

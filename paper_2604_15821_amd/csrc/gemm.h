@@ -571,4 +571,78 @@ __global__ __launch_bounds__(256, 2) void gemm_wgrad_kernel(ALoad al, BLoad bl, 
   gemm_wgrad_block<ALoad, BLoad>(blockIdx.x, smem, al, bl, P, Q, chunks, n_chunks, partial);
 }
 
+// ---------------------------------------------------------- skinny wgrad
+// G[p, q] = sum_r s[r] A[r, p] B[r, q] for a short P (P * Q <= 16384, the
+// radial-filter gradient: P = basis size, Q = d).  A 128-row MFMA tile would
+// be mostly padding there, so the vector units do it: a workgroup owns one
+// chunk of rows and the whole P x Q output, thread t the float4 outputs
+// t + 256 j; rows pass through LDS 16 at a time.  Partials per chunk, reduced
+// like gemm_wgrad's.  s may be null (s = 1).
+constexpr int kSkinnyRows = 16;
+
+template <int NO>
+__global__ __launch_bounds__(256) void wgrad_skinny_kernel(const float* __restrict__ A, const float* __restrict__ s,
+                                                           const float* __restrict__ B, int P, int Q,
+                                                           const WChunk* __restrict__ chunks,
+                                                           const int* __restrict__ n_chunks,
+                                                           float* __restrict__ partial) {
+  __shared__ __attribute__((aligned(16))) float a_s[kSkinnyRows * 32];
+  __shared__ __attribute__((aligned(16))) float b_s[kSkinnyRows * 512];
+  const int c = blockIdx.x;
+  if (c >= *n_chunks) return;
+  const WChunk ch = chunks[c];
+  const int tid = threadIdx.x;
+  const int q4n = Q >> 2, p4n = P >> 2, n_out = P * q4n;
+  float4 acc[NO];
+  int pj[NO], qj[NO];
+#pragma unroll
+  for (int j = 0; j < NO; ++j) {
+    acc[j] = f4zero();
+    const int o = tid + 256 * j;
+    pj[j] = o < n_out ? o / q4n : 0;
+    qj[j] = o < n_out ? o % q4n : 0;
+  }
+  for (int r0 = ch.r0; r0 < ch.r1; r0 += kSkinnyRows) {
+    // stage rows r0 .. r0 + 15 (zeros past the chunk)
+    for (int i = tid; i < kSkinnyRows * p4n; i += 256) {
+      const int rr = i / p4n, k4 = i - rr * p4n;
+      const long long r = (long long)r0 + rr;
+      float4 v = f4zero();
+      if (r < ch.r1) {
+        v = ld4(A + r * P + 4 * k4);
+        if (s) {
+          const float w = s[r];
+          v = make_float4(w * v.x, w * v.y, w * v.z, w * v.w);
+        }
+      }
+      st4(a_s + rr * P + 4 * k4, v);
+    }
+    for (int i = tid; i < kSkinnyRows * q4n; i += 256) {
+      const int rr = i / q4n, k4 = i - rr * q4n;
+      const long long r = (long long)r0 + rr;
+      st4(b_s + rr * Q + 4 * k4, r < ch.r1 ? ld4(B + r * Q + 4 * k4) : f4zero());
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int rr = 0; rr < kSkinnyRows; ++rr) {
+#pragma unroll
+      for (int j = 0; j < NO; ++j) {
+        const float a = a_s[rr * P + pj[j]];
+        const float4 b = ld4(b_s + rr * Q + 4 * qj[j]);
+        acc[j].x += a * b.x;
+        acc[j].y += a * b.y;
+        acc[j].z += a * b.z;
+        acc[j].w += a * b.w;
+      }
+    }
+    __syncthreads();
+  }
+  float4* out = reinterpret_cast<float4*>(partial + (long long)c * P * Q);
+#pragma unroll
+  for (int j = 0; j < NO; ++j) {
+    const int o = tid + 256 * j;
+    if (o < n_out) out[o] = acc[j];
+  }
+}
+
 }  // namespace janus

@@ -51,6 +51,12 @@ struct janus_ctx {
   std::vector<janus_prof_rec> prof_recs;
   std::vector<hipEvent_t> prof_pool;
   size_t prof_used = 0;
+  // second stream for the expert weight gradients, which then run beside the
+  // memory-bound double-backward products (janus_set_concurrency)
+  int concurrent = 0;
+  hipStream_t side = nullptr;
+  std::vector<hipEvent_t> sync_pool;   // fork / join events, reused every step
+  size_t sync_used = 0;
 };
 
 namespace janus {
@@ -63,6 +69,25 @@ struct ProfScope {
   bool on;
   ProfScope(janus_ctx* ctx, hipStream_t s, int cls, double flops, double bytes);
   ~ProfScope();
+};
+
+// Fork / join between the caller's stream and the context's side stream.
+// side_stream() is the stream the weight gradients go to: the side stream when
+// concurrency is on, else the caller's stream itself (then every fork, mark and
+// wait below is a no-op and the step runs in one stream, in the same order).
+struct SideSync {
+  janus_ctx* c;
+  hipStream_t st, sd;
+  hipError_t err = hipSuccess;
+  SideSync(janus_ctx* ctx, hipStream_t main);
+  // event recorded on `from` now (nullptr when both streams are one)
+  hipEvent_t record(hipStream_t from);
+  // `to` waits for everything issued to `from` so far
+  void order(hipStream_t from, hipStream_t to);
+  void fork() { order(st, sd); }
+  void join() { order(sd, st); }
+  hipEvent_t mark() { return record(sd); }
+  void wait(hipEvent_t e);
 };
 
 // Grow `b` to at least `bytes` (contents are not preserved).
@@ -87,15 +112,22 @@ struct Carver {
 inline int max_rows_tiles(long long M, int groups) { return (int)((M + GBM - 1) / GBM) + groups; }
 inline int max_wchunks(long long M, int groups, int kc) { return (int)((M + kc - 1) / kc) + groups; }
 
-// Chunk length of the weight-gradient contraction: long enough to keep the
-// partials small, short enough to give the GPU a few thousand workgroups (at
-// least 256 where the contraction allows); 128 to 16384 rows.
+// Chunk length of the weight-gradient contraction, a power of two from 128 to
+// 16384 rows.  Short chunks give the GPU several rounds of workgroups (a grid
+// of 1.4 rounds leaves most of the second round idle); long chunks keep the
+// partial tiles, written and read back by the reduction, small.  The chunk
+// doubles while the grid exceeds 8192 workgroups, or while the partials
+// exceed half of the operand bytes and the doubled chunk still gives at
+// least 2048 workgroups.
 inline int wgrad_chunk_rows(long long M, int P, int Q) {
-  long long tiles = (long long)((P + GBM - 1) / GBM) * ((Q + GBN - 1) / GBN);
+  const long long tiles = (long long)((P + GBM - 1) / GBM) * ((Q + GBN - 1) / GBN);
+  const double operand_bytes = 4.0 * (double)M * (P + Q);
   auto blocks = [&](long long kc) { return ((M + kc - 1) / kc) * tiles; };
-  long long kc = 1024;
-  while (kc > 128 && blocks(kc) < 256) kc /= 2;
-  while (kc < 16384 && blocks(kc) > 4096) kc *= 2;
+  auto partial_bytes = [&](long long kc) { return 8.0 * (double)((M + kc - 1) / kc) * P * Q; };
+  long long kc = 128;
+  while (kc < 16384 && (blocks(kc) > 8192 ||
+                        (partial_bytes(kc) > 0.5 * operand_bytes && blocks(2 * kc) >= 2048)))
+    kc *= 2;
   return (int)kc;
 }
 
@@ -122,6 +154,28 @@ void launch_wgrad(hipStream_t st, const ALoad& al, const BLoad& bl, int P, int Q
                        n_chunks, partial);
   }
   launch_wgrad_reduce(st, partial, chunk_first, groups, (long long)P * Q, G, accumulate);
+}
+
+// Skinny weight gradient (P * Q <= 16384, P and Q multiples of 4, one group):
+// G (+)= (s * A)^T B over the chunks of the table.
+inline void launch_wgrad_skinny(hipStream_t st, const float* A, const float* s, const float* B, int P, int Q,
+                                const WChunk* chunks, const int* n_chunks, const int* chunk_first, int max_chunks,
+                                float* partial, float* G, int accumulate) {
+  if (max_chunks > 0) {
+    const int no = (P * Q / 4 + 255) / 256;
+    const dim3 grid(max_chunks), blk(256);
+    if (no <= 1)
+      hipLaunchKernelGGL(wgrad_skinny_kernel<1>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+    else if (no <= 2)
+      hipLaunchKernelGGL(wgrad_skinny_kernel<2>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+    else if (no <= 4)
+      hipLaunchKernelGGL(wgrad_skinny_kernel<4>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+    else if (no <= 8)
+      hipLaunchKernelGGL(wgrad_skinny_kernel<8>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+    else
+      hipLaunchKernelGGL(wgrad_skinny_kernel<16>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+  }
+  launch_wgrad_reduce(st, partial, chunk_first, 1, (long long)P * Q, G, accumulate);
 }
 
 void build_tables(hipStream_t st, const int* row_off, int groups, int kc, RowsTile* tiles, int* n_tiles,

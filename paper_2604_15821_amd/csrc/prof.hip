@@ -1,4 +1,5 @@
-// Event-pair profiler of the kernel families (janus_profile_enable / _read).
+// Event-pair profiler of the kernel families (janus_profile_enable / _read)
+// and the fork / join events between the caller's stream and the side stream.
 #include <cstring>
 
 #include "internal.h"
@@ -36,6 +37,32 @@ ProfScope::~ProfScope() {
   if (!on) return;
   (void)hipEventRecord(rec.b, st);
   c->prof_recs.push_back(rec);
+}
+
+SideSync::SideSync(janus_ctx* ctx, hipStream_t main) : c(ctx), st(main), sd(main) {
+  if (c->concurrent && c->side) sd = c->side;
+}
+
+hipEvent_t SideSync::record(hipStream_t from) {
+  if (sd == st || err != hipSuccess) return nullptr;
+  if (c->sync_used == c->sync_pool.size()) {
+    hipEvent_t e;
+    err = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+    if (err != hipSuccess) return nullptr;
+    c->sync_pool.push_back(e);
+  }
+  hipEvent_t e = c->sync_pool[c->sync_used++];
+  err = hipEventRecord(e, from);
+  return err == hipSuccess ? e : nullptr;
+}
+
+void SideSync::order(hipStream_t from, hipStream_t to) {
+  hipEvent_t e = record(from);
+  if (e) err = hipStreamWaitEvent(to, e, 0);
+}
+
+void SideSync::wait(hipEvent_t e) {
+  if (e && err == hipSuccess) err = hipStreamWaitEvent(st, e, 0);
 }
 
 }  // namespace janus

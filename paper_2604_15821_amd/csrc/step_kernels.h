@@ -684,6 +684,9 @@ struct Plan {
   float *Xs, *A, *Sb, *Ab, *Ybs, *Xbar, *Fbar, *g3;
   // temporaries
   float *T1, *T2, *Pe, *Ft, *gpart, *gt, *partC, *partN, *lte, *partial;
+  // expert weight-gradient partials (the side stream's own) and the double
+  // backward's Sbt of block 0 (block t > 0 writes it over Abar of block t-1)
+  float *partial2, *Shat0;
   // chunk-local neighbour list (indices relative to the chunk)
   int *cei, *cej, *crev, *crow, *coff;
   long long* scan;   // scratch of the exclusive scans (triplet CSR, species groups)
@@ -871,6 +874,8 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     part = std::max(part, (long long)p.mcA * d * 3 * d);
   }
   p.partial = cv.take<float>(part);
+  p.partial2 = cv.take<float>((long long)p.mc * d * h);
+  p.Shat0 = cv.take<float>(M * h);
   p.cei = cv.take<int>(Ne + 1);
   p.cej = cv.take<int>(Ne + 1);
   p.crev = cv.take<int>(Ne + 1);

@@ -89,6 +89,7 @@ def _lib():
         lib.janus_grouped_gemm.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
         lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
         lib.janus_set_workspace_limit.argtypes = [vp, i64]
+        lib.janus_set_concurrency.argtypes = [vp, C.c_int]
         lib.janus_last_chunks.argtypes = [vp]
         lib.janus_last_triplets.argtypes = [vp]
         lib.janus_last_triplets.restype = i64
@@ -104,7 +105,8 @@ def exported_symbols():
     names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
              "janus_step_stress", "janus_step_ex",
              "janus_grouped_gemm", "janus_grouped_wgrad", "janus_profile_enable", "janus_profile_read",
-             "janus_set_workspace_limit", "janus_last_chunks", "janus_last_triplets", "janus_strerror"]
+             "janus_set_workspace_limit", "janus_set_concurrency", "janus_last_chunks", "janus_last_triplets",
+             "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
 
@@ -282,6 +284,12 @@ class Context:
         rc = _lib().janus_set_workspace_limit(self.h, int(nbytes))
         if rc:
             raise JanusError(rc, "janus_set_workspace_limit")
+
+    def set_concurrency(self, on: bool):
+        """Expert weight gradients on the context's second stream (True) or on the caller's (False, the default)."""
+        rc = _lib().janus_set_concurrency(self.h, int(bool(on)))
+        if rc:
+            raise JanusError(rc, "janus_set_concurrency")
 
     def last_chunks(self) -> int:
         return int(_lib().janus_last_chunks(self.h))

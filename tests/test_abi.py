@@ -73,3 +73,9 @@ def test_strerror_messages():
     for code in (0, -1, -2, -3, -4, -5):
         assert lib.janus_strerror(code)
     assert b"unknown" in lib.janus_strerror(17)
+
+
+def test_concurrency_switch_rejects_bad_arguments():
+    lib = C.CDLL(janus.LIB_PATH)
+    lib.janus_set_concurrency.argtypes = [C.c_void_p, C.c_int]
+    assert lib.janus_set_concurrency(None, 1) == janus.JANUS_EINVAL
