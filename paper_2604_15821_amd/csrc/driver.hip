@@ -610,7 +610,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       hipLaunchKernelGGL(tri_edge_vec_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, (const int*)p.trow,
                          (const int*)p.trev, (const int*)p.te2, (const float*)p.tc, (const float4*)p.geo,
                          (const float4*)p.tacc, Ne, p.gvec);
-    hipLaunchKernelGGL(force_kernel, dim3(cdiv(N, 256)), b256, 0, st, rowptr, rev, (const float*)p.rbar,
+    hipLaunchKernelGGL(force_kernel, gN, b256, 0, st, rowptr, rev, (const float*)p.rbar,
                        (const float4*)p.geo, (const float4*)(three ? p.gvec : nullptr), N, F);
     if (S_ref || stress_out)
       hipLaunchKernelGGL(stress_kernel, wave_grid(S), b256, 0, st, rowptr, offsets, cell, (const float*)p.rbar,
@@ -829,7 +829,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     LAUNCH_VPL(readout_bwd_kernel, d, gN, b256, 0, st, (const float*)p.z, (const float*)p.vt, wo2,
                (const float*)p.lam, (const int*)p.sid, N, d, p.Zr, p.Tr);
     const int nch = (N + kColChunk - 1) / kColChunk;
-    hipLaunchKernelGGL(colsum_partial_kernel, dim3(cdiv(d, 256), nch), b256, 0, st, (const float*)p.Tr,
+    hipLaunchKernelGGL(colsum_partial_kernel, dim3(cdiv(d, 64), nch), dim3(64), 0, st, (const float*)p.Tr,
                        (long long)N, d, p.colpart);
     hipLaunchKernelGGL(colsum_final_kernel, dim3(cdiv(d, 256)), b256, 0, st, (const float*)p.colpart, nch, d,
                        Gp("w_o2"));
@@ -891,7 +891,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         hipLaunchKernelGGL(edge_logit_kernel, dim3(cdiv((long long)N * Ef, 256)), b256, 0, st, species,
                            (const float*)(p.sprob + (long long)t * nsp * Ef), (const int*)(p.eidf + t * Mf),
                            (const float*)p.gtf, (long long)N, kf, Ef, p.ltf);
-        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
                            (const int*)p.sp_atoms, (const float*)p.ltf, Ef, nsp, Gp(blk(t, "Pf")));
       }
       a_u = p.ut;
@@ -978,11 +978,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         hipLaunchKernelGGL(edge_logit_kernel, dim3(cdiv(Ne * Ee, 256)), b256, 0, st, (const int*)(p.pair + t * Ne),
                            (const float*)(p.pprob + t * np * Ee), (const int*)(p.eid + t * M), (const float*)p.gt, Ne,
                            k, Ee, p.lte);
-        hipLaunchKernelGGL(router_atom_kernel, dim3(cdiv((long long)N * Ee, 256)), b256, 0, st, rowptr, rev, Ee,
+        hipLaunchKernelGGL(router_atom_kernel, gN, b256, 0, st, rowptr, rev, Ee,
                            (const float*)p.lte, N, p.partC, p.partN);
-        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
                            (const int*)p.sp_atoms, (const float*)p.partC, Ee, nsp, Gp(blk(t, "Pc")));
-        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
                            (const int*)p.sp_atoms, (const float*)p.partN, Ee, nsp, Gp(blk(t, "Pn")));
       }
     }
@@ -1039,11 +1039,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                            (const int*)p.trev, E3, (const float*)p.LT3, Ne, p.LB, p.LC);
         hipLaunchKernelGGL(tri_router_atom_kernel, gN, b256, 0, st, rowptr, rev, E3, (const float*)p.LB,
                            (const float*)p.LC, N, p.pa, p.pb, p.pc);
-        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
                            (const int*)p.sp_atoms, (const float*)p.pa, E3, nsp, Gp(blk(t, "P3a")));
-        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
                            (const int*)p.sp_atoms, (const float*)p.pb, E3, nsp, Gp(blk(t, "P3b")));
-        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(64), 0, st, (const int*)p.sp_off,
+        hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
                            (const int*)p.sp_atoms, (const float*)p.pc, E3, nsp, Gp(blk(t, "P3c")));
       }
     }
@@ -1058,7 +1058,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   if (ss.err != hipSuccess) return janus_set_hip_error(ss.err);
   {
     PROF(PROF_OTHER, 0, 8.0 * Nd);
-    hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), dim3(256), 0, st, (const int*)p.sp_off,
+    hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
                        (const int*)p.sp_atoms, (const float*)HV(p.hh, 0), d, nsp, Gp("A"));
     if (cfg.n_tasks) {
       // per-structure sums of dL/dh0, then per label value and per species (composition)

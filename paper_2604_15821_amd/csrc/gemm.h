@@ -572,76 +572,109 @@ __global__ __launch_bounds__(256, 2) void gemm_wgrad_kernel(ALoad al, BLoad bl, 
 }
 
 // ---------------------------------------------------------- skinny wgrad
-// G[p, q] = sum_r s[r] A[r, p] B[r, q] for a short P (P * Q <= 16384, the
+// G[p, q] = sum_r s[r] A[r, p] B[r, q] for a short P (P <= 32, Q <= 512; the
 // radial-filter gradient: P = basis size, Q = d).  A 128-row MFMA tile would
 // be mostly padding there, so the vector units do it: a workgroup owns one
-// chunk of rows and the whole P x Q output, thread t the float4 outputs
-// t + 256 j; rows pass through LDS 16 at a time.  Partials per chunk, reduced
+// chunk of rows and the whole P x Q output; thread t owns output column
+// float4 q4 = t % (Q / 4) of the rows p = g np .. min(g np + np, P) - 1,
+// g = t / (Q / 4), np = ceil(P / (256 / (Q / 4))) <= NO, so each staged B
+// float4 is read once per thread and row.  Rows pass through LDS R = 8192 / Q
+// at a time (R (P + Q) floats of dynamic LDS, at most 48 KB), the next R rows
+// being loaded into registers while the current ones are used; a chunk takes
+// only a few passes, since every workgroup of the grid is resident at once and
+// each pass waits for one round trip to memory.  Partials per chunk, reduced
 // like gemm_wgrad's.  s may be null (s = 1).
-constexpr int kSkinnyRows = 16;
+constexpr int kSkinnyBLoads = 8;   // B float4 per thread and pass: R Q / 4 / 256 = 8
+constexpr int kSkinnyALoads = 4;   // A float4 per thread and pass: R P / 4 / 256 <= 8192 * 32 / (Q 1024) <= 4
+inline int skinny_rows(int Q) { return 8192 / Q; }
 
 template <int NO>
 __global__ __launch_bounds__(256) void wgrad_skinny_kernel(const float* __restrict__ A, const float* __restrict__ s,
                                                            const float* __restrict__ B, int P, int Q,
                                                            const WChunk* __restrict__ chunks,
-                                                           const int* __restrict__ n_chunks,
+                                                           const int* __restrict__ n_chunks, int np,
                                                            float* __restrict__ partial) {
-  __shared__ __attribute__((aligned(16))) float a_s[kSkinnyRows * 32];
-  __shared__ __attribute__((aligned(16))) float b_s[kSkinnyRows * 512];
+  extern __shared__ __attribute__((aligned(16))) float sk_lds[];
+  const int R = 8192 / Q;
+  float* a_s = sk_lds;             // [R][P]
+  float* b_s = sk_lds + R * P;     // [R][Q]
   const int c = blockIdx.x;
   if (c >= *n_chunks) return;
   const WChunk ch = chunks[c];
   const int tid = threadIdx.x;
-  const int q4n = Q >> 2, p4n = P >> 2, n_out = P * q4n;
+  const int q4n = Q >> 2, p4n = P >> 2;
+  const int na = R * p4n, nbq = R * q4n;                          // float4 per pass
+  const int q4 = tid % q4n, p0 = (tid / q4n) * np;               // p0 >= P: idle thread
+  const int nown = P - p0 < np ? P - p0 : np;                     // rows of this thread
   float4 acc[NO];
-  int pj[NO], qj[NO];
 #pragma unroll
-  for (int j = 0; j < NO; ++j) {
-    acc[j] = f4zero();
-    const int o = tid + 256 * j;
-    pj[j] = o < n_out ? o / q4n : 0;
-    qj[j] = o < n_out ? o % q4n : 0;
-  }
-  for (int r0 = ch.r0; r0 < ch.r1; r0 += kSkinnyRows) {
-    // stage rows r0 .. r0 + 15 (zeros past the chunk)
-    for (int i = tid; i < kSkinnyRows * p4n; i += 256) {
-      const int rr = i / p4n, k4 = i - rr * p4n;
-      const long long r = (long long)r0 + rr;
-      float4 v = f4zero();
-      if (r < ch.r1) {
-        v = ld4(A + r * P + 4 * k4);
-        if (s) {
-          const float w = s[r];
-          v = make_float4(w * v.x, w * v.y, w * v.z, w * v.w);
+  for (int j = 0; j < NO; ++j) acc[j] = f4zero();
+  float4 ra[kSkinnyALoads], rb[kSkinnyBLoads];
+  auto load = [&](int r0) {
+#pragma unroll
+    for (int i = 0; i < kSkinnyALoads; ++i) {
+      const int q = tid + 256 * i;
+      if (q < na) {
+        const int rr = q / p4n, k4 = q - rr * p4n;
+        const long long r = (long long)r0 + rr;
+        float4 v = f4zero();
+        if (r < ch.r1) {
+          v = ld4(A + r * P + 4 * k4);
+          if (s) {
+            const float w = s[r];
+            v = make_float4(w * v.x, w * v.y, w * v.z, w * v.w);
+          }
+        }
+        ra[i] = v;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kSkinnyBLoads; ++i) {
+      const int q = tid + 256 * i;
+      if (q < nbq) {
+        const int rr = q / q4n, k4 = q - rr * q4n;
+        const long long r = (long long)r0 + rr;
+        rb[i] = r < ch.r1 ? ld4(B + r * Q + 4 * k4) : f4zero();
+      }
+    }
+  };
+  load(ch.r0);
+  for (int r0 = ch.r0; r0 < ch.r1; r0 += R) {
+#pragma unroll
+    for (int i = 0; i < kSkinnyALoads; ++i) {
+      const int q = tid + 256 * i;
+      if (q < na) st4(a_s + 4 * q, ra[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < kSkinnyBLoads; ++i) {
+      const int q = tid + 256 * i;
+      if (q < nbq) st4(b_s + 4 * q, rb[i]);
+    }
+    __syncthreads();
+    if (r0 + R < ch.r1) load(r0 + R);
+    const int nr = ch.r1 - r0 < R ? ch.r1 - r0 : R;
+    if (p0 < P) {
+#pragma unroll 4
+      for (int rr = 0; rr < nr; ++rr) {
+        const float4 b = ld4(b_s + rr * Q + 4 * q4);
+#pragma unroll
+        for (int j = 0; j < NO; ++j) {
+          if (j >= nown) break;
+          const float a = a_s[rr * P + p0 + j];
+          acc[j].x += a * b.x;
+          acc[j].y += a * b.y;
+          acc[j].z += a * b.z;
+          acc[j].w += a * b.w;
         }
       }
-      st4(a_s + rr * P + 4 * k4, v);
-    }
-    for (int i = tid; i < kSkinnyRows * q4n; i += 256) {
-      const int rr = i / q4n, k4 = i - rr * q4n;
-      const long long r = (long long)r0 + rr;
-      st4(b_s + rr * Q + 4 * k4, r < ch.r1 ? ld4(B + r * Q + 4 * k4) : f4zero());
-    }
-    __syncthreads();
-#pragma unroll 4
-    for (int rr = 0; rr < kSkinnyRows; ++rr) {
-#pragma unroll
-      for (int j = 0; j < NO; ++j) {
-        const float a = a_s[rr * P + pj[j]];
-        const float4 b = ld4(b_s + rr * Q + 4 * qj[j]);
-        acc[j].x += a * b.x;
-        acc[j].y += a * b.y;
-        acc[j].z += a * b.z;
-        acc[j].w += a * b.w;
-      }
     }
     __syncthreads();
   }
-  float4* out = reinterpret_cast<float4*>(partial + (long long)c * P * Q);
+  if (p0 < P) {
+    float4* out = reinterpret_cast<float4*>(partial + (long long)c * P * Q);
 #pragma unroll
-  for (int j = 0; j < NO; ++j) {
-    const int o = tid + 256 * j;
-    if (o < n_out) out[o] = acc[j];
+    for (int j = 0; j < NO; ++j)
+      if (j < nown) out[(long long)(p0 + j) * q4n + q4] = acc[j];
   }
 }
 

@@ -156,24 +156,27 @@ void launch_wgrad(hipStream_t st, const ALoad& al, const BLoad& bl, int P, int Q
   launch_wgrad_reduce(st, partial, chunk_first, groups, (long long)P * Q, G, accumulate);
 }
 
-// Skinny weight gradient (P * Q <= 16384, P and Q multiples of 4, one group):
+// Skinny weight gradient (P <= 32, Q <= 512, P and Q multiples of 4, one group):
 // G (+)= (s * A)^T B over the chunks of the table.
 inline void launch_wgrad_skinny(hipStream_t st, const float* A, const float* s, const float* B, int P, int Q,
                                 const WChunk* chunks, const int* n_chunks, const int* chunk_first, int max_chunks,
                                 float* partial, float* G, int accumulate) {
   if (max_chunks > 0) {
-    const int no = (P * Q / 4 + 255) / 256;
+    // output rows per thread: P over the 256 / (Q / 4) thread groups
+    const int groups = 256 / (Q / 4);
+    const int no = (P + groups - 1) / groups;
     const dim3 grid(max_chunks), blk(256);
+    const size_t lds = sizeof(float) * skinny_rows(Q) * (P + Q);
     if (no <= 1)
-      hipLaunchKernelGGL(wgrad_skinny_kernel<1>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+      hipLaunchKernelGGL(wgrad_skinny_kernel<1>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
     else if (no <= 2)
-      hipLaunchKernelGGL(wgrad_skinny_kernel<2>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+      hipLaunchKernelGGL(wgrad_skinny_kernel<2>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
     else if (no <= 4)
-      hipLaunchKernelGGL(wgrad_skinny_kernel<4>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+      hipLaunchKernelGGL(wgrad_skinny_kernel<4>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
     else if (no <= 8)
-      hipLaunchKernelGGL(wgrad_skinny_kernel<8>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+      hipLaunchKernelGGL(wgrad_skinny_kernel<8>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
     else
-      hipLaunchKernelGGL(wgrad_skinny_kernel<16>, grid, blk, 0, st, A, s, B, P, Q, chunks, n_chunks, partial);
+      hipLaunchKernelGGL(wgrad_skinny_kernel<16>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
   }
   launch_wgrad_reduce(st, partial, chunk_first, 1, (long long)P * Q, G, accumulate);
 }

@@ -93,26 +93,34 @@ __global__ void energy_kernel(const float* __restrict__ eps, const int* __restri
 __global__ void force_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev,
                              const float* __restrict__ rbar, const float4* __restrict__ geo,
                              const float4* __restrict__ gvec, int N, float* __restrict__ F) {
-  const int a = blockIdx.x * blockDim.x + threadIdx.x;
-  if (a >= N) return;
-  double fx = 0, fy = 0, fz = 0;
-  for (int e = rowptr[a]; e < rowptr[a + 1]; ++e) {
-    const int er = rev[e];
-    const float4 u = geo[e], ur = geo[er];
-    const double g = rbar[e], gr = rbar[er];
-    fx += g * u.x - gr * ur.x;
-    fy += g * u.y - gr * ur.y;
-    fz += g * u.z - gr * ur.z;
-    if (gvec) {
-      const float4 v = gvec[e], vr = gvec[er];
-      fx += (double)v.x - vr.x;
-      fy += (double)v.y - vr.y;
-      fz += (double)v.z - vr.z;
+  // one wave per atom: lane l sums the edges l, l + 64, ... of the atom in
+  // order, then the lanes are added in a fixed butterfly (float64 throughout)
+  JANUS_WAVE_LOOP(a, N) {
+    double fx = 0, fy = 0, fz = 0;
+    const int e1 = rowptr[a + 1];
+    for (int e = rowptr[a] + l; e < e1; e += kWave) {
+      const int er = rev[e];
+      const float4 u = geo[e], ur = geo[er];
+      const double g = rbar[e], gr = rbar[er];
+      fx += g * u.x - gr * ur.x;
+      fy += g * u.y - gr * ur.y;
+      fz += g * u.z - gr * ur.z;
+      if (gvec) {
+        const float4 v = gvec[e], vr = gvec[er];
+        fx += (double)v.x - vr.x;
+        fy += (double)v.y - vr.y;
+        fz += (double)v.z - vr.z;
+      }
+    }
+    fx = wave_sum_d(fx);
+    fy = wave_sum_d(fy);
+    fz = wave_sum_d(fz);
+    if (l == 0) {
+      F[3 * a] = (float)fx;
+      F[3 * a + 1] = (float)fy;
+      F[3 * a + 2] = (float)fz;
     }
   }
-  F[3 * a] = (float)fx;
-  F[3 * a + 1] = (float)fy;
-  F[3 * a + 2] = (float)fz;
 }
 
 // |det| of the lattice rows of one structure (its volume).
@@ -291,8 +299,8 @@ __global__ void readout_bwd_kernel(const float* __restrict__ z, const float* __r
   }
 }
 
-// Column sums in two fixed-order stages.
-constexpr int kColChunk = 256;
+// Column sums in two fixed-order stages (chunks of 64 rows, then the chunks).
+constexpr int kColChunk = 64;
 __global__ void colsum_partial_kernel(const float* __restrict__ M, long long rows, int cols,
                                       float* __restrict__ part) {
   const int c = blockIdx.x * blockDim.x + threadIdx.x;
@@ -343,32 +351,74 @@ __global__ void edge_logit_kernel(const int* __restrict__ pair, const float* __r
   lt[g] = p[x] * (pt - s);
 }
 
-// Per atom i and expert x (one thread each): partC = sum over the edges out
-// of i of lt, partN = sum over the edges into i (through rev), in segment order.
+// Per atom i and expert x: partC = sum over the edges out of i of lt, partN =
+// sum over the edges into i (through rev).  One wave per atom; lane l covers
+// expert l % E of the edges l / E, l / E + 64 / E, ... (in order), and the
+// 64 / E edge slots of an expert are added in slot order.  E <= 64.
 __global__ void router_atom_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev, int E,
                                    const float* __restrict__ lt, int N, float* __restrict__ partC,
                                    float* __restrict__ partN) {
-  const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= (long long)N * E) return;
-  const int i = (int)(g / E), x = (int)(g - (long long)i * E);
-  float ac = 0.f, an = 0.f;
-  for (int e = rowptr[i]; e < rowptr[i + 1]; ++e) {
-    ac += lt[(long long)e * E + x];
-    an += lt[(long long)rev[e] * E + x];
+  __shared__ float red[2][256];
+  const int slots = kWave / E;
+  const int w = threadIdx.x >> 6;
+  JANUS_WAVE_LOOP(i, N) {
+    const int x = l % E, j = l / E;
+    float ac = 0.f, an = 0.f;
+    if (j < slots) {
+      const int e1 = rowptr[i + 1];
+      for (int e = rowptr[i] + j; e < e1; e += slots) {
+        ac += lt[(long long)e * E + x];
+        an += lt[(long long)rev[e] * E + x];
+      }
+    }
+    red[0][threadIdx.x] = ac;
+    red[1][threadIdx.x] = an;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (l < E) {
+      float sc = 0.f, sn = 0.f;
+      for (int q = 0; q < slots; ++q) {
+        sc += red[0][64 * w + q * E + l];
+        sn += red[1][64 * w + q * E + l];
+      }
+      partC[i * E + l] = sc;
+      partN[i * E + l] = sn;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  partC[g] = ac;
-  partN[g] = an;
 }
 
-// out[s] = sum over the atoms of species s (in atom order) of rows of M [N, w]; w <= 64 * VPLW.
+// out[s] += sum over the atoms of species s of rows of M [N, w].  A workgroup
+// of 256 threads per species: per pass over min(w, 256) columns, thread t takes
+// column t % cols and the atoms g, g + G, ... of the species (g = t / cols,
+// G = 256 / cols groups, in atom order); the G group sums of a column are then
+// added in group order.
 __global__ void species_rows_kernel(const int* __restrict__ sp_off, const int* __restrict__ sp_atoms,
                                     const float* __restrict__ M, int w, int nsp, float* __restrict__ out) {
+  __shared__ float red[256];
   const int s = blockIdx.x;
   if (s >= nsp) return;
-  for (int c = threadIdx.x; c < w; c += blockDim.x) {
+  const int t = threadIdx.x;
+  const int q0 = sp_off[s], q1 = sp_off[s + 1];
+  const int cols = w < 256 ? w : 256;
+  const int G = 256 / cols;
+  const int cl = t % cols, g = t / cols;
+  for (int c0 = 0; c0 < w; c0 += cols) {
+    const int c = c0 + cl;
     float acc = 0.f;
-    for (int q = sp_off[s]; q < sp_off[s + 1]; ++q) acc += M[(long long)sp_atoms[q] * w + c];
-    out[(long long)s * w + c] += acc;
+    if (g < G && c < w)
+      for (int q = q0 + g; q < q1; q += G) acc += M[(long long)sp_atoms[q] * w + c];
+    red[t] = acc;
+    __syncthreads();
+    if (g == 0 && c < w) {
+      float tot = 0.f;
+      for (int j = 0; j < G; ++j) tot += red[j * cols + cl];
+      out[(long long)s * w + c] += tot;
+    }
+    __syncthreads();
   }
 }
 
