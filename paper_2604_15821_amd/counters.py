@@ -44,13 +44,15 @@ def family(kernel_name: str) -> str:
     n = kernel_name
     if "gemm_rows_kernel" in n:
         return "dense_gemm" if "EpiDense" in n else "expert_gemm"
+    if "wgrad_skinny" in n:
+        return "dense_gemm"
     if "gemm_wgrad_kernel" in n or "wgrad_reduce" in n:
         return "wgrad"
     if re.search(r"(dispatch_x|edge_p[234]|tri_(dispatch|p[234]|combine|gather|combine_p3))_kernel", n):
         return "edge"
     if re.search(r"(combine_fwd|gather_atom|scatter_rev|combine_p3)_kernel", n):
         return "atom"
-    if re.search(r"attn_(fwd|bwd|tan|rev)_kernel", n):
+    if re.search(r"attn_(fwd|bwd|tan|rev)(_mfma)?_kernel", n):
         return "attention"
     if "elementwise_kernel" in n or "vectorized" in n:
         return "copy"
