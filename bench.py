@@ -56,14 +56,18 @@ def cpu_baseline(workload: str, n_struct: int):
                       f"{dt:.1f} s; float64 NumPy, BLAS threads {blas}, affinity {aff}"}
 
 
+# Sources that define the expert GEMM kernels, their operand loaders and epilogues,
+# and their launch configuration: the counter record of that family is valid only for these.
+EXPERT_GEMM_SOURCES = ("common.h", "gemm.h", "internal.h")
+
+
 def kernel_sources_sha256() -> str:
-    """Hash of the library's kernel sources: measured counters are valid only for these."""
+    """Hash of the expert GEMM kernels' sources: measured counters are valid only for these."""
     import hashlib
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
-        if name.endswith((".h", ".hip")):
-            with open(os.path.join(CSRC, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in EXPERT_GEMM_SOURCES:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
 
 

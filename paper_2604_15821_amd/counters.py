@@ -136,7 +136,8 @@ def summarize(workload: str, runs: str) -> str:
         L += ["", "Algorithmic bytes per expert-GEMM launch (average over the 8 products of a block):",
               f"read {ar / 1e6:.0f} MB, write {aw / 1e6:.0f} MB; measured read / algorithmic = "
               f"{rec['fetch_bytes_per_launch'] / ar:.2f}, write = {rec['write_bytes_per_launch'] / aw:.2f}."]
-    L += ["", "Machine-readable record read by bench.py (valid while the kernel sources hash to `sources_sha256`):", "",
+    L += ["", "Machine-readable record read by bench.py (valid while the sources of the expert GEMM kernels, "
+          "`csrc/common.h`, `csrc/gemm.h` and `csrc/internal.h`, hash to `sources_sha256`):", "",
           "traffic-json: " + json.dumps(rec)]
     return "\n".join(L) + "\n"
 
