@@ -176,11 +176,12 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_kernel(
 //   qb_e = sum_l zb_el k_l / sqrt(32),  kb_l = sum_e zb_el q_e / sqrt(32),
 //   vb_l = (sum_e u_e p_el) ob,
 //   dE/dr_e += u'(r_e) [cw_e (query weight) + sum_j u_j exp(s_je - M_j)/Z_j (w_e - cw_j) (key weight)]
-// summed over heads.  QKVb [Ne, 3d] gets (qb | kb | vb).
+// summed over heads.  QKVb [Ne, 3d] gets (qb | kb | vb).  Atoms with at most min_n
+// edges are skipped (the matrix-core kernel takes them).
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu,
     const float* __restrict__ ud, const float* __restrict__ stats, const float* __restrict__ ob, int N, int d, int H,
-    float* __restrict__ QKVb, float* __restrict__ rbar) {
+    float* __restrict__ QKVb, float* __restrict__ rbar, int min_n) {
   __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
   __shared__ float s_sc[kAttnWaves][3][kAttnChunk];
   __shared__ float s_cw[kAttnWaves][kAttnMaxN];
@@ -194,6 +195,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_kernel(
   float* rb = s_rb[wv];
   const long long ld = 3LL * d;
   JANUS_WAVE_LOOP(i, N) {
+    if (rowptr[i + 1] - rowptr[i] <= min_n) continue;
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
     wave_sync();
     for (int j = l; j < n; j += 64) rb[j] = 0.f;
@@ -378,12 +380,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_kernel(
 //   zhb_el = u_e p (b_l - bm)                                            (adjoint of sh_el)
 //   qb_e = sum_l (zb k_l + zhb kh_l)/sqrt(32),  kb_l = sum_e (zb q_e + zhb qh_e)/sqrt(32),
 //   vb_l = alpha sum_e u_e p + beta sum_e (uh_e p + u_e (pz - p zm)).
-// QKVa [Ne, 3d] gets (qb | kb | vb), the adjoints of the primal q, k, v.
+// QKVa [Ne, 3d] gets (qb | kb | vb), the adjoints of the primal q, k, v.  Atoms with at
+// most min_n edges are skipped (the matrix-core kernel takes them).
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
     const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
-    int H, float* __restrict__ QKVa) {
+    int H, float* __restrict__ QKVa, int min_n) {
   __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
   __shared__ float s_ch[kAttnWaves][4][kAttnChunk];
   __shared__ float s_sc[kAttnWaves][6][kAttnMaxN];
@@ -400,6 +403,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
   float* sp_ = s_sc[wv][4];
   const long long ld = 3LL * d;
   JANUS_WAVE_LOOP(i, N) {
+    if (rowptr[i + 1] - rowptr[i] <= min_n) continue;
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
     for (int a = 0; a < H; ++a) {
       const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
@@ -865,6 +869,494 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_mfma_kernel(
     if (j4 == 0) {
       osumh[(long long)i * d + cq + i16] = col0;
       osumh[(long long)i * d + cq + 16 + i16] = col1;
+    }
+  }
+}
+
+// Phase 2 on matrix cores for the atoms whose neighbourhood spans NT 16-row tiles, one
+// wave per (atom, head); same outputs as attn_bwd_kernel except that the envelope
+// terms of dE/dr go to rbh [(e H + a)] (query term cw_e plus key term kl_e of head a)
+// and attn_rbar_kernel adds them to rbar.  Transposed score tiles (key x query) give
+// p, cw and zb = u_q p (w_k - cw_q) in the A-operand layout of qb = zb k; score tiles
+// the other way round (query x key) give zb in the layout of kb = zb^T q, and the
+// per-key sums Pu = sum_q u_q p (vb = Pu ob) and kl = sum_q u_q E (w_k - cw_q).
+template <int NT>
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu,
+    const float* __restrict__ stats, const float* __restrict__ ob, int N, int d, int H, float* __restrict__ QKVb,
+    float* __restrict__ rbh) {
+  const long long ld = 3LL * d;
+  const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
+  JANUS_WAVE_LOOP(item, (long long)N * H) {
+    const int i = (int)(item / H), a = (int)(item - (long long)i * H);
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n == 0 || (n + 15) >> 4 != NT) continue;
+    const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    float qf[NT][8], kf[NT][8];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      frag8(QKV, ld, e0, n, t * 16 + i16, cq + 8 * j4, qf[t]);
+      frag8(QKV, ld, e0, n, t * 16 + i16, ck + 8 * j4, kf[t]);
+    }
+    // ob columns 8 j4 .. 8 j4 + 7 and w_k = ob . v_k for the rows t*16 + i16 (every j4 lane)
+    float obf[8];
+    {
+      const float* po = ob + (long long)i * d + cq + 8 * j4;
+      const float4 x = *reinterpret_cast<const float4*>(po), y = *reinterpret_cast<const float4*>(po + 4);
+      obf[0] = x.x; obf[1] = x.y; obf[2] = x.z; obf[3] = x.w;
+      obf[4] = y.x; obf[5] = y.y; obf[6] = y.z; obf[7] = y.w;
+    }
+    float wrow[NT], urow[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      float vf[8];
+      frag8(QKV, ld, e0, n, t * 16 + i16, cv + 8 * j4, vf);
+      float s = 0.f;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) s += obf[c] * vf[c];
+      wrow[t] = sum_j4(s);
+      const int row = t * 16 + i16;
+      urow[t] = row < n ? uu[e0 + row] : 0.f;
+    }
+    // ---- transposed tiles: lane holds (key kt*16 + 4 j4 + r, query qt*16 + i16)
+    float cw[NT];
+    {
+      f32x4v S[NT][NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int u = 0; u < NT; ++u) S[t][u] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt) S[kt][qt] = mfma16(kf[kt][st], qf[qt][st], S[kt][qt]);
+      float uk[NT][4], wk[NT][4];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          uk[t][r] = __shfl(urow[t], 4 * j4 + r, 64);   // u of key t*16 + 4 j4 + r
+          wk[t][r] = __shfl(wrow[t], 4 * j4 + r, 64);
+        }
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt) {
+        const int q = qt * 16 + i16;
+        const long long sq = ((long long)(e0 + (q < n ? q : n - 1)) * H + a) * 2;
+        const float M = stats[sq], iZ = 1.f / stats[sq + 1];
+        float c = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float p = uk[kt][r] * __expf(S[kt][qt][r] * kAttnScale - M) * iZ;
+            S[kt][qt][r] = p;
+            c += p * wk[kt][r];
+          }
+        cw[qt] = sum_j4(c);
+        // zb = u_q p (w_k - cw_q), in place
+        const float uq = urow[qt];
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) S[kt][qt][r] = uq * S[kt][qt][r] * (wk[kt][r] - cw[qt]);
+      }
+      // qb = (1/sqrt 32) zb k: lane holds (query qt*16 + 4 j4 + r, column ct*16 + i16)
+      f32x4v QB[NT][2];
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt) QB[qt][0] = QB[qt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          const long long row = (long long)(e0 + (key < n ? key : n - 1)) * ld;
+          const float k0 = QKV[row + ck + i16], k1 = QKV[row + ck + 16 + i16];
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt) {
+            QB[qt][0] = mfma16(S[kt][qt][r], k0, QB[qt][0]);
+            QB[qt][1] = mfma16(S[kt][qt][r], k1, QB[qt][1]);
+          }
+        }
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = qt * 16 + 4 * j4 + r;
+          if (q < n) {
+            float* o = QKVb + (long long)(e0 + q) * ld + cq;
+            o[i16] = kAttnScale * QB[qt][0][r];
+            o[16 + i16] = kAttnScale * QB[qt][1][r];
+          }
+        }
+    }
+    // ---- tiles the other way round: lane holds (query qt*16 + 4 j4 + r, key kt*16 + i16)
+    {
+      f32x4v S2[NT][NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int u = 0; u < NT; ++u) S2[t][u] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+          for (int kt = 0; kt < NT; ++kt) S2[qt][kt] = mfma16(qf[qt][st], kf[kt][st], S2[qt][kt]);
+      float pu[NT], kl[NT];
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt) pu[kt] = kl[kt] = 0.f;
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = qt * 16 + 4 * j4 + r;
+          const long long sq = ((long long)(e0 + (q < n ? q : n - 1)) * H + a) * 2;
+          const float M = stats[sq], iZ = 1.f / stats[sq + 1];
+          const float uq = __shfl(urow[qt], 4 * j4 + r, 64);
+          const float cq_ = __shfl(cw[qt], 4 * j4 + r, 64);
+#pragma unroll
+          for (int kt = 0; kt < NT; ++kt) {
+            const float E = __expf(S2[qt][kt][r] * kAttnScale - M) * iZ;
+            const float t = uq * E * (wrow[kt] - cq_);
+            kl[kt] += t;
+            pu[kt] += uq * urow[kt] * E;
+            S2[qt][kt][r] = urow[kt] * t;   // zb (key kt*16 + i16, query q)
+          }
+        }
+      // kb = (1/sqrt 32) zb^T q: lane holds (key kt*16 + 4 j4 + r, column ct*16 + i16)
+      f32x4v KB[NT][2];
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt) KB[kt][0] = KB[kt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = qt * 16 + 4 * j4 + r;
+          const long long row = (long long)(e0 + (q < n ? q : n - 1)) * ld;
+          const float x0 = QKV[row + cq + i16], x1 = QKV[row + cq + 16 + i16];
+#pragma unroll
+          for (int kt = 0; kt < NT; ++kt) {
+            KB[kt][0] = mfma16(S2[qt][kt][r], x0, KB[kt][0]);
+            KB[kt][1] = mfma16(S2[qt][kt][r], x1, KB[kt][1]);
+          }
+        }
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          if (key < n) {
+            float* o = QKVb + (long long)(e0 + key) * ld + ck;
+            o[i16] = kAttnScale * KB[kt][0][r];
+            o[16 + i16] = kAttnScale * KB[kt][1][r];
+          }
+        }
+      // vb = Pu ob (columns 8 j4 .. 8 j4 + 7 of key kt*16 + i16); envelope terms of the edge
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt) {
+        const float P = sum_j4(pu[kt]);
+        const float K = sum_j4(kl[kt]);
+        const int key = kt * 16 + i16;
+        if (key < n) {
+          float* o = QKVb + (long long)(e0 + key) * ld + cv + 8 * j4;
+          *reinterpret_cast<float4*>(o) = make_float4(P * obf[0], P * obf[1], P * obf[2], P * obf[3]);
+          *reinterpret_cast<float4*>(o + 4) = make_float4(P * obf[4], P * obf[5], P * obf[6], P * obf[7]);
+          if (j4 == 0) rbh[(long long)(e0 + key) * H + a] = cw[kt] + K;
+        }
+      }
+    }
+  }
+}
+
+// Phase 4 on matrix cores for the atoms whose neighbourhood spans NT 16-row tiles, one
+// wave per (atom, head); same output as attn_rev_kernel.  Per row t*16 + i16 (every j4
+// lane): u, uh = u' rt, a = alpha.v + beta.vh and b = beta.v (8-column partial dots
+// added over the four lane groups), the query's softmax statistics.  Transposed tiles
+// (key x query) of s and sh give the per-query sums am, bm, zm, pbz and SP, then zb and
+// zhb in the A-operand layout of qb = zb k + zhb kh; tiles the other way round
+// (query x key) give zb, zhb in the layout of kb = zb^T q + zhb^T qh and the per-key
+// sums S1 = sum u_q p, S2 = sum uh_q p + u_q (pz - p zm) of vb = S1 alpha + S2 beta.
+template <int NT>
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
+    const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
+    const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
+    int H, float* __restrict__ QKVa) {
+  const long long ld = 3LL * d;
+  const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
+  JANUS_WAVE_LOOP(item, (long long)N * H) {
+    const int i = (int)(item / H), a = (int)(item - (long long)i * H);
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n == 0 || (n + 15) >> 4 != NT) continue;
+    const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    float alf[8], bef[8];
+    {
+      const float* pa = alpha + (long long)i * d + cq + 8 * j4;
+      const float* pb = beta + (long long)i * d + cq + 8 * j4;
+#pragma unroll
+      for (int c = 0; c < 8; c += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(pa + c), y = *reinterpret_cast<const float4*>(pb + c);
+        alf[c] = x.x; alf[c + 1] = x.y; alf[c + 2] = x.z; alf[c + 3] = x.w;
+        bef[c] = y.x; bef[c + 1] = y.y; bef[c + 2] = y.z; bef[c + 3] = y.w;
+      }
+    }
+    // per row t*16 + i16
+    float urow[NT], uhrow[NT], arow[NT], brow[NT], mrow[NT], izrow[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      float vf[8], wf[8];
+      frag8(QKV, ld, e0, n, t * 16 + i16, cv + 8 * j4, vf);
+      frag8(QKVh, ld, e0, n, t * 16 + i16, cv + 8 * j4, wf);
+      float sa = 0.f, sb = 0.f;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        sa += alf[c] * vf[c] + bef[c] * wf[c];
+        sb += bef[c] * vf[c];
+      }
+      arow[t] = sum_j4(sa);
+      brow[t] = sum_j4(sb);
+      const int row = t * 16 + i16;
+      const int rr = row < n ? row : n - 1;
+      urow[t] = row < n ? uu[e0 + rr] : 0.f;
+      uhrow[t] = row < n ? ud[e0 + rr] * rt[e0 + rr] : 0.f;
+      const long long sq = ((long long)(e0 + rr) * H + a) * 2;
+      mrow[t] = stats[sq];
+      izrow[t] = 1.f / stats[sq + 1];
+    }
+    float bmq[NT], zmq[NT], spq[NT];   // per query t*16 + i16
+    // ---- transposed tiles: lane holds (key kt*16 + 4 j4 + r, query qt*16 + i16)
+    {
+      f32x4v S[NT][NT], Sh[NT][NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int u = 0; u < NT; ++u) S[t][u] = Sh[t][u] = f32x4v{0.f, 0.f, 0.f, 0.f};
+      {
+        float qf[NT][8], kf[NT][8], hf[NT][8];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          frag8(QKV, ld, e0, n, t * 16 + i16, cq + 8 * j4, qf[t]);
+          frag8(QKV, ld, e0, n, t * 16 + i16, ck + 8 * j4, kf[t]);
+        }
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+#pragma unroll
+          for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+            for (int qt = 0; qt < NT; ++qt) S[kt][qt] = mfma16(kf[kt][st], qf[qt][st], S[kt][qt]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) frag8(QKVh, ld, e0, n, t * 16 + i16, cq + 8 * j4, hf[t]);   // qh
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+#pragma unroll
+          for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+            for (int qt = 0; qt < NT; ++qt) Sh[kt][qt] = mfma16(kf[kt][st], hf[qt][st], Sh[kt][qt]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) frag8(QKVh, ld, e0, n, t * 16 + i16, ck + 8 * j4, hf[t]);   // kh
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+#pragma unroll
+          for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+            for (int qt = 0; qt < NT; ++qt) Sh[kt][qt] = mfma16(hf[kt][st], qf[qt][st], Sh[kt][qt]);
+      }
+      // p into S, pz into Sh; per-query sums
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt) {
+        float am = 0.f, bm = 0.f, zm = 0.f, pbz = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int src = 4 * j4 + r;
+            const float uk = __shfl(urow[kt], src, 64), uhk = __shfl(uhrow[kt], src, 64);
+            const float ak = __shfl(arow[kt], src, 64), bk = __shfl(brow[kt], src, 64);
+            const float E = __expf(S[kt][qt][r] * kAttnScale - mrow[qt]) * izrow[qt];
+            const float p = uk * E;
+            const float pz = p * Sh[kt][qt][r] * kAttnScale + uhk * E;
+            S[kt][qt][r] = p;
+            Sh[kt][qt][r] = pz;
+            am += p * ak;
+            bm += p * bk;
+            zm += pz;
+            pbz += pz * bk;
+          }
+        am = sum_j4(am);
+        bm = sum_j4(bm);
+        zm = sum_j4(zm);
+        pbz = sum_j4(pbz);
+        const float ue = urow[qt], uh = uhrow[qt];
+        const float SP = ue * (am + pbz - 2.f * zm * bm) + uh * bm;
+        bmq[qt] = bm;
+        zmq[qt] = zm;
+        spq[qt] = SP;
+        // zb into S, zhb into Sh
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int src = 4 * j4 + r;
+            const float ak = __shfl(arow[kt], src, 64), bk = __shfl(brow[kt], src, 64);
+            const float p = S[kt][qt][r], pz = Sh[kt][qt][r];
+            S[kt][qt][r] = ue * (p * ak + bk * (pz - p * zm) - pz * bm) + uh * p * bk - p * SP;
+            Sh[kt][qt][r] = ue * p * (bk - bm);
+          }
+      }
+      // qb = (1/sqrt 32)(zb k + zhb kh): lane holds (query qt*16 + 4 j4 + r, column ct*16 + i16)
+      f32x4v QB[NT][2];
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt) QB[qt][0] = QB[qt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          const long long row = (long long)(e0 + (key < n ? key : n - 1)) * ld;
+          const float k0 = QKV[row + ck + i16], k1 = QKV[row + ck + 16 + i16];
+          const float h0 = QKVh[row + ck + i16], h1 = QKVh[row + ck + 16 + i16];
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt) {
+            QB[qt][0] = mfma16(S[kt][qt][r], k0, QB[qt][0]);
+            QB[qt][1] = mfma16(S[kt][qt][r], k1, QB[qt][1]);
+            QB[qt][0] = mfma16(Sh[kt][qt][r], h0, QB[qt][0]);
+            QB[qt][1] = mfma16(Sh[kt][qt][r], h1, QB[qt][1]);
+          }
+        }
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = qt * 16 + 4 * j4 + r;
+          if (q < n) {
+            float* o = QKVa + (long long)(e0 + q) * ld + cq;
+            o[i16] = kAttnScale * QB[qt][0][r];
+            o[16 + i16] = kAttnScale * QB[qt][1][r];
+          }
+        }
+    }
+    // ---- tiles the other way round: lane holds (query qt*16 + 4 j4 + r, key kt*16 + i16)
+    {
+      f32x4v S[NT][NT], Sh[NT][NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int u = 0; u < NT; ++u) S[t][u] = Sh[t][u] = f32x4v{0.f, 0.f, 0.f, 0.f};
+      {
+        float qf[NT][8], kf[NT][8], hf[NT][8];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          frag8(QKV, ld, e0, n, t * 16 + i16, cq + 8 * j4, qf[t]);
+          frag8(QKV, ld, e0, n, t * 16 + i16, ck + 8 * j4, kf[t]);
+        }
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+            for (int kt = 0; kt < NT; ++kt) S[qt][kt] = mfma16(qf[qt][st], kf[kt][st], S[qt][kt]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) frag8(QKVh, ld, e0, n, t * 16 + i16, cq + 8 * j4, hf[t]);   // qh
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+            for (int kt = 0; kt < NT; ++kt) Sh[qt][kt] = mfma16(hf[qt][st], kf[kt][st], Sh[qt][kt]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) frag8(QKVh, ld, e0, n, t * 16 + i16, ck + 8 * j4, hf[t]);   // kh
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+#pragma unroll
+          for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+            for (int kt = 0; kt < NT; ++kt) Sh[qt][kt] = mfma16(qf[qt][st], hf[kt][st], Sh[qt][kt]);
+      }
+      float s1[NT], s2[NT];
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt) s1[kt] = s2[kt] = 0.f;
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int src = 4 * j4 + r;
+          const float M = __shfl(mrow[qt], src, 64), iZ = __shfl(izrow[qt], src, 64);
+          const float ue = __shfl(urow[qt], src, 64), uh = __shfl(uhrow[qt], src, 64);
+          const float bm = __shfl(bmq[qt], src, 64), zm = __shfl(zmq[qt], src, 64), SP = __shfl(spq[qt], src, 64);
+#pragma unroll
+          for (int kt = 0; kt < NT; ++kt) {
+            const float E = __expf(S[qt][kt][r] * kAttnScale - M) * iZ;
+            const float p = urow[kt] * E;
+            const float pz = p * Sh[qt][kt][r] * kAttnScale + uhrow[kt] * E;
+            const float ak = arow[kt], bk = brow[kt];
+            s1[kt] += ue * p;
+            s2[kt] += uh * p + ue * (pz - p * zm);
+            S[qt][kt][r] = ue * (p * ak + bk * (pz - p * zm) - pz * bm) + uh * p * bk - p * SP;
+            Sh[qt][kt][r] = ue * p * (bk - bm);
+          }
+        }
+      // kb = (1/sqrt 32)(zb^T q + zhb^T qh): lane holds (key kt*16 + 4 j4 + r, column ct*16 + i16)
+      f32x4v KB[NT][2];
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt) KB[kt][0] = KB[kt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int qt = 0; qt < NT; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = qt * 16 + 4 * j4 + r;
+          const long long row = (long long)(e0 + (q < n ? q : n - 1)) * ld;
+          const float x0 = QKV[row + cq + i16], x1 = QKV[row + cq + 16 + i16];
+          const float h0 = QKVh[row + cq + i16], h1 = QKVh[row + cq + 16 + i16];
+#pragma unroll
+          for (int kt = 0; kt < NT; ++kt) {
+            KB[kt][0] = mfma16(S[qt][kt][r], x0, KB[kt][0]);
+            KB[kt][1] = mfma16(S[qt][kt][r], x1, KB[kt][1]);
+            KB[kt][0] = mfma16(Sh[qt][kt][r], h0, KB[kt][0]);
+            KB[kt][1] = mfma16(Sh[qt][kt][r], h1, KB[kt][1]);
+          }
+        }
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          if (key < n) {
+            float* o = QKVa + (long long)(e0 + key) * ld + ck;
+            o[i16] = kAttnScale * KB[kt][0][r];
+            o[16 + i16] = kAttnScale * KB[kt][1][r];
+          }
+        }
+      // vb = S1 alpha + S2 beta (columns 8 j4 .. 8 j4 + 7 of key kt*16 + i16)
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt) {
+        const float A1 = sum_j4(s1[kt]), A2 = sum_j4(s2[kt]);
+        const int key = kt * 16 + i16;
+        if (key < n) {
+          float* o = QKVa + (long long)(e0 + key) * ld + cv + 8 * j4;
+          *reinterpret_cast<float4*>(o) = make_float4(A1 * alf[0] + A2 * bef[0], A1 * alf[1] + A2 * bef[1],
+                                                      A1 * alf[2] + A2 * bef[2], A1 * alf[3] + A2 * bef[3]);
+          *reinterpret_cast<float4*>(o + 4) = make_float4(A1 * alf[4] + A2 * bef[4], A1 * alf[5] + A2 * bef[5],
+                                                          A1 * alf[6] + A2 * bef[6], A1 * alf[7] + A2 * bef[7]);
+        }
+      }
+    }
+  }
+}
+
+// dE/dr of the edges of the atoms the matrix-core phase-2 kernel took (n <= nmax):
+// rbar_e += u'(r_e) sum over heads a (in order) of rbh[e H + a].  One wave per atom.
+__global__ void attn_rbar_kernel(const int* __restrict__ rowptr, const float* __restrict__ ud,
+                                 const float* __restrict__ rbh, int N, int H, int nmax, float* __restrict__ rbar) {
+  JANUS_WAVE_LOOP(i, N) {
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n > nmax) continue;
+    for (int j = l; j < n; j += kWave) {
+      const long long e = e0 + j;
+      float s = 0.f;
+      for (int a = 0; a < H; ++a) s += rbh[e * H + a];
+      rbar[e] += ud[e] * s;
     }
   }
 }

@@ -542,9 +542,20 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_ATTN, 0, by_attn);
+        // neighbourhoods up to kAttnMfmaN edges on matrix cores, larger ones on the vector units
+#define JANUS_BWD_MFMA(NTV)                                                                                    \
+  hipLaunchKernelGGL(attn_bwd_mfma_kernel<NTV>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),                \
+                     (const float*)p.eu, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t), p.rbh)
+        JANUS_BWD_MFMA(1);
+        JANUS_BWD_MFMA(2);
+        JANUS_BWD_MFMA(3);
+        JANUS_BWD_MFMA(4);
+#undef JANUS_BWD_MFMA
+        hipLaunchKernelGGL(attn_rbar_kernel, gN, b256, 0, st, rowptr, (const float*)p.eud, (const float*)p.rbh, N, H,
+                           kAttnMfmaN, p.rbar);
         hipLaunchKernelGGL(attn_bwd_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)p.eu,
                            (const float*)p.eud, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t),
-                           p.rbar);
+                           p.rbar, kAttnMfmaN);
       }
       {
         PROF(PROF_DENSE_GEMM, f_qkv, 0);
@@ -908,9 +919,19 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_ATTN, 0, by_attn);
+        // neighbourhoods up to kAttnMfmaN edges on matrix cores, larger ones on the vector units
+#define JANUS_REV_MFMA(NTV)                                                                                    \
+  hipLaunchKernelGGL(attn_rev_mfma_kernel<NTV>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),                \
+                     (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,         \
+                     (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa)
+        JANUS_REV_MFMA(1);
+        JANUS_REV_MFMA(2);
+        JANUS_REV_MFMA(3);
+        JANUS_REV_MFMA(4);
+#undef JANUS_REV_MFMA
         hipLaunchKernelGGL(attn_rev_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)QKVht(t),
                            (const float*)p.eu, (const float*)p.eud, (const float*)p.rt, (const float*)STt(t),
-                           (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa);
+                           (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa, kAttnMfmaN);
       }
       {
         PROF(PROF_DENSE_GEMM, 3 * f_qkv, 0);

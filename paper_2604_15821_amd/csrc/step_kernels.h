@@ -770,7 +770,7 @@ struct Plan {
   // sums, first-order adjoints, tangents; temporaries; GEMM tables over Ne rows
   float *eu, *eud;
   float *Mm, *QKV, *stats, *osum, *OB, *QKVb, *MB, *Mh, *QKVh;
-  float *AO, *QKVa, *mta, *osh;
+  float *AO, *QKVa, *mta, *osh, *rbh;
   RowsTile* tilesE;
   int* ntE;
   WChunk* chunksA;
@@ -1051,6 +1051,7 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.QKVa = cv.take<float>(E3d);
     p.mta = cv.take<float>(Ed);
     p.osh = cv.take<float>(Nd + 4);
+    p.rbh = cv.take<float>(Ne * p.H + 4);
     p.tilesE = cv.take<RowsTile>(p.mtE);
     p.ntE = cv.take<int>(1);
     p.chunksA = cv.take<WChunk>(p.mcA);
