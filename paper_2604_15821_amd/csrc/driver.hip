@@ -170,6 +170,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   // kernels that stage W_a (up to 64 KB) in LDS: at most 4 workgroups per CU
   // fit, so a larger grid would only reload W_a
   const dim3 gEa(std::min(gE.x, 1024u));
+  // the same with 8 waves per workgroup sharing one copy of W_a, for the triplet kernel
+  // whose registers would allow 8 waves per SIMD (the dispatch of the triplet tokens)
+  const dim3 gEa8(std::min((unsigned)cdiv(std::max<long long>(Ne, 1), 8), 1024u)), b512(512);
 
   // algorithmic work of one launch of each kernel (matrix products: 2 M N K;
   // memory-bound kernels: bytes that must cross HBM once)
@@ -387,7 +390,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       // triplet tokens -> triplet experts -> messages Q_e of each edge's triplets
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * 4.0 * k3 * d);
-        LAUNCH_VPL_K(tri_dispatch_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
+        LAUNCH_VPL_K(tri_dispatch_kernel, d, k3, gEa8, b512, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
                      (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.u3,
                      Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), POS3(t), Ne, d, Z3s(t));
       }
