@@ -98,6 +98,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown-steps", type=int, default=3,
                     help="untimed steps with every kernel family's events, for the per-family table")
+    ap.add_argument("--workspace-mib", type=int, default=0,
+                    help="cap janus_step's workspace (the batch is then processed in chunks of whole structures)")
     ap.add_argument("--concurrent", action="store_true",
                     help="expert weight gradients on a second stream, beside the expert products")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -130,6 +132,8 @@ def main():
     d = janus.upload(b, "cuda:0")
     ctx = janus.Context(m)
     ctx.set_concurrency(args.concurrent)
+    if args.workspace_mib:
+        ctx.set_workspace_limit(args.workspace_mib << 20)
     nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
     Ne = nl.n_edges
     N, S = b.n_atoms, b.n_struct
@@ -174,7 +178,7 @@ def main():
     ctx.profile(False)
     Nt = ctx.last_triplets()
     ms = (t1 - t0) * 1e3 / args.steps
-    log(f"{ms:.3f} ms/step, loss {float(out[0].cpu()[0]):.6g}")
+    log(f"{ms:.3f} ms/step, loss {float(out[0].cpu()[0]):.6g}, {ctx.last_chunks()} chunk(s)")
 
     kernels = {}
     for name, r in breakdown.items():
@@ -223,6 +227,7 @@ def main():
                    "d_hidden": m.d_hidden, "experts": m.n_experts, "top_k": m.top_k, "blocks": m.n_blocks,
                    "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none",
                    "streams": 2 if args.concurrent else 1,
+                   **({"workspace_mib": args.workspace_mib} if args.workspace_mib else {}),
                    **({"atom_moe": {"experts": m.n_experts_f, "top_k": m.top_k_f, "d_hidden": m.d_hidden_f}}
                       if m.atom_moe else {}),
                    **({"stress_weight": m.w_S} if m.w_S else {}),
