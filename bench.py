@@ -100,8 +100,9 @@ def main():
                     help="untimed steps with every kernel family's events, for the per-family table")
     ap.add_argument("--workspace-mib", type=int, default=0,
                     help="cap janus_step's workspace (the batch is then processed in chunks of whole structures)")
-    ap.add_argument("--concurrent", action="store_true",
-                    help="expert weight gradients on a second stream, beside the expert products")
+    ap.add_argument("--serial", action="store_true",
+                    help="one stream only (by default the expert weight gradients run on a second stream, "
+                         "beside the memory-bound edge and atom kernels)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="one elementwise copy kernel over this many MiB before the run (calibrates HBM counters)")
     args = ap.parse_args()
@@ -131,7 +132,7 @@ def main():
     b = make_batch(args.workload)
     d = janus.upload(b, "cuda:0")
     ctx = janus.Context(m)
-    ctx.set_concurrency(args.concurrent)
+    ctx.set_concurrency(not args.serial)
     if args.workspace_mib:
         ctx.set_workspace_limit(args.workspace_mib << 20)
     nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
@@ -226,7 +227,7 @@ def main():
         "config": {"workload": args.workload, "structures": S, "atoms": N, "edges": Ne, "d": m.d,
                    "d_hidden": m.d_hidden, "experts": m.n_experts, "top_k": m.top_k, "blocks": m.n_blocks,
                    "n_rbf": m.n_rbf, "r_cut": m.r_cut, "parallelism": "none",
-                   "streams": 2 if args.concurrent else 1,
+                   "streams": 1 if args.serial else 2,
                    **({"workspace_mib": args.workspace_mib} if args.workspace_mib else {}),
                    **({"atom_moe": {"experts": m.n_experts_f, "top_k": m.top_k_f, "d_hidden": m.d_hidden_f}}
                       if m.atom_moe else {}),

@@ -333,14 +333,15 @@ int64_t janus_last_triplets(const janus_ctx* ctx);
  * stream that the context owns
  * (created on the context's device at the first step, default priority),
  * forked from and joined back into the caller's stream with events inside
- * the call, so they overlap the memory-bound expert products and edge
- * kernels; janus_step's outputs are still complete once the caller's stream
- * has reached the end of the call.  With on = 0 (the default) every kernel
- * runs on the caller's stream.  The two settings compute bitwise identical results
- * (same kernels, same summation order).  Off by default: the overlap shortens
- * the step by about 2% on the 4096-atom small batch, and the expert products
- * then share the GPU, so their per-launch times no longer describe the
- * kernels alone.  Errors: JANUS_EINVAL (on not 0 or 1).
+ * the call.  Each is forked just before memory-bound edge and atom kernels
+ * of the caller's stream, and the caller's stream joins the second stream
+ * before its next matrix product, so two products never run at the same
+ * time; janus_step's outputs are complete once the caller's stream has
+ * reached the end of the call.  With on = 0 (the default) every kernel runs
+ * on the caller's stream.  The two settings compute bitwise identical
+ * results (same kernels, same summation order); on shortens the step of the
+ * 4096-atom small batch by 1-2%.  Errors: JANUS_EINVAL (ctx null, or on not
+ * 0 or 1).
  */
 int janus_set_concurrency(janus_ctx* ctx, int on);
 

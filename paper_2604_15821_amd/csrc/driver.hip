@@ -648,11 +648,13 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   JANUS_HIP_TRY(hipGetLastError());
 
   // ---- phase 3: double backward of the force loss (hht[t] = loss adjoint of hh[t])
-  // The expert weight gradients go to the side stream (ss.sd), where they run
-  // beside the memory-bound products G5/G6 and the edge kernels.  Buffers they
-  // read: p.T1 (G7, until t1_free), Abar of the block (G7), Sbt (G8).  Sbt of
-  // block t is written over Abar of block t-1 (block 0: p.Shat0), which G7 of
-  // block t-1 has finished reading once t1_free of that block has passed.
+  // The expert weight gradients go to the side stream (ss.sd), forked just before
+  // memory-bound edge and atom kernels of the caller's stream; the caller's stream
+  // joins the side stream before each of its own matrix products, so products never
+  // share the GPU with each other.  Buffers the side stream reads: p.T1 (G7, until
+  // t1_free), Abar of the block (G7), Sbt (G8).  Sbt of block t is written over
+  // Abar of block t-1 (block 0: p.Shat0), which G7 of block t-1 has finished
+  // reading once t1_free of that block has passed.
   SideSync ss(ctx, st);
   hipStream_t sd = ss.sd;
   hipEvent_t t1_free = nullptr;   // side stream done with p.T1 (and with the last Abar it read)
@@ -664,6 +666,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     const float* hht_t = t == 0 ? nullptr : HV(p.hht, t);
     const bool tri_t = three && Nt > 0;
     if (tri_t) {
+      ss.join();   // products of the caller's stream follow
       // double backward of the triplet messages: Zbar~ -> triplet experts -> Ybar3~ -> QX_e
       const float* W1a = Wp(blk(t, "W1a"));
       const float* W2a = Wp(blk(t, "W2a"));
@@ -714,6 +717,15 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                    (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)Xbar(t), hht_t, (const float*)p.rt,
                    p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr), (int)tri_t);
     }
+    // G7 (side stream) beside dW_b and the reverse scatter
+    ss.fork();
+    {
+      // G7: dW1 += Xbt^T Abar (side stream)
+      PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
+      launch_wgrad(sd, LoadPlain{p.T1, d}, LoadPlain{Ab(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
+                   p.partial2, Gp(blk(t, "W1")), 1);
+    }
+    t1_free = ss.mark();
     {
       // dW_b (part 1): (rt B')^T Fbar
       PROF(PROF_DENSE_GEMM, f_filt, 0);
@@ -725,31 +737,26 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       LAUNCH_VPL(scatter_rev_kernel, d, gN, b256, 0, st, rowptr, rev, (const float*)p.Pe, (const float*)nullptr,
                  (const float*)nullptr, N, d, HV(p.h3, t));
     }
-    ss.fork();
-    {
-      // G7: dW1 += Xbt^T Abar (side stream)
-      PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
-      launch_wgrad(sd, LoadPlain{p.T1, d}, LoadPlain{Ab(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
-                   p.partial2, Gp(blk(t, "W1")), 1);
-    }
-    t1_free = ss.mark();
+    ss.join();
     {
       // G5: Abt = Xbt W1 -> Sbt (into Shat(t)), C (into Sb)
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
       launch_rows<false>(st, LoadPlain{p.T1, d}, W1, d, h, TL(t), p.ntiles + t, p.mt,
                          EpiP3{Aa(t), Sb(t), Shat(t), h});
     }
+    {
+      // G6: Ybt = Sbt W2
+      PROF(PROF_EXPERT_GEMM, f_exp, 0);
+      launch_rows<false>(st, LoadPlain{Shat(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
+    }
+    // G8 (side stream) beside the per-atom and per-edge kernels that follow (and those
+    // of the next block up to its G5)
     ss.fork();
     {
       // G8: dW2 += Sbt^T Ybar (side stream)
       PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
       launch_wgrad(sd, LoadPlain{Shat(t), h}, LoadPlain{Ybs(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
                    p.partial2, Gp(blk(t, "W2")), 1);
-    }
-    {
-      // G6: Ybt = Sbt W2
-      PROF(PROF_EXPERT_GEMM, f_exp, 0);
-      launch_rows<false>(st, LoadPlain{Shat(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
     }
     // phase-2 dE/du of this block (hh^{t+1} without the feature-update MoE)
     const float* hbar_u3 = atom ? UU(t) : HV(p.hh, t + 1);
@@ -761,6 +768,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         LAUNCH_VPL_K(edge_combine_p3_kernel, d, k, gE, b256, 0, st, POS(t), GATE(t), (const float*)p.T2,
                      (const float*)MBt(t), Ne, d, p.g3 + t * M, MHt(t));
       }
+      ss.join();
       {
         PROF(PROF_DENSE_GEMM, f_qkv, 0);
         launch_rows<false>(st, LoadPlain{MHt(t), d}, Wp(blk(t, "Wqkv")), d, 3 * d, p.tilesE, p.ntE, p.mtE,
@@ -804,6 +812,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         LAUNCH_VPL_K(gather_atom_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), (const float*)nullptr,
                      (const float*)p.ut, N, d, p.T1f);
       }
+      ss.join();
       {
         PROF(PROF_EXPERT_WGRAD, f_atm, 0);
         launch_wgrad(st, LoadPlain{p.T1f, d}, LoadPlain{Abf(t), hf}, d, hf, CHF(t), p.nchunksf + t, CFF(t), p.mcf,
@@ -830,6 +839,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
     }
   }
+  ss.join();
   {
     // readout part: vt = hht^T W_o1
     PROF(PROF_DENSE_GEMM, f_dense, 0);
@@ -856,7 +866,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                  p.mcN, 1, p.partial, Gp("W_o1"), 1);
     launch_rows<true>(st, LoadPlain{p.Zr, d}, Wo1, d, d, p.tilesN, p.ntN, p.mtN, EpiDense{HV(p.hh, T), d});
   }
-  // G11 and G12 go to the side stream; G12 reads p.T1 until t1_free.
+  // G11 and G12 go to the side stream after G10, beside the edge, router and atom
+  // kernels of the block; the caller's stream joins it before its next product.
+  // G12 reads p.T1 until t1_free.
   for (int t = T - 1; t >= 0; --t) {
     const float* Wb = Wp(blk(t, "W_b"));
     const float* W1 = Wp(blk(t, "W1"));
@@ -873,6 +885,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         LAUNCH_VPL_K(gather_atom_kernel, d, kf, gN, b256, 0, st, iota, POSF(t), (const float*)nullptr,
                      (const float*)HV(p.hh, t + 1), N, d, p.T1f);
       }
+      ss.join();
       {
         PROF(PROF_EXPERT_GEMM, f_atm, 0);
         launch_rows<true>(st, LoadPlain{p.T1f, d}, W2f, d, hf, TLF(t), p.ntilesf + t, p.mtf,
@@ -913,6 +926,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     if (attn) {
       // adjoints of osum and of its tangent -> attention reverse -> primal message adjoints
       const float* Wqkv = Wp(blk(t, "Wqkv"));
+      ss.join();
       {
         PROF(PROF_DENSE_GEMM, 2 * f_dense, 0);
         launch_rows<true>(st, LoadPlain{a_u, d}, Wp(blk(t, "Wo")), d, d, p.tilesN, p.ntN, p.mtN, EpiStore{p.AO, d});
@@ -956,6 +970,18 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)nullptr, a_u, N, d,
                    p.T1);
     }
+    ss.join();
+    {
+      // G9: St = mt W2^T -> At = g SiLU'(A) St + C (into Sb); row sums for the gate adjoint
+      PROF(PROF_EXPERT_GEMM, f_exp, 0);
+      launch_rows<true>(st, LoadPlain{p.T1, d}, W2, d, h, TL(t), p.ntiles + t, p.mt, EpiP4{Aa(t), Sb(t), SG(t), h},
+                        p.gpart);
+    }
+    {
+      // G10: Xt = At W1^T
+      PROF(PROF_EXPERT_GEMM, f_exp, 0);
+      launch_rows<true>(st, LoadPlain{Sb(t), h}, W1, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
+    }
     ss.fork();
     {
       // G12: dW2 += SiLU(A)^T (g mt) (side stream)
@@ -965,22 +991,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     t1_free = ss.mark();
     {
-      // G9: St = mt W2^T -> At = g SiLU'(A) St + C (into Sb); row sums for the gate adjoint
-      PROF(PROF_EXPERT_GEMM, f_exp, 0);
-      launch_rows<true>(st, LoadPlain{p.T1, d}, W2, d, h, TL(t), p.ntiles + t, p.mt, EpiP4{Aa(t), Sb(t), SG(t), h},
-                        p.gpart);
-    }
-    ss.fork();
-    {
       // G11: dW1 += X^T At (side stream)
       PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
       launch_wgrad(sd, LoadPlain{Xs(t), d}, LoadPlain{Sb(t), h}, d, h, CH(t), p.nchunks + t, CF(t), p.mc, Ee,
                    p.partial2, Gp(blk(t, "W1")), 1);
-    }
-    {
-      // G10: Xt = At W1^T
-      PROF(PROF_EXPERT_GEMM, f_exp, 0);
-      launch_rows<true>(st, LoadPlain{Sb(t), h}, W1, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{p.T2, d});
     }
     if (Ne > 0) {
       {
@@ -1019,6 +1033,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         LAUNCH_VPL_K(tri_gather_kernel, d, k3, gE, b256, 0, st, (const int*)p.trow, POS3(t), (const float*)nullptr,
                    (const float*)p.Q, Ne, d, p.T3a);
       }
+      ss.join();
       {
         PROF(PROF_EXPERT_GEMM, f_tri, 0);
         launch_rows<true>(st, LoadPlain{p.T3a, d}, W2a, d, h3, TL3(t), p.ntiles3 + t, p.mt3,
