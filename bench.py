@@ -157,14 +157,17 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # per-family breakdown from a few untimed steps with every family's events
+    # per-family breakdown from a few untimed steps with every family's events, on one
+    # stream, so that each family's rate describes its kernels alone
     nb = args.breakdown_steps
+    ctx.set_concurrency(False)
     ctx.profile(True)
     for _ in range(nb):
         step()
     torch.cuda.synchronize()
     breakdown = ctx.profile_read()
     ctx.profile(False)
+    ctx.set_concurrency(not args.serial)
     # the dominant family (most time) is the one timed inside the timed region
     dom = max(breakdown, key=lambda n: breakdown[n]["ms"])
 
@@ -241,6 +244,8 @@ def main():
         + (24.0 * m.top_k_f * m.d * m.d_hidden_f * N * m.n_blocks if m.atom_moe else 0.0),
         "roofline": roof,
         "kernels": kernels,
+        "kernels_note": "per-family rates from untimed steps on one stream; the roofline's kernel is timed "
+                        "inside the timed region",
     }
     ctx.close()
     if not args.no_cpu_baseline:

@@ -159,14 +159,16 @@ __global__ void combine_fwd_kernel(const int* __restrict__ rowptr, const int* __
     ld_row<VPL>(h + i * d, l, acc);
     const int e0 = rowptr[i], e1 = rowptr[i + 1];
     int e = e0;
-    for (; e + 2 <= e1; e += 2) {
-      float y0[VPL], y1[VPL];
-      sum_slots<VPL, KC>(Yg, pos, e, d, l, y0);
-      sum_slots<VPL, KC>(Yg, pos, e + 1, d, l, y1);
-      add_row<VPL>(acc, y0);
-      add_row<VPL>(acc, y1);
+    // four edges' slot rows in flight per step (one wave per atom: the loop over the
+    // neighbourhood is the wave's latency chain)
+    for (; e + 4 <= e1; e += 4) {
+      float y[4][VPL];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sum_slots<VPL, KC>(Yg, pos, e + u, d, l, y[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add_row<VPL>(acc, y[u]);
     }
-    if (e < e1) {
+    for (; e < e1; ++e) {
       float y0[VPL];
       sum_slots<VPL, KC>(Yg, pos, e, d, l, y0);
       add_row<VPL>(acc, y0);
@@ -183,17 +185,31 @@ __global__ void gather_atom_kernel(const int* __restrict__ rowptr, const int* __
   JANUS_WAVE_LOOP(i, N) {
     float s[VPL];
     ld_row<VPL>(src + i * d, l, s);
-    const int e0 = rowptr[i], e1 = rowptr[i + 1];
-    for (int e = e0; e < e1; ++e) {
+    const long long f0 = (long long)rowptr[i] * KC, f1 = (long long)rowptr[i + 1] * KC;
+    long long f = f0;
+    // eight slot rows per step: their indices (and gates) are loaded together
+    for (; f + 8 <= f1; f += 8) {
+      int q[8];
+      float g[8];
 #pragma unroll
-      for (int c = 0; c < KC; ++c) {
-        const long long f = (long long)e * KC + c;
-        const float g = gate ? gate[f] : 1.f;
+      for (int u = 0; u < 8; ++u) {
+        q[u] = pos[f + u];
+        g[u] = gate ? gate[f + u] : 1.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
         float o[VPL];
 #pragma unroll
-        for (int v = 0; v < VPL; ++v) o[v] = g * s[v];
-        st_row<VPL>(out + (long long)pos[f] * d, l, o);
+        for (int v = 0; v < VPL; ++v) o[v] = g[u] * s[v];
+        st_row<VPL>(out + (long long)q[u] * d, l, o);
       }
+    }
+    for (; f < f1; ++f) {
+      const float g = gate ? gate[f] : 1.f;
+      float o[VPL];
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) o[v] = g * s[v];
+      st_row<VPL>(out + (long long)pos[f] * d, l, o);
     }
   }
 }
@@ -247,16 +263,13 @@ __global__ void scatter_rev_kernel(const int* __restrict__ rowptr, const int* __
     }
     const int e0 = rowptr[a], e1 = rowptr[a + 1];
     int e = e0;
-    for (; e + 4 <= e1; e += 4) {
-      float p0[VPL], p1[VPL], p2[VPL], p3[VPL];
-      ld_row<VPL>(P + (long long)rev[e] * d, l, p0);
-      ld_row<VPL>(P + (long long)rev[e + 1] * d, l, p1);
-      ld_row<VPL>(P + (long long)rev[e + 2] * d, l, p2);
-      ld_row<VPL>(P + (long long)rev[e + 3] * d, l, p3);
-      add_row<VPL>(acc, p0);
-      add_row<VPL>(acc, p1);
-      add_row<VPL>(acc, p2);
-      add_row<VPL>(acc, p3);
+    // eight reverse edges' rows in flight per step
+    for (; e + 8 <= e1; e += 8) {
+      float pr[8][VPL];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) ld_row<VPL>(P + (long long)rev[e + u] * d, l, pr[u]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) add_row<VPL>(acc, pr[u]);
     }
     for (; e < e1; ++e) {
       float p0[VPL];
@@ -316,28 +329,43 @@ __global__ void combine_p3_kernel(const int* __restrict__ rowptr, const int* __r
     float mb[VPL], acc[VPL];
     ld_row<VPL>(hbar_next + i * d, l, mb);
     if (hht) ld_row<VPL>(hht + i * d, l, acc); else zero_row<VPL>(acc);
-    const int e0 = rowptr[i], e1 = rowptr[i + 1];
-    for (int e = e0; e < e1; ++e) {
-      float y[KC][VPL];
+    const long long f0 = (long long)rowptr[i] * KC, f1 = (long long)rowptr[i + 1] * KC;
+    long long f = f0;
+    // eight slot rows (of consecutive edges) in flight per step; each row's dot
+    // product with hbar goes to lane u of the g3 store
+    for (; f + 8 <= f1; f += 8) {
+      float y[8][VPL], g[8];
 #pragma unroll
-      for (int c = 0; c < KC; ++c) ld_row<VPL>(Ybt + (long long)pos[(long long)e * KC + c] * d, l, y[c]);
-      float s[KC];
+      for (int u = 0; u < 8; ++u) {
+        ld_row<VPL>(Ybt + (long long)pos[f + u] * d, l, y[u]);
+        g[u] = gate[f + u];
+      }
+      float o = 0.f;
 #pragma unroll
-      for (int c = 0; c < KC; ++c) {
-        const float g = gate[(long long)e * KC + c];
-        s[c] = 0.f;
+      for (int u = 0; u < 8; ++u) {
+        float su = 0.f;
 #pragma unroll
         for (int v = 0; v < VPL; ++v) {
-          s[c] += y[c][v] * mb[v];
-          acc[v] += g * y[c][v];
+          su += y[u][v] * mb[v];
+          acc[v] += g[u] * y[u][v];
         }
+        su = wave_sum(su);
+        o = l == u ? su : o;
       }
+      if (l < 8) g3[f + l] = o;
+    }
+    for (; f < f1; ++f) {
+      float y[VPL];
+      ld_row<VPL>(Ybt + (long long)pos[f] * d, l, y);
+      const float g = gate[f];
+      float su = 0.f;
 #pragma unroll
-      for (int c = 0; c < KC; ++c) s[c] = wave_sum(s[c]);
-      if (l == 0) {
-#pragma unroll
-        for (int c = 0; c < KC; ++c) g3[(long long)e * KC + c] = s[c];
+      for (int v = 0; v < VPL; ++v) {
+        su += y[v] * mb[v];
+        acc[v] += g * y[v];
       }
+      su = wave_sum(su);
+      if (l == 0) g3[f] = su;
     }
     st_row<VPL>(hht_next + i * d, l, acc);
   }
