@@ -24,6 +24,10 @@ taken in float32 so that both sides take them identically.
 
 beta is a fixed routing bias (it receives no gradient).
 
+With the robust loss (paper Sec. "Multi-task training strategies") L is
+replaced by (1/S) sum_s W(z_s, tau)^2 L_s over per-structure Huber losses L_s
+(``robust_loss_and_seeds``).
+
 With the angular three-body term (``threebody.py``) the edge token gains
 the messages of the bond triplets whose first bond is e:
     X_e   = F_e * h_{j(e)} + q_e,   q_e = sum_{tau = (e, .)} MoE3(Z_tau)
@@ -69,6 +73,8 @@ path follows, so a mistake in either derivation does not cancel.
 from __future__ import annotations
 
 from dataclasses import dataclass
+
+import math
 
 import numpy as np
 import scipy.sparse as sp
@@ -538,6 +544,85 @@ def loss_and_seeds(E, F, E_ref, F_ref, n_atoms_struct, w_E=1.0, w_F=1.0):
     return loss, lam, phi
 
 
+def huber2(r, delta):
+    """rho(r) = r^2 for |r| <= delta, 2 delta |r| - delta^2 beyond (twice the Huber
+    function, so that delta = inf gives the squared error); and rho'(r)."""
+    if math.isinf(delta):
+        return r * r, 2.0 * r
+    a = np.abs(r)
+    rho = np.where(a <= delta, r * r, 2.0 * delta * a - delta * delta)
+    drho = 2.0 * np.clip(r, -delta, delta)
+    return rho, drho
+
+
+def robust_weight(z, tau):
+    """W(z, tau) = exp(-max(z - tau, 0)^2 / 2) and dW/dz: 1 over the normal range
+    z <= tau, a smooth (C^1) monotone decay to 0 beyond it."""
+    x = np.maximum(z - tau, 0.0)
+    W = np.exp(-0.5 * x * x)
+    return W, -x * W
+
+
+def robust_loss_and_seeds(E, F, E_ref, F_ref, offsets, w_E, w_F, delta, tau, task=None, sigma=None,
+                          S_ref=None, w_S=0.0):
+    """Robust multi-task loss of paper Sec. "Multi-task training strategies" and its
+    seeds lam = dL/dE_s, phi = dL/dF_a, psi = dL/dsigma_s.
+
+    L = (1/S) sum_s W(z_s, tau)^2 L_s with the per-structure base loss
+        L_s = w_E rho(E_s/n_s - E_ref,s) + w_F/(3 n_s) sum_{a in s, c} rho(F_ac - F_ref,ac)
+              + w_S/9 sum_q rho(sigma_sq - S_ref,sq)
+    (rho: twice the Huber function of width delta), z_s = (L_s - mu_g)/sd_g standardised
+    over the structures of its task g (all structures without tasks; population standard
+    deviation; z = 0 where sd_g = 0).  The weights are differentiated like the rest:
+    with A_g = sum_{i in g} W_i W'_i L_i and B_g = sum_{i in g} W_i W'_i L_i z_i,
+        dL/dL_j = (1/S) [W_j^2 + (2/sd_g)(W_j W'_j L_j - A_g/n_g - z_j B_g/n_g)].
+    Readings: the form of W and of rho are not given by the paper (it names a smooth
+    monotone soft threshold and an L1 or Huber base loss)."""
+    E = np.asarray(E, np.float64)
+    F = np.asarray(F, np.float64)
+    offsets = np.asarray(offsets, np.int64)
+    S = E.shape[0]
+    n = np.diff(offsets).astype(np.float64)
+    de = E / n - np.asarray(E_ref, np.float64)
+    dF = F - np.asarray(F_ref, np.float64)
+    rE, dE = huber2(de, delta)
+    rF, dFr = huber2(dF, delta)
+    sid = np.repeat(np.arange(S), np.diff(offsets))
+    L = w_E * rE + w_F * np.bincount(sid, weights=rF.sum(axis=1), minlength=S) / (3.0 * n)
+    if w_S:
+        ds = np.asarray(sigma, np.float64) - np.asarray(S_ref, np.float64)
+        rS, dSr = huber2(ds, delta)
+        L = L + w_S * rS.reshape(S, 9).sum(axis=1) / 9.0
+    groups = np.zeros(S, np.int64) if task is None else np.asarray(task, np.int64)
+    z = np.zeros(S)
+    sd = np.zeros(S)
+    for gid in np.unique(groups):
+        m = groups == gid
+        mu = L[m].mean()
+        sdg = np.sqrt(((L[m] - mu) ** 2).mean())
+        sd[m] = sdg
+        if sdg > 0.0:
+            z[m] = (L[m] - mu) / sdg
+    W, dW = robust_weight(z, tau)
+    c = W * W
+    for gid in np.unique(groups):
+        m = groups == gid
+        if sd[m][0] == 0.0:
+            continue
+        ng = m.sum()
+        A = (W * dW * L)[m].sum()
+        B = (W * dW * L * z)[m].sum()
+        c[m] += 2.0 / sd[m][0] * (W[m] * dW[m] * L[m] - A / ng - z[m] * B / ng)
+    c /= S
+    loss = (W * W * L).sum() / S
+    lam = c * w_E * dE / n
+    phi = (c / (3.0 * n) * w_F)[sid][:, None] * dFr
+    psi = None
+    if w_S:
+        psi = (c * w_S / 9.0)[:, None, None] * dSr
+    return loss, lam, phi, psi, {"L": L, "z": z, "W": W}
+
+
 # --------------------------------------------------------------------------- second order
 
 def _moe_tangent(rt, E, W1, W2, X, Xd):
@@ -776,12 +861,19 @@ def training_step(batch, edges=None, return_aux=False):
     N = batch.species.shape[0]
     F = _seg(g.ei, N, G) - _seg(g.ej, N, G)
     sigma = stress(g, G, batch.cell)
-    loss, lam, phi = loss_and_seeds(E, F, batch.E_ref, batch.F_ref, g.n_atoms_struct, m.w_E, m.w_F)
     Psi = None
-    if m.w_S:
-        loss_S, psi = stress_loss_and_seed(sigma, batch.S_ref, E.shape[0], m.w_S)
-        loss = loss + loss_S
-        Psi = psi / np.abs(np.linalg.det(np.asarray(batch.cell, np.float64)))[:, None, None]
+    if getattr(m, "robust", 0):
+        loss, lam, phi, psi, _ = robust_loss_and_seeds(
+            E, F, batch.E_ref, batch.F_ref, batch.offsets, m.w_E, m.w_F, m.huber_delta, m.robust_tau,
+            task=batch.task if m.n_tasks else None, sigma=sigma, S_ref=batch.S_ref, w_S=m.w_S)
+        if m.w_S:
+            Psi = psi / np.abs(np.linalg.det(np.asarray(batch.cell, np.float64)))[:, None, None]
+    else:
+        loss, lam, phi = loss_and_seeds(E, F, batch.E_ref, batch.F_ref, g.n_atoms_struct, m.w_E, m.w_F)
+        if m.w_S:
+            loss_S, psi = stress_loss_and_seed(sigma, batch.S_ref, E.shape[0], m.w_S)
+            loss = loss + loss_S
+            Psi = psi / np.abs(np.linalg.det(np.asarray(batch.cell, np.float64)))[:, None, None]
     grad = weight_gradient(batch.species, g, P, routing, lam, phi, Psi)
     if return_aux:
         return loss, E, F, grad, {"graph": g, "routing": routing, "lam": lam, "phi": phi, "stress": sigma,

@@ -19,6 +19,7 @@ order -> E_ref -> F_ref.
 from __future__ import annotations
 
 import dataclasses
+import math
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -41,7 +42,10 @@ class ModelConfig:
     self-attention over every atom's edge messages (head width d / n_heads).
     n_tasks > 0 adds the task-aware embedding: per-structure task, charge and
     spin labels (indices below n_tasks, n_charges, n_spins) and the element
-    composition each add a vector to the atom embedding.
+    composition each add a vector to the atom embedding.  robust = 1 replaces
+    the mean-squared loss by the robust multi-task loss: per-structure Huber
+    losses of width huber_delta, weighted by a soft threshold at robust_tau
+    standard deviations of the structure's task.
     """
 
     d: int
@@ -70,6 +74,9 @@ class ModelConfig:
     n_tasks: int = 0
     n_charges: int = 0
     n_spins: int = 0
+    robust: int = 0
+    huber_delta: float = math.inf
+    robust_tau: float = 2.0
 
     def weight_shapes(self):
         """Named weight tensors in blob order, with the fan-in used at init.
@@ -161,6 +168,8 @@ _M_STRESS = dataclasses.replace(_M_SMALL, w_S=0.1 * 160.2177 ** 2)
 _M_ATTN = dataclasses.replace(_M_SMALL, n_heads=4)
 # task-aware embedding: 4 datasets, total charges -2..2, spin multiplicities 1..4
 _M_TASK = dataclasses.replace(_M_SMALL, n_tasks=4, n_charges=5, n_spins=4)
+# robust multi-task loss (Huber width 1, down-weighting beyond 2 standard deviations per task)
+_M_ROBUST = dataclasses.replace(_M_TASK, robust=1, huber_delta=1.0, robust_tau=2.0)
 _M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
 
 WORKLOADS = {
@@ -171,6 +180,7 @@ WORKLOADS = {
     "stress": Workload("stress", "ortho", 64, 64, 0.08, _M_STRESS),
     "attention": Workload("attention", "ortho", 64, 64, 0.08, _M_ATTN),
     "multitask": Workload("multitask", "ortho", 64, 64, 0.08, _M_TASK),
+    "robust": Workload("robust", "ortho", 64, 64, 0.08, _M_ROBUST),
     "shard": Workload("shard", "cubic", 256, 128, 0.1, _M_BIG),
     "irregular": Workload("irregular", "mixed", 512, 0, 0.1, _M_BIG, zipf_s=1.2),
 }
