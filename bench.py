@@ -235,6 +235,7 @@ def main():
                    **({"atom_moe": {"experts": m.n_experts_f, "top_k": m.top_k_f, "d_hidden": m.d_hidden_f}}
                       if m.atom_moe else {}),
                    **({"stress_weight": m.w_S} if m.w_S else {}),
+                   **({"robust_loss": {"huber_delta": m.huber_delta, "tau": m.robust_tau}} if m.robust else {}),
                    **({"attention_heads": m.n_heads} if m.n_heads else {}),
                    **({"tasks": m.n_tasks, "charges": m.n_charges, "spins": m.n_spins} if m.n_tasks else {})},
         "edges_per_s": Ne / (ms * 1e-3),

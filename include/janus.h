@@ -89,6 +89,22 @@ enum {
  *              Sec. "Task-aware feature embedding"); then n_charges and
  *              n_spins (>= 1) size the charge and spin tables, and every
  *              structure's labels select rows of them (janus_step_ex)
+ *   robust     0: mean-squared loss w_E/S sum_s (E_s/n_s - E_ref,s)^2
+ *              + w_F/(3N) sum |F - F_ref|^2 (+ w_S/(9S) sum |sigma - S_ref|^2).
+ *              1: the robust multi-task loss of paper Sec. "Multi-task
+ *              training strategies", L = (1/S) sum_s W(z_s, robust_tau)^2 L_s
+ *              with per-structure losses L_s = w_E rho(E_s/n_s - E_ref,s)
+ *              + w_F/(3 n_s) sum_{a in s} rho(F_a - F_ref,a) (+ w_S/9 sum
+ *              rho(sigma_s - S_ref,s)), rho(r) = r^2 for |r| <= huber_delta
+ *              and 2 huber_delta |r| - huber_delta^2 beyond (huber_delta > 0,
+ *              may be +inf), z_s the standard score of L_s among the
+ *              structures of its task (all structures when n_tasks = 0) and
+ *              W(z, tau) = exp(-max(z - tau, 0)^2 / 2).  The gradient
+ *              includes the dependence of the weights on the batch
+ *              statistics.  The robust loss needs the whole batch at once:
+ *              janus_step returns JANUS_EUNSUPPORTED when the workspace
+ *              limit would split the batch into chunks, and at most 256
+ *              tasks.
  */
 typedef struct janus_config {
   int32_t n_species;
@@ -117,6 +133,9 @@ typedef struct janus_config {
   int32_t n_tasks;
   int32_t n_charges;
   int32_t n_spins;
+  int32_t robust;
+  float huber_delta;
+  float robust_tau;
 } janus_config;
 
 typedef struct janus_ctx janus_ctx;

@@ -629,9 +629,15 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     if (S_ref || stress_out)
       hipLaunchKernelGGL(stress_kernel, wave_grid(S), b256, 0, st, rowptr, offsets, cell, (const float*)p.rbar,
                          (const float4*)p.geo, (const float4*)(three ? p.gvec : nullptr), S, p.sig, stress_out);
-    hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
-                       (const float*)F, F_ref, N, ca.S_tot, ca.N_tot, cfg.w_E, cfg.w_F, (const float*)p.sig, S_ref,
-                       cfg.w_S, cell, loss_part, p.lam, p.phi, p.Psi);
+    if (cfg.robust)   // the whole batch is this chunk (checked by the caller)
+      hipLaunchKernelGGL(robust_loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
+                         (const float*)F, F_ref, N, cfg.w_E, cfg.w_F, (const float*)p.sig, S_ref, cfg.w_S, cell,
+                         cfg.huber_delta, cfg.robust_tau, cfg.n_tasks ? labels->task + ca.s0 : (const int*)nullptr,
+                         cfg.n_tasks ? cfg.n_tasks : 1, (const int*)p.sid, p.rob, loss_part, p.lam, p.phi, p.Psi);
+    else
+      hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
+                         (const float*)F, F_ref, N, ca.S_tot, ca.N_tot, cfg.w_E, cfg.w_F, (const float*)p.sig, S_ref,
+                         cfg.w_S, cell, loss_part, p.lam, p.phi, p.Psi);
     if (Ne > 0)
       hipLaunchKernelGGL(rtilde_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, ei, ej, (const float4*)p.geo,
                          (const float*)p.phi, (const int*)p.sid, (const float*)(S_ref ? p.Psi : nullptr), Ne, p.rt,
@@ -1332,6 +1338,8 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
       s0 = s1;
     }
   }
+  // the robust loss standardises the losses of the whole batch before any backward pass
+  if (cfg.robust && chunks.size() > 1) return JANUS_EUNSUPPORTED;
   rc = ensure(ctx->ws, need);
   if (rc) return rc;
   ctx->last_chunks = (int)chunks.size();

@@ -215,6 +215,135 @@ __global__ void loss_kernel(const double* __restrict__ Ed, const float* __restri
   if (t == 0) *loss_part = red[0];
 }
 
+// rho(r) = r^2 for |r| <= delta, 2 delta |r| - delta^2 beyond (twice the Huber
+// function; delta = inf gives the squared error), and rho'(r).
+__device__ __forceinline__ void huber2(double r, double delta, double& rho, double& drho) {
+  const double a = fabs(r);
+  if (a <= delta) {
+    rho = r * r;
+    drho = 2.0 * r;
+  } else {
+    rho = 2.0 * delta * a - delta * delta;
+    drho = r < 0.0 ? -2.0 * delta : 2.0 * delta;
+  }
+}
+
+// Soft threshold of the robust loss: W = exp(-max(z - tau, 0)^2 / 2), dW/dz.
+__device__ __forceinline__ void robust_weight(double z, double tau, double& W, double& dW) {
+  const double x = z > tau ? z - tau : 0.0;
+  W = exp(-0.5 * x * x);
+  dW = -x * W;
+}
+
+constexpr int kRobustMaxGroups = 256;
+
+// Robust multi-task loss (paper Sec. "Multi-task training strategies") over the
+// whole batch (one workgroup; the step runs as one chunk):
+//   L = (1/S) sum_s W(z_s, tau)^2 L_s,
+//   L_s = w_E rho(E_s/n_s - E_ref,s) + w_F/(3 n_s) sum_{a in s, c} rho(dF_ac) + w_S/9 sum_q rho(dsigma_sq),
+//   z_s = (L_s - mu_g) / sd_g over the structures of task g (one group without tasks; z = 0 where sd_g = 0).
+// The seeds differentiate the weights too: with A_g = sum W W' L and B_g = sum W W' L z over g,
+//   dL/dL_s = (1/S) [W_s^2 + (2/sd_g)(W_s W'_s L_s - A_g/n_g - z_s B_g/n_g)],
+// then lam_s, phi_a, Psi_s by the chain rule through L_s.  rob: 2 S doubles of scratch
+// (L_s, then dL/dL_s).  Every sum runs in a fixed order.
+__global__ void robust_loss_kernel(const double* __restrict__ Ed, const float* __restrict__ Eref,
+                                   const int* __restrict__ offsets, int S, const float* __restrict__ F,
+                                   const float* __restrict__ Fref, int N, float wE, float wF,
+                                   const float* __restrict__ sig, const float* __restrict__ Sref, float wS,
+                                   const float* __restrict__ cell, float delta_f, float tau_f,
+                                   const int* __restrict__ task, int n_groups, const int* __restrict__ sid,
+                                   double* __restrict__ rob, double* __restrict__ loss_part, float* __restrict__ lam,
+                                   float* __restrict__ phi, float* __restrict__ Psi) {
+  __shared__ double gst[kRobustMaxGroups][6];   // mu, sd, A, B, count, sum W^2 L
+  const int t = threadIdx.x;
+  const double delta = (double)delta_f, tau = (double)tau_f;
+  double rho, drho;
+  // per-structure base losses
+  for (int s = t; s < S; s += blockDim.x) {
+    const int a0 = offsets[s], a1 = offsets[s + 1];
+    const double n = (double)(a1 - a0);
+    huber2(Ed[s] / n - (double)Eref[s], delta, rho, drho);
+    double L = wE * rho;
+    double rf = 0.0;
+    for (long long q = 3LL * a0; q < 3LL * a1; ++q) {
+      huber2((double)F[q] - (double)Fref[q], delta, rho, drho);
+      rf += rho;
+    }
+    L += wF * rf / (3.0 * n);
+    if (Sref) {
+      double rs = 0.0;
+      for (int q = 0; q < 9; ++q) {
+        huber2((double)sig[9 * s + q] - (double)Sref[9 * s + q], delta, rho, drho);
+        rs += rho;
+      }
+      L += wS * rs / 9.0;
+    }
+    rob[s] = L;
+  }
+  __syncthreads();
+  // statistics of each task group, structures in order
+  for (int g = t; g < n_groups; g += blockDim.x) {
+    double cnt = 0.0, sum = 0.0;
+    for (int s = 0; s < S; ++s)
+      if ((task ? task[s] : 0) == g) {
+        cnt += 1.0;
+        sum += rob[s];
+      }
+    const double mu = cnt > 0.0 ? sum / cnt : 0.0;
+    double var = 0.0;
+    for (int s = 0; s < S; ++s)
+      if ((task ? task[s] : 0) == g) var += (rob[s] - mu) * (rob[s] - mu);
+    const double sd = cnt > 0.0 ? sqrt(var / cnt) : 0.0;
+    double A = 0.0, B = 0.0, lw = 0.0;
+    for (int s = 0; s < S; ++s)
+      if ((task ? task[s] : 0) == g) {
+        const double L = rob[s];
+        const double z = sd > 0.0 ? (L - mu) / sd : 0.0;
+        double W, dW;
+        robust_weight(z, tau, W, dW);
+        A += W * dW * L;
+        B += W * dW * L * z;
+        lw += W * W * L;
+      }
+    gst[g][0] = mu; gst[g][1] = sd; gst[g][2] = A; gst[g][3] = B; gst[g][4] = cnt; gst[g][5] = lw;
+  }
+  __syncthreads();
+  // dL/dL_s, then the energy and stress seeds
+  for (int s = t; s < S; s += blockDim.x) {
+    const int g = task ? task[s] : 0;
+    const double L = rob[s], mu = gst[g][0], sd = gst[g][1];
+    const double z = sd > 0.0 ? (L - mu) / sd : 0.0;
+    double W, dW;
+    robust_weight(z, tau, W, dW);
+    double c = W * W;
+    if (sd > 0.0) c += 2.0 / sd * (W * dW * L - gst[g][2] / gst[g][4] - z * gst[g][3] / gst[g][4]);
+    c /= (double)S;
+    rob[S + s] = c;
+    const double n = (double)(offsets[s + 1] - offsets[s]);
+    huber2(Ed[s] / n - (double)Eref[s], delta, rho, drho);
+    lam[s] = (float)(c * wE * drho / n);
+    if (Sref) {
+      const double iv = 1.0 / cell_volume(cell + 9 * s);
+      for (int q = 0; q < 9; ++q) {
+        huber2((double)sig[9 * s + q] - (double)Sref[9 * s + q], delta, rho, drho);
+        Psi[9 * s + q] = (float)(c * wS / 9.0 * drho * iv);
+      }
+    }
+  }
+  __syncthreads();
+  for (int q = t; q < 3 * N; q += blockDim.x) {
+    const int s = sid[q / 3];
+    const double n = (double)(offsets[s + 1] - offsets[s]);
+    huber2((double)F[q] - (double)Fref[q], delta, rho, drho);
+    phi[q] = (float)(rob[S + s] * wF / (3.0 * n) * drho);
+  }
+  if (t == 0) {
+    double lw = 0.0;
+    for (int g = 0; g < n_groups; ++g) lw += gst[g][5];
+    *loss_part = lw / (double)S;
+  }
+}
+
 // loss = sum of the chunk shares in chunk order.
 __global__ void loss_total_kernel(const double* __restrict__ part, int n, float* __restrict__ loss) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
@@ -692,6 +821,9 @@ int check_config(const janus_config* c) {
   if (!(c->w_S >= 0.f)) return JANUS_EINVAL;
   if (c->n_heads < 0 || (c->n_heads && c->d % c->n_heads)) return JANUS_EINVAL;
   if (c->n_tasks < 0 || (c->n_tasks && (c->n_charges < 1 || c->n_spins < 1))) return JANUS_EINVAL;
+  if (c->robust != 0 && c->robust != 1) return JANUS_EINVAL;
+  if (c->robust && (!(c->huber_delta > 0.f) || c->robust_tau != c->robust_tau)) return JANUS_EINVAL;
+  if (c->robust && c->n_tasks > kRobustMaxGroups) return JANUS_EUNSUPPORTED;
 
   // heads of 32 columns
   if (c->n_heads && c->d / c->n_heads != kAttnDh) return JANUS_EUNSUPPORTED;
@@ -714,6 +846,7 @@ struct Plan {
   float *B, *dB, *rt, *rbar;
   int *sp_cnt, *sp_off, *sp_atoms;
   float *z, *eps, *lam, *phi, *vt, *Zr, *Tr, *colpart, *sig, *Psi, *gs, *gsb;
+  double* rob;   // robust loss: per-structure losses and their adjoints
   float4* gtan;
   double* Ed;
   float *h, *hh, *hht, *h3;   // [(T+1) or T][N, d]; the final-backward adjoint reuses hh
@@ -829,6 +962,7 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.z = cv.take<float>(Nd);
   p.eps = cv.take<float>(N);
   p.lam = cv.take<float>(S);
+  p.rob = cv.take<double>(2LL * S + 2);
   p.phi = cv.take<float>(3LL * N);
   p.sig = cv.take<float>(9LL * S);
   p.gs = cv.take<float>((long long)S * d + 4);

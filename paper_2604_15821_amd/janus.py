@@ -33,7 +33,8 @@ class Config(C.Structure):
         ("top_k3", C.c_int32), ("d_hidden3", C.c_int32), ("n_legendre", C.c_int32), ("w_E", C.c_float),
         ("w_F", C.c_float), ("atom_moe", C.c_int32), ("n_experts_f", C.c_int32), ("top_k_f", C.c_int32),
         ("d_hidden_f", C.c_int32), ("w_S", C.c_float), ("n_heads", C.c_int32), ("n_tasks", C.c_int32),
-        ("n_charges", C.c_int32), ("n_spins", C.c_int32),
+        ("n_charges", C.c_int32), ("n_spins", C.c_int32), ("robust", C.c_int32), ("huber_delta", C.c_float),
+        ("robust_tau", C.c_float),
     ]
 
 

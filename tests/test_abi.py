@@ -58,6 +58,10 @@ def test_pack_unpack_roundtrip():
     (dict(env_p=5), janus.JANUS_EUNSUPPORTED),
     (dict(d_hidden=32), janus.JANUS_EINVAL),
     (dict(r_cut=0.0), janus.JANUS_EINVAL),
+    (dict(robust=2), janus.JANUS_EINVAL),
+    (dict(robust=1, huber_delta=0.0), janus.JANUS_EINVAL),
+    (dict(robust=1, robust_tau=float("nan")), janus.JANUS_EINVAL),
+    (dict(robust=1, n_tasks=300, n_charges=1, n_spins=1), janus.JANUS_EUNSUPPORTED),
 ])
 def test_bad_configs_are_rejected_on_the_host(change, code):
     import dataclasses

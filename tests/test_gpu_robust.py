@@ -1,0 +1,99 @@
+"""Robust multi-task loss (paper Sec. "Multi-task training strategies") on the GPU
+against the float64 oracle: loss and energy 1e-5 relative, forces and every weight
+gradient 1e-3 relative L2, with structures down-weighted by the soft threshold, with
+and without per-task statistics; a step that would need several workspace chunks is
+rejected."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from helpers import TOL_E, TOL_F, TOL_LOSS, TOL_W, banner, energy_error, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+FIXED = ("beta", "beta3", "betaf")
+
+
+def _batch(name):
+    from paper_2604_15821_amd.synth import make_batch, subset
+    if name == "small-8":
+        # no tasks: one group; tau low enough that the worst structures are down-weighted
+        b = subset(make_batch("small"), range(8))
+        return dataclasses.replace(b, model=dataclasses.replace(b.model, robust=1, huber_delta=1.0, robust_tau=0.8))
+    if name == "robust-12":
+        # per-task statistics (4 tasks), Huber width 1
+        b = subset(make_batch("robust"), range(12))
+        return dataclasses.replace(b, model=dataclasses.replace(b.model, robust_tau=0.5))
+    if name == "robust-stress-6":
+        b = subset(make_batch("stress"), range(6))
+        return dataclasses.replace(b, model=dataclasses.replace(b.model, robust=1, huber_delta=0.5, robust_tau=0.7))
+    raise KeyError(name)
+
+
+def _run(b, limit=None):
+    import torch
+    from paper_2604_15821_amd import janus
+    d = janus.upload(b)
+    ctx = janus.Context(b.model)
+    try:
+        if limit is not None:
+            ctx.set_workspace_limit(limit)
+        nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+        loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"],
+                                  d["F_ref"], S_ref=d["S_ref"] if b.model.w_S else None, labels=d["labels"])
+        torch.cuda.synchronize()
+        return float(loss.cpu()[0]), E.cpu().numpy(), F.cpu().numpy(), dW.cpu().numpy()
+    finally:
+        ctx.close()
+
+
+@pytest.fixture(scope="module", params=["small-8", "robust-12", "robust-stress-6"])
+def case(request):
+    from oracle.model import Params, forward_energy, robust_loss_and_seeds, training_step
+    b = _batch(request.param)
+    m = b.model
+    banner("robust", request.param, b.n_struct, "structures", b.n_atoms, "atoms")
+    loss, E, F, grad, aux = training_step(b, return_aux=True)
+    W = robust_loss_and_seeds(E, F, b.E_ref, b.F_ref, b.offsets, m.w_E, m.w_F, m.huber_delta, m.robust_tau,
+                              task=b.task if m.n_tasks else None, sigma=aux["stress"], S_ref=b.S_ref,
+                              w_S=m.w_S)[4]["W"]
+    print("weights", np.round(W, 4))
+    assert (W < 0.999).any() and (W == 1.0).any()
+    _, cache = forward_energy(b.species, aux["graph"], Params.from_weights(b.weights, b.model), aux["routing"])
+    return b, _run(b), (loss, E, F, grad, cache)
+
+
+def test_loss_and_energy(case):
+    b, (g_loss, g_E, g_F, g_W), (loss, E, F, grad, cache) = case
+    print("loss", g_loss, loss)
+    assert energy_error(g_E, E, cache["eps"], b.offsets) <= TOL_E
+    assert abs(g_loss - loss) <= TOL_LOSS * abs(loss)
+
+
+def test_forces(case):
+    b, (g_loss, g_E, g_F, g_W), (loss, E, F, grad, cache) = case
+    assert rel_l2(g_F, F) <= TOL_F
+
+
+def test_weight_gradients(case):
+    from paper_2604_15821_amd import janus
+    b, (g_loss, g_E, g_F, g_W), (loss, E, F, grad, cache) = case
+    got = janus.unpack(g_W, b.model)
+    worst = {}
+    for name, ref in grad.items():
+        if name.rsplit(".", 1)[-1] in FIXED:
+            assert (got[name] == 0).all()
+            continue
+        worst[name] = rel_l2(got[name], ref)
+    print("dW rel L2", {k: f"{v:.2e}" for k, v in worst.items()})
+    assert max(worst.values()) <= TOL_W, worst
+
+
+def test_chunked_robust_step_is_rejected():
+    from paper_2604_15821_amd import janus
+    b = _batch("small-8")
+    banner("robust chunked")
+    with pytest.raises(janus.JanusError) as ex:
+        _run(b, limit=int(2.5 * 1.1e8))
+    assert ex.value.code == janus.JANUS_EUNSUPPORTED
