@@ -118,7 +118,11 @@ def summarize(workload: str, runs: str) -> str:
             d, a = dur.get(fam, [0.0]), agg[fam]
             L.append(f"| {fam} | {a[0]} | {sum(d) / max(len(d), 1):.1f} | {a[1] / a[0] / 1e6:.1f} | "
                      f"{a[2] / a[0] / 1e6:.1f} |")
-    L += ["", "Kernel statistics of the kernel-trace run (rocprofv3 --stats, all dispatches including warm-up):", "",
+    L += ["", "The kernel-trace run uses bench.py's default two streams: in the double and final backward the "
+          "expert weight gradients (wgrad) run beside the edge, atom and small dense kernels, whose averages "
+          "above are therefore longer than alone (`profiles/kernels_small_serial.md` has every kernel on one "
+          "stream); the expert products never overlap another product.",
+          "", "Kernel statistics of the kernel-trace run (rocprofv3 --stats, all dispatches including warm-up):", "",
           "| kernel | calls | avg us | total ms | % |", "|---|---:|---:|---:|---:|"]
     for r in stats[:30]:
         n = re.sub(r"\(.*", "", r["Name"].replace("janus::", ""))
@@ -159,10 +163,12 @@ def algorithmic_bytes(bench_line: dict):
 
 
 def trace_command(workload: str, steps: int, out: str = "$R/gpurun_out") -> str:
-    """The rocprofv3 kernel-trace command of one workload (run from /tmp with TMPDIR=/tmp)."""
+    """The rocprofv3 kernel-trace command of one workload (run from /tmp with TMPDIR=/tmp);
+    a name ending in _serial is that workload run on one stream (bench.py --serial)."""
+    wl, serial = (workload[:-7], " --serial") if workload.endswith("_serial") else (workload, "")
     return (f"rocprofv3 --kernel-trace --stats --output-format csv -d {out}/trace_{workload} -o run -- "
-            f"python3 $R/bench.py --workload {workload} --steps {steps} --warmup 1 --breakdown-steps 1 "
-            f"--no-cpu-baseline")
+            f"python3 $R/bench.py --workload {wl} --steps {steps} --warmup 1 --breakdown-steps 1 "
+            f"--no-cpu-baseline{serial}")
 
 
 def trace_summary(workload: str, runs: str, steps: int) -> str:
@@ -185,7 +191,11 @@ def trace_summary(workload: str, runs: str, steps: int) -> str:
          f"Summarised by `python -m paper_2604_15821_amd.counters --trace {workload} {steps} $R/gpurun_out`.",
          f"All dispatches of the run ({steps} timed + 1 warm-up + 1 breakdown step). Families follow the",
          "kernel names: products that use the expert GEMM kernels (the attention q|k|v and Wo products",
-         "too) count as expert_gemm here; bench.py's own profiler files those under dense_gemm.", "",
+         "too) count as expert_gemm here; bench.py's own profiler files those under dense_gemm.",
+         ("One stream: every kernel ran alone." if workload.endswith("_serial") else
+          "Two streams (bench.py's default): in the double and final backward the expert weight gradients "
+          "run beside the edge, atom and small dense kernels, whose durations here are therefore longer "
+          "than alone; the expert products never overlap another product."), "",
          "| family | dispatches | total ms | % |", "|---|---:|---:|---:|"]
     tot = sum(v[1] for v in fam.values()) or 1.0
     for k, v in sorted(fam.items(), key=lambda kv: -kv[1][1]):
