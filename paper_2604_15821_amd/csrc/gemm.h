@@ -62,6 +62,16 @@ struct RowsTile {   // one 128-row tile of a group
 __device__ __forceinline__ float4 f4zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 __device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 __device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+// Streaming accesses of the epilogues (each element is read or written once per launch).
+__device__ __forceinline__ float4 ld4nt(const float* p) {
+  const f32x4v v = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void st4nt(float* p, float4 v) {
+  const f32x4v x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<f32x4v*>(p));
+}
 
 // XCD-aware block order.  Workgroups are handed to the 8 XCDs round-robin
 // by linear id, and each XCD has its own L2.  Block b runs on XCD b % 8 as
@@ -139,7 +149,7 @@ struct EpiStore {
   using Raw = NoRaw;
   __device__ __forceinline__ Raw load(long long, int) const { return Raw{}; }
   __device__ __forceinline__ float store(long long r, int col, float4 v, const Raw&) const {
-    st4(c + r * ld + col, v);
+    st4nt(c + r * ld + col, v);
     return 0.f;
   }
 };
@@ -156,7 +166,7 @@ struct EpiRowScale {   // c = s[r] * v
   using Raw = float;
   __device__ __forceinline__ Raw load(long long r, int) const { return s[r]; }
   __device__ __forceinline__ float store(long long r, int col, float4 v, const Raw& a) const {
-    st4(c + r * ld + col, make_float4(a * v.x, a * v.y, a * v.z, a * v.w));
+    st4nt(c + r * ld + col, make_float4(a * v.x, a * v.y, a * v.z, a * v.w));
     return 0.f;
   }
 };
@@ -169,10 +179,10 @@ struct EpiAdd {
   static constexpr bool kRowSum = false;
   using Raw = float4;
   __device__ __forceinline__ Raw load(long long row, int col) const {
-    return r ? ld4(r + row * ld + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+    return r ? ld4nt(r + row * ld + col) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   __device__ __forceinline__ float store(long long row, int col, float4 v, const Raw& x) const {
-    st4(c + row * ld + col, make_float4(v.x + x.x, v.y + x.y, v.z + x.z, v.w + x.w));
+    st4nt(c + row * ld + col, make_float4(v.x + x.x, v.y + x.y, v.z + x.z, v.w + x.w));
     return 0.f;
   }
 };
@@ -185,11 +195,11 @@ struct EpiP2 {
   long long ld;
   static constexpr bool kRowSum = false;
   using Raw = float4;
-  __device__ __forceinline__ Raw load(long long r, int c) const { return ld4(A + r * ld + c); }
+  __device__ __forceinline__ Raw load(long long r, int c) const { return ld4nt(A + r * ld + c); }
   __device__ __forceinline__ float store(long long r, int c, float4 v, const Raw& a) const {
     const long long i = r * ld + c;
-    st4(Sb + i, v);
-    st4(Ab + i, make_float4(silu_d1(a.x) * v.x, silu_d1(a.y) * v.y, silu_d1(a.z) * v.z, silu_d1(a.w) * v.w));
+    st4nt(Sb + i, v);
+    st4nt(Ab + i, make_float4(silu_d1(a.x) * v.x, silu_d1(a.y) * v.y, silu_d1(a.z) * v.z, silu_d1(a.w) * v.w));
     return 0.f;
   }
 };
@@ -215,7 +225,7 @@ struct EpiP3 {
   }
   __device__ __forceinline__ Raw load(long long r, int c) const {
     const long long i = r * ld + c;
-    return Raw{ld4(A + i), ld4(Sb + i)};
+    return Raw{ld4nt(A + i), ld4nt(Sb + i)};
   }
   __device__ __forceinline__ float store(long long r, int c, float4 v, const Raw& x) const {
     const long long i = r * ld + c;
@@ -226,8 +236,8 @@ struct EpiP3 {
     d12(a.y, d1, d2); o1.y = d1 * v.y; o2.y = d2 * sb.y * v.y;
     d12(a.z, d1, d2); o1.z = d1 * v.z; o2.z = d2 * sb.z * v.z;
     d12(a.w, d1, d2); o1.w = d1 * v.w; o2.w = d2 * sb.w * v.w;
-    st4(Ab + i, o1);
-    st4(Sb + i, o2);
+    st4nt(Ab + i, o1);
+    st4nt(Sb + i, o2);
     return 0.f;
   }
 };
@@ -251,7 +261,7 @@ struct EpiP4 {
   }
   __device__ __forceinline__ Raw load(long long r, int c) const {
     const long long i = r * ld + c;
-    return Raw{ld4(A + i), ld4(Sb + i), gate[r]};
+    return Raw{ld4nt(A + i), ld4nt(Sb + i), gate[r]};
   }
   __device__ __forceinline__ float store(long long r, int c, float4 v, const Raw& x) const {
     float sum = 0.f;
@@ -260,7 +270,7 @@ struct EpiP4 {
     o.y = one(x.a.y, v.y, x.c.y, x.g, sum);
     o.z = one(x.a.z, v.z, x.c.z, x.g, sum);
     o.w = one(x.a.w, v.w, x.c.w, x.g, sum);
-    st4(Sb + r * ld + c, o);
+    st4nt(Sb + r * ld + c, o);
     return sum;
   }
 };
