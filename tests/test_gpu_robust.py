@@ -97,3 +97,24 @@ def test_chunked_robust_step_is_rejected():
     with pytest.raises(janus.JanusError) as ex:
         _run(b, limit=int(2.5 * 1.1e8))
     assert ex.value.code == janus.JANUS_EUNSUPPORTED
+
+
+def test_full_size_against_oracle():
+    """The whole 64-structure robust workload (the loss couples every structure of a
+    task through its mean and deviation, so no per-structure shortcut applies): the
+    oracle runs the full batch once (about 20 s on the host)."""
+    from oracle.model import Params, forward_energy, training_step
+    from paper_2604_15821_amd import janus
+    from paper_2604_15821_amd.synth import make_batch
+    b = make_batch("robust")
+    banner("robust full-size", b.n_struct, "structures", b.n_atoms, "atoms")
+    g_loss, g_E, g_F, g_W = _run(b)
+    loss, E, F, grad, aux = training_step(b, return_aux=True)
+    _, cache = forward_energy(b.species, aux["graph"], Params.from_weights(b.weights, b.model), aux["routing"])
+    assert energy_error(g_E, E, cache["eps"], b.offsets) <= TOL_E
+    assert abs(g_loss - loss) <= TOL_LOSS * abs(loss)
+    assert rel_l2(g_F, F) <= TOL_F
+    got = janus.unpack(g_W, b.model)
+    worst = max(rel_l2(got[k], ref) for k, ref in grad.items() if k.rsplit(".", 1)[-1] not in FIXED)
+    print("worst dW rel L2", worst)
+    assert worst <= TOL_W
