@@ -376,14 +376,15 @@ __global__ void tri_combine_kernel(const int* __restrict__ trowptr, const int* _
     zero_row<VPL>(acc);
     const int t0 = trowptr[e], t1 = trowptr[e + 1];
     int t = t0;
-    for (; t + 2 <= t1; t += 2) {
-      float y0[VPL], y1[VPL];
-      sum_slots<VPL, KC>(Yg, pos3, t, d, l, y0);
-      sum_slots<VPL, KC>(Yg, pos3, t + 1, d, l, y1);
-      add_row<VPL>(acc, y0);
-      add_row<VPL>(acc, y1);
+    // four triplets' slot rows in flight per step
+    for (; t + 4 <= t1; t += 4) {
+      float y[4][VPL];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sum_slots<VPL, KC>(Yg, pos3, t + u, d, l, y[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add_row<VPL>(acc, y[u]);
     }
-    if (t < t1) {
+    for (; t < t1; ++t) {
       float y0[VPL];
       sum_slots<VPL, KC>(Yg, pos3, t, d, l, y0);
       add_row<VPL>(acc, y0);
@@ -403,16 +404,31 @@ __global__ void tri_gather_kernel(const int* __restrict__ trowptr, const int* __
     if (t0 == t1) continue;
     float s[VPL];
     ld_row<VPL>(src + e * d, l, s);
-    for (int t = t0; t < t1; ++t) {
+    const long long f1 = (long long)t1 * KC;
+    long long f = (long long)t0 * KC;
+    // eight slot rows per step: their indices (and gates) are loaded together
+    for (; f + 8 <= f1; f += 8) {
+      int q[8];
+      float g[8];
 #pragma unroll
-      for (int k = 0; k < KC; ++k) {
-        const long long f = (long long)t * KC + k;
-        const float g = gate3 ? gate3[f] : 1.f;
+      for (int u = 0; u < 8; ++u) {
+        q[u] = pos3[f + u];
+        g[u] = gate3 ? gate3[f + u] : 1.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
         float o[VPL];
 #pragma unroll
-        for (int v = 0; v < VPL; ++v) o[v] = g * s[v];
-        st_row<VPL>(out + (long long)pos3[f] * d, l, o);
+        for (int v = 0; v < VPL; ++v) o[v] = g[u] * s[v];
+        st_row<VPL>(out + (long long)q[u] * d, l, o);
       }
+    }
+    for (; f < f1; ++f) {
+      const float g = gate3 ? gate3[f] : 1.f;
+      float o[VPL];
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) o[v] = g * s[v];
+      st_row<VPL>(out + (long long)pos3[f] * d, l, o);
     }
   }
 }
@@ -640,28 +656,43 @@ __global__ void tri_combine_p3_kernel(const int* __restrict__ trowptr, const int
     float xb[VPL], acc[VPL];
     ld_row<VPL>(Xbar + e * d, l, xb);
     zero_row<VPL>(acc);
-    const int t0 = trowptr[e], t1 = trowptr[e + 1];
-    for (int t = t0; t < t1; ++t) {
-      float y[KC][VPL];
+    const long long f1 = (long long)trowptr[e + 1] * KC;
+    long long f = (long long)trowptr[e] * KC;
+    // eight slot rows in flight per step; each row's dot product with Xbar goes
+    // to lane u of the g3t store
+    for (; f + 8 <= f1; f += 8) {
+      float y[8][VPL], g[8];
 #pragma unroll
-      for (int k = 0; k < KC; ++k) ld_row<VPL>(Ybt3 + (long long)pos3[(long long)t * KC + k] * d, l, y[k]);
-      float s[KC];
+      for (int u = 0; u < 8; ++u) {
+        ld_row<VPL>(Ybt3 + (long long)pos3[f + u] * d, l, y[u]);
+        g[u] = gate3[f + u];
+      }
+      float o = 0.f;
 #pragma unroll
-      for (int k = 0; k < KC; ++k) {
-        const float g = gate3[(long long)t * KC + k];
-        s[k] = 0.f;
+      for (int u = 0; u < 8; ++u) {
+        float su = 0.f;
 #pragma unroll
         for (int v = 0; v < VPL; ++v) {
-          s[k] += y[k][v] * xb[v];
-          acc[v] += g * y[k][v];
+          su += y[u][v] * xb[v];
+          acc[v] += g[u] * y[u][v];
         }
+        su = wave_sum(su);
+        o = l == u ? su : o;
       }
+      if (l < 8) g3t[f + l] = o;
+    }
+    for (; f < f1; ++f) {
+      float y[VPL];
+      ld_row<VPL>(Ybt3 + (long long)pos3[f] * d, l, y);
+      const float g = gate3[f];
+      float su = 0.f;
 #pragma unroll
-      for (int k = 0; k < KC; ++k) s[k] = wave_sum(s[k]);
-      if (l == 0) {
-#pragma unroll
-        for (int k = 0; k < KC; ++k) g3t[(long long)t * KC + k] = s[k];
+      for (int v = 0; v < VPL; ++v) {
+        su += y[v] * xb[v];
+        acc[v] += g * y[v];
       }
+      su = wave_sum(su);
+      if (l == 0) g3t[f] = su;
     }
     st_row<VPL>(QX + e * d, l, acc);
   }
