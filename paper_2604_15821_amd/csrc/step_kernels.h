@@ -258,27 +258,32 @@ __global__ void robust_loss_kernel(const double* __restrict__ Ed, const float* _
   const int t = threadIdx.x;
   const double delta = (double)delta_f, tau = (double)tau_f;
   double rho, drho;
-  // per-structure base losses
-  for (int s = t; s < S; s += blockDim.x) {
+  // per-structure base losses, one wave per structure (lanes over force components,
+  // then a fixed butterfly)
+  const int lane = t & 63;
+  for (int s = t >> 6; s < S; s += blockDim.x >> 6) {
     const int a0 = offsets[s], a1 = offsets[s + 1];
     const double n = (double)(a1 - a0);
-    huber2(Ed[s] / n - (double)Eref[s], delta, rho, drho);
-    double L = wE * rho;
     double rf = 0.0;
-    for (long long q = 3LL * a0; q < 3LL * a1; ++q) {
+    for (long long q = 3LL * a0 + lane; q < 3LL * a1; q += 64) {
       huber2((double)F[q] - (double)Fref[q], delta, rho, drho);
       rf += rho;
     }
-    L += wF * rf / (3.0 * n);
-    if (Sref) {
-      double rs = 0.0;
-      for (int q = 0; q < 9; ++q) {
-        huber2((double)sig[9 * s + q] - (double)Sref[9 * s + q], delta, rho, drho);
-        rs += rho;
+    rf = wave_sum_d(rf);
+    if (lane == 0) {
+      huber2(Ed[s] / n - (double)Eref[s], delta, rho, drho);
+      double L = wE * rho;
+      L += wF * rf / (3.0 * n);
+      if (Sref) {
+        double rs = 0.0;
+        for (int q = 0; q < 9; ++q) {
+          huber2((double)sig[9 * s + q] - (double)Sref[9 * s + q], delta, rho, drho);
+          rs += rho;
+        }
+        L += wS * rs / 9.0;
       }
-      L += wS * rs / 9.0;
+      rob[s] = L;
     }
-    rob[s] = L;
   }
   __syncthreads();
   // statistics of each task group, structures in order
