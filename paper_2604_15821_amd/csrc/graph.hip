@@ -230,14 +230,28 @@ __device__ __forceinline__ void bessel_at(double r, double rcd, int nb, float* _
   envelope_at(r, rcd, u, du);
   const double c = sqrt(2.0 / rcd);
   const double th = M_PI / rcd;
-  for (int n = 1; n <= nb; ++n) {
-    const double k = n * th;
-    double sn, cs;
-    sincos(k * r, &sn, &cs);
-    const double s = sn / r;
-    const double ds = (k * r * cs - sn) / (r * r);
-    B[n - 1] = (float)(c * s * u);
-    dB[n - 1] = (float)(c * (ds * u + s * du));
+  // sin(n x), cos(n x) for x = th r by the angle-addition identities from one sincos
+  // (float64: the recurrence's rounding stays far below the float32 outputs')
+  double s1, c1;
+  sincos(th * r, &s1, &c1);
+  double sn = s1, cs = c1;
+  const double ir = 1.0 / r;
+  // nb is a multiple of 4 and the rows 16-byte aligned: four values per store
+  for (int n0 = 1; n0 <= nb; n0 += 4) {
+    float b[4], db[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const double k = (n0 + q) * th;
+      const double s = sn * ir;
+      const double ds = (k * cs - s) * ir;
+      b[q] = (float)(c * s * u);
+      db[q] = (float)(c * (ds * u + s * du));
+      const double sn1 = sn * c1 + cs * s1;
+      cs = cs * c1 - sn * s1;
+      sn = sn1;
+    }
+    *reinterpret_cast<float4*>(B + n0 - 1) = make_float4(b[0], b[1], b[2], b[3]);
+    *reinterpret_cast<float4*>(dB + n0 - 1) = make_float4(db[0], db[1], db[2], db[3]);
   }
 }
 
