@@ -18,7 +18,7 @@
 
 namespace janus {
 
-constexpr int kSortChunk = 4096;
+constexpr int kSortChunk = 1024;
 
 // Top-k (descending fp32 logit, lower index first on ties) and gates (softmax
 // over all E experts, evaluated in fp64) of one logit row; l32(x) and l64(x)
