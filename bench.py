@@ -107,7 +107,7 @@ def main():
                     help="one elementwise copy kernel over this many MiB before the run (calibrates HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path",
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this library has no multi-GPU path",
               file=sys.stderr)
         sys.exit(2)
 

@@ -48,7 +48,7 @@ enum {
   JANUS_ECAPACITY = -2,    /* edge buffers too small; *n_edges holds the count needed */
   JANUS_ENOMEM = -3,       /* device allocation of the context workspace failed */
   JANUS_EHIP = -4,         /* a HIP runtime call failed */
-  JANUS_EUNSUPPORTED = -5  /* valid input that this build does not handle (non-diagonal cell,
+  JANUS_EUNSUPPORTED = -5  /* valid input that this library does not handle (non-diagonal cell,
                               widths that are not multiples of 64, ...) */
 };
 

@@ -26,8 +26,8 @@ import sys
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def commands(workload: str, out: str = "$R/gpurun_out") -> list[str]:
-    """The three rocprofv3 command lines (run from /tmp with TMPDIR=/tmp, repo at $R)."""
+def commands(workload: str, out: str = "$OUT") -> list[str]:
+    """The three rocprofv3 command lines (run from /tmp with TMPDIR=/tmp, repo at $R, outputs under $OUT)."""
     bench = "python3 $R/bench.py"
     return [
         f"rocprofv3 --kernel-trace --stats --output-format csv -d {out}/tr_k_{workload} -o run -- "
@@ -104,9 +104,9 @@ def summarize(workload: str, runs: str) -> str:
            "launches_counted": ex[0], "fetch_bytes_per_launch": ex[1] / ex[0], "write_bytes_per_launch": ex[2] / ex[0],
            "fetch_scale": kf, "write_scale": kw}
     L = [f"# Kernel time and HBM traffic, training step, workload `{workload}`", "",
-         "Commands (run from /tmp on the MI355X box with `TMPDIR=/tmp`, repo at `$R`), three separate runs:", "",
+         "Commands (run from /tmp on an MI355X with `TMPDIR=/tmp`, repo at `$R`, outputs under `$OUT`), three separate runs:", "",
          "```", *commands(workload), "```", "",
-         f"Summarised by `python -m paper_2604_15821_amd.counters {workload} $R/gpurun_out`.", "",
+         f"Summarised by `python -m paper_2604_15821_amd.counters {workload} $OUT`.", "",
          "FETCH_SIZE and WRITE_SIZE are KiB per dispatch. Each is scaled by what the same counter reads for the",
          "calibration kernel of the `--copy-mib 1024` runs: one elementwise kernel that reads 1 GiB and writes 1 GiB.",
          f"The scale factors are fetch x{kf:.3f} and write x{kw:.3f}. Traffic is counted over every step of the",
@@ -162,7 +162,7 @@ def algorithmic_bytes(bench_line: dict):
     return reads / 8, writes / 8
 
 
-def trace_command(workload: str, steps: int, out: str = "$R/gpurun_out") -> str:
+def trace_command(workload: str, steps: int, out: str = "$OUT") -> str:
     """The rocprofv3 kernel-trace command of one workload (run from /tmp with TMPDIR=/tmp);
     a name ending in _serial is that workload run on one stream (bench.py --serial)."""
     wl, serial = (workload[:-7], " --serial") if workload.endswith("_serial") else (workload, "")
@@ -186,9 +186,9 @@ def trace_summary(workload: str, runs: str, steps: int) -> str:
         lines = [x for x in open(log) if x.startswith("{")]
         bench_line = json.loads(lines[-1]) if lines else None
     L = [f"# Kernel time, training step, workload `{workload}`", "",
-         "Command (run from /tmp on the MI355X box with `TMPDIR=/tmp`, repo at `$R`):", "",
+         "Command (run from /tmp on an MI355X with `TMPDIR=/tmp`, repo at `$R`, outputs under `$OUT`):", "",
          "```", trace_command(workload, steps), "```", "",
-         f"Summarised by `python -m paper_2604_15821_amd.counters --trace {workload} {steps} $R/gpurun_out`.",
+         f"Summarised by `python -m paper_2604_15821_amd.counters --trace {workload} {steps} $OUT`.",
          f"All dispatches of the run ({steps} timed + 1 warm-up + 1 breakdown step). Families follow the",
          "kernel names: products that use the expert GEMM kernels (the attention q|k|v and Wo products",
          "too) count as expert_gemm here; bench.py's own profiler files those under dense_gemm.",
@@ -214,14 +214,14 @@ def trace_summary(workload: str, runs: str, steps: int) -> str:
 if __name__ == "__main__":
     if len(sys.argv) > 1 and sys.argv[1] == "--trace":
         wl, steps = sys.argv[2], int(sys.argv[3])
-        runs = sys.argv[4] if len(sys.argv) > 4 else os.path.join(ROOT, "gpurun_out")
+        runs = sys.argv[4]
         out = os.path.join(ROOT, "profiles", f"kernels_{wl}.md")
         with open(out, "w") as f:
             f.write(trace_summary(wl, runs, steps))
         print(out)
         sys.exit(0)
-    wl = sys.argv[1] if len(sys.argv) > 1 else "small"
-    runs = sys.argv[2] if len(sys.argv) > 2 else os.path.join(ROOT, "gpurun_out")
+    wl = sys.argv[1]
+    runs = sys.argv[2]
     text = summarize(wl, runs)
     out = os.path.join(ROOT, "profiles", f"expert_gemm_{wl}_traffic.md")
     with open(out, "w") as f:

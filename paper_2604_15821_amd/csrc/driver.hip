@@ -26,7 +26,7 @@ extern "C" const char* janus_strerror(int code) {
     case JANUS_ECAPACITY: return "edge buffers too small";
     case JANUS_ENOMEM: return "device allocation failed or a structure does not fit the workspace";
     case JANUS_EHIP: return "HIP runtime error";
-    case JANUS_EUNSUPPORTED: return "configuration or input not supported by this build";
+    case JANUS_EUNSUPPORTED: return "configuration or input not supported by this library";
     default: return "unknown error";
   }
 }
