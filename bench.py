@@ -10,7 +10,7 @@ few untimed steps record HIP events around every kernel family (the
 per-family table); the timed steps then record events around the dominant
 family only, whose average launch time gives the roofline figure.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload small]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload irregular]
 """
 from __future__ import annotations
 
@@ -25,19 +25,20 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA = 157.3e12      # dense fp32 matrix peak of MI355X, FLOP/s
 PEAK_HBM = 8.0e12              # HBM3E bandwidth, B/s
-CSRC = os.path.join(ROOT, "paper_2604_15821_amd", "csrc")
-PROFILES = os.path.join(ROOT, "profiles")
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(workload: str, n_struct: int):
-    """The float64 oracle, untuned, on the first n_struct structures of the batch."""
+def cpu_baseline(b, budget_s: float, seed: int = 0):
+    """The float64 oracle, untuned, timed on a bounded sample of the batch: its structures
+    in a seeded random order, each one full training step of its own (energy, forces and
+    the second-order weight gradient; per structure, the work of a batch step is the same up
+    to the loss normalisation), until budget_s seconds of oracle time have passed."""
+    import numpy as np
     from oracle.model import training_step
-    from paper_2604_15821_amd.synth import make_batch, subset
-    b = subset(make_batch(workload), range(n_struct))
+    from paper_2604_15821_amd.synth import subset
     try:
         from threadpoolctl import threadpool_info
         blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
@@ -47,45 +48,22 @@ def cpu_baseline(workload: str, n_struct: int):
         aff = len(os.sched_getaffinity(0))
     except AttributeError:
         aff = os.cpu_count()
-    t0 = time.perf_counter()
-    training_step(b)
-    dt = time.perf_counter() - t0
+    order = np.random.default_rng(seed).permutation(b.n_struct)
+    atoms, done, dt = 0, 0, 0.0
+    for s in order:
+        sb = subset(b, [int(s)])
+        t0 = time.perf_counter()
+        training_step(sb)
+        dt += time.perf_counter() - t0
+        atoms += sb.n_atoms
+        done += 1
+        if dt >= budget_s:
+            break
     cores = min(aff, blas) if blas else aff
-    return {"value": b.n_atoms / dt, "unit": "atoms/s", "cores": cores, "kind": "oracle",
-            "sample": f"{n_struct} of the batch's structures ({b.n_atoms} atoms), one full training step, "
-                      f"{dt:.1f} s; float64 NumPy, BLAS threads {blas}, affinity {aff}"}
-
-
-# Sources that define the expert GEMM kernels, their operand loaders and epilogues,
-# and their launch configuration: the counter record of that family is valid only for these.
-EXPERT_GEMM_SOURCES = ("common.h", "gemm.h", "internal.h")
-
-
-def kernel_sources_sha256() -> str:
-    """Hash of the expert GEMM kernels' sources: measured counters are valid only for these."""
-    import hashlib
-    h = hashlib.sha256()
-    for name in EXPERT_GEMM_SOURCES:
-        with open(os.path.join(CSRC, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
-    return h.hexdigest()
-
-
-def measured_traffic(workload: str, family: str):
-    """HBM bytes per launch of a kernel family from the committed rocprofv3 counter summary
-    (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy kernel of known size), or None
-    when no summary matches this workload or the kernel sources changed since it was taken."""
-    path = os.path.join(PROFILES, f"{family}_{workload}_traffic.md")
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        for line in f:
-            if line.startswith("traffic-json:"):
-                rec = json.loads(line.split(":", 1)[1])
-                if rec.get("sources_sha256") != kernel_sources_sha256():
-                    return None
-                return rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
-    return None
+    return {"value": atoms / dt, "unit": "atoms/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} of the batch's {b.n_struct} structures in seeded random order ({atoms} atoms), "
+                      f"one full training step each, {dt:.1f} s of oracle time; float64 NumPy, BLAS threads "
+                      f"{blas}, affinity {aff}"}
 
 
 def main():
@@ -93,11 +71,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="small")
-    ap.add_argument("--cpu-structs", type=int, default=40)
+    ap.add_argument("--workload", default="irregular",
+                    help="synthetic batch (default: the 512-structure irregular batch, the largest that fits "
+                         "one GPU; 'shard' is the 256 x 128-atom per-device share of the billion-scale model)")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="oracle time spent on the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--breakdown-steps", type=int, default=3,
-                    help="untimed steps with every kernel family's events, for the per-family table")
+    ap.add_argument("--breakdown-steps", type=int, default=None,
+                    help="untimed steps with every kernel family's events, for the per-family table "
+                         "(default: 3, or 1 when a step takes over a second)")
     ap.add_argument("--workspace-mib", type=int, default=0,
                     help="cap janus_step's workspace (the batch is then processed in chunks of whole structures)")
     ap.add_argument("--serial", action="store_true",
@@ -115,6 +97,7 @@ def main():
     import torch
 
     from paper_2604_15821_amd import janus
+    from paper_2604_15821_amd.counters import measured_traffic
     from paper_2604_15821_amd.synth import WORKLOADS, make_batch
 
     if args.copy_mib > 0:
@@ -153,13 +136,15 @@ def main():
 
     log(f"workload {args.workload}: {S} structures, {N} atoms, {Ne} edges, d={m.d} h={m.d_hidden} "
         f"E={m.n_experts} k={m.top_k} T={m.n_blocks}")
+    tw = time.perf_counter()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    warm_s = (time.perf_counter() - tw) / max(args.warmup, 1)
 
     # per-family breakdown from a few untimed steps with every family's events, on one
     # stream, so that each family's rate describes its kernels alone
-    nb = args.breakdown_steps
+    nb = args.breakdown_steps if args.breakdown_steps is not None else (1 if warm_s > 1.0 else 3)
     ctx.set_concurrency(False)
     ctx.profile(True)
     for _ in range(nb):
@@ -249,8 +234,10 @@ def main():
                         "inside the timed region",
     }
     ctx.close()
+    del d, nl, out
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(args.workload, min(args.cpu_structs, S))
+        res["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 
 

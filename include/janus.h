@@ -101,9 +101,11 @@ enum {
  *              structures of its task (all structures when n_tasks = 0) and
  *              W(z, tau) = exp(-max(z - tau, 0)^2 / 2).  The gradient
  *              includes the dependence of the weights on the batch
- *              statistics.  The robust loss needs the whole batch at once:
- *              janus_step returns JANUS_EUNSUPPORTED when the workspace
- *              limit would split the batch into chunks, and at most 256
+ *              statistics.  The statistics couple every structure of a
+ *              task, so when the workspace splits the batch into chunks the
+ *              step runs the forward and force backward of every chunk
+ *              first, then the statistics, then each chunk again through
+ *              all four phases (the first two are recomputed).  At most 256
  *              tasks.
  */
 typedef struct janus_config {
@@ -201,17 +203,28 @@ typedef struct janus_debug {
   float* gatef;
 } janus_debug;
 
-/* Create a context for `cfg` on the current device.  The context owns its
- * workspace, which grows on demand inside janus_step and is freed by
- * janus_destroy.  Errors: JANUS_EINVAL (cfg out of range),
- * JANUS_EUNSUPPORTED, JANUS_EHIP. */
+/* Create a context for `cfg` on the current device (paper Sec. "Runtime for
+ * multi-phase double-backward execution": the four phases of a step keep
+ * activations and adjoints of every block alive between phases; the context
+ * owns that workspace).  The workspace grows on demand inside janus_step and
+ * is freed by janus_destroy.  `cfg` is read and copied; `out` (host) receives
+ * the context, or NULL on error.  Errors: JANUS_EINVAL (cfg out of range),
+ * JANUS_EUNSUPPORTED (a width or option this library does not implement),
+ * JANUS_EHIP. */
 int janus_create(const janus_config* cfg /* host */, janus_ctx** out /* host */);
 
 /* Free the context and its workspace (NULL is ignored).  The caller must
- * have synchronised every stream the context was used on. */
+ * have synchronised every stream the context was used on.  A library
+ * utility: no passage of the paper defines it. */
 void janus_destroy(janus_ctx* ctx);
 
-/* Layout of the flat weight blob for `cfg`.  Order: A [n_species, d], with the
+/* Layout of the flat weight blob for `cfg`.  The tensors are those of the
+ * model (paper Sec. "MatRIS": embedding, interaction blocks, readout; Sec.
+ * "Sparse MoE routing": per-block expert layers and their routers; Sec.
+ * "Task-aware feature embedding"; Sec. "Multi-head self-attention"); the
+ * paper prints no parameter list, so their shapes and this order are a
+ * reading of this library, kept equal to the order the synthetic generator
+ * draws the weights in.  Order: A [n_species, d], with the
  * task-aware embedding Tk [n_tasks, d], Qe [n_charges, d], Se [n_spins, d],
  * Wc [n_species, d]; for
  * each block t: W_b [n_rbf, d], Pc [n_species, E], Pn [n_species, E],
@@ -327,7 +340,10 @@ int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell, const int
                   float* dLdW, const janus_debug* dbg, void* stream);
 
 /*
- * Workspace of janus_step.  Structures are independent apart from the loss
+ * Workspace of janus_step (paper Sec. "Overview of the problem": the second
+ * derivatives of the force loss roughly double the memory of training; Sec.
+ * "Runtime for multi-phase double-backward execution").  Structures are
+ * independent apart from the loss
  * normalisation, so janus_step processes the batch in chunks of whole
  * structures, in order, each sized so that its workspace fits `bytes`
  * (0, the default: 90% of the device memory free at the time of the call
@@ -391,6 +407,18 @@ int janus_grouped_wgrad(janus_ctx* ctx, const float* A, const float* B, float* G
                         void* stream);
 
 /*
+ * Row-chunk length that janus_grouped_wgrad and the expert weight gradients
+ * of janus_step use for a contraction over M rows into P x Q blocks (host
+ * function, no device work): a power of two from 128 to 16384.  The chunk
+ * doubles while the grid would exceed 8192 workgroups of 128 x 128 output
+ * tiles, or while the partial blocks (written and read back once by the
+ * reduction) would exceed half of the operand bytes and the doubled chunk
+ * still gives at least 2048 workgroups.  Returns the length, or
+ * JANUS_EINVAL for M outside [0, 2^31) or non-positive P, Q.
+ */
+int32_t janus_wgrad_chunk_rows(int64_t M, int32_t P, int32_t Q);
+
+/*
  * Optional profiler of the kernel families of janus_build_edges and
  * janus_step (host-side bookkeeping; HIP events recorded on the caller's
  * stream around each family of launches).
@@ -417,7 +445,8 @@ typedef struct janus_profile_entry {
 int janus_profile_enable(janus_ctx* ctx, int mask);
 int janus_profile_read(janus_ctx* ctx, janus_profile_entry* out /* host */, int32_t cap);
 
-/* Static message for a return code. */
+/* Static message for a return code (a library utility: no passage of the
+ * paper defines it).  Never NULL; unknown codes give "unknown error". */
 const char* janus_strerror(int code);
 
 #ifdef __cplusplus

@@ -59,6 +59,40 @@ def family(kernel_name: str) -> str:
     return "other"
 
 
+# Sources that define the expert GEMM kernels, their operand loaders and epilogues,
+# and their launch configuration: a counter record of that family is valid only for these.
+EXPERT_GEMM_SOURCES = ("common.h", "gemm.h", "internal.h")
+CSRC = os.path.join(ROOT, "paper_2604_15821_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_sources_sha256() -> str:
+    """Hash of the expert GEMM kernels' sources: measured counters are valid only for these."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in EXPERT_GEMM_SOURCES:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, family: str = "expert_gemm"):
+    """HBM bytes per launch of a kernel family from the committed rocprofv3 counter summary
+    (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy kernel of known size), or None
+    when no summary matches this workload or the kernel sources changed since it was taken."""
+    path = os.path.join(PROFILES, f"{family}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-json:"):
+                rec = json.loads(line.split(":", 1)[1])
+                if rec.get("sources_sha256") != kernel_sources_sha256():
+                    return None
+                return rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
+    return None
+
+
 def _counter(path: str, name: str):
     per, names = collections.defaultdict(float), {}
     with open(path) as f:
@@ -73,9 +107,6 @@ def _counter(path: str, name: str):
 
 def summarize(workload: str, runs: str) -> str:
     """Markdown summary of the three runs found under `runs`."""
-    sys.path.insert(0, ROOT)
-    import bench  # noqa: E402  (the source hash and the record format are bench.py's)
-
     fetch, fnames = _counter(f"{runs}/tr_f_{workload}/run_counter_collection.csv", "FETCH_SIZE")
     write, wnames = _counter(f"{runs}/tr_w_{workload}/run_counter_collection.csv", "WRITE_SIZE")
     copy_f = [fetch[k] for k in fetch if family(fnames[k]) == "copy" and fetch[k] > 5e5]
@@ -100,7 +131,7 @@ def summarize(workload: str, runs: str) -> str:
         lines = [x for x in open(log) if x.startswith("{")]
         bench_line = json.loads(lines[-1]) if lines else None
     ex = agg["expert_gemm"]
-    rec = {"workload": workload, "family": "expert_gemm", "sources_sha256": bench.kernel_sources_sha256(),
+    rec = {"workload": workload, "family": "expert_gemm", "sources_sha256": kernel_sources_sha256(),
            "launches_counted": ex[0], "fetch_bytes_per_launch": ex[1] / ex[0], "write_bytes_per_launch": ex[2] / ex[0],
            "fetch_scale": kf, "write_scale": kw}
     L = [f"# Kernel time and HBM traffic, training step, workload `{workload}`", "",

@@ -66,15 +66,20 @@ __device__ __forceinline__ void wave_store32(float* __restrict__ out, const floa
 
 constexpr float kAttnScale = 0.17677669529663687f;   // 1 / sqrt(32)
 
-// Envelope of every edge: u(r/r_c) and du/dr.
+// Envelope of every edge: u(r/r_c) and du/dr, both zero from r = r_c on (an
+// edge of a caller's list at or past the cutoff, a Verlet skin for example,
+// then takes no attention weight, as in the basis).
 __global__ void attn_env_kernel(const float4* __restrict__ geo, long long Ne, float rc, float* __restrict__ uu,
                                 float* __restrict__ ud) {
   const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= Ne) return;
   const double x = (double)geo[e].w / rc;
-  const double x2 = x * x, x5 = x2 * x2 * x, x6 = x5 * x;
-  const double u = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
-  const double du = -168.0 * x5 * (1.0 - x) * (1.0 - x);
+  double u = 0.0, du = 0.0;
+  if (x < 1.0) {
+    const double x2 = x * x, x5 = x2 * x2 * x, x6 = x5 * x;
+    u = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
+    du = -168.0 * x5 * (1.0 - x) * (1.0 - x);
+  }
   uu[e] = (float)u;
   ud[e] = (float)(du / rc);
 }
@@ -1424,7 +1429,7 @@ __global__ void edge_combine_p3_kernel(const int* __restrict__ pos, const float*
   }
 }
 
-// Largest neighbourhood: flag[0] |= 2 when an atom has more than kAttnMaxN edges.
+// Largest neighbourhood: flag[1] |= 1 when an atom has more than kAttnMaxN edges.
 __global__ void attn_degree_check_kernel(const int* __restrict__ rowptr, int N, int* __restrict__ flag) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < N && rowptr[i + 1] - rowptr[i] > kAttnMaxN) atomicOr(flag + 1, 1);

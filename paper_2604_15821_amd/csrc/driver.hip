@@ -121,7 +121,15 @@ struct ChunkArgs {
   long long Nt;                  // triplets of the chunk (three-body term)
   long long t0, Nt_tot;          // first triplet of the chunk, triplets of the batch
   const unsigned char* tshort;   // whole-batch short-bond flags
+  // robust loss: ROBUST_ONE (the batch is this one chunk: base losses, statistics
+  // and seeds here), ROBUST_LOSSES (forward and force backward only, then this
+  // chunk's base losses), ROBUST_SEEDS (seeds from the batch statistics, then the
+  // double and final backward); robust_g: whole-batch [S] base losses, [S] dL/dL_s,
+  // then the loss
+  int robust_mode;
+  double* robust_g;
 };
+enum { ROBUST_OFF = 0, ROBUST_ONE, ROBUST_LOSSES, ROBUST_SEEDS };
 
 __global__ void copy_add_kernel(int* __restrict__ dst, const int* __restrict__ src, long long n, int add) {
   const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -629,12 +637,26 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     if (S_ref || stress_out)
       hipLaunchKernelGGL(stress_kernel, wave_grid(S), b256, 0, st, rowptr, offsets, cell, (const float*)p.rbar,
                          (const float4*)p.geo, (const float4*)(three ? p.gvec : nullptr), S, p.sig, stress_out);
-    if (cfg.robust)   // the whole batch is this chunk (checked by the caller)
-      hipLaunchKernelGGL(robust_loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
-                         (const float*)F, F_ref, N, cfg.w_E, cfg.w_F, (const float*)p.sig, S_ref, cfg.w_S, cell,
-                         cfg.huber_delta, cfg.robust_tau, cfg.n_tasks ? labels->task + ca.s0 : (const int*)nullptr,
-                         cfg.n_tasks ? cfg.n_tasks : 1, (const int*)p.sid, p.rob, loss_part, p.lam, p.phi, p.Psi);
-    else
+    if (cfg.robust) {
+      double* Ls = ca.robust_g;                   // [S_tot] base losses
+      double* cs = ca.robust_g + ca.S_tot;        // [S_tot] dL/dL_s
+      if (ca.robust_mode != ROBUST_SEEDS)
+        hipLaunchKernelGGL(robust_base_kernel, wave_grid(S), b256, 0, st, (const double*)p.Ed, E_ref, offsets, S,
+                           (const float*)F, F_ref, cfg.w_E, cfg.w_F, (const float*)p.sig, S_ref, cfg.w_S,
+                           cfg.huber_delta, Ls + ca.s0);
+      if (ca.robust_mode == ROBUST_LOSSES) {
+        JANUS_HIP_TRY(hipGetLastError());
+        return JANUS_OK;   // the double and final backward wait for the whole batch's statistics
+      }
+      if (ca.robust_mode == ROBUST_ONE)
+        hipLaunchKernelGGL(robust_stats_kernel, dim3(1), dim3(1024), 0, st, (const double*)Ls, ca.S_tot,
+                           cfg.n_tasks ? labels->task : (const int*)nullptr, cfg.n_tasks ? cfg.n_tasks : 1,
+                           cfg.robust_tau, cs, loss_part);
+      hipLaunchKernelGGL(robust_seed_kernel, dim3(cdiv(std::max<long long>(3LL * N, S), 256)), b256, 0, st,
+                         (const double*)p.Ed, E_ref, offsets, S, (const float*)F, F_ref, N, cfg.w_E, cfg.w_F,
+                         (const float*)p.sig, S_ref, cfg.w_S, cell, cfg.huber_delta, (const double*)(cs + ca.s0),
+                         (const int*)p.sid, p.lam, p.phi, p.Psi);
+    } else
       hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, (const double*)p.Ed, E_ref, offsets, S,
                          (const float*)F, F_ref, N, ca.S_tot, ca.N_tot, cfg.w_E, cfg.w_F, (const float*)p.sig, S_ref,
                          cfg.w_S, cell, loss_part, p.lam, p.phi, p.Psi);
@@ -1221,6 +1243,7 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
   gv.take<double>(S + 1);
   gv.take<unsigned char>(three ? Ne + 1 : 1);
   gv.take<long long>(S + 1);
+  gv.take<double>(cfg.robust ? 2LL * S + 1 : 1);
   int rc = ensure(ctx->gbuf, gv.size());
   if (rc) return rc;
   Carver g2(ctx->gbuf.ptr);
@@ -1230,6 +1253,7 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
   double* loss_part = g2.take<double>(S + 1);
   unsigned char* tshort = g2.take<unsigned char>(three ? Ne + 1 : 1);
   long long* scount = g2.take<long long>(S + 1);
+  double* robust_g = g2.take<double>(cfg.robust ? 2LL * S + 1 : 1);
   const size_t need_host = 4 + 2 * (size_t)(S + 1) + 2 * (size_t)(S + 2);
   if (ctx->host_plan_n < need_host) {
     if (ctx->host_plan) (void)hipHostFree(ctx->host_plan);
@@ -1333,13 +1357,13 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
       ca.t0 = tpre[s0];
       ca.Nt_tot = tpre[S];
       ca.tshort = tshort;
+      ca.robust_mode = ROBUST_OFF;
+      ca.robust_g = robust_g;
       chunks.push_back(ca);
       need = std::max(need, b1);
       s0 = s1;
     }
   }
-  // the robust loss standardises the losses of the whole batch before any backward pass
-  if (cfg.robust && chunks.size() > 1) return JANUS_EUNSUPPORTED;
   rc = ensure(ctx->ws, need);
   if (rc) return rc;
   ctx->last_chunks = (int)chunks.size();
@@ -1352,14 +1376,34 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
   ctx->sync_used = 0;
   JANUS_HIP_TRY(hipMemsetAsync(dLdW, 0, sizeof(float) * L.total, st));
   if (dbg && dbg->counts) JANUS_HIP_TRY(hipMemsetAsync(dbg->counts, 0, sizeof(int) * cfg.n_blocks * cfg.n_experts, st));
-  for (const ChunkArgs& ca : chunks) {
+  auto run = [&](ChunkArgs ca, int mode) {
+    ca.robust_mode = mode;
     Plan p;
     plan_layout(p, ctx->ws.ptr, cfg, ca.N, ca.S, ca.Ne, ca.Nt);
-    rc = run_chunk(ctx, st, p, L, ca, pos, cell, species, offsets, nl, W, E_ref, F_ref, S_ref, labels,
-                   loss_part + ca.index, E, F, stress, dLdW, dbg);
-    if (rc) return rc;
+    return run_chunk(ctx, st, p, L, ca, pos, cell, species, offsets, nl, W, E_ref, F_ref, S_ref, labels,
+                     loss_part + ca.index, E, F, stress, dLdW, dbg);
+  };
+  int n_parts = (int)chunks.size();
+  if (cfg.robust && chunks.size() > 1) {
+    // The robust loss standardises every structure's loss within its task, so no
+    // chunk can start its double backward before all forces exist: a first pass
+    // runs every chunk's forward and force backward and keeps its base losses,
+    // the batch statistics follow, and a second pass recomputes each chunk's
+    // forward and force backward (its workspace was reused) before the double
+    // and final backward with the seeds of the batch statistics.
+    for (const ChunkArgs& ca : chunks)
+      if ((rc = run(ca, ROBUST_LOSSES))) return rc;
+    hipLaunchKernelGGL(robust_stats_kernel, dim3(1), dim3(1024), 0, st, (const double*)robust_g, S,
+                       cfg.n_tasks ? labels->task : (const int*)nullptr, cfg.n_tasks ? cfg.n_tasks : 1,
+                       cfg.robust_tau, robust_g + S, loss_part);
+    for (const ChunkArgs& ca : chunks)
+      if ((rc = run(ca, ROBUST_SEEDS))) return rc;
+    n_parts = 1;
+  } else {
+    for (const ChunkArgs& ca : chunks)
+      if ((rc = run(ca, cfg.robust ? ROBUST_ONE : ROBUST_OFF))) return rc;
   }
-  hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1), 0, st, (const double*)loss_part, (int)chunks.size(), loss);
+  hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1), 0, st, (const double*)loss_part, n_parts, loss);
   JANUS_HIP_TRY(hipGetLastError());
   return JANUS_OK;
 }

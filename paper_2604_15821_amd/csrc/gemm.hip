@@ -171,6 +171,11 @@ extern "C" int janus_grouped_gemm(janus_ctx* ctx, const float* A, const float* B
   return JANUS_OK;
 }
 
+extern "C" int32_t janus_wgrad_chunk_rows(int64_t M, int32_t P, int32_t Q) {
+  if (M < 0 || M > INT32_MAX || P <= 0 || Q <= 0) return JANUS_EINVAL;
+  return wgrad_chunk_rows(M, P, Q);
+}
+
 extern "C" int janus_grouped_wgrad(janus_ctx* ctx, const float* A, const float* B, float* G,
                                    const int32_t* row_off, int32_t n_groups, int64_t M, int32_t P, int32_t Q,
                                    void* stream) {

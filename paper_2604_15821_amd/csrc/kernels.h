@@ -9,9 +9,8 @@ namespace janus {
 void launch_validate_struct(hipStream_t st, const int* offsets, int S, int N, const float* cell, float rc,
                             int* flag);
 void launch_atom_struct(hipStream_t st, const int* offsets, int S, int N, int* sid);
-// out[0..n] = exclusive prefix sums of in[0..n-1]; bit 16 of flag if the total overflows int32.
-// Exclusive scan of n ints into out[0..n] (out[n] = total; flag bit 4 if it
-// overflows int32); scratch holds scan_scratch_bytes(n) bytes.
+// Exclusive scan of n ints into out[0..n] (out[n] = total); when the total
+// overflows int32, flag |= 16 (bit 4).  scratch holds scan_scratch_bytes(n) bytes.
 size_t scan_scratch_bytes(long long n);
 void launch_exclusive_scan(hipStream_t st, const int* in, int n, int* out, int* flag, long long* scratch);
 // geo[e] = (u_x, u_y, u_z, r); B, dB [Ne, nb].  With rc3 > 0 also the

@@ -237,31 +237,30 @@ __device__ __forceinline__ void robust_weight(double z, double tau, double& W, d
 
 constexpr int kRobustMaxGroups = 256;
 
-// Robust multi-task loss (paper Sec. "Multi-task training strategies") over the
-// whole batch (one workgroup; the step runs as one chunk):
+// Robust multi-task loss (paper Sec. "Multi-task training strategies"):
 //   L = (1/S) sum_s W(z_s, tau)^2 L_s,
 //   L_s = w_E rho(E_s/n_s - E_ref,s) + w_F/(3 n_s) sum_{a in s, c} rho(dF_ac) + w_S/9 sum_q rho(dsigma_sq),
 //   z_s = (L_s - mu_g) / sd_g over the structures of task g (one group without tasks; z = 0 where sd_g = 0).
 // The seeds differentiate the weights too: with A_g = sum W W' L and B_g = sum W W' L z over g,
 //   dL/dL_s = (1/S) [W_s^2 + (2/sd_g)(W_s W'_s L_s - A_g/n_g - z_s B_g/n_g)],
-// then lam_s, phi_a, Psi_s by the chain rule through L_s.  rob: 2 S doubles of scratch
-// (L_s, then dL/dL_s).  Every sum runs in a fixed order.
-__global__ void robust_loss_kernel(const double* __restrict__ Ed, const float* __restrict__ Eref,
+// then lam_s, phi_a, Psi_s by the chain rule through L_s.  The statistics couple
+// every structure of a task, so the loss runs in three kernels: the base losses
+// L_s of each chunk's structures (once its forces and stresses exist), the
+// statistics and dL/dL_s over the whole batch, then each chunk's seeds.  Every
+// sum runs in a fixed order.
+
+// L_s of the chunk's S structures into Ls[0..S) (one wave per structure: lanes
+// over force components, then a fixed butterfly).
+__global__ void robust_base_kernel(const double* __restrict__ Ed, const float* __restrict__ Eref,
                                    const int* __restrict__ offsets, int S, const float* __restrict__ F,
-                                   const float* __restrict__ Fref, int N, float wE, float wF,
+                                   const float* __restrict__ Fref, float wE, float wF,
                                    const float* __restrict__ sig, const float* __restrict__ Sref, float wS,
-                                   const float* __restrict__ cell, float delta_f, float tau_f,
-                                   const int* __restrict__ task, int n_groups, const int* __restrict__ sid,
-                                   double* __restrict__ rob, double* __restrict__ loss_part, float* __restrict__ lam,
-                                   float* __restrict__ phi, float* __restrict__ Psi) {
-  __shared__ double gst[kRobustMaxGroups][6];   // mu, sd, A, B, count, sum W^2 L
-  const int t = threadIdx.x;
-  const double delta = (double)delta_f, tau = (double)tau_f;
+                                   float delta_f, double* __restrict__ Ls) {
+  const double delta = (double)delta_f;
+  const int lane = threadIdx.x & 63;
+  const int nw = (gridDim.x * blockDim.x) >> 6;
   double rho, drho;
-  // per-structure base losses, one wave per structure (lanes over force components,
-  // then a fixed butterfly)
-  const int lane = t & 63;
-  for (int s = t >> 6; s < S; s += blockDim.x >> 6) {
+  for (int s = (blockIdx.x * blockDim.x + threadIdx.x) >> 6; s < S; s += nw) {
     const int a0 = offsets[s], a1 = offsets[s + 1];
     const double n = (double)(a1 - a0);
     double rf = 0.0;
@@ -282,27 +281,34 @@ __global__ void robust_loss_kernel(const double* __restrict__ Ed, const float* _
         }
         L += wS * rs / 9.0;
       }
-      rob[s] = L;
+      Ls[s] = L;
     }
   }
-  __syncthreads();
-  // statistics of each task group, structures in order
+}
+
+// Statistics of each task group over the whole batch (structures in order) and
+// c_s = dL/dL_s into c[0..S); the loss into *loss.  One workgroup.
+__global__ void robust_stats_kernel(const double* __restrict__ Ls, int S, const int* __restrict__ task,
+                                    int n_groups, float tau_f, double* __restrict__ c, double* __restrict__ loss) {
+  __shared__ double gst[kRobustMaxGroups][6];   // mu, sd, A, B, count, sum W^2 L
+  const int t = threadIdx.x;
+  const double tau = (double)tau_f;
   for (int g = t; g < n_groups; g += blockDim.x) {
     double cnt = 0.0, sum = 0.0;
     for (int s = 0; s < S; ++s)
       if ((task ? task[s] : 0) == g) {
         cnt += 1.0;
-        sum += rob[s];
+        sum += Ls[s];
       }
     const double mu = cnt > 0.0 ? sum / cnt : 0.0;
     double var = 0.0;
     for (int s = 0; s < S; ++s)
-      if ((task ? task[s] : 0) == g) var += (rob[s] - mu) * (rob[s] - mu);
+      if ((task ? task[s] : 0) == g) var += (Ls[s] - mu) * (Ls[s] - mu);
     const double sd = cnt > 0.0 ? sqrt(var / cnt) : 0.0;
     double A = 0.0, B = 0.0, lw = 0.0;
     for (int s = 0; s < S; ++s)
       if ((task ? task[s] : 0) == g) {
-        const double L = rob[s];
+        const double L = Ls[s];
         const double z = sd > 0.0 ? (L - mu) / sd : 0.0;
         double W, dW;
         robust_weight(z, tau, W, dW);
@@ -313,39 +319,53 @@ __global__ void robust_loss_kernel(const double* __restrict__ Ed, const float* _
     gst[g][0] = mu; gst[g][1] = sd; gst[g][2] = A; gst[g][3] = B; gst[g][4] = cnt; gst[g][5] = lw;
   }
   __syncthreads();
-  // dL/dL_s, then the energy and stress seeds
   for (int s = t; s < S; s += blockDim.x) {
     const int g = task ? task[s] : 0;
-    const double L = rob[s], mu = gst[g][0], sd = gst[g][1];
+    const double L = Ls[s], mu = gst[g][0], sd = gst[g][1];
     const double z = sd > 0.0 ? (L - mu) / sd : 0.0;
     double W, dW;
     robust_weight(z, tau, W, dW);
-    double c = W * W;
-    if (sd > 0.0) c += 2.0 / sd * (W * dW * L - gst[g][2] / gst[g][4] - z * gst[g][3] / gst[g][4]);
-    c /= (double)S;
-    rob[S + s] = c;
-    const double n = (double)(offsets[s + 1] - offsets[s]);
-    huber2(Ed[s] / n - (double)Eref[s], delta, rho, drho);
-    lam[s] = (float)(c * wE * drho / n);
-    if (Sref) {
-      const double iv = 1.0 / cell_volume(cell + 9 * s);
-      for (int q = 0; q < 9; ++q) {
-        huber2((double)sig[9 * s + q] - (double)Sref[9 * s + q], delta, rho, drho);
-        Psi[9 * s + q] = (float)(c * wS / 9.0 * drho * iv);
-      }
-    }
-  }
-  __syncthreads();
-  for (int q = t; q < 3 * N; q += blockDim.x) {
-    const int s = sid[q / 3];
-    const double n = (double)(offsets[s + 1] - offsets[s]);
-    huber2((double)F[q] - (double)Fref[q], delta, rho, drho);
-    phi[q] = (float)(rob[S + s] * wF / (3.0 * n) * drho);
+    double cs = W * W;
+    if (sd > 0.0) cs += 2.0 / sd * (W * dW * L - gst[g][2] / gst[g][4] - z * gst[g][3] / gst[g][4]);
+    c[s] = cs / (double)S;
   }
   if (t == 0) {
     double lw = 0.0;
     for (int g = 0; g < n_groups; ++g) lw += gst[g][5];
-    *loss_part = lw / (double)S;
+    *loss = lw / (double)S;
+  }
+}
+
+// Seeds of the chunk's structures and atoms from c = dL/dL_s (c[0..S), the
+// chunk's slice): lam_s, Psi_s per structure, phi_a per force component.
+__global__ void robust_seed_kernel(const double* __restrict__ Ed, const float* __restrict__ Eref,
+                                   const int* __restrict__ offsets, int S, const float* __restrict__ F,
+                                   const float* __restrict__ Fref, int N, float wE, float wF,
+                                   const float* __restrict__ sig, const float* __restrict__ Sref, float wS,
+                                   const float* __restrict__ cell, float delta_f, const double* __restrict__ c,
+                                   const int* __restrict__ sid, float* __restrict__ lam, float* __restrict__ phi,
+                                   float* __restrict__ Psi) {
+  const double delta = (double)delta_f;
+  const long long t0 = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long nt = (long long)gridDim.x * blockDim.x;
+  double rho, drho;
+  for (long long s = t0; s < S; s += nt) {
+    const double n = (double)(offsets[s + 1] - offsets[s]);
+    huber2(Ed[s] / n - (double)Eref[s], delta, rho, drho);
+    lam[s] = (float)(c[s] * wE * drho / n);
+    if (Sref) {
+      const double iv = 1.0 / cell_volume(cell + 9 * s);
+      for (int q = 0; q < 9; ++q) {
+        huber2((double)sig[9 * s + q] - (double)Sref[9 * s + q], delta, rho, drho);
+        Psi[9 * s + q] = (float)(c[s] * wS / 9.0 * drho * iv);
+      }
+    }
+  }
+  for (long long q = t0; q < 3LL * N; q += nt) {
+    const int s = sid[q / 3];
+    const double n = (double)(offsets[s + 1] - offsets[s]);
+    huber2((double)F[q] - (double)Fref[q], delta, rho, drho);
+    phi[q] = (float)(c[s] * wF / (3.0 * n) * drho);
   }
 }
 
@@ -851,7 +871,6 @@ struct Plan {
   float *B, *dB, *rt, *rbar;
   int *sp_cnt, *sp_off, *sp_atoms;
   float *z, *eps, *lam, *phi, *vt, *Zr, *Tr, *colpart, *sig, *Psi, *gs, *gsb;
-  double* rob;   // robust loss: per-structure losses and their adjoints
   float4* gtan;
   double* Ed;
   float *h, *hh, *hht, *h3;   // [(T+1) or T][N, d]; the final-backward adjoint reuses hh
@@ -967,7 +986,6 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.z = cv.take<float>(Nd);
   p.eps = cv.take<float>(N);
   p.lam = cv.take<float>(S);
-  p.rob = cv.take<double>(2LL * S + 2);
   p.phi = cv.take<float>(3LL * N);
   p.sig = cv.take<float>(9LL * S);
   p.gs = cv.take<float>((long long)S * d + 4);

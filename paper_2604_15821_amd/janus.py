@@ -89,6 +89,8 @@ def _lib():
                                       C.POINTER(Labels), vp, vp, vp, vp, vp, C.POINTER(Debug), vp]
         lib.janus_grouped_gemm.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
         lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
+        lib.janus_wgrad_chunk_rows.argtypes = [i64, i32, i32]
+        lib.janus_wgrad_chunk_rows.restype = i32
         lib.janus_set_workspace_limit.argtypes = [vp, i64]
         lib.janus_set_concurrency.argtypes = [vp, C.c_int]
         lib.janus_last_chunks.argtypes = [vp]
@@ -105,10 +107,19 @@ def exported_symbols():
     lib = _lib()
     names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
              "janus_step_stress", "janus_step_ex",
-             "janus_grouped_gemm", "janus_grouped_wgrad", "janus_profile_enable", "janus_profile_read",
+             "janus_grouped_gemm", "janus_grouped_wgrad", "janus_wgrad_chunk_rows", "janus_profile_enable",
+             "janus_profile_read",
              "janus_set_workspace_limit", "janus_set_concurrency", "janus_last_chunks", "janus_last_triplets",
              "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
+
+
+def wgrad_chunk_rows(M: int, P: int, Q: int) -> int:
+    """Row-chunk length of the weight-gradient contraction over M rows into P x Q blocks."""
+    r = int(_lib().janus_wgrad_chunk_rows(int(M), int(P), int(Q)))
+    if r < 0:
+        raise JanusError(r, "janus_wgrad_chunk_rows")
+    return r
 
 
 def make_config(model) -> Config:
@@ -157,6 +168,36 @@ def _ptr(t):
     return C.c_void_p(0 if t is None else t.data_ptr())
 
 
+_DTYPES = {"f32": "float32", "i32": "int32", "i8": "int8"}
+
+
+def _arg(t, name, kind, shape=None, device=None, optional=False):
+    """Check one tensor argument before its address goes to the library: the
+    library reads raw memory, so a wrong dtype, a strided view, a host tensor or
+    a wrong size would be misread rather than rejected.  `shape` may use None
+    for a free dimension; returns the tensor."""
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name}: required")
+    import torch
+    want = getattr(torch, _DTYPES[kind])
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor, got {type(t).__name__}")
+    if t.dtype != want:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected {want}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: must be a device tensor (got {t.device})")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name}: on {t.device}, expected {device}")
+    if shape is not None:
+        if t.dim() != len(shape) or any(w is not None and int(n) != int(w) for n, w in zip(t.shape, shape)):
+            raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
 def _stream():
     import torch
     return C.c_void_p(torch.cuda.current_stream().cuda_stream)
@@ -180,6 +221,11 @@ class Context:
     """A libjanus context on the current device."""
 
     def __init__(self, model):
+        import torch
+        # PyTorch carries its own HIP runtime next to the library's; when the library's
+        # initialises first, PyTorch's then finds no device, so PyTorch goes first
+        if torch.cuda.is_available():
+            torch.cuda.current_device()
         self.model = model
         self.cfg = make_config(model)
         h = C.c_void_p()
@@ -187,6 +233,7 @@ class Context:
         if rc:
             raise JanusError(rc, "janus_create")
         self.h = h
+        self.n_weights = weight_layout(model)[1]
         self.capacity = 0
         self._nl_bufs = None
 
@@ -210,6 +257,7 @@ class Context:
         dev = pos.device
         N = pos.shape[0]
         S = cell.shape[0]
+        self._check_geometry(pos, cell, offsets)
         rowptr = torch.empty(N + 1, dtype=torch.int32, device=dev)
         ne = C.c_int64(0)
         cap = int(capacity if capacity is not None else max(self.capacity, 1))
@@ -235,12 +283,58 @@ class Context:
         """Rebuild into existing buffers (capacity = their size); returns the edge count."""
         ne = C.c_int64(0)
         cap = int(nl.ei.shape[0])
+        self._check_geometry(pos, cell, offsets)
+        self._check_edges(nl, pos.shape[0], pos.device, room=True)
         rc = _lib().janus_build_edges(self.h, _ptr(pos), _ptr(cell), _ptr(offsets), pos.shape[0], cell.shape[0],
                                       cap, _ptr(nl.ei), _ptr(nl.ej), _ptr(nl.shift), _ptr(nl.rowptr), _ptr(nl.rev),
                                       C.byref(ne), _stream())
         if rc:
             raise JanusError(rc, "janus_build_edges")
         return int(ne.value)
+
+    # ------------------------------------------------------- argument checks
+    @staticmethod
+    def _check_geometry(pos, cell, offsets):
+        dev = pos.device
+        _arg(pos, "pos", "f32", (None, 3))
+        _arg(cell, "cell", "f32", (None, 3, 3), dev)
+        _arg(offsets, "offsets", "i32", (cell.shape[0] + 1,), dev)
+
+    @staticmethod
+    def _check_edges(nl, N, dev, room=False):
+        """Edge arrays of a neighbour list: [Ne] each ([capacity] with room=True: the
+        buffers a rebuild writes into), shift [Ne, 3], rowptr [N+1]."""
+        n = int(nl.ei.shape[0]) if room else nl.n_edges
+        _arg(nl.rowptr, "nl.rowptr", "i32", (N + 1,), dev)
+        for name, t in (("nl.ei", nl.ei), ("nl.ej", nl.ej), ("nl.rev", nl.rev)):
+            _arg(t, name, "i32", (n,), dev)
+        sh = nl.shift.reshape(-1) if nl.shift is not None and nl.shift.is_contiguous() else nl.shift
+        _arg(sh, "nl.shift", "i8", (3 * n,), dev)
+
+    def _check_step(self, pos, cell, species, offsets, nl, W, E_ref, F_ref, out, S_ref, stress, labels):
+        m = self.model
+        dev = pos.device
+        self._check_geometry(pos, cell, offsets)
+        N, S = pos.shape[0], cell.shape[0]
+        _arg(species, "species", "i32", (N,), dev)
+        self._check_edges(nl, N, dev)
+        total = self.n_weights
+        _arg(W, "W", "f32", (total,), dev)
+        _arg(E_ref, "E_ref", "f32", (S,), dev)
+        _arg(F_ref, "F_ref", "f32", (N, 3), dev)
+        # a missing S_ref (with w_S > 0) or missing labels (with n_tasks > 0) is the library's
+        # JANUS_EINVAL; only the layout of what is passed is checked here
+        _arg(S_ref, "S_ref", "f32", (S, 3, 3), dev, optional=True)
+        _arg(stress, "stress", "f32", (S, 3, 3), dev, optional=True)
+        if out is not None:
+            loss, E, F, dW = out
+            _arg(loss, "loss", "f32", (1,), dev)
+            _arg(E, "E", "f32", (S,), dev)
+            _arg(F, "F", "f32", (N, 3), dev)
+            _arg(dW, "dLdW", "f32", (total,), dev)
+        if labels is not None:
+            for name, t in zip(("task", "charge", "spin"), labels):
+                _arg(t, f"labels.{name}", "i32", (S,), dev)
 
     # ----------------------------------------------------------------- step
     def step(self, pos, cell, species, offsets, nl: NeighborList, W, E_ref, F_ref, out=None, debug=None,
@@ -254,6 +348,7 @@ class Context:
         dev = pos.device
         N = pos.shape[0]
         S = cell.shape[0]
+        self._check_step(pos, cell, species, offsets, nl, W, E_ref, F_ref, out, S_ref, stress, labels)
         if out is None:
             out = (torch.empty(1, dtype=torch.float32, device=dev), torch.empty(S, dtype=torch.float32, device=dev),
                    torch.empty(N, 3, dtype=torch.float32, device=dev), torch.empty_like(W))
@@ -325,8 +420,14 @@ class Context:
     def grouped_gemm(self, A, B, row_off, K, N, trans_b, out=None):
         import torch
         M = A.shape[0]
+        dev = A.device
+        G = row_off.shape[0] - 1
+        _arg(A, "A", "f32", (M, K))
+        _arg(B, "B", "f32", (G, N, K) if trans_b else (G, K, N), dev)
+        _arg(row_off, "row_off", "i32", (G + 1,), dev)
         if out is None:
             out = torch.empty(M, N, dtype=torch.float32, device=A.device)
+        _arg(out, "out", "f32", (M, N), dev)
         rc = _lib().janus_grouped_gemm(self.h, _ptr(A), _ptr(B), _ptr(out), _ptr(row_off), row_off.shape[0] - 1, M,
                                        K, N, int(trans_b), _stream())
         if rc:
@@ -338,8 +439,13 @@ class Context:
         M, P = A.shape
         Q = B.shape[1]
         G = row_off.shape[0] - 1
+        dev = A.device
+        _arg(A, "A", "f32", (M, P))
+        _arg(B, "B", "f32", (M, Q), dev)
+        _arg(row_off, "row_off", "i32", (G + 1,), dev)
         if out is None:
             out = torch.empty(G, P, Q, dtype=torch.float32, device=A.device)
+        _arg(out, "out", "f32", (G, P, Q), dev)
         rc = _lib().janus_grouped_wgrad(self.h, _ptr(A), _ptr(B), _ptr(out), _ptr(row_off), G, M, P, Q, _stream())
         if rc:
             raise JanusError(rc, "janus_grouped_wgrad")

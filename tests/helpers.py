@@ -36,3 +36,19 @@ TOL_E = 1e-5
 TOL_LOSS = 1e-5
 TOL_F = 1e-3
 TOL_W = 1e-3
+
+
+def sketch_keys(seed, index, n, K):
+    """Bucket and sign of every entry for the count sketch of tensor number `index`
+    (seeded, so the expected sketch can be stored and the measured one recomputed)."""
+    rng = np.random.default_rng([seed, index])
+    return rng.integers(0, K, n), rng.integers(0, 2, n) * 2.0 - 1.0
+
+
+def count_sketch(x, keys, K):
+    """Linear sketch of a tensor: bucket k holds the sum of s_i x_i over the entries i
+    hashed to k.  For any vector v, |sketch(v)|^2 is an unbiased estimate of |v|^2 with
+    relative standard deviation at most sqrt(2 / K), so |sketch(a) - sketch(b)| estimates
+    |a - b| (the relative L2 error of a stored tensor) without storing the tensor."""
+    h, s = keys
+    return np.bincount(h, weights=s * np.asarray(x, np.float64).ravel(), minlength=K)

@@ -83,3 +83,38 @@ def test_concurrency_switch_rejects_bad_arguments():
     lib = C.CDLL(janus.LIB_PATH)
     lib.janus_set_concurrency.argtypes = [C.c_void_p, C.c_int]
     assert lib.janus_set_concurrency(None, 1) == janus.JANUS_EINVAL
+
+
+def test_binding_rejects_misfit_tensors_before_the_library():
+    """The library reads raw memory, so the binding refuses a wrong dtype, a strided
+    view or a host tensor instead of passing its address."""
+    import torch
+    pos = torch.zeros(4, 3)
+    with pytest.raises(TypeError):
+        janus._arg(pos.double(), "pos", "f32", (None, 3))
+    with pytest.raises(TypeError):
+        janus._arg(torch.zeros(3, dtype=torch.int64), "offsets", "i32", (3,))
+    with pytest.raises(ValueError, match="contiguous"):
+        janus._arg(torch.zeros(3, 4).t(), "pos", "f32", (None, 3))
+    with pytest.raises(ValueError, match="device"):
+        janus._arg(pos, "pos", "f32", (None, 3))
+    with pytest.raises(ValueError, match="device"):
+        janus.Context._check_geometry(pos, torch.zeros(1, 3, 3), torch.zeros(2, dtype=torch.int32))
+    assert janus._arg(None, "stress", "f32", optional=True) is None
+    with pytest.raises(ValueError):
+        janus._arg(None, "W", "f32")
+
+
+def test_wgrad_chunk_rule():
+    """Chunk length of the weight-gradient contraction: 512 rows for the small batch's
+    expert products (337,996 slot rows, 128 x 512 blocks), 16384 at the full-size
+    expert shape (over a million rows, 512 x 2048 blocks), bounds 128 and 16384."""
+    assert janus.wgrad_chunk_rows(337_996, 128, 512) == 512
+    assert janus.wgrad_chunk_rows(1_200_000, 512, 2048) == 16384
+    assert janus.wgrad_chunk_rows(2_000_000, 2048, 512) == 16384
+    assert janus.wgrad_chunk_rows(100, 64, 64) == 128
+    assert janus.wgrad_chunk_rows(0, 64, 64) == 128
+    with pytest.raises(janus.JanusError):
+        janus.wgrad_chunk_rows(-1, 64, 64)
+    with pytest.raises(janus.JanusError):
+        janus.wgrad_chunk_rows(10, 0, 64)

@@ -120,3 +120,42 @@ def test_neighbourhood_too_large_is_rejected():
     with pytest.raises(janus.JanusError) as ex:
         _run(b)
     assert ex.value.code == janus.JANUS_EUNSUPPORTED
+
+
+def test_edges_beyond_the_cutoff_contribute_nothing():
+    """A caller's list may hold edges at or past r_cut (a Verlet list with a skin): their
+    basis and attention envelope are zero, so the step equals the oracle's on its own list
+    of edges shorter than r_cut.  The list here is built with a 0.8 A skin (about 1.5x the
+    edges, so some neighbourhoods pass 64 edges and use the vector-unit kernels)."""
+    import torch
+    from oracle.model import Params, forward_energy, training_step
+    from paper_2604_15821_amd import janus
+    b = _batch("attention-4")
+    m = b.model
+    banner("attention, list with a skin beyond r_cut", b.n_struct, "structures")
+    loss, E, F, grad, aux = training_step(b, return_aux=True)
+    _, cache = forward_energy(b.species, aux["graph"], Params.from_weights(b.weights, m), aux["routing"])
+    d = janus.upload(b)
+    skin = janus.Context(dataclasses.replace(m, r_cut=m.r_cut + 0.8))
+    ctx = janus.Context(m)
+    try:
+        nl = skin.build_edges(d["pos"], d["cell"], d["offsets"])
+        deg = np.diff(nl.rowptr.cpu().numpy())
+        print(f"  {nl.n_edges} edges with the skin (oracle: {aux['graph'].ei.size}), "
+              f"neighbourhoods {deg.min()}..{deg.max()}", flush=True)
+        assert nl.n_edges > 1.3 * aux["graph"].ei.size and deg.max() > 64
+        g_loss, g_E, g_F, g_W = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"],
+                                         d["F_ref"])
+        torch.cuda.synchronize()
+        g_loss, g_E, g_F, g_W = float(g_loss.cpu()[0]), g_E.cpu().numpy(), g_F.cpu().numpy(), g_W.cpu().numpy()
+    finally:
+        ctx.close()
+        skin.close()
+    assert np.isfinite(g_F).all() and np.isfinite(g_W).all()
+    assert energy_error(g_E, E, cache["eps"], b.offsets) <= TOL_E
+    assert abs(g_loss - loss) <= TOL_LOSS * abs(loss)
+    assert rel_l2(g_F, F) <= TOL_F
+    got = janus.unpack(g_W, m)
+    worst = max(rel_l2(got[k], ref) for k, ref in grad.items() if k.rsplit(".", 1)[-1] not in FIXED)
+    print(f"  worst dW rel L2 {worst:.2e}", flush=True)
+    assert worst <= TOL_W

@@ -1,8 +1,7 @@
 """Robust multi-task loss (paper Sec. "Multi-task training strategies") on the GPU
 against the float64 oracle: loss and energy 1e-5 relative, forces and every weight
 gradient 1e-3 relative L2, with structures down-weighted by the soft threshold, with
-and without per-task statistics; a step that would need several workspace chunks is
-rejected."""
+and without per-task statistics, in one workspace chunk and split over several."""
 import dataclasses
 
 import numpy as np
@@ -90,13 +89,57 @@ def test_weight_gradients(case):
     assert max(worst.values()) <= TOL_W, worst
 
 
-def test_chunked_robust_step_is_rejected():
+def _run_chunked(b, min_chunks):
+    """_run with the smallest of a few workspace caps that splits b into at least min_chunks."""
+    import torch
     from paper_2604_15821_amd import janus
-    b = _batch("small-8")
-    banner("robust chunked")
-    with pytest.raises(janus.JanusError) as ex:
-        _run(b, limit=int(2.5 * 1.1e8))
-    assert ex.value.code == janus.JANUS_EUNSUPPORTED
+    d = janus.upload(b)
+    for limit in (1.0e8, 1.4e8, 2.0e8, 2.8e8, 4.0e8, 5.6e8):
+        ctx = janus.Context(b.model)
+        try:
+            ctx.set_workspace_limit(int(limit))
+            nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+            loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"],
+                                      d["F_ref"], S_ref=d["S_ref"] if b.model.w_S else None, labels=d["labels"])
+            torch.cuda.synchronize()
+            chunks = ctx.last_chunks()
+        except janus.JanusError as ex:
+            assert ex.code == janus.JANUS_ENOMEM
+            continue
+        finally:
+            ctx.close()
+        if chunks >= min_chunks:
+            print("  workspace cap", limit, "->", chunks, "chunks", flush=True)
+            return chunks, (float(loss.cpu()[0]), E.cpu().numpy(), F.cpu().numpy(), dW.cpu().numpy())
+    raise AssertionError("no cap gave enough chunks")
+
+
+@pytest.mark.parametrize("name", ["small-8", "robust-12"])
+def test_chunked_robust_step_matches_single_pass_and_oracle(name):
+    """With the batch split over workspace chunks the robust loss runs in two passes
+    (base losses of every chunk, batch statistics, then each chunk's four phases):
+    energies and forces bitwise equal to the one-chunk step, loss and weight gradients
+    equal up to summation order, and everything within tolerance of the oracle."""
+    from oracle.model import Params, forward_energy, training_step
+    from paper_2604_15821_amd import janus
+    b = _batch(name)
+    banner("robust chunked", name)
+    one = _run(b)
+    chunks, many = _run_chunked(b, 3)
+    assert chunks >= 3
+    assert (one[1] == many[1]).all() and (one[2] == many[2]).all()
+    assert abs(one[0] - many[0]) <= 1e-6 * abs(one[0])
+    assert rel_l2(many[3], one[3]) <= 1e-5
+    loss, E, F, grad, aux = training_step(b, return_aux=True)
+    _, cache = forward_energy(b.species, aux["graph"], Params.from_weights(b.weights, b.model), aux["routing"])
+    g_loss, g_E, g_F, g_W = many
+    assert energy_error(g_E, E, cache["eps"], b.offsets) <= TOL_E
+    assert abs(g_loss - loss) <= TOL_LOSS * abs(loss)
+    assert rel_l2(g_F, F) <= TOL_F
+    got = janus.unpack(g_W, b.model)
+    worst = max(rel_l2(got[k], ref) for k, ref in grad.items() if k.rsplit(".", 1)[-1] not in FIXED)
+    print("  worst dW rel L2", worst, flush=True)
+    assert worst <= TOL_W
 
 
 def test_full_size_against_oracle():
@@ -118,3 +161,59 @@ def test_full_size_against_oracle():
     worst = max(rel_l2(got[k], ref) for k, ref in grad.items() if k.rsplit(".", 1)[-1] not in FIXED)
     print("worst dW rel L2", worst)
     assert worst <= TOL_W
+
+
+def test_robust_loss_on_the_irregular_batch():
+    """The robust loss on the 512-structure irregular batch (59 k atoms, several
+    workspace chunks): finite outputs; the loss equals the robust loss recomputed in
+    float64 from the returned energies and forces; a finer chunking gives bitwise equal
+    energies and forces and the same loss and weight gradient up to summation order."""
+    import torch
+    from paper_2604_15821_amd import janus
+    from paper_2604_15821_amd.synth import make_batch
+    b = make_batch("irregular")
+    m = dataclasses.replace(b.model, robust=1, huber_delta=1.0, robust_tau=1.0)
+    b = dataclasses.replace(b, model=m)
+    d = janus.upload(b)
+    outs = []
+    for limit in (0, None):
+        ctx = janus.Context(m)
+        try:
+            if limit is None:
+                ctx.set_workspace_limit(120 << 30)
+            nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+            banner("robust irregular", "default workspace" if limit == 0 else "finer chunks")
+            loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"],
+                                      d["F_ref"])
+            torch.cuda.synchronize()
+            chunks = ctx.last_chunks()
+            outs.append((float(loss.cpu()[0]), E.cpu().numpy(), F.cpu().numpy(), dW.cpu().numpy(), chunks))
+            print(f"  {chunks} chunks, loss {outs[-1][0]:.6g}", flush=True)
+            del loss, E, F, dW, nl
+        finally:
+            ctx.close()
+        torch.cuda.empty_cache()
+    (l0, E0, F0, W0, c0), (l1, E1, F1, W1, c1) = outs
+    assert c0 >= 2 and c1 > c0
+    assert np.isfinite(E0).all() and np.isfinite(F0).all() and np.isfinite(W0).all()
+    assert (E0 == E1).all() and (F0 == F1).all()
+    assert abs(l0 - l1) <= 1e-6 * abs(l0)
+    assert rel_l2(W1, W0) <= 1e-5
+    # the robust loss of the returned energies and forces (one task group)
+    n = np.diff(b.offsets).astype(np.float64)
+    delta = 1.0
+
+    def rho(r):
+        a = np.abs(r)
+        return np.where(a <= delta, r * r, 2 * delta * a - delta * delta)
+
+    de = E0.astype(np.float64) / n - b.E_ref.astype(np.float64)
+    rf = rho(F0.astype(np.float64) - b.F_ref.astype(np.float64)).sum(1)
+    Ls = m.w_E * rho(de) + m.w_F * np.add.reduceat(rf, b.offsets[:-1]) / (3.0 * n)
+    z = (Ls - Ls.mean()) / Ls.std()
+    W = np.exp(-0.5 * np.maximum(z - m.robust_tau, 0.0) ** 2)
+    ref = float((W * W * Ls).sum() / b.n_struct)
+    print(f"  loss {l0:.8g}, recomputed {ref:.8g}, down-weighted structures {(W < 1).sum()}", flush=True)
+    assert (W < 1).any()
+    assert abs(l0 - ref) <= 1e-5 * abs(ref)
+
