@@ -24,7 +24,8 @@ definition of the quantity it returns:
   tangent      o-dot for input tangents (q, k, v, lu)-dot
   backward     adjoints of q, k, v and lu for an adjoint of o
   dual_reverse adjoints of the primal and tangent inputs for adjoints of
-               o and of o-dot (the reverse sweep through both).
+               o and of o-dot (the reverse sweep through both), optionally
+               including the key weights lu and their tangents rho.
 """
 from __future__ import annotations
 
@@ -65,9 +66,10 @@ def backward(q, k, v, lu, ob):
     return zb @ k / c, zb.T @ q / c, p.T @ ob, zb.sum(0)
 
 
-def dual_reverse(q, k, v, lu, qd, kd, vd, rho, Po, To):
+def dual_reverse(q, k, v, lu, qd, kd, vd, rho, Po, To, key_bias=False):
     """Reverse sweep through (o, o-dot) = tangent(...): Po, To are the adjoints of o and
-    o-dot.  Returns the adjoints of (q, k, v) and of (qd, kd, vd)."""
+    o-dot.  Returns the adjoints of (q, k, v) and of (qd, kd, vd); with key_bias, also
+    those of the key weights lu and of their tangents rho, each [n]."""
     c = np.sqrt(q.shape[1])
     p = weights(q, k, lu)
     zd = (qd @ k.T + q @ kd.T) / c + rho[None, :]
@@ -87,4 +89,7 @@ def dual_reverse(q, k, v, lu, qd, kd, vd, rho, Po, To):
     kb = (zb.T @ q + zdb.T @ qd) / c
     qdb = zdb @ k / c
     kdb = zdb.T @ q / c
+    if key_bias:
+        # z = q k^T / c + lu (per key), zd = (...) / c + rho (per key)
+        return (qb, kb, vb), (qdb, kdb, vdb), (zb.sum(0), zdb.sum(0))
     return (qb, kb, vb), (qdb, kdb, vdb)

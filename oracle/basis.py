@@ -113,6 +113,18 @@ def silu_family(a):
     return _rowwise(_silu_family, np.asarray(a, np.float64), 3)
 
 
+def legendre2(x, n_l):
+    """P_l(x), P_l'(x) and P_l''(x) for l = 0..n_l-1 -> [M, n_l] each: the Bonnet
+    recurrence and its derivatives, (d/dx) P_{l+1} = (l+1) P_l + x P_l' and
+    (d2/dx2) P_{l+1} = (l+2) P_l' + x P_l''."""
+    P, dP = legendre(x, n_l)
+    x = np.asarray(x, np.float64)
+    d2P = np.zeros(x.shape + (n_l,))
+    for l in range(1, n_l - 1):
+        d2P[..., l + 1] = (l + 2) * dP[..., l] + x * d2P[..., l]
+    return P, dP, d2P
+
+
 def legendre(x, n_l):
     """P_l(x) and P_l'(x) for l = 0..n_l-1 (Bonnet recurrence) -> [M, n_l] each."""
     x = np.asarray(x, np.float64)

@@ -397,9 +397,12 @@ def _attn_tangent(g, P, t, m, md, lu, rho, N):
     return osum, osumd
 
 
-def _attn_reverse(g, P, t, m, md, lu, rho, Pu, Tu, N):
+def _attn_reverse(g, P, t, m, md, lu, rho, Pu, Tu, N, bias=None):
     """Reverse sweep of u = h + osum Wo, ud = hd + osumd Wo through the attention:
-    returns the adjoints of the messages and of their tangents, dWqkv and dWo."""
+    returns the adjoints of the messages and of their tangents, dWqkv and dWo.  With
+    bias = (Plu, Trho) (arrays [Ne]), also adds the adjoints of every edge's log
+    envelope lu and of its tangent rho (as a key inside the softmax and as the query
+    weight u = exp(lu))."""
     d = m.shape[1]
     Wqkv, Wo = P.blk(t, "Wqkv"), P.blk(t, "Wo")
     QKV, QKVd = m @ Wqkv, md @ Wqkv
@@ -412,10 +415,17 @@ def _attn_reverse(g, P, t, m, md, lu, rho, Pu, Tu, N):
         # osum = sum u o, osumd = sum u od + u rho o: adjoints of o and od per query
         uq = np.exp(l)[:, None]
         A, B = Po[i, cols][None, :], To[i, cols][None, :]
-        (qb, kb, vb), (qdb, kdb, vdb) = attn.dual_reverse(q, k, v, l, qd, kd, vd, r,
-                                                          uq * (A + r[:, None] * B), uq * B)
+        res = attn.dual_reverse(q, k, v, l, qd, kd, vd, r, uq * (A + r[:, None] * B), uq * B,
+                                key_bias=bias is not None)
+        (qb, kb, vb), (qdb, kdb, vdb) = res[0], res[1]
         PQ[a:b, cols], PQ[a:b, d + cols], PQ[a:b, 2 * d + cols] = qb, kb, vb
         TQ[a:b, cols], TQ[a:b, d + cols], TQ[a:b, 2 * d + cols] = qdb, kdb, vdb
+        if bias is not None:
+            # osum = sum_e u_e o_e, osumd = sum_e u_e (od_e + rho_e o_e), u_e = exp(lu_e)
+            o, od = attn.tangent(q, k, v, l, qd, kd, vd, r)
+            oA, oB, odB = (o * A).sum(1), (o * B).sum(1), (od * B).sum(1)
+            bias[0][a:b] += res[2][0] + uq[:, 0] * (oA + odB + r * oB)
+            bias[1][a:b] += res[2][1] + uq[:, 0] * oB
     _attn_heads(g, P, fn, N, QKV, QKVd, lu, rho)
     dWqkv = m.T @ PQ + md.T @ TQ
     return PQ @ Wqkv.T, TQ @ Wqkv.T, dWqkv, dWo
@@ -756,11 +766,14 @@ def _logit_adjoint(rt, Pg):
     return rt.prob * (Pp - (rt.prob * Pp).sum(1, keepdims=True))
 
 
-def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
+def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None, geo=None):
     """dL/dtheta = d/dtheta [sum_s lam_s E_s - D_phi E] by reverse over the tangent sweep
     (with Psi, the tangent also carries the strain direction of the stress seeds).
 
-    Adjoint names: Pq is the adjoint of primal q, Tq the adjoint of tangent q.
+    Adjoint names: Pq is the adjoint of primal q, Tq the adjoint of tangent q.  With a
+    dict `geo`, the same sweep also leaves there the adjoints of the geometric inputs
+    of the bracket: B and Bd = B' rdot [Ne, Nb], with the three-body term G and Gd
+    [Nt, L*Nb], with attention the log envelope lu and its tangent rho [Ne].
     """
     N = species.shape[0]
     Ne = g.ei.shape[0]
@@ -770,6 +783,12 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
     grad = {n: np.zeros_like(v) for n, v in P.w.items()}
     S_ = P.w["A"].shape[0]
 
+    if geo is not None:
+        geo["B"], geo["Bd"] = np.zeros_like(g.B), np.zeros_like(g.B)
+        if g.tri is not None:
+            geo["G"], geo["Gd"] = np.zeros_like(g.tri.G), np.zeros_like(g.tri.G)
+        if P.heads:
+            geo["lu"], geo["rho"] = np.zeros(Ne), np.zeros(Ne)
     lam_atom = lam[g.struct_of_atom][:, None]
     # Psi = sum_i lam_s(i) w_o2.SiLU(z_i) - sum_i w_o2.(SiLU'(z_i) zd_i)
     Pz = lam_atom * silu_d1(z) * wo2 - silu_d2(z) * zd * wo2
@@ -793,7 +812,8 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
         if P.heads:
             m, md = _moe_tangent(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd)
             lu, dlu = _attn_env(g, P)
-            Pm, Tm, dWqkv, dWo = _attn_reverse(g, P, t, m, md, lu, dlu * tc["rdot"], Ph, Th, N)
+            Pm, Tm, dWqkv, dWo = _attn_reverse(g, P, t, m, md, lu, dlu * tc["rdot"], Ph, Th, N,
+                                               bias=None if geo is None else (geo["lu"], geo["rho"]))
             grad[f"blocks.{t}.Wqkv"] = dWqkv
             grad[f"blocks.{t}.Wo"] = dWo
         else:
@@ -805,6 +825,9 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
         PF = PX * h[g.ej] + TX * hd[g.ej]
         TFd = TX * h[g.ej]
         grad[f"blocks.{t}.W_b"] = g.B.T @ PF + Bdot.T @ TFd
+        if geo is not None:
+            geo["B"] += PF @ P.blk(t, "W_b").T
+            geo["Bd"] += TFd @ P.blk(t, "W_b").T
         Ph_new = Ph + _seg(g.ej, N, PX * F + TX * Fd)
         Th_new = Th + _seg(g.ej, N, TX * F)
         # gates: g_ec = softmax(l_e)[eid_ec];  l_e = Pc[Z_i] + Pn[Z_j] + beta
@@ -823,6 +846,9 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
             PZpre = PZ * hj2 + TZ * hdj2
             TZpred = TZ * hj2
             grad[f"blocks.{t}.W_a"] = tri.G.T @ PZpre + Gd.T @ TZpred
+            if geo is not None:
+                geo["G"] += PZpre @ P.blk(t, "W_a").T
+                geo["Gd"] += TZpred @ P.blk(t, "W_a").T
             j2 = g.ej[tri.te2]
             Ph_new = Ph_new + _seg(j2, N, PZ * Zpre + TZ * Zpred)
             Th_new = Th_new + _seg(j2, N, TZ * Zpre)
@@ -843,14 +869,61 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None):
     return grad
 
 
+def position_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None, model=None):
+    """dL/dR [N, 3] with lam = dL/dE, phi = dL/dF (and Psi = dL/dsigma / V) held fixed.
+
+    Paper Sec. "MatRIS": F = -dE/dR and the stress are derivatives of E, so with the
+    seeds frozen the loss varies with the positions like
+        Phi = sum_s lam_s E_s - D E,   D E = sum_e G_e . ddot_e,
+        ddot_e = phi_j - phi_i - Psi_s d_e,
+    because -D E = sum_a phi_a . F_a + sum_s psi_s : sigma_s.  Phi is the bracket whose
+    weight gradient weight_gradient takes, so the same reverse sweep through the primal
+    and tangent quantities gives the adjoints of its geometric inputs (B, Bd = B' rdot,
+    and with the options G, Gd, lu, rho); the chain rule through
+        r_e = |d_e|, rdot_e = u_e . ddot_e, Bd = B'(r) rdot  (B'' enters here),
+        lu = log u(r / r_c), rho = (d lu / dr) rdot,
+    and the triplet features (their second partial derivatives enter through Gd) then
+    gives dL/dd_e, and dL/dR_a = sum_{e: j(e) = a} dL/dd_e - sum_{e: i(e) = a} dL/dd_e.
+    """
+    N = species.shape[0]
+    Ne = g.ei.shape[0]
+    geo = {}
+    grad = weight_gradient(species, g, P, routing, lam, phi, Psi, geo=geo)
+    ddot = displacement_tangent(g, phi, Psi)
+    rdot = (ddot * g.u).sum(1)
+    nb = g.B.shape[1]
+    _, dB, d2B = bessel_basis(g.r, P.r_cut, nb)
+    adj_r = (geo["B"] * dB).sum(1) + rdot * (geo["Bd"] * d2B).sum(1)
+    adj_rdot = (geo["Bd"] * dB).sum(1)
+    if P.heads:
+        u, du, d2u = envelope(g.r / P.r_cut)
+        dlu = du / (u * P.r_cut)                                   # d log u / dr
+        d2lu = (d2u / u - (du / u) ** 2) / P.r_cut ** 2
+        adj_r = adj_r + geo["lu"] * dlu + geo["rho"] * rdot * d2lu
+        adj_rdot = adj_rdot + geo["rho"] * dlu
+    # rdot_e = u_e . ddot_e:  d rdot / d d_e = (ddot - rdot u) / r - Psi^T u
+    Psi_e = None if Psi is None else Psi[g.struct_of_atom[g.ei]]
+    grad_rdot = (ddot - rdot[:, None] * g.u) / g.r[:, None]
+    if Psi_e is not None:
+        grad_rdot = grad_rdot - np.einsum("eba,eb->ea", Psi_e, g.u)
+    adj_d = adj_r[:, None] * g.u + adj_rdot[:, None] * grad_rdot
+    if g.tri is not None:
+        m = model
+        adj_d = adj_d + tb.displacement_adjoint(g.tri, g.r, g.u, geo["G"], Ne)
+        adj_d = adj_d + tb.tangent_displacement_adjoint(g.tri, g.r, g.u, ddot, Psi_e, geo["Gd"], m.r_cut3,
+                                                        m.n_rbf, m.n_legendre, Ne)
+    return _seg(g.ej, N, adj_d) - _seg(g.ei, N, adj_d), grad
+
+
 # --------------------------------------------------------------------------- one step
 
-def training_step(batch, edges=None, return_aux=False):
+def training_step(batch, edges=None, return_aux=False, positions=False):
     """One full training step on a synthetic batch.
 
     Returns loss, E [S], F [N,3], grad (dict name -> float64 array with the
     weight's shape).  With return_aux, also the graph, the routing and the
-    stress [S,3,3].  With w_S > 0 the loss has the stress term.
+    stress [S,3,3].  With w_S > 0 the loss has the stress term.  With positions,
+    the aux dict also holds dL/dR [N,3] (position_gradient).
     """
     m = batch.model
     P = Params.from_weights(batch.weights, m)
@@ -874,10 +947,14 @@ def training_step(batch, edges=None, return_aux=False):
             loss_S, psi = stress_loss_and_seed(sigma, batch.S_ref, E.shape[0], m.w_S)
             loss = loss + loss_S
             Psi = psi / np.abs(np.linalg.det(np.asarray(batch.cell, np.float64)))[:, None, None]
-    grad = weight_gradient(batch.species, g, P, routing, lam, phi, Psi)
+    dLdR = None
+    if positions:
+        dLdR, grad = position_gradient(batch.species, g, P, routing, lam, phi, Psi, model=m)
+    else:
+        grad = weight_gradient(batch.species, g, P, routing, lam, phi, Psi)
     if return_aux:
         return loss, E, F, grad, {"graph": g, "routing": routing, "lam": lam, "phi": phi, "stress": sigma,
-                                  "Psi": Psi}
+                                  "Psi": Psi, "dLdR": dLdR}
     return loss, E, F, grad
 
 
