@@ -407,6 +407,25 @@ int janus_grouped_wgrad(janus_ctx* ctx, const float* A, const float* B, float* G
                         void* stream);
 
 /*
+ * janus_grouped_gemm that allocates nothing, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and errors as
+ * janus_grouped_gemm, without the context; runs on the current device.  The
+ * tile table lives in a fixed 4 MiB device array of the library (one per
+ * device, held from the first call on that device until the process ends;
+ * that first call looks up its address, a host-side query), so
+ *   ceil(M / 128) + n_groups <= 262128
+ * (about 33.5 M rows); larger sizes return JANUS_ENOMEM before any launch.
+ * Every call on a device shares its array: calls that overlap on one device
+ * (concurrent streams, or host threads) race on it and must be serialised by
+ * the caller.  Each call rewrites every table entry it reads, so nothing
+ * needs clearing between calls.
+ */
+int janus_grouped_gemm_noalloc(const float* A, const float* B, float* C, const int32_t* row_off,
+                               int32_t n_groups, int64_t M, int32_t K, int32_t N, int32_t trans_b,
+                               void* stream);
+
+/*
  * Row-chunk length that janus_grouped_wgrad and the expert weight gradients
  * of janus_step use for a contraction over M rows into P x Q blocks (host
  * function, no device work): a power of two from 128 to 16384.  The chunk

@@ -24,7 +24,8 @@ extern "C" const char* janus_strerror(int code) {
     case JANUS_OK: return "ok";
     case JANUS_EINVAL: return "invalid argument (sizes, offsets, species or edge indices)";
     case JANUS_ECAPACITY: return "edge buffers too small";
-    case JANUS_ENOMEM: return "device allocation failed or a structure does not fit the workspace";
+    case JANUS_ENOMEM:
+      return "device allocation failed, a structure does not fit the workspace, or the sizes exceed a fixed scratch";
     case JANUS_EHIP: return "HIP runtime error";
     case JANUS_EUNSUPPORTED: return "configuration or input not supported by this library";
     default: return "unknown error";

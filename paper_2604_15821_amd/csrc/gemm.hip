@@ -1,5 +1,6 @@
 // Tables, chunk reduction and the standalone grouped-GEMM entry points.
 #include <cstring>
+#include <mutex>
 
 #include "internal.h"
 
@@ -162,6 +163,69 @@ extern "C" int janus_grouped_gemm(janus_ctx* ctx, const float* A, const float* B
   Carver c2(ctx->aux.ptr);
   RowsTile* tiles = c2.take<RowsTile>(mt);
   int* nt = c2.take<int>(1);
+  build_tables(st, row_off, n_groups, 0, tiles, nt, nullptr, nullptr, nullptr);
+  if (trans_b)
+    launch_rows<true>(st, LoadPlain{A, K}, B, K, N, tiles, nt, mt, EpiStore{C, N});
+  else
+    launch_rows<false>(st, LoadPlain{A, K}, B, K, N, tiles, nt, mt, EpiStore{C, N});
+  JANUS_HIP_TRY(hipGetLastError());
+  return JANUS_OK;
+}
+
+// Fixed scratch of janus_grouped_gemm_noalloc: the tile table and its count.
+// One copy per device, allocated with the library's code object on that
+// device and held until the process ends; host code uses only the address
+// returned by hipGetSymbolAddress for the current device, never the symbol.
+constexpr size_t kNoAllocScratchBytes = size_t(4) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of the current device's scratch, looked up once per device.
+int noalloc_scratch(void** out) {
+  int dev = 0;
+  JANUS_HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return JANUS_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    JANUS_HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return JANUS_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return JANUS_OK;
+}
+
+}  // namespace
+
+// Largest tile table the fixed scratch holds (tiles first, then the count).
+static int noalloc_max_tiles() {
+  return (int)((kNoAllocScratchBytes - 256) / sizeof(RowsTile));
+}
+
+extern "C" int janus_grouped_gemm_noalloc(const float* A, const float* B, float* C, const int32_t* row_off,
+                                          int32_t n_groups, int64_t M, int32_t K, int32_t N, int32_t trans_b,
+                                          void* stream) {
+  if ((M > 0 && (!A || !C)) || !B || !row_off || n_groups < 1 || n_groups > 1024 || M < 0 || M > INT32_MAX ||
+      K <= 0 || K % GBK || N <= 0 || N % 64)
+    return JANUS_EINVAL;
+  const int mt = max_rows_tiles(M, n_groups);
+  if (mt > noalloc_max_tiles()) return JANUS_ENOMEM;
+  void* base = nullptr;
+  int rc = noalloc_scratch(&base);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Carver cv(base);
+  RowsTile* tiles = cv.take<RowsTile>(mt);
+  int* nt = cv.take<int>(1);
+  if (cv.size() > kNoAllocScratchBytes) return JANUS_ENOMEM;
+  // the table kernel rewrites the count and every tile the launch reads, so
+  // nothing left by an earlier call is used
   build_tables(st, row_off, n_groups, 0, tiles, nt, nullptr, nullptr, nullptr);
   if (trans_b)
     launch_rows<true>(st, LoadPlain{A, K}, B, K, N, tiles, nt, mt, EpiStore{C, N});

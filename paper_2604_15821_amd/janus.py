@@ -89,6 +89,7 @@ def _lib():
                                       C.POINTER(Labels), vp, vp, vp, vp, vp, C.POINTER(Debug), vp]
         lib.janus_grouped_gemm.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
         lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
+        lib.janus_grouped_gemm_noalloc.argtypes = [vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
         lib.janus_wgrad_chunk_rows.argtypes = [i64, i32, i32]
         lib.janus_wgrad_chunk_rows.restype = i32
         lib.janus_set_workspace_limit.argtypes = [vp, i64]
@@ -107,8 +108,8 @@ def exported_symbols():
     lib = _lib()
     names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
              "janus_step_stress", "janus_step_ex",
-             "janus_grouped_gemm", "janus_grouped_wgrad", "janus_wgrad_chunk_rows", "janus_profile_enable",
-             "janus_profile_read",
+             "janus_grouped_gemm", "janus_grouped_gemm_noalloc", "janus_grouped_wgrad", "janus_wgrad_chunk_rows",
+             "janus_profile_enable", "janus_profile_read",
              "janus_set_workspace_limit", "janus_set_concurrency", "janus_last_chunks", "janus_last_triplets",
              "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
@@ -450,6 +451,23 @@ class Context:
         if rc:
             raise JanusError(rc, "janus_grouped_wgrad")
         return out
+
+
+def grouped_gemm_noalloc(A, B, row_off, K, N, trans_b, out):
+    """janus_grouped_gemm_noalloc on the current device: C = A x B_g per row group into
+    the caller's `out`, with the tile table in the library's fixed scratch (no allocation)."""
+    M = A.shape[0]
+    dev = A.device
+    G = row_off.shape[0] - 1
+    _arg(A, "A", "f32", (M, K))
+    _arg(B, "B", "f32", (G, N, K) if trans_b else (G, K, N), dev)
+    _arg(row_off, "row_off", "i32", (G + 1,), dev)
+    _arg(out, "out", "f32", (M, N), dev)
+    rc = _lib().janus_grouped_gemm_noalloc(_ptr(A), _ptr(B), _ptr(out), _ptr(row_off), G, M, K, N, int(trans_b),
+                                           _stream())
+    if rc:
+        raise JanusError(rc, "janus_grouped_gemm_noalloc")
+    return out
 
 
 def upload(batch, device="cuda:0"):
