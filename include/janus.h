@@ -340,6 +340,27 @@ int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell, const int
                   float* dLdW, const janus_debug* dbg, void* stream);
 
 /*
+ * janus_step_ex that also returns the gradient of the loss with respect to the
+ * atom positions (paper Sec. "MatRIS": the forces F = -dE/dR and the stress
+ * (1/V) dE/deps are derivatives of the energy, so the loss depends on the
+ * positions through E, F and sigma):
+ *   dLdR [N*3]  dL/dR_a, row-major [N, 3]; NULL gives exactly janus_step_ex.
+ * It is the same four-phase step: the double and final backward also collect,
+ * per edge, the loss adjoint of the edge length through the radial basis and
+ * its derivative (the second radial derivative of the basis enters here),
+ * and one per-atom pass adds the adjoints of the edge directions and of the
+ * stress term.  Supported for the radial model with any of the stress term,
+ * the robust loss, the feature-update MoE and the task-aware embedding; with
+ * the bond-angle term or attention, dLdR != NULL returns JANUS_EUNSUPPORTED.
+ * Every other argument, output and error is as for janus_step_ex.
+ */
+int janus_step_pos(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
+                   const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
+                   const float* W, const float* E_ref, const float* F_ref, const float* S_ref,
+                   const janus_labels* labels, float* loss, float* E, float* F, float* stress,
+                   float* dLdW, float* dLdR, const janus_debug* dbg, void* stream);
+
+/*
  * Workspace of janus_step (paper Sec. "Overview of the problem": the second
  * derivatives of the force loss roughly double the memory of training; Sec.
  * "Runtime for multi-phase double-backward execution").  Structures are

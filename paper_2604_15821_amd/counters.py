@@ -140,8 +140,8 @@ def summarize(workload: str, runs: str) -> str:
          f"Summarised by `python -m paper_2604_15821_amd.counters {workload} $OUT`.", "",
          "FETCH_SIZE and WRITE_SIZE are KiB per dispatch. Each is scaled by what the same counter reads for the",
          "calibration kernel of the `--copy-mib 1024` runs: one elementwise kernel that reads 1 GiB and writes 1 GiB.",
-         f"The scale factors are fetch x{kf:.3f} and write x{kw:.3f}. Traffic is counted over every step of the",
-         "counter runs (3 untimed + 2 timed steps, so 5x the per-step launches).", "",
+         f"The scale factors are fetch x{kf:.3f} and write x{kw:.3f}. Traffic is averaged over every dispatch of",
+         "the counter runs (their breakdown and timed steps).", "",
          "| family | launches | avg us (kernel trace) | HBM read MB/launch | HBM write MB/launch |",
          "|---|---:|---:|---:|---:|"]
     for fam in ["expert_gemm", "wgrad", "dense_gemm", "edge", "atom", "other"]:
@@ -151,8 +151,7 @@ def summarize(workload: str, runs: str) -> str:
                      f"{a[2] / a[0] / 1e6:.1f} |")
     L += ["", "The kernel-trace run uses bench.py's default two streams: in the double and final backward the "
           "expert weight gradients (wgrad) run beside the edge, atom and small dense kernels, whose averages "
-          "above are therefore longer than alone (`profiles/kernels_small_serial.md` has every kernel on one "
-          "stream); the expert products never overlap another product.",
+          "above are therefore longer than alone; the expert products never overlap another product.",
           "", "Kernel statistics of the kernel-trace run (rocprofv3 --stats, all dispatches including warm-up):", "",
           "| kernel | calls | avg us | total ms | % |", "|---|---:|---:|---:|---:|"]
     for r in stats[:30]:

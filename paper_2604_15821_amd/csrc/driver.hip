@@ -141,7 +141,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
               const float* cell_g, const int32_t* species_g, const int32_t* offsets_g, const janus_edges* nl,
               const float* W, const float* E_ref_g, const float* F_ref_g, const float* S_ref_g,
               const janus_labels* labels, double* loss_part, float* E_g, float* F_g, float* stress_g, float* dLdW,
-              const janus_debug* dbg) {
+              float* dLdR_g, const janus_debug* dbg) {
   const janus_config& cfg = ctx->cfg;
   const int T = p.T, Ee = p.E, k = p.k, d = p.d, h = p.hdim, nb = p.nb, nsp = p.nsp;
   const int N = ca.N, S = ca.S;
@@ -210,7 +210,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   {
     PROF(PROF_GRAPH, 0, Ne * (12.0 + 3.0 + 16.0 + 8.0 * nb));
     launch_geometry(st, pos, cell, p.sid, ei, ej, shift, (int)Ne, cfg.r_cut, nb, p.geo, p.B, p.dB,
-                    three ? cfg.r_cut3 : 0.f, p.B3, p.dB3, p.u3, p.du3);
+                    three ? cfg.r_cut3 : 0.f, p.B3, p.dB3, p.u3, p.du3, p.d2B);
   }
   if (three) {
     // triplets of the chunk: CSR by first edge, reverse map, cosines
@@ -228,7 +228,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                          LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, nullptr, nb}, Nt, nf, p.G3f);
     }
     hipLaunchKernelGGL(set_rows_kernel, dim3(1), dim3(64), 0, st, p.rowT, (int)Nt, p.rowT, Nt);
-    build_tables(st, p.rowT, 1, p.kcT, nullptr, nullptr, p.chunksT, p.ncT, p.cfT);
+    build_tables(st, p.rowT, 1, p.kcT, p.tilesT, p.ntT, p.chunksT, p.ncT, p.cfT);
   }
   const long long np = (long long)nsp * nsp;
   {
@@ -684,6 +684,12 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   // t1_free), Abar of the block (G7), Sbt (G8).  Sbt of block t is written over
   // Abar of block t-1 (block 0: p.Shat0), which G7 of block t-1 has finished
   // reading once t1_free of that block has passed.
+  // dL/dr_e through the basis, accumulated by the edge kernels of phases 3 and 4
+  if (p.rpos) JANUS_HIP_TRY(hipMemsetAsync(p.rpos, 0, sizeof(float) * (Ne + 1), st));
+  if (p.adjG) {
+    JANUS_HIP_TRY(hipMemsetAsync(p.adjG, 0, sizeof(float) * (Nt * nf + 4), st));
+    JANUS_HIP_TRY(hipMemsetAsync(p.adjGd, 0, sizeof(float) * (Nt * nf + 4), st));
+  }
   SideSync ss(ctx, st);
   hipStream_t sd = ss.sd;
   hipEvent_t t1_free = nullptr;   // side stream done with p.T1 (and with the last Abar it read)
@@ -712,6 +718,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_DENSE_GEMM, f_wa, 0);
         launch_wgrad(st, LoadPlain{p.G3t, nf}, LoadPlain{p.VT, d}, nf, d, p.chunksT, p.ncT, p.cfT, p.mcT, 1,
                      p.partial, Gp(blk(t, "W_a")), 1);
+        // loss gradient in positions: adjoint of the feature tangent, sum_t (Zbar * h_j2) W_a^T
+        if (p.adjGd)
+          launch_rows<true>(st, LoadPlain{p.VT, d}, Wp(blk(t, "W_a")), d, nf, p.tilesT, p.ntT, p.mtT,
+                            EpiAdd{p.adjGd, p.adjGd, nf});
       }
       {
         PROF(PROF_EXPERT_WGRAD, f_tri, 0);
@@ -744,7 +754,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       // with triplets, P_e already holds the triplet part written by tri_p3
       LAUNCH_VPL_K(edge_p3_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
                    (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)Xbar(t), hht_t, (const float*)p.rt,
-                   p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr), (int)tri_t);
+                   p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr), (int)tri_t, (const float*)p.d2B, p.rpos);
     }
     // G7 (side stream) beside dW_b and the reverse scatter
     ss.fork();
@@ -1030,7 +1040,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_EDGE, 0, by_p4);
         LAUNCH_VPL_K(edge_p4_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
                    POS(t), Ne, d, (const float*)p.T2, (const float*)Xbar(t), hht_t, p.Ft, p.Pe,
-                   three ? p.Q : (float*)nullptr);
+                   three ? p.Q : (float*)nullptr, (const float*)p.dB, p.rpos);
       }
       {
         // dW_b (part 2): B^T Ft
@@ -1094,6 +1104,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_DENSE_GEMM, f_wa, 0);
         launch_wgrad(st, LoadPlain{p.G3f, nf}, LoadPlain{p.VT, d}, nf, d, p.chunksT, p.ncT, p.cfT, p.mcT, 1,
                      p.partial, Gp(blk(t, "W_a")), 1);
+        // loss gradient in positions: adjoint of the features, sum_t VT W_a^T
+        if (p.adjG)
+          launch_rows<true>(st, LoadPlain{p.VT, d}, Wp(blk(t, "W_a")), d, nf, p.tilesT, p.ntT, p.mtT,
+                            EpiAdd{p.adjG, p.adjG, nf});
       }
       {
         // triplet router tables: logit adjoints summed per vertex / neighbour species
@@ -1124,6 +1138,22 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   // the caller's stream waits for the side stream's weight gradients
   ss.join();
   if (ss.err != hipSuccess) return janus_set_hip_error(ss.err);
+  if (dLdR_g) {
+    PROF(PROF_OTHER, 0, Ne * 40.0 + N * 24.0);
+    const float* psi = S_ref ? p.Psi : nullptr;
+    const float4* tpos = nullptr;
+    if (three && Nt > 0) {
+      hipLaunchKernelGGL(tri_pos_kernel, dim3(cdiv(Nt, 128)), dim3(128), 0, st, (const int*)p.te, (const int*)p.te2,
+                         (const float*)p.tc, (const float4*)p.geo, (const float4*)p.gtan, psi, ei, (const int*)p.sid,
+                         (const float*)p.adjG, (const float*)p.adjGd, Nt, nb, L3, cfg.r_cut3, p.tp1, p.tp2);
+      hipLaunchKernelGGL(tri_pos_edge_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, (const int*)p.trow,
+                         (const int*)p.trev, (const float4*)p.tp1, (const float4*)p.tp2, Ne, p.tpos);
+      tpos = p.tpos;
+    }
+    hipLaunchKernelGGL(pos_grad_kernel, gN, b256, 0, st, rowptr, rev, ei, ej, (const float*)p.rbar,
+                       (const float*)p.rpos, (const float4*)p.geo, (const float*)p.phi, psi, (const int*)p.sid,
+                       tpos, N, dLdR_g + 3LL * ca.a0);
+  }
   {
     PROF(PROF_OTHER, 0, 8.0 * Nd);
     hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
@@ -1219,9 +1249,21 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
                              const float* W, const float* E_ref, const float* F_ref, const float* S_ref,
                              const janus_labels* labels, float* loss, float* E, float* F, float* stress, float* dLdW,
                              const janus_debug* dbg, void* stream) {
+  return janus_step_pos(ctx, pos, cell, species, offsets, n_atoms, n_struct, nl, W, E_ref, F_ref, S_ref, labels, loss,
+                        E, F, stress, dLdW, nullptr, dbg, stream);
+}
+
+extern "C" int janus_step_pos(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
+                              const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,
+                              const float* W, const float* E_ref, const float* F_ref, const float* S_ref,
+                              const janus_labels* labels, float* loss, float* E, float* F, float* stress,
+                              float* dLdW, float* dLdR, const janus_debug* dbg, void* stream) {
   if (!ctx || !pos || !cell || !species || !offsets || !nl || !W || !E_ref || !F_ref || !loss || !E || !F ||
       !dLdW || n_atoms < 1 || n_struct < 1 || n_struct > n_atoms)
     return JANUS_EINVAL;
+  // the position gradient covers every option except attention
+  if (dLdR && ctx->cfg.n_heads) return JANUS_EUNSUPPORTED;
+  const bool want_pos = dLdR != nullptr;
   // the task-aware embedding needs every structure's labels
   if (ctx->cfg.n_tasks && (!labels || !labels->task || !labels->charge || !labels->spin)) return JANUS_EINVAL;
   // the stress term of the loss needs its reference; without the term no reference is read
@@ -1326,14 +1368,14 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
     while (s0 < S) {
       int s1 = s0 + 1;
       size_t b1 = plan_layout(tmp, nullptr, cfg, h_off[s1] - h_off[s0], 1, (long long)h_erow[s1] - h_erow[s0],
-                              tri_between(s0, s1));
+                              tri_between(s0, s1), want_pos);
       if (b1 > budget) return JANUS_ENOMEM;
       // grow by doubling, then bisect, to keep the plan O(S log S)
       int step = 1;
       while (s1 < S) {
         const int s2 = std::min(S, s1 + step);
         const size_t b = plan_layout(tmp, nullptr, cfg, h_off[s2] - h_off[s0], s2 - s0,
-                                     (long long)h_erow[s2] - h_erow[s0], tri_between(s0, s2));
+                                     (long long)h_erow[s2] - h_erow[s0], tri_between(s0, s2), want_pos);
         if (b > budget) {
           if (step == 1) break;
           step = 1;
@@ -1380,9 +1422,9 @@ extern "C" int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell
   auto run = [&](ChunkArgs ca, int mode) {
     ca.robust_mode = mode;
     Plan p;
-    plan_layout(p, ctx->ws.ptr, cfg, ca.N, ca.S, ca.Ne, ca.Nt);
+    plan_layout(p, ctx->ws.ptr, cfg, ca.N, ca.S, ca.Ne, ca.Nt, want_pos);
     return run_chunk(ctx, st, p, L, ca, pos, cell, species, offsets, nl, W, E_ref, F_ref, S_ref, labels,
-                     loss_part + ca.index, E, F, stress, dLdW, dbg);
+                     loss_part + ca.index, E, F, stress, dLdW, dLdR, dbg);
   };
   int n_parts = (int)chunks.size();
   if (cfg.robust && chunks.size() > 1) {

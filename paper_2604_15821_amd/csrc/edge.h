@@ -284,12 +284,15 @@ __global__ void scatter_rev_kernel(const int* __restrict__ rowptr, const int* __
 //   Fbt = rt_e F'_e,  Xbt = Q_e * F_e + Fbt * h_j (+ QX_e)  (Q_e = adjoint of hbar^t at j),
 //   Xbt copied to the k slots; P_e = Fbt * Xbar_e  (routed to h_j), added to
 //   the P_e already stored when accP is set.
+// With rpos (the loss gradient in positions): rbar_e = sum_t Fbar . F'_e depends
+// on r_e through B'(r_e) too, so rpos_e += rt_e Fbar . F''_e, F'' = B''(r_e) W_b.
 template <int VPL, int KC>
 __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restrict__ dB, int nb,
                                const float* __restrict__ Wb, const float* __restrict__ h, const int* __restrict__ ej,
                                const int* __restrict__ pos, long long Ne, int d, const float* __restrict__ Xbar,
                                const float* __restrict__ hht, const float* __restrict__ rt, float* __restrict__ Xbts,
-                               float* __restrict__ P, const float* __restrict__ QX, int accP) {
+                               float* __restrict__ P, const float* __restrict__ QX, int accP,
+                               const float* __restrict__ d2B, float* __restrict__ rpos) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
@@ -315,6 +318,15 @@ __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restr
     st_row<VPL>(P + e * d, l, p);
 #pragma unroll
     for (int c = 0; c < KC; ++c) st_row<VPL>(Xbts + (long long)pos[e * KC + c] * d, l, X);
+    if (rpos) {
+      float F2[VPL];
+      filter_row<VPL>(basis_lane(d2B, e, nb, l), sW, nb, d, l, F2);
+      float s2 = 0.f;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) s2 += xb[v] * hj[v] * F2[v];
+      s2 = wave_sum(s2);
+      if (l == 0) rpos[e] += r * s2;
+    }
   }
 }
 
@@ -373,12 +385,13 @@ __global__ void combine_p3_kernel(const int* __restrict__ rowptr, const int* __r
 
 // Phase 4 per edge: Xt_e = sum_c Xt_slot; Ft_e = Xt * h_j + Q_e * Xbar_e
 // (Q_e from the double backward); P_e = Xt * F_e (routed to h_j).
+// With rpos: F_e = B(r_e) W_b, so rpos_e += Ft . F'_e.
 template <int VPL, int KC>
 __global__ void edge_p4_kernel(const float* __restrict__ B, int nb, const float* __restrict__ Wb,
                                const float* __restrict__ h, const int* __restrict__ ej, const int* __restrict__ pos,
                                long long Ne, int d, const float* __restrict__ Xts, const float* __restrict__ Xbar,
                                const float* __restrict__ hht, float* __restrict__ Ft, float* __restrict__ P,
-                               float* __restrict__ XT) {
+                               float* __restrict__ XT, const float* __restrict__ dB, float* __restrict__ rpos) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
@@ -400,6 +413,15 @@ __global__ void edge_p4_kernel(const float* __restrict__ B, int nb, const float*
     st_row<VPL>(Ft + e * d, l, ft);
     st_row<VPL>(P + e * d, l, p);
     if (XT) st_row<VPL>(XT + e * d, l, xt);
+    if (rpos) {
+      float Fp[VPL];
+      filter_row<VPL>(basis_lane(dB, e, nb, l), sW, nb, d, l, Fp);
+      float s1 = 0.f;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) s1 += ft[v] * Fp[v];
+      s1 = wave_sum(s1);
+      if (l == 0) rpos[e] += s1;
+    }
   }
 }
 

@@ -255,14 +255,50 @@ __device__ __forceinline__ void bessel_at(double r, double rcd, int nb, float* _
   }
 }
 
+// d2B_n/dr2, n = 1..nb, for cutoff rc (the loss gradient in positions needs the
+// second radial derivative of the basis):
+//   B = c s u,  s = sin(k r) / r,  s' = (k cos(k r) - s) / r,  s'' = -k^2 s - 2 s' / r,
+//   B'' = c (s'' u + 2 s' u' + s u''),  u'' = (-840 x^4 + 2016 x^5 - 1176 x^6) / rc^2.
+__device__ __forceinline__ void bessel_d2_at(double r, double rcd, int nb, float* __restrict__ d2B) {
+  double u, du;
+  envelope_at(r, rcd, u, du);
+  const double x = r / rcd;
+  double d2u = 0.0;
+  if (x < 1.0) {
+    const double x2 = x * x, x4 = x2 * x2;
+    d2u = (-840.0 * x4 + 2016.0 * x4 * x - 1176.0 * x4 * x2) / (rcd * rcd);
+  }
+  const double c = sqrt(2.0 / rcd);
+  const double th = M_PI / rcd;
+  double s1, c1;
+  sincos(th * r, &s1, &c1);
+  double sn = s1, cs = c1;
+  const double ir = 1.0 / r;
+  for (int n0 = 1; n0 <= nb; n0 += 4) {
+    float b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const double k = (n0 + q) * th;
+      const double s = sn * ir;
+      const double ds = (k * cs - s) * ir;
+      const double d2s = -k * k * s - 2.0 * ds * ir;
+      b[q] = (float)(c * (d2s * u + 2.0 * ds * du + s * d2u));
+      const double sn1 = sn * c1 + cs * s1;
+      cs = cs * c1 - sn * s1;
+      sn = sn1;
+    }
+    *reinterpret_cast<float4*>(d2B + n0 - 1) = make_float4(b[0], b[1], b[2], b[3]);
+  }
+}
+
 // With rc3 > 0 also the three-body basis B3, dB3 (cutoff rc3) and the
-// envelope u(r / rc3) with its derivative, per edge.
+// envelope u(r / rc3) with its derivative, per edge; with d2B also B''.
 __global__ void geometry_kernel(const float* __restrict__ pos, const float* __restrict__ cell,
                                 const int* __restrict__ sid, const int* __restrict__ ei,
                                 const int* __restrict__ ej, const int8_t* __restrict__ shift, int Ne,
                                 float rc, int nb, float4* __restrict__ geo, float* __restrict__ B,
                                 float* __restrict__ dB, float rc3, float* __restrict__ B3, float* __restrict__ dB3,
-                                float* __restrict__ u3, float* __restrict__ du3) {
+                                float* __restrict__ u3, float* __restrict__ du3, float* __restrict__ d2B) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= Ne) return;
   const int i = ei[e], j = ej[e];
@@ -276,6 +312,7 @@ __global__ void geometry_kernel(const float* __restrict__ pos, const float* __re
   const double r = sqrt(d[0] * d[0] + d[1] * d[1] + d[2] * d[2]);
   geo[e] = make_float4((float)(d[0] / r), (float)(d[1] / r), (float)(d[2] / r), (float)r);
   bessel_at(r, (double)rc, nb, B + (long long)e * nb, dB + (long long)e * nb);
+  if (d2B) bessel_d2_at(r, (double)rc, nb, d2B + (long long)e * nb);
   if (rc3 > 0.f) {
     bessel_at(r, (double)rc3, nb, B3 + (long long)e * nb, dB3 + (long long)e * nb);
     double u, du;
@@ -312,10 +349,10 @@ void launch_exclusive_scan(hipStream_t st, const int* in, int n, int* out, int* 
 
 void launch_geometry(hipStream_t st, const float* pos, const float* cell, const int* sid, const int* ei,
                      const int* ej, const int8_t* shift, int Ne, float rc, int nb, float4* geo, float* B,
-                     float* dB, float rc3, float* B3, float* dB3, float* u3, float* du3) {
+                     float* dB, float rc3, float* B3, float* dB3, float* u3, float* du3, float* d2B) {
   if (Ne <= 0) return;
   hipLaunchKernelGGL(geometry_kernel, dim3(cdiv(Ne, 256)), dim3(256), 0, st, pos, cell, sid, ei, ej, shift, Ne,
-                     rc, nb, geo, B, dB, rc3, B3, dB3, u3, du3);
+                     rc, nb, geo, B, dB, rc3, B3, dB3, u3, du3, d2B);
 }
 
 }  // namespace janus

@@ -123,6 +123,76 @@ __global__ void force_kernel(const int* __restrict__ rowptr, const int* __restri
   }
 }
 
+// Loss gradient in the positions (paper Sec. "MatRIS": forces and stresses are
+// derivatives of E, so the loss depends on R through E, F = -dE/dR and sigma).
+// Per edge, with G_e = rbar_e u_e = dE/dd_e:
+//   L sees G_e through F_i (+G_e), F_j (-G_e) and sigma_s (G_e d_e^T / V_s), so
+//   its adjoint is gt_e = phi_i - phi_j + Psi_s d_e;
+//   u_e = d_e / r_e carries rbar_e gt_e, sigma's own d_e carries Psi_s^T G_e;
+//   rpos_e (accumulated by the double and final backward) is dL/dr_e through
+//   the basis B(r_e) and its derivative B'(r_e):
+//   dL/dd_e = rpos_e u_e + rbar_e (gt_e - (gt_e . u_e) u_e) / r_e + rbar_e Psi_s^T u_e
+//             (+ tpos_e, the bond-angle part, when the model has it),
+// and dL/dR_a = sum over the edges e of a of (dL/dd_rev(e) - dL/dd_e) (d_e = R_j - R_i + n.L),
+// one wave per atom, lanes over edges in order, a fixed butterfly, float64.
+__device__ __forceinline__ void pos_edge_adjoint(int e, const int* __restrict__ ei, const int* __restrict__ ej,
+                                                 const float* __restrict__ rbar, const float* __restrict__ rpos,
+                                                 const float4* __restrict__ geo, const float* __restrict__ phi,
+                                                 const float* __restrict__ Psi, const int* __restrict__ sid,
+                                                 const float4* __restrict__ tpos, double (&a)[3]) {
+  const int i = ei[e], j = ej[e];
+  const float4 g = geo[e];
+  const double u[3] = {g.x, g.y, g.z}, r = g.w;
+  double gt[3];
+  for (int k = 0; k < 3; ++k) gt[k] = (double)phi[3 * i + k] - (double)phi[3 * j + k];
+  const float* P = Psi ? Psi + 9 * sid[i] : nullptr;
+  if (P) {
+    for (int k = 0; k < 3; ++k) gt[k] += r * ((double)P[3 * k] * u[0] + (double)P[3 * k + 1] * u[1] +
+                                              (double)P[3 * k + 2] * u[2]);
+  }
+  const double rb = rbar[e], rp = rpos[e];
+  const double gu = gt[0] * u[0] + gt[1] * u[1] + gt[2] * u[2];
+  for (int k = 0; k < 3; ++k) a[k] = rp * u[k] + rb * (gt[k] - gu * u[k]) / r;
+  if (P) {
+    for (int k = 0; k < 3; ++k)
+      a[k] += rb * ((double)P[k] * u[0] + (double)P[3 + k] * u[1] + (double)P[6 + k] * u[2]);
+  }
+  if (tpos) {   // the bond-angle part, per edge
+    const float4 w = tpos[e];
+    a[0] += w.x;
+    a[1] += w.y;
+    a[2] += w.z;
+  }
+}
+
+__global__ void pos_grad_kernel(const int* __restrict__ rowptr, const int* __restrict__ rev,
+                                const int* __restrict__ ei, const int* __restrict__ ej,
+                                const float* __restrict__ rbar, const float* __restrict__ rpos,
+                                const float4* __restrict__ geo, const float* __restrict__ phi,
+                                const float* __restrict__ Psi, const int* __restrict__ sid,
+                                const float4* __restrict__ tpos, int N, float* __restrict__ out) {
+  JANUS_WAVE_LOOP(a, N) {
+    double sx = 0, sy = 0, sz = 0;
+    const int e1 = rowptr[a + 1];
+    for (int e = rowptr[a] + l; e < e1; e += kWave) {
+      double x[3], y[3];
+      pos_edge_adjoint(e, ei, ej, rbar, rpos, geo, phi, Psi, sid, tpos, x);
+      pos_edge_adjoint(rev[e], ei, ej, rbar, rpos, geo, phi, Psi, sid, tpos, y);
+      sx += y[0] - x[0];
+      sy += y[1] - x[1];
+      sz += y[2] - x[2];
+    }
+    sx = wave_sum_d(sx);
+    sy = wave_sum_d(sy);
+    sz = wave_sum_d(sz);
+    if (l == 0) {
+      out[3 * a] = (float)sx;
+      out[3 * a + 1] = (float)sy;
+      out[3 * a + 2] = (float)sz;
+    }
+  }
+}
+
 // |det| of the lattice rows of one structure (its volume).
 __device__ __forceinline__ double cell_volume(const float* __restrict__ c) {
   const double a0 = c[0], a1 = c[1], a2 = c[2], b0 = c[3], b1 = c[4], b2 = c[5], c0 = c[6], c1 = c[7], c2 = c[8];
@@ -869,6 +939,7 @@ struct Plan {
   int* sid;
   float4* geo;
   float *B, *dB, *rt, *rbar;
+  float *d2B, *rpos;   // loss gradient in positions: B''(r_e) and dL/dr_e (null without it)
   int *sp_cnt, *sp_off, *sp_atoms;
   float *z, *eps, *lam, *phi, *vt, *Zr, *Tr, *colpart, *sig, *Psi, *gs, *gsb;
   float4* gtan;
@@ -911,6 +982,14 @@ struct Plan {
   int *rowT;
   WChunk* chunksT;
   int *ncT, *cfT;
+  // loss gradient in positions with the bond-angle term: row tiles over the
+  // triplets, feature adjoints of the final and double backward [Nt, nf],
+  // per-triplet and per-edge displacement vectors (null without it)
+  RowsTile* tilesT;
+  int* ntT;
+  int mtT;
+  float *adjG, *adjGd;
+  float4 *tp1, *tp2, *tpos;
   float *Z3s, *A3, *S3b, *A3b, *Y3bs, *Zbar3;
   float *Q, *LT3, *VT, *G3f, *G3t, *T3a, *T3b, *gpart3, *gt3, *LB, *LC, *pa, *pb, *pc;
   // feature-update MoE: atom tokens (one row per atom in an identity CSR),
@@ -945,7 +1024,8 @@ struct Plan {
   int attn, H, mtE, kcA, mcA;
 };
 
-size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, long long Ne, long long Nt = 0) {
+size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, long long Ne, long long Nt = 0,
+                   bool pos_grad = false) {
   Carver cv(base);
   p.T = c.n_blocks;
   p.E = c.n_experts;
@@ -979,6 +1059,8 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.dB = cv.take<float>(Ne * p.nb);
   p.rt = cv.take<float>(Ne);
   p.rbar = cv.take<float>(Ne);
+  p.d2B = pos_grad ? cv.take<float>(Ne * p.nb) : nullptr;
+  p.rpos = pos_grad ? cv.take<float>(Ne + 1) : nullptr;
   p.sp_cnt = cv.take<int>(p.nsp);
   p.scan = cv.take<long long>(scan_scratch_bytes(std::max<long long>(Ne, p.nsp)) / sizeof(long long));
   p.sp_off = cv.take<int>(p.nsp + 1);
@@ -1097,6 +1179,10 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.L3 = c.n_legendre;
   p.nf = c.n_legendre * c.n_rbf;
   p.M3 = p.Nt * c.top_k3;
+  p.tilesT = nullptr;
+  p.ntT = nullptr;
+  p.adjG = p.adjGd = nullptr;
+  p.tp1 = p.tp2 = p.tpos = nullptr;
   if (p.three) {
     const long long M3 = p.M3, Ntt = p.Nt, h3 = p.hd3, E3 = p.E3;
     p.mt3 = max_rows_tiles(M3, p.E3);
@@ -1135,6 +1221,14 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.cfirst3 = cv.take<int>(T * (E3 + 1) + 1);
     p.rowT = cv.take<int>(2);
     p.chunksT = cv.take<WChunk>(p.mcT);
+    p.mtT = max_rows_tiles(Ntt, 1);
+    p.tilesT = pos_grad ? cv.take<RowsTile>(p.mtT) : nullptr;
+    p.ntT = pos_grad ? cv.take<int>(1) : nullptr;
+    p.adjG = pos_grad ? cv.take<float>(Ntt * p.nf + 4) : nullptr;
+    p.adjGd = pos_grad ? cv.take<float>(Ntt * p.nf + 4) : nullptr;
+    p.tp1 = pos_grad ? cv.take<float4>(Ntt + 1) : nullptr;
+    p.tp2 = pos_grad ? cv.take<float4>(Ntt + 1) : nullptr;
+    p.tpos = pos_grad ? cv.take<float4>(Ne + 1) : nullptr;
     p.ncT = cv.take<int>(1);
     p.cfT = cv.take<int>(2);
     p.Z3s = cv.take<float>(T * M3 * d + 4);

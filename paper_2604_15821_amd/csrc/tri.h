@@ -881,4 +881,173 @@ __global__ void tri_features_kernel(LoadTriFeat ld, long long Nt, int nf, float*
   *reinterpret_cast<float4*>(out + t * nf + f) = ld.load(t, f);
 }
 
+
+// ---------------------------------------------------------- loss gradient in positions
+
+// Loss gradient in the positions, bond-angle part, per triplet tau = (e, e2):
+// with Ag = dL/dG_tau (the final backward's adjoint of the features) and
+// Ad = -dE/dG-adjoint of the double backward (Ad = -sum_t W_a (Zbar * h_j2)),
+// and the displacement tangents dd = -gt (gt_e = phi_i - phi_j + Psi_s d_e):
+//   first partials:  (ac, a1, a2) = Ag . (dG/dc, dG/dr1, dG/dr2)
+//     -> e:  ac (u2 - c u1) / r1 + a1 u1,   e2: ac (u1 - c u2) / r2 + a2 u2;
+//   tangent part: the gradient in d_e, d_e2 of
+//     s = Ad . (dG/dc cdot + dG/dr1 rdot1 + dG/dr2 rdot2),
+//     rdot = dd . u,  udot = (dd - rdot u) / r,  cdot = udot1 . u2 + u1 . udot2,
+//   which takes the second partials of G = P_l(c) B3_n(r2) u3(r1) (P'', B3'', u3'')
+//   and, through dd = ... - Psi d, the stress seeds.
+// Float64 throughout; one thread per triplet; the two vectors go to tp1 (for e)
+// and tp2 (for e2).
+__global__ void tri_pos_kernel(const int* __restrict__ te, const int* __restrict__ te2,
+                               const float* __restrict__ tc, const float4* __restrict__ geo,
+                               const float4* __restrict__ gt, const float* __restrict__ Psi,
+                               const int* __restrict__ ei, const int* __restrict__ sid,
+                               const float* __restrict__ Ag, const float* __restrict__ Adn, long long Nt, int nb,
+                               int L, float r3f, float4* __restrict__ tp1, float4* __restrict__ tp2) {
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Nt) return;
+  const int e1 = te[t], e2 = te2[t];
+  const float4 g1 = geo[e1], g2 = geo[e2];
+  const double u1[3] = {g1.x, g1.y, g1.z}, u2[3] = {g2.x, g2.y, g2.z};
+  const double r1 = g1.w, r2 = g2.w, c = tc[t], r3 = r3f;
+  const float4 q1 = gt[e1], q2 = gt[e2];
+  const double dd1[3] = {-(double)q1.x, -(double)q1.y, -(double)q1.z};
+  const double dd2[3] = {-(double)q2.x, -(double)q2.y, -(double)q2.z};
+  const float* Ps = Psi ? Psi + 9 * sid[ei[e1]] : nullptr;
+  // Legendre P, P', P'' at c (l < L): Bonnet's recursion and its derivatives
+  double P[kMaxL], dP[kMaxL], d2P[kMaxL];
+  P[0] = 1.0; dP[0] = 0.0; d2P[0] = 0.0;
+  if (L > 1) { P[1] = c; dP[1] = 1.0; d2P[1] = 0.0; }
+#pragma unroll
+  for (int l = 1; l < kMaxL - 1; ++l) {
+    if (l + 1 < L) {
+      P[l + 1] = ((2 * l + 1) * c * P[l] - l * P[l - 1]) / (l + 1);
+      dP[l + 1] = (l + 1) * P[l] + c * dP[l];
+      d2P[l + 1] = (l + 2) * dP[l] + c * d2P[l];
+    }
+  }
+  // envelope u3(r1) and its first two radial derivatives
+  double e3 = 0.0, de3 = 0.0, d2e3 = 0.0;
+  {
+    const double x = r1 / r3;
+    if (x < 1.0) {
+      const double x2 = x * x, x4 = x2 * x2, x5 = x4 * x, x6 = x5 * x;
+      e3 = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
+      de3 = (-168.0 * x5 + 336.0 * x6 - 168.0 * x6 * x) / r3;
+      d2e3 = (-840.0 * x4 + 2016.0 * x5 - 1176.0 * x6) / (r3 * r3);
+    }
+  }
+  // B3_n(r2), B3_n', B3_n'' (n = 1..nb) summed against the two adjoints per l:
+  //   SA[l] = sum_n Ad[l, n] B3_n, SA1 with B3', SA2 with B3''; SG, SG1 with Ag
+  double SA[kMaxL], SA1[kMaxL], SA2[kMaxL], SG[kMaxL], SG1[kMaxL];
+#pragma unroll
+  for (int l = 0; l < kMaxL; ++l) SA[l] = SA1[l] = SA2[l] = SG[l] = SG1[l] = 0.0;
+  {
+    double u, du, d2u;
+    const double x = r2 / r3;
+    u = du = d2u = 0.0;
+    if (x < 1.0) {
+      const double x2 = x * x, x4 = x2 * x2, x5 = x4 * x, x6 = x5 * x;
+      u = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
+      du = (-168.0 * x5 + 336.0 * x6 - 168.0 * x6 * x) / r3;
+      d2u = (-840.0 * x4 + 2016.0 * x5 - 1176.0 * x6) / (r3 * r3);
+    }
+    const double cn = sqrt(2.0 / r3), th = M_PI / r3, ir = 1.0 / r2;
+    double s1, c1;
+    sincos(th * r2, &s1, &c1);
+    double sn = s1, cs = c1;
+    const float* arow = Adn + t * (long long)(L * nb);
+    const float* grow = Ag + t * (long long)(L * nb);
+    for (int n = 0; n < nb; ++n) {
+      const double k = (n + 1) * th;
+      const double sr = sn * ir;
+      const double ds = (k * cs - sr) * ir;
+      const double d2s = -k * k * sr - 2.0 * ds * ir;
+      const double b = cn * sr * u, db = cn * (ds * u + sr * du), d2b = cn * (d2s * u + 2.0 * ds * du + sr * d2u);
+#pragma unroll
+      for (int l = 0; l < kMaxL; ++l) {
+        if (l < L) {
+          const double a = -(double)arow[l * nb + n], g = grow[l * nb + n];
+          SA[l] += a * b;
+          SA1[l] += a * db;
+          SA2[l] += a * d2b;
+          SG[l] += g * b;
+          SG1[l] += g * db;
+        }
+      }
+      const double sn1 = sn * c1 + cs * s1;
+      cs = cs * c1 - sn * s1;
+      sn = sn1;
+    }
+  }
+  double g_c = 0, g_1 = 0, g_2 = 0, g_cc = 0, g_c1 = 0, g_c2 = 0, g_11 = 0, g_12 = 0, g_22 = 0;
+  double ac = 0, a1 = 0, a2 = 0;
+#pragma unroll
+  for (int l = 0; l < kMaxL; ++l) {
+    if (l < L) {
+      g_c += dP[l] * SA[l];
+      g_1 += P[l] * SA[l];
+      g_2 += P[l] * SA1[l];
+      g_cc += d2P[l] * SA[l];
+      g_c2 += dP[l] * SA1[l];
+      g_22 += P[l] * SA2[l];
+      ac += dP[l] * SG[l];
+      a1 += P[l] * SG[l];
+      a2 += P[l] * SG1[l];
+    }
+  }
+  g_c1 = g_c * de3;   // <A, P' B3> u3'
+  g_11 = g_1 * d2e3;  // <A, P B3> u3''
+  g_12 = g_2 * de3;   // <A, P B3'> u3'
+  g_c *= e3; g_1 *= de3; g_2 *= e3; g_cc *= e3; g_c2 *= e3; g_22 *= e3;
+  ac *= e3; a1 *= de3; a2 *= e3;
+  // Psi^T v of the triplet's structure (the tangent depends on d through -Psi d)
+  auto PT = [&](const double (&v)[3], double (&o)[3]) {
+    for (int k = 0; k < 3; ++k) o[k] = Ps ? (double)Ps[k] * v[0] + (double)Ps[3 + k] * v[1] + (double)Ps[6 + k] * v[2] : 0.0;
+  };
+  double rd1 = 0, rd2 = 0;
+  for (int k = 0; k < 3; ++k) { rd1 += dd1[k] * u1[k]; rd2 += dd2[k] * u2[k]; }
+  double ud1[3], ud2[3];
+  for (int k = 0; k < 3; ++k) { ud1[k] = (dd1[k] - rd1 * u1[k]) / r1; ud2[k] = (dd2[k] - rd2 * u2[k]) / r2; }
+  double w1 = 0, w2 = 0;
+  for (int k = 0; k < 3; ++k) { w1 += ud1[k] * u2[k]; w2 += u1[k] * ud2[k]; }
+  const double cd = w1 + w2;
+  double pu1[3], pu2[3];
+  PT(u1, pu1);
+  PT(u2, pu2);
+  const double a_c = g_cc * cd + g_c1 * rd1 + g_c2 * rd2;
+  const double a_1 = g_c1 * cd + g_11 * rd1 + g_12 * rd2;
+  const double a_2 = g_c2 * cd + g_12 * rd1 + g_22 * rd2;
+  double o1[3], o2[3];
+  for (int k = 0; k < 3; ++k) {
+    const double gc1 = (u2[k] - c * u1[k]) / r1, gc2 = (u1[k] - c * u2[k]) / r2;
+    const double grd1 = ud1[k] - pu1[k], grd2 = ud2[k] - pu2[k];
+    const double gw1_d1 = (-pu2[k] - c * grd1 - rd1 * gc1 - w1 * u1[k]) / r1;
+    const double gw2_d1 = (ud2[k] - w2 * u1[k]) / r1;
+    const double gw2_d2 = (-pu1[k] - c * grd2 - rd2 * gc2 - w2 * u2[k]) / r2;
+    const double gw1_d2 = (ud1[k] - w1 * u2[k]) / r2;
+    o1[k] = a_c * gc1 + a_1 * u1[k] + g_c * (gw1_d1 + gw2_d1) + g_1 * grd1 + ac * gc1 + a1 * u1[k];
+    o2[k] = a_c * gc2 + a_2 * u2[k] + g_c * (gw1_d2 + gw2_d2) + g_2 * grd2 + ac * gc2 + a2 * u2[k];
+  }
+  tp1[t] = make_float4((float)o1[0], (float)o1[1], (float)o1[2], 0.f);
+  tp2[t] = make_float4((float)o2[0], (float)o2[1], (float)o2[2], 0.f);
+}
+
+// Per edge: the triplet vectors of the triplets where e is the first edge
+// (tp1 over tseg(e)) and where it is the second (tp2 of trev over tseg(e)),
+// added in triplet order.
+__global__ void tri_pos_edge_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
+                                    const float4* __restrict__ tp1, const float4* __restrict__ tp2, long long Ne,
+                                    float4* __restrict__ out) {
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  double x = 0, y = 0, z = 0;
+  for (int t = trowptr[e]; t < trowptr[e + 1]; ++t) {
+    const float4 a = tp1[t], b = tp2[trev[t]];
+    x += (double)a.x + b.x;
+    y += (double)a.y + b.y;
+    z += (double)a.z + b.z;
+  }
+  out[e] = make_float4((float)x, (float)y, (float)z, 0.f);
+}
+
 }  // namespace janus

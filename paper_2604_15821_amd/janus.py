@@ -87,6 +87,8 @@ def _lib():
                                           vp, vp, vp, C.POINTER(Debug), vp]
         lib.janus_step_ex.argtypes = [vp, vp, vp, vp, vp, i32, i32, C.POINTER(Edges), vp, vp, vp, vp,
                                       C.POINTER(Labels), vp, vp, vp, vp, vp, C.POINTER(Debug), vp]
+        lib.janus_step_pos.argtypes = [vp, vp, vp, vp, vp, i32, i32, C.POINTER(Edges), vp, vp, vp, vp,
+                                       C.POINTER(Labels), vp, vp, vp, vp, vp, vp, C.POINTER(Debug), vp]
         lib.janus_grouped_gemm.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
         lib.janus_grouped_wgrad.argtypes = [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp]
         lib.janus_grouped_gemm_noalloc.argtypes = [vp, vp, vp, vp, i32, i64, i32, i32, i32, vp]
@@ -107,9 +109,10 @@ def exported_symbols():
     """Names the library exports (checked against include/janus.h by the CPU tests)."""
     lib = _lib()
     names = ["janus_create", "janus_destroy", "janus_weight_layout", "janus_build_edges", "janus_step",
-             "janus_step_stress", "janus_step_ex",
+             "janus_step_stress", "janus_step_ex", "janus_step_pos",
              "janus_grouped_gemm", "janus_grouped_gemm_noalloc", "janus_grouped_wgrad", "janus_wgrad_chunk_rows",
-             "janus_profile_enable", "janus_profile_read",
+             "janus_profile_enable",
+             "janus_profile_read",
              "janus_set_workspace_limit", "janus_set_concurrency", "janus_last_chunks", "janus_last_triplets",
              "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
@@ -339,12 +342,13 @@ class Context:
 
     # ----------------------------------------------------------------- step
     def step(self, pos, cell, species, offsets, nl: NeighborList, W, E_ref, F_ref, out=None, debug=None,
-             S_ref=None, stress=None, labels=None):
+             S_ref=None, stress=None, labels=None, dLdR=None):
         """One training step; returns (loss [1], E [S], F [N,3], dLdW [like W]) device tensors.
 
         With S_ref [S,3,3] (needed when the model's w_S > 0) or a stress output
         tensor [S,3,3], writes the stress into `stress`; labels = (task, charge,
-        spin) int32 device tensors [S] (needed when the model has n_tasks > 0)."""
+        spin) int32 device tensors [S] (needed when the model has n_tasks > 0);
+        with a dLdR tensor [N,3], also writes the loss gradient in the positions."""
         import torch
         dev = pos.device
         N = pos.shape[0]
@@ -359,7 +363,14 @@ class Context:
         if debug is not None:
             dbg = Debug(*[_ptr(debug.get(k)).value for k in Debug.KEYS])
         dbgp = C.byref(dbg) if dbg is not None else None
-        if S_ref is None and stress is None and labels is None:
+        _arg(dLdR, "dLdR", "f32", (N, 3), dev, optional=True)
+        if dLdR is not None:
+            lab = Labels(*[_ptr(x).value for x in labels]) if labels is not None else None
+            rc = _lib().janus_step_pos(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S,
+                                       C.byref(edges), _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(S_ref),
+                                       C.byref(lab) if lab is not None else None, _ptr(loss), _ptr(E), _ptr(F),
+                                       _ptr(stress), _ptr(dW), _ptr(dLdR), dbgp, _stream())
+        elif S_ref is None and stress is None and labels is None:
             rc = _lib().janus_step(self.h, _ptr(pos), _ptr(cell), _ptr(species), _ptr(offsets), N, S, C.byref(edges),
                                    _ptr(W), _ptr(E_ref), _ptr(F_ref), _ptr(loss), _ptr(E), _ptr(F), _ptr(dW), dbgp,
                                    _stream())
