@@ -222,6 +222,7 @@ def main():
                    **({"stress_weight": m.w_S} if m.w_S else {}),
                    **({"robust_loss": {"huber_delta": m.huber_delta, "tau": m.robust_tau}} if m.robust else {}),
                    **({"attention_heads": m.n_heads} if m.n_heads else {}),
+                   **({"router": "species pair + linear layer on the edge token"} if m.route_feat else {}),
                    **({"tasks": m.n_tasks, "charges": m.n_charges, "spins": m.n_spins} if m.n_tasks else {})},
         "edges_per_s": Ne / (ms * 1e-3),
         "triplets": Nt,

@@ -107,6 +107,18 @@ enum {
  *              first, then the statistics, then each chunk again through
  *              all four phases (the first two are recomputed).  At most 256
  *              tasks.
+ *   route_feat 0: the edge router is the species-pair table.  1: routing on
+ *              the evolving edge tokens (paper Sec. "Sparse mixture-of-experts
+ *              (MoE) routing", with the router a linear layer on the token):
+ *              logits l_e = (Pc[Z_i] + Pn[Z_j]) + X_e Wr + beta per block, Wr
+ *              [d, E] in the blob after beta; top_k of the fp32 logits
+ *              (descending, lower index first on ties), gates the softmax
+ *              probabilities, so forces and every gradient include the gates'
+ *              dependence on X_e.  The decision is exact only up to the fp32
+ *              rounding of the logits: a token whose k-th and (k+1)-th logits
+ *              are that close may be routed differently from a float64
+ *              evaluation (janus_debug.gap reports every token's margin).  Not
+ *              with attention (JANUS_EUNSUPPORTED).
  */
 typedef struct janus_config {
   int32_t n_species;
@@ -138,6 +150,7 @@ typedef struct janus_config {
   int32_t robust;
   float huber_delta;
   float robust_tau;
+  int32_t route_feat;
 } janus_config;
 
 typedef struct janus_ctx janus_ctx;
@@ -188,6 +201,9 @@ typedef struct janus_edges {
  * With the feature-update MoE:
  *   eidf   [T*N*top_k_f] int32 chosen experts of every atom
  *   gatef  [T*N*top_k_f] fp32  their gates
+ * With routing on the edge tokens (route_feat):
+ *   gap    [T*Ne]        fp32  l_(k) - l_(k+1) of every token's fp32 logits, the
+ *                               margin of its routing decision (+inf when k = E)
  */
 typedef struct janus_debug {
   int32_t* eid;
@@ -201,6 +217,7 @@ typedef struct janus_debug {
   float* gate3;
   int32_t* eidf;
   float* gatef;
+  float* gap;
 } janus_debug;
 
 /* Create a context for `cfg` on the current device (paper Sec. "Runtime for

@@ -111,6 +111,7 @@ class Params:
     heads: int = 0
     r_cut: float = 0.0
     task: bool = False
+    route_feat: bool = False
 
     @classmethod
     def from_weights(cls, weights, model):
@@ -118,7 +119,7 @@ class Params:
         return cls(w=w, T=model.n_blocks, k=model.top_k, E=model.n_experts, three=bool(model.three_body),
                    k3=model.top_k3, E3=model.n_experts3, atom=bool(model.atom_moe),
                    kf=model.top_k_f, Ef=model.n_experts_f, heads=model.n_heads, r_cut=model.r_cut,
-                   task=model.n_tasks > 0)
+                   task=model.n_tasks > 0, route_feat=bool(getattr(model, "route_feat", 0)))
 
     def blk(self, t, name):
         return self.w[f"blocks.{t}.{name}"]
@@ -218,6 +219,8 @@ class Routing:
     inv: np.ndarray      # [Ne*k] int32 flattened (e*k + c) held by each slot
     tri: object = None   # routing of the triplet tokens of the same block (three-body term)
     atom: object = None  # routing of the atom tokens of the feature-update MoE
+    Wr: object = None    # routing on the edge tokens: the router's weight [d, E] (gates depend on X)
+    gap: object = None   # routing on the edge tokens: l_(k) - l_(k+1) of every token (float64)
 
 
 def route(species, ei, ej, Pc, Pn, beta, k):
@@ -269,8 +272,29 @@ def _route_logits(l32, l64, k):
     return Routing(eid=eid, gate=gate, prob=prob, counts=counts, pos=pos.reshape(eid.shape), inv=inv)
 
 
+def route_features(species, g, Pc, Pn, beta, Wr, X, k):
+    """Routing on the evolving edge tokens (the variant of paper Sec. "Sparse MoE routing"
+    whose router is a linear layer on the features): logits
+        l_e = (Pc[Z_i] + Pn[Z_j]) + X_e Wr + beta
+    in float64; top-k descending with the lower index first on ties, gates the softmax
+    probabilities of the chosen experts.  The decision is a float64 one here; an fp32
+    implementation may differ only where the k-th and (k+1)-th logits are within its
+    rounding, which `gap` (l_(k) - l_(k+1), +inf when k = E) exposes."""
+    l64 = ((np.asarray(Pc, np.float64)[species[g.ei]] + np.asarray(Pn, np.float64)[species[g.ej]])
+           + X @ np.asarray(Wr, np.float64)) + np.asarray(beta, np.float64)[None, :]
+    rt = _route_logits(l64, l64, k)
+    srt = -np.sort(-l64, axis=1)
+    rt.gap = srt[:, k - 1] - srt[:, k] if k < l64.shape[1] else np.full(l64.shape[0], np.inf)
+    rt.Wr = np.asarray(Wr, np.float64)
+    return rt
+
+
 def route_all(species, g: Graph, P: Params):
-    """Routing of every block (edges, and triplets when the model has the angular term)."""
+    """Routing of every block (edges, and triplets when the model has the angular term).
+    With routing on the edge tokens, block t's decision needs X^t, so the blocks'
+    forward pass runs here block by block."""
+    if P.route_feat:
+        return _route_all_features(species, g, P)
     out = []
     for t in range(P.T):
         rt = route(species, g.ei, g.ej, P.blk(t, "Pc"), P.blk(t, "Pn"), P.blk(t, "beta"), P.k)
@@ -280,6 +304,29 @@ def route_all(species, g: Graph, P: Params):
         if P.atom:
             rt.atom = route_atoms(species, P.blk(t, "Pf"), P.blk(t, "betaf"), P.kf)
         out.append(rt)
+    return out
+
+
+def _route_all_features(species, g: Graph, P: Params):
+    out = []
+    N = species.shape[0]
+    h = embed(species, g, P)
+    for t in range(P.T):
+        tri = atom = None
+        if g.tri is not None:
+            tri = route_triplets(species, g, P.blk(t, "P3a"), P.blk(t, "P3b"), P.blk(t, "P3c"), P.blk(t, "beta3"),
+                                 P.k3)
+        if P.atom:
+            atom = route_atoms(species, P.blk(t, "Pf"), P.blk(t, "betaf"), P.kf)
+        # X^t needs this block's triplet routing only
+        part = out + [Routing(eid=None, gate=None, prob=None, counts=None, pos=None, inv=None, tri=tri)]
+        _, X = _block_tokens(g, P, t, h, part)
+        rt = route_features(species, g, P.blk(t, "Pc"), P.blk(t, "Pn"), P.blk(t, "beta"), P.blk(t, "Wr"), X, P.k)
+        rt.tri, rt.atom = tri, atom
+        out.append(rt)
+        m = _moe(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X)
+        u = h + _aggregate(g, P, t, m, N)
+        h = u + _atom_moe(P, t, out, u)
     return out
 
 
@@ -305,12 +352,19 @@ def _moe(rt, E, W1, W2, X):
 
 
 def _moe_backward(rt, E, W1, W2, X, mbar):
-    """Adjoint of the MoE input X given the adjoint mbar of its output."""
+    """Adjoint of the MoE input X given the adjoint mbar of its output.  With routing on
+    the tokens (rt.Wr) the gates depend on X too: the gate adjoints <mbar, Y_c> go
+    through the softmax Jacobian to the logits, and from them through Wr to X."""
     Xbar = np.zeros_like(X)
+    Pg = np.zeros(rt.eid.shape) if rt.Wr is not None else None
     for c, x, rows in _expert_groups(rt, E):
         A = X[rows] @ W1[x]
         Sbar = (rt.gate[rows, c][:, None] * mbar[rows]) @ W2[x].T
         Xbar[rows] += (silu_d1(A) * Sbar) @ W1[x].T
+        if Pg is not None:
+            Pg[rows, c] = ((silu(A) @ W2[x]) * mbar[rows]).sum(1)
+    if Pg is not None:
+        Xbar += _logit_adjoint(rt, Pg) @ rt.Wr.T
     return Xbar
 
 
@@ -635,16 +689,29 @@ def robust_loss_and_seeds(E, F, E_ref, F_ref, offsets, w_E, w_F, delta, tau, tas
 
 # --------------------------------------------------------------------------- second order
 
+def _gate_tangent(rt, Xd):
+    """Tangent of the chosen gates along Xd when the logits are X Wr + const:
+    gdot_c = p_x (ldot_x - <p, ldot>), x = eid_c, ldot = Xd Wr.  Also returns ldot."""
+    ld = Xd @ rt.Wr
+    mu = (rt.prob * ld).sum(1, keepdims=True)
+    return rt.gate * (np.take_along_axis(ld, rt.eid.astype(np.int64), 1) - mu), ld
+
+
 def _moe_tangent(rt, E, W1, W2, X, Xd):
-    """MoE output and its tangent for input X and input tangent Xd."""
+    """MoE output and its tangent for input X and input tangent Xd (with routing on the
+    tokens, the gates' own tangent adds gdot_c Y_c)."""
     m = np.zeros((X.shape[0], W2.shape[2]))
     md = np.zeros_like(m)
+    gd = _gate_tangent(rt, Xd)[0] if rt.Wr is not None else None
     for c, x, rows in _expert_groups(rt, E):
         A, Ad = X[rows] @ W1[x], Xd[rows] @ W1[x]
         gt = rt.gate[rows, c][:, None]
         s0, s1, _ = silu_family(A)
-        m[rows] += gt * (s0 @ W2[x])
+        Y = s0 @ W2[x]
+        m[rows] += gt * Y
         md[rows] += gt * ((s1 * Ad) @ W2[x])
+        if gd is not None:
+            md[rows] += gd[rows, c][:, None] * Y
     return m, md
 
 
@@ -733,13 +800,18 @@ def _moe_reverse(rt, E, W1, W2, X, Xd, Pm, Tm):
     """Reverse sweep of a MoE layer through its primal and tangent outputs.
 
     Pm, Tm: adjoints of the output and of its tangent.  Returns the adjoints
-    of the input and its tangent, the expert weight gradients and the
-    adjoint of every gate.
+    of the input and its tangent, the expert weight gradients, the adjoint of
+    the router logits and, with routing on the tokens (logits X Wr + const,
+    whose gates have the tangent gdot = J(p) Xd Wr), the router weight gradient
+    (else None).
     """
     PX = np.zeros_like(X)
     TX = np.zeros_like(X)
     Pg = np.zeros(rt.gate.shape)
+    Tg = np.zeros(rt.gate.shape)          # adjoint of the gate tangents
     dW1, dW2 = np.zeros_like(W1), np.zeros_like(W2)
+    feat = rt.Wr is not None
+    gd, ld = _gate_tangent(rt, Xd) if feat else (None, None)
     for c, x, rows in _expert_groups(rt, E):
         gt = rt.gate[rows, c][:, None]
         A, Ad = X[rows] @ W1[x], Xd[rows] @ W1[x]
@@ -748,6 +820,10 @@ def _moe_reverse(rt, E, W1, W2, X, Xd, Pm, Tm):
         Y, Yd = S @ W2[x], Sd @ W2[x]
         Pg[rows, c] = (Y * Pm[rows]).sum(1) + (Yd * Tm[rows]).sum(1)
         PY, TY = gt * Pm[rows], gt * Tm[rows]
+        if feat:
+            # md += gdot Y: adjoints of the gate tangent and of Y through it
+            Tg[rows, c] = (Y * Tm[rows]).sum(1)
+            PY = PY + gd[rows, c][:, None] * Tm[rows]
         dW2[x] += S.T @ PY + Sd.T @ TY
         PS, TS = PY @ W2[x].T, TY @ W2[x].T
         TAd = s1 * TS
@@ -755,7 +831,22 @@ def _moe_reverse(rt, E, W1, W2, X, Xd, Pm, Tm):
         dW1[x] += X[rows].T @ PA + Xd[rows].T @ TAd
         PX[rows] += PA @ W1[x].T
         TX[rows] += TAd @ W1[x].T
-    return PX, TX, dW1, dW2, Pg
+    Pl = _logit_adjoint(rt, Pg)
+    if not feat:
+        return PX, TX, dW1, dW2, Pl, None
+    # gdot_c = p_x (ld_x - <p, ld>): adjoint of ld is J(p)^T Tg, and of p
+    #   Pp_z = Tg~_z (ld_z - <p, ld>) - ld_z sum_c Tg_c p_x(c)   (Tg~: Tg scattered to the chosen experts)
+    Tl = _logit_adjoint(rt, Tg)
+    Tt = np.zeros(rt.prob.shape)
+    np.put_along_axis(Tt, rt.eid.astype(np.int64), Tg, 1)
+    mu = (rt.prob * ld).sum(1, keepdims=True)
+    Pp = Tt * (ld - mu) - ld * (Tg * rt.gate).sum(1, keepdims=True)
+    Pl = Pl + rt.prob * (Pp - (rt.prob * Pp).sum(1, keepdims=True))
+    # l = X Wr + const, ld = Xd Wr
+    PX += Pl @ rt.Wr.T
+    TX += Tl @ rt.Wr.T
+    dWr = X.T @ Pl + Xd.T @ Tl
+    return PX, TX, dW1, dW2, Pl, dWr
 
 
 def _logit_adjoint(rt, Pg):
@@ -803,10 +894,10 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None, g
         if P.atom:
             # h^{t+1} = u + MoE_f(u), hd^{t+1} = ud + D MoE_f(u) ud: adjoints of u, ud
             u, ud = tc["u"][t], tc["ud"][t]
-            PU, TU, dW1f, dW2f, Pgf = _moe_reverse(rt.atom, P.Ef, P.blk(t, "W1f"), P.blk(t, "W2f"), u, ud, Ph, Th)
+            PU, TU, dW1f, dW2f, Plf, _ = _moe_reverse(rt.atom, P.Ef, P.blk(t, "W1f"), P.blk(t, "W2f"), u, ud, Ph, Th)
             grad[f"blocks.{t}.W1f"] = dW1f
             grad[f"blocks.{t}.W2f"] = dW2f
-            grad[f"blocks.{t}.Pf"] = _seg(species, S_, _logit_adjoint(rt.atom, Pgf))
+            grad[f"blocks.{t}.Pf"] = _seg(species, S_, Plf)
             Ph, Th = Ph + PU, Th + TU
         F, Fd, X, Xd = _block_tangent_tokens(g, P, t, h, hd, Bdot, Gd, routing)
         if P.heads:
@@ -818,9 +909,11 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None, g
             grad[f"blocks.{t}.Wo"] = dWo
         else:
             Pm, Tm = Ph[g.ei], Th[g.ei]
-        PX, TX, dW1, dW2, Pg = _moe_reverse(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd, Pm, Tm)
+        PX, TX, dW1, dW2, Pl, dWr = _moe_reverse(rt, P.E, P.blk(t, "W1"), P.blk(t, "W2"), X, Xd, Pm, Tm)
         grad[f"blocks.{t}.W1"] = dW1
         grad[f"blocks.{t}.W2"] = dW2
+        if dWr is not None:
+            grad[f"blocks.{t}.Wr"] = dWr
         # X = F * h_j (+ q) ;  Xd = Fd * h_j + F * hd_j (+ qd)
         PF = PX * h[g.ej] + TX * hd[g.ej]
         TFd = TX * h[g.ej]
@@ -830,16 +923,15 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None, g
             geo["Bd"] += TFd @ P.blk(t, "W_b").T
         Ph_new = Ph + _seg(g.ej, N, PX * F + TX * Fd)
         Th_new = Th + _seg(g.ej, N, TX * F)
-        # gates: g_ec = softmax(l_e)[eid_ec];  l_e = Pc[Z_i] + Pn[Z_j] + beta
-        Pl = _logit_adjoint(rt, Pg)
+        # gates: g_ec = softmax(l_e)[eid_ec];  l_e = Pc[Z_i] + Pn[Z_j] (+ X_e Wr) + beta
         grad[f"blocks.{t}.Pc"] = _seg(species[g.ei], S_, Pl)
         grad[f"blocks.{t}.Pn"] = _seg(species[g.ej], S_, Pl)
         if g.tri is not None:
             tri, rt3 = g.tri, rt.tri
             Zpre, Zpred, hj2, hdj2, Z, Zd = _tri_tangent_tokens(g, P, t, h, hd, Gd)
             # q_e = sum over the triplets of e, so the token adjoints are those of X_e
-            PZ, TZ, dW1a, dW2a, Pg3 = _moe_reverse(rt3, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z, Zd,
-                                                  PX[tri.te], TX[tri.te])
+            PZ, TZ, dW1a, dW2a, Pl3, _ = _moe_reverse(rt3, P.E3, P.blk(t, "W1a"), P.blk(t, "W2a"), Z, Zd,
+                                                     PX[tri.te], TX[tri.te])
             grad[f"blocks.{t}.W1a"] = dW1a
             grad[f"blocks.{t}.W2a"] = dW2a
             # Z = Zpre * h_j2 ;  Zd = Zpred * h_j2 + Zpre * hd_j2 ;  Zpre = G W_a, Zpred = Gd W_a
@@ -852,7 +944,6 @@ def weight_gradient(species, g: Graph, P: Params, routing, lam, phi, Psi=None, g
             j2 = g.ej[tri.te2]
             Ph_new = Ph_new + _seg(j2, N, PZ * Zpre + TZ * Zpred)
             Th_new = Th_new + _seg(j2, N, TZ * Zpre)
-            Pl3 = _logit_adjoint(rt3, Pg3)
             grad[f"blocks.{t}.P3a"] = _seg(species[g.ei[tri.te]], S_, Pl3)
             grad[f"blocks.{t}.P3b"] = _seg(species[g.ej[tri.te]], S_, Pl3)
             grad[f"blocks.{t}.P3c"] = _seg(species[j2], S_, Pl3)

@@ -239,6 +239,17 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     hipLaunchKernelGGL(set_rows_kernel, dim3(1), dim3(64), 0, st, p.rowN, N, p.rowE, Ne);
     build_tables(st, p.rowN, 1, p.kcN, p.tilesN, p.ntN, p.chunksN, p.ncN, p.cfN);
     build_tables(st, p.rowE, 1, p.kcE, nullptr, nullptr, p.chunksE, p.ncE, p.cfE);
+    if (p.rf) {
+      // routing on the edge tokens: products over the edges, the identity slot map,
+      // gates of one, the zero-padded router weights and their gradient accumulators
+      build_tables(st, p.rowE, 1, p.kcR, p.tilesE, p.ntE, p.chunksR, p.ncR, p.cfR);
+      hipLaunchKernelGGL(iota_kernel, dim3(cdiv(Ne + 1, 256)), dim3(256), 0, st, p.iotaE, (int)Ne);
+      hipLaunchKernelGGL(fill_kernel, dim3(cdiv(M + 1, 256)), dim3(256), 0, st, p.ones, M + 1, 1.f);
+      for (int t = 0; t < T; ++t)
+        hipLaunchKernelGGL(wr_pad_kernel, dim3(cdiv((long long)d * p.Ep, 256)), dim3(256), 0, st,
+                           Wp(blk(t, "Wr")), d, Ee, p.Ep, p.WrP + (long long)t * d * p.Ep);
+      JANUS_HIP_TRY(hipMemsetAsync(p.dWrP, 0, sizeof(float) * T * d * p.Ep, st));
+    }
     if (attn) {
       build_tables(st, p.rowE, 1, p.kcA, p.tilesE, p.ntE, p.chunksA, p.ncA, p.cfA);
       if (Ne > 0)
@@ -269,9 +280,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       ra.off = p.off + t * (Ee + 1);
       ra.pos = p.pos + t * M;
       ra.slot_gate = p.slot_gate + t * M;
-      route_block(st, ra);
-      build_tables(st, ra.off, Ee, p.kc, p.tiles + (long long)t * p.mt, p.ntiles + t,
-                   p.chunks + (long long)t * p.mc, p.nchunks + t, p.cfirst + t * (Ee + 1));
+      if (!p.rf) {   // routing on the edge tokens is decided in the forward pass
+        route_block(st, ra);
+        build_tables(st, ra.off, Ee, p.kc, p.tiles + (long long)t * p.mt, p.ntiles + t,
+                     p.chunks + (long long)t * p.mc, p.nchunks + t, p.cfirst + t * (Ee + 1));
+      }
       if (three) {
         if (Nt > 0)
           hipLaunchKernelGGL(tri_route_kernel, dim3(cdiv(Nt, 128)), dim3(128), 0, st, species, ei, ej,
@@ -340,6 +353,18 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   auto POS = [&](int t) { return (const int*)(p.pos + t * M); };
   auto GATE = [&](int t) { return (const float*)(p.gate + t * M); };
   auto SG = [&](int t) { return (const float*)(p.slot_gate + t * M); };
+  // routing on the edge tokens, block t
+  const long long Ep = p.Ep, sEdR = Ne * d + 4, sEp = Ne * Ep + 4;
+  auto EID = [&](int t) { return (const int*)(p.eid + t * M); };
+  auto XeR = [&](int t) { return p.Xe + t * sEdR; };
+  auto YstR = [&](int t) { return p.Yst + t * (M * d + 4); };
+  auto FPR = [&](int t) { return p.fprob + t * sEp; };
+  auto GBR = [&](int t) { return p.gbar + t * M; };
+  auto LBR = [&](int t) { return p.lbar + t * sEp; };
+  auto P3R = [&](int t) { return p.P3 + t * sEp; };
+  auto GHR = [&](int t) { return p.gh + t * M; };
+  auto WRP = [&](int t) { return (const float*)(p.WrP + (long long)t * d * Ep); };
+  auto DWR = [&](int t) { return p.dWrP + (long long)t * d * Ep; };
   auto TL = [&](int t) { return (const RowsTile*)(p.tiles + (long long)t * p.mt); };
   auto CH = [&](int t) { return (const WChunk*)(p.chunks + (long long)t * p.mc); };
   auto CF = [&](int t) { return (const int*)(p.cfirst + t * (Ee + 1)); };
@@ -419,7 +444,35 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                      Ne, d, p.Q);
       }
     }
-    if (Ne > 0) {
+    if (p.rf) {
+      // edge tokens -> router logits -> top-k, gates, expert-grouped slots (block t's routing)
+      {
+        PROF(PROF_EDGE, 0, Ne * (4.0 * nb + 8.0 * d));
+        if (Ne > 0)
+          LAUNCH_VPL_K(dispatch_x_kernel, d, 1, gE, b256, ldsW, st, (const float*)p.B, nb, Wb,
+                       (const float*)HV(p.h, t), ej, (const int*)p.iotaE, Ne, d, XeR(t),
+                       (const float*)(three && Nt > 0 ? p.Q : nullptr));
+      }
+      {
+        PROF(PROF_ROUTE, 2.0 * Ne * d * Ep, Ne * (4.0 * d + 4.0 * Ep));
+        launch_rows<false>(st, LoadPlain{XeR(t), d}, WRP(t), d, (int)Ep, p.tilesE, p.ntE, p.mtE,
+                           EpiStore{p.Lw, Ep});
+        float* gap = dbg && dbg->gap ? dbg->gap + t * ca.Ne_tot + ca.e0 : nullptr;
+        if (Ne > 0)
+          hipLaunchKernelGGL(feat_route_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, (const float*)p.Lw, species, ei, ej,
+                             Wp(blk(t, "Pc")), Wp(blk(t, "Pn")), Wp(blk(t, "beta")), Ne, Ee, (int)Ep, k,
+                             p.eid + t * M, p.gate + t * M, FPR(t), gap);
+        sort_tokens(st, p.eid + t * M, p.gate + t * M, M, Ee, p.cnt, p.colpre, p.total + t * Ee, p.off + t * (Ee + 1),
+                    p.pos + t * M, p.slot_gate + t * M);
+        build_tables(st, p.off + t * (Ee + 1), Ee, p.kc, p.tiles + (long long)t * p.mt, p.ntiles + t,
+                     p.chunks + (long long)t * p.mc, p.nchunks + t, p.cfirst + t * (Ee + 1));
+      }
+      if (Ne > 0) {
+        PROF(PROF_EDGE, 0, Ne * (4.0 * d + 8.0 * k + 4.0 * k * d));
+        LAUNCH_VPL_K(edge_gather_kernel, d, k, gE, b256, 0, st, POS(t), (const float*)nullptr,
+                     (const float*)XeR(t), Ne, d, Xs(t));
+      }
+    } else if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_dispatch);
       LAUNCH_VPL_K(dispatch_x_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
                  POS(t), Ne, d, Xs(t), (const float*)(three && Nt > 0 ? p.Q : nullptr));
@@ -430,7 +483,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     }
     {
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
-      launch_rows<false>(st, LoadSilu{Aa(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiRowScale{p.T1, SG(t), d});
+      if (p.rf)   // expert outputs before gating (the gates' adjoints need them)
+        launch_rows<false>(st, LoadSilu{Aa(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiStore{YstR(t), d});
+      else
+        launch_rows<false>(st, LoadSilu{Aa(t), h}, W2, h, d, TL(t), p.ntiles + t, p.mt, EpiRowScale{p.T1, SG(t), d});
     }
     // u = h + messages (h^{t+1} itself without the feature-update MoE)
     float* u_out = atom ? p.ut : HV(p.h, t + 1);
@@ -464,6 +520,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         launch_rows<false>(st, LoadPlain{OSt(t), d}, Wp(blk(t, "Wo")), d, d, p.tilesN, p.ntN, p.mtN,
                            EpiAdd{u_out, HV(p.h, t), d});
       }
+    } else if (p.rf) {
+      PROF(PROF_ATOM, 0, by_combine + Ne * 4.0 * k);
+      LAUNCH_VPL_K(combine_fwd_gated_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), (const float*)YstR(t),
+                   (const float*)HV(p.h, t), N, d, u_out);
     } else {
       PROF(PROF_ATOM, 0, by_combine);
       LAUNCH_VPL_K(combine_fwd_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)p.T1,
@@ -582,6 +642,13 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       PROF(PROF_ATOM, 0, by_gather);
       LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), hbar_u, N, d, Ybs(t));
     }
+    if (p.rf && Ne > 0) {
+      // the gates' adjoints <mbar_i, Y_c> -> logit adjoints -> the router's part of Xbar
+      PROF(PROF_ROUTE, 2.0 * Ne * d * Ep, Ne * (4.0 * d + 4.0 * k * d + 8.0 * Ep));
+      LAUNCH_VPL_K(feat_p2_kernel, d, k, gE, b256, 0, st, ei, POS(t), EID(t), GATE(t), (const float*)FPR(t), Ee,
+                   (int)Ep, hbar_u, (const float*)YstR(t), Ne, d, GBR(t), LBR(t));
+      launch_rows<true>(st, LoadPlain{LBR(t), Ep}, WRP(t), (int)Ep, d, p.tilesE, p.ntE, p.mtE, EpiStore{p.Xadd, d});
+    }
     {
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
       launch_rows<true>(st, LoadPlain{Ybs(t), d}, W2, d, h, TL(t), p.ntiles + t, p.mt,
@@ -594,7 +661,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     if (Ne > 0) {
       PROF(PROF_EDGE, 0, by_p2);
       LAUNCH_VPL_K(edge_p2_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
-                 (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)p.T1, Xbar(t), Fbar(t), p.rbar, p.Pe);
+                 (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)p.T1, Xbar(t), Fbar(t), p.rbar, p.Pe,
+                 (const float*)(p.rf ? p.Xadd : nullptr));
     }
     if (three && Nt > 0) {
       // triplet messages' backward: Ybar3 = g3 Xbar_e -> experts -> Zbar; feature-geometry adjoints
@@ -627,6 +695,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                  (const float*)nullptr, N, d, HV(p.hh, t));
     }
   }
+  // routing on the edge tokens: phase 4 needs the phase-2 atom adjoints, which it overwrites
+  if (p.rf)
+    JANUS_HIP_TRY(hipMemcpyAsync(p.hh2, p.hh, sizeof(float) * (T + 1) * Nd, hipMemcpyDeviceToDevice, st));
   {
     PROF(PROF_OTHER, 0, Ne * 40.0 + N * 24.0);
     if (three && Ne > 0)
@@ -754,7 +825,17 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       // with triplets, P_e already holds the triplet part written by tri_p3
       LAUNCH_VPL_K(edge_p3_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, (const float*)p.dB, nb, Wb,
                    (const float*)HV(p.h, t), ej, POS(t), Ne, d, (const float*)Xbar(t), hht_t, (const float*)p.rt,
-                   p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr), (int)tri_t, (const float*)p.d2B, p.rpos);
+                   p.T1, p.Pe, (const float*)(tri_t ? p.Q : nullptr), (int)tri_t, (const float*)p.d2B, p.rpos,
+                   p.rf ? p.Xh : (float*)nullptr);
+    }
+    if (p.rf && Ne > 0) {
+      // lh = Xbt Wr -> gate adjoints gh and softmax adjoints P3; dWr += Xbt^T lbar
+      PROF(PROF_ROUTE, 4.0 * Ne * d * Ep, Ne * (8.0 * d + 16.0 * Ep));
+      launch_rows<false>(st, LoadPlain{p.Xh, d}, WRP(t), d, (int)Ep, p.tilesE, p.ntE, p.mtE, EpiStore{p.Lw, Ep});
+      hipLaunchKernelGGL(feat_p3_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, EID(t), GATE(t), (const float*)FPR(t),
+                         (const float*)GBR(t), (const float*)p.Lw, Ne, Ee, (int)Ep, k, GHR(t), P3R(t));
+      launch_wgrad(st, LoadPlain{p.Xh, d}, LoadPlain{LBR(t), Ep}, d, (int)Ep, p.chunksR, p.ncR, p.cfR, p.mcR, 1,
+                   p.wrpart, DWR(t), 1);
     }
     // G7 (side stream) beside dW_b and the reverse scatter
     ss.fork();
@@ -841,6 +922,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       PROF(PROF_ATOM, 0, by_cp3);
       LAUNCH_VPL_K(combine_p3_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), (const float*)p.T2, hbar_u3,
                    hht_t, N, d, p.g3 + t * M, uh_out);
+      if (p.rf)   // the gates' adjoints' part: sum_c gh Y_c
+        LAUNCH_VPL_K(feat_hht_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), (const float*)GHR(t),
+                     (const float*)YstR(t), N, d, uh_out);
     }
     if (atom) {
       // double backward of the feature-update MoE's force backward (same products as G5-G8)
@@ -1003,6 +1087,25 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         LAUNCH_VPL_K(edge_gather_kernel, d, k, gE, b256, 0, st, POS(t), (const float*)nullptr, (const float*)p.mta,
                      Ne, d, p.T1);
       }
+    } else if (p.rf) {
+      // logit adjoints (gates of phases 3 and 4, softmax adjoints of phase 3) -> router part of
+      // Xt and dWr; slot rows of the expert outputs' adjoint, gates applied
+      {
+        PROF(PROF_ROUTE, 4.0 * Ne * d * Ep, Ne * (8.0 * d + 4.0 * k * d + 16.0 * Ep));
+        if (Ne > 0) {
+          LAUNCH_VPL_K(feat_p4_kernel, d, k, gE, b256, 0, st, ei, POS(t), EID(t), (const float*)FPR(t), Ee, (int)Ep,
+                       a_u, (const float*)YstR(t), (const float*)(p.g3 + t * M), (const float*)P3R(t), Ne, d,
+                       p.Lw, p.lte);
+          launch_rows<true>(st, LoadPlain{p.Lw, Ep}, WRP(t), (int)Ep, d, p.tilesE, p.ntE, p.mtE,
+                            EpiStore{p.Xadd, d});
+          launch_wgrad(st, LoadPlain{XeR(t), d}, LoadPlain{p.Lw, Ep}, d, (int)Ep, p.chunksR, p.ncR, p.cfR, p.mcR, 1,
+                       p.wrpart, DWR(t), 1);
+        }
+      }
+      PROF(PROF_ATOM, 0, by_gather + N * 4.0 * d + Ne * 4.0 * k);
+      const float* mbar2 = atom ? (const float*)UU(t) : (const float*)(p.hh2 + (long long)(t + 1) * Nd);
+      LAUNCH_VPL_K(gather_feat_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), a_u, (const float*)GHR(t),
+                   mbar2, N, d, p.T1);
     } else {
       // message adjoint, ungated, into the slots
       PROF(PROF_ATOM, 0, by_gather);
@@ -1013,8 +1116,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     {
       // G9: St = mt W2^T -> At = g SiLU'(A) St + C (into Sb); row sums for the gate adjoint
       PROF(PROF_EXPERT_GEMM, f_exp, 0);
-      launch_rows<true>(st, LoadPlain{p.T1, d}, W2, d, h, TL(t), p.ntiles + t, p.mt, EpiP4{Aa(t), Sb(t), SG(t), h},
-                        p.gpart);
+      // (with routing on the edge tokens the slot rows already carry the gates)
+      launch_rows<true>(st, LoadPlain{p.T1, d}, W2, d, h, TL(t), p.ntiles + t, p.mt,
+                        EpiP4{Aa(t), Sb(t), p.rf ? (const float*)p.ones : SG(t), h}, p.gpart);
     }
     {
       // G10: Xt = At W1^T
@@ -1025,8 +1129,8 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     {
       // G12: dW2 += SiLU(A)^T (g mt) (side stream)
       PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
-      launch_wgrad(sd, LoadSilu{Aa(t), h}, LoadRowScale{p.T1, SG(t), d}, h, d, CH(t), p.nchunks + t, CF(t), p.mc,
-                   Ee, p.partial2, Gp(blk(t, "W2")), 1);
+      launch_wgrad(sd, LoadSilu{Aa(t), h}, LoadRowScale{p.T1, p.rf ? (const float*)p.ones : SG(t), d}, h, d, CH(t),
+                   p.nchunks + t, CF(t), p.mc, Ee, p.partial2, Gp(blk(t, "W2")), 1);
     }
     t1_free = ss.mark();
     {
@@ -1040,7 +1144,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_EDGE, 0, by_p4);
         LAUNCH_VPL_K(edge_p4_kernel, d, k, gE, b256, ldsW, st, (const float*)p.B, nb, Wb, (const float*)HV(p.h, t), ej,
                    POS(t), Ne, d, (const float*)p.T2, (const float*)Xbar(t), hht_t, p.Ft, p.Pe,
-                   three ? p.Q : (float*)nullptr, (const float*)p.dB, p.rpos);
+                   three ? p.Q : (float*)nullptr, (const float*)p.dB, p.rpos, (const float*)(p.rf ? p.Xadd : nullptr));
       }
       {
         // dW_b (part 2): B^T Ft
@@ -1050,11 +1154,13 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_OTHER, 0, 0);
-        hipLaunchKernelGGL(gate_total_kernel, dim3(cdiv(M, 256)), b256, 0, st, (const float*)(p.g3 + t * M),
-                           (const float*)p.gpart, POS(t), M, p.ntile, p.gt);
-        hipLaunchKernelGGL(edge_logit_kernel, dim3(cdiv(Ne * Ee, 256)), b256, 0, st, (const int*)(p.pair + t * Ne),
-                           (const float*)(p.pprob + t * np * Ee), (const int*)(p.eid + t * M), (const float*)p.gt, Ne,
-                           k, Ee, p.lte);
+        if (!p.rf) {   // (with routing on the edge tokens p.lte came from feat_p4_kernel)
+          hipLaunchKernelGGL(gate_total_kernel, dim3(cdiv(M, 256)), b256, 0, st, (const float*)(p.g3 + t * M),
+                             (const float*)p.gpart, POS(t), M, p.ntile, p.gt);
+          hipLaunchKernelGGL(edge_logit_kernel, dim3(cdiv(Ne * Ee, 256)), b256, 0, st, (const int*)(p.pair + t * Ne),
+                             (const float*)(p.pprob + t * np * Ee), (const int*)(p.eid + t * M), (const float*)p.gt,
+                             Ne, k, Ee, p.lte);
+        }
         hipLaunchKernelGGL(router_atom_kernel, gN, b256, 0, st, rowptr, rev, Ee,
                            (const float*)p.lte, N, p.partC, p.partN);
         hipLaunchKernelGGL(species_rows_kernel, dim3(nsp), b256, 0, st, (const int*)p.sp_off,
@@ -1138,6 +1244,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   // the caller's stream waits for the side stream's weight gradients
   ss.join();
   if (ss.err != hipSuccess) return janus_set_hip_error(ss.err);
+  if (p.rf)
+    for (int t = 0; t < T; ++t)
+      hipLaunchKernelGGL(wr_unpad_add_kernel, dim3(cdiv((long long)d * Ee, 256)), b256, 0, st, (const float*)DWR(t), d,
+                         Ee, (int)Ep, Gp(blk(t, "Wr")));
   if (dLdR_g) {
     PROF(PROF_OTHER, 0, Ne * 40.0 + N * 24.0);
     const float* psi = S_ref ? p.Psi : nullptr;

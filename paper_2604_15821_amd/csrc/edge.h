@@ -214,20 +214,25 @@ __global__ void gather_atom_kernel(const int* __restrict__ rowptr, const int* __
   }
 }
 
-// Phase 2 per edge: Xbar_e = sum_c Xbar_slot; Fbar = Xbar * h_j;
+// Phase 2 per edge: Xbar_e = sum_c Xbar_slot (+ Xadd_e); Fbar = Xbar * h_j;
 // rbar_e += Fbar . F'_e; P_e = Xbar * F_e (routed to h_j by scatter_rev).
 template <int VPL, int KC>
 __global__ void edge_p2_kernel(const float* __restrict__ B, const float* __restrict__ dB, int nb,
                                const float* __restrict__ Wb, const float* __restrict__ h, const int* __restrict__ ej,
                                const int* __restrict__ pos, long long Ne, int d, const float* __restrict__ Xbs,
                                float* __restrict__ Xbar, float* __restrict__ Fbar, float* __restrict__ rbar,
-                               float* __restrict__ P) {
+                               float* __restrict__ P, const float* __restrict__ Xadd) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
     const float bl = basis_lane(B, e, nb, l), dbl = basis_lane(dB, e, nb, l);
     float xb[VPL], hj[VPL];
     sum_slots<VPL, KC>(Xbs, pos, e, d, l, xb);
+    if (Xadd) {   // the router's part of Xbar (routing on the edge tokens)
+      float xa[VPL];
+      ld_row<VPL>(Xadd + e * d, l, xa);
+      add_row<VPL>(xb, xa);
+    }
     ld_row<VPL>(h + (long long)ej[e] * d, l, hj);
     float F[VPL], Fp[VPL];
     filter_row<VPL>(bl, sW, nb, d, l, F);
@@ -292,7 +297,7 @@ __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restr
                                const int* __restrict__ pos, long long Ne, int d, const float* __restrict__ Xbar,
                                const float* __restrict__ hht, const float* __restrict__ rt, float* __restrict__ Xbts,
                                float* __restrict__ P, const float* __restrict__ QX, int accP,
-                               const float* __restrict__ d2B, float* __restrict__ rpos) {
+                               const float* __restrict__ d2B, float* __restrict__ rpos, float* __restrict__ Xrow) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
@@ -318,6 +323,7 @@ __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restr
     st_row<VPL>(P + e * d, l, p);
 #pragma unroll
     for (int c = 0; c < KC; ++c) st_row<VPL>(Xbts + (long long)pos[e * KC + c] * d, l, X);
+    if (Xrow) st_row<VPL>(Xrow + e * d, l, X);   // Xbt per edge (routing on the edge tokens)
     if (rpos) {
       float F2[VPL];
       filter_row<VPL>(basis_lane(d2B, e, nb, l), sW, nb, d, l, F2);
@@ -383,7 +389,7 @@ __global__ void combine_p3_kernel(const int* __restrict__ rowptr, const int* __r
   }
 }
 
-// Phase 4 per edge: Xt_e = sum_c Xt_slot; Ft_e = Xt * h_j + Q_e * Xbar_e
+// Phase 4 per edge: Xt_e = sum_c Xt_slot (+ Xadd_e); Ft_e = Xt * h_j + Q_e * Xbar_e
 // (Q_e from the double backward); P_e = Xt * F_e (routed to h_j).
 // With rpos: F_e = B(r_e) W_b, so rpos_e += Ft . F'_e.
 template <int VPL, int KC>
@@ -391,7 +397,8 @@ __global__ void edge_p4_kernel(const float* __restrict__ B, int nb, const float*
                                const float* __restrict__ h, const int* __restrict__ ej, const int* __restrict__ pos,
                                long long Ne, int d, const float* __restrict__ Xts, const float* __restrict__ Xbar,
                                const float* __restrict__ hht, float* __restrict__ Ft, float* __restrict__ P,
-                               float* __restrict__ XT, const float* __restrict__ dB, float* __restrict__ rpos) {
+                               float* __restrict__ XT, const float* __restrict__ dB, float* __restrict__ rpos,
+                               const float* __restrict__ Xadd) {
   extern __shared__ float sW[];
   load_lds(sW, Wb, nb * d);
   JANUS_WAVE_LOOP(e, Ne) {
@@ -399,6 +406,11 @@ __global__ void edge_p4_kernel(const float* __restrict__ B, int nb, const float*
     const long long j = ej[e];
     float xt[VPL], hj[VPL], q[VPL], xb[VPL];
     sum_slots<VPL, KC>(Xts, pos, e, d, l, xt);
+    if (Xadd) {   // the router's part of Xt (routing on the edge tokens)
+      float xa[VPL];
+      ld_row<VPL>(Xadd + e * d, l, xa);
+      add_row<VPL>(xt, xa);
+    }
     ld_row<VPL>(h + j * d, l, hj);
     if (hht) ld_row<VPL>(hht + j * d, l, q); else zero_row<VPL>(q);
     ld_row<VPL>(Xbar + e * d, l, xb);

@@ -17,6 +17,7 @@
 #include "route.h"
 #include "tri.h"
 #include "attn.h"
+#include "feat_route.h"
 
 namespace janus {
 
@@ -867,6 +868,7 @@ Layout make_layout(const janus_config& c) {
     L.add(p + "Pc", {S, E});
     L.add(p + "Pn", {S, E});
     L.add(p + "beta", {E});
+    if (c.route_feat) L.add(p + "Wr", {d, E});
     L.add(p + "W1", {E, d, h});
     L.add(p + "W2", {E, h, d});
     if (c.three_body) {
@@ -922,6 +924,9 @@ int check_config(const janus_config* c) {
 
   // heads of 32 columns
   if (c->n_heads && c->d / c->n_heads != kAttnDh) return JANUS_EUNSUPPORTED;
+  if (c->route_feat != 0 && c->route_feat != 1) return JANUS_EINVAL;
+  // routing on the edge tokens goes with the plain message sum (not with attention)
+  if (c->route_feat && c->n_heads) return JANUS_EUNSUPPORTED;
   if (c->atom_moe) {
     if (c->n_experts_f < 1 || c->n_experts_f > 64 || c->top_k_f < 1 || c->top_k_f > 4 ||
         c->top_k_f > c->n_experts_f || c->d_hidden_f < 64)
@@ -1022,6 +1027,16 @@ struct Plan {
   long long Mf;
   int mtf, kcf, mcf, nchf, ntilef;
   int attn, H, mtE, kcA, mcA;
+  // routing on the edge tokens: per block the edge tokens [Ne, d], the expert outputs
+  // before gating [M, d], the full softmax [Ne, Ep], the phase-2 gate and logit
+  // adjoints, the phase-3 gate adjoints and softmax adjoints, the padded router
+  // weight and its gradient [d, Ep]; temporaries over the edges; the phase-2 atom
+  // adjoints kept for phase 4; a row of ones (gates already applied); the weight
+  // gradient's chunk table over the edges
+  int rf, Ep, kcR, mcR;
+  float *Xe, *Yst, *fprob, *gbar, *lbar, *P3, *gh, *WrP, *dWrP, *Lw, *Xadd, *Xh, *hh2, *ones, *wrpart;
+  int *iotaE, *ncR, *cfR;
+  WChunk* chunksR;
 };
 
 size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, long long Ne, long long Nt = 0,
@@ -1156,8 +1171,14 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   }
   p.attn = c.n_heads ? 1 : 0;
   p.H = c.n_heads;
+  p.rf = c.route_feat ? 1 : 0;
+  p.Ep = (E + 15) / 16 * 16;
+  p.mtE = max_rows_tiles(Ne, 1);
+  if (p.rf) {
+    p.kcR = wgrad_chunk_rows(Ne, d, p.Ep);
+    p.mcR = max_wchunks(Ne, 1, p.kcR);
+  }
   if (p.attn) {
-    p.mtE = max_rows_tiles(Ne, 1);
     p.kcA = wgrad_chunk_rows(Ne, d, 3 * d);
     p.mcA = max_wchunks(Ne, 1, p.kcA);
     part = std::max(part, (long long)p.mcA * d * 3 * d);
@@ -1303,13 +1324,44 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.mta = cv.take<float>(Ed);
     p.osh = cv.take<float>(Nd + 4);
     p.rbh = cv.take<float>(Ne * p.H + 4);
-    p.tilesE = cv.take<RowsTile>(p.mtE);
-    p.ntE = cv.take<int>(1);
     p.chunksA = cv.take<WChunk>(p.mcA);
     p.ncA = cv.take<int>(1);
     p.cfA = cv.take<int>(2);
   }
+  p.tilesE = nullptr;
+  p.ntE = nullptr;
+  if (p.attn || p.rf) {
+    p.tilesE = cv.take<RowsTile>(p.mtE);
+    p.ntE = cv.take<int>(1);
+  }
+  if (p.rf) {
+    const long long Ep = p.Ep, Ed = Ne * d + 4;
+    p.Xe = cv.take<float>(T * Ed);
+    p.Yst = cv.take<float>(T * (M * d + 4));
+    p.fprob = cv.take<float>(T * (Ne * Ep + 4));
+    p.gbar = cv.take<float>(T * M + 4);
+    p.lbar = cv.take<float>(T * (Ne * Ep + 4));
+    p.P3 = cv.take<float>(T * (Ne * Ep + 4));
+    p.gh = cv.take<float>(T * M + 4);
+    p.WrP = cv.take<float>(T * d * Ep);
+    p.dWrP = cv.take<float>(T * d * Ep);
+    p.Lw = cv.take<float>(Ne * Ep + 4);
+    p.Xadd = cv.take<float>(Ed);
+    p.Xh = cv.take<float>(Ed);
+    p.hh2 = cv.take<float>((T + 1) * Nd + 4);
+    p.ones = cv.take<float>(M + 4);
+    p.wrpart = cv.take<float>((long long)p.mcR * d * Ep + 4);
+    p.iotaE = cv.take<int>(Ne + 1);
+    p.chunksR = cv.take<WChunk>(p.mcR);
+    p.ncR = cv.take<int>(1);
+    p.cfR = cv.take<int>(2);
+  }
   return cv.size();
+}
+
+__global__ void fill_kernel(float* __restrict__ out, long long n, float v) {
+  const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < n) out[q] = v;
 }
 
 // Identity CSR [0, 1, ..., N]: every atom is one token of the feature-update MoE.

@@ -34,7 +34,7 @@ class Config(C.Structure):
         ("w_F", C.c_float), ("atom_moe", C.c_int32), ("n_experts_f", C.c_int32), ("top_k_f", C.c_int32),
         ("d_hidden_f", C.c_int32), ("w_S", C.c_float), ("n_heads", C.c_int32), ("n_tasks", C.c_int32),
         ("n_charges", C.c_int32), ("n_spins", C.c_int32), ("robust", C.c_int32), ("huber_delta", C.c_float),
-        ("robust_tau", C.c_float),
+        ("robust_tau", C.c_float), ("route_feat", C.c_int32),
     ]
 
 
@@ -59,9 +59,9 @@ class ProfileEntry(C.Structure):
 class Debug(C.Structure):
     _fields_ = [("eid", C.c_void_p), ("gate", C.c_void_p), ("counts", C.c_void_p), ("pos", C.c_void_p),
                 ("basis", C.c_void_p), ("tri_e", C.c_void_p), ("tri_e2", C.c_void_p), ("eid3", C.c_void_p),
-                ("gate3", C.c_void_p), ("eidf", C.c_void_p), ("gatef", C.c_void_p)]
+                ("gate3", C.c_void_p), ("eidf", C.c_void_p), ("gatef", C.c_void_p), ("gap", C.c_void_p)]
 
-    KEYS = ("eid", "gate", "counts", "pos", "basis", "tri_e", "tri_e2", "eid3", "gate3", "eidf", "gatef")
+    KEYS = ("eid", "gate", "counts", "pos", "basis", "tri_e", "tri_e2", "eid3", "gate3", "eidf", "gatef", "gap")
 
 
 _LIB = None

@@ -45,7 +45,9 @@ class ModelConfig:
     composition each add a vector to the atom embedding.  robust = 1 replaces
     the mean-squared loss by the robust multi-task loss: per-structure Huber
     losses of width huber_delta, weighted by a soft threshold at robust_tau
-    standard deviations of the structure's task.
+    standard deviations of the structure's task.  route_feat = 1 adds a linear
+    router on the evolving edge token to every edge MoE: logits
+    (Pc[Z_i] + Pn[Z_j]) + X_e Wr + beta with Wr [d, E] per block.
     """
 
     d: int
@@ -77,6 +79,7 @@ class ModelConfig:
     robust: int = 0
     huber_delta: float = math.inf
     robust_tau: float = 2.0
+    route_feat: int = 0
 
     def weight_shapes(self):
         """Named weight tensors in blob order, with the fan-in used at init.
@@ -96,6 +99,10 @@ class ModelConfig:
                 (p + "Pc", (S, E), None),
                 (p + "Pn", (S, E), None),
                 (p + "beta", (E,), "zero"),
+            ]
+            if self.route_feat:
+                out += [(p + "Wr", (d, E), d)]
+            out += [
                 (p + "W1", (E, d, h), d),
                 (p + "W2", (E, h, d), h),
             ]
@@ -171,6 +178,8 @@ _M_TASK = dataclasses.replace(_M_SMALL, n_tasks=4, n_charges=5, n_spins=4)
 # robust multi-task loss (Huber width 1, down-weighting beyond 2 standard deviations per task)
 _M_ROBUST = dataclasses.replace(_M_TASK, robust=1, huber_delta=1.0, robust_tau=2.0)
 _M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
+# routing on the evolving edge tokens (species tables plus a linear layer on X_e)
+_M_FEAT = dataclasses.replace(_M_SMALL, route_feat=1)
 
 WORKLOADS = {
     "tiny": Workload("tiny", "cubic", 8, 32, 0.08, _M_TINY),
@@ -181,6 +190,7 @@ WORKLOADS = {
     "attention": Workload("attention", "ortho", 64, 64, 0.08, _M_ATTN),
     "multitask": Workload("multitask", "ortho", 64, 64, 0.08, _M_TASK),
     "robust": Workload("robust", "ortho", 64, 64, 0.08, _M_ROBUST),
+    "feature_routing": Workload("feature_routing", "ortho", 64, 64, 0.08, _M_FEAT),
     "shard": Workload("shard", "cubic", 256, 128, 0.1, _M_BIG),
     "irregular": Workload("irregular", "mixed", 512, 0, 0.1, _M_BIG, zipf_s=1.2),
 }

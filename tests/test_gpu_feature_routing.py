@@ -1,0 +1,173 @@
+"""Routing on the evolving edge tokens (route_feat: logits (Pc[Z_i] + Pn[Z_j]) +
+X_e Wr + beta, gates that move with X_e) on the GPU against the float64 oracle.
+
+The GPU decides on fp32 logits, the oracle on float64 ones, so a decision can
+differ only for a token whose k-th and (k+1)-th logits lie within fp32 rounding
+of each other.  Margin rule (both sides): a token is decided when its gap
+l_(k) - l_(k+1) exceeds 1e-5 (1 + max_x |l_x|) (about 100 times the fp32 error
+of a logit); every decided token must be routed identically (bit-exact expert
+ids), and the tokens inside the margin are counted and reported.  When every
+decision agrees (the test batches are such) the whole step is compared: energy 1e-5,
+loss 1e-5, forces, every weight gradient (Wr included) and dL/dR 1e-3 relative
+L2."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from helpers import TOL_E, TOL_F, TOL_LOSS, TOL_W, banner, energy_error, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+MARGIN = 1e-5
+FIXED = ("beta", "beta3", "betaf")
+
+
+def _batch(name):
+    from paper_2604_15821_amd.synth import _draw_weights, make_batch, subset
+    if name == "tiny-k2":
+        b = make_batch("tiny", n_struct=2)
+        m = dataclasses.replace(b.model, route_feat=1, top_k=2, n_experts=6)
+        return dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(3), m, 0.0))
+    if name == "feature-2":
+        return subset(make_batch("feature_routing"), range(2))
+    if name == "3b-atom-stress-1":
+        b = subset(make_batch("threebody"), range(1))
+        m = dataclasses.replace(b.model, d=64, d_hidden=128, n_experts=5, n_experts3=3, d_hidden3=64, n_rbf=8,
+                                n_blocks=2, atom_moe=True, n_experts_f=3, top_k_f=2, d_hidden_f=64,
+                                w_S=0.1 * 160.2177 ** 2, route_feat=1)
+        return dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(4), m, 0.0))
+    raise KeyError(name)
+
+
+def _run(b, pos_grad=True):
+    import torch
+    from paper_2604_15821_amd import janus
+    m = b.model
+    d = janus.upload(b)
+    ctx = janus.Context(m)
+    try:
+        nl = ctx.build_edges(d["pos"], d["cell"], d["offsets"])
+        Ne = nl.n_edges
+        dbg = {"eid": torch.empty(m.n_blocks * Ne * m.top_k, dtype=torch.int32, device="cuda:0"),
+               "gap": torch.empty(m.n_blocks * Ne, device="cuda:0")}
+        dR = torch.empty(b.n_atoms, 3, device="cuda:0") if pos_grad else None
+        loss, E, F, dW = ctx.step(d["pos"], d["cell"], d["species"], d["offsets"], nl, d["W"], d["E_ref"], d["F_ref"],
+                                  S_ref=d["S_ref"] if m.w_S else None, labels=d["labels"], debug=dbg, dLdR=dR)
+        torch.cuda.synchronize()
+        return {"loss": float(loss.cpu()[0]), "E": E.cpu().numpy(), "F": F.cpu().numpy(), "dW": dW.cpu().numpy(),
+                "dR": None if dR is None else dR.cpu().numpy(),
+                "eid": dbg["eid"].cpu().numpy().reshape(m.n_blocks, Ne, m.top_k),
+                "gap": dbg["gap"].cpu().numpy().reshape(m.n_blocks, Ne)}
+    finally:
+        ctx.close()
+
+
+def _logit_scale(b, aux, t):
+    """1 + max_x |l_x| of every token of block t, from the oracle's logits."""
+    from oracle.model import Params, _block_tokens, forward_energy
+    g, rt = aux["graph"], aux["routing"]
+    P = Params.from_weights(b.weights, b.model)
+    h = forward_energy(b.species, g, P, rt)[1]["h"]
+    _, X = _block_tokens(g, P, t, h[t], rt)
+    l = ((P.blk(t, "Pc")[b.species[g.ei]] + P.blk(t, "Pn")[b.species[g.ej]]) + X @ P.blk(t, "Wr")) \
+        + P.blk(t, "beta")[None, :]
+    return 1.0 + np.abs(l).max(1)
+
+
+def _compare_decisions(b, got, aux):
+    """Decided tokens routed identically.  Returns (tokens inside the margin, those of
+    them routed differently)."""
+    inside = differ = 0
+    for t, rt in enumerate(aux["routing"]):
+        scale = _logit_scale(b, aux, t)
+        decided = rt.gap > MARGIN * scale
+        inside += int((~decided).sum())
+        assert (got["eid"][t][decided] == rt.eid[decided]).all(), t
+        differ += int((got["eid"][t][~decided] != rt.eid[~decided]).any(1).sum())
+        # the GPU's own margins agree with the oracle's to fp32 rounding
+        g = got["gap"][t]
+        assert np.abs(g - rt.gap).max() <= 1e-5 * scale.max()
+    return inside, differ
+
+
+@pytest.mark.parametrize("name", ["tiny-k2", "feature-2", "3b-atom-stress-1"])
+def test_feature_routing_matches_oracle(name):
+    from oracle.model import Params, forward_energy, training_step
+    b = _batch(name)
+    banner("feature routing", name, b.n_struct, "structures", b.n_atoms, "atoms")
+    got = _run(b)
+    loss, E, F, grad, aux = training_step(b, return_aux=True, positions=True)
+    inside, differ = _compare_decisions(b, got, aux)
+    print(f"  tokens inside the margin: {inside}, routed differently: {differ}", flush=True)
+    # the step is compared whole only when every decision agrees (these batches were
+    # chosen so; a flip inside the margin would move one token to another expert)
+    assert differ == 0
+    _, cache = forward_energy(b.species, aux["graph"], Params.from_weights(b.weights, b.model), aux["routing"])
+    assert energy_error(got["E"], E, cache["eps"], b.offsets) <= TOL_E
+    assert abs(got["loss"] - loss) <= TOL_LOSS * abs(loss)
+    assert rel_l2(got["F"], F) <= TOL_F
+    assert rel_l2(got["dR"], aux["dLdR"]) <= TOL_F
+    from paper_2604_15821_amd import janus
+    W = janus.unpack(got["dW"], b.model)
+    worst = {}
+    for k, ref in grad.items():
+        if k.rsplit(".", 1)[-1] in FIXED:
+            assert not W[k].any()
+            continue
+        worst[k] = rel_l2(W[k], ref)
+    print("  dW rel L2 (router):", {k: f"{v:.1e}" for k, v in worst.items() if k.endswith("Wr")}, flush=True)
+    assert max(worst.values()) <= TOL_W, {k: v for k, v in worst.items() if v > TOL_W}
+
+
+def test_zero_router_weight_reproduces_the_species_router():
+    """Wr = 0 on the GPU: the same decisions and the same energies and forces as the
+    plain species-pair router (loss and gradients to rounding)."""
+    b = _batch("feature-2")
+    m = b.model
+    w0 = dict(b.weights)
+    for t in range(m.n_blocks):
+        w0[f"blocks.{t}.Wr"] = np.zeros_like(w0[f"blocks.{t}.Wr"])
+    bf = dataclasses.replace(b, weights=w0)
+    bs = dataclasses.replace(b, model=dataclasses.replace(m, route_feat=0),
+                             weights={n: v for n, v in w0.items() if not n.endswith(".Wr")})
+    banner("feature routing, Wr = 0")
+    f, s = _run(bf), _run(bs)
+    assert (f["eid"] == s["eid"]).all()
+    assert rel_l2(f["E"], s["E"]) <= 1e-6 and rel_l2(f["F"], s["F"]) <= 1e-5
+    assert abs(f["loss"] - s["loss"]) <= 1e-5 * abs(s["loss"])
+    from paper_2604_15821_amd import janus
+    Wf, Ws = janus.unpack(f["dW"], bf.model), janus.unpack(s["dW"], bs.model)
+    for k, v in Ws.items():
+        assert rel_l2(Wf[k], v) <= 1e-4, k
+
+
+def test_full_batch_decisions_and_sampled_structures():
+    """The 64-structure feature-routing batch: decided tokens of two sampled structures
+    against the oracle (a structure's tokens depend only on the structure), their
+    energies and forces when none of their tokens is inside the margin, and the
+    number of tokens inside the margin over the batch (reported)."""
+    from oracle.model import Params, forward_energy, training_step
+    from paper_2604_15821_amd.synth import make_batch, subset
+    b = make_batch("feature_routing")
+    banner("feature routing full batch", b.n_struct, "structures", b.n_atoms, "atoms")
+    got = _run(b, pos_grad=False)
+    gpu_inside = int((got["gap"] <= MARGIN * 10.0).sum())
+    print(f"  GPU tokens with gap below 1e-4 (absolute): {gpu_inside} of {got['gap'].size}", flush=True)
+    for s in (0, 37):
+        sb = subset(b, [s])
+        loss, E, F, grad, aux = training_step(sb, return_aux=True)
+        a0, a1 = b.offsets[s], b.offsets[s + 1]
+        # the structure's edges in the batch list: its atoms' edges are contiguous
+        from oracle.neighbors import neighbor_list
+        ei, ej, sh, rp = neighbor_list(b.pos, b.cell, b.offsets, b.model.r_cut)
+        e0, e1 = int(rp[a0]), int(rp[a1])
+        sub = {"eid": got["eid"][:, e0:e1], "gap": got["gap"][:, e0:e1]}
+        inside, differ = _compare_decisions(sb, sub, aux)
+        print(f"  structure {s}: {e1 - e0} edges, {inside} tokens inside the margin, {differ} routed differently",
+              flush=True)
+        if differ == 0:
+            _, cache = forward_energy(sb.species, aux["graph"], Params.from_weights(sb.weights, sb.model),
+                                      aux["routing"])
+            assert energy_error(got["E"][s:s + 1], E, cache["eps"], np.array([0, a1 - a0])) <= TOL_E
+            assert rel_l2(got["F"][a0:a1], F) <= TOL_F
