@@ -466,11 +466,11 @@ int janus_grouped_gemm_noalloc(const float* A, const float* B, float* C, const i
 /*
  * Row-chunk length that janus_grouped_wgrad and the expert weight gradients
  * of janus_step use for a contraction over M rows into P x Q blocks (host
- * function, no device work): a power of two from 128 to 16384.  The chunk
- * doubles while the grid would exceed 8192 workgroups of 128 x 128 output
- * tiles, or while the partial blocks (written and read back once by the
- * reduction) would exceed half of the operand bytes and the doubled chunk
- * still gives at least 2048 workgroups.  Returns the length, or
+ * function, no device work): a power of two from 128 to 2048.  It starts
+ * at 2048 and halves while the grid has fewer than 4096 workgroups of
+ * 128 x 128 output tiles and the partial blocks of the halved chunk (written
+ * and read back once by the reduction) stay within half of the operand
+ * bytes.  Returns the length, or
  * JANUS_EINVAL for M outside [0, 2^31) or non-positive P, Q.
  */
 int32_t janus_wgrad_chunk_rows(int64_t M, int32_t P, int32_t Q);

@@ -113,21 +113,22 @@ inline int max_rows_tiles(long long M, int groups) { return (int)((M + GBM - 1) 
 inline int max_wchunks(long long M, int groups, int kc) { return (int)((M + kc - 1) / kc) + groups; }
 
 // Chunk length of the weight-gradient contraction, a power of two from 128 to
-// 16384 rows.  Short chunks give the GPU several rounds of workgroups (a grid
-// of 1.4 rounds leaves most of the second round idle); long chunks keep the
-// partial tiles, written and read back by the reduction, small.  The chunk
-// doubles while the grid exceeds 8192 workgroups, or while the partials
-// exceed half of the operand bytes and the doubled chunk still gives at
-// least 2048 workgroups.
+// 2048 rows.  A 2048-row chunk is 128 LDS stages, the K loop of the K = 2048
+// expert products.  Longer chunks are slower at full size (512 x 2048 blocks
+// over 1.8 M rows: 16384-row chunks take 16 % longer, partial reduction
+// included): the tiles of one chunk share its operand rows through L2 only
+// while they run in step, and the last round of long workgroups leaves most
+// of the GPU idle.  Shorter chunks are taken while the grid has fewer than
+// 4096 workgroups (four rounds of the 1024 that are resident at once), as long
+// as the partial tiles of the halved chunk (written and read back once by the
+// reduction) stay within half of the operand bytes.
 inline int wgrad_chunk_rows(long long M, int P, int Q) {
   const long long tiles = (long long)((P + GBM - 1) / GBM) * ((Q + GBN - 1) / GBN);
   const double operand_bytes = 4.0 * (double)M * (P + Q);
   auto blocks = [&](long long kc) { return ((M + kc - 1) / kc) * tiles; };
   auto partial_bytes = [&](long long kc) { return 8.0 * (double)((M + kc - 1) / kc) * P * Q; };
-  long long kc = 128;
-  while (kc < 16384 && (blocks(kc) > 8192 ||
-                        (partial_bytes(kc) > 0.5 * operand_bytes && blocks(2 * kc) >= 2048)))
-    kc *= 2;
+  long long kc = 2048;
+  while (kc > 128 && blocks(kc) < 4096 && partial_bytes(kc / 2) <= 0.5 * operand_bytes) kc /= 2;
   return (int)kc;
 }
 

@@ -107,12 +107,14 @@ def test_binding_rejects_misfit_tensors_before_the_library():
 
 def test_wgrad_chunk_rule():
     """Chunk length of the weight-gradient contraction: 512 rows for the small batch's
-    expert products (337,996 slot rows, 128 x 512 blocks), 16384 at the full-size
-    expert shape (over a million rows, 512 x 2048 blocks), bounds 128 and 16384."""
+    expert products (337,996 slot rows, 128 x 512 blocks: 2644 workgroups, where 256
+    rows would double the partial tiles past half of the operand bytes), 2048 at the
+    full-size expert shape (over a million rows, 512 x 2048 blocks), bounds 128 and 2048."""
     assert janus.wgrad_chunk_rows(337_996, 128, 512) == 512
-    assert janus.wgrad_chunk_rows(1_200_000, 512, 2048) == 16384
-    assert janus.wgrad_chunk_rows(2_000_000, 2048, 512) == 16384
-    assert janus.wgrad_chunk_rows(100, 64, 64) == 128
+    assert janus.wgrad_chunk_rows(1_200_000, 512, 2048) == 2048
+    assert janus.wgrad_chunk_rows(2_000_000, 2048, 512) == 2048
+    assert janus.wgrad_chunk_rows(20_000, 128, 512) == 512
+    assert janus.wgrad_chunk_rows(100, 64, 64) == 2048
     assert janus.wgrad_chunk_rows(0, 64, 64) == 128
     with pytest.raises(janus.JanusError):
         janus.wgrad_chunk_rows(-1, 64, 64)

@@ -8,7 +8,7 @@ weight-gradient block are one more contraction each (sum over p of G_g[p, q]
 = sum over rows of (sum_p A[r, p]) B[r, q]), computed in float64 over every
 row.  The rows are grouped like the irregular batch's routing: one
 Zipf-heavy expert, a few empty ones, the rest log-uniform, with groups of
-1, 127, 128, 16383, 16384 and 16385 rows at the tile and chunk boundaries.
+1, 127, 128, 2047, 2048 and 2049 rows at the tile and chunk boundaries.
 Inputs are standard normal from a seeded device generator."""
 import numpy as np
 import pytest
@@ -21,7 +21,7 @@ D, H, GROUPS = 512, 2048, 64
 M_ROWS = 1_200_000
 EMPTY = (5, 17, 40)
 HEAVY = 23
-EDGE_SIZES = {2: 1, 3: 127, 4: 128, 7: 16383, 8: 16384, 9: 16385}
+EDGE_SIZES = {2: 1, 3: 127, 4: 128, 7: 2047, 8: 2048, 9: 2049}
 
 
 def _row_offsets(seed):
@@ -94,14 +94,14 @@ def test_grouped_gemm_full_size_sampled_rows(ctx, K, N, trans_b):
 
 
 def test_grouped_wgrad_full_size(ctx):
-    """G_g = A_g^T B_g with P = d, Q = h over 1.2 M rows: 16384-row chunks (the length the
+    """G_g = A_g^T B_g with P = d, Q = h over 1.2 M rows: 2048-row chunks (the length the
     expert weight gradients of the full-size workloads use), 4096 sampled entries and
     every column and row sum against float64, empty experts exactly zero."""
     import torch
     from paper_2604_15821_amd import janus
     P, Q = D, H
     kc = janus.wgrad_chunk_rows(M_ROWS, P, Q)
-    assert kc == 16384
+    assert kc == 2048
     banner("grouped_wgrad full size", M_ROWS, "rows", P, Q, "chunk", kc)
     off = _row_offsets(2)
     A = _randn((M_ROWS, P), 21)
