@@ -283,6 +283,24 @@ int janus_build_edges(janus_ctx* ctx, const float* pos, const float* cell, const
                       int8_t* shift, int32_t* rowptr, int32_t* rev, int64_t* n_edges, void* stream);
 
 /*
+ * How janus_build_edges finds the candidates of the test above (paper Sec.
+ * "MatRIS", graph generation; the list itself does not depend on it).
+ * All pairs: every centre tests every (j, n) of its structure, n_s * n_images
+ * candidates.  Cell list: the bounding box of a structure's atoms is cut into
+ * bins at least r_cut wide (at most n_s bins); for each image n a centre tests
+ * only the atoms of the bins that the ball of radius r_cut around X_i - s(n)
+ * reaches (widened far beyond fp32 rounding), with the same fp32 test, and
+ * sorts what it keeps into the canonical order, so both give the same list bit
+ * for bit.  mode 0 (default): the cell list for a structure with
+ * n_s * n_images >= 32768 whose box holds at least 27 bins, all pairs
+ * otherwise; 1: the cell list for every structure; 2: all pairs for every
+ * structure.  A centre with more than 512 neighbours is written by the
+ * all-pairs kernel in every mode.  Errors: JANUS_EINVAL (ctx null, mode
+ * outside 0..2).
+ */
+int janus_set_edge_builder(janus_ctx* ctx, int32_t mode);
+
+/*
  * One training step (paper Sec. "Runtime for multi-phase double-backward
  * execution": forward, force backward, double backward of the force loss,
  * final backward of the energy loss).

@@ -68,18 +68,23 @@ def neighbor_list(pos, cell, offsets, r_cut):
         shift = (imf[:, 0:1] * L[0][None, :] + imf[:, 1:2] * L[1][None, :]) + imf[:, 2:3] * L[2][None, :]
         shift = shift.astype(np.float32)
         p = pos32[a:b]
-        diff = p[None, :, :] - p[:, None, :]                      # [i, j, 3] = X_j - X_i
-        dvec = diff[:, :, None, :] + shift[None, None, :, :]      # [i, j, img, 3]
-        dx, dy, dz = dvec[..., 0], dvec[..., 1], dvec[..., 2]
-        r2 = (dx * dx + dy * dy) + dz * dz
-        keep = r2 < rc2
         zero = int(np.nonzero((img == 0).all(1))[0][0])
-        idx = np.arange(n)
-        keep[idx, idx, zero] = False
-        ii, jj, kk = np.nonzero(keep)                              # C order = canonical order
-        ei_l.append((ii + a).astype(np.int32))
-        ej_l.append((jj + a).astype(np.int32))
-        sh_l.append(img[kk].astype(np.int8))
+        # centres in blocks of rows (the [i, j, img] arrays of a large structure would not
+        # fit in memory); blocks in order keep the canonical order
+        blk = max(1, int(2e7 // (n * img.shape[0])))
+        for i0 in range(0, n, blk):
+            i1 = min(n, i0 + blk)
+            diff = p[None, :, :] - p[i0:i1, None, :]                  # [i, j, 3] = X_j - X_i
+            dvec = diff[:, :, None, :] + shift[None, None, :, :]      # [i, j, img, 3]
+            dx, dy, dz = dvec[..., 0], dvec[..., 1], dvec[..., 2]
+            r2 = (dx * dx + dy * dy) + dz * dz
+            keep = r2 < rc2
+            idx = np.arange(i0, i1)
+            keep[idx - i0, idx, zero] = False
+            ii, jj, kk = np.nonzero(keep)                              # C order = canonical order
+            ei_l.append((ii + a + i0).astype(np.int32))
+            ej_l.append((jj + a).astype(np.int32))
+            sh_l.append(img[kk].astype(np.int8))
     if ei_l:
         ei = np.concatenate(ei_l)
         ej = np.concatenate(ej_l)

@@ -44,6 +44,7 @@ struct janus_ctx {
   size_t host_plan_n = 0;
   long long ws_limit = 0;     // workspace cap in bytes (0: from free device memory)
   int last_chunks = 0;        // chunks used by the last janus_step
+  int edge_builder = 0;       // janus_set_edge_builder mode (0 auto, 1 cell lists, 2 all pairs)
   long long last_triplets = 0; // triplets of the last janus_step's batch
   // profiler: event pairs recorded around kernel families while enabled
   bool prof_on = false;

@@ -96,6 +96,7 @@ def _lib():
         lib.janus_wgrad_chunk_rows.restype = i32
         lib.janus_set_workspace_limit.argtypes = [vp, i64]
         lib.janus_set_concurrency.argtypes = [vp, C.c_int]
+        lib.janus_set_edge_builder.argtypes = [vp, C.c_int32]
         lib.janus_last_chunks.argtypes = [vp]
         lib.janus_last_triplets.argtypes = [vp]
         lib.janus_last_triplets.restype = i64
@@ -113,8 +114,8 @@ def exported_symbols():
              "janus_grouped_gemm", "janus_grouped_gemm_noalloc", "janus_grouped_wgrad", "janus_wgrad_chunk_rows",
              "janus_profile_enable",
              "janus_profile_read",
-             "janus_set_workspace_limit", "janus_set_concurrency", "janus_last_chunks", "janus_last_triplets",
-             "janus_strerror"]
+             "janus_set_workspace_limit", "janus_set_concurrency", "janus_set_edge_builder", "janus_last_chunks",
+             "janus_last_triplets", "janus_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
 
@@ -398,6 +399,12 @@ class Context:
         rc = _lib().janus_set_concurrency(self.h, int(bool(on)))
         if rc:
             raise JanusError(rc, "janus_set_concurrency")
+
+    def set_edge_builder(self, mode: int):
+        """Candidate search of build_edges: 0 automatic, 1 cell list everywhere, 2 all pairs everywhere."""
+        rc = _lib().janus_set_edge_builder(self.h, int(mode))
+        if rc:
+            raise JanusError(rc, "janus_set_edge_builder")
 
     def last_chunks(self) -> int:
         return int(_lib().janus_last_chunks(self.h))

@@ -130,3 +130,22 @@ def test_triplets_are_ordered_pairs_of_short_bonds():
     assert te.size == int((ns * (ns - 1)).sum())
     key = te.astype(np.int64) * ei.size + te2
     assert np.all(np.diff(key) > 0)
+
+
+def test_large_cell_against_periodic_kdtree():
+    """A 5,000-atom cubic cell (the centres go through the oracle in many row blocks):
+    the same pair set as a periodic k-d tree, one image per pair, canonical order."""
+    rng = np.random.default_rng(11)
+    L = np.float32(40.0)
+    pos = (rng.random((5000, 3)) * L).astype(np.float32)
+    rc = 6.0
+    ei, ej, sh, rp = _one(pos, [L] * 3, rc)
+    tree = cKDTree(pos.astype(np.float64), boxsize=float(L))
+    inner = tree.query_pairs(rc - 1e-4, output_type="ndarray")
+    outer = tree.query_pairs(rc + 1e-4, output_type="ndarray")
+    key = ei.astype(np.int64) * 5000 + ej
+    assert np.all(np.diff(key) > 0)                   # canonical (i, j) order, one image per pair
+    want_in = np.concatenate([inner[:, 0] * 5000 + inner[:, 1], inner[:, 1] * 5000 + inner[:, 0]])
+    want_out = np.concatenate([outer[:, 0] * 5000 + outer[:, 1], outer[:, 1] * 5000 + outer[:, 0]])
+    assert np.isin(want_in, key).all() and np.isin(key, want_out).all()
+    reverse_map(ei, ej, sh, 5000)
