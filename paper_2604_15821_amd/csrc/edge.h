@@ -101,6 +101,26 @@ __device__ __forceinline__ void filter_row(float b_lane, const float* sW, int nb
   }
 }
 
+// F = b W_b and F' = b' W_b together: each staged row of W_b is read once.
+template <int VPL>
+__device__ __forceinline__ void filter_rows2(float b_lane, float db_lane, const float* sW, int nb, int d, int l,
+                                             float (&F)[VPL], float (&Fp)[VPL]) {
+  zero_row<VPL>(F);
+  zero_row<VPL>(Fp);
+#pragma unroll 4
+  for (int n = 0; n < nb; ++n) {
+    const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(b_lane), n));
+    const float db = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(db_lane), n));
+    float w[VPL];
+    ld_row<VPL>(sW + n * d, l, w);
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      F[v] += b * w[v];
+      Fp[v] += db * w[v];
+    }
+  }
+}
+
 __device__ __forceinline__ void load_lds(float* s, const float* g, int n) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) s[i] = g[i];
   __syncthreads();
@@ -235,8 +255,7 @@ __global__ void edge_p2_kernel(const float* __restrict__ B, const float* __restr
     }
     ld_row<VPL>(h + (long long)ej[e] * d, l, hj);
     float F[VPL], Fp[VPL];
-    filter_row<VPL>(bl, sW, nb, d, l, F);
-    filter_row<VPL>(dbl, sW, nb, d, l, Fp);
+    filter_rows2<VPL>(bl, dbl, sW, nb, d, l, F, Fp);
     float fb[VPL], p[VPL];
     float s = 0.f;
 #pragma unroll
@@ -310,8 +329,7 @@ __global__ void edge_p3_kernel(const float* __restrict__ B, const float* __restr
     ld_row<VPL>(Xbar + e * d, l, xb);
     if (QX) ld_row<VPL>(QX + e * d, l, qx); else zero_row<VPL>(qx);
     float F[VPL], Fp[VPL];
-    filter_row<VPL>(bl, sW, nb, d, l, F);
-    filter_row<VPL>(dbl, sW, nb, d, l, Fp);
+    filter_rows2<VPL>(bl, dbl, sW, nb, d, l, F, Fp);
     float X[VPL], p[VPL];
     if (accP) ld_row<VPL>(P + e * d, l, p); else zero_row<VPL>(p);
 #pragma unroll
