@@ -185,6 +185,20 @@ def main():
             + (f"{e.get('tflops', 0):7.2f} TFLOP/s " if 'tflops' in e else "")
             + (f"{e.get('gbs', 0):8.1f} GB/s" if 'gbs' in e else ""))
 
+    if m.n_heads and "attention" in kernels:
+        # Algorithmic attention work: per ordered (query, key) pair of a neighbourhood and
+        # head, the distinct 32-long contractions of the four passes (forward q.k and p v;
+        # force backward q.k, p w k, p k and t q; tangent q.k, qh.k, q.kh, pz v, p v, p vh;
+        # final backward q.k, qh.k, q.kh, zb k, zhb kh, zb q, zhb qh): 19 of 2 * 32 flops.
+        deg = torch.diff(nl.rowptr.to(torch.int64)).double()
+        attn_flops = 19.0 * 64.0 * m.n_heads * m.n_blocks * float((deg * deg).sum())
+        e = kernels["attention"]
+        e["flops_per_step"] = attn_flops
+        e["tflops"] = attn_flops / (e["ms_per_step"] * 1e-3) / 1e12
+        e["mfma_frac"] = e["tflops"] * 1e12 / PEAK_FP32_MFMA
+        log(f"  attention     {e['tflops']:.2f} TFLOP/s of algorithmic contractions, "
+            f"{e['mfma_frac']:.3f} of the fp32 matrix peak")
+
     # roofline of the dominant family, from its events inside the timed region
     r = prof[dom]
     if r["flops"] > 0:

@@ -8,15 +8,13 @@
 //   p_el  = u_l exp(s_el) / sum_j u_j exp(s_ej)        (u = edge envelope)
 //   o_e   = sum_l p_el v_l
 //   osum_i = sum_e u_e o_e                              (then u_i = h_i + osum_i Wo)
-// One wave per atom loops over the heads.  Passes with one lane per query
-// keep the query row in registers and read every key row once per 64
-// queries (all lanes the same row); passes with one lane per key do the
-// transpose.  The rows a pass loops over are staged in LDS 32 at a time (each
-// wave its own region) and read back as broadcasts.  Per-query softmax
-// statistics (max of s, Z = sum u exp(s - max)) are stored by the forward and
-// reused by the three backward phases.  Per-edge scalars shared between the
-// passes of one head live in LDS, so a neighbourhood holds at most kAttnMaxN
-// edges (checked before the step).
+// Two kernel families run the four passes (forward, force backward, tangent,
+// final backward), both on the matrix cores: neighbourhoods of up to
+// kAttnMfmaN edges hold every 16-row tile of one (atom, head) in registers
+// (below); larger ones, up to kAttnMaxN edges, sweep the tiles (attn_tiled.h).
+// Per-query softmax statistics (max of s, Z = sum u exp(s - max)) are stored by
+// the forward and reused by the three backward passes.  The neighbourhood limit
+// is checked before the step.
 #pragma once
 
 #include "edge.h"
@@ -38,12 +36,6 @@ __device__ __forceinline__ void ld32(const float* __restrict__ p, float* x) {
   }
 }
 
-__device__ __forceinline__ void st32(float* __restrict__ p, const float* x) {
-#pragma unroll
-  for (int c = 0; c < kAttnDh; c += 4)
-    *reinterpret_cast<float4*>(p + c) = make_float4(x[c], x[c + 1], x[c + 2], x[c + 3]);
-}
-
 // Four independent partial sums: a single 32-long chain of dependent multiply-adds
 // leaves the vector unit waiting on each result.
 __device__ __forceinline__ float dot32(const float* a, const float* b) {
@@ -51,17 +43,6 @@ __device__ __forceinline__ float dot32(const float* a, const float* b) {
 #pragma unroll
   for (int c = 0; c < kAttnDh; ++c) s[c & 3] += a[c] * b[c];
   return (s[0] + s[1]) + (s[2] + s[3]);
-}
-
-// Row sums of a per-lane 32-vector over the wave, stored by lanes 0..31.
-__device__ __forceinline__ void wave_store32(float* __restrict__ out, const float* x, int l) {
-  float mine = 0.f;
-#pragma unroll
-  for (int c = 0; c < kAttnDh; ++c) {
-    const float s = wave_sum(x[c]);
-    mine = l == c ? s : mine;
-  }
-  if (l < kAttnDh) out[l] = mine;
 }
 
 constexpr float kAttnScale = 0.17677669529663687f;   // 1 / sqrt(32)
@@ -84,494 +65,11 @@ __global__ void attn_env_kernel(const float4* __restrict__ geo, long long Ne, fl
   ud[e] = (float)(du / rc);
 }
 
-constexpr int kAttnChunk = 32;   // key (or query) rows staged in LDS at a time
-
 // Orders one wave's LDS writes before its later reads (and reads before later overwrites).
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// Up to four 32-column blocks of the rows of one neighbourhood.
-struct AttnCols {
-  const float* p[4];
-};
-
-// Stage rows row0 .. row0+cnt-1 (cnt <= kAttnChunk) into LDS, NM column blocks per
-// row: lds[r * NM*32 + m*32 + c] = src.p[m][(row0 + r) * ld + c].  Two lanes per row.
-template <int NM>
-__device__ __forceinline__ void stage_rows(float* lds, const AttnCols& src, long long ld, long long row0, int cnt,
-                                           int l) {
-  const int r = l >> 1, hf = (l & 1) * 16;
-  if (r < cnt) {
-#pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      const float* g = src.p[m] + (row0 + r) * ld + hf;
-      float* s = lds + r * NM * kAttnDh + m * kAttnDh + hf;
-#pragma unroll
-      for (int c = 0; c < 16; c += 4) *reinterpret_cast<float4*>(s + c) = *reinterpret_cast<const float4*>(g + c);
-    }
-  }
-}
-
-// Phase 1: osum_i (one wave per atom; lanes = queries).  stats[(e*H + a)*2 + {0,1}] = (max s, Z).
-// Atoms with at most min_n edges are skipped (the matrix-core kernel takes them).
-__global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_kernel(
-    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu, int N, int d, int H,
-    float* __restrict__ stats, float* __restrict__ osum, int min_n) {
-  __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
-  __shared__ float s_u[kAttnWaves][kAttnChunk];
-  const int wv = threadIdx.x >> 6;
-  float* rows = s_rows[wv];
-  float* su = s_u[wv];
-  const long long ld = 3LL * d;
-  JANUS_WAVE_LOOP(i, N) {
-    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
-    if (n <= min_n) continue;
-    for (int a = 0; a < H; ++a) {
-      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
-      const AttnCols kvc{{QKV + ck, QKV + cv, nullptr, nullptr}};
-      float acc[kAttnDh];
-#pragma unroll
-      for (int c = 0; c < kAttnDh; ++c) acc[c] = 0.f;
-      for (int q0 = 0; q0 < n; q0 += 64) {
-        const bool valid = q0 + l < n;
-        const long long e = e0 + (valid ? q0 + l : 0);
-        float q[kAttnDh], o[kAttnDh];
-        ld32(QKV + e * ld + cq, q);
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) o[c] = 0.f;
-        float M = -INFINITY, Z = 0.f;
-        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
-          const int cnt = min(kAttnChunk, n - j0);
-          wave_sync();
-          stage_rows<2>(rows, kvc, ld, e0 + j0, cnt, l);
-          if (l < cnt) su[l] = uu[e0 + j0 + l];
-          wave_sync();
-          for (int jj = 0; jj < cnt; ++jj) {
-            float k[kAttnDh], v[kAttnDh];
-            ld32(rows + jj * 2 * kAttnDh, k);
-            const float s = dot32(q, k) * kAttnScale;
-            const float Mn = fmaxf(M, s);
-            const float f = __expf(M - Mn), g = su[jj] * __expf(s - Mn);
-            Z = Z * f + g;
-            ld32(rows + jj * 2 * kAttnDh + kAttnDh, v);
-#pragma unroll
-            for (int c = 0; c < kAttnDh; ++c) o[c] = o[c] * f + g * v[c];
-            M = Mn;
-          }
-        }
-        const float w = valid ? uu[e] / Z : 0.f;
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) acc[c] += w * o[c];
-        if (valid) {
-          stats[(e * H + a) * 2] = M;
-          stats[(e * H + a) * 2 + 1] = Z;
-        }
-      }
-      wave_store32(osum + (long long)i * d + cq, acc, l);
-    }
-  }
-}
-
-// Phase 2 (force backward), for ob_i = dE/du_i Wo^T (the adjoint of osum_i):
-//   adjoint of o_e = u_e ob,  w_l = ob . v_l,  cw_e = sum_l p_el w_l,
-//   zb_el = u_e p_el (w_l - cw_e)                    (adjoint of s_el and of log u_l)
-//   qb_e = sum_l zb_el k_l / sqrt(32),  kb_l = sum_e zb_el q_e / sqrt(32),
-//   vb_l = (sum_e u_e p_el) ob,
-//   dE/dr_e += u'(r_e) [cw_e (query weight) + sum_j u_j exp(s_je - M_j)/Z_j (w_e - cw_j) (key weight)]
-// summed over heads.  QKVb [Ne, 3d] gets (qb | kb | vb).  Atoms with at most min_n
-// edges are skipped (the matrix-core kernel takes them).
-__global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_kernel(
-    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu,
-    const float* __restrict__ ud, const float* __restrict__ stats, const float* __restrict__ ob, int N, int d, int H,
-    float* __restrict__ QKVb, float* __restrict__ rbar, int min_n) {
-  __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
-  __shared__ float s_sc[kAttnWaves][3][kAttnChunk];
-  __shared__ float s_cw[kAttnWaves][kAttnMaxN];
-  __shared__ float s_rb[kAttnWaves][kAttnMaxN];
-  const int wv = threadIdx.x >> 6;
-  float* rows = s_rows[wv];
-  float* s0 = s_sc[wv][0];
-  float* s1v = s_sc[wv][1];
-  float* s2 = s_sc[wv][2];
-  float* cw = s_cw[wv];
-  float* rb = s_rb[wv];
-  const long long ld = 3LL * d;
-  JANUS_WAVE_LOOP(i, N) {
-    if (rowptr[i + 1] - rowptr[i] <= min_n) continue;
-    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
-    wave_sync();
-    for (int j = l; j < n; j += 64) rb[j] = 0.f;
-    for (int a = 0; a < H; ++a) {
-      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
-      const AttnCols kvc{{QKV + ck, QKV + cv, nullptr, nullptr}};
-      const AttnCols qc{{QKV + cq, nullptr, nullptr, nullptr}};
-      float obr[kAttnDh];
-      ld32(ob + (long long)i * d + cq, obr);
-      // queries
-      for (int q0 = 0; q0 < n; q0 += 64) {
-        const bool valid = q0 + l < n;
-        const long long e = e0 + (valid ? q0 + l : 0);
-        float q[kAttnDh], A1[kAttnDh], A2[kAttnDh];
-        ld32(QKV + e * ld + cq, q);
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) A1[c] = A2[c] = 0.f;
-        const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
-        float sw = 0.f;
-        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
-          const int cnt = min(kAttnChunk, n - j0);
-          wave_sync();
-          stage_rows<2>(rows, kvc, ld, e0 + j0, cnt, l);
-          if (l < cnt) s0[l] = uu[e0 + j0 + l];
-          wave_sync();
-          for (int jj = 0; jj < cnt; ++jj) {
-            float k[kAttnDh], v[kAttnDh];
-            ld32(rows + jj * 2 * kAttnDh, k);
-            ld32(rows + jj * 2 * kAttnDh + kAttnDh, v);
-            const float p = s0[jj] * __expf(dot32(q, k) * kAttnScale - M) * iZ;
-            const float w = dot32(obr, v);
-            sw += p * w;
-#pragma unroll
-            for (int c = 0; c < kAttnDh; ++c) {
-              A1[c] += p * w * k[c];
-              A2[c] += p * k[c];
-            }
-          }
-        }
-        const float ue = uu[e] * kAttnScale;
-        float qb[kAttnDh];
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) qb[c] = ue * (A1[c] - sw * A2[c]);
-        if (valid) {
-          st32(QKVb + e * ld + cq, qb);
-          cw[q0 + l] = sw;
-          rb[q0 + l] += sw;
-        }
-      }
-      // keys
-      for (int k0 = 0; k0 < n; k0 += 64) {
-        const bool valid = k0 + l < n;
-        const long long key = e0 + (valid ? k0 + l : 0);
-        float k[kAttnDh], v[kAttnDh], kb[kAttnDh];
-        ld32(QKV + key * ld + ck, k);
-        ld32(QKV + key * ld + cv, v);
-        const float w = dot32(obr, v), uk = uu[key];
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) kb[c] = 0.f;
-        float Pu = 0.f, kl = 0.f;
-        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
-          const int cnt = min(kAttnChunk, n - j0);
-          wave_sync();
-          stage_rows<1>(rows, qc, ld, e0 + j0, cnt, l);
-          if (l < cnt) {
-            const long long e = e0 + j0 + l;
-            s0[l] = stats[(e * H + a) * 2];
-            s1v[l] = 1.f / stats[(e * H + a) * 2 + 1];
-            s2[l] = uu[e];
-          }
-          wave_sync();
-          for (int jj = 0; jj < cnt; ++jj) {
-            float q[kAttnDh];
-            ld32(rows + jj * kAttnDh, q);
-            const float E = __expf(dot32(q, k) * kAttnScale - s0[jj]) * s1v[jj];
-            const float ue = s2[jj];
-            const float t = ue * E * (w - cw[j0 + jj]);
-            kl += t;
-            Pu += ue * uk * E;
-#pragma unroll
-            for (int c = 0; c < kAttnDh; ++c) kb[c] += uk * t * q[c];
-          }
-        }
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) {
-          kb[c] *= kAttnScale;
-          v[c] = Pu * obr[c];
-        }
-        if (valid) {
-          st32(QKVb + key * ld + ck, kb);
-          st32(QKVb + key * ld + cv, v);
-          rb[k0 + l] += kl;
-        }
-      }
-    }
-    wave_sync();
-    for (int j = l; j < n; j += 64) rbar[e0 + j] += ud[e0 + j] * rb[j];
-  }
-}
-
-// Phase 3 (double backward as a tangent sweep): tangents qh, kh, vh of q, k, v and
-// uh = u' rt of the envelope.  Per query:
-//   pz_el = p_el sh_el + uh_l exp(s_el - M_e)/Z_e   (p times the tangent of s + log u)
-//   oh_e  = sum_l pz_el v_l - (sum_l pz_el) o_e + sum_l p_el vh_l
-//   osumh_i = sum_e (u_e oh_e + uh_e o_e).
-__global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_kernel(
-    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
-    const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
-    const float* __restrict__ stats, int N, int d, int H, float* __restrict__ osumh, int min_n) {
-  __shared__ float s_rows[kAttnWaves][kAttnChunk * 4 * kAttnDh];
-  __shared__ float s_sc[kAttnWaves][2][kAttnChunk];
-  const int wv = threadIdx.x >> 6;
-  float* rows = s_rows[wv];
-  float* su = s_sc[wv][0];
-  float* sh = s_sc[wv][1];
-  const long long ld = 3LL * d;
-  JANUS_WAVE_LOOP(i, N) {
-    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
-    if (n <= min_n) continue;
-    for (int a = 0; a < H; ++a) {
-      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
-      const AttnCols cols{{QKV + ck, QKVh + ck, QKV + cv, QKVh + cv}};
-      float acc[kAttnDh];
-#pragma unroll
-      for (int c = 0; c < kAttnDh; ++c) acc[c] = 0.f;
-      for (int q0 = 0; q0 < n; q0 += 64) {
-        const bool valid = q0 + l < n;
-        const long long e = e0 + (valid ? q0 + l : 0);
-        float q[kAttnDh], qh[kAttnDh], A1[kAttnDh], A2[kAttnDh], A3[kAttnDh];
-        ld32(QKV + e * ld + cq, q);
-        ld32(QKVh + e * ld + cq, qh);
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) A1[c] = A2[c] = A3[c] = 0.f;
-        const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
-        float s1 = 0.f;
-        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
-          const int cnt = min(kAttnChunk, n - j0);
-          wave_sync();
-          stage_rows<4>(rows, cols, ld, e0 + j0, cnt, l);
-          if (l < cnt) {
-            su[l] = uu[e0 + j0 + l];
-            sh[l] = ud[e0 + j0 + l] * rt[e0 + j0 + l];
-          }
-          wave_sync();
-          for (int jj = 0; jj < cnt; ++jj) {
-            const float* r = rows + jj * 4 * kAttnDh;
-            float x[kAttnDh];
-            ld32(r, x);                                   // k
-            float shv = dot32(qh, x);
-            const float E = __expf(dot32(q, x) * kAttnScale - M) * iZ;
-            ld32(r + kAttnDh, x);                         // kh
-            shv = (shv + dot32(q, x)) * kAttnScale;
-            const float p = su[jj] * E;
-            const float pz = p * shv + sh[jj] * E;
-            s1 += pz;
-            ld32(r + 2 * kAttnDh, x);                     // v
-#pragma unroll
-            for (int c = 0; c < kAttnDh; ++c) {
-              A1[c] += pz * x[c];
-              A2[c] += p * x[c];
-            }
-            ld32(r + 3 * kAttnDh, x);                     // vh
-#pragma unroll
-            for (int c = 0; c < kAttnDh; ++c) A3[c] += p * x[c];
-          }
-        }
-        const float ue = valid ? uu[e] : 0.f, uh = valid ? ud[e] * rt[e] : 0.f;
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) acc[c] += ue * (A1[c] - s1 * A2[c] + A3[c]) + uh * A2[c];
-      }
-      wave_store32(osumh + (long long)i * d + cq, acc, l);
-    }
-  }
-}
-
-// Phase 4 (final backward through the forward and its tangent): alpha_i = adjoint of
-// osum_i (times Wo^T), beta_i = adjoint of the tangent osumh_i (= the phase-2 ob_i).
-// Per query the adjoints of o_e and oh_e are u_e alpha + uh_e beta and u_e beta; with
-// a_l = alpha.v_l + beta.vh_l, b_l = beta.v_l and, per query, am = sum p a, bm = sum p b,
-// zm = sum pz, pbz = sum pz b, SP = u_e (am + pbz - 2 zm bm) + uh_e bm:
-//   zb_el  = u_e (p a_l + b_l (pz - p zm) - pz bm) + uh_e p b_l - p SP   (adjoint of s_el)
-//   zhb_el = u_e p (b_l - bm)                                            (adjoint of sh_el)
-//   qb_e = sum_l (zb k_l + zhb kh_l)/sqrt(32),  kb_l = sum_e (zb q_e + zhb qh_e)/sqrt(32),
-//   vb_l = alpha sum_e u_e p + beta sum_e (uh_e p + u_e (pz - p zm)).
-// QKVa [Ne, 3d] gets (qb | kb | vb), the adjoints of the primal q, k, v.  Atoms with at
-// most min_n edges are skipped (the matrix-core kernel takes them).
-__global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
-    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
-    const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
-    const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
-    int H, float* __restrict__ QKVa, int min_n) {
-  __shared__ float s_rows[kAttnWaves][kAttnChunk * 2 * kAttnDh];
-  __shared__ float s_ch[kAttnWaves][4][kAttnChunk];
-  __shared__ float s_sc[kAttnWaves][6][kAttnMaxN];
-  const int wv = threadIdx.x >> 6;
-  float* rows = s_rows[wv];
-  float* c0 = s_ch[wv][0];
-  float* c1 = s_ch[wv][1];
-  float* c2 = s_ch[wv][2];
-  float* c3 = s_ch[wv][3];
-  float* sa = s_sc[wv][0];
-  float* sb = s_sc[wv][1];
-  float* bm_ = s_sc[wv][2];
-  float* zm_ = s_sc[wv][3];
-  float* sp_ = s_sc[wv][4];
-  const long long ld = 3LL * d;
-  JANUS_WAVE_LOOP(i, N) {
-    if (rowptr[i + 1] - rowptr[i] <= min_n) continue;
-    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
-    for (int a = 0; a < H; ++a) {
-      const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
-      const AttnCols kc{{QKV + ck, QKVh + ck, nullptr, nullptr}};
-      const AttnCols qc{{QKV + cq, QKVh + cq, nullptr, nullptr}};
-      wave_sync();
-      // per key: a_l, b_l
-      for (int k0 = 0; k0 < n; k0 += 64) {
-        const bool valid = k0 + l < n;
-        const long long key = e0 + (valid ? k0 + l : 0);
-        float x[kAttnDh], v[kAttnDh];
-        ld32(QKV + key * ld + cv, v);
-        ld32(beta + (long long)i * d + cq, x);
-        const float bj = dot32(x, v);
-        float aj = 0.f;
-        ld32(QKVh + key * ld + cv, v);
-        aj += dot32(x, v);
-        ld32(QKV + key * ld + cv, v);
-        ld32(alpha + (long long)i * d + cq, x);
-        aj += dot32(x, v);
-        if (valid) {
-          sa[k0 + l] = aj;
-          sb[k0 + l] = bj;
-        }
-      }
-      // queries, sweep 1: per-query sums
-      for (int q0 = 0; q0 < n; q0 += 64) {
-        const bool valid = q0 + l < n;
-        const long long e = e0 + (valid ? q0 + l : 0);
-        float q[kAttnDh], qh[kAttnDh];
-        ld32(QKV + e * ld + cq, q);
-        ld32(QKVh + e * ld + cq, qh);
-        const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
-        float am = 0.f, bm = 0.f, zm = 0.f, pbz = 0.f;
-        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
-          const int cnt = min(kAttnChunk, n - j0);
-          wave_sync();
-          stage_rows<2>(rows, kc, ld, e0 + j0, cnt, l);
-          if (l < cnt) {
-            c0[l] = uu[e0 + j0 + l];
-            c1[l] = ud[e0 + j0 + l] * rt[e0 + j0 + l];
-          }
-          wave_sync();
-          for (int jj = 0; jj < cnt; ++jj) {
-            float x[kAttnDh];
-            ld32(rows + jj * 2 * kAttnDh, x);
-            float shv = dot32(qh, x);
-            const float E = __expf(dot32(q, x) * kAttnScale - M) * iZ;
-            ld32(rows + jj * 2 * kAttnDh + kAttnDh, x);
-            shv = (shv + dot32(q, x)) * kAttnScale;
-            const float p = c0[jj] * E;
-            const float pz = p * shv + c1[jj] * E;
-            const float aj = sa[j0 + jj], bj = sb[j0 + jj];
-            am += p * aj;
-            bm += p * bj;
-            zm += pz;
-            pbz += pz * bj;
-          }
-        }
-        const float ue = uu[e], uh = ud[e] * rt[e];
-        if (valid) {
-          bm_[q0 + l] = bm;
-          zm_[q0 + l] = zm;
-          sp_[q0 + l] = ue * (am + pbz - 2.f * zm * bm) + uh * bm;
-        }
-      }
-      // queries, sweep 2: qb
-      for (int q0 = 0; q0 < n; q0 += 64) {
-        const bool valid = q0 + l < n;
-        const int jq = valid ? q0 + l : 0;
-        const long long e = e0 + jq;
-        float q[kAttnDh], qh[kAttnDh], qb[kAttnDh];
-        ld32(QKV + e * ld + cq, q);
-        ld32(QKVh + e * ld + cq, qh);
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) qb[c] = 0.f;
-        const float M = stats[(e * H + a) * 2], iZ = 1.f / stats[(e * H + a) * 2 + 1];
-        const float ue = uu[e], uh = ud[e] * rt[e];
-        wave_sync();
-        const float bm = bm_[jq], zm = zm_[jq], SP = sp_[jq];
-        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
-          const int cnt = min(kAttnChunk, n - j0);
-          wave_sync();
-          stage_rows<2>(rows, kc, ld, e0 + j0, cnt, l);
-          if (l < cnt) {
-            c0[l] = uu[e0 + j0 + l];
-            c1[l] = ud[e0 + j0 + l] * rt[e0 + j0 + l];
-          }
-          wave_sync();
-          for (int jj = 0; jj < cnt; ++jj) {
-            float k[kAttnDh], kh[kAttnDh];
-            ld32(rows + jj * 2 * kAttnDh, k);
-            ld32(rows + jj * 2 * kAttnDh + kAttnDh, kh);
-            const float E = __expf(dot32(q, k) * kAttnScale - M) * iZ;
-            const float shv = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
-            const float p = c0[jj] * E;
-            const float pz = p * shv + c1[jj] * E;
-            const float aj = sa[j0 + jj], bj = sb[j0 + jj];
-            const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
-            const float zhb = ue * p * (bj - bm);
-#pragma unroll
-            for (int c = 0; c < kAttnDh; ++c) qb[c] += zb * k[c] + zhb * kh[c];
-          }
-        }
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) qb[c] *= kAttnScale;
-        if (valid) st32(QKVa + e * ld + cq, qb);
-      }
-      // keys: kb and vb
-      for (int k0 = 0; k0 < n; k0 += 64) {
-        const bool valid = k0 + l < n;
-        const int jk = valid ? k0 + l : 0;
-        const long long key = e0 + jk;
-        float k[kAttnDh], kh[kAttnDh], kb[kAttnDh];
-        ld32(QKV + key * ld + ck, k);
-        ld32(QKVh + key * ld + ck, kh);
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) kb[c] = 0.f;
-        const float uk = uu[key], uhk = ud[key] * rt[key], aj = sa[jk], bj = sb[jk];
-        float S1 = 0.f, S2 = 0.f;
-        for (int j0 = 0; j0 < n; j0 += kAttnChunk) {
-          const int cnt = min(kAttnChunk, n - j0);
-          wave_sync();
-          stage_rows<2>(rows, qc, ld, e0 + j0, cnt, l);
-          if (l < cnt) {
-            const long long e = e0 + j0 + l;
-            c0[l] = stats[(e * H + a) * 2];
-            c1[l] = 1.f / stats[(e * H + a) * 2 + 1];
-            c2[l] = uu[e];
-            c3[l] = ud[e] * rt[e];
-          }
-          wave_sync();
-          for (int jj = 0; jj < cnt; ++jj) {
-            float q[kAttnDh], qh[kAttnDh];
-            ld32(rows + jj * 2 * kAttnDh, q);
-            ld32(rows + jj * 2 * kAttnDh + kAttnDh, qh);
-            const float E = __expf(dot32(q, k) * kAttnScale - c0[jj]) * c1[jj];
-            const float shv = (dot32(qh, k) + dot32(q, kh)) * kAttnScale;
-            const float p = uk * E;
-            const float pz = p * shv + uhk * E;
-            const float ue = c2[jj], uh = c3[jj];
-            const int jq = j0 + jj;
-            const float bm = bm_[jq], zm = zm_[jq], SP = sp_[jq];
-            const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
-            const float zhb = ue * p * (bj - bm);
-            S1 += ue * p;
-            S2 += uh * p + ue * (pz - p * zm);
-#pragma unroll
-            for (int c = 0; c < kAttnDh; ++c) kb[c] += zb * q[c] + zhb * qh[c];
-          }
-        }
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) kb[c] *= kAttnScale;
-        if (valid) st32(QKVa + key * ld + ck, kb);
-        float al[kAttnDh], be[kAttnDh];
-        ld32(alpha + (long long)i * d + cq, al);
-        ld32(beta + (long long)i * d + cq, be);
-#pragma unroll
-        for (int c = 0; c < kAttnDh; ++c) kb[c] = S1 * al[c] + S2 * be[c];
-        if (valid) st32(QKVa + key * ld + cv, kb);
-      }
-    }
-  }
 }
 
 // ------------------------------------------------------------ matrix-core kernels
@@ -584,6 +82,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_kernel(
 // following product with the values, so no data moves between the two products.
 constexpr int kAttnMfmaN = 64;
 constexpr int kAttnTiles = kAttnMfmaN / 16;
+static_assert(kAttnMfmaN % 16 == 0 && kAttnTiles >= 1 && kAttnTiles <= 4, "the register-resident kernels exist for 1 to 4 tiles");
 
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
@@ -614,7 +113,7 @@ __device__ __forceinline__ float max_j4(float v) {
 
 // Phase 1 on matrix cores for the atoms whose neighbourhood spans NT 16-row tiles
 // (NT = 1 also takes the atoms without edges); one instance per NT keeps the register
-// use of the small neighbourhoods small.  Same outputs as attn_fwd_kernel.
+// use of the small neighbourhoods small.  Same outputs as attn_fwd_tiled_kernel.
 template <int NT>
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_mfma_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu, int N, int d, int H,
@@ -745,7 +244,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_mfma_kernel(
 
 // Phase 3 on matrix cores for the atoms whose neighbourhood spans NT 16-row tiles
 // (NT = 1 also takes the atoms without edges), one wave per (atom, head); same output as
-// attn_tan_kernel.  Transposed score tiles S = k.q and Sh = k.qh + kh.q give, per
+// attn_tan_tiled_kernel.  Transposed score tiles S = k.q and Sh = k.qh + kh.q give, per
 // (key, query), p = u_k E and pz = p sh + uh_k E with E = exp(s - M_q)/Z_q (stored
 // statistics); then oh = pz v - (sum pz) o + p vh with o = p v, three value products
 // chained on the probability tiles as in the forward.
@@ -879,7 +378,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_mfma_kernel(
 }
 
 // Phase 2 on matrix cores for the atoms whose neighbourhood spans NT 16-row tiles, one
-// wave per (atom, head); same outputs as attn_bwd_kernel except that the envelope
+// wave per (atom, head); same outputs as attn_bwd_tiled_kernel: the envelope
 // terms of dE/dr go to rbh [(e H + a)] (query term cw_e plus key term kl_e of head a)
 // and attn_rbar_kernel adds them to rbar.  Transposed score tiles (key x query) give
 // p, cw and zb = u_q p (w_k - cw_q) in the A-operand layout of qb = zb k; score tiles
@@ -1076,7 +575,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
 }
 
 // Phase 4 on matrix cores for the atoms whose neighbourhood spans NT 16-row tiles, one
-// wave per (atom, head); same output as attn_rev_kernel.  Per row t*16 + i16 (every j4
+// wave per (atom, head); same output as attn_rev_tiled_kernel.  Per row t*16 + i16 (every j4
 // lane): u, uh = u' rt, a = alpha.v + beta.vh and b = beta.v (8-column partial dots
 // added over the four lane groups), the query's softmax statistics.  Transposed tiles
 // (key x query) of s and sh give the per-query sums am, bm, zm, pbz and SP, then zb and

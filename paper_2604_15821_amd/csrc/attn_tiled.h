@@ -1,0 +1,493 @@
+// Matrix-core passes of the neighbourhood self-attention for neighbourhoods of
+// kAttnMfmaN + 1 .. kAttnMaxN edges (the register-resident kernels of attn.h take
+// the smaller ones).  One wave per (atom, head) walks 16-row tiles: a sweep over
+// query tiles (keys of each tile pair visited in turn) forms every per-query sum
+// and the products of the scores with key or value rows, a sweep over key tiles
+// (queries visited in turn) forms the per-key sums; scores are recomputed in each
+// sweep from the stored softmax statistics.  Score tiles come in two orientations
+// on v_mfma_f32_16x16x4_f32:
+//   keys x queries (score_kq): lane (i16, j4) holds the scores of query i16 with
+//     keys 4 j4 + r, r = 0..3 -- the A operand of a product contracted over keys;
+//   queries x keys (score_qk): lane (i16, j4) holds key i16 with queries 4 j4 + r
+//     -- the A operand of a product contracted over queries.
+// Per-row scalars that one sweep produces and the other reads live in LDS (per
+// wave, kAttnMaxN entries each).  The arithmetic per (query, key) pair is that of
+// the register-resident kernels (attn.h).
+#pragma once
+
+#include "attn.h"
+
+namespace janus {
+
+__device__ __forceinline__ f32x4v score_kq(const float (&kf)[8], const float (&qf)[8], f32x4v s) {
+#pragma unroll
+  for (int st = 0; st < 8; ++st) s = mfma16(kf[st], qf[st], s);
+  return s;
+}
+__device__ __forceinline__ f32x4v score_qk(const float (&qf)[8], const float (&kf)[8], f32x4v s) {
+#pragma unroll
+  for (int st = 0; st < 8; ++st) s = mfma16(qf[st], kf[st], s);
+  return s;
+}
+__device__ __forceinline__ f32x4v zero4() { return f32x4v{0.f, 0.f, 0.f, 0.f}; }
+
+// B operand of a product contracted over rows: columns c0 + i16 and c0 + 16 + i16 of
+// row `row` of the neighbourhood (clamped to it; the A operand is zero past n).
+__device__ __forceinline__ void cols2(const float* __restrict__ base, long long ld, int e0, int n, int row, int c0,
+                                      int i16, float& x0, float& x1) {
+  const float* p = base + (long long)(e0 + (row < n ? row : n - 1)) * ld + c0 + i16;
+  x0 = p[0];
+  x1 = p[16];
+}
+
+// Phase 1 for neighbourhoods of more than kAttnMfmaN edges.  Same outputs as
+// attn_fwd_mfma_kernel: stats (max s, Z) per (query, head) and osum_i.
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_tiled_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu, int N, int d, int H,
+    float* __restrict__ stats, float* __restrict__ osum) {
+  const long long ld = 3LL * d;
+  const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
+  JANUS_WAVE_LOOP(item, (long long)N * H) {
+    const int i = (int)(item / H), a = (int)(item - (long long)i * H);
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n <= kAttnMfmaN) continue;
+    const int nt = (n + 15) >> 4;
+    const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    float col0 = 0.f, col1 = 0.f;
+    for (int qt = 0; qt < nt; ++qt) {
+      float qf[8];
+      frag8(QKV, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qf);
+      // max over the keys of query qt*16 + i16
+      float M = -INFINITY;
+      for (int kt = 0; kt < nt; ++kt) {
+        float kf[8];
+        frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
+        const f32x4v S = score_kq(kf, qf, zero4());
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (kt * 16 + 4 * j4 + r < n) M = fmaxf(M, S[r] * kAttnScale);
+      }
+      M = max_j4(M);
+      // Z and the unnormalised o = sum_l u_l exp(s - M) v_l (rows: queries qt*16 + 4*j4 + r)
+      float Z = 0.f;
+      f32x4v O0 = zero4(), O1 = zero4();
+      for (int kt = 0; kt < nt; ++kt) {
+        float kf[8];
+        frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
+        const f32x4v S = score_kq(kf, qf, zero4());
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          const float u = key < n ? uu[e0 + key] : 0.f;
+          const float pv = u * __expf(S[r] * kAttnScale - M);
+          Z += pv;
+          float v0, v1;
+          cols2(QKV, ld, e0, n, key, cv, i16, v0, v1);
+          O0 = mfma16(pv, v0, O0);
+          O1 = mfma16(pv, v1, O1);
+        }
+      }
+      Z = sum_j4(Z);
+      const int qq = qt * 16 + i16;
+      if (j4 == 0 && qq < n) {
+        stats[((long long)(e0 + qq) * H + a) * 2] = M;
+        stats[((long long)(e0 + qq) * H + a) * 2 + 1] = Z;
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int q = qt * 16 + 4 * j4 + r;
+        const float Zq = __shfl(Z, 4 * j4 + r, 64);
+        const float w = q < n ? uu[e0 + q] / Zq : 0.f;
+        col0 += w * O0[r];
+        col1 += w * O1[r];
+      }
+    }
+    col0 = sum_j4(col0);
+    col1 = sum_j4(col1);
+    if (j4 == 0) {
+      osum[(long long)i * d + cq + i16] = col0;
+      osum[(long long)i * d + cq + 16 + i16] = col1;
+    }
+  }
+}
+
+// Phase 3 (tangent) for neighbourhoods of more than kAttnMfmaN edges; same output as
+// attn_tan_mfma_kernel: osumh_i = sum_q u_q oh_q + uh_q o_q,
+// oh_q = sum_l pz_ql v_l - (sum_l pz_ql) o_q + sum_l p_ql vh_l.
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_tiled_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
+    const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
+    const float* __restrict__ stats, int N, int d, int H, float* __restrict__ osumh) {
+  const long long ld = 3LL * d;
+  const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
+  JANUS_WAVE_LOOP(item, (long long)N * H) {
+    const int i = (int)(item / H), a = (int)(item - (long long)i * H);
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n <= kAttnMfmaN) continue;
+    const int nt = (n + 15) >> 4;
+    const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    float col0 = 0.f, col1 = 0.f;
+    for (int qt = 0; qt < nt; ++qt) {
+      float qf[8], qhf[8];
+      frag8(QKV, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qf);
+      frag8(QKVh, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qhf);
+      const int qq = qt * 16 + i16, qc = qq < n ? qq : n - 1;
+      const long long sq = ((long long)(e0 + qc) * H + a) * 2;
+      const float M = stats[sq], iZ = 1.f / stats[sq + 1];
+      f32x4v A1[2] = {zero4(), zero4()}, A2[2] = {zero4(), zero4()}, A3[2] = {zero4(), zero4()};
+      float s1 = 0.f;
+      for (int kt = 0; kt < nt; ++kt) {
+        float kf[8], khf[8];
+        frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
+        frag8(QKVh, ld, e0, n, kt * 16 + i16, ck + 8 * j4, khf);
+        const f32x4v S = score_kq(kf, qf, zero4());
+        const f32x4v Sh = score_kq(khf, qf, score_kq(kf, qhf, zero4()));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          const int kk = key < n ? key : n - 1;
+          const float uk = key < n ? uu[e0 + kk] : 0.f, uhk = key < n ? ud[e0 + kk] * rt[e0 + kk] : 0.f;
+          const float E = __expf(S[r] * kAttnScale - M) * iZ;
+          const float p = uk * E;
+          const float pz = p * Sh[r] * kAttnScale + uhk * E;
+          s1 += pz;
+          float v0, v1, w0, w1;
+          cols2(QKV, ld, e0, n, key, cv, i16, v0, v1);
+          cols2(QKVh, ld, e0, n, key, cv, i16, w0, w1);
+          A1[0] = mfma16(pz, v0, A1[0]);
+          A1[1] = mfma16(pz, v1, A1[1]);
+          A2[0] = mfma16(p, v0, A2[0]);
+          A2[1] = mfma16(p, v1, A2[1]);
+          A3[0] = mfma16(p, w0, A3[0]);
+          A3[1] = mfma16(p, w1, A3[1]);
+        }
+      }
+      s1 = sum_j4(s1);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int q = qt * 16 + 4 * j4 + r;
+        const float s1r = __shfl(s1, 4 * j4 + r, 64);
+        const float u = q < n ? uu[e0 + q] : 0.f, uh = q < n ? ud[e0 + q] * rt[e0 + q] : 0.f;
+        col0 += u * (A1[0][r] - s1r * A2[0][r] + A3[0][r]) + uh * A2[0][r];
+        col1 += u * (A1[1][r] - s1r * A2[1][r] + A3[1][r]) + uh * A2[1][r];
+      }
+    }
+    col0 = sum_j4(col0);
+    col1 = sum_j4(col1);
+    if (j4 == 0) {
+      osumh[(long long)i * d + cq + i16] = col0;
+      osumh[(long long)i * d + cq + 16 + i16] = col1;
+    }
+  }
+}
+
+// Phase 2 (force backward) for neighbourhoods of more than kAttnMfmaN edges; same
+// outputs as attn_bwd_mfma_kernel: QKVb rows (qb | kb | vb) and rbh[e H + a] = cw_e + kl_e.
+//   w_l = ob . v_l, cw_q = sum_l p_ql w_l, qb_q = u_q (sum_l p w_l k_l - cw_q sum_l p k_l) / sqrt(32),
+//   t_ql = u_q E_ql (w_l - cw_q), kl_l = sum_q t_ql, kb_l = u_l sum_q t_ql q_q / sqrt(32),
+//   vb_l = (sum_q u_q u_l E_ql) ob.
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_tiled_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu,
+    const float* __restrict__ stats, const float* __restrict__ ob, int N, int d, int H, float* __restrict__ QKVb,
+    float* __restrict__ rbh) {
+  __shared__ float s_w[kAttnWaves][kAttnMaxN];
+  __shared__ float s_cw[kAttnWaves][kAttnMaxN];
+  float* wk = s_w[threadIdx.x >> 6];
+  float* cw = s_cw[threadIdx.x >> 6];
+  const long long ld = 3LL * d;
+  const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
+  JANUS_WAVE_LOOP(item, (long long)N * H) {
+    const int i = (int)(item / H), a = (int)(item - (long long)i * H);
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n <= kAttnMfmaN) continue;
+    const int nt = (n + 15) >> 4;
+    const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    const float* obh = ob + (long long)i * d + cq;
+    wave_sync();
+    {
+      float obr[kAttnDh];
+      ld32(obh, obr);
+      for (int k = l; k < n; k += 64) {
+        float v[kAttnDh];
+        ld32(QKV + (long long)(e0 + k) * ld + cv, v);
+        wk[k] = dot32(obr, v);
+      }
+    }
+    wave_sync();
+    // queries: cw and qb
+    for (int qt = 0; qt < nt; ++qt) {
+      float qf[8];
+      frag8(QKV, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qf);
+      const int qq = qt * 16 + i16, qc = qq < n ? qq : n - 1;
+      const long long sq = ((long long)(e0 + qc) * H + a) * 2;
+      const float M = stats[sq], iZ = 1.f / stats[sq + 1];
+      f32x4v A1[2] = {zero4(), zero4()}, A2[2] = {zero4(), zero4()};
+      float sw = 0.f;
+      for (int kt = 0; kt < nt; ++kt) {
+        float kf[8];
+        frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
+        const f32x4v S = score_kq(kf, qf, zero4());
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          const int kk = key < n ? key : n - 1;
+          const float p = (key < n ? uu[e0 + kk] : 0.f) * __expf(S[r] * kAttnScale - M) * iZ;
+          const float pw = p * wk[kk];
+          sw += pw;
+          float k0, k1;
+          cols2(QKV, ld, e0, n, key, ck, i16, k0, k1);
+          A1[0] = mfma16(pw, k0, A1[0]);
+          A1[1] = mfma16(pw, k1, A1[1]);
+          A2[0] = mfma16(p, k0, A2[0]);
+          A2[1] = mfma16(p, k1, A2[1]);
+        }
+      }
+      sw = sum_j4(sw);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int q = qt * 16 + 4 * j4 + r;
+        const float swq = __shfl(sw, 4 * j4 + r, 64);
+        if (q < n) {
+          const float uq = uu[e0 + q] * kAttnScale;
+          float* out = QKVb + (long long)(e0 + q) * ld + cq + i16;
+          out[0] = uq * (A1[0][r] - swq * A2[0][r]);
+          out[16] = uq * (A1[1][r] - swq * A2[1][r]);
+        }
+      }
+      if (j4 == 0 && qq < n) cw[qq] = sw;
+    }
+    wave_sync();
+    // keys: kb, vb and the key term of rbh
+    const float ob0 = obh[i16], ob1 = obh[16 + i16];
+    for (int kt = 0; kt < nt; ++kt) {
+      float kf[8];
+      frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
+      const int kn = kt * 16 + i16, kc = kn < n ? kn : n - 1;
+      const float uk = kn < n ? uu[e0 + kc] : 0.f, w = wk[kc];
+      f32x4v KB[2] = {zero4(), zero4()};
+      float Pu = 0.f, kl = 0.f;
+      for (int qt = 0; qt < nt; ++qt) {
+        float qf[8];
+        frag8(QKV, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qf);
+        const f32x4v S = score_qk(qf, kf, zero4());
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = qt * 16 + 4 * j4 + r;
+          const int qc = q < n ? q : n - 1;
+          const long long sq = ((long long)(e0 + qc) * H + a) * 2;
+          const float uq = q < n ? uu[e0 + qc] : 0.f;
+          const float E = __expf(S[r] * kAttnScale - stats[sq]) / stats[sq + 1];
+          const float t = uq * E * (w - cw[qc]);
+          kl += t;
+          Pu += uq * uk * E;
+          float q0, q1;
+          cols2(QKV, ld, e0, n, q, cq, i16, q0, q1);
+          KB[0] = mfma16(uk * t, q0, KB[0]);
+          KB[1] = mfma16(uk * t, q1, KB[1]);
+        }
+      }
+      kl = sum_j4(kl);
+      Pu = sum_j4(Pu);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = kt * 16 + 4 * j4 + r;
+        const float Pur = __shfl(Pu, 4 * j4 + r, 64);
+        if (key < n) {
+          float* out = QKVb + (long long)(e0 + key) * ld;
+          out[ck + i16] = KB[0][r] * kAttnScale;
+          out[ck + 16 + i16] = KB[1][r] * kAttnScale;
+          out[cv + i16] = Pur * ob0;
+          out[cv + 16 + i16] = Pur * ob1;
+        }
+      }
+      if (j4 == 0 && kn < n) rbh[(long long)(e0 + kn) * H + a] = cw[kn] + kl;
+    }
+  }
+}
+
+// Phase 4 (final backward through the forward and its tangent) for neighbourhoods of
+// more than kAttnMfmaN edges; same output as attn_rev_mfma_kernel.  alpha_i is the
+// adjoint of osum_i, beta_i that of the tangent osumh_i; per query the adjoints of o_q
+// and oh_q are u_q alpha + uh_q beta and u_q beta.  With a_l = alpha.v_l + beta.vh_l,
+// b_l = beta.v_l and, per query, am = sum p a, bm = sum p b, zm = sum pz, pbz = sum pz b,
+// SP = u_q (am + pbz - 2 zm bm) + uh_q bm:
+//   zb_ql  = u_q (p a_l + b_l (pz - p zm) - pz bm) + uh_q p b_l - p SP   (adjoint of s_ql)
+//   zhb_ql = u_q p (b_l - bm)                                            (adjoint of sh_ql)
+//   qb_q = sum_l (zb k_l + zhb kh_l) / sqrt(32),  kb_l = sum_q (zb q_q + zhb qh_q) / sqrt(32),
+//   vb_l = alpha sum_q u_q p + beta sum_q (uh_q p + u_q (pz - p zm)).
+// QKVa rows get (qb | kb | vb), the adjoints of the primal q, k, v.
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
+    const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
+    const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
+    const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
+    int H, float* __restrict__ QKVa) {
+  __shared__ float s_sc[kAttnWaves][5][kAttnMaxN];
+  float* sa = s_sc[threadIdx.x >> 6][0];
+  float* sb = s_sc[threadIdx.x >> 6][1];
+  float* bm_ = s_sc[threadIdx.x >> 6][2];
+  float* zm_ = s_sc[threadIdx.x >> 6][3];
+  float* sp_ = s_sc[threadIdx.x >> 6][4];
+  const long long ld = 3LL * d;
+  const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
+  JANUS_WAVE_LOOP(item, (long long)N * H) {
+    const int i = (int)(item / H), a = (int)(item - (long long)i * H);
+    const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
+    if (n <= kAttnMfmaN) continue;
+    const int nt = (n + 15) >> 4;
+    const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    const float* al = alpha + (long long)i * d + cq;
+    const float* be = beta + (long long)i * d + cq;
+    wave_sync();
+    // per key: a_l = alpha . v_l + beta . vh_l, b_l = beta . v_l
+    {
+      float alr[kAttnDh], ber[kAttnDh];
+      ld32(al, alr);
+      ld32(be, ber);
+      for (int k = l; k < n; k += 64) {
+        float v[kAttnDh], vh[kAttnDh];
+        ld32(QKV + (long long)(e0 + k) * ld + cv, v);
+        ld32(QKVh + (long long)(e0 + k) * ld + cv, vh);
+        sa[k] = dot32(alr, v) + dot32(ber, vh);
+        sb[k] = dot32(ber, v);
+      }
+    }
+    wave_sync();
+    // queries: per-query sums, then qb
+    for (int qt = 0; qt < nt; ++qt) {
+      float qf[8], qhf[8];
+      frag8(QKV, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qf);
+      frag8(QKVh, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qhf);
+      const int qq = qt * 16 + i16, qc = qq < n ? qq : n - 1;
+      const long long sq = ((long long)(e0 + qc) * H + a) * 2;
+      const float M = stats[sq], iZ = 1.f / stats[sq + 1];
+      float am = 0.f, bm = 0.f, zm = 0.f, pbz = 0.f;
+      for (int kt = 0; kt < nt; ++kt) {
+        float kf[8], khf[8];
+        frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
+        frag8(QKVh, ld, e0, n, kt * 16 + i16, ck + 8 * j4, khf);
+        const f32x4v S = score_kq(kf, qf, zero4());
+        const f32x4v Sh = score_kq(khf, qf, score_kq(kf, qhf, zero4()));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          const int kk = key < n ? key : n - 1;
+          const float uk = key < n ? uu[e0 + kk] : 0.f, uhk = key < n ? ud[e0 + kk] * rt[e0 + kk] : 0.f;
+          const float E = __expf(S[r] * kAttnScale - M) * iZ;
+          const float p = uk * E;
+          const float pz = p * Sh[r] * kAttnScale + uhk * E;
+          const float aj = sa[kk], bj = sb[kk];
+          am += p * aj;
+          bm += p * bj;
+          zm += pz;
+          pbz += pz * bj;
+        }
+      }
+      am = sum_j4(am);
+      bm = sum_j4(bm);
+      zm = sum_j4(zm);
+      pbz = sum_j4(pbz);
+      const float ue = uu[e0 + qc], uh = ud[e0 + qc] * rt[e0 + qc];
+      const float SP = ue * (am + pbz - 2.f * zm * bm) + uh * bm;
+      if (j4 == 0 && qq < n) {
+        bm_[qq] = bm;
+        zm_[qq] = zm;
+        sp_[qq] = SP;
+      }
+      f32x4v QB[2] = {zero4(), zero4()};
+      for (int kt = 0; kt < nt; ++kt) {
+        float kf[8], khf[8];
+        frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
+        frag8(QKVh, ld, e0, n, kt * 16 + i16, ck + 8 * j4, khf);
+        const f32x4v S = score_kq(kf, qf, zero4());
+        const f32x4v Sh = score_kq(khf, qf, score_kq(kf, qhf, zero4()));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt * 16 + 4 * j4 + r;
+          const int kk = key < n ? key : n - 1;
+          const float uk = key < n ? uu[e0 + kk] : 0.f, uhk = key < n ? ud[e0 + kk] * rt[e0 + kk] : 0.f;
+          const float E = __expf(S[r] * kAttnScale - M) * iZ;
+          const float p = uk * E;
+          const float pz = p * Sh[r] * kAttnScale + uhk * E;
+          const float aj = sa[kk], bj = sb[kk];
+          const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
+          const float zhb = ue * p * (bj - bm);
+          float k0, k1, h0, h1;
+          cols2(QKV, ld, e0, n, key, ck, i16, k0, k1);
+          cols2(QKVh, ld, e0, n, key, ck, i16, h0, h1);
+          QB[0] = mfma16(zb, k0, QB[0]);
+          QB[1] = mfma16(zb, k1, QB[1]);
+          QB[0] = mfma16(zhb, h0, QB[0]);
+          QB[1] = mfma16(zhb, h1, QB[1]);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int q = qt * 16 + 4 * j4 + r;
+        if (q < n) {
+          float* out = QKVa + (long long)(e0 + q) * ld + cq + i16;
+          out[0] = QB[0][r] * kAttnScale;
+          out[16] = QB[1][r] * kAttnScale;
+        }
+      }
+    }
+    wave_sync();
+    // keys: kb and vb
+    const float al0 = al[i16], al1 = al[16 + i16], be0 = be[i16], be1 = be[16 + i16];
+    for (int kt = 0; kt < nt; ++kt) {
+      float kf[8], khf[8];
+      frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
+      frag8(QKVh, ld, e0, n, kt * 16 + i16, ck + 8 * j4, khf);
+      const int kn = kt * 16 + i16, kc = kn < n ? kn : n - 1;
+      const float uk = kn < n ? uu[e0 + kc] : 0.f, uhk = kn < n ? ud[e0 + kc] * rt[e0 + kc] : 0.f;
+      const float aj = sa[kc], bj = sb[kc];
+      f32x4v KB[2] = {zero4(), zero4()};
+      float S1 = 0.f, S2 = 0.f;
+      for (int qt = 0; qt < nt; ++qt) {
+        float qf[8], qhf[8];
+        frag8(QKV, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qf);
+        frag8(QKVh, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qhf);
+        const f32x4v S = score_qk(qf, kf, zero4());
+        const f32x4v Sh = score_qk(qf, khf, score_qk(qhf, kf, zero4()));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = qt * 16 + 4 * j4 + r;
+          const int qc = q < n ? q : n - 1;
+          const long long sq = ((long long)(e0 + qc) * H + a) * 2;
+          // padded query rows take no part (p = pz = 0)
+          const float E = q < n ? __expf(S[r] * kAttnScale - stats[sq]) / stats[sq + 1] : 0.f;
+          const float p = uk * E;
+          const float pz = p * Sh[r] * kAttnScale + uhk * E;
+          const float ue = q < n ? uu[e0 + qc] : 0.f, uh = q < n ? ud[e0 + qc] * rt[e0 + qc] : 0.f;
+          const float bm = bm_[qc], zm = zm_[qc], SP = sp_[qc];
+          const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
+          const float zhb = ue * p * (bj - bm);
+          S1 += ue * p;
+          S2 += uh * p + ue * (pz - p * zm);
+          float q0, q1, h0, h1;
+          cols2(QKV, ld, e0, n, q, cq, i16, q0, q1);
+          cols2(QKVh, ld, e0, n, q, cq, i16, h0, h1);
+          KB[0] = mfma16(zb, q0, KB[0]);
+          KB[1] = mfma16(zb, q1, KB[1]);
+          KB[0] = mfma16(zhb, h0, KB[0]);
+          KB[1] = mfma16(zhb, h1, KB[1]);
+        }
+      }
+      S1 = sum_j4(S1);
+      S2 = sum_j4(S2);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = kt * 16 + 4 * j4 + r;
+        const float S1r = __shfl(S1, 4 * j4 + r, 64), S2r = __shfl(S2, 4 * j4 + r, 64);
+        if (key < n) {
+          float* out = QKVa + (long long)(e0 + key) * ld;
+          out[ck + i16] = KB[0][r] * kAttnScale;
+          out[ck + 16 + i16] = KB[1][r] * kAttnScale;
+          out[cv + i16] = S1r * al0 + S2r * be0;
+          out[cv + 16 + i16] = S1r * al1 + S2r * be1;
+        }
+      }
+    }
+  }
+}
+
+}  // namespace janus

@@ -503,17 +503,20 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_ATTN, 0, by_attn);
-        // neighbourhoods up to kAttnMfmaN edges on matrix cores, larger ones on the vector units
+        // neighbourhoods up to kAttnMfmaN edges on register-resident tiles, larger ones on tiled sweeps
         hipLaunchKernelGGL(attn_fwd_mfma_kernel<1>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
                            (const float*)p.eu, N, d, H, STt(t), OSt(t));
-        hipLaunchKernelGGL(attn_fwd_mfma_kernel<2>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+        if (2 <= kAttnTiles)
+          hipLaunchKernelGGL(attn_fwd_mfma_kernel<2>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
                            (const float*)p.eu, N, d, H, STt(t), OSt(t));
-        hipLaunchKernelGGL(attn_fwd_mfma_kernel<3>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+        if (3 <= kAttnTiles)
+          hipLaunchKernelGGL(attn_fwd_mfma_kernel<3>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
                            (const float*)p.eu, N, d, H, STt(t), OSt(t));
-        hipLaunchKernelGGL(attn_fwd_mfma_kernel<4>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+        if (4 <= kAttnTiles)
+          hipLaunchKernelGGL(attn_fwd_mfma_kernel<4>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
                            (const float*)p.eu, N, d, H, STt(t), OSt(t));
-        hipLaunchKernelGGL(attn_fwd_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)p.eu, N,
-                           d, H, STt(t), OSt(t), kAttnMfmaN);
+        hipLaunchKernelGGL(attn_fwd_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
       }
       {
         PROF(PROF_DENSE_GEMM, f_dense, 0);
@@ -614,20 +617,19 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_ATTN, 0, by_attn);
-        // neighbourhoods up to kAttnMfmaN edges on matrix cores, larger ones on the vector units
+        // neighbourhoods up to kAttnMfmaN edges on register-resident tiles, larger ones on tiled sweeps
 #define JANUS_BWD_MFMA(NTV)                                                                                    \
   hipLaunchKernelGGL(attn_bwd_mfma_kernel<NTV>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),                \
                      (const float*)p.eu, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t), p.rbh)
         JANUS_BWD_MFMA(1);
-        JANUS_BWD_MFMA(2);
-        JANUS_BWD_MFMA(3);
-        JANUS_BWD_MFMA(4);
+        if (2 <= kAttnTiles) JANUS_BWD_MFMA(2);
+        if (3 <= kAttnTiles) JANUS_BWD_MFMA(3);
+        if (4 <= kAttnTiles) JANUS_BWD_MFMA(4);
 #undef JANUS_BWD_MFMA
+        hipLaunchKernelGGL(attn_bwd_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                           (const float*)p.eu, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t), p.rbh);
         hipLaunchKernelGGL(attn_rbar_kernel, gN, b256, 0, st, rowptr, (const float*)p.eud, (const float*)p.rbh, N, H,
-                           kAttnMfmaN, p.rbar);
-        hipLaunchKernelGGL(attn_bwd_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)p.eu,
-                           (const float*)p.eud, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t),
-                           p.rbar, kAttnMfmaN);
+                           kAttnMaxN, p.rbar);
       }
       {
         PROF(PROF_DENSE_GEMM, f_qkv, 0);
@@ -901,13 +903,13 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                      (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,         \
                      (const float*)STt(t), N, d, H, p.osh)
         JANUS_TAN_MFMA(1);
-        JANUS_TAN_MFMA(2);
-        JANUS_TAN_MFMA(3);
-        JANUS_TAN_MFMA(4);
+        if (2 <= kAttnTiles) JANUS_TAN_MFMA(2);
+        if (3 <= kAttnTiles) JANUS_TAN_MFMA(3);
+        if (4 <= kAttnTiles) JANUS_TAN_MFMA(4);
 #undef JANUS_TAN_MFMA
-        hipLaunchKernelGGL(attn_tan_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)QKVht(t),
-                           (const float*)p.eu, (const float*)p.eud, (const float*)p.rt, (const float*)STt(t), N, d, H,
-                           p.osh, kAttnMfmaN);
+        hipLaunchKernelGGL(attn_tan_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                           (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,
+                           (const float*)STt(t), N, d, H, p.osh);
       }
       {
         PROF(PROF_DENSE_GEMM, 2 * f_dense, 0);
@@ -1059,19 +1061,19 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_ATTN, 0, by_attn);
-        // neighbourhoods up to kAttnMfmaN edges on matrix cores, larger ones on the vector units
+        // neighbourhoods up to kAttnMfmaN edges on register-resident tiles, larger ones on tiled sweeps
 #define JANUS_REV_MFMA(NTV)                                                                                    \
   hipLaunchKernelGGL(attn_rev_mfma_kernel<NTV>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),                \
                      (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,         \
                      (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa)
         JANUS_REV_MFMA(1);
-        JANUS_REV_MFMA(2);
-        JANUS_REV_MFMA(3);
-        JANUS_REV_MFMA(4);
+        if (2 <= kAttnTiles) JANUS_REV_MFMA(2);
+        if (3 <= kAttnTiles) JANUS_REV_MFMA(3);
+        if (4 <= kAttnTiles) JANUS_REV_MFMA(4);
 #undef JANUS_REV_MFMA
-        hipLaunchKernelGGL(attn_rev_kernel, gN, b256, 0, st, rowptr, (const float*)QKVt(t), (const float*)QKVht(t),
-                           (const float*)p.eu, (const float*)p.eud, (const float*)p.rt, (const float*)STt(t),
-                           (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa, kAttnMfmaN);
+        hipLaunchKernelGGL(attn_rev_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                           (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,
+                           (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa);
       }
       {
         PROF(PROF_DENSE_GEMM, 3 * f_qkv, 0);

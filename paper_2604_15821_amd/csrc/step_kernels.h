@@ -17,6 +17,7 @@
 #include "route.h"
 #include "tri.h"
 #include "attn.h"
+#include "attn_tiled.h"
 #include "feat_route.h"
 
 namespace janus {

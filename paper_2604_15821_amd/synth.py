@@ -178,6 +178,8 @@ _M_TASK = dataclasses.replace(_M_SMALL, n_tasks=4, n_charges=5, n_spins=4)
 # robust multi-task loss (Huber width 1, down-weighting beyond 2 standard deviations per task)
 _M_ROBUST = dataclasses.replace(_M_TASK, robust=1, huber_delta=1.0, robust_tau=2.0)
 _M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
+# attention over large neighbourhoods (about 110 edges per atom at 0.12 atoms / A^3), d = 256, 8 heads
+_M_ATTN_WIDE = dataclasses.replace(_M_SMALL, d=256, n_heads=8, r_cut=6.0)
 # routing on the evolving edge tokens (species tables plus a linear layer on X_e)
 _M_FEAT = dataclasses.replace(_M_SMALL, route_feat=1)
 
@@ -188,6 +190,7 @@ WORKLOADS = {
     "atom_moe": Workload("atom_moe", "ortho", 64, 64, 0.08, _M_ATOM),
     "stress": Workload("stress", "ortho", 64, 64, 0.08, _M_STRESS),
     "attention": Workload("attention", "ortho", 64, 64, 0.08, _M_ATTN),
+    "attention_wide": Workload("attention_wide", "ortho", 64, 64, 0.12, _M_ATTN_WIDE),
     "multitask": Workload("multitask", "ortho", 64, 64, 0.08, _M_TASK),
     "robust": Workload("robust", "ortho", 64, 64, 0.08, _M_ROBUST),
     "feature_routing": Workload("feature_routing", "ortho", 64, 64, 0.08, _M_FEAT),

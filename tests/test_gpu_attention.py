@@ -1,9 +1,11 @@
 """Neighbourhood self-attention on the GPU against the float64 oracle: energy
 1e-5, loss 1e-5, forces and every weight gradient (Wqkv and Wo included)
 1e-3 relative L2, run-to-run determinism; with the other optional terms
-(bond angles, feature-update MoE, stress) and on a crystal/molecule mix
-(neighbourhoods of 3 to 99 edges, so more than one 64-query sweep); a
-neighbourhood larger than the kernels hold is rejected before anything runs."""
+(bond angles, feature-update MoE, stress), on a crystal/molecule mix
+(neighbourhoods of 3 to 99 edges) and on a d = 512, 16-head model with
+neighbourhoods of about 60 to 140 edges (both the register-resident kernels and
+the tiled sweeps); a neighbourhood larger than the kernels hold is rejected
+before anything runs."""
 import dataclasses
 
 import numpy as np
@@ -41,6 +43,19 @@ def _batch(name):
         b = subset(b, picks)
         m = dataclasses.replace(b.model, d=64, d_hidden=128, n_experts=6, n_rbf=8, n_blocks=2, n_heads=2)
         return dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(5), m, 1.2))
+    if name == "wide-attn":
+        # d = 512 with 16 heads of 32; a 40-atom cell at 0.08 / A^3 (neighbourhoods of about
+        # 60 to 80 edges, both sides of the 64-edge split) and one at 0.145 / A^3 (about 125
+        # to 140 edges, nine 16-row tiles)
+        from paper_2604_15821_amd.synth import Batch, Workload
+        m = dataclasses.replace(make_batch("tiny").model, d=512, d_hidden=128, n_experts=4, top_k=2, n_rbf=8,
+                                n_blocks=2, r_cut=6.0, n_heads=16)
+        b1 = make_batch(Workload("wide-a", "ortho", 1, 40, 0.08, m))
+        b2 = make_batch(Workload("wide-b", "ortho", 1, 40, 0.145, m))
+        cat = lambda f: np.concatenate([getattr(b1, f), getattr(b2, f)], 0)
+        off = np.array([0, b1.n_atoms, b1.n_atoms + b2.n_atoms], np.int32)
+        return Batch(pos=cat("pos"), cell=cat("cell"), species=cat("species"), offsets=off, E_ref=cat("E_ref"),
+                     F_ref=cat("F_ref"), weights=b1.weights, model=m, name="wide-attn")
     raise KeyError(name)
 
 
@@ -62,7 +77,7 @@ def _run(b, reps=1):
     return outs
 
 
-CASES = ["tiny-2heads", "attention-4", "3b-atom-stress-attn", "mixed-attn"]
+CASES = ["tiny-2heads", "attention-4", "3b-atom-stress-attn", "mixed-attn", "wide-attn"]
 
 
 @pytest.fixture(scope="module", params=CASES)
@@ -126,7 +141,7 @@ def test_edges_beyond_the_cutoff_contribute_nothing():
     """A caller's list may hold edges at or past r_cut (a Verlet list with a skin): their
     basis and attention envelope are zero, so the step equals the oracle's on its own list
     of edges shorter than r_cut.  The list here is built with a 0.8 A skin (about 1.5x the
-    edges, so some neighbourhoods pass 64 edges and use the vector-unit kernels)."""
+    edges, so some neighbourhoods pass 64 edges and use the tiled sweeps)."""
     import torch
     from oracle.model import Params, forward_energy, training_step
     from paper_2604_15821_amd import janus
