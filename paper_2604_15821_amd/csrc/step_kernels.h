@@ -813,9 +813,14 @@ __global__ void species_rows_gather_kernel(const float* __restrict__ A, const in
   h[q] = A[(long long)species[i] * d + (q - i * d)];
 }
 
+// Workgroups of four waves over `items`, at most 2048: one full set of resident
+// workgroups (256 CUs x 8 of them at 8 waves per SIMD), each wave then looping over
+// its items.  The edge kernels stage W_b in LDS once per workgroup; with 8192
+// workgroups they ran 13-16 % longer on the small batch (4096 and 1024: 5 % and
+// 30 % longer than 2048).
 inline dim3 wave_grid(long long items) {
   long long blocks = (items + 3) / 4;
-  if (blocks > 8192) blocks = 8192;
+  if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
   return dim3((unsigned)blocks);
 }
