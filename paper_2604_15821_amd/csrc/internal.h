@@ -133,6 +133,20 @@ inline int wgrad_chunk_rows(long long M, int P, int Q) {
   return (int)kc;
 }
 
+// Chunk length of the skinny weight gradient (wgrad_skinny_kernel, one workgroup
+// per chunk): a multiple of the rows it stages per pass, long enough that all chunks
+// fit in one set of resident workgroups (CUs x workgroups per CU at the kernel
+// instance's register and LDS use, queried from the runtime), so no second, mostly
+// idle round runs.  On the small batch (169 k rows, 16 x 128) 192-row chunks take 3
+// passes in one round, against 128-row chunks' 2 passes in 1.3 rounds.
+int skinny_chunk_rows(long long M, int P, int Q);
+
+// Output rows per thread of the skinny weight gradient for P x Q (its template argument).
+inline int skinny_rows_per_thread(int P, int Q) {
+  const int groups = 256 / (Q / 4);
+  return (P + groups - 1) / groups;
+}
+
 void launch_wgrad_reduce(hipStream_t st, const float* partial, const int* chunk_first, int groups,
                          long long PQ, float* G, int accumulate);
 
@@ -165,8 +179,7 @@ inline void launch_wgrad_skinny(hipStream_t st, const float* A, const float* s, 
                                 float* partial, float* G, int accumulate) {
   if (max_chunks > 0) {
     // output rows per thread: P over the 256 / (Q / 4) thread groups
-    const int groups = 256 / (Q / 4);
-    const int no = (P + groups - 1) / groups;
+    const int no = skinny_rows_per_thread(P, Q);
     const dim3 grid(max_chunks), blk(256);
     const size_t lds = sizeof(float) * skinny_rows(Q) * (P + Q);
     if (no <= 1)

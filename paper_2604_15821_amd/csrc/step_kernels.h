@@ -1068,7 +1068,7 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
   p.mtN = max_rows_tiles(N, 1);
   p.kcN = wgrad_chunk_rows(N, d, d);
   p.mcN = max_wchunks(N, 1, p.kcN);
-  p.kcE = wgrad_chunk_rows(Ne, p.nb, d);
+  p.kcE = skinny_chunk_rows(Ne, p.nb, d);
   p.mcE = max_wchunks(Ne, 1, p.kcE);
   p.nch = sort_chunks(M);
   p.ntile = (h + GBN - 1) / GBN;
