@@ -52,7 +52,7 @@ def family(kernel_name: str) -> str:
         return "edge"
     if re.search(r"(combine_fwd|gather_atom|scatter_rev|combine_p3)_kernel", n):
         return "atom"
-    if re.search(r"attn_(fwd|bwd|tan|rev)(_mfma)?_kernel", n):
+    if re.search(r"attn_(fwd|bwd|tan|rev)(_mfma|_tiled)?_kernel", n):
         return "attention"
     if "elementwise_kernel" in n or "vectorized" in n:
         return "copy"
@@ -180,12 +180,18 @@ def algorithmic_bytes(bench_line: dict):
     """Average algorithmic HBM bytes (read, write) per expert-GEMM launch of a block of the
     edge MoE, from the workload of a bench.py line: the 8 products G1-G6, G9, G10 over
     M = k Ne slot rows with [M, h] and [M, d] fp32 tensors (operands, stored
-    pre-activations and adjoints read once, outputs written once).  None with triplets
-    (their products join the family)."""
+    pre-activations and adjoints read once, outputs written once; M per launch, that is
+    per workspace chunk).  None with triplets (their products join the family)."""
     if not bench_line or bench_line.get("triplets", 0):
         return None
     c = bench_line["config"]
-    M = c["top_k"] * c["edges"]
+    # slot rows of one launch: a batch split over workspace chunks runs every product once
+    # per chunk, so M comes from the roofline's per-launch work (2 M d h) when it is there
+    roof = bench_line.get("roofline") or {}
+    if roof.get("kernel") == "expert_gemm" and roof.get("flops_per_launch"):
+        M = roof["flops_per_launch"] / (2.0 * c["d"] * c["d_hidden"])
+    else:
+        M = c["top_k"] * c["edges"]
     H, D = 4.0 * M * c["d_hidden"], 4.0 * M * c["d"]
     reads = D + H + (D + H) + H + (D + 2 * H) + H + (D + 2 * H) + H      # G1 G2 G3 G4 G5 G6 G9 G10
     writes = H + D + 2 * H + D + 2 * H + D + H + D
