@@ -40,11 +40,32 @@ __device__ __forceinline__ void cols2(const float* __restrict__ base, long long 
   x1 = p[16];
 }
 
+// Per-row scalars of one neighbourhood staged in the wave's LDS region before its
+// sweeps, so the tile loops read them from LDS: the envelope u, its tangent
+// uh = u' rt (when uh is wanted) and the softmax statistics M, 1/Z of head a (when
+// stats is given).  Call between wave_sync()s.
+__device__ __forceinline__ void stage_rows(int e0, int n, int H, int a, const float* __restrict__ uu,
+                                           const float* __restrict__ ud, const float* __restrict__ rt,
+                                           const float* __restrict__ stats, float* su, float* suh, float* sM,
+                                           float* siZ, int l) {
+  for (int k = l; k < n; k += 64) {
+    su[k] = uu[e0 + k];
+    if (suh) suh[k] = ud[e0 + k] * rt[e0 + k];
+    if (sM) {
+      const long long sq = ((long long)(e0 + k) * H + a) * 2;
+      sM[k] = stats[sq];
+      siZ[k] = 1.f / stats[sq + 1];
+    }
+  }
+}
+
 // Phase 1 for neighbourhoods of more than kAttnMfmaN edges.  Same outputs as
 // attn_fwd_mfma_kernel: stats (max s, Z) per (query, head) and osum_i.
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_tiled_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu, int N, int d, int H,
     float* __restrict__ stats, float* __restrict__ osum) {
+  __shared__ float s_u[kAttnWaves][kAttnMaxN];
+  float* su = s_u[threadIdx.x >> 6];
   const long long ld = 3LL * d;
   const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
   JANUS_WAVE_LOOP(item, (long long)N * H) {
@@ -53,6 +74,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_tiled_kernel(
     if (n <= kAttnMfmaN) continue;
     const int nt = (n + 15) >> 4;
     const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    wave_sync();
+    stage_rows(e0, n, H, a, uu, nullptr, nullptr, nullptr, su, nullptr, nullptr, nullptr, l);
+    wave_sync();
     float col0 = 0.f, col1 = 0.f;
     for (int qt = 0; qt < nt; ++qt) {
       float qf[8];
@@ -78,7 +102,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_tiled_kernel(
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int key = kt * 16 + 4 * j4 + r;
-          const float u = key < n ? uu[e0 + key] : 0.f;
+          const float u = key < n ? su[key] : 0.f;
           const float pv = u * __expf(S[r] * kAttnScale - M);
           Z += pv;
           float v0, v1;
@@ -97,7 +121,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_fwd_tiled_kernel(
       for (int r = 0; r < 4; ++r) {
         const int q = qt * 16 + 4 * j4 + r;
         const float Zq = __shfl(Z, 4 * j4 + r, 64);
-        const float w = q < n ? uu[e0 + q] / Zq : 0.f;
+        const float w = q < n ? su[q] / Zq : 0.f;
         col0 += w * O0[r];
         col1 += w * O1[r];
       }
@@ -118,6 +142,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_tiled_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
     const float* __restrict__ stats, int N, int d, int H, float* __restrict__ osumh) {
+  __shared__ float s_u[kAttnWaves][2][kAttnMaxN];
+  float* su = s_u[threadIdx.x >> 6][0];
+  float* suh = s_u[threadIdx.x >> 6][1];
   const long long ld = 3LL * d;
   const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
   JANUS_WAVE_LOOP(item, (long long)N * H) {
@@ -126,6 +153,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_tiled_kernel(
     if (n <= kAttnMfmaN) continue;
     const int nt = (n + 15) >> 4;
     const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
+    wave_sync();
+    stage_rows(e0, n, H, a, uu, ud, rt, nullptr, su, suh, nullptr, nullptr, l);
+    wave_sync();
     float col0 = 0.f, col1 = 0.f;
     for (int qt = 0; qt < nt; ++qt) {
       float qf[8], qhf[8];
@@ -146,7 +176,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_tiled_kernel(
         for (int r = 0; r < 4; ++r) {
           const int key = kt * 16 + 4 * j4 + r;
           const int kk = key < n ? key : n - 1;
-          const float uk = key < n ? uu[e0 + kk] : 0.f, uhk = key < n ? ud[e0 + kk] * rt[e0 + kk] : 0.f;
+          const float uk = key < n ? su[kk] : 0.f, uhk = key < n ? suh[kk] : 0.f;
           const float E = __expf(S[r] * kAttnScale - M) * iZ;
           const float p = uk * E;
           const float pz = p * Sh[r] * kAttnScale + uhk * E;
@@ -167,7 +197,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_tiled_kernel(
       for (int r = 0; r < 4; ++r) {
         const int q = qt * 16 + 4 * j4 + r;
         const float s1r = __shfl(s1, 4 * j4 + r, 64);
-        const float u = q < n ? uu[e0 + q] : 0.f, uh = q < n ? ud[e0 + q] * rt[e0 + q] : 0.f;
+        const float u = q < n ? su[q] : 0.f, uh = q < n ? suh[q] : 0.f;
         col0 += u * (A1[0][r] - s1r * A2[0][r] + A3[0][r]) + uh * A2[0][r];
         col1 += u * (A1[1][r] - s1r * A2[1][r] + A3[1][r]) + uh * A2[1][r];
       }
@@ -190,10 +220,12 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_tiled_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu,
     const float* __restrict__ stats, const float* __restrict__ ob, int N, int d, int H, float* __restrict__ QKVb,
     float* __restrict__ rbh) {
-  __shared__ float s_w[kAttnWaves][kAttnMaxN];
-  __shared__ float s_cw[kAttnWaves][kAttnMaxN];
-  float* wk = s_w[threadIdx.x >> 6];
-  float* cw = s_cw[threadIdx.x >> 6];
+  __shared__ float s_sc[kAttnWaves][5][kAttnMaxN];
+  float* wk = s_sc[threadIdx.x >> 6][0];
+  float* cw = s_sc[threadIdx.x >> 6][1];
+  float* su = s_sc[threadIdx.x >> 6][2];
+  float* sM = s_sc[threadIdx.x >> 6][3];
+  float* siZ = s_sc[threadIdx.x >> 6][4];
   const long long ld = 3LL * d;
   const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
   JANUS_WAVE_LOOP(item, (long long)N * H) {
@@ -204,6 +236,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_tiled_kernel(
     const int cq = a * kAttnDh, ck = d + a * kAttnDh, cv = 2 * d + a * kAttnDh;
     const float* obh = ob + (long long)i * d + cq;
     wave_sync();
+    stage_rows(e0, n, H, a, uu, nullptr, nullptr, stats, su, nullptr, sM, siZ, l);
     {
       float obr[kAttnDh];
       ld32(obh, obr);
@@ -231,7 +264,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_tiled_kernel(
         for (int r = 0; r < 4; ++r) {
           const int key = kt * 16 + 4 * j4 + r;
           const int kk = key < n ? key : n - 1;
-          const float p = (key < n ? uu[e0 + kk] : 0.f) * __expf(S[r] * kAttnScale - M) * iZ;
+          const float p = (key < n ? su[kk] : 0.f) * __expf(S[r] * kAttnScale - M) * iZ;
           const float pw = p * wk[kk];
           sw += pw;
           float k0, k1;
@@ -248,7 +281,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_tiled_kernel(
         const int q = qt * 16 + 4 * j4 + r;
         const float swq = __shfl(sw, 4 * j4 + r, 64);
         if (q < n) {
-          const float uq = uu[e0 + q] * kAttnScale;
+          const float uq = su[q] * kAttnScale;
           float* out = QKVb + (long long)(e0 + q) * ld + cq + i16;
           out[0] = uq * (A1[0][r] - swq * A2[0][r]);
           out[16] = uq * (A1[1][r] - swq * A2[1][r]);
@@ -263,7 +296,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_tiled_kernel(
       float kf[8];
       frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
       const int kn = kt * 16 + i16, kc = kn < n ? kn : n - 1;
-      const float uk = kn < n ? uu[e0 + kc] : 0.f, w = wk[kc];
+      const float uk = kn < n ? su[kc] : 0.f, w = wk[kc];
       f32x4v KB[2] = {zero4(), zero4()};
       float Pu = 0.f, kl = 0.f;
       for (int qt = 0; qt < nt; ++qt) {
@@ -274,9 +307,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_tiled_kernel(
         for (int r = 0; r < 4; ++r) {
           const int q = qt * 16 + 4 * j4 + r;
           const int qc = q < n ? q : n - 1;
-          const long long sq = ((long long)(e0 + qc) * H + a) * 2;
-          const float uq = q < n ? uu[e0 + qc] : 0.f;
-          const float E = __expf(S[r] * kAttnScale - stats[sq]) / stats[sq + 1];
+          const float uq = q < n ? su[qc] : 0.f;
+          const float E = __expf(S[r] * kAttnScale - sM[qc]) * siZ[qc];
           const float t = uq * E * (w - cw[qc]);
           kl += t;
           Pu += uq * uk * E;
@@ -321,7 +353,11 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
     const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
     int H, float* __restrict__ QKVa) {
-  __shared__ float s_sc[kAttnWaves][5][kAttnMaxN];
+  __shared__ float s_sc[kAttnWaves][9][kAttnMaxN];
+  float* su = s_sc[threadIdx.x >> 6][5];
+  float* suh = s_sc[threadIdx.x >> 6][6];
+  float* sM = s_sc[threadIdx.x >> 6][7];
+  float* siZ = s_sc[threadIdx.x >> 6][8];
   float* sa = s_sc[threadIdx.x >> 6][0];
   float* sb = s_sc[threadIdx.x >> 6][1];
   float* bm_ = s_sc[threadIdx.x >> 6][2];
@@ -338,6 +374,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
     const float* al = alpha + (long long)i * d + cq;
     const float* be = beta + (long long)i * d + cq;
     wave_sync();
+    stage_rows(e0, n, H, a, uu, ud, rt, stats, su, suh, sM, siZ, l);
     // per key: a_l = alpha . v_l + beta . vh_l, b_l = beta . v_l
     {
       float alr[kAttnDh], ber[kAttnDh];
@@ -371,7 +408,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
         for (int r = 0; r < 4; ++r) {
           const int key = kt * 16 + 4 * j4 + r;
           const int kk = key < n ? key : n - 1;
-          const float uk = key < n ? uu[e0 + kk] : 0.f, uhk = key < n ? ud[e0 + kk] * rt[e0 + kk] : 0.f;
+          const float uk = key < n ? su[kk] : 0.f, uhk = key < n ? suh[kk] : 0.f;
           const float E = __expf(S[r] * kAttnScale - M) * iZ;
           const float p = uk * E;
           const float pz = p * Sh[r] * kAttnScale + uhk * E;
@@ -386,7 +423,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
       bm = sum_j4(bm);
       zm = sum_j4(zm);
       pbz = sum_j4(pbz);
-      const float ue = uu[e0 + qc], uh = ud[e0 + qc] * rt[e0 + qc];
+      const float ue = su[qc], uh = suh[qc];
       const float SP = ue * (am + pbz - 2.f * zm * bm) + uh * bm;
       if (j4 == 0 && qq < n) {
         bm_[qq] = bm;
@@ -404,7 +441,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
         for (int r = 0; r < 4; ++r) {
           const int key = kt * 16 + 4 * j4 + r;
           const int kk = key < n ? key : n - 1;
-          const float uk = key < n ? uu[e0 + kk] : 0.f, uhk = key < n ? ud[e0 + kk] * rt[e0 + kk] : 0.f;
+          const float uk = key < n ? su[kk] : 0.f, uhk = key < n ? suh[kk] : 0.f;
           const float E = __expf(S[r] * kAttnScale - M) * iZ;
           const float p = uk * E;
           const float pz = p * Sh[r] * kAttnScale + uhk * E;
@@ -438,7 +475,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
       frag8(QKV, ld, e0, n, kt * 16 + i16, ck + 8 * j4, kf);
       frag8(QKVh, ld, e0, n, kt * 16 + i16, ck + 8 * j4, khf);
       const int kn = kt * 16 + i16, kc = kn < n ? kn : n - 1;
-      const float uk = kn < n ? uu[e0 + kc] : 0.f, uhk = kn < n ? ud[e0 + kc] * rt[e0 + kc] : 0.f;
+      const float uk = kn < n ? su[kc] : 0.f, uhk = kn < n ? suh[kc] : 0.f;
       const float aj = sa[kc], bj = sb[kc];
       f32x4v KB[2] = {zero4(), zero4()};
       float S1 = 0.f, S2 = 0.f;
@@ -452,12 +489,11 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
         for (int r = 0; r < 4; ++r) {
           const int q = qt * 16 + 4 * j4 + r;
           const int qc = q < n ? q : n - 1;
-          const long long sq = ((long long)(e0 + qc) * H + a) * 2;
           // padded query rows take no part (p = pz = 0)
-          const float E = q < n ? __expf(S[r] * kAttnScale - stats[sq]) / stats[sq + 1] : 0.f;
+          const float E = q < n ? __expf(S[r] * kAttnScale - sM[qc]) * siZ[qc] : 0.f;
           const float p = uk * E;
           const float pz = p * Sh[r] * kAttnScale + uhk * E;
-          const float ue = q < n ? uu[e0 + qc] : 0.f, uh = q < n ? ud[e0 + qc] * rt[e0 + qc] : 0.f;
+          const float ue = q < n ? su[qc] : 0.f, uh = q < n ? suh[qc] : 0.f;
           const float bm = bm_[qc], zm = zm_[qc], SP = sp_[qc];
           const float zb = ue * (p * aj + bj * (pz - p * zm) - pz * bm) + uh * p * bj - p * SP;
           const float zhb = ue * p * (bj - bm);
