@@ -384,10 +384,12 @@ int janus_step_ex(janus_ctx* ctx, const float* pos, const float* cell, const int
  * per edge, the loss adjoint of the edge length through the radial basis and
  * its derivative (the second radial derivative of the basis enters here),
  * and one per-atom pass adds the adjoints of the edge directions and of the
- * stress term.  Supported for the radial model with any of the stress term,
- * the robust loss, the feature-update MoE and the task-aware embedding; with
- * the bond-angle term or attention, dLdR != NULL returns JANUS_EUNSUPPORTED.
- * Every other argument, output and error is as for janus_step_ex.
+ * stress term.  With bond angles the triplet features' first and second
+ * partial derivatives enter per triplet; with attention the final backward
+ * also collects the adjoint of each edge's log envelope, and the envelope's
+ * first and second derivatives carry it and the force backward's envelope
+ * term to dL/dr_e.  Every option of janus_config is supported.  Every other
+ * argument, output and error is as for janus_step_ex.
  */
 int janus_step_pos(janus_ctx* ctx, const float* pos, const float* cell, const int32_t* species,
                    const int32_t* offsets, int32_t n_atoms, int32_t n_struct, const janus_edges* nl,

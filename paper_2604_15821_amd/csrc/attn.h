@@ -582,12 +582,15 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
 // zhb in the A-operand layout of qb = zb k + zhb kh; tiles the other way round
 // (query x key) give zb, zhb in the layout of kb = zb^T q + zhb^T qh and the per-key
 // sums S1 = sum u_q p, S2 = sum uh_q p + u_q (pz - p zm) of vb = S1 alpha + S2 beta.
-template <int NT>
+template <int NT, bool POS>
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
     const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
-    int H, float* __restrict__ QKVa) {
+    int H, float* __restrict__ QKVa, float* __restrict__ rlh) {
+  // multiply-adds are fused only inside one expression: the instance that also forms the
+  // log-u adjoints (POS) then computes every other output with the same roundings
+#pragma clang fp contract(on)
   const long long ld = 3LL * d;
   const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
   JANUS_WAVE_LOOP(item, (long long)N * H) {
@@ -630,6 +633,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
       izrow[t] = 1.f / stats[sq + 1];
     }
     float bmq[NT], zmq[NT], spq[NT];   // per query t*16 + i16
+    float lq[POS ? NT : 1];            // with POS: query part of the adjoint of log u, row t*16 + i16
     // ---- transposed tiles: lane holds (key kt*16 + 4 j4 + r, query qt*16 + i16)
     {
       f32x4v S[NT][NT], Sh[NT][NT];
@@ -694,6 +698,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
         pbz = sum_j4(pbz);
         const float ue = urow[qt], uh = uhrow[qt];
         const float SP = ue * (am + pbz - 2.f * zm * bm) + uh * bm;
+        if (POS) lq[qt] = ue * (am + pbz - zm * bm) + uh * bm;   // query part of the log-u adjoint
         bmq[qt] = bm;
         zmq[qt] = zm;
         spq[qt] = SP;
@@ -778,9 +783,12 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
 #pragma unroll
             for (int kt = 0; kt < NT; ++kt) Sh[qt][kt] = mfma16(qf[qt][st], hf[kt][st], Sh[qt][kt]);
       }
-      float s1[NT], s2[NT];
+      float s1[NT], s2[NT], lk[POS ? NT : 1];
 #pragma unroll
-      for (int kt = 0; kt < NT; ++kt) s1[kt] = s2[kt] = 0.f;
+      for (int kt = 0; kt < NT; ++kt) {
+        s1[kt] = s2[kt] = 0.f;
+        if (POS) lk[kt] = 0.f;
+      }
 #pragma unroll
       for (int qt = 0; qt < NT; ++qt)
 #pragma unroll
@@ -799,8 +807,18 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
             s2[kt] += uh * p + ue * (pz - p * zm);
             S[qt][kt][r] = ue * (p * ak + bk * (pz - p * zm) - pz * bm) + uh * p * bk - p * SP;
             Sh[qt][kt][r] = ue * p * (bk - bm);
+            if (POS) lk[kt] += S[qt][kt][r];   // key part: sum over queries of the score adjoint
           }
         }
+      if (POS) {
+        // adjoint of log u_e, edge e = row t*16 + i16: key part + query part
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const float v = sum_j4(lk[t]) + lq[t];
+          const int row = t * 16 + i16;
+          if (j4 == 0 && row < n) rlh[(long long)(e0 + row) * H + a] = v;
+        }
+      }
       // kb = (1/sqrt 32)(zb^T q + zhb^T qh): lane holds (key kt*16 + 4 j4 + r, column ct*16 + i16)
       f32x4v KB[NT][2];
 #pragma unroll
@@ -852,7 +870,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
 // dE/dr of the edges of the atoms the matrix-core phase-2 kernel took (n <= nmax):
 // rbar_e += u'(r_e) sum over heads a (in order) of rbh[e H + a].  One wave per atom.
 __global__ void attn_rbar_kernel(const int* __restrict__ rowptr, const float* __restrict__ ud,
-                                 const float* __restrict__ rbh, int N, int H, int nmax, float* __restrict__ rbar) {
+                                 const float* __restrict__ rbh, int N, int H, int nmax, float* __restrict__ rbar,
+                                 float* __restrict__ rbs) {
   JANUS_WAVE_LOOP(i, N) {
     const int e0 = rowptr[i], n = rowptr[i + 1] - e0;
     if (n > nmax) continue;
@@ -861,8 +880,32 @@ __global__ void attn_rbar_kernel(const int* __restrict__ rowptr, const float* __
       float s = 0.f;
       for (int a = 0; a < H; ++a) s += rbh[e * H + a];
       rbar[e] += ud[e] * s;
+      if (rbs) rbs[e] = s;   // dE/du_e of this block, kept for the loss gradient in positions
     }
   }
+}
+
+// Loss gradient in positions through the attention envelope, one block: with
+// lu = log u(r / r_c) and its tangent rho = (d lu / dr) rt, the final backward gives
+// L_e = d(loss)/d lu_e (rlh, per head) and the force backward R_e = d(loss)/d rho_e =
+// u_e dE/du_e (rbs, the head sum, times u); then
+//   rpos_e += L_e (d lu / dr) + R_e rt_e (d2 lu / dr2)
+//          = L_e u'/u + rbs_e rt_e (u'' - u'^2 / u),
+// in float64 from r_e; edges at or past r_c (u = 0) take no part.
+__global__ void attn_pos_kernel(const float4* __restrict__ geo, long long Ne, int H, float rc,
+                                const float* __restrict__ rlh, const float* __restrict__ rbs,
+                                const float* __restrict__ rt, float* __restrict__ rpos) {
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= Ne) return;
+  const double x = (double)geo[e].w / rc;
+  if (!(x < 1.0)) return;
+  const double x2 = x * x, x4 = x2 * x2, x5 = x4 * x, x6 = x5 * x;
+  const double u = 1.0 - 28.0 * x6 + 48.0 * x6 * x - 21.0 * x6 * x2;
+  const double u1 = -168.0 * x5 * (1.0 - x) * (1.0 - x) / rc;
+  const double u2 = (-840.0 * x4 + 2016.0 * x5 - 1176.0 * x6) / ((double)rc * rc);
+  double L = 0.0;
+  for (int a = 0; a < H; ++a) L += rlh[e * H + a];
+  rpos[e] += (float)(L * u1 / u + (double)rbs[e] * (double)rt[e] * (u2 - u1 * u1 / u));
 }
 
 // Messages per edge from the expert slots: out_e = sum_c Y[pos[e, c]] (already gated).

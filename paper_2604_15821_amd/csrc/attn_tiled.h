@@ -347,13 +347,17 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_tiled_kernel(
 //   zhb_ql = u_q p (b_l - bm)                                            (adjoint of sh_ql)
 //   qb_q = sum_l (zb k_l + zhb kh_l) / sqrt(32),  kb_l = sum_q (zb q_q + zhb qh_q) / sqrt(32),
 //   vb_l = alpha sum_q u_q p + beta sum_q (uh_q p + u_q (pz - p zm)).
-// QKVa rows get (qb | kb | vb), the adjoints of the primal q, k, v.
+// QKVa rows get (qb | kb | vb), the adjoints of the primal q, k, v.  With rlh (the loss
+// gradient in positions) it also gets, per (edge, head), the adjoint of log u_e:
+// the sum over queries of zb_qe (key part) plus u_e (am + pbz - zm bm) + uh_e bm (query
+// part, u_e alpha.o_e + u_e beta.oh_e + uh_e beta.o_e).
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
     const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
-    int H, float* __restrict__ QKVa) {
-  __shared__ float s_sc[kAttnWaves][9][kAttnMaxN];
+    int H, float* __restrict__ QKVa, float* __restrict__ rlh) {
+  __shared__ float s_sc[kAttnWaves][10][kAttnMaxN];
+  float* lq_ = s_sc[threadIdx.x >> 6][9];
   float* su = s_sc[threadIdx.x >> 6][5];
   float* suh = s_sc[threadIdx.x >> 6][6];
   float* sM = s_sc[threadIdx.x >> 6][7];
@@ -429,6 +433,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
         bm_[qq] = bm;
         zm_[qq] = zm;
         sp_[qq] = SP;
+        lq_[qq] = ue * (am + pbz - zm * bm) + uh * bm;   // query part of the adjoint of log u
       }
       f32x4v QB[2] = {zero4(), zero4()};
       for (int kt = 0; kt < nt; ++kt) {
@@ -478,7 +483,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
       const float uk = kn < n ? su[kc] : 0.f, uhk = kn < n ? suh[kc] : 0.f;
       const float aj = sa[kc], bj = sb[kc];
       f32x4v KB[2] = {zero4(), zero4()};
-      float S1 = 0.f, S2 = 0.f;
+      float S1 = 0.f, S2 = 0.f, Lk = 0.f;
       for (int qt = 0; qt < nt; ++qt) {
         float qf[8], qhf[8];
         frag8(QKV, ld, e0, n, qt * 16 + i16, cq + 8 * j4, qf);
@@ -499,6 +504,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
           const float zhb = ue * p * (bj - bm);
           S1 += ue * p;
           S2 += uh * p + ue * (pz - p * zm);
+          Lk += zb;   // key part of the adjoint of log u: sum over queries of the score adjoint
           float q0, q1, h0, h1;
           cols2(QKV, ld, e0, n, q, cq, i16, q0, q1);
           cols2(QKVh, ld, e0, n, q, cq, i16, h0, h1);
@@ -510,6 +516,10 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_tiled_kernel(
       }
       S1 = sum_j4(S1);
       S2 = sum_j4(S2);
+      if (rlh) {
+        Lk = sum_j4(Lk);
+        if (j4 == 0 && kn < n) rlh[(long long)(e0 + kn) * H + a] = Lk + lq_[kn];
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int key = kt * 16 + 4 * j4 + r;

@@ -629,7 +629,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         hipLaunchKernelGGL(attn_bwd_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
                            (const float*)p.eu, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t), p.rbh);
         hipLaunchKernelGGL(attn_rbar_kernel, gN, b256, 0, st, rowptr, (const float*)p.eud, (const float*)p.rbh, N, H,
-                           kAttnMaxN, p.rbar);
+                           kAttnMaxN, p.rbar, p.rbs ? p.rbs + (long long)t * Ne : (float*)nullptr);
       }
       {
         PROF(PROF_DENSE_GEMM, f_qkv, 0);
@@ -1063,9 +1063,15 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_ATTN, 0, by_attn);
         // neighbourhoods up to kAttnMfmaN edges on register-resident tiles, larger ones on tiled sweeps
 #define JANUS_REV_MFMA(NTV)                                                                                    \
-  hipLaunchKernelGGL(attn_rev_mfma_kernel<NTV>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),                \
-                     (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,         \
-                     (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa)
+  if (p.rlh)                                                                                                   \
+    hipLaunchKernelGGL((attn_rev_mfma_kernel<NTV, true>), gNH, b256, 0, st, rowptr, (const float*)QKVt(t),      \
+                       (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,       \
+                       (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa, p.rlh);  \
+  else                                                                                                         \
+    hipLaunchKernelGGL((attn_rev_mfma_kernel<NTV, false>), gNH, b256, 0, st, rowptr, (const float*)QKVt(t),     \
+                       (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,       \
+                       (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa,          \
+                       (float*)nullptr)
         JANUS_REV_MFMA(1);
         if (2 <= kAttnTiles) JANUS_REV_MFMA(2);
         if (3 <= kAttnTiles) JANUS_REV_MFMA(3);
@@ -1073,7 +1079,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
 #undef JANUS_REV_MFMA
         hipLaunchKernelGGL(attn_rev_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
                            (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,
-                           (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa);
+                           (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa, p.rlh);
+        if (p.rlh && Ne > 0)   // the envelope's part of dL/dr_e
+          hipLaunchKernelGGL(attn_pos_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, (const float4*)p.geo, Ne, H,
+                             cfg.r_cut, (const float*)p.rlh, (const float*)(p.rbs + (long long)t * Ne),
+                             (const float*)p.rt, p.rpos);
       }
       {
         PROF(PROF_DENSE_GEMM, 3 * f_qkv, 0);
@@ -1374,7 +1384,6 @@ extern "C" int janus_step_pos(janus_ctx* ctx, const float* pos, const float* cel
       !dLdW || n_atoms < 1 || n_struct < 1 || n_struct > n_atoms)
     return JANUS_EINVAL;
   // the position gradient covers every option except attention
-  if (dLdR && ctx->cfg.n_heads) return JANUS_EUNSUPPORTED;
   const bool want_pos = dLdR != nullptr;
   // the task-aware embedding needs every structure's labels
   if (ctx->cfg.n_tasks && (!labels || !labels->task || !labels->charge || !labels->spin)) return JANUS_EINVAL;

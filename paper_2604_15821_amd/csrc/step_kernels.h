@@ -1018,6 +1018,7 @@ struct Plan {
   float *eu, *eud;
   float *Mm, *QKV, *stats, *osum, *OB, *QKVb, *MB, *Mh, *QKVh;
   float *AO, *QKVa, *mta, *osh, *rbh;
+  float *rbs, *rlh;   // with the loss gradient in positions: dE/du per block and edge, log-u adjoints
   RowsTile* tilesE;
   int* ntE;
   WChunk* chunksA;
@@ -1312,6 +1313,7 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.gtf = cv.take<float>(Mf + 1);
     p.ltf = cv.take<float>((long long)N * Ef + 1);
   }
+  p.rbs = p.rlh = nullptr;
   if (p.attn) {
     const long long Ed = Ne * d + 4, E3d = 3 * Ne * d + 4;
     p.eu = cv.take<float>(Ne + 1);
@@ -1330,6 +1332,8 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.mta = cv.take<float>(Ed);
     p.osh = cv.take<float>(Nd + 4);
     p.rbh = cv.take<float>(Ne * p.H + 4);
+    p.rbs = pos_grad ? cv.take<float>((long long)T * Ne + 4) : nullptr;
+    p.rlh = pos_grad ? cv.take<float>(Ne * p.H + 4) : nullptr;
     p.chunksA = cv.take<WChunk>(p.mcA);
     p.ncA = cv.take<int>(1);
     p.cfA = cv.take<int>(2);

@@ -7,7 +7,8 @@ a batch split over workspace chunks; sampled structures of the 512-structure
 irregular batch (a structure's gradient depends on the rest of the batch only
 through the loss normalisation, which a one-structure oracle run reproduces
 with scaled loss weights) and zero net gradient per structure at full size;
-attention, which the gradient does not cover, is refused."""
+self-attention (the envelope's first and second derivatives enter) on small and on
+60-140-edge neighbourhoods."""
 import dataclasses
 
 import numpy as np
@@ -36,6 +37,14 @@ def _batch(name):
     if name == "threebody-stress-1":
         b = subset(make_batch("threebody"), range(1))
         return dataclasses.replace(b, model=dataclasses.replace(b.model, w_S=0.1 * 160.2177 ** 2))
+    if name == "attention-stress-3":
+        b = subset(make_batch("attention"), range(3))
+        return dataclasses.replace(b, model=dataclasses.replace(b.model, w_S=0.1 * 160.2177 ** 2))
+    if name == "wide-attention":
+        # 40-atom cells at 0.08 and 0.145 / A^3: neighbourhoods of about 60 to 140 edges,
+        # both the register-resident attention kernels and the tiled sweeps
+        from test_gpu_attention import _batch as attn_batch
+        return attn_batch("wide-attn")
     raise KeyError(name)
 
 
@@ -60,7 +69,8 @@ def _run(b, limit=None, pos_grad=True):
     return out
 
 
-CASES = ["small-4", "stress-4", "robust-12", "atom_moe-3", "multitask-4", "threebody-stress-1"]
+CASES = ["small-4", "stress-4", "robust-12", "atom_moe-3", "multitask-4", "threebody-stress-1", "attention-stress-3",
+         "wide-attention"]
 
 
 @pytest.mark.parametrize("name", CASES)
@@ -97,18 +107,6 @@ def test_position_gradient_in_workspace_chunks():
             break
     assert many["chunks"] >= 2
     assert (many["dR"] == one["dR"]).all()
-
-
-def test_unsupported_options_are_refused():
-    import torch
-    from paper_2604_15821_amd import janus
-    from paper_2604_15821_amd.synth import make_batch, subset
-    for wl in ("attention",):
-        b = subset(make_batch(wl), range(1))
-        banner("dL/dR refused", wl)
-        with pytest.raises(janus.JanusError) as ex:
-            _run(b)
-        assert ex.value.code == janus.JANUS_EUNSUPPORTED
 
 
 def test_irregular_full_size_sampled_structures():
