@@ -33,6 +33,8 @@
 // epilogue reads of four pieces before it uses any of them.
 #pragma once
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace janus {
@@ -582,110 +584,116 @@ __global__ __launch_bounds__(256, 2) void gemm_wgrad_kernel(ALoad al, BLoad bl, 
 }
 
 // ---------------------------------------------------------- skinny wgrad
-// G[p, q] = sum_r s[r] A[r, p] B[r, q] for a short P (P <= 32, Q <= 512; the
-// radial-filter gradient: P = basis size, Q = d).  A 128-row MFMA tile would
-// be mostly padding there, so the vector units do it: a workgroup owns one
-// chunk of rows and the whole P x Q output; thread t owns output column
-// float4 q4 = t % (Q / 4) of the rows p = g np .. min(g np + np, P) - 1,
-// g = t / (Q / 4), np = ceil(P / (256 / (Q / 4))) <= NO, so each staged B
-// float4 is read once per thread and row.  Rows pass through LDS R = 8192 / Q
-// at a time (R (P + Q) floats of dynamic LDS, at most 48 KB), the next R rows
-// being loaded into registers while the current ones are used; a chunk takes
-// only a few passes, since every workgroup of the grid is resident at once and
-// each pass waits for one round trip to memory.  Partials per chunk, reduced
-// like gemm_wgrad's.  s may be null (s = 1).
-constexpr int kSkinnyBLoads = 8;   // B float4 per thread and pass: R Q / 4 / 256 = 8
-constexpr int kSkinnyALoads = 4;   // A float4 per thread and pass: R P / 4 / 256 <= 8192 * 32 / (Q 1024) <= 4
-inline int skinny_rows(int Q) { return 8192 / Q; }
+// G[p, q] = sum_r s[r] A[r, p] B[r, q] for a short P (P <= 32, a multiple of 4;
+// Q = 64, 128, 256 or 512: the radial-filter gradient, P = basis size, Q = d).
+// A 128-row MFMA tile would be mostly padding there, so the vector units do it,
+// straight from global memory.  A workgroup owns one chunk of rows and the whole
+// P x Q output.  Lane l of a wave owns CW = min(4, Q / 64) consecutive columns of
+// a 64 CW-wide column slice; the NS = Q / (64 CW) slices and RG = 4 / NS row
+// groups split the four waves, wave (g, slice) accumulating all P output rows of
+// its columns over the chunk rows g, g + RG, g + 2 RG, ...  A row's P values of A
+// and its scale are the same for the whole wave, so they come through scalar loads
+// and the vector registers hold only B and the accumulators; each step takes U
+// rows and issues all their loads before using any.  Per row, b' = s[r] B[r, :]
+// (B[r, :] if s is null) and acc[p] += A[r, p] b'.  The row groups are summed
+// through LDS (P Q floats of dynamic LDS) in group order, and the workgroup writes
+// one partial per chunk, reduced like gemm_wgrad's.
+inline int skinny_cw(int Q) { return Q >= 256 ? 4 : Q / 64; }
+inline int skinny_rows(int Q) {   // rows of one step of the workgroup (U = 4 rows per row group)
+  return 4 * (4 / (Q / (64 * skinny_cw(Q))));
+}
 
-template <int NO>
+template <int PM, int CW>
 __global__ __launch_bounds__(256) void wgrad_skinny_kernel(const float* __restrict__ A, const float* __restrict__ s,
                                                            const float* __restrict__ B, int P, int Q,
                                                            const WChunk* __restrict__ chunks,
-                                                           const int* __restrict__ n_chunks, int np,
+                                                           const int* __restrict__ n_chunks,
                                                            float* __restrict__ partial) {
+  constexpr int U = 8;
   extern __shared__ __attribute__((aligned(16))) float sk_lds[];
-  const int R = 8192 / Q;
-  float* a_s = sk_lds;             // [R][P]
-  float* b_s = sk_lds + R * P;     // [R][Q]
   const int c = blockIdx.x;
   if (c >= *n_chunks) return;
   const WChunk ch = chunks[c];
-  const int tid = threadIdx.x;
-  const int q4n = Q >> 2, p4n = P >> 2;
-  const int na = R * p4n, nbq = R * q4n;                          // float4 per pass
-  const int q4 = tid % q4n, p0 = (tid / q4n) * np;               // p0 >= P: idle thread
-  const int nown = P - p0 < np ? P - p0 : np;                     // rows of this thread
-  float4 acc[NO];
+  const int NS = Q / (64 * CW), RG = 4 / NS;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, la = lane % P;
+  const int g = w / NS, col = (w - g * NS) * 64 * CW + lane * CW;
+  float acc[PM][CW];
 #pragma unroll
-  for (int j = 0; j < NO; ++j) acc[j] = f4zero();
-  float4 ra[kSkinnyALoads], rb[kSkinnyBLoads];
-  auto load = [&](int r0) {
+  for (int p = 0; p < PM; ++p)
 #pragma unroll
-    for (int i = 0; i < kSkinnyALoads; ++i) {
-      const int q = tid + 256 * i;
-      if (q < na) {
-        const int rr = q / p4n, k4 = q - rr * p4n;
-        const long long r = (long long)r0 + rr;
-        float4 v = f4zero();
-        if (r < ch.r1) {
-          v = ld4(A + r * P + 4 * k4);
-          if (s) {
-            const float w = s[r];
-            v = make_float4(w * v.x, w * v.y, w * v.z, w * v.w);
-          }
-        }
-        ra[i] = v;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < kSkinnyBLoads; ++i) {
-      const int q = tid + 256 * i;
-      if (q < nbq) {
-        const int rr = q / q4n, k4 = q - rr * q4n;
-        const long long r = (long long)r0 + rr;
-        rb[i] = r < ch.r1 ? ld4(B + r * Q + 4 * k4) : f4zero();
-      }
+    for (int k = 0; k < CW; ++k) acc[p][k] = 0.f;
+  auto load_b = [&](long long r, float* v) {
+    const float* q = B + r * Q + col;
+    if constexpr (CW == 4) {
+      const float4 x = ld4(q);
+      v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    } else if constexpr (CW == 2) {
+      const float2 x = *reinterpret_cast<const float2*>(q);
+      v[0] = x.x; v[1] = x.y;
+    } else {
+      v[0] = *q;
     }
   };
-  load(ch.r0);
-  for (int r0 = ch.r0; r0 < ch.r1; r0 += R) {
+  // lane l holds A[r, l mod P]; row p's value is read from lane p (lanes p >= P
+  // hold a repeated column: those accumulator rows are never stored)
+  auto sweep = [&](auto scaled) {
+    constexpr bool SC = decltype(scaled)::value;
+    auto row = [&](float av, float sc, const float* b) {
+      float x[CW];
 #pragma unroll
-    for (int i = 0; i < kSkinnyALoads; ++i) {
-      const int q = tid + 256 * i;
-      if (q < na) st4(a_s + 4 * q, ra[i]);
+      for (int k = 0; k < CW; ++k) x[k] = SC ? sc * b[k] : b[k];
+      const int ai = __float_as_int(av);
+#pragma unroll
+      for (int p = 0; p < PM; ++p) {
+        const float ap = __int_as_float(__builtin_amdgcn_readlane(ai, p));
+#pragma unroll
+        for (int k = 0; k < CW; ++k) acc[p][k] += ap * x[k];
+      }
+    };
+    long long r = (long long)ch.r0 + g;
+    for (; r + (long long)(U - 1) * RG < ch.r1; r += (long long)U * RG) {
+      float b[U][CW], av[U], sc[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const long long ru = r + (long long)u * RG;
+        load_b(ru, b[u]);
+        av[u] = A[ru * P + la];
+        sc[u] = SC ? s[ru] : 1.f;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) row(av[u], sc[u], b[u]);
     }
-#pragma unroll
-    for (int i = 0; i < kSkinnyBLoads; ++i) {
-      const int q = tid + 256 * i;
-      if (q < nbq) st4(b_s + 4 * q, rb[i]);
+    for (; r < ch.r1; r += RG) {
+      float b[CW];
+      load_b(r, b);
+      row(A[r * P + la], SC ? s[r] : 1.f, b);
     }
-    __syncthreads();
-    if (r0 + R < ch.r1) load(r0 + R);
-    const int nr = ch.r1 - r0 < R ? ch.r1 - r0 : R;
-    if (p0 < P) {
-#pragma unroll 4
-      for (int rr = 0; rr < nr; ++rr) {
-        const float4 b = ld4(b_s + rr * Q + 4 * q4);
+  };
+  if (s)
+    sweep(std::true_type{});
+  else
+    sweep(std::false_type{});
+  float* red = sk_lds;   // [P][Q]
+  for (int gg = 0; gg < RG; ++gg) {
+    if (g == gg) {
 #pragma unroll
-        for (int j = 0; j < NO; ++j) {
-          if (j >= nown) break;
-          const float a = a_s[rr * P + p0 + j];
-          acc[j].x += a * b.x;
-          acc[j].y += a * b.y;
-          acc[j].z += a * b.z;
-          acc[j].w += a * b.w;
+      for (int p = 0; p < PM; ++p) {
+        if (p < P) {
+#pragma unroll
+          for (int k = 0; k < CW; ++k) {
+            float v = acc[p][k];
+            if (gg) v += red[p * Q + col + k];
+            red[p * Q + col + k] = v;
+          }
         }
       }
     }
     __syncthreads();
   }
-  if (p0 < P) {
-    float4* out = reinterpret_cast<float4*>(partial + (long long)c * P * Q);
-#pragma unroll
-    for (int j = 0; j < NO; ++j)
-      if (j < nown) out[(long long)(p0 + j) * q4n + q4] = acc[j];
-  }
+  float4* out = reinterpret_cast<float4*>(partial + (long long)c * P * Q);
+  const float4* red4 = reinterpret_cast<const float4*>(red);
+  for (int i = threadIdx.x; i < P * Q / 4; i += 256) out[i] = red4[i];
 }
 
 }  // namespace janus

@@ -110,19 +110,11 @@ __global__ void wgrad_reduce_kernel(const float* __restrict__ partial, const int
 }
 
 int skinny_chunk_rows(long long M, int P, int Q) {
-  const int no = skinny_rows_per_thread(P, Q);
-  const size_t lds = sizeof(float) * skinny_rows(Q) * (P + Q);
+  const size_t lds = sizeof(float) * P * Q;
   int per_cu = 0, dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e == hipSuccess) {
-    const void* k = no <= 1 ? (const void*)wgrad_skinny_kernel<1>
-                    : no <= 2 ? (const void*)wgrad_skinny_kernel<2>
-                    : no <= 4 ? (const void*)wgrad_skinny_kernel<4>
-                    : no <= 8 ? (const void*)wgrad_skinny_kernel<8>
-                              : (const void*)wgrad_skinny_kernel<16>;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 256, lds);
-  }
+  if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, skinny_kernel(P, Q), 256, lds);
   const long long slots = (e == hipSuccess && per_cu > 0 && cus > 0) ? (long long)per_cu * cus : 1024;
   const long long R = skinny_rows(Q);
   const long long per = (M + slots - 1) / slots;

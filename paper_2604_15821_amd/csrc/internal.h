@@ -134,17 +134,21 @@ inline int wgrad_chunk_rows(long long M, int P, int Q) {
 }
 
 // Chunk length of the skinny weight gradient (wgrad_skinny_kernel, one workgroup
-// per chunk): a multiple of the rows it stages per pass, long enough that all chunks
-// fit in one set of resident workgroups (CUs x workgroups per CU at the kernel
-// instance's register and LDS use, queried from the runtime), so no second, mostly
-// idle round runs.  On the small batch (169 k rows, 16 x 128) 192-row chunks take 3
-// passes in one round, against 128-row chunks' 2 passes in 1.3 rounds.
+// per chunk): a multiple of the rows of one of its steps, long enough that all
+// chunks fit in one set of resident workgroups (CUs x workgroups per CU at the
+// kernel instance's register and LDS use, queried from the runtime), so no
+// second, mostly idle round runs.
 int skinny_chunk_rows(long long M, int P, int Q);
 
-// Output rows per thread of the skinny weight gradient for P x Q (its template argument).
-inline int skinny_rows_per_thread(int P, int Q) {
-  const int groups = 256 / (Q / 4);
-  return (P + groups - 1) / groups;
+// Instance of the skinny weight gradient for P x Q: P rounded up to 8, 16 or 32,
+// and the columns per lane.
+template <int PM, int CW>
+const void* skinny_instance() { return (const void*)wgrad_skinny_kernel<PM, CW>; }
+inline const void* skinny_kernel(int P, int Q) {
+  const int cw = skinny_cw(Q);
+#define JANUS_SKINNY_CW(PM) (cw == 4 ? skinny_instance<PM, 4>() : cw == 2 ? skinny_instance<PM, 2>() : skinny_instance<PM, 1>())
+  return P <= 8 ? JANUS_SKINNY_CW(8) : P <= 16 ? JANUS_SKINNY_CW(16) : JANUS_SKINNY_CW(32);
+#undef JANUS_SKINNY_CW
 }
 
 void launch_wgrad_reduce(hipStream_t st, const float* partial, const int* chunk_first, int groups,
@@ -178,20 +182,9 @@ inline void launch_wgrad_skinny(hipStream_t st, const float* A, const float* s, 
                                 const WChunk* chunks, const int* n_chunks, const int* chunk_first, int max_chunks,
                                 float* partial, float* G, int accumulate) {
   if (max_chunks > 0) {
-    // output rows per thread: P over the 256 / (Q / 4) thread groups
-    const int no = skinny_rows_per_thread(P, Q);
-    const dim3 grid(max_chunks), blk(256);
-    const size_t lds = sizeof(float) * skinny_rows(Q) * (P + Q);
-    if (no <= 1)
-      hipLaunchKernelGGL(wgrad_skinny_kernel<1>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
-    else if (no <= 2)
-      hipLaunchKernelGGL(wgrad_skinny_kernel<2>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
-    else if (no <= 4)
-      hipLaunchKernelGGL(wgrad_skinny_kernel<4>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
-    else if (no <= 8)
-      hipLaunchKernelGGL(wgrad_skinny_kernel<8>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
-    else
-      hipLaunchKernelGGL(wgrad_skinny_kernel<16>, grid, blk, lds, st, A, s, B, P, Q, chunks, n_chunks, no, partial);
+    void* args[] = {(void*)&A, (void*)&s, (void*)&B, (void*)&P, (void*)&Q, (void*)&chunks, (void*)&n_chunks,
+                    (void*)&partial};
+    (void)hipLaunchKernel(skinny_kernel(P, Q), dim3(max_chunks), dim3(256), args, sizeof(float) * P * Q, st);
   }
   launch_wgrad_reduce(st, partial, chunk_first, 1, (long long)P * Q, G, accumulate);
 }
