@@ -101,6 +101,19 @@ __device__ __forceinline__ void frag8(const float* __restrict__ base, long long 
   x[4] = z * b.x; x[5] = z * b.y; x[6] = z * b.z; x[7] = z * b.w;
 }
 
+// Sum over the 16 lanes i16 of each lane group (every lane gets its group's sum):
+// DPP quad_perm 1032, quad_perm 2301, half-row mirror, row mirror.
+template <int CTRL>
+__device__ __forceinline__ float attn_dpp_add(float v) {
+  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float sum_i16(float v) {
+  v = attn_dpp_add<0xB1>(v);
+  v = attn_dpp_add<0x4E>(v);
+  v = attn_dpp_add<0x141>(v);
+  return attn_dpp_add<0x140>(v);
+}
+
 // Sum (or max) over the four lane groups j4 of a value owned by row i16.
 __device__ __forceinline__ float sum_j4(float v) {
   v += __shfl_xor(v, 16, 64);
@@ -381,14 +394,18 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_tan_mfma_kernel(
 // wave per (atom, head); same outputs as attn_bwd_tiled_kernel: the envelope
 // terms of dE/dr go to rbh [(e H + a)] (query term cw_e plus key term kl_e of head a)
 // and attn_rbar_kernel adds them to rbar.  Transposed score tiles (key x query) give
-// p, cw and zb = u_q p (w_k - cw_q) in the A-operand layout of qb = zb k; score tiles
-// the other way round (query x key) give zb in the layout of kb = zb^T q, and the
-// per-key sums Pu = sum_q u_q p (vb = Pu ob) and kl = sum_q u_q E (w_k - cw_q).
+// p, cw and zb = u_q p (w_k - cw_q) in the A-operand layout of qb = zb k, and the per-key
+// sums Pu = sum_q u_q p (vb = Pu ob) and kl = sum_q u_q E (w_k - cw_q) by adding over
+// the 16 query lanes; each zb tile is transposed through LDS (1 KB per wave) into the
+// layout of kb = zb^T q.
 template <int NT>
-__global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
+__global__ __launch_bounds__(64 * kAttnWaves, NT <= 3 ? 2 : 1) void attn_bwd_mfma_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ uu,
     const float* __restrict__ stats, const float* __restrict__ ob, int N, int d, int H, float* __restrict__ QKVb,
     float* __restrict__ rbh) {
+  constexpr int LT = 20;   // row stride of a transposed tile (floats)
+  __shared__ __attribute__((aligned(16))) float s_tr[kAttnWaves][16 * LT];
+  float* tz = s_tr[threadIdx.x >> 6];
   const long long ld = 3LL * d;
   const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
   JANUS_WAVE_LOOP(item, (long long)N * H) {
@@ -423,7 +440,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
       urow[t] = row < n ? uu[e0 + row] : 0.f;
     }
     // ---- transposed tiles: lane holds (key kt*16 + 4 j4 + r, query qt*16 + i16)
-    float cw[NT];
     {
       f32x4v S[NT][NT];
 #pragma unroll
@@ -444,6 +460,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
           uk[t][r] = __shfl(urow[t], 4 * j4 + r, 64);   // u of key t*16 + 4 j4 + r
           wk[t][r] = __shfl(wrow[t], 4 * j4 + r, 64);
         }
+      // per key kt*16 + 4 j4 + r, partial over this lane's queries: sum u_q p, and
+      // kl = sum u_q E (w_k - cw_q)
+      float pu[NT][4], kl[NT][4], cw[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) pu[t][r] = kl[t][r] = 0.f;
 #pragma unroll
       for (int qt = 0; qt < NT; ++qt) {
         const int q = qt * 16 + i16;
@@ -454,9 +477,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
         for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = uk[kt][r] * __expf(S[kt][qt][r] * kAttnScale - M) * iZ;
-            S[kt][qt][r] = p;
-            c += p * wk[kt][r];
+            const float E = __expf(S[kt][qt][r] * kAttnScale - M) * iZ;
+            S[kt][qt][r] = E;
+            c += uk[kt][r] * E * wk[kt][r];
           }
         cw[qt] = sum_j4(c);
         // zb = u_q p (w_k - cw_q), in place
@@ -464,77 +487,91 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
 #pragma unroll
         for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) S[kt][qt][r] = uq * S[kt][qt][r] * (wk[kt][r] - cw[qt]);
+          for (int r = 0; r < 4; ++r) {
+            const float E = S[kt][qt][r], p = uk[kt][r] * E, dw = wk[kt][r] - cw[qt];
+            pu[kt][r] += uq * p;
+            kl[kt][r] += uq * E * dw;
+            S[kt][qt][r] = uq * p * dw;
+          }
       }
       // qb = (1/sqrt 32) zb k: lane holds (query qt*16 + 4 j4 + r, column ct*16 + i16)
-      f32x4v QB[NT][2];
+      {
+        f32x4v QB[NT][2];
 #pragma unroll
-      for (int qt = 0; qt < NT; ++qt) QB[qt][0] = QB[qt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
+        for (int qt = 0; qt < NT; ++qt) QB[qt][0] = QB[qt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kt = 0; kt < NT; ++kt)
+        for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = kt * 16 + 4 * j4 + r;
-          const long long row = (long long)(e0 + (key < n ? key : n - 1)) * ld;
-          const float k0 = QKV[row + ck + i16], k1 = QKV[row + ck + 16 + i16];
+          for (int r = 0; r < 4; ++r) {
+            const int key = kt * 16 + 4 * j4 + r;
+            const long long row = (long long)(e0 + (key < n ? key : n - 1)) * ld;
+            const float k0 = QKV[row + ck + i16], k1 = QKV[row + ck + 16 + i16];
 #pragma unroll
-          for (int qt = 0; qt < NT; ++qt) {
-            QB[qt][0] = mfma16(S[kt][qt][r], k0, QB[qt][0]);
-            QB[qt][1] = mfma16(S[kt][qt][r], k1, QB[qt][1]);
+            for (int qt = 0; qt < NT; ++qt) {
+              QB[qt][0] = mfma16(S[kt][qt][r], k0, QB[qt][0]);
+              QB[qt][1] = mfma16(S[kt][qt][r], k1, QB[qt][1]);
+            }
           }
-        }
-#pragma unroll
-      for (int qt = 0; qt < NT; ++qt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int q = qt * 16 + 4 * j4 + r;
-          if (q < n) {
-            float* o = QKVb + (long long)(e0 + q) * ld + cq;
-            o[i16] = kAttnScale * QB[qt][0][r];
-            o[16 + i16] = kAttnScale * QB[qt][1][r];
-          }
-        }
-    }
-    // ---- tiles the other way round: lane holds (query qt*16 + 4 j4 + r, key kt*16 + i16)
-    {
-      f32x4v S2[NT][NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int u = 0; u < NT; ++u) S2[t][u] = f32x4v{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int st = 0; st < 8; ++st)
 #pragma unroll
         for (int qt = 0; qt < NT; ++qt)
 #pragma unroll
-          for (int kt = 0; kt < NT; ++kt) S2[qt][kt] = mfma16(qf[qt][st], kf[kt][st], S2[qt][kt]);
-      float pu[NT], kl[NT];
+          for (int r = 0; r < 4; ++r) {
+            const int q = qt * 16 + 4 * j4 + r;
+            if (q < n) {
+              float* o = QKVb + (long long)(e0 + q) * ld + cq;
+              o[i16] = kAttnScale * QB[qt][0][r];
+              o[16 + i16] = kAttnScale * QB[qt][1][r];
+            }
+          }
+      }
+      // ---- per-key sums over the 16 query lanes: lane (i16, j4) then holds those of keys
+      // kt*16 + 4 j4 + r.  vb = Pu ob: lane i16 writes key 4 j4 + i16 / 4, columns
+      // 8 (i16 % 4) ..; envelope term of edge e = 4 j4 + i16 (lanes i16 < 4): cw_e + kl_e
+      const int rs = i16 >> 2, cg = i16 & 3;
+      float obw[8];
+      {
+        const float* po = ob + (long long)i * d + cq + 8 * cg;
+        const float4 x = *reinterpret_cast<const float4*>(po), y = *reinterpret_cast<const float4*>(po + 4);
+        obw[0] = x.x; obw[1] = x.y; obw[2] = x.z; obw[3] = x.w;
+        obw[4] = y.x; obw[5] = y.y; obw[6] = y.z; obw[7] = y.w;
+      }
 #pragma unroll
-      for (int kt = 0; kt < NT; ++kt) pu[kt] = kl[kt] = 0.f;
-#pragma unroll
-      for (int qt = 0; qt < NT; ++qt)
+      for (int kt = 0; kt < NT; ++kt) {
+        float P = 0.f, K = 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int q = qt * 16 + 4 * j4 + r;
-          const long long sq = ((long long)(e0 + (q < n ? q : n - 1)) * H + a) * 2;
-          const float M = stats[sq], iZ = 1.f / stats[sq + 1];
-          const float uq = __shfl(urow[qt], 4 * j4 + r, 64);
-          const float cq_ = __shfl(cw[qt], 4 * j4 + r, 64);
-#pragma unroll
-          for (int kt = 0; kt < NT; ++kt) {
-            const float E = __expf(S2[qt][kt][r] * kAttnScale - M) * iZ;
-            const float t = uq * E * (wrow[kt] - cq_);
-            kl[kt] += t;
-            pu[kt] += uq * urow[kt] * E;
-            S2[qt][kt][r] = urow[kt] * t;   // zb (key kt*16 + i16, query q)
-          }
+          const float v1 = sum_i16(pu[kt][r]), v2 = sum_i16(kl[kt][r]);
+          P = rs == r ? v1 : P;
+          K = cg == r ? v2 : K;
         }
-      // kb = (1/sqrt 32) zb^T q: lane holds (key kt*16 + 4 j4 + r, column ct*16 + i16)
+        const int key = kt * 16 + 4 * j4 + rs;
+        if (key < n) {
+          float* o = QKVb + (long long)(e0 + key) * ld + cv + 8 * cg;
+          *reinterpret_cast<float4*>(o) = make_float4(P * obw[0], P * obw[1], P * obw[2], P * obw[3]);
+          *reinterpret_cast<float4*>(o + 4) = make_float4(P * obw[4], P * obw[5], P * obw[6], P * obw[7]);
+        }
+        const float c = __shfl(cw[kt], 4 * j4 + cg, 64);   // cw of row kt*16 + 4 j4 + cg
+        const int row = kt * 16 + 4 * j4 + cg;
+        if (i16 < 4 && row < n) rbh[(long long)(e0 + row) * H + a] = c + K;
+      }
+      // ---- kb = (1/sqrt 32) zb^T q: each zb tile transposed through LDS, lane (i16, j4)
+      // receiving (query qt*16 + 4 j4 + r, key kt*16 + i16); lane holds (key kt*16 + 4 j4 + r,
+      // column ct*16 + i16) of kb
       f32x4v KB[NT][2];
 #pragma unroll
       for (int kt = 0; kt < NT; ++kt) KB[kt][0] = KB[kt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int qt = 0; qt < NT; ++qt)
+      for (int qt = 0; qt < NT; ++qt) {
+        float zt[NT][4];
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt) {
+          *reinterpret_cast<float4*>(tz + i16 * LT + 4 * j4) =
+              make_float4(S[kt][qt][0], S[kt][qt][1], S[kt][qt][2], S[kt][qt][3]);
+          wave_sync();
+#pragma unroll
+          for (int r = 0; r < 4; ++r) zt[kt][r] = tz[(4 * j4 + r) * LT + i16];
+          wave_sync();
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int q = qt * 16 + 4 * j4 + r;
@@ -542,10 +579,11 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
           const float x0 = QKV[row + cq + i16], x1 = QKV[row + cq + 16 + i16];
 #pragma unroll
           for (int kt = 0; kt < NT; ++kt) {
-            KB[kt][0] = mfma16(S2[qt][kt][r], x0, KB[kt][0]);
-            KB[kt][1] = mfma16(S2[qt][kt][r], x1, KB[kt][1]);
+            KB[kt][0] = mfma16(zt[kt][r], x0, KB[kt][0]);
+            KB[kt][1] = mfma16(zt[kt][r], x1, KB[kt][1]);
           }
         }
+      }
 #pragma unroll
       for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
@@ -557,19 +595,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
             o[16 + i16] = kAttnScale * KB[kt][1][r];
           }
         }
-      // vb = Pu ob (columns 8 j4 .. 8 j4 + 7 of key kt*16 + i16); envelope terms of the edge
-#pragma unroll
-      for (int kt = 0; kt < NT; ++kt) {
-        const float P = sum_j4(pu[kt]);
-        const float K = sum_j4(kl[kt]);
-        const int key = kt * 16 + i16;
-        if (key < n) {
-          float* o = QKVb + (long long)(e0 + key) * ld + cv + 8 * j4;
-          *reinterpret_cast<float4*>(o) = make_float4(P * obf[0], P * obf[1], P * obf[2], P * obf[3]);
-          *reinterpret_cast<float4*>(o + 4) = make_float4(P * obf[4], P * obf[5], P * obf[6], P * obf[7]);
-          if (j4 == 0) rbh[(long long)(e0 + key) * H + a] = cw[kt] + K;
-        }
-      }
     }
   }
 }
@@ -579,11 +604,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_bwd_mfma_kernel(
 // lane): u, uh = u' rt, a = alpha.v + beta.vh and b = beta.v (8-column partial dots
 // added over the four lane groups), the query's softmax statistics.  Transposed tiles
 // (key x query) of s and sh give the per-query sums am, bm, zm, pbz and SP, then zb and
-// zhb in the A-operand layout of qb = zb k + zhb kh; tiles the other way round
-// (query x key) give zb, zhb in the layout of kb = zb^T q + zhb^T qh and the per-key
-// sums S1 = sum u_q p, S2 = sum uh_q p + u_q (pz - p zm) of vb = S1 alpha + S2 beta.
+// zhb in the A-operand layout of qb = zb k + zhb kh.  The same tiles give the per-key
+// sums S1 = sum u_q p, S2 = sum uh_q p + u_q (pz - p zm) of vb = S1 alpha + S2 beta (and,
+// with POS, sum_q zb) by adding over the 16 query lanes, and each (zb, zhb) tile pair is
+// transposed through LDS (2 KB per wave) into the A-operand layout of
+// kb = zb^T q + zhb^T qh, so no score tile is formed twice.
 template <int NT, bool POS>
-__global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
+__global__ __launch_bounds__(64 * kAttnWaves, NT <= 3 && !POS ? 2 : 1) void attn_rev_mfma_kernel(
     const int* __restrict__ rowptr, const float* __restrict__ QKV, const float* __restrict__ QKVh,
     const float* __restrict__ uu, const float* __restrict__ ud, const float* __restrict__ rt,
     const float* __restrict__ stats, const float* __restrict__ alpha, const float* __restrict__ beta, int N, int d,
@@ -591,6 +618,10 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
   // multiply-adds are fused only inside one expression: the instance that also forms the
   // log-u adjoints (POS) then computes every other output with the same roundings
 #pragma clang fp contract(on)
+  constexpr int LT = 20;   // row stride of a transposed tile (floats)
+  __shared__ __attribute__((aligned(16))) float s_tr[kAttnWaves][2][16 * LT];
+  float* tz = s_tr[threadIdx.x >> 6][0];
+  float* th = s_tr[threadIdx.x >> 6][1];
   const long long ld = 3LL * d;
   const int i16 = threadIdx.x & 15, j4 = (threadIdx.x >> 4) & 3;
   JANUS_WAVE_LOOP(item, (long long)N * H) {
@@ -632,8 +663,16 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
       mrow[t] = stats[sq];
       izrow[t] = 1.f / stats[sq + 1];
     }
-    float bmq[NT], zmq[NT], spq[NT];   // per query t*16 + i16
     float lq[POS ? NT : 1];            // with POS: query part of the adjoint of log u, row t*16 + i16
+    // per key kt*16 + 4 j4 + r, partial over this lane's queries: S1, S2 (and sum_q zb)
+    float c1[NT][4], c2[NT][4], c3[POS ? NT : 1][4];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        c1[t][r] = c2[t][r] = 0.f;
+        if (POS) c3[t][r] = 0.f;
+      }
     // ---- transposed tiles: lane holds (key kt*16 + 4 j4 + r, query qt*16 + i16)
     {
       f32x4v S[NT][NT], Sh[NT][NT];
@@ -699,10 +738,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
         const float ue = urow[qt], uh = uhrow[qt];
         const float SP = ue * (am + pbz - 2.f * zm * bm) + uh * bm;
         if (POS) lq[qt] = ue * (am + pbz - zm * bm) + uh * bm;   // query part of the log-u adjoint
-        bmq[qt] = bm;
-        zmq[qt] = zm;
-        spq[qt] = SP;
-        // zb into S, zhb into Sh
+        // zb into S, zhb into Sh; this query's terms of the per-key sums
 #pragma unroll
         for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
@@ -710,8 +746,12 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
             const int src = 4 * j4 + r;
             const float ak = __shfl(arow[kt], src, 64), bk = __shfl(brow[kt], src, 64);
             const float p = S[kt][qt][r], pz = Sh[kt][qt][r];
-            S[kt][qt][r] = ue * (p * ak + bk * (pz - p * zm) - pz * bm) + uh * p * bk - p * SP;
+            c1[kt][r] += ue * p;
+            c2[kt][r] += uh * p + ue * (pz - p * zm);
+            const float zb = ue * (p * ak + bk * (pz - p * zm) - pz * bm) + uh * p * bk - p * SP;
+            S[kt][qt][r] = zb;
             Sh[kt][qt][r] = ue * p * (bk - bm);
+            if (POS) c3[kt][r] += zb;   // key part of the log-u adjoint
           }
       }
       // qb = (1/sqrt 32)(zb k + zhb kh): lane holds (query qt*16 + 4 j4 + r, column ct*16 + i16)
@@ -745,86 +785,72 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
             o[16 + i16] = kAttnScale * QB[qt][1][r];
           }
         }
-    }
-    // ---- tiles the other way round: lane holds (query qt*16 + 4 j4 + r, key kt*16 + i16)
-    {
-      f32x4v S[NT][NT], Sh[NT][NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int u = 0; u < NT; ++u) S[t][u] = Sh[t][u] = f32x4v{0.f, 0.f, 0.f, 0.f};
+      // ---- per-key sums over the 16 query lanes: lane (i16, j4) then holds those of keys
+      // kt*16 + 4 j4 + r; lane i16 writes key 4 j4 + i16 / 4, columns 8 (i16 % 4) ..
+      const int rs = i16 >> 2, cg = i16 & 3;
+      float alw[8], bew[8];
       {
-        float qf[NT][8], kf[NT][8], hf[NT][8];
+        const float* pa = alpha + (long long)i * d + cq + 8 * cg;
+        const float* pb = beta + (long long)i * d + cq + 8 * cg;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          frag8(QKV, ld, e0, n, t * 16 + i16, cq + 8 * j4, qf[t]);
-          frag8(QKV, ld, e0, n, t * 16 + i16, ck + 8 * j4, kf[t]);
+        for (int c = 0; c < 8; c += 4) {
+          const float4 x = *reinterpret_cast<const float4*>(pa + c), y = *reinterpret_cast<const float4*>(pb + c);
+          alw[c] = x.x; alw[c + 1] = x.y; alw[c + 2] = x.z; alw[c + 3] = x.w;
+          bew[c] = y.x; bew[c + 1] = y.y; bew[c + 2] = y.z; bew[c + 3] = y.w;
         }
-#pragma unroll
-        for (int st = 0; st < 8; ++st)
-#pragma unroll
-          for (int qt = 0; qt < NT; ++qt)
-#pragma unroll
-            for (int kt = 0; kt < NT; ++kt) S[qt][kt] = mfma16(qf[qt][st], kf[kt][st], S[qt][kt]);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) frag8(QKVh, ld, e0, n, t * 16 + i16, cq + 8 * j4, hf[t]);   // qh
-#pragma unroll
-        for (int st = 0; st < 8; ++st)
-#pragma unroll
-          for (int qt = 0; qt < NT; ++qt)
-#pragma unroll
-            for (int kt = 0; kt < NT; ++kt) Sh[qt][kt] = mfma16(hf[qt][st], kf[kt][st], Sh[qt][kt]);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) frag8(QKVh, ld, e0, n, t * 16 + i16, ck + 8 * j4, hf[t]);   // kh
-#pragma unroll
-        for (int st = 0; st < 8; ++st)
-#pragma unroll
-          for (int qt = 0; qt < NT; ++qt)
-#pragma unroll
-            for (int kt = 0; kt < NT; ++kt) Sh[qt][kt] = mfma16(qf[qt][st], hf[kt][st], Sh[qt][kt]);
       }
-      float s1[NT], s2[NT], lk[POS ? NT : 1];
 #pragma unroll
       for (int kt = 0; kt < NT; ++kt) {
-        s1[kt] = s2[kt] = 0.f;
-        if (POS) lk[kt] = 0.f;
-      }
-#pragma unroll
-      for (int qt = 0; qt < NT; ++qt)
+        float A1 = 0.f, A2 = 0.f, L = 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int src = 4 * j4 + r;
-          const float M = __shfl(mrow[qt], src, 64), iZ = __shfl(izrow[qt], src, 64);
-          const float ue = __shfl(urow[qt], src, 64), uh = __shfl(uhrow[qt], src, 64);
-          const float bm = __shfl(bmq[qt], src, 64), zm = __shfl(zmq[qt], src, 64), SP = __shfl(spq[qt], src, 64);
-#pragma unroll
-          for (int kt = 0; kt < NT; ++kt) {
-            const float E = __expf(S[qt][kt][r] * kAttnScale - M) * iZ;
-            const float p = urow[kt] * E;
-            const float pz = p * Sh[qt][kt][r] * kAttnScale + uhrow[kt] * E;
-            const float ak = arow[kt], bk = brow[kt];
-            s1[kt] += ue * p;
-            s2[kt] += uh * p + ue * (pz - p * zm);
-            S[qt][kt][r] = ue * (p * ak + bk * (pz - p * zm) - pz * bm) + uh * p * bk - p * SP;
-            Sh[qt][kt][r] = ue * p * (bk - bm);
-            if (POS) lk[kt] += S[qt][kt][r];   // key part: sum over queries of the score adjoint
+          const float v1 = sum_i16(c1[kt][r]), v2 = sum_i16(c2[kt][r]);
+          A1 = rs == r ? v1 : A1;
+          A2 = rs == r ? v2 : A2;
+          if (POS) {
+            const float v3 = sum_i16(c3[kt][r]);
+            L = cg == r ? v3 : L;
           }
         }
-      if (POS) {
-        // adjoint of log u_e, edge e = row t*16 + i16: key part + query part
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          const float v = sum_j4(lk[t]) + lq[t];
-          const int row = t * 16 + i16;
-          if (j4 == 0 && row < n) rlh[(long long)(e0 + row) * H + a] = v;
+        const int key = kt * 16 + 4 * j4 + rs;
+        if (key < n) {
+          // vb = S1 alpha + S2 beta
+          float* o = QKVa + (long long)(e0 + key) * ld + cv + 8 * cg;
+          *reinterpret_cast<float4*>(o) = make_float4(A1 * alw[0] + A2 * bew[0], A1 * alw[1] + A2 * bew[1],
+                                                      A1 * alw[2] + A2 * bew[2], A1 * alw[3] + A2 * bew[3]);
+          *reinterpret_cast<float4*>(o + 4) = make_float4(A1 * alw[4] + A2 * bew[4], A1 * alw[5] + A2 * bew[5],
+                                                          A1 * alw[6] + A2 * bew[6], A1 * alw[7] + A2 * bew[7]);
+        }
+        if (POS) {
+          // adjoint of log u_e, edge e = kt*16 + 4 j4 + cg: key part + query part (row e's lane)
+          const float q = __shfl(lq[kt], 4 * j4 + cg, 64);
+          const int row = kt * 16 + 4 * j4 + cg;
+          if (i16 < 4 && row < n) rlh[(long long)(e0 + row) * H + a] = L + q;
         }
       }
-      // kb = (1/sqrt 32)(zb^T q + zhb^T qh): lane holds (key kt*16 + 4 j4 + r, column ct*16 + i16)
+      // ---- kb = (1/sqrt 32)(zb^T q + zhb^T qh): each (zb, zhb) tile pair transposed through
+      // LDS, lane (i16, j4) receiving (query qt*16 + 4 j4 + r, key kt*16 + i16); lane holds
+      // (key kt*16 + 4 j4 + r, column ct*16 + i16) of kb
       f32x4v KB[NT][2];
 #pragma unroll
       for (int kt = 0; kt < NT; ++kt) KB[kt][0] = KB[kt][1] = f32x4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int qt = 0; qt < NT; ++qt)
+      for (int qt = 0; qt < NT; ++qt) {
+        float zt[NT][4], ht[NT][4];
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt) {
+          *reinterpret_cast<float4*>(tz + i16 * LT + 4 * j4) =
+              make_float4(S[kt][qt][0], S[kt][qt][1], S[kt][qt][2], S[kt][qt][3]);
+          *reinterpret_cast<float4*>(th + i16 * LT + 4 * j4) =
+              make_float4(Sh[kt][qt][0], Sh[kt][qt][1], Sh[kt][qt][2], Sh[kt][qt][3]);
+          wave_sync();
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            zt[kt][r] = tz[(4 * j4 + r) * LT + i16];
+            ht[kt][r] = th[(4 * j4 + r) * LT + i16];
+          }
+          wave_sync();
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int q = qt * 16 + 4 * j4 + r;
@@ -833,12 +859,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
           const float h0 = QKVh[row + cq + i16], h1 = QKVh[row + cq + 16 + i16];
 #pragma unroll
           for (int kt = 0; kt < NT; ++kt) {
-            KB[kt][0] = mfma16(S[qt][kt][r], x0, KB[kt][0]);
-            KB[kt][1] = mfma16(S[qt][kt][r], x1, KB[kt][1]);
-            KB[kt][0] = mfma16(Sh[qt][kt][r], h0, KB[kt][0]);
-            KB[kt][1] = mfma16(Sh[qt][kt][r], h1, KB[kt][1]);
+            KB[kt][0] = mfma16(zt[kt][r], x0, KB[kt][0]);
+            KB[kt][1] = mfma16(zt[kt][r], x1, KB[kt][1]);
+            KB[kt][0] = mfma16(ht[kt][r], h0, KB[kt][0]);
+            KB[kt][1] = mfma16(ht[kt][r], h1, KB[kt][1]);
           }
         }
+      }
 #pragma unroll
       for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
@@ -850,19 +877,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rev_mfma_kernel(
             o[16 + i16] = kAttnScale * KB[kt][1][r];
           }
         }
-      // vb = S1 alpha + S2 beta (columns 8 j4 .. 8 j4 + 7 of key kt*16 + i16)
-#pragma unroll
-      for (int kt = 0; kt < NT; ++kt) {
-        const float A1 = sum_j4(s1[kt]), A2 = sum_j4(s2[kt]);
-        const int key = kt * 16 + i16;
-        if (key < n) {
-          float* o = QKVa + (long long)(e0 + key) * ld + cv + 8 * j4;
-          *reinterpret_cast<float4*>(o) = make_float4(A1 * alf[0] + A2 * bef[0], A1 * alf[1] + A2 * bef[1],
-                                                      A1 * alf[2] + A2 * bef[2], A1 * alf[3] + A2 * bef[3]);
-          *reinterpret_cast<float4*>(o + 4) = make_float4(A1 * alf[4] + A2 * bef[4], A1 * alf[5] + A2 * bef[5],
-                                                          A1 * alf[6] + A2 * bef[6], A1 * alf[7] + A2 * bef[7]);
-        }
-      }
     }
   }
 }

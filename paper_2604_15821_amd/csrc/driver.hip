@@ -1063,15 +1063,17 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_ATTN, 0, by_attn);
         // neighbourhoods up to kAttnMfmaN edges on register-resident tiles, larger ones on tiled sweeps
 #define JANUS_REV_MFMA(NTV)                                                                                    \
-  if (p.rlh)                                                                                                   \
-    hipLaunchKernelGGL((attn_rev_mfma_kernel<NTV, true>), gNH, b256, 0, st, rowptr, (const float*)QKVt(t),      \
-                       (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,       \
-                       (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa, p.rlh);  \
-  else                                                                                                         \
-    hipLaunchKernelGGL((attn_rev_mfma_kernel<NTV, false>), gNH, b256, 0, st, rowptr, (const float*)QKVt(t),     \
-                       (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,       \
-                       (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa,          \
-                       (float*)nullptr)
+  do {                                                                                                         \
+    if (p.rlh)                                                                                                 \
+      hipLaunchKernelGGL((attn_rev_mfma_kernel<NTV, true>), gNH, b256, 0, st, rowptr, (const float*)QKVt(t),    \
+                         (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,     \
+                         (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa, p.rlh); \
+    else                                                                                                       \
+      hipLaunchKernelGGL((attn_rev_mfma_kernel<NTV, false>), gNH, b256, 0, st, rowptr, (const float*)QKVt(t),   \
+                         (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,     \
+                         (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa,        \
+                         (float*)nullptr);                                                                     \
+  } while (0)
         JANUS_REV_MFMA(1);
         if (2 <= kAttnTiles) JANUS_REV_MFMA(2);
         if (3 <= kAttnTiles) JANUS_REV_MFMA(3);
