@@ -21,6 +21,10 @@
 //   (dG/dc W_a)   = u3 sum_l P'_l s_l
 //   (dG/dr2 W_a)  = u3 sum_l P_l  s'_l
 //   (dG/dr1 W_a)  = u3' sum_l P_l s_l .
+// The sums over l are polynomials in c of degree < L whose coefficients depend
+// on the second edge only: the expert-token kernels rewrite s_l and s'_l once per
+// edge in powers of c (a_k = sum_l C_lk s_l, C_lk the coefficient of c^k in P_l)
+// and evaluate each triplet's value and c-derivative by Horner's rule.
 #pragma once
 
 #include "edge.h"
@@ -173,27 +177,54 @@ __global__ void tri_route_kernel(const int* __restrict__ species, const int* __r
 // cosines, u3 values and slot positions are loaded one triplet per lane, 64
 // at a time, and broadcast with readlane.
 
+// Power-series coefficients of the Legendre polynomials, C[l][k] = [c^k] P_l(c),
+// from Bonnet's recursion (l + 1) P_{l+1} = (2 l + 1) c P_l - l P_{l-1}.
+struct LegendreCoef {
+  float c[kMaxL][kMaxL];
+};
+constexpr LegendreCoef legendre_coef() {
+  double t[kMaxL][kMaxL] = {};
+  t[0][0] = 1.0;
+  t[1][1] = 1.0;
+  for (int l = 1; l + 1 < kMaxL; ++l)
+    for (int k = 0; k < kMaxL; ++k)
+      t[l + 1][k] = ((2 * l + 1) * (k > 0 ? t[l][k - 1] : 0.0) - l * t[l - 1][k]) / (l + 1);
+  LegendreCoef m{};
+  for (int l = 0; l < kMaxL; ++l)
+    for (int k = 0; k < kMaxL; ++k) m.c[l][k] = (float)t[l][k];
+  return m;
+}
+constexpr LegendreCoef kLegendreCoef = legendre_coef();
+
+// s[l] (Legendre basis, zero for l >= L) -> a[k] = sum_l C[l][k] s[l] (powers of c).
+template <int VPL>
+__device__ __forceinline__ void legendre_to_powers(float (&s)[kMaxL][VPL]) {
+  float a[kMaxL][VPL];
+#pragma unroll
+  for (int k = 0; k < kMaxL; ++k) {
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) a[k][v] = 0.f;
+#pragma unroll
+    for (int l = k; l < kMaxL; ++l) {
+      if (kLegendreCoef.c[l][k] != 0.f) {
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) a[k][v] += kLegendreCoef.c[l][k] * s[l][v];
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kMaxL; ++k)
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) s[k][v] = a[k][v];
+}
+
 __device__ __forceinline__ float bcast(float x, int q) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), q));
 }
 __device__ __forceinline__ int bcast(int x, int q) { return __builtin_amdgcn_readlane(x, q); }
 
-// Legendre values and derivatives P_q(c), P'_q(c) for q < kMaxL (Bonnet's
-// recursion, the division by q + 1 taken as a product with its reciprocal).
-__device__ __forceinline__ void legendre_all(float c, float (&P)[kMaxL], float (&dP)[kMaxL]) {
-  P[0] = 1.f;
-  dP[0] = 0.f;
-  P[1] = c;
-  dP[1] = 1.f;
-#pragma unroll
-  for (int q = 1; q + 1 < kMaxL; ++q) {
-    constexpr float one = 1.f;
-    P[q + 1] = ((2 * q + 1) * c * P[q] - q * P[q - 1]) * (one / (q + 1));
-    dP[q + 1] = (q + 1) * P[q] + c * dP[q];
-  }
-}
-
-// s[q] = sum_n b_n sWa[(q Nb + n), cols of lane l] for q < L; b held one value per lane.
+// s[q] = sum_n b_n sWa[(q Nb + n), cols of lane l] for q < L (b held one value per
+// lane), returned in powers of c.
 template <int VPL>
 __device__ __forceinline__ void feat_sums(float b_lane, const float* sWa, int nb, int L, int d, int l,
                                           float (&s)[kMaxL][VPL]) {
@@ -211,6 +242,7 @@ __device__ __forceinline__ void feat_sums(float b_lane, const float* sWa, int nb
       }
     }
   }
+  legendre_to_powers<VPL>(s);
 }
 
 // The same sums for two basis rows (B3 and B3') in one pass over W_a.
@@ -237,6 +269,8 @@ __device__ __forceinline__ void feat_sums2(float b_lane, float db_lane, const fl
       }
     }
   }
+  legendre_to_powers<VPL>(s);
+  legendre_to_powers<VPL>(sp);
 }
 
 // Per-triplet scalars of up to 64 triplets trev[tb + lane] (tb + lane < t1),
@@ -296,31 +330,33 @@ struct PassTri {
   }
 };
 
-// (G W_a) row of one triplet and, with DERIV, (dG/dc W_a), (dG/dr1 W_a), (dG/dr2 W_a).
+// (G W_a) row of one triplet and, with DERIV, (dG/dc W_a), (dG/dr1 W_a), (dG/dr2 W_a),
+// from the per-edge coefficients in powers of c (s, and sp for the B3' sums): value and
+// c-derivative by one Horner pass over the kMaxL coefficients (those of degree >= L
+// are zero).
 template <int VPL, bool DERIV>
 __device__ __forceinline__ void tri_feat(float c, float u, float du, int L, const float (&s)[kMaxL][VPL],
                                          const float (&sp)[kMaxL][VPL], float (&z)[VPL], float (&wc)[VPL],
                                          float (&w1)[VPL], float (&w2)[VPL]) {
-  float P[kMaxL], dP[kMaxL];
-  legendre_all(c, P, dP);
-  zero_row<VPL>(z);
-  if (DERIV) {
-    zero_row<VPL>(wc);
-    zero_row<VPL>(w2);
-  }
+  (void)L;
 #pragma unroll
-  for (int q = 0; q < kMaxL; ++q) {
-    if (q < L) {
-#pragma unroll
-      for (int v = 0; v < VPL; ++v) {
-        z[v] += P[q] * s[q][v];
-        if (DERIV) {
-          wc[v] += dP[q] * s[q][v];
-          w2[v] += P[q] * sp[q][v];
-        }
-      }
+  for (int v = 0; v < VPL; ++v) {
+    z[v] = s[kMaxL - 1][v];
+    if (DERIV) {
+      wc[v] = 0.f;
+      w2[v] = sp[kMaxL - 1][v];
     }
   }
+#pragma unroll
+  for (int k = kMaxL - 2; k >= 0; --k)
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      if (DERIV) {
+        wc[v] = wc[v] * c + z[v];
+        w2[v] = w2[v] * c + sp[k][v];
+      }
+      z[v] = z[v] * c + s[k][v];
+    }
 #pragma unroll
   for (int v = 0; v < VPL; ++v) {
     if (DERIV) {
