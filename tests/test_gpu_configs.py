@@ -1,7 +1,9 @@
 """Model shapes that the five workloads do not reach, against the oracle:
 embedding width 256 and 512 with the three-body term, top-k of 3 and 4,
 expert counts that are not powers of two, hidden widths that leave a partial
-64-column GEMM tile (192, 320), few Legendre orders and basis functions,
+64-column GEMM tile (192, 320), few Legendre orders and basis functions, the
+largest Legendre order (8: the power-series coefficients of the angle features
+are largest there),
 Zipf-skewed routing on a crystal/molecule mix (empty experts), and the
 feature-update MoE at top-k 1, 3 and 4 (alone, with the three-body term,
 and with every expert chosen)."""
@@ -31,6 +33,10 @@ def _configs():
             "3b-d512", "cubic", 1, 32, 0.08,
             ModelConfig(d=512, n_rbf=8, n_blocks=1, n_experts=2, top_k=2, d_hidden=64, r_cut=5.0, three_body=True,
                         r_cut3=3.5, n_experts3=4, top_k3=4, d_hidden3=64, n_legendre=4), seed=11),
+        "3b-d128-L8": Workload(
+            "3b-L8", "cubic", 2, 32, 0.08,
+            ModelConfig(d=128, n_rbf=8, n_blocks=1, n_experts=3, top_k=2, d_hidden=128, r_cut=5.0, three_body=True,
+                        r_cut3=3.5, n_experts3=3, top_k3=2, d_hidden3=64, n_legendre=8), seed=23),
         "atom-d64-kf1-Ef5-hf192": Workload(
             "atom-d64", "cubic", 4, 20, 0.08,
             ModelConfig(d=64, n_rbf=8, n_blocks=2, n_experts=3, top_k=2, d_hidden=128, r_cut=4.5, atom_moe=True,
