@@ -223,6 +223,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                          (const int*)p.trow, Ne, p.te, p.te2);
       hipLaunchKernelGGL(tri_rev_kernel, dim3(cdiv(Nt, 256)), dim3(256), 0, st, (const int*)p.te,
                          (const int*)p.te2, (const int*)p.trow, (const float4*)p.geo, Nt, p.trev, p.tc);
+      hipLaunchKernelGGL(tri_lane_kernel, dim3(cdiv(Nt, 256)), dim3(256), 0, st, (const int*)p.trev,
+                         (const int*)p.te, (const float*)p.tc, (const float*)p.u3, (const float*)p.du3, Nt,
+                         p.tlane);
       // feature rows G of every triplet, for dW_a of the final backward
       hipLaunchKernelGGL(tri_features_kernel, dim3(cdiv(Nt * (nf / 4), 256)), dim3(256), 0, st,
                          LoadTriFeat{p.te, p.te2, p.tc, p.B3, p.dB3, p.u3, p.du3, nullptr, nb}, Nt, nf, p.G3f);
@@ -292,6 +295,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                              Wp(blk(t, "P3c")), Wp(blk(t, "beta3")), E3, k3, p.eid3 + t * M3, p.gate3 + t * M3);
         sort_tokens(st, p.eid3 + t * M3, p.gate3 + t * M3, M3, E3, p.cnt3, p.colpre3, p.total3 + t * E3,
                     p.off3 + t * (E3 + 1), p.pos3 + t * M3, p.slot_gate3 + t * M3);
+        if (Nt > 0)
+          hipLaunchKernelGGL(tri_pos_rev_kernel, dim3(cdiv(Nt, 256)), dim3(256), 0, st, (const int*)p.trev,
+                             (const int*)(p.pos3 + t * M3), Nt, k3, p.pos3r + t * M3);
         build_tables(st, p.off3 + t * (E3 + 1), E3, p.kc3, p.tiles3 + (long long)t * p.mt3, p.ntiles3 + t,
                      p.chunks3 + (long long)t * p.mc3, p.nchunks3 + t, p.cfirst3 + t * (E3 + 1));
       }
@@ -325,6 +331,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
 
   // triplet views of block t
   auto POS3 = [&](int t) { return (const int*)(p.pos3 + t * M3); };
+  auto POS3R = [&](int t) { return (const int*)(p.pos3r + t * M3); };
   auto GATE3 = [&](int t) { return (const float*)(p.gate3 + t * M3); };
   auto SG3 = [&](int t) { return (const float*)(p.slot_gate3 + t * M3); };
   auto TL3 = [&](int t) { return (const RowsTile*)(p.tiles3 + (long long)t * p.mt3); };
@@ -424,9 +431,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       // triplet tokens -> triplet experts -> messages Q_e of each edge's triplets
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * 4.0 * k3 * d);
-        LAUNCH_VPL_K(tri_dispatch_kernel, d, k3, gEa8, b512, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
-                     (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.u3,
-                     Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), POS3(t), Ne, d, Z3s(t));
+        LAUNCH_VPL_K(tri_dispatch_kernel, d, k3, gEa8, b512, ldsWa, st, (const int*)p.trow,
+                     (const float4*)p.tlane, (const float*)p.B3, Wp(blk(t, "W_a")), nb, L3, ej,
+                     (const float*)HV(p.h, t), POS3R(t), Ne, d, Z3s(t));
       }
       {
         PROF(PROF_EXPERT_GEMM, f_tri, 0);
@@ -685,10 +692,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 4.0 * d + 32.0) + Ne * (4.0 * nb + 8.0 * d));
-        LAUNCH_VPL_K(tri_p2_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
-                     (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.dB3,
-                     (const float*)p.u3, (const float*)p.du3, Wp(blk(t, "W_a")), nb, L3, ej,
-                     (const float*)HV(p.h, t), POS3(t), Ne, d, (const float*)p.T3a, Zbar3(t), p.tacc, p.Pe);
+        LAUNCH_VPL_K(tri_p2_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const float4*)p.tlane,
+                     (const float*)p.B3, (const float*)p.dB3, Wp(blk(t, "W_a")), nb, L3, ej,
+                     (const float*)HV(p.h, t), POS3R(t), Ne, d, (const float*)p.T3a, Zbar3(t), p.tacc, p.Pe);
       }
     }
     {
@@ -780,11 +786,10 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       const float* W2a = Wp(blk(t, "W2a"));
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 8.0 * d + 20.0) + Ne * (4.0 * nb + 8.0 * d));
-        LAUNCH_VPL_K(tri_p3_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
-                     (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.dB3,
-                     (const float*)p.u3, (const float*)p.du3, Wp(blk(t, "W_a")), nb, L3, ej,
-                     (const float*)HV(p.h, t), hht_t, (const float4*)p.tct, (const float*)Zbar3(t), POS3(t), Ne, d,
-                     p.T3a, p.VT, p.Pe);
+        LAUNCH_VPL_K(tri_p3_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const float4*)p.tlane,
+                     (const float*)p.B3, (const float*)p.dB3, Wp(blk(t, "W_a")), nb, L3, ej,
+                     (const float*)HV(p.h, t), hht_t, (const float4*)p.tct, (const float*)Zbar3(t), POS3R(t), Ne,
+                     d, p.T3a, p.VT, p.Pe);
       }
       {
         // dW_a (part 1): Gt^T (Zbar * h_j2)
@@ -1214,10 +1219,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_EDGE, 0, by_tri_idx + Nt * (4.0 * k3 * d + 8.0 * d) + Ne * 12.0 * d);
-        LAUNCH_VPL_K(tri_p4_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const int*)p.trev,
-                     (const int*)p.te, (const float*)p.tc, (const float*)p.B3, (const float*)p.u3,
-                     Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), hht_t, (const float*)Zbar3(t),
-                     POS3(t), Ne, d, (const float*)p.T3b, p.VT, p.Pe);
+        LAUNCH_VPL_K(tri_p4_kernel, d, k3, gEa, b256, ldsWa, st, (const int*)p.trow, (const float4*)p.tlane,
+                     (const float*)p.B3, Wp(blk(t, "W_a")), nb, L3, ej, (const float*)HV(p.h, t), hht_t,
+                     (const float*)Zbar3(t), POS3R(t), Ne, d, (const float*)p.T3b, p.VT, p.Pe);
       }
       {
         // dW_a (part 2): G^T (Zt * h_j2 + Q * Zbar)

@@ -984,7 +984,9 @@ struct Plan {
   int *tcount, *trow, *te, *te2, *trev;
   float *tc, *B3, *dB3, *u3, *du3;
   float4 *tacc, *tct, *gvec;
+  float4* tlane;   // per-triplet scalars in second-edge order (tri_lane_kernel)
   int *eid3, *pos3, *total3, *off3, *cnt3, *colpre3;
+  int* pos3r;      // pos3 in second-edge order, per block
   float *gate3, *slot_gate3, *g3t;
   RowsTile* tiles3;
   int* ntiles3;
@@ -1233,9 +1235,11 @@ size_t plan_layout(Plan& p, void* base, const janus_config& c, int N, int S, lon
     p.tacc = cv.take<float4>(Ntt + 1);
     p.tct = cv.take<float4>(Ntt + 1);
     p.gvec = cv.take<float4>(Ne + 1);
+    p.tlane = cv.take<float4>(Ntt + 1);
     p.eid3 = cv.take<int>(T * M3 + 1);
     p.gate3 = cv.take<float>(T * M3 + 1);
     p.pos3 = cv.take<int>(T * M3 + 1);
+    p.pos3r = cv.take<int>(T * M3 + 1);
     p.slot_gate3 = cv.take<float>(T * M3 + 1);
     p.g3t = cv.take<float>(T * M3 + 1);
     p.total3 = cv.take<int>(T * E3);

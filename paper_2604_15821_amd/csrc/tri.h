@@ -172,10 +172,11 @@ __global__ void tri_route_kernel(const int* __restrict__ species, const int* __r
 // The expert-token kernels run one wave per second edge e2: the sums
 //   s_l = sum_n B3_n(r_e2) W_a[l Nb + n, :]   (and s'_l with B3')
 // depend on e2 only, so they are formed once per edge; each triplet
-// tau = (e, e2) then needs only its Legendre values P_l(c_tau) and u3(r_e).
+// tau = (e, e2) then needs only its cosine c_tau and u3(r_e).
 // The triplets whose second edge is e2 are trev[tseg(e2)]; their indices,
-// cosines, u3 values and slot positions are loaded one triplet per lane, 64
-// at a time, and broadcast with readlane.
+// cosines, u3 values and slot positions, stored once per step (per block for
+// the slots) in that order, are loaded one triplet per lane, 64 at a time, and
+// broadcast with readlane.
 
 // Power-series coefficients of the Legendre polynomials, C[l][k] = [c^k] P_l(c),
 // from Bonnet's recursion (l + 1) P_{l+1} = (2 l + 1) c P_l - l P_{l-1}.
@@ -273,25 +274,47 @@ __device__ __forceinline__ void feat_sums2(float b_lane, float db_lane, const fl
   legendre_to_powers<VPL>(sp);
 }
 
-// Per-triplet scalars of up to 64 triplets trev[tb + lane] (tb + lane < t1),
-// one triplet per lane (lanes past t1 repeat the last triplet).
+// Per-triplet scalars in second-edge order, once per step: position t' of trev
+// holds (c, u3(r_e), u3'(r_e), tau as int bits) of triplet tau = trev[t'] = (e, e2),
+// so the expert-token kernels read a batch of triplets with one coalesced load
+// instead of three dependent gathers (trev, then tc and te, then u3).
+__global__ void tri_lane_kernel(const int* __restrict__ trev, const int* __restrict__ te,
+                                const float* __restrict__ tc, const float* __restrict__ u3,
+                                const float* __restrict__ du3, long long Nt, float4* __restrict__ tlane) {
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Nt) return;
+  const int tau = trev[t];
+  const int e1 = te[tau];
+  tlane[t] = make_float4(tc[tau], u3[e1], du3[e1], __int_as_float(tau));
+}
+
+// Slot positions of one block's triplet routing in the same order:
+// pos3r[t' KC + k] = pos3[trev[t'] KC + k].
+__global__ void tri_pos_rev_kernel(const int* __restrict__ trev, const int* __restrict__ pos3, long long Nt, int KC,
+                                   int* __restrict__ pos3r) {
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Nt) return;
+  const long long tau = trev[t];
+  for (int k = 0; k < KC; ++k) pos3r[t * KC + k] = pos3[tau * KC + k];
+}
+
+// Per-triplet scalars of up to 64 triplets at positions tb + lane (< t1) of the
+// second-edge order, one triplet per lane (lanes past t1 repeat the last triplet).
 template <int KC>
 struct TriLane {
   int tau;
   float c, u, du;
   int pos[KC];
-  __device__ __forceinline__ void load(const int* __restrict__ trev, const int* __restrict__ te,
-                                       const float* __restrict__ tc, const float* __restrict__ u3,
-                                       const float* __restrict__ du3, const int* __restrict__ pos3, int tb, int t1,
-                                       int l) {
+  __device__ __forceinline__ void load(const float4* __restrict__ tlane, const int* __restrict__ pos3r, int tb,
+                                       int t1, int l) {
     const int tl = tb + l < t1 ? tb + l : t1 - 1;
-    tau = trev[tl];
-    c = tc[tau];
-    const int e1 = te[tau];
-    u = u3[e1];
-    du = du3 ? du3[e1] : 0.f;
+    const float4 v = tlane[tl];
+    c = v.x;
+    u = v.y;
+    du = v.z;
+    tau = __float_as_int(v.w);
 #pragma unroll
-    for (int k = 0; k < KC; ++k) pos[k] = pos3[(long long)tau * KC + k];
+    for (int k = 0; k < KC; ++k) pos[k] = pos3r[(long long)tl * KC + k];
   }
 };
 
@@ -372,12 +395,10 @@ __device__ __forceinline__ void tri_feat(float c, float u, float du, int L, cons
 
 // Z_tau = (G W_a) * h_{j(e2)} into the triplet expert slots.
 template <int VPL, int KC>
-__global__ void tri_dispatch_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
-                                    const int* __restrict__ te, const float* __restrict__ tc,
-                                    const float* __restrict__ B3, const float* __restrict__ u3,
-                                    const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
-                                    const float* __restrict__ h, const int* __restrict__ pos3, long long Ne, int d,
-                                    float* __restrict__ Zs) {
+__global__ void tri_dispatch_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
+                                    const float* __restrict__ B3, const float* __restrict__ Wa, int nb, int L,
+                                    const int* __restrict__ ej, const float* __restrict__ h,
+                                    const int* __restrict__ pos3r, long long Ne, int d, float* __restrict__ Zs) {
   extern __shared__ float sWa[];
   load_lds(sWa, Wa, L * nb * d);
   JANUS_WAVE_LOOP(e2, Ne) {
@@ -388,7 +409,7 @@ __global__ void tri_dispatch_kernel(const int* __restrict__ trowptr, const int* 
     ld_row<VPL>(h + (long long)ej[e2] * d, l, hj);
     for (int tb = t0; tb < t1; tb += 64) {
       TriLane<KC> tl;
-      tl.load(trev, te, tc, u3, nullptr, pos3, tb, t1, l);
+      tl.load(tlane, pos3r, tb, t1, l);
       const int n = t1 - tb < 64 ? t1 - tb : 64;
       for (int q = 0; q < n; ++q) {
         float z[VPL], wc[VPL], w1[VPL], w2[VPL];
@@ -476,12 +497,10 @@ __global__ void tri_gather_kernel(const int* __restrict__ trowptr, const int* __
 // and P[e2] += sum over the triplets of e2 of Zbar * (G W_a) (routed to h_j2),
 // added in trev[tseg(e2)] order.
 template <int VPL, int KC>
-__global__ void tri_p2_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
-                              const int* __restrict__ te, const float* __restrict__ tc,
+__global__ void tri_p2_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
                               const float* __restrict__ B3, const float* __restrict__ dB3,
-                              const float* __restrict__ u3, const float* __restrict__ du3,
                               const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
-                              const float* __restrict__ h, const int* __restrict__ pos3, long long Ne, int d,
+                              const float* __restrict__ h, const int* __restrict__ pos3r, long long Ne, int d,
                               const float* __restrict__ Zbs, float* __restrict__ Zbar, float4* __restrict__ acc,
                               float* __restrict__ P) {
   extern __shared__ float sWa[];
@@ -495,7 +514,7 @@ __global__ void tri_p2_kernel(const int* __restrict__ trowptr, const int* __rest
     ld_row<VPL>(P + e2 * d, l, pr);
     for (int tb = t0; tb < t1; tb += 64) {
       TriLane<KC> tl;
-      tl.load(trev, te, tc, u3, du3, pos3, tb, t1, l);
+      tl.load(tlane, pos3r, tb, t1, l);
       const int n = t1 - tb < 64 ? t1 - tb : 64;
       // lane q keeps the geometry adjoints of triplet q of the batch
       float my_ac = 0.f, my_a1 = 0.f, my_a2 = 0.f;
@@ -616,14 +635,12 @@ __global__ void tri_ctilde_kernel(const int* __restrict__ te, const int* __restr
 // and P[e2] = sum over the triplets of e2 of vt * Zbar (routed to h_j2),
 // written for every edge (zero without triplets).
 template <int VPL, int KC>
-__global__ void tri_p3_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
-                              const int* __restrict__ te, const float* __restrict__ tc,
+__global__ void tri_p3_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
                               const float* __restrict__ B3, const float* __restrict__ dB3,
-                              const float* __restrict__ u3, const float* __restrict__ du3,
                               const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
                               const float* __restrict__ h, const float* __restrict__ hht,
                               const float4* __restrict__ ct, const float* __restrict__ Zbar,
-                              const int* __restrict__ pos3, long long Ne, int d, float* __restrict__ Zbts,
+                              const int* __restrict__ pos3r, long long Ne, int d, float* __restrict__ Zbts,
                               float* __restrict__ V, float* __restrict__ P) {
   extern __shared__ float sWa[];
   load_lds(sWa, Wa, L * nb * d);
@@ -639,7 +656,7 @@ __global__ void tri_p3_kernel(const int* __restrict__ trowptr, const int* __rest
       if (hht) ld_row<VPL>(hht + j2 * d, l, qh); else zero_row<VPL>(qh);
       for (int tb = t0; tb < t1; tb += 64) {
         TriLane<KC> tl;
-        tl.load(trev, te, tc, u3, du3, pos3, tb, t1, l);
+        tl.load(tlane, pos3r, tb, t1, l);
         const float4 cl = ct[tl.tau];
         const int n = t1 - tb < 64 ? t1 - tb : 64;
         auto pass = [&](const PassTri<VPL, KC>& cur, int q0) {
@@ -740,12 +757,11 @@ __global__ void tri_combine_p3_kernel(const int* __restrict__ trowptr, const int
 //   ZP = Zt * h_j2 + Q * Zbar   (loss adjoint of G W_a; dW_a += G^T ZP)
 // and P[e2] += sum over the triplets of e2 of Zt * (G W_a) (routed to h_j2).
 template <int VPL, int KC>
-__global__ void tri_p4_kernel(const int* __restrict__ trowptr, const int* __restrict__ trev,
-                              const int* __restrict__ te, const float* __restrict__ tc,
-                              const float* __restrict__ B3, const float* __restrict__ u3,
-                              const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
-                              const float* __restrict__ h, const float* __restrict__ hht,
-                              const float* __restrict__ Zbar, const int* __restrict__ pos3, long long Ne, int d,
+__global__ void tri_p4_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
+                              const float* __restrict__ B3, const float* __restrict__ Wa, int nb, int L,
+                              const int* __restrict__ ej, const float* __restrict__ h,
+                              const float* __restrict__ hht, const float* __restrict__ Zbar,
+                              const int* __restrict__ pos3r, long long Ne, int d,
                               const float* __restrict__ Zts, float* __restrict__ ZP, float* __restrict__ P) {
   extern __shared__ float sWa[];
   load_lds(sWa, Wa, L * nb * d);
@@ -760,7 +776,7 @@ __global__ void tri_p4_kernel(const int* __restrict__ trowptr, const int* __rest
     ld_row<VPL>(P + e2 * d, l, pr);
     for (int tb = t0; tb < t1; tb += 64) {
       TriLane<KC> tl;
-      tl.load(trev, te, tc, u3, nullptr, pos3, tb, t1, l);
+      tl.load(tlane, pos3r, tb, t1, l);
       const int n = t1 - tb < 64 ? t1 - tb : 64;
       auto pass = [&](const PassRows<VPL, KC>& cur, const PassTri<VPL, KC>& curb, int q0) {
         float zt[2][VPL];
