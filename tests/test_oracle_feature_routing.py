@@ -8,7 +8,8 @@
 * forces against central differences of the energy (the gates move with the
   positions through X_e); the loss against central differences in the weights
   (Wr, the species tables, the experts, the radial filter, the embedding) and in
-  the positions; every step checked to leave the decisions unchanged;
+  the positions; every step checked to leave the decisions unchanged; both also
+  with self-attention over the neighbourhoods (and its Wqkv, Wo);
 * the decision gaps l_(k) - l_(k+1) are those of the sorted logits (reported)."""
 import dataclasses
 
@@ -21,9 +22,9 @@ from oracle.neighbors import neighbor_list
 from paper_2604_15821_amd.synth import _draw_weights, make_batch
 
 
-def _batch(k=2, seed=3, n_struct=2, wr_scale=1.0):
+def _batch(k=2, seed=3, n_struct=2, wr_scale=1.0, heads=0):
     b = make_batch("tiny", n_struct=n_struct)
-    m = dataclasses.replace(b.model, route_feat=1, top_k=k, n_experts=5)
+    m = dataclasses.replace(b.model, route_feat=1, top_k=k, n_experts=5, n_heads=heads)
     w = _draw_weights(np.random.default_rng(seed), m, 0.0)
     for t in range(m.n_blocks):
         w[f"blocks.{t}.Wr"] = (w[f"blocks.{t}.Wr"] * wr_scale).astype(np.float32)
@@ -85,8 +86,9 @@ def test_decisions_are_the_stable_sort_of_the_logits():
         assert (rt[t].gap >= 0).all()
 
 
-def test_forces_match_central_differences():
-    b = _batch(k=2)
+@pytest.mark.parametrize("heads", [0, 2])
+def test_forces_match_central_differences(heads):
+    b = _batch(k=2, heads=heads)
     m = b.model
     edges = neighbor_list(b.pos, b.cell, b.offsets, m.r_cut)
     pos = b.pos.astype(np.float64)
@@ -108,8 +110,9 @@ def test_forces_match_central_differences():
             assert fd == pytest.approx(F[a, c], rel=1e-6, abs=1e-9 * np.abs(F).max()), (a, c)
 
 
-def test_loss_gradient_matches_central_differences():
-    b = _batch(k=2)
+@pytest.mark.parametrize("heads", [0, 2])
+def test_loss_gradient_matches_central_differences(heads):
+    b = _batch(k=2, heads=heads)
     m = b.model
     edges = neighbor_list(b.pos, b.cell, b.offsets, m.r_cut)
     loss, E, F, grad, aux = training_step(b, edges=edges, return_aux=True, positions=True)
@@ -125,6 +128,8 @@ def test_loss_gradient_matches_central_differences():
     rng = np.random.default_rng(4)
     names = ["blocks.0.Wr", "blocks.1.Wr", "blocks.0.Pc", "blocks.1.Pn", "blocks.0.W1", "blocks.1.W2",
              "blocks.0.W_b", "A", "W_o1"]
+    if heads:
+        names += ["blocks.0.Wqkv", "blocks.1.Wo"]
     for name in names:
         w = b.weights[name].astype(np.float64)
         scale = np.abs(grad[name]).max()
