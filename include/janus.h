@@ -117,8 +117,9 @@ enum {
  *              dependence on X_e.  The decision is exact only up to the fp32
  *              rounding of the logits: a token whose k-th and (k+1)-th logits
  *              are that close may be routed differently from a float64
- *              evaluation (janus_debug.gap reports every token's margin).  Not
- *              with attention (JANUS_EUNSUPPORTED).
+ *              evaluation (janus_debug.gap reports every token's margin).  With
+ *              attention the gates act on the edge messages that the attention
+ *              layer takes.
  */
 typedef struct janus_config {
   int32_t n_species;

@@ -501,7 +501,11 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       // messages per edge -> q|k|v -> attention over each neighbourhood -> u = h + osum Wo
       {
         PROF(PROF_EDGE, 0, Ne * (4.0 * k + 4.0 * k * d + 4.0 * d));
-        LAUNCH_VPL_K(edge_sum_kernel, d, k, gE, b256, 0, st, POS(t), (const float*)p.T1, Ne, d, MM(t));
+        if (p.rf)   // the expert outputs are stored before gating: gate them here
+          LAUNCH_VPL_K(combine_fwd_gated_kernel, d, k, gE, b256, 0, st, (const int*)p.iotaE, POS(t), GATE(t),
+                       (const float*)YstR(t), (const float*)nullptr, Ne, d, MM(t));
+        else
+          LAUNCH_VPL_K(edge_sum_kernel, d, k, gE, b256, 0, st, POS(t), (const float*)p.T1, Ne, d, MM(t));
       }
       {
         PROF(PROF_DENSE_GEMM, f_qkv, 0);
@@ -652,10 +656,12 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       LAUNCH_VPL_K(gather_atom_kernel, d, k, gN, b256, 0, st, rowptr, POS(t), GATE(t), hbar_u, N, d, Ybs(t));
     }
     if (p.rf && Ne > 0) {
-      // the gates' adjoints <mbar_i, Y_c> -> logit adjoints -> the router's part of Xbar
+      // the gates' adjoints <mbar, Y_c> -> logit adjoints -> the router's part of Xbar
+      // (mbar: the centre atom's dE/du, or with attention the edge's message adjoint)
       PROF(PROF_ROUTE, 2.0 * Ne * d * Ep, Ne * (4.0 * d + 4.0 * k * d + 8.0 * Ep));
-      LAUNCH_VPL_K(feat_p2_kernel, d, k, gE, b256, 0, st, ei, POS(t), EID(t), GATE(t), (const float*)FPR(t), Ee,
-                   (int)Ep, hbar_u, (const float*)YstR(t), Ne, d, GBR(t), LBR(t));
+      LAUNCH_VPL_K(feat_p2_kernel, d, k, gE, b256, 0, st, attn ? (const int*)p.iotaE : ei, POS(t), EID(t), GATE(t),
+                   (const float*)FPR(t), Ee, (int)Ep, attn ? (const float*)MBt(t) : hbar_u, (const float*)YstR(t),
+                   Ne, d, GBR(t), LBR(t));
       launch_rows<true>(st, LoadPlain{LBR(t), Ep}, WRP(t), (int)Ep, d, p.tilesE, p.ntE, p.mtE, EpiStore{p.Xadd, d});
     }
     {
@@ -894,6 +900,9 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         PROF(PROF_EDGE, 0, Ne * (8.0 * d + 12.0 * k + 4.0 * k * d));
         LAUNCH_VPL_K(edge_combine_p3_kernel, d, k, gE, b256, 0, st, POS(t), GATE(t), (const float*)p.T2,
                      (const float*)MBt(t), Ne, d, p.g3 + t * M, MHt(t));
+        if (p.rf)   // the gates' part of the message tangent: sum_c gh Y_c
+          LAUNCH_VPL_K(feat_hht_kernel, d, k, gE, b256, 0, st, (const int*)p.iotaE, POS(t), (const float*)GHR(t),
+                       (const float*)YstR(t), Ne, d, MHt(t));
       }
       ss.join();
       {
@@ -1101,7 +1110,22 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
         launch_wgrad(st, LoadPlain{MHt(t), d}, LoadPlain{QKVbt(t), 3LL * d}, d, 3 * d, p.chunksA, p.ncA, p.cfA,
                      p.mcA, 1, p.partial, Gp(blk(t, "Wqkv")), 1);
       }
-      {
+      if (p.rf) {
+        // as below, with the edges' own message adjoints (mt from the attention reverse,
+        // mbar from the force backward's attention pass)
+        PROF(PROF_ROUTE, 4.0 * Ne * d * Ep, Ne * (8.0 * d + 4.0 * k * d + 16.0 * Ep));
+        if (Ne > 0) {
+          LAUNCH_VPL_K(feat_p4_kernel, d, k, gE, b256, 0, st, (const int*)p.iotaE, POS(t), EID(t),
+                       (const float*)FPR(t), Ee, (int)Ep, (const float*)p.mta, (const float*)YstR(t),
+                       (const float*)(p.g3 + t * M), (const float*)P3R(t), Ne, d, p.Lw, p.lte);
+          launch_rows<true>(st, LoadPlain{p.Lw, Ep}, WRP(t), (int)Ep, d, p.tilesE, p.ntE, p.mtE,
+                            EpiStore{p.Xadd, d});
+          launch_wgrad(st, LoadPlain{XeR(t), d}, LoadPlain{p.Lw, Ep}, d, (int)Ep, p.chunksR, p.ncR, p.cfR, p.mcR, 1,
+                       p.wrpart, DWR(t), 1);
+        }
+        LAUNCH_VPL_K(gather_feat_kernel, d, k, gE, b256, 0, st, (const int*)p.iotaE, POS(t), GATE(t),
+                     (const float*)p.mta, (const float*)GHR(t), (const float*)MBt(t), Ne, d, p.T1);
+      } else {
         PROF(PROF_EDGE, 0, Ne * (4.0 * d + 4.0 * k + 4.0 * k * d));
         LAUNCH_VPL_K(edge_gather_kernel, d, k, gE, b256, 0, st, POS(t), (const float*)nullptr, (const float*)p.mta,
                      Ne, d, p.T1);

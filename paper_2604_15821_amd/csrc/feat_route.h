@@ -2,7 +2,9 @@
 // (MoE) routing", with the router a linear layer on the token): per block t
 //   l_e = (Pc[Z_i] + Pn[Z_j]) + X_e Wr + beta,   top-k of the fp32 logits,
 //   gates g_ec = p_e[x_c] with p_e = softmax(l_e) over all E experts,
-// so the gates move with X_e and the four phases carry their derivatives:
+// so the gates move with X_e and the four phases carry their derivatives (mbar_i,
+// mt_i and the tangent below are the atom's; with self-attention they are the edge's
+// own message adjoints and tangent, read through identity index maps):
 //   phase 2 (forces):  gbar_c = <mbar_i, Y_c>,  lbar = J(p)^T gbar,
 //                      Xbar_e += Wr lbar   (J(p) = diag(p) - p p^T);
 //   phase 3 (double backward), from Xh = the loss adjoint of Xbar:
@@ -88,14 +90,16 @@ __global__ void feat_route_kernel(const float* __restrict__ XW, const int* __res
   if (gap) gap[e] = k < E ? lk - next : INFINITY;
 }
 
-// h'_i = h_i + sum_{e in seg(i)} sum_c g_ec Y[pos[e, c]]  (Y before gating).
+// h'_i = h_i + sum_{e in seg(i)} sum_c g_ec Y[pos[e, c]]  (Y before gating; h may be
+// null: zero).  With the identity segments (rowptr[e] = e) it forms the gated
+// message of every edge, the attention layer's tokens.
 template <int VPL, int KC>
 __global__ void combine_fwd_gated_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos,
                                          const float* __restrict__ gate, const float* __restrict__ Y,
-                                         const float* __restrict__ h, int N, int d, float* __restrict__ hn) {
+                                         const float* __restrict__ h, long long N, int d, float* __restrict__ hn) {
   JANUS_WAVE_LOOP(i, N) {
     float acc[VPL];
-    ld_row<VPL>(h + i * d, l, acc);
+    if (h) ld_row<VPL>(h + i * d, l, acc); else zero_row<VPL>(acc);
     const long long f1 = (long long)rowptr[i + 1] * KC;
     long long f = (long long)rowptr[i] * KC;
     for (; f + 4 <= f1; f += 4) {
@@ -190,10 +194,11 @@ __global__ void feat_p3_kernel(const int* __restrict__ eid, const float* __restr
   }
 }
 
-// Phase 3 per atom: hht'_i += sum_{e in seg(i)} sum_c gh_ec Y[pos[e, c]].
+// Phase 3 per atom: hht'_i += sum_{e in seg(i)} sum_c gh_ec Y[pos[e, c]] (with the
+// identity segments, per edge: the gates' part of the message tangent).
 template <int VPL, int KC>
 __global__ void feat_hht_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos,
-                                const float* __restrict__ gh, const float* __restrict__ Y, int N, int d,
+                                const float* __restrict__ gh, const float* __restrict__ Y, long long N, int d,
                                 float* __restrict__ hht) {
   JANUS_WAVE_LOOP(i, N) {
     float acc[VPL];
@@ -211,12 +216,14 @@ __global__ void feat_hht_kernel(const int* __restrict__ rowptr, const int* __res
 }
 
 // Phase 4: slot rows of the loss adjoint of the expert outputs,
-//   out[pos[e, c]] = g_ec mt_i + gh_ec mbar_i.
+//   out[pos[e, c]] = g_ec mt_i + gh_ec mbar_i
+// (with the identity segments and per-edge mt, mbar: the attention layer's message
+// adjoints).
 template <int VPL, int KC>
 __global__ void gather_feat_kernel(const int* __restrict__ rowptr, const int* __restrict__ pos,
                                    const float* __restrict__ gate, const float* __restrict__ mt,
-                                   const float* __restrict__ gh, const float* __restrict__ mbar, int N, int d,
-                                   float* __restrict__ out) {
+                                   const float* __restrict__ gh, const float* __restrict__ mbar, long long N,
+                                   int d, float* __restrict__ out) {
   JANUS_WAVE_LOOP(i, N) {
     float a[VPL], b[VPL];
     ld_row<VPL>(mt + i * d, l, a);

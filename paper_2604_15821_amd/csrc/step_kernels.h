@@ -931,8 +931,6 @@ int check_config(const janus_config* c) {
   // heads of 32 columns
   if (c->n_heads && c->d / c->n_heads != kAttnDh) return JANUS_EUNSUPPORTED;
   if (c->route_feat != 0 && c->route_feat != 1) return JANUS_EINVAL;
-  // routing on the edge tokens goes with the plain message sum (not with attention)
-  if (c->route_feat && c->n_heads) return JANUS_EUNSUPPORTED;
   if (c->atom_moe) {
     if (c->n_experts_f < 1 || c->n_experts_f > 64 || c->top_k_f < 1 || c->top_k_f > 4 ||
         c->top_k_f > c->n_experts_f || c->d_hidden_f < 64)

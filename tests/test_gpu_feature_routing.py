@@ -9,7 +9,7 @@ of a logit); every decided token must be routed identically (bit-exact expert
 ids), and the tokens inside the margin are counted and reported.  When every
 decision agrees (the test batches are such) the whole step is compared: energy 1e-5,
 loss 1e-5, forces, every weight gradient (Wr included) and dL/dR 1e-3 relative
-L2."""
+L2; also with self-attention over the neighbourhoods (2 and 4 heads)."""
 import dataclasses
 
 import numpy as np
@@ -31,6 +31,20 @@ def _batch(name):
         return dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(3), m, 0.0))
     if name == "feature-2":
         return subset(make_batch("feature_routing"), range(2))
+    if name == "tiny-k2-attn":
+        b = make_batch("tiny", n_struct=2)
+        m = dataclasses.replace(b.model, route_feat=1, top_k=2, n_experts=6, n_heads=2)
+        return dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(5), m, 0.0))
+    if name == "attention-feature-2":
+        # Wr at half its drawn scale: at full scale this random model's energy surface is
+        # steep (loss 458 against 21, forces 10x larger), and the fp32 rounding of the
+        # forces alone puts the loss 7e-5 off (errors 1e-6 to 3e-5 at half scale)
+        b = subset(make_batch("attention"), range(2))
+        m = dataclasses.replace(b.model, route_feat=1, w_S=0.1 * 160.2177 ** 2)
+        w = _draw_weights(np.random.default_rng(6), m, 0.0)
+        for t in range(m.n_blocks):
+            w[f"blocks.{t}.Wr"] = (0.5 * w[f"blocks.{t}.Wr"]).astype(np.float32)
+        return dataclasses.replace(b, model=m, weights=w)
     if name == "3b-atom-stress-1":
         b = subset(make_batch("threebody"), range(1))
         m = dataclasses.replace(b.model, d=64, d_hidden=128, n_experts=5, n_experts3=3, d_hidden3=64, n_rbf=8,
@@ -91,7 +105,7 @@ def _compare_decisions(b, got, aux):
     return inside, differ
 
 
-@pytest.mark.parametrize("name", ["tiny-k2", "feature-2", "3b-atom-stress-1"])
+@pytest.mark.parametrize("name", ["tiny-k2", "feature-2", "3b-atom-stress-1", "tiny-k2-attn", "attention-feature-2"])
 def test_feature_routing_matches_oracle(name):
     from oracle.model import Params, forward_energy, training_step
     b = _batch(name)
