@@ -84,8 +84,8 @@ enum {
  *              janus_step_stress, stresses in energy / length^3)
  *   n_heads    0, or the number of heads of the self-attention over every
  *              atom's edge messages (paper Sec. "Multi-head self-attention");
- *              must divide d, and the kernels implement heads of 32 columns
- *              (d / n_heads = 32; other widths: JANUS_EUNSUPPORTED)
+ *              must divide d, with heads of 32, 64 or 128 columns
+ *              (d / n_heads; other widths: JANUS_EUNSUPPORTED)
  *   n_tasks    0, or the number of tasks of the task-aware embedding (paper
  *              Sec. "Task-aware feature embedding"); then n_charges and
  *              n_spins (>= 1) size the charge and spin tables, and every

@@ -207,6 +207,21 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   if (atom) hipLaunchKernelGGL(iota_kernel, dim3(cdiv(N + 1, 256)), dim3(256), 0, st, p.iota, N);
   const bool attn = p.attn != 0;
   const int H = p.H;
+  // head width: the register-resident kernels (heads of 32 columns, neighbourhoods of
+  // up to kAttnMfmaN edges) and the tiled sweeps beside them; wider heads take the
+  // tiled sweeps for every atom (nmin = -1)
+  const int dh = attn ? d / H : 0;
+  const bool attn_reg = dh == kAttnDh;
+  const int nmin = attn_reg ? kAttnMfmaN : -1;
+#define JANUS_ATTN_TILED(kern, ...)                                                    \
+  do {                                                                                 \
+    if (dh == 32)                                                                      \
+      hipLaunchKernelGGL(kern<32>, gNH, b256, 0, st, __VA_ARGS__);                     \
+    else if (dh == 64)                                                                 \
+      hipLaunchKernelGGL(kern<64>, gNH, b256, 0, st, __VA_ARGS__);                     \
+    else                                                                               \
+      hipLaunchKernelGGL(kern<128>, gNH, b256, 0, st, __VA_ARGS__);                    \
+  } while (0)
   {
     PROF(PROF_GRAPH, 0, Ne * (12.0 + 3.0 + 16.0 + 8.0 * nb));
     launch_geometry(st, pos, cell, p.sid, ei, ej, shift, (int)Ne, cfg.r_cut, nb, p.geo, p.B, p.dB,
@@ -515,19 +530,21 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       {
         PROF(PROF_ATTN, 0, by_attn);
         // neighbourhoods up to kAttnMfmaN edges on register-resident tiles, larger ones on tiled sweeps
-        hipLaunchKernelGGL(attn_fwd_mfma_kernel<1>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
-                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
-        if (2 <= kAttnTiles)
-          hipLaunchKernelGGL(attn_fwd_mfma_kernel<2>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
-                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
-        if (3 <= kAttnTiles)
-          hipLaunchKernelGGL(attn_fwd_mfma_kernel<3>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
-                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
-        if (4 <= kAttnTiles)
-          hipLaunchKernelGGL(attn_fwd_mfma_kernel<4>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
-                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
-        hipLaunchKernelGGL(attn_fwd_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
-                           (const float*)p.eu, N, d, H, STt(t), OSt(t));
+        if (attn_reg) {
+          hipLaunchKernelGGL(attn_fwd_mfma_kernel<1>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                             (const float*)p.eu, N, d, H, STt(t), OSt(t));
+          if (2 <= kAttnTiles)
+            hipLaunchKernelGGL(attn_fwd_mfma_kernel<2>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                               (const float*)p.eu, N, d, H, STt(t), OSt(t));
+          if (3 <= kAttnTiles)
+            hipLaunchKernelGGL(attn_fwd_mfma_kernel<3>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                               (const float*)p.eu, N, d, H, STt(t), OSt(t));
+          if (4 <= kAttnTiles)
+            hipLaunchKernelGGL(attn_fwd_mfma_kernel<4>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
+                               (const float*)p.eu, N, d, H, STt(t), OSt(t));
+        }
+        JANUS_ATTN_TILED(attn_fwd_tiled_kernel, rowptr, (const float*)QKVt(t), (const float*)p.eu, N, d, H, nmin,
+                         STt(t), OSt(t));
       }
       {
         PROF(PROF_DENSE_GEMM, f_dense, 0);
@@ -632,13 +649,15 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
 #define JANUS_BWD_MFMA(NTV)                                                                                    \
   hipLaunchKernelGGL(attn_bwd_mfma_kernel<NTV>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),                \
                      (const float*)p.eu, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t), p.rbh)
-        JANUS_BWD_MFMA(1);
-        if (2 <= kAttnTiles) JANUS_BWD_MFMA(2);
-        if (3 <= kAttnTiles) JANUS_BWD_MFMA(3);
-        if (4 <= kAttnTiles) JANUS_BWD_MFMA(4);
+        if (attn_reg) {
+          JANUS_BWD_MFMA(1);
+          if (2 <= kAttnTiles) JANUS_BWD_MFMA(2);
+          if (3 <= kAttnTiles) JANUS_BWD_MFMA(3);
+          if (4 <= kAttnTiles) JANUS_BWD_MFMA(4);
+        }
 #undef JANUS_BWD_MFMA
-        hipLaunchKernelGGL(attn_bwd_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
-                           (const float*)p.eu, (const float*)STt(t), (const float*)OBt(t), N, d, H, QKVbt(t), p.rbh);
+        JANUS_ATTN_TILED(attn_bwd_tiled_kernel, rowptr, (const float*)QKVt(t), (const float*)p.eu,
+                         (const float*)STt(t), (const float*)OBt(t), N, d, H, nmin, QKVbt(t), p.rbh);
         hipLaunchKernelGGL(attn_rbar_kernel, gN, b256, 0, st, rowptr, (const float*)p.eud, (const float*)p.rbh, N, H,
                            kAttnMaxN, p.rbar, p.rbs ? p.rbs + (long long)t * Ne : (float*)nullptr);
       }
@@ -916,14 +935,16 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
   hipLaunchKernelGGL(attn_tan_mfma_kernel<NTV>, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),                \
                      (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,         \
                      (const float*)STt(t), N, d, H, p.osh)
-        JANUS_TAN_MFMA(1);
-        if (2 <= kAttnTiles) JANUS_TAN_MFMA(2);
-        if (3 <= kAttnTiles) JANUS_TAN_MFMA(3);
-        if (4 <= kAttnTiles) JANUS_TAN_MFMA(4);
+        if (attn_reg) {
+          JANUS_TAN_MFMA(1);
+          if (2 <= kAttnTiles) JANUS_TAN_MFMA(2);
+          if (3 <= kAttnTiles) JANUS_TAN_MFMA(3);
+          if (4 <= kAttnTiles) JANUS_TAN_MFMA(4);
+        }
 #undef JANUS_TAN_MFMA
-        hipLaunchKernelGGL(attn_tan_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
-                           (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,
-                           (const float*)STt(t), N, d, H, p.osh);
+        JANUS_ATTN_TILED(attn_tan_tiled_kernel, rowptr, (const float*)QKVt(t), (const float*)QKVht(t),
+                         (const float*)p.eu, (const float*)p.eud, (const float*)p.rt, (const float*)STt(t), N, d, H,
+                         nmin, p.osh);
       }
       {
         PROF(PROF_DENSE_GEMM, 2 * f_dense, 0);
@@ -1088,14 +1109,16 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
                          (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa,        \
                          (float*)nullptr);                                                                     \
   } while (0)
-        JANUS_REV_MFMA(1);
-        if (2 <= kAttnTiles) JANUS_REV_MFMA(2);
-        if (3 <= kAttnTiles) JANUS_REV_MFMA(3);
-        if (4 <= kAttnTiles) JANUS_REV_MFMA(4);
+        if (attn_reg) {
+          JANUS_REV_MFMA(1);
+          if (2 <= kAttnTiles) JANUS_REV_MFMA(2);
+          if (3 <= kAttnTiles) JANUS_REV_MFMA(3);
+          if (4 <= kAttnTiles) JANUS_REV_MFMA(4);
+        }
 #undef JANUS_REV_MFMA
-        hipLaunchKernelGGL(attn_rev_tiled_kernel, gNH, b256, 0, st, rowptr, (const float*)QKVt(t),
-                           (const float*)QKVht(t), (const float*)p.eu, (const float*)p.eud, (const float*)p.rt,
-                           (const float*)STt(t), (const float*)p.AO, (const float*)OBt(t), N, d, H, p.QKVa, p.rlh);
+        JANUS_ATTN_TILED(attn_rev_tiled_kernel, rowptr, (const float*)QKVt(t), (const float*)QKVht(t),
+                         (const float*)p.eu, (const float*)p.eud, (const float*)p.rt, (const float*)STt(t),
+                         (const float*)p.AO, (const float*)OBt(t), N, d, H, nmin, p.QKVa, p.rlh);
         if (p.rlh && Ne > 0)   // the envelope's part of dL/dr_e
           hipLaunchKernelGGL(attn_pos_kernel, dim3(cdiv(Ne, 256)), b256, 0, st, (const float4*)p.geo, Ne, H,
                              cfg.r_cut, (const float*)p.rlh, (const float*)(p.rbs + (long long)t * Ne),

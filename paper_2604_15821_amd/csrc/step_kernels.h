@@ -928,8 +928,9 @@ int check_config(const janus_config* c) {
   if (c->robust && (!(c->huber_delta > 0.f) || c->robust_tau != c->robust_tau)) return JANUS_EINVAL;
   if (c->robust && c->n_tasks > kRobustMaxGroups) return JANUS_EUNSUPPORTED;
 
-  // heads of 32 columns
-  if (c->n_heads && c->d / c->n_heads != kAttnDh) return JANUS_EUNSUPPORTED;
+  // heads of 32, 64 or 128 columns
+  if (c->n_heads && c->d / c->n_heads != 32 && c->d / c->n_heads != 64 && c->d / c->n_heads != 128)
+    return JANUS_EUNSUPPORTED;
   if (c->route_feat != 0 && c->route_feat != 1) return JANUS_EINVAL;
   if (c->atom_moe) {
     if (c->n_experts_f < 1 || c->n_experts_f > 64 || c->top_k_f < 1 || c->top_k_f > 4 ||

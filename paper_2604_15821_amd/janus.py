@@ -72,6 +72,10 @@ def _lib():
     if _LIB is None:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"libjanus is not built ({LIB_PATH}); run paper_2604_15821_amd.build")
+        # PyTorch's HIP runtime must be in the process before the library is: loaded
+        # first, the library would bring in a second runtime (its link-time one), and
+        # device memory of one runtime is not valid in the other
+        import torch  # noqa: F401
         lib = C.CDLL(LIB_PATH)
         vp, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
         lib.janus_strerror.restype = C.c_char_p

@@ -6,6 +6,7 @@ import os
 import re
 
 import pytest
+import torch  # noqa: F401  (PyTorch's HIP runtime first: the library then binds to it)
 
 from paper_2604_15821_amd import janus
 from paper_2604_15821_amd.synth import WORKLOADS, ModelConfig
@@ -62,6 +63,9 @@ def test_pack_unpack_roundtrip():
     (dict(robust=1, huber_delta=0.0), janus.JANUS_EINVAL),
     (dict(robust=1, robust_tau=float("nan")), janus.JANUS_EINVAL),
     (dict(robust=1, n_tasks=300, n_charges=1, n_spins=1), janus.JANUS_EUNSUPPORTED),
+    (dict(n_heads=4), janus.JANUS_EUNSUPPORTED),          # heads of 16 columns
+    (dict(d=256, n_heads=1), janus.JANUS_EUNSUPPORTED),   # one head of 256 columns
+    (dict(n_heads=3), janus.JANUS_EINVAL),                # does not divide d
 ])
 def test_bad_configs_are_rejected_on_the_host(change, code):
     import dataclasses

@@ -4,8 +4,9 @@
 (bond angles, feature-update MoE, stress), on a crystal/molecule mix
 (neighbourhoods of 3 to 99 edges) and on a d = 512, 16-head model with
 neighbourhoods of about 60 to 140 edges (both the register-resident kernels and
-the tiled sweeps); a neighbourhood larger than the kernels hold is rejected
-before anything runs."""
+the tiled sweeps); heads of 64 and 128 columns (the tiled sweeps for every
+neighbourhood; 4 heads of 128 at d = 512); a neighbourhood larger than the
+kernels hold is rejected before anything runs."""
 import dataclasses
 
 import numpy as np
@@ -56,6 +57,18 @@ def _batch(name):
         off = np.array([0, b1.n_atoms, b1.n_atoms + b2.n_atoms], np.int32)
         return Batch(pos=cat("pos"), cell=cat("cell"), species=cat("species"), offsets=off, E_ref=cat("E_ref"),
                      F_ref=cat("F_ref"), weights=b1.weights, model=m, name="wide-attn")
+    if name == "dh64-mixed":
+        # two heads of 64 columns (every neighbourhood on the tiled sweeps), molecules
+        # and a crystal: 3 to about 100 edges per atom
+        b = _batch("mixed-attn")
+        m = dataclasses.replace(b.model, d=128, n_heads=2, w_S=W_S)
+        return dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(7), m, 1.2))
+    if name == "dh128-4heads":
+        # four heads of 128 columns at d = 512 (the head count and width of the paper's
+        # larger models' attention), with the stress term
+        b = make_batch("tiny", n_struct=2)
+        m = dataclasses.replace(b.model, d=512, d_hidden=128, n_experts=3, top_k=2, n_heads=4, w_S=W_S)
+        return dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(8), m, 0.0))
     raise KeyError(name)
 
 
@@ -77,7 +90,7 @@ def _run(b, reps=1):
     return outs
 
 
-CASES = ["tiny-2heads", "attention-4", "3b-atom-stress-attn", "mixed-attn", "wide-attn"]
+CASES = ["tiny-2heads", "attention-4", "3b-atom-stress-attn", "mixed-attn", "wide-attn", "dh64-mixed", "dh128-4heads"]
 
 
 @pytest.fixture(scope="module", params=CASES)

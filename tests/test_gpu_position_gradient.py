@@ -45,6 +45,9 @@ def _batch(name):
         # both the register-resident attention kernels and the tiled sweeps
         from test_gpu_attention import _batch as attn_batch
         return attn_batch("wide-attn")
+    if name == "dh64-attention":
+        from test_gpu_attention import _batch as attn_batch
+        return attn_batch("dh64-mixed")
     raise KeyError(name)
 
 
@@ -70,7 +73,7 @@ def _run(b, limit=None, pos_grad=True):
 
 
 CASES = ["small-4", "stress-4", "robust-12", "atom_moe-3", "multitask-4", "threebody-stress-1", "attention-stress-3",
-         "wide-attention"]
+         "wide-attention", "dh64-attention"]
 
 
 @pytest.mark.parametrize("name", CASES)
