@@ -187,11 +187,12 @@ def main():
 
     if m.n_heads and "attention" in kernels:
         # Algorithmic attention work: per ordered (query, key) pair of a neighbourhood and
-        # head, the distinct 32-long contractions of the four passes (forward q.k and p v;
-        # force backward q.k, p w k, p k and t q; tangent q.k, qh.k, q.kh, pz v, p v, p vh;
-        # final backward q.k, qh.k, q.kh, zb k, zhb kh, zb q, zhb qh): 19 of 2 * 32 flops.
+        # head, the distinct contractions over the head's d / H columns in the four passes
+        # (forward q.k and p v; force backward q.k, p w k, p k and t q; tangent q.k, qh.k,
+        # q.kh, pz v, p v, p vh; final backward q.k, qh.k, q.kh, zb k, zhb kh, zb q, zhb qh):
+        # 19 of 2 d / H flops.
         deg = torch.diff(nl.rowptr.to(torch.int64)).double()
-        attn_flops = 19.0 * 64.0 * m.n_heads * m.n_blocks * float((deg * deg).sum())
+        attn_flops = 19.0 * 2.0 * (m.d // m.n_heads) * m.n_heads * m.n_blocks * float((deg * deg).sum())
         e = kernels["attention"]
         e["flops_per_step"] = attn_flops
         e["tflops"] = attn_flops / (e["ms_per_step"] * 1e-3) / 1e12

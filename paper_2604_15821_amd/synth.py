@@ -180,6 +180,9 @@ _M_ROBUST = dataclasses.replace(_M_TASK, robust=1, huber_delta=1.0, robust_tau=2
 _M_BIG = ModelConfig(d=512, n_rbf=16, n_blocks=4, n_experts=64, top_k=2, d_hidden=2048, r_cut=6.0)
 # attention over large neighbourhoods (about 110 edges per atom at 0.12 atoms / A^3), d = 256, 8 heads
 _M_ATTN_WIDE = dataclasses.replace(_M_SMALL, d=256, n_heads=8, r_cut=6.0)
+# four heads of 128 columns at d = 512 (the head count and width of the paper's larger
+# models' attention) on the small batch's structures
+_M_ATTN_H128 = dataclasses.replace(_M_SMALL, d=512, n_heads=4)
 # routing on the evolving edge tokens (species tables plus a linear layer on X_e)
 _M_FEAT = dataclasses.replace(_M_SMALL, route_feat=1)
 
@@ -191,6 +194,7 @@ WORKLOADS = {
     "stress": Workload("stress", "ortho", 64, 64, 0.08, _M_STRESS),
     "attention": Workload("attention", "ortho", 64, 64, 0.08, _M_ATTN),
     "attention_wide": Workload("attention_wide", "ortho", 64, 64, 0.12, _M_ATTN_WIDE),
+    "attention_h128": Workload("attention_h128", "ortho", 64, 64, 0.08, _M_ATTN_H128),
     "multitask": Workload("multitask", "ortho", 64, 64, 0.08, _M_TASK),
     "robust": Workload("robust", "ortho", 64, 64, 0.08, _M_ROBUST),
     "feature_routing": Workload("feature_routing", "ortho", 64, 64, 0.08, _M_FEAT),
