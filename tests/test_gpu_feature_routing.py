@@ -45,6 +45,14 @@ def _batch(name):
         for t in range(m.n_blocks):
             w[f"blocks.{t}.Wr"] = (0.5 * w[f"blocks.{t}.Wr"]).astype(np.float32)
         return dataclasses.replace(b, model=m, weights=w)
+    if name == "3b-atom-attn-stress-1":
+        # every optional term at once: bond angles, the feature-update MoE, attention,
+        # the stress term, routing on the edge tokens
+        b = subset(make_batch("threebody"), range(1))
+        m = dataclasses.replace(b.model, d=64, d_hidden=128, n_experts=5, n_experts3=3, d_hidden3=64, n_rbf=8,
+                                n_blocks=2, atom_moe=True, n_experts_f=3, top_k_f=2, d_hidden_f=64,
+                                w_S=0.1 * 160.2177 ** 2, route_feat=1, n_heads=2)
+        return dataclasses.replace(b, model=m, weights=_draw_weights(np.random.default_rng(9), m, 0.0))
     if name == "3b-atom-stress-1":
         b = subset(make_batch("threebody"), range(1))
         m = dataclasses.replace(b.model, d=64, d_hidden=128, n_experts=5, n_experts3=3, d_hidden3=64, n_rbf=8,
@@ -105,7 +113,8 @@ def _compare_decisions(b, got, aux):
     return inside, differ
 
 
-@pytest.mark.parametrize("name", ["tiny-k2", "feature-2", "3b-atom-stress-1", "tiny-k2-attn", "attention-feature-2"])
+@pytest.mark.parametrize("name", ["tiny-k2", "feature-2", "3b-atom-stress-1", "tiny-k2-attn", "attention-feature-2",
+                                  "3b-atom-attn-stress-1"])
 def test_feature_routing_matches_oracle(name):
     from oracle.model import Params, forward_energy, training_step
     b = _batch(name)

@@ -8,7 +8,7 @@ irregular batch (a structure's gradient depends on the rest of the batch only
 through the loss normalisation, which a one-structure oracle run reproduces
 with scaled loss weights) and zero net gradient per structure at full size;
 self-attention (the envelope's first and second derivatives enter) on small and on
-60-140-edge neighbourhoods."""
+60-140-edge neighbourhoods, and with heads of 64 and 128 columns."""
 import dataclasses
 
 import numpy as np
@@ -48,6 +48,9 @@ def _batch(name):
     if name == "dh64-attention":
         from test_gpu_attention import _batch as attn_batch
         return attn_batch("dh64-mixed")
+    if name == "dh128-attention":
+        from test_gpu_attention import _batch as attn_batch
+        return attn_batch("dh128-4heads")
     raise KeyError(name)
 
 
@@ -73,7 +76,7 @@ def _run(b, limit=None, pos_grad=True):
 
 
 CASES = ["small-4", "stress-4", "robust-12", "atom_moe-3", "multitask-4", "threebody-stress-1", "attention-stress-3",
-         "wide-attention", "dh64-attention"]
+         "wide-attention", "dh64-attention", "dh128-attention"]
 
 
 @pytest.mark.parametrize("name", CASES)
