@@ -34,6 +34,16 @@ namespace janus {
 
 constexpr int kMaxL = 8;
 
+// Waves per SIMD the per-triplet kernels are compiled for: four (128 registers) while
+// a lane holds at most 2 columns of a row, two (256) for the wider rows of d = 256 and
+// 512, whose sums and derivative rows do not fit 128 registers.  The force-backward
+// kernel at d = 512 (8 columns per lane) runs one wave per SIMD: at two it spills, and
+// took twice as long; the other two spill little or nothing at two and stay there.
+template <int VPL>
+constexpr int kTriWaves = VPL <= 2 ? 4 : 2;
+template <int VPL>
+constexpr int kTriWavesP2 = VPL <= 4 ? kTriWaves<VPL> : 1;
+
 __device__ __forceinline__ void legendre_d(float c, int L, float* P, float* dP) {
   P[0] = 1.f;
   dP[0] = 0.f;
@@ -497,7 +507,7 @@ __global__ void tri_gather_kernel(const int* __restrict__ trowptr, const int* __
 // and P[e2] += sum over the triplets of e2 of Zbar * (G W_a) (routed to h_j2),
 // added in trev[tseg(e2)] order.
 template <int VPL, int KC>
-__global__ void tri_p2_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
+__global__ __launch_bounds__(256, kTriWavesP2<VPL>) void tri_p2_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
                               const float* __restrict__ B3, const float* __restrict__ dB3,
                               const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
                               const float* __restrict__ h, const int* __restrict__ pos3r, long long Ne, int d,
@@ -635,7 +645,7 @@ __global__ void tri_ctilde_kernel(const int* __restrict__ te, const int* __restr
 // and P[e2] = sum over the triplets of e2 of vt * Zbar (routed to h_j2),
 // written for every edge (zero without triplets).
 template <int VPL, int KC>
-__global__ void tri_p3_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
+__global__ __launch_bounds__(256, kTriWaves<VPL>) void tri_p3_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
                               const float* __restrict__ B3, const float* __restrict__ dB3,
                               const float* __restrict__ Wa, int nb, int L, const int* __restrict__ ej,
                               const float* __restrict__ h, const float* __restrict__ hht,
@@ -757,7 +767,7 @@ __global__ void tri_combine_p3_kernel(const int* __restrict__ trowptr, const int
 //   ZP = Zt * h_j2 + Q * Zbar   (loss adjoint of G W_a; dW_a += G^T ZP)
 // and P[e2] += sum over the triplets of e2 of Zt * (G W_a) (routed to h_j2).
 template <int VPL, int KC>
-__global__ void tri_p4_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
+__global__ __launch_bounds__(256, kTriWaves<VPL>) void tri_p4_kernel(const int* __restrict__ trowptr, const float4* __restrict__ tlane,
                               const float* __restrict__ B3, const float* __restrict__ Wa, int nb, int L,
                               const int* __restrict__ ej, const float* __restrict__ h,
                               const float* __restrict__ hht, const float* __restrict__ Zbar,
@@ -949,7 +959,7 @@ __global__ void tri_features_kernel(LoadTriFeat ld, long long Nt, int nf, float*
 //   and, through dd = ... - Psi d, the stress seeds.
 // Float64 throughout; one thread per triplet; the two vectors go to tp1 (for e)
 // and tp2 (for e2).
-__global__ void tri_pos_kernel(const int* __restrict__ te, const int* __restrict__ te2,
+__global__ __launch_bounds__(128, 2) void tri_pos_kernel(const int* __restrict__ te, const int* __restrict__ te2,
                                const float* __restrict__ tc, const float4* __restrict__ geo,
                                const float4* __restrict__ gt, const float* __restrict__ Psi,
                                const int* __restrict__ ei, const int* __restrict__ sid,
