@@ -11,8 +11,10 @@ kernel sources still hash to the recorded value.
 
     python -m paper_2604_15821_amd.counters <workload> <directory with the run outputs>
     python -m paper_2604_15821_amd.counters --trace <workload> <steps> <directory>
+    python -m paper_2604_15821_amd.counters --mfma <workload> <directory>
 
-The second form summarises a kernel-trace run alone into profiles/kernels_<workload>.md.
+The second form summarises a kernel-trace run alone into profiles/kernels_<workload>.md,
+the third a counter pass of executed matrix work into profiles/mfma_<workload>.md.
 """
 from __future__ import annotations
 
@@ -247,7 +249,101 @@ def trace_summary(workload: str, runs: str, steps: int) -> str:
     return "\n".join(L) + "\n"
 
 
+# Executed fp32 matrix work and matrix-pipe busy cycles per dispatch.  rocprofv3's own
+# derived metrics define MfmaFlopsF32 = 512 SQ_INSTS_VALU_MFMA_MOPS_F32 and MfmaUtil =
+# sum(SQ_VALU_MFMA_BUSY_CYCLES) / (max over XCDs of GRBM_GUI_ACTIVE x 1024 SIMDs); the CSV
+# gives GRBM_GUI_ACTIVE summed over the 8 XCDs, whose max is taken as that sum / 8.
+MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE")
+N_XCD, N_SIMD = 8, 1024
+MFMA_RUN_STEPS = 2   # the counter pass below runs one breakdown step and one timed step
+
+
+def mfma_command(workload: str, out: str = "$OUT") -> str:
+    """The rocprofv3 counter pass of one workload (run from /tmp with TMPDIR=/tmp)."""
+    return (f"rocprofv3 --pmc {' '.join(MFMA_COUNTERS)} --output-format csv -d {out}/tr_m_{workload} -o run -- "
+            f"python3 $R/bench.py --workload {workload} --steps 1 --warmup 0 --breakdown-steps 1 --no-cpu-baseline")
+
+
+# bench.py's family names for the counter families whose work is all on the matrix cores
+# (bench.py's dense family also counts the skinny bias-weight gradients, which run on the
+# vector ALU, so its executed matrix work is not comparable)
+_BENCH_FAMILY = {"expert_gemm": "expert_gemm", "wgrad": "expert_wgrad"}
+
+
+def mfma_summary(workload: str, runs: str) -> str:
+    """Markdown summary of one counter pass: executed fp32 MFMA work against the algorithmic
+    work bench.py counts, matrix-pipe busy fraction and clock, per kernel and per family."""
+    per = collections.defaultdict(lambda: collections.defaultdict(float))
+    names, dur = {}, {}
+    with open(f"{runs}/tr_m_{workload}/run_counter_collection.csv") as f:
+        for r in csv.DictReader(f):
+            k = int(r["Dispatch_Id"])
+            per[k][r["Counter_Name"]] += float(r["Counter_Value"])
+            names[k] = r["Kernel_Name"]
+            dur[k] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+    bench_line = None
+    log = f"{runs}/tr_m_{workload}.log"
+    if os.path.exists(log):
+        lines = [x for x in open(log) if x.startswith("{")]
+        bench_line = json.loads(lines[-1]) if lines else None
+    kern = collections.defaultdict(lambda: [0, 0.0, 0.0, 0.0, 0.0])   # dispatches, s, flops, busy, gui/8
+    fam = collections.defaultdict(lambda: [0, 0.0])                   # dispatches, executed flops
+    for k, c in per.items():
+        n = re.sub(r"\(.*", "", names[k].replace("janus::", ""))
+        flops = 512.0 * c["SQ_INSTS_VALU_MFMA_MOPS_F32"]
+        a = kern[n]
+        a[0] += 1
+        a[1] += dur[k]
+        a[2] += flops
+        a[3] += c["SQ_VALU_MFMA_BUSY_CYCLES"]
+        a[4] += c["GRBM_GUI_ACTIVE"] / N_XCD
+        f = fam[family(names[k])]
+        f[0] += 1
+        f[1] += flops
+    L = [f"# Executed fp32 matrix work, training step, workload `{workload}`", "",
+         "Command (run from /tmp on an MI355X with `TMPDIR=/tmp`, repo at `$R`, outputs under `$OUT`):", "",
+         "```", mfma_command(workload), "```", "",
+         f"Summarised by `python -m paper_2604_15821_amd.counters --mfma {workload} $OUT`. Executed work is "
+         "512 x SQ_INSTS_VALU_MFMA_MOPS_F32 (rocprofv3's MfmaFlopsF32); the matrix-pipe busy fraction is "
+         "SQ_VALU_MFMA_BUSY_CYCLES over (GRBM_GUI_ACTIVE / 8) x 1024 SIMDs (its MfmaUtil; the CSV sums "
+         "GRBM_GUI_ACTIVE over the 8 XCDs); the clock is GRBM_GUI_ACTIVE / 8 over the dispatch's duration. "
+         "Dispatches run one at a time under the counter pass, so durations are those of each kernel alone.", ""]
+    if bench_line:
+        L += ["Per family, per training step (the algorithmic work is what bench.py counts for the same run: "
+              "2 x rows x K x N per product, no padding):", "",
+              "| family | dispatches per step | executed TFLOP per step | algorithmic TFLOP per step | executed / algorithmic |",
+              "|---|---:|---:|---:|---:|"]
+        fams = _BENCH_FAMILY
+        if bench_line["config"].get("attention_heads"):
+            # the q|k|v and Wo products run on the expert kernels but count as dense in bench.py
+            fams = {"attention": "attention"}
+        for cf, bf in fams.items():
+            kb = bench_line.get("kernels", {}).get(bf)
+            if not kb or not fam[cf][0]:
+                continue
+            steps = MFMA_RUN_STEPS
+            alg = kb.get("flops_per_step", kb["tflops"] * kb["ms_per_step"] * 1e9) * 1e-12
+            ex = fam[cf][1] / steps / 1e12
+            L.append(f"| {cf} | {fam[cf][0] / steps:.0f} | {ex:.3f} | {alg:.3f} | {ex / alg:.4f} |")
+        L.append("")
+    L += ["| kernel | dispatches | avg us | executed GFLOP per dispatch | TFLOP/s | MFMA busy | clock GHz |",
+          "|---|---:|---:|---:|---:|---:|---:|"]
+    for n, a in sorted(kern.items(), key=lambda kv: -kv[1][1]):
+        if a[2] <= 0:
+            continue
+        L.append(f"| `{n}` | {a[0]} | {a[1] / a[0] * 1e6:.1f} | {a[2] / a[0] / 1e9:.2f} | {a[2] / a[1] / 1e12:.1f} | "
+                 f"{a[3] / (a[4] * N_SIMD):.3f} | {a[4] / a[1] / 1e9:.2f} |")
+    return "\n".join(L) + "\n"
+
+
 if __name__ == "__main__":
+    if len(sys.argv) > 1 and sys.argv[1] == "--mfma":
+        wl, runs = sys.argv[2], sys.argv[3]
+        out = os.path.join(ROOT, "profiles", f"mfma_{wl}.md")
+        with open(out, "w") as f:
+            f.write(mfma_summary(wl, runs))
+        print(out)
+        sys.exit(0)
     if len(sys.argv) > 1 and sys.argv[1] == "--trace":
         wl, steps = sys.argv[2], int(sys.argv[3])
         runs = sys.argv[4]
