@@ -69,8 +69,9 @@ def cpu_baseline(b, budget_s: float, seed: int = 0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    # defaults: about a minute of timed work on the full-size batch (6.2 s per step)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="irregular",
                     help="synthetic batch (default: the 512-structure irregular batch, the largest that fits "
                          "one GPU; 'shard' is the 256 x 128-atom per-device share of the billion-scale model)")
