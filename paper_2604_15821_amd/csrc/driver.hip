@@ -1062,7 +1062,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_EXPERT_WGRAD, f_atm, 0);
-        launch_wgrad(st, LoadSilu{Af(t), hf}, LoadRowScale{p.T1f, SGF(t), d}, hf, d, CHF(t), p.nchunksf + t, CFF(t),
+        launch_wgrad(st, LoadSiluRowScale{Af(t), SGF(t), hf}, LoadPlain{p.T1f, d}, hf, d, CHF(t), p.nchunksf + t, CFF(t),
                      p.mcf, Ef, p.partial, Gp(blk(t, "W2f")), 1);
       }
       {
@@ -1195,7 +1195,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
     {
       // G12: dW2 += SiLU(A)^T (g mt) (side stream)
       PROFS(sd, PROF_EXPERT_WGRAD, f_exp, 0);
-      launch_wgrad(sd, LoadSilu{Aa(t), h}, LoadRowScale{p.T1, p.rf ? (const float*)p.ones : SG(t), d}, h, d, CH(t),
+      launch_wgrad(sd, LoadSiluRowScale{Aa(t), p.rf ? (const float*)p.ones : SG(t), h}, LoadPlain{p.T1, d}, h, d, CH(t),
                    p.nchunks + t, CF(t), p.mc, Ee, p.partial2, Gp(blk(t, "W2")), 1);
     }
     t1_free = ss.mark();
@@ -1261,7 +1261,7 @@ int run_chunk(janus_ctx* ctx, hipStream_t st, Plan& p, const Layout& L, const Ch
       }
       {
         PROF(PROF_EXPERT_WGRAD, f_tri, 0);
-        launch_wgrad(st, LoadSilu{A3(t), h3}, LoadRowScale{p.T3a, SG3(t), d}, h3, d, CH3(t), p.nchunks3 + t, CF3(t),
+        launch_wgrad(st, LoadSiluRowScale{A3(t), SG3(t), h3}, LoadPlain{p.T3a, d}, h3, d, CH3(t), p.nchunks3 + t, CF3(t),
                      p.mc3, E3, p.partial, Gp(blk(t, "W2a")), 1);
       }
       {

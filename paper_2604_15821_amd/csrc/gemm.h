@@ -114,7 +114,7 @@ struct LoadSilu {   // SiLU of stored pre-activations
   }
 };
 
-struct LoadRowScale {   // s[r] * p[r, k]
+struct LoadSiluRowScale {   // s[r] * SiLU(p[r, k])
   const float* p;
   const float* s;
   long long ld;
@@ -124,7 +124,7 @@ struct LoadRowScale {   // s[r] * p[r, k]
   };
   __device__ __forceinline__ Raw load(long long r, int k) const { return Raw{ld4(p + r * ld + k), s[r]}; }
   __device__ __forceinline__ float4 apply(const Raw& x, int) const {
-    return make_float4(x.s * x.v.x, x.s * x.v.y, x.s * x.v.z, x.s * x.v.w);
+    return make_float4(x.s * silu(x.v.x), x.s * silu(x.v.y), x.s * silu(x.v.z), x.s * silu(x.v.w));
   }
 };
 
@@ -600,30 +600,28 @@ __device__ __forceinline__ void gemm_wgrad_block(int vb, float* smem, const ALoa
 
   StageKM<ALoad> sa;
   StageKM<BLoad> sb;
-  // plain operands: whole 16-row stages load directly into LDS (swizzled layout), the
-  // chunk's last partial stage through registers (its rows past the chunk become zeros)
-  constexpr bool D = IsPlainLoad<ALoad>::value && IsPlainLoad<BLoad>::value;
+  // Both operands in the unpadded swizzled [k][m] layout.  A plain operand loads its whole
+  // 16-row stages straight into LDS, and the chunk's last partial stage through registers
+  // (its rows past the chunk become zeros); a transformed operand always goes through
+  // registers.
+  constexpr bool DA = IsPlainLoad<ALoad>::value, DB = IsPlainLoad<BLoad>::value;
   auto stage_load = [&](long long rk, int buf) {
-    if (D && rk + GBK <= ch.r1) {
-      const LoadPlain& a = reinterpret_cast<const LoadPlain&>(al);
-      const LoadPlain& b = reinterpret_cast<const LoadPlain&>(bl);
-      direct_km(a.p, a.ld, rk, p0, P, sA(buf), tid);
-      direct_km(b.p, b.ld, rk, q0, Q, sB(buf), tid);
+    const bool full = rk + GBK <= ch.r1;
+    if constexpr (DA) {
+      if (full) direct_km(al.p, al.ld, rk, p0, P, sA(buf), tid); else sa.load(al, rk, ch.r1, p0, P, tid);
     } else {
       sa.load(al, rk, ch.r1, p0, P, tid);
+    }
+    if constexpr (DB) {
+      if (full) direct_km(bl.p, bl.ld, rk, q0, Q, sB(buf), tid); else sb.load(bl, rk, ch.r1, q0, Q, tid);
+    } else {
       sb.load(bl, rk, ch.r1, q0, Q, tid);
     }
   };
   auto stage_store = [&](long long rk, int buf) {
-    if (D) {
-      if (rk + GBK > ch.r1) {
-        sa.store_sw(al, sA(buf), p0, tid);
-        sb.store_sw(bl, sB(buf), q0, tid);
-      }
-    } else {
-      sa.store(al, sA(buf), p0, tid);
-      sb.store(bl, sB(buf), q0, tid);
-    }
+    const bool full = rk + GBK <= ch.r1;
+    if (!DA || !full) sa.store_sw(al, sA(buf), p0, tid);
+    if (!DB || !full) sb.store_sw(bl, sB(buf), q0, tid);
   };
   stage_load(ch.r0, 0);
   stage_store(ch.r0, 0);
@@ -637,7 +635,7 @@ __device__ __forceinline__ void gemm_wgrad_block(int vb, float* smem, const ALoa
     const long long rk = (long long)ch.r0 + (kt + 1) * GBK;
     if (more) stage_load(rk, cur ^ 1);
     __builtin_amdgcn_s_setprio(1);
-    mfma_stage<false, false, D>(sA(cur), sB(cur), wm, wn, lr, hf, acc);
+    mfma_stage<false, false, true>(sA(cur), sB(cur), wm, wn, lr, hf, acc);
     __builtin_amdgcn_s_setprio(0);
     if (more) stage_store(rk, cur ^ 1);
     wait_direct();
