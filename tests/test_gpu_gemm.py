@@ -31,6 +31,9 @@ CASES = [
     ([1000, 260], 512, 128),
     ([3], 16, 64),
     ([0, 0], 64, 64),
+    # a last column tile with 64 of its 128 columns (and rows of 130 and 7)
+    ([130, 0, 7], 32, 192),
+    ([64, 200], 96, 320),
 ]
 
 
@@ -70,6 +73,9 @@ WG_CASES = [
     ([4097], 16, 128),
     ([513, 20], 512, 128),
     ([0, 0, 0], 8, 64),
+    # partial column tiles on both sides, chunks ending inside and on a 16-row stage
+    ([300, 45, 0, 16], 192, 64),
+    ([1000], 48, 320),
 ]
 
 
