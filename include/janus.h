@@ -23,8 +23,10 @@
  *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
  *    NULL is the default stream).  Outputs are valid once the stream has
  *    been synchronised.  janus_build_edges and janus_step each perform one
- *    small synchronous device-to-host read (edge count, input validation
- *    flag) on that stream before they launch the rest of their work.
+ *    small synchronous device-to-host read (edge count; input validation
+ *    flags and per-structure edge counts for the workspace plan) on that
+ *    stream before they launch the rest of their work, and janus_step with
+ *    the bond-angle term a second one (per-structure triplet counts).
  *  - Return value: JANUS_OK (0) or a negative JANUS_E* code; a message for
  *    it comes from janus_strerror().  On error no output has been written,
  *    except *n_edges for JANUS_ECAPACITY.
