@@ -28,7 +28,7 @@ def _record(workload):
     return json.loads(line.split(":", 1)[1])
 
 
-@pytest.mark.parametrize("workload", ["irregular", "small"])
+@pytest.mark.parametrize("workload", ["irregular", "shard", "small"])
 def test_traffic_record_is_used_only_for_its_sources(monkeypatch, workload):
     from paper_2604_15821_amd import counters
     rec = _record(workload)
